@@ -1,0 +1,444 @@
+// extern "C" entry points: argument validation (before any GPU work), status
+// codes, and the op-level entry points used for kernel-by-kernel parity.
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "../../include/ekya.h"
+#include "../../include/ekya_ops.h"
+#include "rng.hpp"
+#include "runtime.hpp"
+
+struct ekya_ctx {
+  ekya::Ctx c;
+};
+
+namespace {
+
+thread_local std::string g_noctx_err;
+
+ekya_status fail(ekya_ctx* ctx, ekya_status s, const std::string& msg) {
+  if (ctx) ctx->c.err = msg; else g_noctx_err = msg;
+  return s;
+}
+
+bool valid_precision(int p) { return p == EKYA_FP32 || p == EKYA_BF16; }
+
+ekya_status check_frames(ekya_ctx* ctx, int H, int W) {
+  if (H < 32 || W < 32 || H > 4096 || W > 4096)
+    return fail(ctx, EKYA_ERR_INVALID_ARG, "frame height and width must be in [32, 4096]");
+  return EKYA_OK;
+}
+
+ekya_status hip_status(hipError_t e) {
+  if (e == hipSuccess) return EKYA_OK;
+  g_noctx_err = std::string("HIP error: ") + hipGetErrorString(e);
+  return e == hipErrorOutOfMemory ? EKYA_ERR_NOMEM : EKYA_ERR_HIP;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t ekya_weights_count(int n_classes) {
+  if (n_classes < 1 || n_classes > 1024) return 0;
+  return (size_t)ekya::Net::build(n_classes, 0).total;
+}
+
+const char* ekya_status_str(ekya_status s) {
+  switch (s) {
+    case EKYA_OK: return "ok";
+    case EKYA_ERR_INVALID_ARG: return "invalid argument";
+    case EKYA_ERR_NOMEM: return "out of device memory";
+    case EKYA_ERR_HIP: return "HIP runtime error";
+    case EKYA_ERR_NONFINITE: return "non-finite training loss";
+    case EKYA_ERR_UNSUPPORTED: return "unsupported";
+  }
+  return "unknown status";
+}
+
+const char* ekya_last_error(const ekya_ctx* ctx) {
+  return ctx ? ctx->c.err.c_str() : g_noctx_err.c_str();
+}
+
+ekya_status ekya_create(ekya_ctx** out, int hip_device, int n_classes) {
+  if (!out) return fail(nullptr, EKYA_ERR_INVALID_ARG, "out is null");
+  *out = nullptr;
+  if (n_classes < 1 || n_classes > 1024)
+    return fail(nullptr, EKYA_ERR_INVALID_ARG, "n_classes must be in [1, 1024]");
+  int n = 0;
+  if (hipGetDeviceCount(&n) != hipSuccess || n == 0)
+    return fail(nullptr, EKYA_ERR_HIP, "no HIP device available");
+  if (hip_device < 0 || hip_device >= n)
+    return fail(nullptr, EKYA_ERR_INVALID_ARG, "hip_device out of range");
+  ekya_ctx* c = new (std::nothrow) ekya_ctx();
+  if (!c) return fail(nullptr, EKYA_ERR_NOMEM, "host allocation failed");
+  hipError_t e = ekya::ctx_init(c->c, hip_device, n_classes);
+  if (e != hipSuccess) {
+    ekya::ctx_free(c->c);
+    delete c;
+    return fail(nullptr, e == hipErrorOutOfMemory ? EKYA_ERR_NOMEM : EKYA_ERR_HIP,
+                std::string("HIP error: ") + hipGetErrorString(e));
+  }
+  *out = c;
+  return EKYA_OK;
+}
+
+void ekya_destroy(ekya_ctx* ctx) {
+  if (!ctx) return;
+  ekya::ctx_free(ctx->c);
+  delete ctx;
+}
+
+static ekya_status check_train(ekya_ctx* ctx, int k, double frac, int epochs, float lr, float mu,
+                               int batch) {
+  if (k < 1 || k > 6) return fail(ctx, EKYA_ERR_INVALID_ARG, "k_trainable must be in [1, 6]");
+  if (!(frac > 0.0 && frac <= 1.0))
+    return fail(ctx, EKYA_ERR_INVALID_ARG, "subsample_frac must be in (0, 1]");
+  if (epochs < 1 || epochs > EKYA_MAX_EPOCHS)
+    return fail(ctx, EKYA_ERR_INVALID_ARG, "epochs must be in [1, EKYA_MAX_EPOCHS]");
+  if (!(lr > 0.f) || !std::isfinite(lr)) return fail(ctx, EKYA_ERR_INVALID_ARG, "lr must be > 0");
+  if (!(mu >= 0.f && mu < 1.f)) return fail(ctx, EKYA_ERR_INVALID_ARG, "momentum must be in [0, 1)");
+  if (batch < 1 || batch > 4096) return fail(ctx, EKYA_ERR_INVALID_ARG, "batch must be in [1, 4096]");
+  return EKYA_OK;
+}
+
+ekya_status ekya_retrain(ekya_ctx* ctx, float* weights, int k_trainable, const void* frames,
+                         const int32_t* labels, int n_frames, int H, int W,
+                         const void* heldout_frames, const int32_t* heldout_labels, int n_heldout,
+                         const ekya_train_opts* opts, ekya_retrain_result* result, void* stream) {
+  if (!ctx) return fail(nullptr, EKYA_ERR_INVALID_ARG, "ctx is null");
+  if (!weights || !frames || !labels || !heldout_frames || !heldout_labels || !opts || !result)
+    return fail(ctx, EKYA_ERR_INVALID_ARG, "null pointer argument");
+  if (n_frames < 1 || n_frames > (1 << 24))
+    return fail(ctx, EKYA_ERR_INVALID_ARG, "n_frames must be in [1, 2^24]");
+  if (n_heldout < 1 || n_heldout > (1 << 24))
+    return fail(ctx, EKYA_ERR_INVALID_ARG, "n_heldout must be in [1, 2^24]");
+  if (ekya_status s = check_frames(ctx, H, W)) return s;
+  if (!valid_precision(opts->precision))
+    return fail(ctx, EKYA_ERR_INVALID_ARG, "precision must be EKYA_FP32 or EKYA_BF16");
+  if (ekya_status s = check_train(ctx, k_trainable, opts->subsample_frac, opts->epochs, opts->lr,
+                                  opts->momentum, opts->batch))
+    return s;
+  if (result->step_loss_capacity < 0 || (result->step_loss_capacity > 0 && !result->step_loss))
+    return fail(ctx, EKYA_ERR_INVALID_ARG, "step_loss capacity without a buffer");
+  ctx->c.err.clear();
+  return ekya::run_retrain(ctx->c, weights, k_trainable, frames, labels, n_frames, H, W,
+                           heldout_frames, heldout_labels, n_heldout, *opts, result,
+                           (hipStream_t)stream);
+}
+
+ekya_status ekya_profile(ekya_ctx* ctx, const float* weights, const ekya_profile_cfg* cfgs,
+                         int n_cfgs, const void* frames, const int32_t* labels, int n_frames,
+                         int H, int W, const void* heldout_frames, const int32_t* heldout_labels,
+                         int n_heldout, uint64_t subsample_seed, int precision, int concurrent,
+                         ekya_profile_result* results) {
+  if (!ctx) return fail(nullptr, EKYA_ERR_INVALID_ARG, "ctx is null");
+  if (!weights || !cfgs || !frames || !labels || !heldout_frames || !heldout_labels || !results)
+    return fail(ctx, EKYA_ERR_INVALID_ARG, "null pointer argument");
+  if (n_cfgs < 1 || n_cfgs > 256) return fail(ctx, EKYA_ERR_INVALID_ARG, "n_cfgs must be in [1, 256]");
+  if (n_frames < 1 || n_frames > (1 << 24))
+    return fail(ctx, EKYA_ERR_INVALID_ARG, "n_frames must be in [1, 2^24]");
+  if (n_heldout < 1 || n_heldout > (1 << 24))
+    return fail(ctx, EKYA_ERR_INVALID_ARG, "n_heldout must be in [1, 2^24]");
+  if (ekya_status s = check_frames(ctx, H, W)) return s;
+  if (!valid_precision(precision))
+    return fail(ctx, EKYA_ERR_INVALID_ARG, "precision must be EKYA_FP32 or EKYA_BF16");
+  for (int i = 0; i < n_cfgs; ++i) {
+    const ekya_profile_cfg& c = cfgs[i];
+    if (ekya_status s = check_train(ctx, c.k_trainable, c.subsample_frac, c.epochs, c.lr, c.momentum,
+                                    c.batch))
+      return s;
+  }
+  ctx->c.err.clear();
+  return ekya::run_profile(ctx->c, weights, cfgs, n_cfgs, frames, labels, n_frames, H, W,
+                           heldout_frames, heldout_labels, n_heldout, subsample_seed, precision,
+                           concurrent, results);
+}
+
+ekya_status ekya_infer(ekya_ctx* ctx, const float* weights, const void* frames, int n, int H,
+                       int W, int resolution, int precision, int32_t* labels_out, void* stream) {
+  if (!ctx) return fail(nullptr, EKYA_ERR_INVALID_ARG, "ctx is null");
+  if (n < 0 || n > (1 << 26)) return fail(ctx, EKYA_ERR_INVALID_ARG, "n must be in [0, 2^26]");
+  if (n == 0) return EKYA_OK;
+  if (!weights || !frames || !labels_out) return fail(ctx, EKYA_ERR_INVALID_ARG, "null pointer argument");
+  if (ekya_status s = check_frames(ctx, H, W)) return s;
+  if (resolution < 32 || resolution > 4096)
+    return fail(ctx, EKYA_ERR_INVALID_ARG, "resolution must be in [32, 4096]");
+  if (!valid_precision(precision))
+    return fail(ctx, EKYA_ERR_INVALID_ARG, "precision must be EKYA_FP32 or EKYA_BF16");
+  ctx->c.err.clear();
+  return ekya::run_infer(ctx->c, weights, frames, n, H, W, resolution, precision, labels_out,
+                         (hipStream_t)stream);
+}
+
+int ekya_training_subset(int n_frames, double subsample_frac, uint64_t seed, int32_t* idx_out,
+                         int capacity) {
+  if (n_frames < 1 || !(subsample_frac > 0.0 && subsample_frac <= 1.0) || !idx_out) return -1;
+  const int n = ekya::subset_count(n_frames, subsample_frac);
+  if (n > capacity) return -1;
+  std::vector<int32_t> s = ekya::training_subset(n_frames, subsample_frac, seed);
+  std::memcpy(idx_out, s.data(), n * sizeof(int32_t));
+  return n;
+}
+
+int ekya_epoch_order(int n, uint64_t seed, int epoch, int32_t* order_out) {
+  if (n < 1 || epoch < 0 || !order_out) return -1;
+  std::vector<int32_t> o = ekya::epoch_order(n, seed, epoch);
+  std::memcpy(order_out, o.data(), n * sizeof(int32_t));
+  return 0;
+}
+
+}  // extern "C"
+
+// ------------------------------------------------------------------ ops
+namespace {
+
+struct Tmp {
+  std::vector<void*> ptrs;
+  ~Tmp() {
+    for (void* p : ptrs) (void)hipFree(p);
+  }
+  template <typename T> T* get(size_t n) {
+    void* p = nullptr;
+    if (hipMalloc(&p, std::max<size_t>(n, 1) * sizeof(T) + 64) != hipSuccess) return nullptr;
+    ptrs.push_back(p);
+    return reinterpret_cast<T*>(p);
+  }
+};
+
+bool chan_ok(int dt, int C, bool allow3) {
+  if (allow3 && C == 3) return true;
+  return C > 0 && C % ekya::dtype_vec(dt) == 0;
+}
+
+// Repack fp32 [K][C][R][S] weights into the kernels' low-precision layouts.
+hipError_t pack_one(int dt, const float* w, int K, int C, int R, int S, int Cp, Tmp& tmp,
+                    void** krsc, void** crsk, hipStream_t st) {
+  const long long n = (long long)K * C * R * S;
+  float* m = tmp.get<float>(n);
+  long long* tab = tmp.get<long long>(16);
+  const size_t es = ekya::dtype_size(dt);
+  char* sh = tmp.get<char>((size_t)(K * R * S * Cp + n) * es);
+  if (!m || !tab || !sh) return hipErrorOutOfMemory;
+  long long h[13] = {0, K, C, R, S, 0, K, R, S, C, Cp, 0, (long long)K * R * S * Cp};
+  EKYA_HIP(hipMemcpy(tab, h, sizeof(h), hipMemcpyHostToDevice));
+  EKYA_HIP(ekya::permute_weights(w, m, tab, 1, n, 1, st));
+  EKYA_HIP(ekya::pack_conv_weights(dt, m, tab + 5, 1, sh, st));
+  *krsc = sh;
+  *crsk = sh + (size_t)K * R * S * Cp * es;
+  return hipSuccess;
+}
+
+hipError_t pad_input(int dt, const void* x, int N, int H, int W, int C, int& Cp, Tmp& tmp,
+                     const void** xp, hipStream_t st) {
+  Cp = C;
+  *xp = x;
+  if (C != 3) return hipSuccess;
+  Cp = ekya::dtype_vec(dt);
+  void* p = tmp.get<char>((size_t)N * H * W * Cp * ekya::dtype_size(dt));
+  if (!p) return hipErrorOutOfMemory;
+  EKYA_HIP(ekya::frames_to_padded(dt, x, nullptr, N, H, W, Cp, p, st));
+  *xp = p;
+  return hipSuccess;
+}
+
+ekya::ConvGeom make_geom(int N, int H, int W, int Cp, int K, int R, int S, int stride, int pad) {
+  ekya::ConvGeom g;
+  g.N = N; g.H = H; g.W = W; g.C = Cp; g.K = K; g.R = R; g.S = S;
+  g.stride = stride; g.pad = pad;
+  g.P = (H + 2 * pad - R) / stride + 1;
+  g.Q = (W + 2 * pad - S) / stride + 1;
+  return g;
+}
+
+bool conv_args_ok(int dt, int N, int H, int W, int C, int K, int R, int S, int stride, int pad,
+                  bool allow3) {
+  if (!valid_precision(dt) || N < 1 || H < 1 || W < 1 || K < 1 || R < 1 || S < 1 || stride < 1 ||
+      pad < 0)
+    return false;
+  if (!chan_ok(dt, C, allow3) || K % ekya::dtype_vec(dt) != 0) return false;
+  if (H + 2 * pad < R || W + 2 * pad < S) return false;
+  return true;
+}
+
+ekya_status sync_status(hipStream_t st, hipError_t e) {
+  if (e == hipSuccess) e = hipStreamSynchronize(st);
+  return hip_status(e);
+}
+
+}  // namespace
+
+extern "C" {
+
+ekya_status ekya_op_conv2d(int precision, const void* x, int N, int H, int W, int C,
+                           const float* w, int K, int R, int S, int stride, int pad, void* y,
+                           void* stream) {
+  if (!x || !w || !y || !conv_args_ok(precision, N, H, W, C, K, R, S, stride, pad, true))
+    return fail(nullptr, EKYA_ERR_INVALID_ARG, "invalid conv2d arguments");
+  hipStream_t st = (hipStream_t)stream;
+  Tmp tmp;
+  int Cp;
+  const void* xp;
+  void *krsc, *crsk;
+  hipError_t e = pad_input(precision, x, N, H, W, C, Cp, tmp, &xp, st);
+  if (e == hipSuccess) e = pack_one(precision, w, K, C, R, S, Cp, tmp, &krsc, &crsk, st);
+  if (e == hipSuccess)
+    e = ekya::conv_fwd(precision, make_geom(N, H, W, Cp, K, R, S, stride, pad), xp, krsc, y,
+                       ekya::ConvEpilogue(), st);
+  return sync_status(st, e);
+}
+
+ekya_status ekya_op_conv2d_dgrad(int precision, const void* dy, const float* w, int N, int H,
+                                 int W, int C, int K, int R, int S, int stride, int pad, void* dx,
+                                 void* stream) {
+  if (!dy || !w || !dx || !conv_args_ok(precision, N, H, W, C, K, R, S, stride, pad, false))
+    return fail(nullptr, EKYA_ERR_INVALID_ARG, "invalid conv2d_dgrad arguments");
+  hipStream_t st = (hipStream_t)stream;
+  Tmp tmp;
+  void *krsc, *crsk;
+  hipError_t e = pack_one(precision, w, K, C, R, S, C, tmp, &krsc, &crsk, st);
+  if (e == hipSuccess)
+    e = ekya::conv_dgrad(precision, make_geom(N, H, W, C, K, R, S, stride, pad), dy, crsk, dx,
+                         nullptr, st);
+  return sync_status(st, e);
+}
+
+ekya_status ekya_op_conv2d_wgrad(int precision, const void* x, const void* dy, int N, int H,
+                                 int W, int C, int K, int R, int S, int stride, int pad,
+                                 float* dw, void* stream) {
+  if (!x || !dy || !dw || !conv_args_ok(precision, N, H, W, C, K, R, S, stride, pad, true))
+    return fail(nullptr, EKYA_ERR_INVALID_ARG, "invalid conv2d_wgrad arguments");
+  hipStream_t st = (hipStream_t)stream;
+  Tmp tmp;
+  int Cp;
+  const void* xp;
+  hipError_t e = pad_input(precision, x, N, H, W, C, Cp, tmp, &xp, st);
+  ekya::ConvGeom g = make_geom(N, H, W, Cp, K, R, S, stride, pad);
+  float* part = tmp.get<float>(ekya::conv_wgrad_workspace_floats(precision, g));
+  float* krsc = tmp.get<float>((size_t)K * R * S * C);
+  long long* tab = tmp.get<long long>(8);
+  if (!part || !krsc || !tab) e = hipErrorOutOfMemory;
+  if (e == hipSuccess) e = ekya::conv_wgrad(precision, g, xp, dy, part, krsc, C, st);
+  if (e == hipSuccess) {
+    long long h[5] = {0, K, C, R, S};
+    e = hipMemcpy(tab, h, sizeof(h), hipMemcpyHostToDevice);
+  }
+  if (e == hipSuccess) e = ekya::permute_weights(krsc, dw, tab, 1, (long long)K * C * R * S, 0, st);
+  return sync_status(st, e);
+}
+
+ekya_status ekya_op_batchnorm_train(int precision, const void* z, long long M, int C,
+                                    const float* gamma, const float* beta, float* running_mean,
+                                    float* running_var, int relu, void* y, float* mean_out,
+                                    float* invstd_out, void* stream) {
+  if (!valid_precision(precision) || !z || !gamma || !beta || !y || !mean_out || !invstd_out ||
+      M < 1 || !chan_ok(precision, C, false) || C > 2048 ||
+      (running_mean == nullptr) != (running_var == nullptr))
+    return fail(nullptr, EKYA_ERR_INVALID_ARG, "invalid batchnorm_train arguments");
+  hipStream_t st = (hipStream_t)stream;
+  Tmp tmp;
+  float* part = tmp.get<float>(ekya::bn_partials_floats(M, C));
+  float* ss = tmp.get<float>(2 * (size_t)C);
+  hipError_t e = (part && ss) ? hipSuccess : hipErrorOutOfMemory;
+  if (e == hipSuccess)
+    e = ekya::bn_train_stats(precision, z, M, C, gamma, beta, running_mean, running_var, mean_out,
+                             invstd_out, ss, ss + C, part, st);
+  if (e == hipSuccess) e = ekya::bn_apply(precision, z, M, C, mean_out, ss, beta, nullptr, relu, y, st);
+  return sync_status(st, e);
+}
+
+ekya_status ekya_op_batchnorm_backward(int precision, const void* dy, const void* y_relu,
+                                       const void* z, long long M, int C, const float* gamma,
+                                       const float* mean, const float* invstd, void* dz,
+                                       float* dgamma, float* dbeta, void* stream) {
+  if (!valid_precision(precision) || !dy || !z || !gamma || !mean || !invstd || !dz || !dgamma ||
+      !dbeta || M < 1 || !chan_ok(precision, C, false) || C > 2048)
+    return fail(nullptr, EKYA_ERR_INVALID_ARG, "invalid batchnorm_backward arguments");
+  hipStream_t st = (hipStream_t)stream;
+  Tmp tmp;
+  float* part = tmp.get<float>(ekya::bn_partials_floats(M, C));
+  hipError_t e = part ? hipSuccess : hipErrorOutOfMemory;
+  if (e == hipSuccess)
+    e = ekya::bn_backward(precision, dy, y_relu, z, M, C, gamma, mean, invstd, dgamma, dbeta, dz,
+                          nullptr, part, st);
+  return sync_status(st, e);
+}
+
+ekya_status ekya_op_maxpool(int precision, const void* x, int N, int H, int W, int C, void* y,
+                            uint8_t* arg, void* stream) {
+  if (!valid_precision(precision) || !x || !y || N < 1 || H < 1 || W < 1 ||
+      !chan_ok(precision, C, false))
+    return fail(nullptr, EKYA_ERR_INVALID_ARG, "invalid maxpool arguments");
+  hipStream_t st = (hipStream_t)stream;
+  return sync_status(st, ekya::maxpool_fwd(precision, x, N, H, W, C, y, arg, st));
+}
+
+ekya_status ekya_op_maxpool_backward(int precision, const void* dy, const uint8_t* arg, int N,
+                                     int H, int W, int C, void* dx, void* stream) {
+  if (!valid_precision(precision) || !dy || !arg || !dx || N < 1 || H < 1 || W < 1 ||
+      !chan_ok(precision, C, false))
+    return fail(nullptr, EKYA_ERR_INVALID_ARG, "invalid maxpool_backward arguments");
+  hipStream_t st = (hipStream_t)stream;
+  return sync_status(st, ekya::maxpool_bwd(precision, dy, arg, N, H, W, C, dx, st));
+}
+
+ekya_status ekya_op_avgpool(int precision, const void* x, int N, int H, int W, int C, float* f,
+                            void* stream) {
+  if (!valid_precision(precision) || !x || !f || N < 1 || H < 1 || W < 1 || C < 1)
+    return fail(nullptr, EKYA_ERR_INVALID_ARG, "invalid avgpool arguments");
+  hipStream_t st = (hipStream_t)stream;
+  return sync_status(st, ekya::avgpool_fwd(precision, x, N, H * W, C, f, st));
+}
+
+ekya_status ekya_op_avgpool_backward(int precision, const float* df, int N, int H, int W, int C,
+                                     void* dx, void* stream) {
+  if (!valid_precision(precision) || !df || !dx || N < 1 || H < 1 || W < 1 || C < 1)
+    return fail(nullptr, EKYA_ERR_INVALID_ARG, "invalid avgpool_backward arguments");
+  hipStream_t st = (hipStream_t)stream;
+  return sync_status(st, ekya::avgpool_bwd(precision, df, N, H * W, C, dx, st));
+}
+
+ekya_status ekya_op_linear(const float* f, const float* Wt, const float* b, int N, int I, int J,
+                           float* z, void* stream) {
+  if (!f || !Wt || !b || !z || N < 1 || I < 1 || J < 1)
+    return fail(nullptr, EKYA_ERR_INVALID_ARG, "invalid linear arguments");
+  hipStream_t st = (hipStream_t)stream;
+  return sync_status(st, ekya::fc_fwd(f, Wt, b, N, I, J, z, st));
+}
+
+ekya_status ekya_op_linear_backward(const float* dz, const float* f, const float* Wt, int N,
+                                    int I, int J, float* dW, float* db, float* df, void* stream) {
+  if (!dz || !f || !Wt || !dW || !db || N < 1 || I < 1 || J < 1)
+    return fail(nullptr, EKYA_ERR_INVALID_ARG, "invalid linear_backward arguments");
+  hipStream_t st = (hipStream_t)stream;
+  return sync_status(st, ekya::fc_bwd(dz, f, Wt, N, I, J, dW, db, df, st));
+}
+
+ekya_status ekya_op_softmax_ce(const float* z, const int32_t* labels, int N, int J, float* dz,
+                               float* out, void* stream) {
+  if (!z || !labels || !dz || !out || N < 1 || J < 1)
+    return fail(nullptr, EKYA_ERR_INVALID_ARG, "invalid softmax_ce arguments");
+  hipStream_t st = (hipStream_t)stream;
+  return sync_status(st, ekya::softmax_ce(z, labels, nullptr, N, J, dz, out, st));
+}
+
+ekya_status ekya_op_sgd(float* w, float* v, const float* g, long long n, float lr, float mu,
+                        void* stream) {
+  if (!w || !v || !g || n < 0) return fail(nullptr, EKYA_ERR_INVALID_ARG, "invalid sgd arguments");
+  hipStream_t st = (hipStream_t)stream;
+  return sync_status(st, ekya::sgd_momentum(w, v, g, n, lr, mu, st));
+}
+
+ekya_status ekya_op_resize(int precision, const void* frames, int n, int H, int W, int r,
+                           void* out, void* stream) {
+  if (!valid_precision(precision) || !frames || !out || n < 1 || H < 1 || W < 1 || r < 1)
+    return fail(nullptr, EKYA_ERR_INVALID_ARG, "invalid resize arguments");
+  hipStream_t st = (hipStream_t)stream;
+  return sync_status(st, ekya::resize_to_padded(precision, frames, n, H, W, r, 3, out, st));
+}
+
+}  // extern "C"

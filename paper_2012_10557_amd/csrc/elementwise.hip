@@ -1,0 +1,832 @@
+// Memory-bound kernels of the retraining step: BatchNorm statistics, apply and
+// backward; pooling; the classifier layer; softmax cross-entropy; SGD with
+// momentum; frame gather / padding / resize; weight repacking.  Every
+// reduction is two-level with a fixed order, so results do not depend on
+// scheduling (concurrent and sequential runs are bitwise equal).
+#include <algorithm>
+#include <type_traits>
+
+#include "kernels.hpp"
+
+namespace ekya {
+namespace {
+
+constexpr float BN_EPS = 1e-5f;
+constexpr float BN_MOMENTUM = 0.1f;
+
+template <typename T> __device__ __forceinline__ void unit_to_f(uint4 u, float* v) {
+  Unit<T> x;
+  x.u = u;
+#pragma unroll
+  for (int i = 0; i < Elt<T>::E; ++i) v[i] = to_f(x.e[i]);
+}
+template <typename T> __device__ __forceinline__ uint4 f_to_unit(const float* v) {
+  Unit<T> x;
+#pragma unroll
+  for (int i = 0; i < Elt<T>::E; ++i) x.e[i] = from_f<T>(v[i]);
+  return x.u;
+}
+
+inline int grid_for(long long n, int per_block = 256, int cap = 8192) {
+  long long b = cdivl(n, per_block);
+  if (b < 1) b = 1;
+  return (int)std::min<long long>(b, cap);
+}
+
+// Chunking of the M rows for per-channel reductions.
+inline int bn_chunks(long long M) {
+  long long c = cdivl(M, 64);
+  if (c > 1024) c = 1024;
+  if (c < 1) c = 1;
+  return (int)c;
+}
+
+// --------------------------------------------------------- BN statistics
+// Per chunk of rows: shifted sums S1 = sum(z - K), S2 = sum((z - K)^2) with the
+// shift K[c] = z[0][c]; all chunks share K, so the final sums are plain adds.
+template <typename T>
+__global__ __launch_bounds__(256) void bn_stats_partial(const T* z, long long M, int C,
+                                                        long long rows_per_chunk, float* part) {
+  constexpr int E = Elt<T>::E;
+  const int tpr = C / E;              // threads per row
+  const int rpi = 256 / tpr;          // rows in flight
+  const int t = threadIdx.x;
+  const int cu = t % tpr, rsub = t / tpr;
+  const long long r0 = blockIdx.x * rows_per_chunk;
+  const long long r1 = std::min<long long>(M, r0 + rows_per_chunk);
+  float s1[E], s2[E], K[E];
+#pragma unroll
+  for (int i = 0; i < E; ++i) s1[i] = s2[i] = 0.f;
+  if (rsub < rpi) {
+    unit_to_f<T>(*reinterpret_cast<const uint4*>(z + cu * E), K);
+    for (long long r = r0 + rsub; r < r1; r += rpi) {
+      float v[E];
+      unit_to_f<T>(*reinterpret_cast<const uint4*>(z + r * C + cu * E), v);
+#pragma unroll
+      for (int i = 0; i < E; ++i) {
+        float d = v[i] - K[i];
+        s1[i] += d;
+        s2[i] += d * d;
+      }
+    }
+  }
+  __shared__ float sh[2][256 * 8];
+#pragma unroll
+  for (int i = 0; i < E; ++i) {
+    sh[0][t * E + i] = s1[i];
+    sh[1][t * E + i] = s2[i];
+  }
+  __syncthreads();
+  // thread c (< C) sums the rpi partials of channel c in a fixed order
+  for (int c = t; c < C; c += 256) {
+    int u = c / E, i = c % E;
+    float a = 0.f, b = 0.f;
+    for (int rs = 0; rs < rpi; ++rs) {
+      a += sh[0][(rs * tpr + u) * E + i];
+      b += sh[1][(rs * tpr + u) * E + i];
+    }
+    part[(long long)blockIdx.x * 2 * C + c] = a;
+    part[(long long)blockIdx.x * 2 * C + C + c] = b;
+  }
+}
+
+template <typename T>
+__global__ void bn_stats_final(const T* z, const float* part, int nchunks, long long M, int C,
+                               const float* gamma, const float* beta, float* rm, float* rv,
+                               float* mean, float* invstd, float* scale, float* shift) {
+  int c = blockIdx.x * blockDim.x + threadIdx.x;
+  if (c >= C) return;
+  double a = 0.0, b = 0.0;
+  for (int k = 0; k < nchunks; ++k) {
+    a += part[(long long)k * 2 * C + c];
+    b += part[(long long)k * 2 * C + C + c];
+  }
+  const double Kc = (double)to_f(z[c]);
+  const double d = a / (double)M;
+  double var = b / (double)M - d * d;
+  if (var < 0.0) var = 0.0;
+  const float mu = (float)(Kc + d);
+  const float is = (float)(1.0 / sqrt(var + (double)BN_EPS));
+  mean[c] = mu;
+  invstd[c] = is;
+  const float sc = gamma[c] * is;
+  scale[c] = sc;
+  shift[c] = beta[c] - mu * sc;
+  if (rm) {
+    const double unb = M > 1 ? var * (double)M / (double)(M - 1) : var;
+    rm[c] = (1.f - BN_MOMENTUM) * rm[c] + BN_MOMENTUM * mu;
+    rv[c] = (1.f - BN_MOMENTUM) * rv[c] + BN_MOMENTUM * (float)unb;
+  }
+}
+
+template <typename T>
+__global__ void bn_apply_kernel(const T* z, long long units, int C, const float* mean,
+                                const float* scale, const float* beta, const T* res, int relu,
+                                T* y) {
+  constexpr int E = Elt<T>::E;
+  for (long long u = blockIdx.x * (long long)blockDim.x + threadIdx.x; u < units;
+       u += (long long)gridDim.x * blockDim.x) {
+    const int c0 = (int)((u * E) % C);
+    float v[E], r[E];
+    unit_to_f<T>(reinterpret_cast<const uint4*>(z)[u], v);
+    if (res) unit_to_f<T>(reinterpret_cast<const uint4*>(res)[u], r);
+#pragma unroll
+    for (int i = 0; i < E; ++i) {
+      // (z - mean) * scale + beta: no cancellation when invstd is large
+      float t = (v[i] - mean[c0 + i]) * scale[c0 + i] + beta[c0 + i];
+      if (res) t += r[i];
+      if (relu) t = fmaxf(t, 0.f);
+      v[i] = t;
+    }
+    reinterpret_cast<uint4*>(y)[u] = f_to_unit<T>(v);
+  }
+}
+
+// tab row: gamma_off, beta_off, rm_off, rv_off, C, out_off
+__global__ void bn_fold_kernel(const float* p, const long long* tab, float* out) {
+  const long long* t = tab + 6 * blockIdx.x;
+  const int C = (int)t[4];
+  for (int c = threadIdx.x; c < C; c += blockDim.x) {
+    float sc = p[t[0] + c] / sqrtf(p[t[3] + c] + BN_EPS);
+    out[t[5] + c] = sc;
+    out[t[5] + C + c] = p[t[1] + c] - p[t[2] + c] * sc;
+  }
+}
+
+// ------------------------------------------------------------ BN backward
+// partials: S_g = sum g, S_gx = sum g * (z - mean), g = dy * [y > 0].
+template <typename T>
+__global__ __launch_bounds__(256) void bn_bwd_partial(const T* dy, const T* y, const T* z,
+                                                      long long M, int C,
+                                                      long long rows_per_chunk,
+                                                      const float* mean, float* part) {
+  constexpr int E = Elt<T>::E;
+  const int tpr = C / E;
+  const int rpi = 256 / tpr;
+  const int t = threadIdx.x;
+  const int cu = t % tpr, rsub = t / tpr;
+  const long long r0 = blockIdx.x * rows_per_chunk;
+  const long long r1 = std::min<long long>(M, r0 + rows_per_chunk);
+  float s1[E], s2[E], mu[E];
+#pragma unroll
+  for (int i = 0; i < E; ++i) {
+    s1[i] = s2[i] = 0.f;
+    mu[i] = mean[cu * E + i];
+  }
+  if (rsub < rpi) {
+    for (long long r = r0 + rsub; r < r1; r += rpi) {
+      const long long off = r * C + cu * E;
+      float g[E], zz[E];
+      unit_to_f<T>(*reinterpret_cast<const uint4*>(dy + off), g);
+      unit_to_f<T>(*reinterpret_cast<const uint4*>(z + off), zz);
+      if (y) {
+        float yy[E];
+        unit_to_f<T>(*reinterpret_cast<const uint4*>(y + off), yy);
+#pragma unroll
+        for (int i = 0; i < E; ++i) g[i] = yy[i] > 0.f ? g[i] : 0.f;
+      }
+#pragma unroll
+      for (int i = 0; i < E; ++i) {
+        s1[i] += g[i];
+        s2[i] += g[i] * (zz[i] - mu[i]);
+      }
+    }
+  }
+  __shared__ float sh[2][256 * 8];
+#pragma unroll
+  for (int i = 0; i < E; ++i) {
+    sh[0][t * E + i] = s1[i];
+    sh[1][t * E + i] = s2[i];
+  }
+  __syncthreads();
+  for (int c = t; c < C; c += 256) {
+    int u = c / E, i = c % E;
+    float a = 0.f, b = 0.f;
+    for (int rs = 0; rs < rpi; ++rs) {
+      a += sh[0][(rs * tpr + u) * E + i];
+      b += sh[1][(rs * tpr + u) * E + i];
+    }
+    part[(long long)blockIdx.x * 2 * C + c] = a;
+    part[(long long)blockIdx.x * 2 * C + C + c] = b;
+  }
+}
+
+// coef[3C]: dz = a*g + b + c*(z - mean)
+__global__ void bn_bwd_final(const float* part, int nchunks, long long M, int C,
+                             const float* gamma, const float* invstd, float* dgamma, float* dbeta,
+                             float* coef) {
+  int c = blockIdx.x * blockDim.x + threadIdx.x;
+  if (c >= C) return;
+  double sg = 0.0, sgx = 0.0;
+  for (int k = 0; k < nchunks; ++k) {
+    sg += part[(long long)k * 2 * C + c];
+    sgx += part[(long long)k * 2 * C + C + c];
+  }
+  const float is = invstd[c];
+  const float db = (float)sg;
+  const float dg = (float)(sgx * (double)is);
+  dbeta[c] = db;
+  dgamma[c] = dg;
+  const float a = gamma[c] * is;
+  coef[c] = a;
+  coef[C + c] = -a * db / (float)M;
+  coef[2 * C + c] = -a * is * dg / (float)M;
+}
+
+template <typename T>
+__global__ void bn_bwd_apply(const T* dy, const T* y, const T* z, long long units, int C,
+                             const float* mean, const float* coef, T* dz, T* g_out) {
+  constexpr int E = Elt<T>::E;
+  for (long long u = blockIdx.x * (long long)blockDim.x + threadIdx.x; u < units;
+       u += (long long)gridDim.x * blockDim.x) {
+    const int c0 = (int)((u * E) % C);
+    float g[E], zz[E];
+    unit_to_f<T>(reinterpret_cast<const uint4*>(dy)[u], g);
+    unit_to_f<T>(reinterpret_cast<const uint4*>(z)[u], zz);
+    if (y) {
+      float yy[E];
+      unit_to_f<T>(reinterpret_cast<const uint4*>(y)[u], yy);
+#pragma unroll
+      for (int i = 0; i < E; ++i) g[i] = yy[i] > 0.f ? g[i] : 0.f;
+    }
+    if (g_out) reinterpret_cast<uint4*>(g_out)[u] = f_to_unit<T>(g);
+    float o[E];
+#pragma unroll
+    for (int i = 0; i < E; ++i) {
+      const int c = c0 + i;
+      o[i] = coef[c] * g[i] + coef[C + c] + coef[2 * C + c] * (zz[i] - mean[c]);
+    }
+    reinterpret_cast<uint4*>(dz)[u] = f_to_unit<T>(o);
+  }
+}
+
+// ---------------------------------------------------------------- pooling
+template <typename T>
+__global__ void maxpool_fwd_kernel(const T* x, int N, int H, int W, int C, int P, int Q, T* y,
+                                   uint8_t* arg) {
+  constexpr int E = Elt<T>::E;
+  const int cu = C / E;
+  const long long units = (long long)N * P * Q * cu;
+  for (long long u = blockIdx.x * (long long)blockDim.x + threadIdx.x; u < units;
+       u += (long long)gridDim.x * blockDim.x) {
+    const int c0 = (int)(u % cu) * E;
+    const long long pix = u / cu;
+    const int q = (int)(pix % Q), p = (int)((pix / Q) % P), n = (int)(pix / ((long long)P * Q));
+    float best[E];
+    int ba[E];
+#pragma unroll
+    for (int i = 0; i < E; ++i) {
+      best[i] = -INFINITY;
+      ba[i] = 0;
+    }
+    for (int r = 0; r < 3; ++r) {
+      const int h = 2 * p + r - 1;
+      if (h < 0 || h >= H) continue;
+      for (int s = 0; s < 3; ++s) {
+        const int w = 2 * q + s - 1;
+        if (w < 0 || w >= W) continue;
+        float v[E];
+        unit_to_f<T>(*reinterpret_cast<const uint4*>(x + (((long long)n * H + h) * W + w) * C + c0), v);
+#pragma unroll
+        for (int i = 0; i < E; ++i)
+          if (v[i] > best[i]) {
+            best[i] = v[i];
+            ba[i] = r * 3 + s;
+          }
+      }
+    }
+    reinterpret_cast<uint4*>(y)[u] = f_to_unit<T>(best);
+    if (arg) {
+#pragma unroll
+      for (int i = 0; i < E; ++i) arg[u * E + i] = (uint8_t)ba[i];
+    }
+  }
+}
+
+template <typename T>
+__global__ void maxpool_bwd_kernel(const T* dy, const uint8_t* arg, int N, int H, int W, int C,
+                                   int P, int Q, T* dx) {
+  constexpr int E = Elt<T>::E;
+  const int cu = C / E;
+  const long long units = (long long)N * H * W * cu;
+  for (long long u = blockIdx.x * (long long)blockDim.x + threadIdx.x; u < units;
+       u += (long long)gridDim.x * blockDim.x) {
+    const int c0 = (int)(u % cu) * E;
+    const long long pix = u / cu;
+    const int w = (int)(pix % W), h = (int)((pix / W) % H), n = (int)(pix / ((long long)H * W));
+    float acc[E];
+#pragma unroll
+    for (int i = 0; i < E; ++i) acc[i] = 0.f;
+    for (int r = 0; r < 3; ++r) {
+      const int hp = h + 1 - r;
+      if (hp < 0 || (hp & 1) || (hp >> 1) >= P) continue;
+      for (int s = 0; s < 3; ++s) {
+        const int wp = w + 1 - s;
+        if (wp < 0 || (wp & 1) || (wp >> 1) >= Q) continue;
+        const long long o = (((long long)n * P + (hp >> 1)) * Q + (wp >> 1)) * C + c0;
+        float g[E];
+        unit_to_f<T>(*reinterpret_cast<const uint4*>(dy + o), g);
+#pragma unroll
+        for (int i = 0; i < E; ++i)
+          if (arg[o + i] == r * 3 + s) acc[i] += g[i];
+      }
+    }
+    reinterpret_cast<uint4*>(dx)[u] = f_to_unit<T>(acc);
+  }
+}
+
+template <typename T>
+__global__ void avgpool_fwd_kernel(const T* x, int N, int HW, int C, float* f) {
+  const long long n_out = (long long)N * C;
+  for (long long i = blockIdx.x * (long long)blockDim.x + threadIdx.x; i < n_out;
+       i += (long long)gridDim.x * blockDim.x) {
+    const int c = (int)(i % C);
+    const long long n = i / C;
+    float s = 0.f;
+    for (int k = 0; k < HW; ++k) s += to_f(x[(n * HW + k) * C + c]);
+    f[i] = s / (float)HW;
+  }
+}
+
+template <typename T>
+__global__ void avgpool_bwd_kernel(const float* df, int N, int HW, int C, T* dx) {
+  const long long n_el = (long long)N * HW * C;
+  const float inv = 1.f / (float)HW;
+  for (long long i = blockIdx.x * (long long)blockDim.x + threadIdx.x; i < n_el;
+       i += (long long)gridDim.x * blockDim.x) {
+    const int c = (int)(i % C);
+    const long long n = i / ((long long)HW * C);
+    dx[i] = from_f<T>(df[n * C + c] * inv);
+  }
+}
+
+// ------------------------------------------------------------- classifier
+__global__ void fc_fwd_kernel(const float* f, const float* W, const float* b, int N, int I, int J,
+                              float* z) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= N * J) return;
+  const int n = i / J, j = i % J;
+  float s = 0.f;
+  for (int k = 0; k < I; ++k) s += f[(long long)n * I + k] * W[(long long)j * I + k];
+  z[i] = s + b[j];
+}
+
+__global__ __launch_bounds__(256) void softmax_ce_kernel(const float* z, const int32_t* labels,
+                                                         const int32_t* idx, int N, int J,
+                                                         float* dz, float* out) {
+  __shared__ float sl[256];
+  __shared__ int sc[256];
+  __shared__ int sn[256];
+  float loss = 0.f;
+  int correct = 0, bad = 0;
+  for (int n = threadIdx.x; n < N; n += 256) {
+    const float* zr = z + (long long)n * J;
+    const int y = labels[idx ? idx[n] : n];
+    if (y < 0 || y >= J) {  // invalid label: flag it, no gradient from this row
+      bad = 1;
+      for (int j = 0; j < J; ++j) dz[(long long)n * J + j] = 0.f;
+      continue;
+    }
+    float m = zr[0];
+    int am = 0;
+    for (int j = 1; j < J; ++j)
+      if (zr[j] > m) {
+        m = zr[j];
+        am = j;
+      }
+    float se = 0.f;
+    for (int j = 0; j < J; ++j) se += expf(zr[j] - m);
+    const float lse = m + logf(se);
+    const float l = lse - zr[y];
+    if (!isfinite(l)) bad = 1;
+    loss += l;
+    correct += (am == y);
+    for (int j = 0; j < J; ++j)
+      dz[(long long)n * J + j] = (expf(zr[j] - lse) - (j == y ? 1.f : 0.f)) / (float)N;
+  }
+  sl[threadIdx.x] = loss;
+  sc[threadIdx.x] = correct;
+  sn[threadIdx.x] = bad;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float L = 0.f;
+    int C = 0, B = 0;
+    for (int t = 0; t < 256; ++t) {
+      L += sl[t];
+      C += sc[t];
+      B |= sn[t];
+    }
+    out[0] = L / (float)N;
+    out[1] = (float)C;
+    out[2] = (float)B;
+  }
+}
+
+__global__ void fc_bwd_w_kernel(const float* dz, const float* f, int N, int I, int J, float* dW,
+                                float* db) {
+  const int t = blockIdx.x * blockDim.x + threadIdx.x;
+  if (t < J * I) {
+    const int j = t / I, i = t % I;
+    float s = 0.f;
+    for (int n = 0; n < N; ++n) s += dz[(long long)n * J + j] * f[(long long)n * I + i];
+    dW[t] = s;
+  }
+  if (t < J) {
+    float s = 0.f;
+    for (int n = 0; n < N; ++n) s += dz[(long long)n * J + t];
+    db[t] = s;
+  }
+}
+
+__global__ void fc_bwd_x_kernel(const float* dz, const float* W, int N, int I, int J, float* df) {
+  const long long t = blockIdx.x * (long long)blockDim.x + threadIdx.x;
+  if (t >= (long long)N * I) return;
+  const int n = (int)(t / I), i = (int)(t % I);
+  float s = 0.f;
+  for (int j = 0; j < J; ++j) s += dz[(long long)n * J + j] * W[(long long)j * I + i];
+  df[t] = s;
+}
+
+__global__ __launch_bounds__(256) void count_correct_kernel(const float* z, const int32_t* labels,
+                                                            int N, int J, int32_t* count) {
+  __shared__ int sc[256];
+  int c = 0;
+  for (int n = threadIdx.x; n < N; n += 256) {
+    const float* zr = z + (long long)n * J;
+    float m = zr[0];
+    int am = 0;
+    for (int j = 1; j < J; ++j)
+      if (zr[j] > m) {
+        m = zr[j];
+        am = j;
+      }
+    c += (am == labels[n]);
+  }
+  sc[threadIdx.x] = c;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int s = 0;
+    for (int t = 0; t < 256; ++t) s += sc[t];
+    *count += s;
+  }
+}
+
+__global__ void argmax_kernel(const float* z, int N, int J, int32_t* out) {
+  const int n = blockIdx.x * blockDim.x + threadIdx.x;
+  if (n >= N) return;
+  const float* zr = z + (long long)n * J;
+  float m = zr[0];
+  int am = 0;
+  for (int j = 1; j < J; ++j)
+    if (zr[j] > m) {
+      m = zr[j];
+      am = j;
+    }
+  out[n] = am;
+}
+
+// --------------------------------------------------------------- optimiser
+__global__ void sgd_kernel(float* w, float* v, const float* g, long long n, float lr, float mu) {
+  for (long long i = blockIdx.x * (long long)blockDim.x + threadIdx.x; i < n;
+       i += (long long)gridDim.x * blockDim.x) {
+    const float vn = mu * v[i] + g[i];
+    v[i] = vn;
+    w[i] = w[i] - lr * vn;
+  }
+}
+
+// ----------------------------------------------------------- data movement
+__global__ void gather_rows_kernel(const uint4* src, const int32_t* idx, int n, long long row_units,
+                                   uint4* dst) {
+  const long long total = (long long)n * row_units;
+  for (long long t = blockIdx.x * (long long)blockDim.x + threadIdx.x; t < total;
+       t += (long long)gridDim.x * blockDim.x) {
+    const long long r = t / row_units, u = t % row_units;
+    const long long sr = idx ? idx[r] : r;
+    dst[t] = src[sr * row_units + u];
+  }
+}
+
+template <typename T>
+__global__ void frames_to_padded_kernel(const T* src, const int32_t* idx, int n, long long hw,
+                                        int Cp, T* dst) {
+  const long long total = (long long)n * hw;
+  for (long long t = blockIdx.x * (long long)blockDim.x + threadIdx.x; t < total;
+       t += (long long)gridDim.x * blockDim.x) {
+    const long long f = t / hw, p = t % hw;
+    const long long sf = idx ? idx[f] : f;
+    const T* s = src + (sf * hw + p) * 3;
+    T* d = dst + t * Cp;
+    for (int c = 0; c < Cp; ++c) d[c] = c < 3 ? s[c] : from_f<T>(0.f);
+  }
+}
+
+__device__ __forceinline__ void src_coord(int dst, int n_in, int n_out, int& i0, int& i1,
+                                          float& lam) {
+  float s = ((float)dst + 0.5f) * ((float)n_in / (float)n_out) - 0.5f;
+  if (s < 0.f) s = 0.f;
+  i0 = min((int)floorf(s), n_in - 1);
+  i1 = min(i0 + 1, n_in - 1);
+  lam = s - (float)i0;
+}
+
+template <typename T>
+__global__ void resize_kernel(const T* src, int n, int H, int W, int r, int Cp, T* dst) {
+  const long long total = (long long)n * r * r;
+  for (long long t = blockIdx.x * (long long)blockDim.x + threadIdx.x; t < total;
+       t += (long long)gridDim.x * blockDim.x) {
+    const int ox = (int)(t % r), oy = (int)((t / r) % r);
+    const long long f = t / ((long long)r * r);
+    int y0, y1, x0, x1;
+    float ly, lx;
+    src_coord(oy, H, r, y0, y1, ly);
+    src_coord(ox, W, r, x0, x1, lx);
+    const T* s = src + f * H * W * 3;
+    T* d = dst + t * Cp;
+    for (int c = 0; c < Cp; ++c) {
+      if (c >= 3) {
+        d[c] = from_f<T>(0.f);
+        continue;
+      }
+      const float a = to_f(s[((long long)y0 * W + x0) * 3 + c]);
+      const float b = to_f(s[((long long)y0 * W + x1) * 3 + c]);
+      const float cc = to_f(s[((long long)y1 * W + x0) * 3 + c]);
+      const float dd = to_f(s[((long long)y1 * W + x1) * 3 + c]);
+      const float top0 = a * (1.f - ly) + cc * ly;   // rows first, then columns
+      const float top1 = b * (1.f - ly) + dd * ly;
+      d[c] = from_f<T>(top0 * (1.f - lx) + top1 * lx);
+    }
+  }
+}
+
+template <typename T>
+__global__ void cast_kernel(const float* src, long long n, T* dst) {
+  for (long long i = blockIdx.x * (long long)blockDim.x + threadIdx.x; i < n;
+       i += (long long)gridDim.x * blockDim.x)
+    dst[i] = from_f<T>(src[i]);
+}
+
+// ------------------------------------------------------- weight repacking
+// tab row: src_off, K, R, S, C0, Cp, krsc_off, crsk_off
+template <typename T>
+__global__ void pack_conv_kernel(const float* master, const long long* tab, T* shadow) {
+  const long long* t = tab + 8 * blockIdx.y;
+  const int K = (int)t[1], R = (int)t[2], S = (int)t[3], C0 = (int)t[4], Cp = (int)t[5];
+  const long long n = (long long)K * R * S * Cp;
+  const float* src = master + t[0];
+  T* krsc = shadow + t[6];
+  T* crsk = t[7] >= 0 ? shadow + t[7] : nullptr;
+  for (long long i = blockIdx.x * (long long)blockDim.x + threadIdx.x; i < n;
+       i += (long long)gridDim.x * blockDim.x) {
+    const int c = (int)(i % Cp);
+    const long long krs = i / Cp;
+    const float v = c < C0 ? src[krs * C0 + c] : 0.f;
+    krsc[i] = from_f<T>(v);
+    if (crsk && c < C0) {
+      const int s = (int)(krs % S), r = (int)((krs / S) % R), k = (int)(krs / ((long long)R * S));
+      crsk[(((long long)c * R + r) * S + s) * K + k] = from_f<T>(v);
+    }
+  }
+}
+
+// tab row: off, K, C, R, S
+__global__ void permute_kernel(const float* src, float* dst, const long long* tab, int ntab,
+                               long long total, int to_internal) {
+  for (long long i = blockIdx.x * (long long)blockDim.x + threadIdx.x; i < total;
+       i += (long long)gridDim.x * blockDim.x) {
+    int lo = 0, hi = ntab - 1;  // last row with off <= i
+    while (lo < hi) {
+      int mid = (lo + hi + 1) >> 1;
+      if (tab[5 * mid] <= i) lo = mid; else hi = mid - 1;
+    }
+    const long long* t = tab + 5 * lo;
+    const long long off = t[0], l = i - off;
+    const int C = (int)t[2], R = (int)t[3], S = (int)t[4];
+    if (R * S * C == 1 || (R == 1 && S == 1)) {  // no reordering needed
+      dst[i] = src[i];
+      continue;
+    }
+    if (to_internal) {
+      // l indexes [K][C][R][S]; destination [K][R][S][C]
+      const int s = (int)(l % S), r = (int)((l / S) % R), c = (int)((l / ((long long)S * R)) % C);
+      const long long k = l / ((long long)S * R * C);
+      dst[off + ((k * R + r) * S + s) * C + c] = src[i];
+    } else {
+      // l indexes [K][R][S][C]; destination [K][C][R][S]
+      const int c = (int)(l % C), s = (int)((l / C) % S), r = (int)((l / ((long long)C * S)) % R);
+      const long long k = l / ((long long)C * S * R);
+      dst[off + ((k * C + c) * R + r) * S + s] = src[i];
+    }
+  }
+}
+
+template <typename F>
+hipError_t by_type(int dt, F&& f) {
+  if (dt == DT_F32) f((float*)nullptr); else f((bf16*)nullptr);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+size_t bn_partials_floats(long long M, int C) { return (size_t)bn_chunks(M) * 2 * C + 3 * C; }
+
+hipError_t bn_train_stats(int dt, const void* z, long long M, int C, const float* gamma,
+                          const float* beta, float* rm, float* rv, float* mean, float* invstd,
+                          float* scale, float* shift, float* partials, hipStream_t stream) {
+  if (M == 0) return hipSuccess;
+  const int nch = bn_chunks(M);
+  const long long rpc = cdivl(M, nch);
+  return by_type(dt, [&](auto* tp) {
+    using T = std::remove_pointer_t<decltype(tp)>;
+    hipLaunchKernelGGL(bn_stats_partial<T>, dim3(nch), dim3(256), 0, stream, (const T*)z, M, C,
+                       rpc, partials);
+    hipLaunchKernelGGL(bn_stats_final<T>, dim3(cdiv(C, 256)), dim3(256), 0, stream, (const T*)z,
+                       partials, nch, M, C, gamma, beta, rm, rv, mean, invstd, scale, shift);
+  });
+}
+
+hipError_t bn_apply(int dt, const void* z, long long M, int C, const float* mean,
+                    const float* scale, const float* beta, const void* res, int relu, void* y,
+                    hipStream_t stream) {
+  const long long units = M * C / dtype_vec(dt);
+  if (units == 0) return hipSuccess;
+  return by_type(dt, [&](auto* tp) {
+    using T = std::remove_pointer_t<decltype(tp)>;
+    hipLaunchKernelGGL(bn_apply_kernel<T>, dim3(grid_for(units)), dim3(256), 0, stream,
+                       (const T*)z, units, C, mean, scale, beta, (const T*)res, relu, (T*)y);
+  });
+}
+
+hipError_t bn_fold(const float* params, const long long* tab, int n, float* out,
+                   hipStream_t stream) {
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(bn_fold_kernel, dim3(n), dim3(256), 0, stream, params, tab, out);
+  return hipGetLastError();
+}
+
+hipError_t bn_backward(int dt, const void* dy, const void* y, const void* z, long long M, int C,
+                       const float* gamma, const float* mean, const float* invstd, float* dgamma,
+                       float* dbeta, void* dz, void* g_out, float* partials, hipStream_t stream) {
+  if (M == 0) return hipSuccess;
+  const int nch = bn_chunks(M);
+  const long long rpc = cdivl(M, nch);
+  float* coef = partials + (size_t)nch * 2 * C;
+  const long long units = M * C / dtype_vec(dt);
+  return by_type(dt, [&](auto* tp) {
+    using T = std::remove_pointer_t<decltype(tp)>;
+    hipLaunchKernelGGL(bn_bwd_partial<T>, dim3(nch), dim3(256), 0, stream, (const T*)dy,
+                       (const T*)y, (const T*)z, M, C, rpc, mean, partials);
+    hipLaunchKernelGGL(bn_bwd_final, dim3(cdiv(C, 256)), dim3(256), 0, stream, partials, nch, M, C,
+                       gamma, invstd, dgamma, dbeta, coef);
+    hipLaunchKernelGGL(bn_bwd_apply<T>, dim3(grid_for(units)), dim3(256), 0, stream, (const T*)dy,
+                       (const T*)y, (const T*)z, units, C, mean, coef, (T*)dz, (T*)g_out);
+  });
+}
+
+hipError_t maxpool_fwd(int dt, const void* x, int N, int H, int W, int C, void* y, uint8_t* arg,
+                       hipStream_t stream) {
+  const int P = (H - 1) / 2 + 1, Q = (W - 1) / 2 + 1;
+  const long long units = (long long)N * P * Q * C / dtype_vec(dt);
+  if (units == 0) return hipSuccess;
+  return by_type(dt, [&](auto* tp) {
+    using T = std::remove_pointer_t<decltype(tp)>;
+    hipLaunchKernelGGL(maxpool_fwd_kernel<T>, dim3(grid_for(units)), dim3(256), 0, stream,
+                       (const T*)x, N, H, W, C, P, Q, (T*)y, arg);
+  });
+}
+
+hipError_t maxpool_bwd(int dt, const void* dy, const uint8_t* arg, int N, int H, int W, int C,
+                       void* dx, hipStream_t stream) {
+  const int P = (H - 1) / 2 + 1, Q = (W - 1) / 2 + 1;
+  const long long units = (long long)N * H * W * C / dtype_vec(dt);
+  if (units == 0) return hipSuccess;
+  return by_type(dt, [&](auto* tp) {
+    using T = std::remove_pointer_t<decltype(tp)>;
+    hipLaunchKernelGGL(maxpool_bwd_kernel<T>, dim3(grid_for(units)), dim3(256), 0, stream,
+                       (const T*)dy, arg, N, H, W, C, P, Q, (T*)dx);
+  });
+}
+
+hipError_t avgpool_fwd(int dt, const void* x, int N, int HW, int C, float* f, hipStream_t stream) {
+  const long long n = (long long)N * C;
+  if (n == 0) return hipSuccess;
+  return by_type(dt, [&](auto* tp) {
+    using T = std::remove_pointer_t<decltype(tp)>;
+    hipLaunchKernelGGL(avgpool_fwd_kernel<T>, dim3(grid_for(n)), dim3(256), 0, stream, (const T*)x,
+                       N, HW, C, f);
+  });
+}
+
+hipError_t avgpool_bwd(int dt, const float* df, int N, int HW, int C, void* dx,
+                       hipStream_t stream) {
+  const long long n = (long long)N * HW * C;
+  if (n == 0) return hipSuccess;
+  return by_type(dt, [&](auto* tp) {
+    using T = std::remove_pointer_t<decltype(tp)>;
+    hipLaunchKernelGGL(avgpool_bwd_kernel<T>, dim3(grid_for(n)), dim3(256), 0, stream, df, N, HW,
+                       C, (T*)dx);
+  });
+}
+
+hipError_t fc_fwd(const float* f, const float* W, const float* b, int N, int I, int J, float* z,
+                  hipStream_t stream) {
+  if (N == 0) return hipSuccess;
+  hipLaunchKernelGGL(fc_fwd_kernel, dim3(cdiv(N * J, 256)), dim3(256), 0, stream, f, W, b, N, I,
+                     J, z);
+  return hipGetLastError();
+}
+
+hipError_t softmax_ce(const float* z, const int32_t* labels, const int32_t* idx, int N, int J,
+                      float* dz, float* out, hipStream_t stream) {
+  hipLaunchKernelGGL(softmax_ce_kernel, dim3(1), dim3(256), 0, stream, z, labels, idx, N, J, dz,
+                     out);
+  return hipGetLastError();
+}
+
+hipError_t fc_bwd(const float* dz, const float* f, const float* W, int N, int I, int J, float* dW,
+                  float* db, float* df, hipStream_t stream) {
+  hipLaunchKernelGGL(fc_bwd_w_kernel, dim3(cdiv(J * I, 256)), dim3(256), 0, stream, dz, f, N, I, J,
+                     dW, db);
+  if (df) {
+    hipLaunchKernelGGL(fc_bwd_x_kernel, dim3(grid_for((long long)N * I)), dim3(256), 0, stream, dz,
+                       W, N, I, J, df);
+  }
+  return hipGetLastError();
+}
+
+hipError_t count_correct(const float* z, const int32_t* labels, int N, int J, int32_t* count,
+                         hipStream_t stream) {
+  hipLaunchKernelGGL(count_correct_kernel, dim3(1), dim3(256), 0, stream, z, labels, N, J, count);
+  return hipGetLastError();
+}
+
+hipError_t argmax_rows(const float* z, int N, int J, int32_t* out, hipStream_t stream) {
+  if (N == 0) return hipSuccess;
+  hipLaunchKernelGGL(argmax_kernel, dim3(cdiv(N, 256)), dim3(256), 0, stream, z, N, J, out);
+  return hipGetLastError();
+}
+
+hipError_t sgd_momentum(float* w, float* v, const float* g, long long n, float lr, float mu,
+                        hipStream_t stream) {
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(sgd_kernel, dim3(grid_for(n)), dim3(256), 0, stream, w, v, g, n, lr, mu);
+  return hipGetLastError();
+}
+
+hipError_t gather_rows(const void* src, const int32_t* idx, int n, long long row_bytes, void* dst,
+                       hipStream_t stream) {
+  const long long ru = row_bytes / 16;
+  if (n == 0 || ru == 0) return hipSuccess;
+  hipLaunchKernelGGL(gather_rows_kernel, dim3(grid_for(n * ru)), dim3(256), 0, stream,
+                     (const uint4*)src, idx, n, ru, (uint4*)dst);
+  return hipGetLastError();
+}
+
+hipError_t frames_to_padded(int dt, const void* frames, const int32_t* idx, int n, int H, int W,
+                            int Cp, void* dst, hipStream_t stream) {
+  const long long hw = (long long)H * W;
+  if (n == 0) return hipSuccess;
+  return by_type(dt, [&](auto* tp) {
+    using T = std::remove_pointer_t<decltype(tp)>;
+    hipLaunchKernelGGL(frames_to_padded_kernel<T>, dim3(grid_for(n * hw)), dim3(256), 0, stream,
+                       (const T*)frames, idx, n, hw, Cp, (T*)dst);
+  });
+}
+
+hipError_t resize_to_padded(int dt, const void* frames, int n, int H, int W, int r, int Cp,
+                            void* dst, hipStream_t stream) {
+  const long long total = (long long)n * r * r;
+  if (total == 0) return hipSuccess;
+  return by_type(dt, [&](auto* tp) {
+    using T = std::remove_pointer_t<decltype(tp)>;
+    hipLaunchKernelGGL(resize_kernel<T>, dim3(grid_for(total)), dim3(256), 0, stream,
+                       (const T*)frames, n, H, W, r, Cp, (T*)dst);
+  });
+}
+
+hipError_t cast_from_f32(int dt, const float* src, long long n, void* dst, hipStream_t stream) {
+  if (n == 0) return hipSuccess;
+  return by_type(dt, [&](auto* tp) {
+    using T = std::remove_pointer_t<decltype(tp)>;
+    hipLaunchKernelGGL(cast_kernel<T>, dim3(grid_for(n)), dim3(256), 0, stream, src, n, (T*)dst);
+  });
+}
+
+hipError_t pack_conv_weights(int dt, const float* master, const long long* tab, int n,
+                             void* shadow, hipStream_t stream) {
+  if (n == 0) return hipSuccess;
+  return by_type(dt, [&](auto* tp) {
+    using T = std::remove_pointer_t<decltype(tp)>;
+    hipLaunchKernelGGL(pack_conv_kernel<T>, dim3(256, n), dim3(256), 0, stream, master, tab,
+                       (T*)shadow);
+  });
+}
+
+hipError_t permute_weights(const float* src, float* dst, const long long* tab, int n,
+                           long long total, int to_internal, hipStream_t stream) {
+  hipLaunchKernelGGL(permute_kernel, dim3(grid_for(total)), dim3(256), 0, stream, src, dst, tab, n,
+                     total, to_internal);
+  return hipGetLastError();
+}
+
+}  // namespace ekya

@@ -1,0 +1,127 @@
+// Host-side launchers of every kernel of the library.  All pointers are device
+// pointers; every call is asynchronous on `stream` and returns the launch status.
+#pragma once
+
+#include "common.hpp"
+
+namespace ekya {
+
+enum DType { DT_F32 = 0, DT_BF16 = 1 };
+inline size_t dtype_size(int dt) { return dt == DT_F32 ? 4 : 2; }
+inline int dtype_vec(int dt) { return dt == DT_F32 ? 4 : 8; }
+
+// ------------------------------------------------------------- convolution
+struct ConvGeom {
+  int N, H, W, C;     // input NHWC; C is the stored (padded) channel count
+  int K, R, S;        // output channels, kernel rows/cols
+  int stride, pad;
+  int P, Q;           // output spatial size
+};
+
+// Epilogue of the forward conv: y = acc * scale[k] + shift[k] (+ res) (ReLU),
+// any of scale/shift/res may be null (scale null = 1, shift null = 0).
+struct ConvEpilogue {
+  const float* scale = nullptr;
+  const float* shift = nullptr;
+  const void* res = nullptr;
+  int relu = 0;
+};
+
+// y[N,P,Q,K] = conv(x[N,H,W,C], w[K,R,S,C]) with the epilogue.
+hipError_t conv_fwd(int dt, const ConvGeom& g, const void* x, const void* w_krsc, void* y,
+                    const ConvEpilogue& epi, hipStream_t stream);
+// dx[N,H,W,C] = conv-transpose of dy[N,P,Q,K] with wT[C,R,S,K] (+ res[N,H,W,C]).
+hipError_t conv_dgrad(int dt, const ConvGeom& g, const void* dy, const void* w_crsk, void* dx,
+                      const void* res, hipStream_t stream);
+// Split count and partial-buffer size (floats) the weight gradient will use.
+int conv_wgrad_splits(int dt, const ConvGeom& g);
+size_t conv_wgrad_workspace_floats(int dt, const ConvGeom& g);
+// dw[K,R,S,C0] (fp32, unpadded channel count C0 <= C) = sum over pixels of
+// dy x im2col(x); deterministic split-K through `partials`.
+hipError_t conv_wgrad(int dt, const ConvGeom& g, const void* x, const void* dy, float* partials,
+                      float* dw, int C0, hipStream_t stream);
+
+// ---------------------------------------------------------------- BatchNorm
+// Per-channel statistics of z[M, C] (NHWC rows).  Writes mean and 1/sqrt(var+eps)
+// (biased variance) and, when rm/rv are non-null, updates running statistics
+// with momentum 0.1 and the unbiased variance.  Also writes scale = gamma*invstd,
+// shift = beta - mean*scale.  `partials` needs bn_partials_floats(M, C).
+size_t bn_partials_floats(long long M, int C);
+hipError_t bn_train_stats(int dt, const void* z, long long M, int C, const float* gamma,
+                          const float* beta, float* rm, float* rv, float* mean, float* invstd,
+                          float* scale, float* shift, float* partials, hipStream_t stream);
+// y = (z - mean)*scale + beta (+ res) (ReLU), elementwise over [M, C].
+hipError_t bn_apply(int dt, const void* z, long long M, int C, const float* mean,
+                    const float* scale, const float* beta, const void* res, int relu, void* y,
+                    hipStream_t stream);
+// Eval-mode fold for `n` BatchNorm layers given by tables of parameter offsets
+// into `params`: scale = gamma / sqrt(rv + eps), shift = beta - rm * scale,
+// written at out_off[i] (scale) and out_off[i] + C[i] (shift) of `out`.
+hipError_t bn_fold(const float* params, const long long* tab, int n, float* out,
+                   hipStream_t stream);
+// Backward of train-mode BN (with the ReLU mask y > 0 when y != null):
+// g = dy * [y > 0]; dgamma = sum g*xhat; dbeta = sum g;
+// dz = gamma*invstd*(g - dbeta/M - xhat*dgamma/M).  Writes dgamma/dbeta and
+// dz; when g_out != null also writes g.
+hipError_t bn_backward(int dt, const void* dy, const void* y, const void* z, long long M, int C,
+                       const float* gamma, const float* mean, const float* invstd, float* dgamma,
+                       float* dbeta, void* dz, void* g_out, float* partials, hipStream_t stream);
+
+// ------------------------------------------------------------------ pooling
+hipError_t maxpool_fwd(int dt, const void* x, int N, int H, int W, int C, void* y, uint8_t* arg,
+                       hipStream_t stream);
+hipError_t maxpool_bwd(int dt, const void* dy, const uint8_t* arg, int N, int H, int W, int C,
+                       void* dx, hipStream_t stream);
+// f[N, C] (fp32) = mean over H*W of x.
+hipError_t avgpool_fwd(int dt, const void* x, int N, int HW, int C, float* f, hipStream_t stream);
+hipError_t avgpool_bwd(int dt, const float* df, int N, int HW, int C, void* dx,
+                       hipStream_t stream);
+
+// --------------------------------------------------------------- classifier
+// z[N, J] = f[N, I] W[J, I]^T + b
+hipError_t fc_fwd(const float* f, const float* Wt, const float* b, int N, int I, int J, float* z,
+                  hipStream_t stream);
+// Softmax cross-entropy over rows of z[N, J] with labels (selected through
+// `idx` when non-null): dz = (softmax - onehot)/N, out[0] = mean loss,
+// out[1] = correct count (as float), out[2] = non-finite flag.
+hipError_t softmax_ce(const float* z, const int32_t* labels, const int32_t* idx, int N, int J,
+                      float* dz, float* out, hipStream_t stream);
+// dW[J, I] = dz^T f, db = column sums of dz, df = dz W (df may be null).
+hipError_t fc_bwd(const float* dz, const float* f, const float* Wt, int N, int I, int J, float* dW,
+                  float* db, float* df, hipStream_t stream);
+// Count of rows whose argmax matches the label, accumulated into *count.
+hipError_t count_correct(const float* z, const int32_t* labels, int N, int J, int32_t* count,
+                         hipStream_t stream);
+hipError_t argmax_rows(const float* z, int N, int J, int32_t* out, hipStream_t stream);
+
+// -------------------------------------------------------------- optimiser
+// v = mu v + g; w = w - lr v over n floats.
+hipError_t sgd_momentum(float* w, float* v, const float* g, long long n, float lr, float mu,
+                        hipStream_t stream);
+
+// ---------------------------------------------------------- data movement
+// dst row i = src row idx[i] (idx null: row i), rows of `row_bytes` (multiple of 16).
+hipError_t gather_rows(const void* src, const int32_t* idx, int n, long long row_bytes, void* dst,
+                       hipStream_t stream);
+// Frames [n, H, W, 3] (row idx[i] when idx != null) -> [n, H, W, Cp] with
+// zero channels 3..Cp-1.
+hipError_t frames_to_padded(int dt, const void* frames, const int32_t* idx, int n, int H, int W,
+                            int Cp, void* dst, hipStream_t stream);
+// Bilinear resize (half-pixel centres, clamped) of frames [n, H, W, 3] to
+// [n, r, r, Cp] with zero padding channels.
+hipError_t resize_to_padded(int dt, const void* frames, int n, int H, int W, int r, int Cp,
+                            void* dst, hipStream_t stream);
+// Element-wise fp32 -> dt copy.
+hipError_t cast_from_f32(int dt, const float* src, long long n, void* dst, hipStream_t stream);
+
+// ------------------------------------------------------ weight (re)packing
+// Table row per conv (all entries long long): src_off (fp32, [K][R][S][C0]),
+// K, R, S, C0, Cp, krsc_off (elements of dt), crsk_off (elements, -1 = skip).
+hipError_t pack_conv_weights(int dt, const float* master, const long long* tab, int n,
+                             void* shadow, hipStream_t stream);
+// Table row per tensor: off, K, C, R, S (conv) or off, n, 0, 0, 0 (other):
+// to_internal = 1 permutes [K][C][R][S] -> [K][R][S][C], 0 the inverse.
+hipError_t permute_weights(const float* src, float* dst, const long long* tab, int n,
+                           long long total, int to_internal, hipStream_t stream);
+
+}  // namespace ekya

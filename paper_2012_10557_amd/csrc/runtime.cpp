@@ -1,0 +1,976 @@
+// Retraining, micro-profiling and inference jobs.
+//
+// Retraining of the last k stages (sections 3.2 and 4.3):
+//   1. draw the uniform training subset S of the window (host, seeded);
+//   2. run the frozen stages once per frame of S and of the held-out set, in
+//      eval mode, into the feature cache (stages below the lowest trainable
+//      stage never change during the job, so this is an exact reuse);
+//   3. for every epoch: visit S in a seeded random order in batches (last
+//      partial batch kept); per batch gather cached features, run the
+//      trainable stages in train mode, mean softmax cross-entropy, backward
+//      through the trainable stages only, SGD with momentum, repack the
+//      low-precision weight copies;
+//   4. after every epoch measure held-out accuracy in eval mode (the
+//      micro-profiler's per-epoch accuracy, section 4.3) and the epoch's GPU
+//      time (resource demand per epoch at the full GPU, section 4.3).
+// All device work of a job is ordered on one stream; the host reads results
+// once at the end.
+#include "runtime.hpp"
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <thread>
+
+#include "rng.hpp"
+
+namespace ekya {
+
+hipError_t DeviceBuf::ensure(size_t bytes) {
+  if (bytes <= cap) return hipSuccess;
+  if (p) {
+    hipError_t e = hipDeviceSynchronize();
+    if (e != hipSuccess) return e;
+    e = hipFree(p);
+    if (e != hipSuccess) return e;
+    p = nullptr;
+    cap = 0;
+  }
+  size_t want = bytes + bytes / 8 + (1 << 20);
+  hipError_t e = hipMalloc(&p, want);
+  if (e != hipSuccess) {
+    p = nullptr;
+    return e;
+  }
+  cap = want;
+  return hipSuccess;
+}
+
+void DeviceBuf::release() {
+  if (p) (void)hipFree(p);
+  p = nullptr;
+  cap = 0;
+}
+
+// ----------------------------------------------------------------- tables
+static hipError_t upload_tables(const Net& net, Tables& t) {
+  std::vector<long long> all;
+  std::vector<std::pair<const long long**, size_t>> fix;
+  auto put = [&](const std::vector<long long>& v, const long long** dst, int* n, int row) {
+    fix.push_back({dst, all.size()});
+    *n = (int)(v.size() / row);
+    all.insert(all.end(), v.begin(), v.end());
+  };
+  put(net.permute_table(), &t.permute, &t.n_permute, 5);
+  put(net.fold_table(0, 5), &t.fold_all, &t.n_fold_all, 6);
+  put(net.pack_table(0, 4, false), &t.pack_all, &t.n_pack_all, 8);
+  for (int lo = 0; lo <= 5; ++lo) {
+    put(net.fold_table(lo, 5), &t.fold_train[lo], &t.n_fold_train[lo], 6);
+    put(net.pack_table(0, lo - 1, false), &t.pack_frozen[lo], &t.n_pack_frozen[lo], 8);
+    put(net.pack_table(lo, 4, true), &t.pack_train[lo], &t.n_pack_train[lo], 8);
+  }
+  EKYA_HIP(t.buf.ensure(all.size() * sizeof(long long) + 16));
+  EKYA_HIP(hipMemcpy(t.buf.p, all.data(), all.size() * sizeof(long long), hipMemcpyHostToDevice));
+  for (auto& f : fix) *f.first = reinterpret_cast<const long long*>(t.buf.p) + f.second;
+  return hipSuccess;
+}
+
+hipError_t ctx_init(Ctx& c, int device, int n_classes) {
+  c.device = device;
+  c.n_classes = n_classes;
+  EKYA_HIP(hipSetDevice(device));
+  for (int dt = 0; dt < 2; ++dt) {
+    c.net[dt] = Net::build(n_classes, dt);
+    EKYA_HIP(upload_tables(c.net[dt], c.tabs[dt]));
+  }
+  EKYA_HIP(hipEventCreateWithFlags(&c.infer_done, hipEventDisableTiming));
+  return hipSuccess;
+}
+
+void ctx_free(Ctx& c) {
+  (void)hipSetDevice(c.device);
+  (void)hipDeviceSynchronize();
+  for (hipStream_t s : c.streams) (void)hipStreamDestroy(s);
+  c.streams.clear();
+  if (c.infer_done) (void)hipEventDestroy(c.infer_done);
+  c.infer_done = nullptr;
+  c.retrain_ws.release();
+  c.infer_ws.release();
+  c.profile_ws.release();
+  for (auto& t : c.tabs) t.buf.release();
+}
+
+// --------------------------------------------------------- eval forward
+// Buffers for running stages in eval mode on up to `cap` frames.
+struct EvalBufs {
+  void *p0 = nullptr, *p1 = nullptr, *t1 = nullptr, *sc = nullptr;
+  float* pooled = nullptr;
+  float* logits = nullptr;
+};
+
+static long long max_act_elems(const Net& net, const Geo& g, int lo, int hi) {
+  long long m = 0;
+  if (lo <= 0 && hi >= 0) m = std::max(m, (long long)g.sh * g.sw * 64);
+  for (size_t i = 1; i < net.conv.size(); ++i) {
+    const ConvL& c = net.conv[i];
+    if (c.stage < lo || c.stage > hi) continue;
+    m = std::max(m, (long long)g.ih[i] * g.iw[i] * c.cin);
+    m = std::max(m, (long long)g.oh[i] * g.ow[i] * c.cout);
+  }
+  return std::max(m, 512LL);
+}
+
+static void plan_eval(Arena& a, const Net& net, const Geo& g, int lo, int hi, int cap, EvalBufs& b) {
+  const size_t es = dtype_size(net.dt);
+  const long long m = max_act_elems(net, g, lo, hi) * cap;
+  b.p0 = a.take_bytes(m * es);
+  b.p1 = a.take_bytes(m * es);
+  b.t1 = a.take_bytes(m * es);
+  b.sc = a.take_bytes(m * es);
+  b.pooled = a.take<float>((size_t)cap * 512);
+  b.logits = a.take<float>((size_t)cap * net.n_classes);
+}
+
+static ConvGeom conv_geom(const Net& net, const Geo& g, int ci, int n) {
+  const ConvL& c = net.conv[ci];
+  ConvGeom cg;
+  cg.N = n;
+  cg.H = g.ih[ci];
+  cg.W = g.iw[ci];
+  cg.C = c.cin_pad;
+  cg.K = c.cout;
+  cg.R = c.R;
+  cg.S = c.S;
+  cg.stride = c.stride;
+  cg.pad = c.pad;
+  cg.P = g.oh[ci];
+  cg.Q = g.ow[ci];
+  return cg;
+}
+
+static inline const char* shadow_at(const Net& net, const void* shadow, long long off) {
+  return reinterpret_cast<const char*>(shadow) + off * (long long)dtype_size(net.dt);
+}
+
+// Run stages lo..hi in eval mode (BatchNorm folded into the conv epilogue) on
+// n frames.  Output: hi <= 3: the stage's output tensor; hi == 4: the pooled
+// fp32 features [n, 512]; hi == 5: fp32 logits [n, classes].
+static hipError_t eval_forward(const Net& net, const Geo& g, const void* shadow, const float* fold,
+                               const float* master, int lo, int hi, const void* x, int n,
+                               EvalBufs& b, void* out, hipStream_t st) {
+  const int dt = net.dt;
+  const void* cur = x;
+  auto fold_scale = [&](int bi) { return fold + 2 * net.bn[bi].st; };
+  auto fold_shift = [&](int bi) { return fold + 2 * net.bn[bi].st + net.bn[bi].C; };
+  for (int s = lo; s <= hi; ++s) {
+    if (s == 0) {
+      ConvEpilogue e;
+      e.scale = fold_scale(net.conv[0].bn);
+      e.shift = fold_shift(net.conv[0].bn);
+      e.relu = 1;
+      EKYA_HIP(conv_fwd(dt, conv_geom(net, g, 0, n), cur, shadow_at(net, shadow, net.conv[0].sh_krsc),
+                        b.t1, e, st));
+      void* dst = (hi == 0) ? out : b.p0;
+      EKYA_HIP(maxpool_fwd(dt, b.t1, n, g.sh, g.sw, 64, dst, nullptr, st));
+      cur = dst;
+    } else if (s <= 4) {
+      int nb_in_stage = 0;
+      for (const BlockL& bl : net.blk) nb_in_stage += (bl.stage == s);
+      int bidx = 0;
+      for (const BlockL& bl : net.blk) {
+        if (bl.stage != s) continue;
+        const bool last = (++bidx == nb_in_stage);
+        void* dst = (last && hi == s && s <= 3) ? out : (cur == b.p0 ? b.p1 : b.p0);
+        ConvEpilogue e1;
+        e1.scale = fold_scale(net.conv[bl.c1].bn);
+        e1.shift = fold_shift(net.conv[bl.c1].bn);
+        e1.relu = 1;
+        EKYA_HIP(conv_fwd(dt, conv_geom(net, g, bl.c1, n), cur,
+                          shadow_at(net, shadow, net.conv[bl.c1].sh_krsc), b.t1, e1, st));
+        const void* res = cur;
+        if (bl.cd >= 0) {
+          ConvEpilogue ed;
+          ed.scale = fold_scale(net.conv[bl.cd].bn);
+          ed.shift = fold_shift(net.conv[bl.cd].bn);
+          EKYA_HIP(conv_fwd(dt, conv_geom(net, g, bl.cd, n), cur,
+                            shadow_at(net, shadow, net.conv[bl.cd].sh_krsc), b.sc, ed, st));
+          res = b.sc;
+        }
+        ConvEpilogue e2;
+        e2.scale = fold_scale(net.conv[bl.c2].bn);
+        e2.shift = fold_shift(net.conv[bl.c2].bn);
+        e2.res = res;
+        e2.relu = 1;
+        EKYA_HIP(conv_fwd(dt, conv_geom(net, g, bl.c2, n), b.t1,
+                          shadow_at(net, shadow, net.conv[bl.c2].sh_krsc), dst, e2, st));
+        cur = dst;
+      }
+      if (s == 4) {
+        float* pd = (hi == 4) ? reinterpret_cast<float*>(out) : b.pooled;
+        EKYA_HIP(avgpool_fwd(dt, cur, n, g.lh[4] * g.lw[4], 512, pd, st));
+        cur = pd;
+      }
+    } else {  // s == 5
+      EKYA_HIP(fc_fwd(reinterpret_cast<const float*>(cur), master + net.fc_w, master + net.fc_b, n,
+                      512, net.n_classes, reinterpret_cast<float*>(out), st));
+    }
+  }
+  return hipSuccess;
+}
+
+// ----------------------------------------------------------- train job
+struct BlockAct {
+  void *X = nullptr, *Z1 = nullptr, *A1 = nullptr, *Z2 = nullptr, *Zd = nullptr, *OUT = nullptr;
+};
+
+struct TrainJob {
+  // configuration
+  const Net* net = nullptr;
+  const Tables* tabs = nullptr;
+  Geo geo;
+  int dt = 0, k = 1, lowest = 5;
+  int B = 64, n_s = 0, n_h = 0, epochs = 1, n_steps = 0;
+  float lr = 0.01f, mu = 0.9f;
+  hipStream_t st = nullptr;
+  // inputs
+  const float* weights = nullptr;  // canonical
+  const void* frames = nullptr;
+  const int32_t* labels = nullptr;
+  const void* hframes = nullptr;
+  const int32_t* hlabels = nullptr;
+  const void* cache = nullptr;     // training rows (positions in S), lowest >= 1
+  const void* hcache = nullptr;    // held-out rows
+  long long row_bytes = 0;
+  std::vector<int32_t> h_order, h_fidx;  // host copies (epochs x n_s)
+  // device buffers
+  float *master = nullptr, *grad = nullptr, *mom = nullptr;
+  void* shadow = nullptr;
+  float *bn_mean = nullptr, *bn_invstd = nullptr, *bn_scale = nullptr, *bn_shift = nullptr;
+  float* fold = nullptr;
+  int32_t *d_order = nullptr, *d_fidx = nullptr;
+  void* x0 = nullptr;
+  void* stem_Z = nullptr;
+  void* stem_A = nullptr;
+  uint8_t* stem_arg = nullptr;
+  std::vector<BlockAct> acts;  // per block of the network (only trainable ones set)
+  void* g[6] = {nullptr};      // gradient scratch
+  float *pooled = nullptr, *logits = nullptr, *dz = nullptr, *dpooled = nullptr;
+  float* ws = nullptr;         // split-K / BatchNorm partials
+  float* ce_out = nullptr;     // n_steps x 3
+  int32_t* hcount = nullptr;   // epochs
+  EvalBufs eval;
+  int eval_cap = 0;
+  void* eval_in = nullptr;     // padded frames for held-out eval when lowest == 0
+  hipEvent_t ev[EKYA_MAX_EPOCHS + 1] = {nullptr};
+};
+
+static size_t ws_floats(const TrainJob& j) {
+  const Net& net = *j.net;
+  size_t m = 0;
+  for (size_t i = 0; i < net.conv.size(); ++i) {
+    const ConvL& c = net.conv[i];
+    if (c.stage < j.lowest || c.stage > 4) continue;
+    ConvGeom cg = conv_geom(net, j.geo, (int)i, j.B);
+    m = std::max(m, conv_wgrad_workspace_floats(j.dt, cg));
+    m = std::max(m, bn_partials_floats((long long)j.B * cg.P * cg.Q, c.cout));
+  }
+  return std::max<size_t>(m, 16);
+}
+
+static long long train_max_elems(const TrainJob& j) {
+  return max_act_elems(*j.net, j.geo, j.lowest, 4);
+}
+
+// Assign every device buffer of a job (arena sizing pass when a.base == null).
+static void plan_job(Arena& a, TrainJob& j) {
+  const Net& net = *j.net;
+  const size_t es = dtype_size(j.dt);
+  const long long tb = net.stage_begin[j.lowest];
+  j.master = a.take<float>(net.total);
+  j.grad = a.take<float>(net.total);
+  j.mom = a.take<float>(net.total);
+  (void)tb;
+  j.shadow = a.take_bytes(net.shadow_elems * es);
+  j.bn_mean = a.take<float>(net.bn_channels);
+  j.bn_invstd = a.take<float>(net.bn_channels);
+  j.bn_scale = a.take<float>(net.bn_channels);
+  j.bn_shift = a.take<float>(net.bn_channels);
+  j.fold = a.take<float>(2 * net.bn_channels);
+  j.d_order = a.take<int32_t>((size_t)j.epochs * j.n_s);
+  j.d_fidx = a.take<int32_t>((size_t)j.epochs * j.n_s);
+  const long long in_elems = j.geo.stage_in_elems(net, j.lowest);
+  const size_t in_es = (j.lowest == 5) ? 4 : es;
+  j.x0 = a.take_bytes((size_t)j.B * in_elems * in_es);
+  j.acts.assign(net.blk.size(), BlockAct());
+  if (j.lowest == 0) {
+    j.stem_Z = a.take_bytes((size_t)j.B * j.geo.sh * j.geo.sw * 64 * es);
+    j.stem_A = a.take_bytes((size_t)j.B * j.geo.sh * j.geo.sw * 64 * es);
+    j.stem_arg = a.take<uint8_t>((size_t)j.B * j.geo.mh * j.geo.mw * 64);
+  }
+  for (size_t bi = 0; bi < net.blk.size(); ++bi) {
+    const BlockL& b = net.blk[bi];
+    if (b.stage < j.lowest || b.stage > 4) continue;
+    BlockAct& t = j.acts[bi];
+    const long long o1 = (long long)j.geo.oh[b.c1] * j.geo.ow[b.c1] * net.conv[b.c1].cout * j.B;
+    t.Z1 = a.take_bytes(o1 * es);
+    t.A1 = a.take_bytes(o1 * es);
+    t.Z2 = a.take_bytes(o1 * es);
+    t.OUT = a.take_bytes(o1 * es);
+    if (b.cd >= 0) t.Zd = a.take_bytes(o1 * es);
+    if (j.lowest == 0 && b.stage == 1 && bi == 0) {
+      // input of layer1 comes from the stem's max pool
+      t.X = a.take_bytes((size_t)j.B * j.geo.mh * j.geo.mw * 64 * es);
+    }
+  }
+  const long long gmax = train_max_elems(j) * j.B;
+  if (j.lowest <= 4)
+    for (int i = 0; i < 6; ++i) j.g[i] = a.take_bytes(gmax * es);
+  j.pooled = a.take<float>((size_t)j.B * 512);
+  j.dpooled = a.take<float>((size_t)j.B * 512);
+  j.logits = a.take<float>((size_t)j.B * net.n_classes);
+  j.dz = a.take<float>((size_t)j.B * net.n_classes);
+  j.ws = a.take<float>(ws_floats(j));
+  j.ce_out = a.take<float>((size_t)j.n_steps * 3);
+  j.hcount = a.take<int32_t>(j.epochs);
+  j.eval_cap = std::max(1, std::min(j.n_h, 256));
+  plan_eval(a, net, j.geo, j.lowest, 5, j.eval_cap, j.eval);
+  if (j.lowest == 0) j.eval_in = a.take_bytes((size_t)j.eval_cap * in_elems * es);
+}
+
+static inline float* bnp(float* base, const BnL& b) { return base + b.st; }
+
+// Train-mode forward of stages lowest..5 on the batch in x0 (nb frames).
+static hipError_t train_forward(TrainJob& j, int nb) {
+  const Net& net = *j.net;
+  const int dt = j.dt;
+  hipStream_t st = j.st;
+  auto bn_train = [&](int bi, const void* z, long long M) {
+    const BnL& b = net.bn[bi];
+    return bn_train_stats(dt, z, M, b.C, j.master + b.g, j.master + b.b, j.master + b.rm,
+                          j.master + b.rv, bnp(j.bn_mean, b), bnp(j.bn_invstd, b),
+                          bnp(j.bn_scale, b), bnp(j.bn_shift, b), j.ws, st);
+  };
+  auto mu = [&](int bi) { return bnp(j.bn_mean, net.bn[bi]); };
+  auto sc = [&](int bi) { return bnp(j.bn_scale, net.bn[bi]); };
+  auto be = [&](int bi) { return j.master + net.bn[bi].b; };
+  const void* cur = j.x0;
+  for (int s = j.lowest; s <= 4; ++s) {
+    if (s == 0) {
+      ConvGeom cg = conv_geom(net, j.geo, 0, nb);
+      EKYA_HIP(conv_fwd(dt, cg, cur, shadow_at(net, j.shadow, net.conv[0].sh_krsc), j.stem_Z,
+                        ConvEpilogue(), st));
+      const long long M = (long long)nb * cg.P * cg.Q;
+      EKYA_HIP(bn_train(net.conv[0].bn, j.stem_Z, M));
+      EKYA_HIP(bn_apply(dt, j.stem_Z, M, 64, mu(net.conv[0].bn), sc(net.conv[0].bn), be(net.conv[0].bn), nullptr, 1,
+                        j.stem_A, st));
+      void* xm = j.acts[0].X;
+      EKYA_HIP(maxpool_fwd(dt, j.stem_A, nb, j.geo.sh, j.geo.sw, 64, xm, j.stem_arg, st));
+      cur = xm;
+      continue;
+    }
+    for (size_t bi = 0; bi < net.blk.size(); ++bi) {
+      const BlockL& b = net.blk[bi];
+      if (b.stage != s) continue;
+      BlockAct& t = j.acts[bi];
+      t.X = const_cast<void*>(cur);
+      ConvGeom g1 = conv_geom(net, j.geo, b.c1, nb);
+      const long long M = (long long)nb * g1.P * g1.Q;
+      const int C = net.conv[b.c1].cout;
+      EKYA_HIP(conv_fwd(dt, g1, t.X, shadow_at(net, j.shadow, net.conv[b.c1].sh_krsc), t.Z1,
+                        ConvEpilogue(), st));
+      EKYA_HIP(bn_train(net.conv[b.c1].bn, t.Z1, M));
+      EKYA_HIP(bn_apply(dt, t.Z1, M, C, mu(net.conv[b.c1].bn), sc(net.conv[b.c1].bn), be(net.conv[b.c1].bn), nullptr, 1,
+                        t.A1, st));
+      EKYA_HIP(conv_fwd(dt, conv_geom(net, j.geo, b.c2, nb), t.A1,
+                        shadow_at(net, j.shadow, net.conv[b.c2].sh_krsc), t.Z2, ConvEpilogue(), st));
+      EKYA_HIP(bn_train(net.conv[b.c2].bn, t.Z2, M));
+      const void* res = t.X;
+      if (b.cd >= 0) {
+        EKYA_HIP(conv_fwd(dt, conv_geom(net, j.geo, b.cd, nb), t.X,
+                          shadow_at(net, j.shadow, net.conv[b.cd].sh_krsc), t.Zd, ConvEpilogue(), st));
+        EKYA_HIP(bn_train(net.conv[b.cd].bn, t.Zd, M));
+        EKYA_HIP(bn_apply(dt, t.Zd, M, C, mu(net.conv[b.cd].bn), sc(net.conv[b.cd].bn), be(net.conv[b.cd].bn), nullptr, 0,
+                          j.g[0], st));
+        res = j.g[0];
+      }
+      EKYA_HIP(bn_apply(dt, t.Z2, M, C, mu(net.conv[b.c2].bn), sc(net.conv[b.c2].bn), be(net.conv[b.c2].bn), res, 1, t.OUT,
+                        st));
+      cur = t.OUT;
+    }
+    if (s == 4) {
+      EKYA_HIP(avgpool_fwd(dt, cur, nb, j.geo.lh[4] * j.geo.lw[4], 512, j.pooled, st));
+      cur = j.pooled;
+    }
+  }
+  const float* f = (j.lowest == 5) ? reinterpret_cast<const float*>(j.x0) : j.pooled;
+  return fc_fwd(f, j.master + net.fc_w, j.master + net.fc_b, nb, 512, net.n_classes, j.logits, st);
+}
+
+// Backward of stages 5..lowest from dz (already in j.dz); gradients land in j.grad.
+static hipError_t train_backward(TrainJob& j, int nb) {
+  const Net& net = *j.net;
+  const int dt = j.dt;
+  hipStream_t st = j.st;
+  const float* f = (j.lowest == 5) ? reinterpret_cast<const float*>(j.x0) : j.pooled;
+  EKYA_HIP(fc_bwd(j.dz, f, j.master + net.fc_w, nb, 512, net.n_classes, j.grad + net.fc_w,
+                  j.grad + net.fc_b, j.lowest == 5 ? nullptr : j.dpooled, st));
+  if (j.lowest == 5) return hipSuccess;
+  void* dout = j.g[1];
+  void* dnext = j.g[2];
+  void* gG = j.g[3];
+  void* gZ = j.g[4];
+  void* gA = j.g[5];
+  void* gZd = j.g[0];
+  EKYA_HIP(avgpool_bwd(dt, j.dpooled, nb, j.geo.lh[4] * j.geo.lw[4], 512, dout, st));
+  auto bn_bwd = [&](int bi, const void* dy, const void* ymask, const void* z, long long M, void* dz,
+                    void* gout) {
+    const BnL& b = net.bn[bi];
+    return bn_backward(dt, dy, ymask, z, M, b.C, j.master + b.g, bnp(j.bn_mean, b),
+                       bnp(j.bn_invstd, b), j.grad + b.g, j.grad + b.b, dz, gout, j.ws, st);
+  };
+  auto wgrad = [&](int ci, const void* x, const void* dy, int n) {
+    const ConvL& c = net.conv[ci];
+    return conv_wgrad(dt, conv_geom(net, j.geo, ci, n), x, dy, j.ws, j.grad + c.off, c.cin, st);
+  };
+  auto dgrad = [&](int ci, const void* dy, void* dx, const void* res, int n) {
+    return conv_dgrad(dt, conv_geom(net, j.geo, ci, n), dy,
+                      shadow_at(net, j.shadow, net.conv[ci].sh_crsk), dx, res, st);
+  };
+  for (int s = 4; s >= j.lowest; --s) {
+    if (s == 0) {
+      // stem: max-pool backward, BN + ReLU backward, weight gradient
+      EKYA_HIP(maxpool_bwd(dt, dout, j.stem_arg, nb, j.geo.sh, j.geo.sw, 64, gA, st));
+      const long long M = (long long)nb * j.geo.sh * j.geo.sw;
+      EKYA_HIP(bn_bwd(net.conv[0].bn, gA, j.stem_A, j.stem_Z, M, gZ, nullptr));
+      EKYA_HIP(wgrad(0, j.x0, gZ, nb));
+      break;
+    }
+    int first_bi = -1;
+    for (size_t bi = 0; bi < net.blk.size(); ++bi)
+      if (net.blk[bi].stage == s && first_bi < 0) first_bi = (int)bi;
+    for (int bi = (int)net.blk.size() - 1; bi >= 0; --bi) {
+      const BlockL& b = net.blk[bi];
+      if (b.stage != s) continue;
+      BlockAct& t = j.acts[bi];
+      const bool need_dx = !(s == j.lowest && bi == first_bi);
+      ConvGeom g1 = conv_geom(net, j.geo, b.c1, nb);
+      const long long M = (long long)nb * g1.P * g1.Q;
+      // g = dOut * [OUT > 0]; BN2 backward
+      EKYA_HIP(bn_bwd(net.conv[b.c2].bn, dout, t.OUT, t.Z2, M, gZ, gG));
+      const void* dx_sc = gG;
+      if (b.cd >= 0) {
+        EKYA_HIP(bn_bwd(net.conv[b.cd].bn, gG, nullptr, t.Zd, M, gZd, nullptr));
+        EKYA_HIP(wgrad(b.cd, t.X, gZd, nb));
+        if (need_dx) EKYA_HIP(dgrad(b.cd, gZd, dnext, nullptr, nb));
+        dx_sc = dnext;
+      }
+      EKYA_HIP(wgrad(b.c2, t.A1, gZ, nb));
+      EKYA_HIP(dgrad(b.c2, gZ, gA, nullptr, nb));
+      EKYA_HIP(bn_bwd(net.conv[b.c1].bn, gA, t.A1, t.Z1, M, gZ, nullptr));
+      EKYA_HIP(wgrad(b.c1, t.X, gZ, nb));
+      if (need_dx) {
+        EKYA_HIP(dgrad(b.c1, gZ, dnext, dx_sc, nb));
+        std::swap(dout, dnext);
+      }
+    }
+  }
+  return hipSuccess;
+}
+
+// Fill the feature cache rows [row0, row0 + n) from frames (optionally
+// through idx), chunk by chunk.
+static hipError_t build_cache(const Net& net, const Geo& g, const void* shadow, const float* fold,
+                              const float* master, int lowest, const void* frames,
+                              const int32_t* d_idx, int n, void* cache, long long row_bytes,
+                              long long row0, void* padded, int cap, EvalBufs& eb,
+                              hipStream_t st) {
+  const size_t es = dtype_size(net.dt);
+  const long long fbytes = (long long)g.H * g.W * 3 * es;
+  for (int i0 = 0; i0 < n; i0 += cap) {
+    const int cnt = std::min(cap, n - i0);
+    const void* src = d_idx ? frames : reinterpret_cast<const char*>(frames) + i0 * fbytes;
+    EKYA_HIP(frames_to_padded(net.dt, src, d_idx ? d_idx + i0 : nullptr, cnt, g.H, g.W,
+                              net.conv[0].cin_pad, padded, st));
+    void* out = reinterpret_cast<char*>(cache) + (row0 + i0) * row_bytes;
+    EKYA_HIP(eval_forward(net, g, shadow, fold, master, 0, lowest - 1, padded, cnt, eb, out, st));
+  }
+  return hipSuccess;
+}
+
+// Initial device state of a job: internal-layout master weights, zeroed
+// gradients/momentum, folded eval BatchNorm, low-precision weight copies.
+static hipError_t job_setup(TrainJob& j) {
+  const Net& net = *j.net;
+  const Tables& t = *j.tabs;
+  EKYA_HIP(permute_weights(j.weights, j.master, t.permute, t.n_permute, net.total, 1, j.st));
+  EKYA_HIP(hipMemsetAsync(j.grad, 0, net.total * sizeof(float), j.st));
+  EKYA_HIP(hipMemsetAsync(j.mom, 0, net.total * sizeof(float), j.st));
+  EKYA_HIP(hipMemsetAsync(j.hcount, 0, j.epochs * sizeof(int32_t), j.st));
+  EKYA_HIP(bn_fold(j.master, t.fold_all, t.n_fold_all, j.fold, j.st));
+  EKYA_HIP(pack_conv_weights(j.dt, j.master, t.pack_frozen[j.lowest], t.n_pack_frozen[j.lowest],
+                             j.shadow, j.st));
+  EKYA_HIP(pack_conv_weights(j.dt, j.master, t.pack_train[j.lowest], t.n_pack_train[j.lowest],
+                             j.shadow, j.st));
+  EKYA_HIP(hipMemcpyAsync(j.d_order, j.h_order.data(), j.h_order.size() * sizeof(int32_t),
+                          hipMemcpyHostToDevice, j.st));
+  EKYA_HIP(hipMemcpyAsync(j.d_fidx, j.h_fidx.data(), j.h_fidx.size() * sizeof(int32_t),
+                          hipMemcpyHostToDevice, j.st));
+  return hipSuccess;
+}
+
+// The epoch loop (after setup and cache build); records an event per epoch.
+static hipError_t job_epochs(TrainJob& j) {
+  const Net& net = *j.net;
+  const Tables& t = *j.tabs;
+  const size_t es = dtype_size(j.dt);
+  const long long tb = net.stage_begin[j.lowest];
+  const long long fbytes = (long long)j.geo.H * j.geo.W * 3 * es;
+  int step = 0;
+  EKYA_HIP(hipEventRecord(j.ev[0], j.st));
+  for (int e = 0; e < j.epochs; ++e) {
+    for (int b0 = 0; b0 < j.n_s; b0 += j.B) {
+      const int nb = std::min(j.B, j.n_s - b0);
+      const int32_t* ord = j.d_order + (size_t)e * j.n_s + b0;
+      const int32_t* fid = j.d_fidx + (size_t)e * j.n_s + b0;
+      if (j.lowest == 0)
+        EKYA_HIP(frames_to_padded(j.dt, j.frames, fid, nb, j.geo.H, j.geo.W, net.conv[0].cin_pad,
+                                  j.x0, j.st));
+      else
+        EKYA_HIP(gather_rows(j.cache, ord, nb, j.row_bytes, j.x0, j.st));
+      EKYA_HIP(train_forward(j, nb));
+      EKYA_HIP(softmax_ce(j.logits, j.labels, fid, nb, net.n_classes, j.dz, j.ce_out + 3 * step,
+                          j.st));
+      EKYA_HIP(train_backward(j, nb));
+      EKYA_HIP(sgd_momentum(j.master + tb, j.mom + tb, j.grad + tb, net.total - tb, j.lr, j.mu,
+                            j.st));
+      EKYA_HIP(pack_conv_weights(j.dt, j.master, t.pack_train[j.lowest],
+                                 t.n_pack_train[j.lowest], j.shadow, j.st));
+      ++step;
+    }
+    // held-out accuracy in eval mode with the current running statistics
+    EKYA_HIP(bn_fold(j.master, t.fold_train[j.lowest], t.n_fold_train[j.lowest], j.fold, j.st));
+    for (int h0 = 0; h0 < j.n_h; h0 += j.eval_cap) {
+      const int cnt = std::min(j.eval_cap, j.n_h - h0);
+      const void* in;
+      if (j.lowest == 0) {
+        EKYA_HIP(frames_to_padded(j.dt, reinterpret_cast<const char*>(j.hframes) + h0 * fbytes,
+                                  nullptr, cnt, j.geo.H, j.geo.W, net.conv[0].cin_pad, j.eval_in,
+                                  j.st));
+        in = j.eval_in;
+      } else {
+        in = reinterpret_cast<const char*>(j.hcache) + (long long)h0 * j.row_bytes;
+      }
+      EKYA_HIP(eval_forward(net, j.geo, j.shadow, j.fold, j.master, j.lowest, 5, in, cnt, j.eval,
+                            j.eval.logits, j.st));
+      EKYA_HIP(count_correct(j.eval.logits, j.hlabels + h0, cnt, net.n_classes, j.hcount + e,
+                             j.st));
+    }
+    EKYA_HIP(hipEventRecord(j.ev[e + 1], j.st));
+  }
+  return hipSuccess;
+}
+
+static void job_prepare_host(TrainJob& j, const std::vector<int32_t>& S, uint64_t shuffle_seed) {
+  j.h_order.resize((size_t)j.epochs * j.n_s);
+  j.h_fidx.resize((size_t)j.epochs * j.n_s);
+  for (int e = 0; e < j.epochs; ++e) {
+    std::vector<int32_t> o = epoch_order(j.n_s, shuffle_seed, e);
+    for (int i = 0; i < j.n_s; ++i) {
+      j.h_order[(size_t)e * j.n_s + i] = o[i];
+      j.h_fidx[(size_t)e * j.n_s + i] = S[o[i]];
+    }
+  }
+  j.n_steps = j.epochs * ((j.n_s + j.B - 1) / j.B);
+}
+
+struct JobResult {
+  std::vector<float> ce;       // n_steps x 3
+  std::vector<int32_t> hc;     // epochs
+  std::vector<float> secs;     // epochs
+  ekya_status status = EKYA_OK;
+};
+
+static hipError_t job_collect(TrainJob& j, JobResult& r) {
+  r.ce.resize((size_t)j.n_steps * 3);
+  r.hc.resize(j.epochs);
+  r.secs.resize(j.epochs);
+  EKYA_HIP(hipMemcpyAsync(r.ce.data(), j.ce_out, r.ce.size() * sizeof(float), hipMemcpyDeviceToHost,
+                          j.st));
+  EKYA_HIP(hipMemcpyAsync(r.hc.data(), j.hcount, r.hc.size() * sizeof(int32_t),
+                          hipMemcpyDeviceToHost, j.st));
+  EKYA_HIP(hipStreamSynchronize(j.st));
+  for (int e = 0; e < j.epochs; ++e) {
+    float ms = 0.f;
+    EKYA_HIP(hipEventElapsedTime(&ms, j.ev[e], j.ev[e + 1]));
+    r.secs[e] = ms * 1e-3f;
+  }
+  r.status = EKYA_OK;
+  for (int s = 0; s < j.n_steps; ++s)
+    if (r.ce[3 * s + 2] != 0.f || !std::isfinite(r.ce[3 * s])) {
+      r.status = EKYA_ERR_NONFINITE;
+      break;
+    }
+  return hipSuccess;
+}
+
+static hipError_t create_events(TrainJob& j) {
+  for (int e = 0; e <= j.epochs; ++e) EKYA_HIP(hipEventCreate(&j.ev[e]));
+  return hipSuccess;
+}
+static void destroy_events(TrainJob& j) {
+  for (int e = 0; e <= EKYA_MAX_EPOCHS; ++e)
+    if (j.ev[e]) {
+      (void)hipEventDestroy(j.ev[e]);
+      j.ev[e] = nullptr;
+    }
+}
+
+#define EKYA_CHECK_HIP(expr)                                   \
+  do {                                                         \
+    hipError_t e_ = (expr);                                    \
+    if (e_ != hipSuccess) {                                    \
+      c.err = std::string("HIP error: ") + hipGetErrorString(e_); \
+      return e_ == hipErrorOutOfMemory ? EKYA_ERR_NOMEM : EKYA_ERR_HIP; \
+    }                                                          \
+  } while (0)
+
+// --------------------------------------------------------------- retrain
+ekya_status run_retrain(Ctx& c, float* weights, int k, const void* frames, const int32_t* labels,
+                        int n_frames, int H, int W, const void* hframes, const int32_t* hlabels,
+                        int n_heldout, const ekya_train_opts& o, ekya_retrain_result* res,
+                        hipStream_t stream) {
+  EKYA_CHECK_HIP(hipSetDevice(c.device));
+  const int dt = o.precision;
+  TrainJob j;
+  j.net = &c.net[dt];
+  j.tabs = &c.tabs[dt];
+  j.geo = Geo::build(*j.net, H, W);
+  j.dt = dt;
+  j.k = k;
+  j.lowest = 6 - k;
+  j.B = o.batch;
+  j.epochs = o.epochs;
+  j.lr = o.lr;
+  j.mu = o.momentum;
+  j.st = stream;
+  j.weights = weights;
+  j.frames = frames;
+  j.labels = labels;
+  j.hframes = hframes;
+  j.hlabels = hlabels;
+  j.n_h = n_heldout;
+  std::vector<int32_t> S = training_subset(n_frames, o.subsample_frac, o.seed);
+  j.n_s = (int)S.size();
+  job_prepare_host(j, S, o.seed);
+  const Net& net = *j.net;
+  const size_t es = dtype_size(dt);
+  const long long feat = j.geo.stage_in_elems(net, j.lowest);
+  j.row_bytes = feat * ((j.lowest == 5) ? 4 : es);
+  const int ccap = 128;  // frames per cache-build chunk
+
+  // plan: job buffers + cache + cache-build scratch
+  auto plan = [&](Arena& a, void*& cache, int32_t*& d_S, void*& padded, EvalBufs& ceb) {
+    plan_job(a, j);
+    cache = nullptr;
+    d_S = nullptr;
+    padded = nullptr;
+    if (j.lowest >= 1) {
+      cache = a.take_bytes((size_t)(j.n_s + j.n_h) * j.row_bytes);
+      d_S = a.take<int32_t>(j.n_s);
+      padded = a.take_bytes((size_t)ccap * j.geo.H * j.geo.W * net.conv[0].cin_pad * es);
+      plan_eval(a, net, j.geo, 0, j.lowest - 1, ccap, ceb);
+    }
+  };
+  Arena meas;
+  void *cache, *padded;
+  int32_t* d_S;
+  EvalBufs ceb;
+  plan(meas, cache, d_S, padded, ceb);
+  EKYA_CHECK_HIP(c.retrain_ws.ensure(meas.used));
+  Arena real;
+  real.base = reinterpret_cast<char*>(c.retrain_ws.p);
+  plan(real, cache, d_S, padded, ceb);
+  j.cache = cache;
+  j.hcache = cache ? reinterpret_cast<char*>(cache) + (long long)j.n_s * j.row_bytes : nullptr;
+
+  EKYA_CHECK_HIP(create_events(j));
+  hipEvent_t p0 = nullptr, p1 = nullptr;
+  EKYA_CHECK_HIP(hipEventCreate(&p0));
+  EKYA_CHECK_HIP(hipEventCreate(&p1));
+  auto run = [&]() -> hipError_t {
+    EKYA_HIP(job_setup(j));
+    EKYA_HIP(hipEventRecord(p0, stream));
+    if (j.lowest >= 1) {
+      EKYA_HIP(hipMemcpyAsync(d_S, S.data(), S.size() * sizeof(int32_t), hipMemcpyHostToDevice,
+                              stream));
+      EKYA_HIP(build_cache(net, j.geo, j.shadow, j.fold, j.master, j.lowest, frames, d_S, j.n_s,
+                           cache, j.row_bytes, 0, padded, ccap, ceb, stream));
+      EKYA_HIP(build_cache(net, j.geo, j.shadow, j.fold, j.master, j.lowest, hframes, nullptr,
+                           j.n_h, cache, j.row_bytes, j.n_s, padded, ccap, ceb, stream));
+    }
+    EKYA_HIP(hipEventRecord(p1, stream));
+    EKYA_HIP(job_epochs(j));
+    // write back: internal -> canonical (frozen parts round-trip exactly)
+    EKYA_HIP(permute_weights(j.master, weights, c.tabs[dt].permute, c.tabs[dt].n_permute,
+                             net.total, 0, stream));
+    return hipSuccess;
+  };
+  hipError_t he = run();
+  JobResult r;
+  if (he == hipSuccess) he = job_collect(j, r);
+  float pms = 0.f;
+  if (he == hipSuccess) he = hipEventElapsedTime(&pms, p0, p1);
+  destroy_events(j);
+  (void)hipEventDestroy(p0);
+  (void)hipEventDestroy(p1);
+  EKYA_CHECK_HIP(he);
+
+  res->n_train = j.n_s;
+  res->n_epochs = j.epochs;
+  res->n_steps = j.n_steps;
+  res->prefix_seconds = pms * 1e-3f;
+  const int spe = (j.n_s + j.B - 1) / j.B;
+  for (int e = 0; e < j.epochs; ++e) {
+    res->heldout_acc[e] = j.n_h ? (float)r.hc[e] / (float)j.n_h : 0.f;
+    res->epoch_seconds[e] = r.secs[e];
+    double l = 0.0;
+    for (int s = 0; s < spe; ++s) l += r.ce[3 * (e * spe + s)];
+    res->epoch_loss[e] = (float)(l / spe);
+  }
+  res->heldout_acc_final = res->heldout_acc[j.epochs - 1];
+  if (res->step_loss)
+    for (int s = 0; s < std::min(j.n_steps, res->step_loss_capacity); ++s)
+      res->step_loss[s] = r.ce[3 * s];
+  if (r.status != EKYA_OK) c.err = "training loss is not finite";
+  return r.status;
+}
+
+// --------------------------------------------------------------- profile
+ekya_status run_profile(Ctx& c, const float* weights, const ekya_profile_cfg* cfgs, int n_cfgs,
+                        const void* frames, const int32_t* labels, int n_frames, int H, int W,
+                        const void* hframes, const int32_t* hlabels, int n_heldout,
+                        uint64_t subsample_seed, int precision, int concurrent,
+                        ekya_profile_result* out) {
+  EKYA_CHECK_HIP(hipSetDevice(c.device));
+  const int dt = precision;
+  const Net& net = c.net[dt];
+  const Geo geo = Geo::build(net, H, W);
+  const size_t es = dtype_size(dt);
+  // one shared draw; each candidate uses a prefix of it
+  int n_max = 0;
+  for (int i = 0; i < n_cfgs; ++i)
+    n_max = std::max(n_max, subset_count(n_frames, cfgs[i].subsample_frac));
+  const std::vector<int32_t> S = partial_shuffle(n_frames, n_max, subsample_seed);
+  // streams: one per candidate, created on first use
+  while ((int)c.streams.size() < n_cfgs + 1) {
+    hipStream_t s;
+    EKYA_CHECK_HIP(hipStreamCreateWithFlags(&s, hipStreamNonBlocking));
+    c.streams.push_back(s);
+  }
+  hipStream_t s0 = c.streams[n_cfgs];
+  // caches per distinct lowest stage >= 1, over the n_max frames + held-out
+  struct CacheInfo {
+    int lowest;
+    int n_rows_s;  // training rows (prefix of S) held
+    long long row_bytes;
+    void* p;
+  };
+  std::vector<CacheInfo> caches;
+  for (int i = 0; i < n_cfgs; ++i) {
+    const int lo = 6 - cfgs[i].k_trainable;
+    if (lo == 0) continue;
+    const int ns = subset_count(n_frames, cfgs[i].subsample_frac);
+    bool found = false;
+    for (auto& ci : caches)
+      if (ci.lowest == lo) {
+        ci.n_rows_s = std::max(ci.n_rows_s, ns);
+        found = true;
+      }
+    if (!found)
+      caches.push_back({lo, ns, geo.stage_in_elems(net, lo) * (long long)((lo == 5) ? 4 : es), nullptr});
+  }
+  std::vector<TrainJob> jobs(n_cfgs);
+  for (int i = 0; i < n_cfgs; ++i) {
+    TrainJob& j = jobs[i];
+    const ekya_profile_cfg& cf = cfgs[i];
+    j.net = &net;
+    j.tabs = &c.tabs[dt];
+    j.geo = geo;
+    j.dt = dt;
+    j.k = cf.k_trainable;
+    j.lowest = 6 - cf.k_trainable;
+    j.B = cf.batch;
+    j.epochs = cf.epochs;
+    j.lr = cf.lr;
+    j.mu = cf.momentum;
+    j.st = c.streams[i];
+    j.weights = weights;
+    j.frames = frames;
+    j.labels = labels;
+    j.hframes = hframes;
+    j.hlabels = hlabels;
+    j.n_h = n_heldout;
+    j.n_s = subset_count(n_frames, cf.subsample_frac);
+    std::vector<int32_t> Si(S.begin(), S.begin() + j.n_s);
+    job_prepare_host(j, Si, cf.shuffle_seed);
+  }
+  const int ccap = 128;
+  int32_t* d_S = nullptr;
+  void* padded = nullptr;
+  EvalBufs ceb;
+  float *pmaster = nullptr, *pfold = nullptr;
+  void* pshadow = nullptr;
+  auto plan = [&](Arena& a) {
+    for (auto& j : jobs) plan_job(a, j);
+    for (auto& ci : caches) {
+      ci.p = a.take_bytes((size_t)(ci.n_rows_s + n_heldout) * ci.row_bytes);
+    }
+    d_S = a.take<int32_t>(std::max(1, n_max));
+    padded = a.take_bytes((size_t)ccap * H * W * net.conv[0].cin_pad * es);
+    plan_eval(a, net, geo, 0, 4, ccap, ceb);
+    pmaster = a.take<float>(net.total);
+    pfold = a.take<float>(2 * net.bn_channels);
+    pshadow = a.take_bytes(net.shadow_elems * es);
+  };
+  Arena meas;
+  plan(meas);
+  EKYA_CHECK_HIP(c.profile_ws.ensure(meas.used));
+  Arena real;
+  real.base = reinterpret_cast<char*>(c.profile_ws.p);
+  plan(real);
+
+  // caches: the frozen prefix of the starting weights, built once per depth on s0
+  const Tables& t = c.tabs[dt];
+  auto build = [&]() -> hipError_t {
+    EKYA_HIP(permute_weights(weights, pmaster, t.permute, t.n_permute, net.total, 1, s0));
+    EKYA_HIP(bn_fold(pmaster, t.fold_all, t.n_fold_all, pfold, s0));
+    EKYA_HIP(pack_conv_weights(dt, pmaster, t.pack_all, t.n_pack_all, pshadow, s0));
+    if (!caches.empty())
+      EKYA_HIP(hipMemcpyAsync(d_S, S.data(), S.size() * sizeof(int32_t), hipMemcpyHostToDevice, s0));
+    for (auto& ci : caches) {
+      EKYA_HIP(build_cache(net, geo, pshadow, pfold, pmaster, ci.lowest, frames, d_S, ci.n_rows_s,
+                           ci.p, ci.row_bytes, 0, padded, ccap, ceb, s0));
+      EKYA_HIP(build_cache(net, geo, pshadow, pfold, pmaster, ci.lowest, hframes, nullptr,
+                           n_heldout, ci.p, ci.row_bytes, ci.n_rows_s, padded, ccap, ceb, s0));
+    }
+    return hipSuccess;
+  };
+  hipError_t he = build();
+  if (he == hipSuccess) he = hipStreamSynchronize(s0);
+  // held-out rows of a depth's cache sit after its n_rows_s training rows
+  for (int i = 0; i < n_cfgs && he == hipSuccess; ++i) {
+    TrainJob& j = jobs[i];
+    for (auto& ci : caches)
+      if (ci.lowest == j.lowest) {
+        j.cache = ci.p;
+        j.row_bytes = ci.row_bytes;
+        j.hcache = reinterpret_cast<char*>(ci.p) + (long long)ci.n_rows_s * ci.row_bytes;
+      }
+  }
+  std::vector<hipError_t> errs(n_cfgs, hipSuccess);
+  auto run_job = [&](int i) {
+    TrainJob& j = jobs[i];
+    hipError_t e = create_events(j);
+    if (e == hipSuccess) e = job_setup(j);
+    if (e == hipSuccess) e = job_epochs(j);
+    errs[i] = e;
+  };
+  if (he == hipSuccess) {
+    if (concurrent) {
+      std::vector<std::thread> th;
+      for (int i = 0; i < n_cfgs; ++i) th.emplace_back([&, i]() {
+        (void)hipSetDevice(c.device);
+        run_job(i);
+      });
+      for (auto& x : th) x.join();
+    } else {
+      for (int i = 0; i < n_cfgs; ++i) {
+        run_job(i);
+        if (errs[i] == hipSuccess) errs[i] = hipStreamSynchronize(jobs[i].st);
+      }
+    }
+  }
+  ekya_status overall = EKYA_OK;
+  for (int i = 0; i < n_cfgs; ++i) {
+    TrainJob& j = jobs[i];
+    ekya_profile_result& o = out[i];
+    std::memset(&o, 0, sizeof(o));
+    hipError_t e = (he != hipSuccess) ? he : errs[i];
+    JobResult r;
+    if (e == hipSuccess) e = job_collect(j, r);
+    if (e != hipSuccess) {
+      o.status = (e == hipErrorOutOfMemory) ? EKYA_ERR_NOMEM : EKYA_ERR_HIP;
+      c.err = std::string("HIP error: ") + hipGetErrorString(e);
+      overall = (ekya_status)o.status;
+    } else {
+      o.status = r.status;
+      o.n_train = j.n_s;
+      for (int ep = 0; ep < j.epochs; ++ep) {
+        o.heldout_acc[ep] = n_heldout ? (float)r.hc[ep] / (float)n_heldout : 0.f;
+        o.epoch_seconds[ep] = r.secs[ep];
+      }
+      o.heldout_acc_final = o.heldout_acc[j.epochs - 1];
+      if (r.status != EKYA_OK && overall == EKYA_OK) {
+        overall = r.status;
+        c.err = "training loss is not finite";
+      }
+    }
+    destroy_events(j);
+  }
+  return overall;
+}
+
+// ----------------------------------------------------------------- infer
+ekya_status run_infer(Ctx& c, const float* weights, const void* frames, int n, int H, int W,
+                      int resolution, int precision, int32_t* labels_out, hipStream_t stream) {
+  EKYA_CHECK_HIP(hipSetDevice(c.device));
+  const int dt = precision;
+  const Net& net = c.net[dt];
+  const Geo geo = Geo::build(net, resolution, resolution);
+  const size_t es = dtype_size(dt);
+  const int cap = 256;
+  float *master = nullptr, *fold = nullptr;
+  void *shadow = nullptr, *padded = nullptr;
+  EvalBufs eb;
+  auto plan = [&](Arena& a) {
+    master = a.take<float>(net.total);
+    fold = a.take<float>(2 * net.bn_channels);
+    shadow = a.take_bytes(net.shadow_elems * es);
+    padded = a.take_bytes((size_t)cap * resolution * resolution * net.conv[0].cin_pad * es);
+    plan_eval(a, net, geo, 0, 5, cap, eb);
+  };
+  Arena meas;
+  plan(meas);
+  // the previous inference call may still be using the workspace
+  EKYA_CHECK_HIP(hipStreamWaitEvent(stream, c.infer_done, 0));
+  if (meas.used > c.infer_ws.cap) EKYA_CHECK_HIP(hipEventSynchronize(c.infer_done));
+  EKYA_CHECK_HIP(c.infer_ws.ensure(meas.used));
+  Arena real;
+  real.base = reinterpret_cast<char*>(c.infer_ws.p);
+  plan(real);
+  const Tables& t = c.tabs[dt];
+  auto run = [&]() -> hipError_t {
+    EKYA_HIP(permute_weights(weights, master, t.permute, t.n_permute, net.total, 1, stream));
+    EKYA_HIP(bn_fold(master, t.fold_all, t.n_fold_all, fold, stream));
+    EKYA_HIP(pack_conv_weights(dt, master, t.pack_all, t.n_pack_all, shadow, stream));
+    const long long fbytes = (long long)H * W * 3 * es;
+    for (int i0 = 0; i0 < n; i0 += cap) {
+      const int cnt = std::min(cap, n - i0);
+      const void* src = reinterpret_cast<const char*>(frames) + i0 * fbytes;
+      if (resolution == H && resolution == W)
+        EKYA_HIP(frames_to_padded(dt, src, nullptr, cnt, H, W, net.conv[0].cin_pad, padded, stream));
+      else
+        EKYA_HIP(resize_to_padded(dt, src, cnt, H, W, resolution, net.conv[0].cin_pad, padded,
+                                  stream));
+      EKYA_HIP(eval_forward(net, geo, shadow, fold, master, 0, 5, padded, cnt, eb, eb.logits,
+                            stream));
+      EKYA_HIP(argmax_rows(eb.logits, cnt, net.n_classes, labels_out + i0, stream));
+    }
+    EKYA_HIP(hipEventRecord(c.infer_done, stream));
+    return hipSuccess;
+  };
+  EKYA_CHECK_HIP(run());
+  return EKYA_OK;
+}
+
+}  // namespace ekya
