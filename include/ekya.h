@@ -169,6 +169,22 @@ ekya_status ekya_profile(ekya_ctx* ctx, const float* weights, const ekya_profile
 ekya_status ekya_infer(ekya_ctx* ctx, const float* weights, const void* frames, int n, int H,
                        int W, int resolution, int precision, int32_t* labels_out, void* stream);
 
+/* ------------------------------------------------------------ kernel timing
+ * Per-kernel GPU time, the measurement the micro-profiler rests on (the
+ * resource demand of a configuration is measured as GPU time, section 4.3),
+ * broken down by GEMM kernel.  ekya_set_kernel_timing(ctx, 1) clears the
+ * statistics and makes later ekya_retrain / ekya_infer calls on this context
+ * bracket every convolution GEMM launch with two HIP events on the launch's
+ * stream (0 turns it off; statistics are kept).  ekya_kernel_timing reads
+ * entry `index` (0-based; waits for the recorded launches to finish): kernel
+ * name into name (NUL-terminated, truncated to name_cap), launch count, summed
+ * event time in ms, summed algorithmic flops (2*N*P*Q*K*R*S*C) and bytes
+ * (input + weights + output).  Returns 0, or -1 past the last entry or on
+ * invalid arguments. */
+ekya_status ekya_set_kernel_timing(ekya_ctx* ctx, int enable);
+int ekya_kernel_timing(ekya_ctx* ctx, int index, char* name, int name_cap, long long* launches,
+                       double* total_ms, double* flops, double* bytes);
+
 /* ------------------------------------------------------------ host helpers
  * The uniform training subset ekya_retrain draws (section 4.3, "Training data
  * sampling"): writes round-half-up(frac * n_frames) (>= 1) distinct frame

@@ -80,6 +80,10 @@ _SIGS = {
     "ekya_profile": (_I, [_P, _P, ctypes.POINTER(ProfileCfg), _I, _P, _P, _I, _I, _I, _P, _P, _I,
                           ctypes.c_uint64, _I, _I, ctypes.POINTER(ProfileResult)]),
     "ekya_infer": (_I, [_P, _P, _P, _I, _I, _I, _I, _I, _P, _P]),
+    "ekya_set_kernel_timing": (_I, [_P, _I]),
+    "ekya_kernel_timing": (_I, [_P, _I, ctypes.c_char_p, _I, ctypes.POINTER(_LL),
+                                ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double),
+                                ctypes.POINTER(ctypes.c_double)]),
     "ekya_training_subset": (_I, [_I, ctypes.c_double, ctypes.c_uint64, _P, _I]),
     "ekya_epoch_order": (_I, [_I, ctypes.c_uint64, _I, _P]),
     "ekya_op_conv2d": (_I, [_I, _P, _I, _I, _I, _I, _P, _I, _I, _I, _I, _I, _P, _P]),
@@ -175,6 +179,28 @@ def ekya_destroy(ctx) -> None:
 
 def ekya_weights_count(n_classes: int = 6) -> int:
     return int(load().ekya_weights_count(n_classes))
+
+
+def ekya_set_kernel_timing(ctx, enable: bool) -> None:
+    _check(load().ekya_set_kernel_timing(ctx, 1 if enable else 0), ctx)
+
+
+def ekya_kernel_timing(ctx) -> List[dict]:
+    """All timed GEMM kernels: name, launches, total_ms, flops, bytes."""
+    lib = load()
+    out = []
+    i = 0
+    while True:
+        name = ctypes.create_string_buffer(256)
+        n = _LL()
+        ms, fl, by = ctypes.c_double(), ctypes.c_double(), ctypes.c_double()
+        if lib.ekya_kernel_timing(ctx, i, name, 256, ctypes.byref(n), ctypes.byref(ms),
+                                  ctypes.byref(fl), ctypes.byref(by)) != 0:
+            break
+        out.append({"name": name.value.decode(), "launches": n.value, "total_ms": ms.value,
+                    "flops": fl.value, "bytes": by.value})
+        i += 1
+    return out
 
 
 def ekya_training_subset(n_frames: int, subsample_frac: float, seed: int) -> List[int]:

@@ -2,7 +2,9 @@
 // codes, and the op-level entry points used for kernel-by-kernel parity.
 #include <algorithm>
 #include <cmath>
+#include <cstdio>
 #include <cstring>
+#include <iterator>
 #include <new>
 #include <string>
 #include <vector>
@@ -175,6 +177,32 @@ ekya_status ekya_infer(ekya_ctx* ctx, const float* weights, const void* frames, 
                          (hipStream_t)stream);
 }
 
+ekya_status ekya_set_kernel_timing(ekya_ctx* ctx, int enable) {
+  if (!ctx) return fail(nullptr, EKYA_ERR_INVALID_ARG, "ctx is null");
+  if (enable) {
+    hipError_t e = ekya::ctx_collect_timing(ctx->c);
+    if (e != hipSuccess) return fail(ctx, EKYA_ERR_HIP, std::string("HIP error: ") + hipGetErrorString(e));
+    ctx->c.stats.clear();
+  }
+  ctx->c.timing = enable != 0;
+  return EKYA_OK;
+}
+
+int ekya_kernel_timing(ekya_ctx* ctx, int index, char* name, int name_cap, long long* launches,
+                       double* total_ms, double* flops, double* bytes) {
+  if (!ctx || index < 0 || !name || name_cap < 1) return -1;
+  if (ekya::ctx_collect_timing(ctx->c) != hipSuccess) return -1;
+  if (index >= (int)ctx->c.stats.size()) return -1;
+  auto it = ctx->c.stats.begin();
+  std::advance(it, index);
+  std::snprintf(name, name_cap, "%s", it->first.c_str());
+  if (launches) *launches = it->second.launches;
+  if (total_ms) *total_ms = it->second.ms;
+  if (flops) *flops = it->second.flops;
+  if (bytes) *bytes = it->second.bytes;
+  return 0;
+}
+
 int ekya_training_subset(int n_frames, double subsample_frac, uint64_t seed, int32_t* idx_out,
                          int capacity) {
   if (n_frames < 1 || !(subsample_frac > 0.0 && subsample_frac <= 1.0) || !idx_out) return -1;
@@ -286,24 +314,29 @@ ekya_status ekya_op_conv2d(int precision, const void* x, int N, int H, int W, in
   void *krsc, *crsk;
   hipError_t e = pad_input(precision, x, N, H, W, C, Cp, tmp, &xp, st);
   if (e == hipSuccess) e = pack_one(precision, w, K, C, R, S, Cp, tmp, &krsc, &crsk, st);
-  if (e == hipSuccess)
-    e = ekya::conv_fwd(precision, make_geom(N, H, W, Cp, K, R, S, stride, pad), xp, krsc, y,
-                       ekya::ConvEpilogue(), st);
+  const ekya::ConvGeom g = make_geom(N, H, W, Cp, K, R, S, stride, pad);
+  const size_t wsf = ekya::conv_split_workspace_floats(precision, g, false);
+  float* ws = wsf ? tmp.get<float>(wsf) : nullptr;
+  if (wsf && !ws) e = hipErrorOutOfMemory;
+  if (e == hipSuccess) e = ekya::conv_fwd(precision, g, xp, krsc, y, ekya::ConvEpilogue(), ws, wsf, st);
   return sync_status(st, e);
 }
 
 ekya_status ekya_op_conv2d_dgrad(int precision, const void* dy, const float* w, int N, int H,
                                  int W, int C, int K, int R, int S, int stride, int pad, void* dx,
                                  void* stream) {
-  if (!dy || !w || !dx || !conv_args_ok(precision, N, H, W, C, K, R, S, stride, pad, false))
+  if (!dy || !w || !dx || !conv_args_ok(precision, N, H, W, C, K, R, S, stride, pad, false) ||
+      K % (8 * ekya::dtype_vec(precision)) != 0 || stride > 2)
     return fail(nullptr, EKYA_ERR_INVALID_ARG, "invalid conv2d_dgrad arguments");
   hipStream_t st = (hipStream_t)stream;
   Tmp tmp;
   void *krsc, *crsk;
   hipError_t e = pack_one(precision, w, K, C, R, S, C, tmp, &krsc, &crsk, st);
-  if (e == hipSuccess)
-    e = ekya::conv_dgrad(precision, make_geom(N, H, W, C, K, R, S, stride, pad), dy, crsk, dx,
-                         nullptr, st);
+  const ekya::ConvGeom g = make_geom(N, H, W, C, K, R, S, stride, pad);
+  const size_t wsf = ekya::conv_split_workspace_floats(precision, g, true);
+  float* ws = wsf ? tmp.get<float>(wsf) : nullptr;
+  if (wsf && !ws) e = hipErrorOutOfMemory;
+  if (e == hipSuccess) e = ekya::conv_dgrad(precision, g, dy, crsk, dx, nullptr, ws, wsf, st);
   return sync_status(st, e);
 }
 

@@ -1,13 +1,21 @@
 // Convolution forward, data-gradient and weight-gradient as implicit GEMMs on
 // MFMA (gfx950).  One block-tiled main loop (256 threads, 2 x 2 waves, LDS
-// double buffering of 16-byte k-contiguous units) is shared by three operand
-// policies:
+// double buffering of 16-byte k-contiguous units, one stage of global->register
+// prefetch) is shared by three operand policies:
 //   forward : D[k][pix]   = sum_(r,s,c)  w[k][r][s][c]  * x(pix; r,s,c)
 //   dgrad   : D[c][pix]   = sum_(r,s,k)  wT[c][r][s][k] * dy(pix; r,s,k)
 //   wgrad   : D[rsc][k]   = sum_(pix)    x(pix; rsc)    * dy[pix][k]
 // Rows of D are MFMA rows (the lane's four accumulator values are four
 // consecutive rows), so forward/dgrad lanes own four consecutive NHWC channels
 // and wgrad lanes own four consecutive (r,s,c) entries of one output channel.
+//
+// A stage covers KU units (KU*E reduction elements) of every tile row.  When
+// the channel count is a multiple of that, a stage never straddles a filter
+// tap, so the tap (r, s) and channel offset are block-uniform scalars that
+// advance incrementally and the per-unit address is a bounds test plus an add.
+// Forward and dgrad split the reduction over blockIdx.z when the output has too
+// few tiles to fill the chip; partial sums go to an fp32 buffer that a second
+// kernel adds up in a fixed order (deterministic) and finishes with the epilogue.
 #include <algorithm>
 
 #include "kernels.hpp"
@@ -45,6 +53,23 @@ template <> __device__ __forceinline__ void load4<bf16>(const bf16* src, float (
   for (int i = 0; i < 4; ++i) v[i] = (float)p.e[i];
 }
 
+__device__ __forceinline__ uint4 ld16(const void* p) { return *reinterpret_cast<const uint4*>(p); }
+
+// Quotient of non-negative a < 2^22 by d > 0, with inv = 1.0f / d.
+__device__ __forceinline__ int fdiv(int a, int d, float inv) {
+  int q = (int)((float)a * inv);
+  if (q * d > a) --q;
+  if ((q + 1) * d <= a) ++q;
+  return q;
+}
+
+// Split-K output: partial sums in [split][col][row] fp32 (col = pixel).
+struct SplitOut {
+  float* part;
+  int splits;
+  int stages_per_split;
+};
+
 // ------------------------------------------------------------------ forward
 template <typename T> struct FwdArgs {
   ConvGeom g;
@@ -52,97 +77,131 @@ template <typename T> struct FwdArgs {
   const T* w;
   T* y;
   ConvEpilogue epi;
+  SplitOut so;
 };
 
-template <typename T, int BM, int BN>
+template <typename T, int BM, int BN, int KU_, bool UT>
 struct FwdPolicy {
   static constexpr int E = Elt<T>::E;
-  static constexpr int KU = 4;
+  static constexpr int KU = KU_;
   static constexpr int UA = BM * KU / NT;
   static constexpr int UB = BN * KU / NT;
   using Args = FwdArgs<T>;
 
-  int Ktot, m0, n0;
+  int Ktot, m0, n0, s_begin, s_end;
   const T* arow[UA];
-  int au[UA];
-  const T* bimg[UB];
+  const T* bptr[UB];   // UT: pixel origin + this unit's channel offset
   int bh0[UB], bw0[UB], bu[UB];
   bool bok[UB];
+  int tr, ts, tc;      // UT: tap and channel offset of the next stage to fetch
   uint4 ra[UA], rb[UB];
 
-  __device__ void init(const Args& a, int m0_, int n0_, int /*split*/) {
+  __device__ void init(const Args& a, int m0_, int n0_, int split) {
     const ConvGeom& g = a.g;
     m0 = m0_;
     n0 = n0_;
     Ktot = g.R * g.S * g.C;
+    const int ns = cdiv(Ktot, KU * E);
+    s_begin = min(ns, split * a.so.stages_per_split);
+    s_end = min(ns, s_begin + a.so.stages_per_split);
 #pragma unroll
     for (int i = 0; i < UA; ++i) {
-      int q = threadIdx.x + NT * i, row = q / KU;
-      au[i] = q % KU;
-      int k = m0 + row;
-      arow[i] = (k < g.K) ? a.w + (long long)k * Ktot : nullptr;
+      const int q = threadIdx.x + NT * i, k = m0 + q / KU;
+      arow[i] = (k < g.K) ? a.w + (long long)k * Ktot + (q % KU) * E : nullptr;
     }
     const int npix = g.N * g.P * g.Q;
 #pragma unroll
     for (int i = 0; i < UB; ++i) {
-      int q = threadIdx.x + NT * i, row = q / KU;
+      const int q = threadIdx.x + NT * i, pix = n0 + q / KU;
       bu[i] = q % KU;
-      int pix = n0 + row;
       bok[i] = pix < npix;
-      int pp = bok[i] ? pix : 0;
-      int n = pp / (g.P * g.Q), rem = pp % (g.P * g.Q);
-      int p = rem / g.Q, qq = rem % g.Q;
-      bimg[i] = a.x + (long long)n * g.H * g.W * g.C;
+      const int pp = bok[i] ? pix : 0;
+      const int n = pp / (g.P * g.Q), rem = pp % (g.P * g.Q);
+      const int p = rem / g.Q, qq = rem % g.Q;
       bh0[i] = p * g.stride - g.pad;
       bw0[i] = qq * g.stride - g.pad;
+      bptr[i] = a.x + (long long)n * g.H * g.W * g.C;
+      if (UT) bptr[i] += ((long long)bh0[i] * g.W + bw0[i]) * g.C + bu[i] * E;
+    }
+    if (UT) {
+      const int k0 = s_begin * KU * E;
+      const int rs = k0 / g.C;
+      tc = k0 - rs * g.C;
+      tr = rs / g.S;
+      ts = rs - tr * g.S;
     }
   }
-  __device__ int num_stages(const Args&) const { return cdiv(Ktot, KU * E); }
+  __device__ int first_stage() const { return s_begin; }
+  __device__ int end_stage() const { return s_end; }
   __device__ void fetch(const Args& a, int st) {
     const ConvGeom& g = a.g;
+    const int k0 = st * KU * E;
 #pragma unroll
-    for (int i = 0; i < UA; ++i) {
-      int k = st * KU * E + au[i] * E;
-      ra[i] = (arow[i] && k < Ktot) ? *reinterpret_cast<const uint4*>(arow[i] + k) : zero_unit();
-    }
+    for (int i = 0; i < UA; ++i)
+      ra[i] = (arow[i] && (UT || k0 + (int)((threadIdx.x + NT * i) % KU) * E < Ktot))
+                  ? ld16(arow[i] + k0) : zero_unit();
+    if (UT) {
+      const long long off = ((long long)tr * g.W + ts) * g.C + tc;
 #pragma unroll
-    for (int i = 0; i < UB; ++i) {
-      int k = st * KU * E + bu[i] * E;
-      uint4 v = zero_unit();
-      if (bok[i] && k < Ktot) {
-        int c = k % g.C, rs = k / g.C;
-        int r = rs / g.S, s = rs % g.S;
-        int h = bh0[i] + r, w = bw0[i] + s;
-        if (h >= 0 && h < g.H && w >= 0 && w < g.W)
-          v = *reinterpret_cast<const uint4*>(bimg[i] + ((long long)h * g.W + w) * g.C + c);
+      for (int i = 0; i < UB; ++i) {
+        const bool in = bok[i] && (unsigned)(bh0[i] + tr) < (unsigned)g.H &&
+                        (unsigned)(bw0[i] + ts) < (unsigned)g.W;
+        rb[i] = in ? ld16(bptr[i] + off) : zero_unit();
       }
-      rb[i] = v;
+      tc += KU * E;
+      if (tc >= g.C) {
+        tc = 0;
+        if (++ts == g.S) {
+          ts = 0;
+          ++tr;
+        }
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < UB; ++i) {
+        const int k = k0 + bu[i] * E;
+        uint4 v = zero_unit();
+        if (bok[i] && k < Ktot) {
+          const int c = k % g.C, rs = k / g.C;
+          const int r = rs / g.S, s = rs % g.S;
+          const int h = bh0[i] + r, w = bw0[i] + s;
+          if (h >= 0 && h < g.H && w >= 0 && w < g.W)
+            v = ld16(bptr[i] + ((long long)h * g.W + w) * g.C + c);
+        }
+        rb[i] = v;
+      }
     }
   }
   template <int PITCH>
   __device__ void commit(uint4* As, uint4* Bs) {
 #pragma unroll
     for (int i = 0; i < UA; ++i) {
-      int q = threadIdx.x + NT * i;
+      const int q = threadIdx.x + NT * i;
       As[(q / KU) * PITCH + q % KU] = ra[i];
     }
 #pragma unroll
     for (int i = 0; i < UB; ++i) {
-      int q = threadIdx.x + NT * i;
+      const int q = threadIdx.x + NT * i;
       Bs[(q / KU) * PITCH + q % KU] = rb[i];
     }
   }
   // row = output channel, col = output pixel; v = 4 consecutive channels
   __device__ void out4(const Args& a, int row, int col, float (&v)[4]) {
     const ConvGeom& g = a.g;
-    if (row >= g.K || col >= g.N * g.P * g.Q) return;
+    const int npix = g.N * g.P * g.Q;
+    if (row >= g.K || col >= npix) return;
+    const long long off = (long long)col * g.K + row;
+    if (a.so.splits > 1) {
+      float* dst = a.so.part + (long long)blockIdx.z * npix * g.K + off;
+      *reinterpret_cast<float4*>(dst) = make_float4(v[0], v[1], v[2], v[3]);
+      return;
+    }
     const ConvEpilogue& e = a.epi;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       if (e.scale) v[i] *= e.scale[row + i];
       if (e.shift) v[i] += e.shift[row + i];
     }
-    long long off = (long long)col * g.K + row;
     if (e.res) {
       float r[4];
       load4<T>(reinterpret_cast<const T*>(e.res) + off, r);
@@ -164,92 +223,103 @@ template <typename T> struct DgradArgs {
   const T* wt;  // [C][R][S][K]
   T* dx;
   const T* res;
+  SplitOut so;
 };
 
-template <typename T, int BM, int BN>
+// Requires K % (KU*E) == 0 (every stage within one tap) and stride 1 or 2.
+template <typename T, int BM, int BN, int KU_, bool UT>
 struct DgradPolicy {
   static constexpr int E = Elt<T>::E;
-  static constexpr int KU = 4;
+  static constexpr int KU = KU_;
   static constexpr int UA = BM * KU / NT;
   static constexpr int UB = BN * KU / NT;
   using Args = DgradArgs<T>;
 
-  int Ktot, m0, n0;
+  int Ktot, m0, n0, s_begin, s_end;
   const T* arow[UA];
-  int au[UA];
-  const T* bimg[UB];
-  int bh[UB], bw[UB], bu[UB];
+  const T* bimg[UB];   // image base + this unit's channel offset
+  int bh[UB], bw[UB];  // input pixel + pad
   bool bok[UB];
+  int tr, ts, tk;
   uint4 ra[UA], rb[UB];
 
-  __device__ void init(const Args& a, int m0_, int n0_, int) {
+  __device__ void init(const Args& a, int m0_, int n0_, int split) {
     const ConvGeom& g = a.g;
     m0 = m0_;
     n0 = n0_;
     Ktot = g.R * g.S * g.K;
+    const int ns = cdiv(Ktot, KU * E);
+    s_begin = min(ns, split * a.so.stages_per_split);
+    s_end = min(ns, s_begin + a.so.stages_per_split);
 #pragma unroll
     for (int i = 0; i < UA; ++i) {
-      int q = threadIdx.x + NT * i, row = q / KU;
-      au[i] = q % KU;
-      int c = m0 + row;
-      arow[i] = (c < g.C) ? a.wt + (long long)c * Ktot : nullptr;
+      const int q = threadIdx.x + NT * i, c = m0 + q / KU;
+      arow[i] = (c < g.C) ? a.wt + (long long)c * Ktot + (q % KU) * E : nullptr;
     }
     const int npix = g.N * g.H * g.W;
 #pragma unroll
     for (int i = 0; i < UB; ++i) {
-      int q = threadIdx.x + NT * i, row = q / KU;
-      bu[i] = q % KU;
-      int pix = n0 + row;
+      const int q = threadIdx.x + NT * i, pix = n0 + q / KU;
       bok[i] = pix < npix;
-      int pp = bok[i] ? pix : 0;
-      int n = pp / (g.H * g.W), rem = pp % (g.H * g.W);
-      bimg[i] = a.dy + (long long)n * g.P * g.Q * g.K;
+      const int pp = bok[i] ? pix : 0;
+      const int n = pp / (g.H * g.W), rem = pp % (g.H * g.W);
+      bimg[i] = a.dy + (long long)n * g.P * g.Q * g.K + (q % KU) * E;
       bh[i] = rem / g.W + g.pad;
       bw[i] = rem % g.W + g.pad;
     }
+    const int k0 = s_begin * KU * E;
+    const int rs = k0 / g.K;
+    tk = k0 - rs * g.K;
+    tr = rs / g.S;
+    ts = rs - tr * g.S;
   }
-  __device__ int num_stages(const Args&) const { return cdiv(Ktot, KU * E); }
+  __device__ int first_stage() const { return s_begin; }
+  __device__ int end_stage() const { return s_end; }
   __device__ void fetch(const Args& a, int st) {
     const ConvGeom& g = a.g;
+    const int k0 = st * KU * E;
 #pragma unroll
-    for (int i = 0; i < UA; ++i) {
-      int k = st * KU * E + au[i] * E;
-      ra[i] = (arow[i] && k < Ktot) ? *reinterpret_cast<const uint4*>(arow[i] + k) : zero_unit();
-    }
+    for (int i = 0; i < UA; ++i) ra[i] = arow[i] ? ld16(arow[i] + k0) : zero_unit();
+    const int sh = g.stride == 2 ? 1 : 0;
 #pragma unroll
     for (int i = 0; i < UB; ++i) {
-      int k = st * KU * E + bu[i] * E;
-      uint4 v = zero_unit();
-      if (bok[i] && k < Ktot) {
-        int kk = k % g.K, rs = k / g.K;
-        int r = rs / g.S, s = rs % g.S;
-        int hp = bh[i] - r, wp = bw[i] - s;
-        if (hp >= 0 && wp >= 0 && hp % g.stride == 0 && wp % g.stride == 0) {
-          int p = hp / g.stride, q = wp / g.stride;
-          if (p < g.P && q < g.Q)
-            v = *reinterpret_cast<const uint4*>(bimg[i] + ((long long)p * g.Q + q) * g.K + kk);
-        }
+      const int hp = bh[i] - tr, wp = bw[i] - ts;
+      const int p = hp >> sh, q = wp >> sh;
+      const bool in = bok[i] && hp >= 0 && wp >= 0 && ((hp | wp) & sh) == 0 && p < g.P && q < g.Q;
+      rb[i] = in ? ld16(bimg[i] + ((long long)p * g.Q + q) * g.K + tk) : zero_unit();
+    }
+    tk += KU * E;
+    if (tk >= g.K) {
+      tk = 0;
+      if (++ts == g.S) {
+        ts = 0;
+        ++tr;
       }
-      rb[i] = v;
     }
   }
   template <int PITCH>
   __device__ void commit(uint4* As, uint4* Bs) {
 #pragma unroll
     for (int i = 0; i < UA; ++i) {
-      int q = threadIdx.x + NT * i;
+      const int q = threadIdx.x + NT * i;
       As[(q / KU) * PITCH + q % KU] = ra[i];
     }
 #pragma unroll
     for (int i = 0; i < UB; ++i) {
-      int q = threadIdx.x + NT * i;
+      const int q = threadIdx.x + NT * i;
       Bs[(q / KU) * PITCH + q % KU] = rb[i];
     }
   }
   __device__ void out4(const Args& a, int row, int col, float (&v)[4]) {
     const ConvGeom& g = a.g;
-    if (row >= g.C || col >= g.N * g.H * g.W) return;
-    long long off = (long long)col * g.C + row;
+    const int npix = g.N * g.H * g.W;
+    if (row >= g.C || col >= npix) return;
+    const long long off = (long long)col * g.C + row;
+    if (a.so.splits > 1) {
+      float* dst = a.so.part + (long long)blockIdx.z * npix * g.C + off;
+      *reinterpret_cast<float4*>(dst) = make_float4(v[0], v[1], v[2], v[3]);
+      return;
+    }
     if (a.res) {
       float r[4];
       load4<T>(a.res + off, r);
@@ -272,7 +342,7 @@ template <typename T> struct WgradArgs {
   int m_per_split;
 };
 
-template <typename T, int BM, int BN>
+template <typename T, int BM, int BN, int KU_, bool UT_>
 struct WgradPolicy {
   static constexpr int E = Elt<T>::E;
   static constexpr int KU = E;               // units (of E pixels) per row per stage
@@ -282,8 +352,8 @@ struct WgradPolicy {
   using Args = WgradArgs<T>;
 
   int m0, n0, mb, me, RSC;
+  float inv_pq, inv_q;
   uint4 rv[NBLK][E];
-  // A-block geometry (x side)
   int ar[NBLK], as_[NBLK], ac[NBLK];
   bool aok[NBLK];
 
@@ -295,16 +365,17 @@ struct WgradPolicy {
     const int M = g.N * g.P * g.Q;
     mb = split * a.m_per_split;
     me = min(M, mb + a.m_per_split);
+    inv_pq = 1.0f / (float)(g.P * g.Q);
+    inv_q = 1.0f / (float)g.Q;
 #pragma unroll
     for (int j = 0; j < NBLK; ++j) {
-      int b = threadIdx.x + NT * j;
+      const int b = threadIdx.x + NT * j;
       aok[j] = false;
       if (b < NA) {
-        int rg = b % (BM / E);
-        int i0 = m0 + rg * E;
+        const int i0 = m0 + (b % (BM / E)) * E;
         if (i0 < RSC) {
           aok[j] = true;
-          int rs = i0 / g.C;
+          const int rs = i0 / g.C;
           ac[j] = i0 % g.C;
           ar[j] = rs / g.S;
           as_[j] = rs % g.S;
@@ -312,31 +383,31 @@ struct WgradPolicy {
       }
     }
   }
-  __device__ int num_stages(const Args&) const {
-    return me > mb ? cdiv(me - mb, KU * E) : 0;
-  }
+  __device__ int first_stage() const { return 0; }
+  __device__ int end_stage() const { return me > mb ? cdiv(me - mb, KU * E) : 0; }
   __device__ void fetch(const Args& a, int st) {
     const ConvGeom& g = a.g;
 #pragma unroll
     for (int j = 0; j < NBLK; ++j) {
-      int b = threadIdx.x + NT * j;
+      const int b = threadIdx.x + NT * j;
 #pragma unroll
       for (int e = 0; e < E; ++e) rv[j][e] = zero_unit();
       if (b < NA) {
         if (!aok[j]) continue;
-        int u = b / (BM / E);
-        int m = mb + st * KU * E + u * E;
+        const int u = b / (BM / E);
+        const int m = mb + st * KU * E + u * E;
         if (m >= me) continue;
-        int PQ = g.P * g.Q;
-        int n = m / PQ, rem = m % PQ;
-        int p = rem / g.Q, q = rem % g.Q;
+        const int PQ = g.P * g.Q;
+        int n = fdiv(m, PQ, inv_pq);
+        const int rem = m - n * PQ;
+        int p = fdiv(rem, g.Q, inv_q);
+        int q = rem - p * g.Q;
 #pragma unroll
         for (int e = 0; e < E; ++e) {
           if (m + e < me) {
-            int h = p * g.stride - g.pad + ar[j], w = q * g.stride - g.pad + as_[j];
-            if (h >= 0 && h < g.H && w >= 0 && w < g.W)
-              rv[j][e] = *reinterpret_cast<const uint4*>(
-                  a.x + (((long long)n * g.H + h) * g.W + w) * g.C + ac[j]);
+            const int h = p * g.stride - g.pad + ar[j], w = q * g.stride - g.pad + as_[j];
+            if ((unsigned)h < (unsigned)g.H && (unsigned)w < (unsigned)g.W)
+              rv[j][e] = ld16(a.x + (((long long)n * g.H + h) * g.W + w) * g.C + ac[j]);
           }
           if (++q == g.Q) {
             q = 0;
@@ -348,15 +419,13 @@ struct WgradPolicy {
         }
         transpose_block(rv[j], (T*)nullptr);
       } else if (b < NA + NB) {
-        int bb = b - NA;
-        int rg = bb % (BN / E), u = bb / (BN / E);
-        int k0 = n0 + rg * E;
-        int m = mb + st * KU * E + u * E;
+        const int bb = b - NA;
+        const int k0 = n0 + (bb % (BN / E)) * E;
+        const int m = mb + st * KU * E + (bb / (BN / E)) * E;
         if (k0 >= g.K) continue;
 #pragma unroll
         for (int e = 0; e < E; ++e)
-          if (m + e < me)
-            rv[j][e] = *reinterpret_cast<const uint4*>(a.dy + (long long)(m + e) * g.K + k0);
+          if (m + e < me) rv[j][e] = ld16(a.dy + (long long)(m + e) * g.K + k0);
         transpose_block(rv[j], (T*)nullptr);
       }
     }
@@ -365,14 +434,14 @@ struct WgradPolicy {
   __device__ void commit(uint4* As, uint4* Bs) {
 #pragma unroll
     for (int j = 0; j < NBLK; ++j) {
-      int b = threadIdx.x + NT * j;
+      const int b = threadIdx.x + NT * j;
       if (b < NA) {
-        int rg = b % (BM / E), u = b / (BM / E);
+        const int rg = b % (BM / E), u = b / (BM / E);
 #pragma unroll
         for (int e = 0; e < E; ++e) As[(rg * E + e) * PITCH + u] = rv[j][e];
       } else if (b < NA + NB) {
-        int bb = b - NA;
-        int rg = bb % (BN / E), u = bb / (BN / E);
+        const int bb = b - NA;
+        const int rg = bb % (BN / E), u = bb / (BN / E);
 #pragma unroll
         for (int e = 0; e < E; ++e) Bs[(rg * E + e) * PITCH + u] = rv[j][e];
       }
@@ -403,7 +472,7 @@ __global__ __launch_bounds__(NT) void gemm_kernel(typename Pol::Args args) {
 
   Pol pol;
   pol.init(args, m0, n0, blockIdx.z);
-  const int ns = pol.num_stages(args);
+  const int s0 = pol.first_stage(), s1 = pol.end_stage();
 
   f32x4 acc[TI][TJ];
 #pragma unroll
@@ -411,15 +480,15 @@ __global__ __launch_bounds__(NT) void gemm_kernel(typename Pol::Args args) {
 #pragma unroll
     for (int j = 0; j < TJ; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  if (ns > 0) {
-    pol.fetch(args, 0);
+  if (s0 < s1) {
+    pol.fetch(args, s0);
     pol.template commit<PITCH>(smem, smem + BM * PITCH);
   }
   __syncthreads();
-  for (int st = 0; st < ns; ++st) {
-    uint4* As = smem + (st & 1) * (BM + BN) * PITCH;
+  for (int st = s0; st < s1; ++st) {
+    uint4* As = smem + ((st - s0) & 1) * (BM + BN) * PITCH;
     uint4* Bs = As + BM * PITCH;
-    if (st + 1 < ns) pol.fetch(args, st + 1);
+    if (st + 1 < s1) pol.fetch(args, st + 1);
 #pragma unroll
     for (int u0 = 0; u0 < KU; u0 += 4) {
       uint4 fa[TI], fb[TJ];
@@ -432,8 +501,8 @@ __global__ __launch_bounds__(NT) void gemm_kernel(typename Pol::Args args) {
 #pragma unroll
         for (int j = 0; j < TJ; ++j) mma_unit(acc[i][j], fa[i], fb[j], (T*)nullptr);
     }
-    if (st + 1 < ns) {
-      uint4* An = smem + ((st + 1) & 1) * (BM + BN) * PITCH;
+    if (st + 1 < s1) {
+      uint4* An = smem + ((st + 1 - s0) & 1) * (BM + BN) * PITCH;
       pol.template commit<PITCH>(An, An + BM * PITCH);
     }
     __syncthreads();
@@ -448,16 +517,49 @@ __global__ __launch_bounds__(NT) void gemm_kernel(typename Pol::Args args) {
     }
 }
 
+// Sum of split-K partials [split][npix][C] in split order, then the epilogue.
 template <typename T>
+__global__ void split_reduce_kernel(const float* part, int splits, long long npix, int C,
+                                    ConvEpilogue e, T* y) {
+  const long long n4 = npix * C / 4;
+  const long long stride = npix * C;
+  for (long long i = blockIdx.x * (long long)blockDim.x + threadIdx.x; i < n4;
+       i += (long long)gridDim.x * blockDim.x) {
+    const long long off = i * 4;
+    const int row = (int)(off % C);
+    float4 s = *reinterpret_cast<const float4*>(part + off);
+    for (int z = 1; z < splits; ++z) {
+      const float4 t = *reinterpret_cast<const float4*>(part + z * stride + off);
+      s.x += t.x; s.y += t.y; s.z += t.z; s.w += t.w;
+    }
+    float v[4] = {s.x, s.y, s.z, s.w};
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      if (e.scale) v[k] *= e.scale[row + k];
+      if (e.shift) v[k] += e.shift[row + k];
+    }
+    if (e.res) {
+      float r[4];
+      load4<T>(reinterpret_cast<const T*>(e.res) + off, r);
+#pragma unroll
+      for (int k = 0; k < 4; ++k) v[k] += r[k];
+    }
+    if (e.relu) {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) v[k] = fmaxf(v[k], 0.f);
+    }
+    store4<T>(y + off, v);
+  }
+}
+
 __global__ void wgrad_reduce_kernel(const float* part, int splits, int K, int RS, int C, int C0,
                                     float* dw) {
-  long long n = (long long)K * RS * C0;
-  long long stride = (long long)K * RS * C;
+  const long long n = (long long)K * RS * C0;
+  const long long stride = (long long)K * RS * C;
   for (long long i = blockIdx.x * (long long)blockDim.x + threadIdx.x; i < n;
        i += (long long)gridDim.x * blockDim.x) {
-    int c = i % C0;
-    long long krs = i / C0;
-    long long src = krs * C + c;
+    const int c = (int)(i % C0);
+    const long long src = (i / C0) * C + c;
     float s = 0.f;
     for (int z = 0; z < splits; ++z) s += part[z * stride + src];
     dw[i] = s;
@@ -465,29 +567,94 @@ __global__ void wgrad_reduce_kernel(const float* part, int splits, int K, int RS
 }
 
 // -------------------------------------------------------------- launching
-template <typename T, template <typename, int, int> class PolT, int BM, int BN>
-hipError_t launch_gemm(const typename PolT<T, BM, BN>::Args& args, int rows, int cols, int splits,
-                       hipStream_t stream) {
+thread_local KernelTimer* t_timer = nullptr;
+
+template <typename T> const char* tname();
+template <> const char* tname<float>() { return "f32"; }
+template <> const char* tname<bf16>() { return "bf16"; }
+template <template <typename, int, int, int, bool> class PolT> const char* pname();
+template <> const char* pname<FwdPolicy>() { return "conv_fwd"; }
+template <> const char* pname<DgradPolicy>() { return "conv_dgrad"; }
+template <> const char* pname<WgradPolicy>() { return "conv_wgrad"; }
+
+// Algorithmic cost of a conv: 2*N*P*Q*K*R*S*C0 flops; bytes = input + weights + output.
+struct Cost {
+  double flops, bytes;
+};
+
+Cost conv_cost(const ConvGeom& g, int C0, size_t es, bool fp32_out) {
+  const double m = (double)g.N * g.P * g.Q;
+  Cost c;
+  c.flops = 2.0 * m * g.K * g.R * g.S * C0;
+  const double x = (double)g.N * g.H * g.W * g.C, w = (double)g.K * g.R * g.S * g.C,
+               y = m * g.K;
+  c.bytes = (x + y) * es + w * (fp32_out ? 4.0 : (double)es);
+  return c;
+}
+
+template <typename T, template <typename, int, int, int, bool> class PolT, int BM, int BN, int KU,
+          bool UT>
+hipError_t launch_gemm(const typename PolT<T, BM, BN, KU, UT>::Args& args, int rows, int cols,
+                       int splits, hipStream_t stream, Cost cost) {
   dim3 grid(cdiv(cols, BN), cdiv(rows, BM), splits);
-  hipLaunchKernelGGL((gemm_kernel<T, BM, BN, PolT<T, BM, BN>>), grid, dim3(NT), 0, stream, args);
-  return hipGetLastError();
+  KernelTimer* t = t_timer;
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  if (t) {
+    e0 = t->take();
+    e1 = t->take();
+    EKYA_HIP(hipEventRecord(e0, stream));
+  }
+  hipLaunchKernelGGL((gemm_kernel<T, BM, BN, PolT<T, BM, BN, KU, UT>>), grid, dim3(NT), 0, stream,
+                     args);
+  hipError_t e = hipGetLastError();
+  if (t && e == hipSuccess) {
+    EKYA_HIP(hipEventRecord(e1, stream));
+    t->recs.push_back({std::string(pname<PolT>()) + "<" + tname<T>() + "," + std::to_string(BM) +
+                           "," + std::to_string(BN) + (UT ? "" : ",gather") + ">",
+                       cost.flops, cost.bytes, e0, e1});
+  }
+  return e;
 }
 
-// Choose the tile for a rows x cols output: 128 rows when there are >= 128
-// rows; 128 columns only when that still leaves enough blocks for the chip.
-inline void pick_tile(int rows, int cols, int& bm, int& bn) {
-  bm = rows >= 128 ? 128 : 64;
-  long long blocks128 = (long long)cdiv(cols, 128) * cdiv(rows, bm);
-  bn = blocks128 >= 512 ? 128 : 64;
+// Tile and split for a rows x cols output with `ns` reduction stages: the
+// largest tile that yields enough blocks for the chip, else split the
+// reduction (keeping >= 4 stages per split).
+struct Plan {
+  int bm, bn, splits, sps;
+};
+constexpr long long kTargetBlocks = 512;
+
+Plan plan_tiles(int rows, int cols, int ns, bool allow_split) {
+  Plan p{64, 64, 1, ns};
+  const int cand[4][2] = {{128, 128}, {128, 64}, {64, 128}, {64, 64}};
+  for (auto& c : cand) {
+    if (c[0] == 128 && rows < 128) continue;
+    const long long blocks = (long long)cdiv(cols, c[1]) * cdiv(rows, c[0]);
+    if (blocks >= kTargetBlocks) {
+      p.bm = c[0];
+      p.bn = c[1];
+      return p;
+    }
+  }
+  // too few tiles: 128-row tiles when possible, split the reduction
+  p.bm = rows >= 128 ? 128 : 64;
+  p.bn = 64;
+  const long long blocks = (long long)cdiv(cols, p.bn) * cdiv(rows, p.bm);
+  if (allow_split) {
+    int s = (int)std::min<long long>(cdivl(kTargetBlocks, blocks), std::max(1, ns / 4));
+    s = std::max(1, std::min(s, 16));
+    p.sps = cdiv(ns, s);
+    p.splits = cdiv(ns, p.sps);
+  }
+  return p;
 }
 
-template <typename T, template <typename, int, int> class PolT>
-hipError_t dispatch_tile(const typename PolT<T, 64, 64>::Args& args, int rows, int cols,
-                         hipStream_t stream) {
-  int bm, bn;
-  pick_tile(rows, cols, bm, bn);
-#define EKYA_TILE(BM_, BN_) \
-  if (bm == BM_ && bn == BN_) return launch_gemm<T, PolT, BM_, BN_>(args, rows, cols, 1, stream);
+template <typename T, template <typename, int, int, int, bool> class PolT, int KU, bool UT>
+hipError_t dispatch_tile(const typename PolT<T, 64, 64, KU, UT>::Args& args, const Plan& p,
+                         int rows, int cols, hipStream_t stream, Cost cost) {
+#define EKYA_TILE(BM_, BN_)                                                                    \
+  if (p.bm == BM_ && p.bn == BN_)                                                              \
+    return launch_gemm<T, PolT, BM_, BN_, KU, UT>(args, rows, cols, p.splits, stream, cost);
   EKYA_TILE(64, 64)
   EKYA_TILE(64, 128)
   EKYA_TILE(128, 64)
@@ -497,23 +664,99 @@ hipError_t dispatch_tile(const typename PolT<T, 64, 64>::Args& args, int rows, i
 }
 
 template <typename T>
+hipError_t split_finish(const float* part, int splits, long long npix, int C, const ConvEpilogue& e,
+                        void* y, hipStream_t stream) {
+  const long long n4 = npix * C / 4;
+  const int blocks = (int)std::min<long long>(cdivl(n4, 256), 8192);
+  hipLaunchKernelGGL(split_reduce_kernel<T>, dim3(blocks), dim3(256), 0, stream, part, splits,
+                     npix, C, e, (T*)y);
+  return hipGetLastError();
+}
+
+constexpr int KU_MAIN = 8;
+
+template <typename T>
 hipError_t conv_fwd_t(const ConvGeom& g, const void* x, const void* w, void* y,
-                      const ConvEpilogue& epi, hipStream_t stream) {
-  // All tile variants share one Args layout.
-  FwdArgs<T> a{g, (const T*)x, (const T*)w, (T*)y, epi};
-  return dispatch_tile<T, FwdPolicy>(a, g.K, g.N * g.P * g.Q, stream);
+                      const ConvEpilogue& epi, float* ws, size_t ws_floats, hipStream_t stream) {
+  constexpr int E = Elt<T>::E;
+  const bool ut = g.C % (KU_MAIN * E) == 0;
+  const int ns = cdiv(g.R * g.S * g.C, KU_MAIN * E);
+  const long long npix = (long long)g.N * g.P * g.Q;
+  Plan p = plan_tiles(g.K, (int)npix, ns, ut && ws != nullptr);
+  if (p.splits > 1 && (size_t)p.splits * npix * g.K > ws_floats) {
+    p.splits = 1;
+    p.sps = ns;
+  }
+  FwdArgs<T> a{g, (const T*)x, (const T*)w, (T*)y, epi, SplitOut{ws, p.splits, p.sps}};
+  const Cost cost = conv_cost(g, g.C0 ? g.C0 : g.C, sizeof(T), false);
+  hipError_t e;
+  if (ut) {
+    e = dispatch_tile<T, FwdPolicy, KU_MAIN, true>(a, p, g.K, (int)npix, stream, cost);
+  } else {
+    // image stem: C is one 16-byte unit; reduction elements decoded unit by unit
+    const int ns4 = cdiv(g.R * g.S * g.C, 4 * E);
+    a.so = SplitOut{nullptr, 1, ns4};
+    if (npix / 128 >= kTargetBlocks)
+      e = launch_gemm<T, FwdPolicy, 64, 128, 4, false>(a, g.K, (int)npix, 1, stream, cost);
+    else
+      e = launch_gemm<T, FwdPolicy, 64, 64, 4, false>(a, g.K, (int)npix, 1, stream, cost);
+  }
+  if (e != hipSuccess || p.splits <= 1 || !ut) return e;
+  return split_finish<T>(ws, p.splits, npix, g.K, epi, y, stream);
 }
 
 template <typename T>
 hipError_t conv_dgrad_t(const ConvGeom& g, const void* dy, const void* wt, void* dx,
-                        const void* res, hipStream_t stream) {
-  DgradArgs<T> a{g, (const T*)dy, (const T*)wt, (T*)dx, (const T*)res};
-  return dispatch_tile<T, DgradPolicy>(a, g.C, g.N * g.H * g.W, stream);
+                        const void* res, float* ws, size_t ws_floats, hipStream_t stream) {
+  constexpr int E = Elt<T>::E;
+  if (g.K % (KU_MAIN * E) != 0 || (g.stride != 1 && g.stride != 2)) return hipErrorInvalidValue;
+  const int ns = cdiv(g.R * g.S * g.K, KU_MAIN * E);
+  const long long npix = (long long)g.N * g.H * g.W;
+  Plan p = plan_tiles(g.C, (int)npix, ns, ws != nullptr);
+  if (p.splits > 1 && (size_t)p.splits * npix * g.C > ws_floats) {
+    p.splits = 1;
+    p.sps = ns;
+  }
+  DgradArgs<T> a{g, (const T*)dy, (const T*)wt, (T*)dx, (const T*)res, SplitOut{ws, p.splits, p.sps}};
+  hipError_t e = dispatch_tile<T, DgradPolicy, KU_MAIN, true>(a, p, g.C, (int)npix, stream,
+                                                              conv_cost(g, g.C, sizeof(T), false));
+  if (e != hipSuccess || p.splits <= 1) return e;
+  ConvEpilogue ep;
+  ep.res = res;
+  return split_finish<T>(ws, p.splits, npix, g.C, ep, dx, stream);
 }
 
 int wgrad_stage_m(int dt) { return dt == DT_F32 ? 16 : 64; }
 
 }  // namespace
+
+hipEvent_t KernelTimer::take() {
+  if (!pool.empty()) {
+    hipEvent_t e = pool.back();
+    pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  (void)hipEventCreate(&e);
+  return e;
+}
+void set_thread_timer(KernelTimer* t) { t_timer = t; }
+KernelTimer* thread_timer() { return t_timer; }
+
+size_t conv_split_workspace_floats(int dt, const ConvGeom& g, bool dgrad) {
+  const int E = dtype_vec(dt);
+  if (dgrad) {
+    const int ns = cdiv(g.R * g.S * g.K, KU_MAIN * E);
+    const long long npix = (long long)g.N * g.H * g.W;
+    const Plan p = plan_tiles(g.C, (int)npix, ns, true);
+    return p.splits > 1 ? (size_t)p.splits * npix * g.C : 0;
+  }
+  if (g.C % (KU_MAIN * E) != 0) return 0;
+  const int ns = cdiv(g.R * g.S * g.C, KU_MAIN * E);
+  const long long npix = (long long)g.N * g.P * g.Q;
+  const Plan p = plan_tiles(g.K, (int)npix, ns, true);
+  return p.splits > 1 ? (size_t)p.splits * npix * g.K : 0;
+}
 
 int conv_wgrad_splits(int dt, const ConvGeom& g) {
   const long long M = (long long)g.N * g.P * g.Q;
@@ -533,17 +776,17 @@ size_t conv_wgrad_workspace_floats(int dt, const ConvGeom& g) {
 }
 
 hipError_t conv_fwd(int dt, const ConvGeom& g, const void* x, const void* w, void* y,
-                    const ConvEpilogue& epi, hipStream_t stream) {
+                    const ConvEpilogue& epi, float* ws, size_t ws_floats, hipStream_t stream) {
   if (g.N * g.P * g.Q == 0) return hipSuccess;
-  return dt == DT_F32 ? conv_fwd_t<float>(g, x, w, y, epi, stream)
-                      : conv_fwd_t<bf16>(g, x, w, y, epi, stream);
+  return dt == DT_F32 ? conv_fwd_t<float>(g, x, w, y, epi, ws, ws_floats, stream)
+                      : conv_fwd_t<bf16>(g, x, w, y, epi, ws, ws_floats, stream);
 }
 
 hipError_t conv_dgrad(int dt, const ConvGeom& g, const void* dy, const void* wt, void* dx,
-                      const void* res, hipStream_t stream) {
+                      const void* res, float* ws, size_t ws_floats, hipStream_t stream) {
   if (g.N * g.H * g.W == 0) return hipSuccess;
-  return dt == DT_F32 ? conv_dgrad_t<float>(g, dy, wt, dx, res, stream)
-                      : conv_dgrad_t<bf16>(g, dy, wt, dx, res, stream);
+  return dt == DT_F32 ? conv_dgrad_t<float>(g, dy, wt, dx, res, ws, ws_floats, stream)
+                      : conv_dgrad_t<bf16>(g, dy, wt, dx, res, ws, ws_floats, stream);
 }
 
 hipError_t conv_wgrad(int dt, const ConvGeom& g, const void* x, const void* dy, float* partials,
@@ -554,29 +797,22 @@ hipError_t conv_wgrad(int dt, const ConvGeom& g, const void* x, const void* dy, 
   const int mps = (int)(cdivl(cdivl(M, splits), stage) * stage);
   const int rows = g.R * g.S * g.C;
   const int bn = g.K >= 128 ? 128 : 64;
+  const Cost cost = conv_cost(g, C0, dtype_size(dt), true);
   hipError_t e;
   if (dt == DT_F32) {
-    if (bn == 128) {
-      WgradArgs<float> a{g, (const float*)x, (const float*)dy, partials, mps};
-      e = launch_gemm<float, WgradPolicy, 128, 128>(a, rows, g.K, splits, stream);
-    } else {
-      WgradArgs<float> a{g, (const float*)x, (const float*)dy, partials, mps};
-      e = launch_gemm<float, WgradPolicy, 128, 64>(a, rows, g.K, splits, stream);
-    }
+    WgradArgs<float> a{g, (const float*)x, (const float*)dy, partials, mps};
+    e = bn == 128 ? launch_gemm<float, WgradPolicy, 128, 128, 4, true>(a, rows, g.K, splits, stream, cost)
+                  : launch_gemm<float, WgradPolicy, 128, 64, 4, true>(a, rows, g.K, splits, stream, cost);
   } else {
-    if (bn == 128) {
-      WgradArgs<bf16> a{g, (const bf16*)x, (const bf16*)dy, partials, mps};
-      e = launch_gemm<bf16, WgradPolicy, 128, 128>(a, rows, g.K, splits, stream);
-    } else {
-      WgradArgs<bf16> a{g, (const bf16*)x, (const bf16*)dy, partials, mps};
-      e = launch_gemm<bf16, WgradPolicy, 128, 64>(a, rows, g.K, splits, stream);
-    }
+    WgradArgs<bf16> a{g, (const bf16*)x, (const bf16*)dy, partials, mps};
+    e = bn == 128 ? launch_gemm<bf16, WgradPolicy, 128, 128, 8, true>(a, rows, g.K, splits, stream, cost)
+                  : launch_gemm<bf16, WgradPolicy, 128, 64, 8, true>(a, rows, g.K, splits, stream, cost);
   }
   if (e != hipSuccess) return e;
-  long long n = (long long)g.K * g.R * g.S * C0;
-  int blocks = (int)std::min<long long>(cdivl(n, 256), 4096);
-  hipLaunchKernelGGL(wgrad_reduce_kernel<float>, dim3(blocks), dim3(256), 0, stream, partials,
-                     splits, g.K, g.R * g.S, g.C, C0, dw);
+  const long long n = (long long)g.K * g.R * g.S * C0;
+  const int blocks = (int)std::min<long long>(cdivl(n, 256), 4096);
+  hipLaunchKernelGGL(wgrad_reduce_kernel, dim3(blocks), dim3(256), 0, stream, partials, splits, g.K,
+                     g.R * g.S, g.C, C0, dw);
   return hipGetLastError();
 }
 

@@ -2,9 +2,28 @@
 // pointers; every call is asynchronous on `stream` and returns the launch status.
 #pragma once
 
+#include <string>
+#include <vector>
+
 #include "common.hpp"
 
 namespace ekya {
+
+// Opt-in timing of the GEMM launches: when a thread has a timer installed,
+// every conv GEMM launch is bracketed by two events on its stream and logged
+// with its algorithmic flops and bytes (read once the stream has finished).
+struct LaunchRecord {
+  std::string name;
+  double flops, bytes;
+  hipEvent_t e0, e1;
+};
+struct KernelTimer {
+  std::vector<LaunchRecord> recs;
+  std::vector<hipEvent_t> pool;
+  hipEvent_t take();
+};
+void set_thread_timer(KernelTimer* t);
+KernelTimer* thread_timer();
 
 enum DType { DT_F32 = 0, DT_BF16 = 1 };
 inline size_t dtype_size(int dt) { return dt == DT_F32 ? 4 : 2; }
@@ -16,6 +35,7 @@ struct ConvGeom {
   int K, R, S;        // output channels, kernel rows/cols
   int stride, pad;
   int P, Q;           // output spatial size
+  int C0 = 0;         // real input channels (0: same as C); only used for cost accounting
 };
 
 // Epilogue of the forward conv: y = acc * scale[k] + shift[k] (+ res) (ReLU),
@@ -27,12 +47,16 @@ struct ConvEpilogue {
   int relu = 0;
 };
 
-// y[N,P,Q,K] = conv(x[N,H,W,C], w[K,R,S,C]) with the epilogue.
+// y[N,P,Q,K] = conv(x[N,H,W,C], w[K,R,S,C]) with the epilogue.  `ws` (fp32,
+// ws_floats) holds split-reduction partials when the output has too few tiles
+// (conv_split_workspace_floats tells how much; null or too small: no split).
 hipError_t conv_fwd(int dt, const ConvGeom& g, const void* x, const void* w_krsc, void* y,
-                    const ConvEpilogue& epi, hipStream_t stream);
+                    const ConvEpilogue& epi, float* ws, size_t ws_floats, hipStream_t stream);
 // dx[N,H,W,C] = conv-transpose of dy[N,P,Q,K] with wT[C,R,S,K] (+ res[N,H,W,C]).
+// Needs K a multiple of 64 (bf16) / 32 (fp32) and stride 1 or 2.
 hipError_t conv_dgrad(int dt, const ConvGeom& g, const void* dy, const void* w_crsk, void* dx,
-                      const void* res, hipStream_t stream);
+                      const void* res, float* ws, size_t ws_floats, hipStream_t stream);
+size_t conv_split_workspace_floats(int dt, const ConvGeom& g, bool dgrad);
 // Split count and partial-buffer size (floats) the weight gradient will use.
 int conv_wgrad_splits(int dt, const ConvGeom& g);
 size_t conv_wgrad_workspace_floats(int dt, const ConvGeom& g);

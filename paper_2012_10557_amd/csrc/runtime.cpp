@@ -87,9 +87,29 @@ hipError_t ctx_init(Ctx& c, int device, int n_classes) {
   return hipSuccess;
 }
 
+hipError_t ctx_collect_timing(Ctx& c) {
+  for (LaunchRecord& r : c.timer.recs) {
+    EKYA_HIP(hipEventSynchronize(r.e1));
+    float ms = 0.f;
+    EKYA_HIP(hipEventElapsedTime(&ms, r.e0, r.e1));
+    KernelStat& st = c.stats[r.name];
+    st.launches += 1;
+    st.ms += ms;
+    st.flops += r.flops;
+    st.bytes += r.bytes;
+    c.timer.pool.push_back(r.e0);
+    c.timer.pool.push_back(r.e1);
+  }
+  c.timer.recs.clear();
+  return hipSuccess;
+}
+
 void ctx_free(Ctx& c) {
   (void)hipSetDevice(c.device);
   (void)hipDeviceSynchronize();
+  (void)ctx_collect_timing(c);
+  for (hipEvent_t e : c.timer.pool) (void)hipEventDestroy(e);
+  c.timer.pool.clear();
   for (hipStream_t s : c.streams) (void)hipStreamDestroy(s);
   c.streams.clear();
   if (c.infer_done) (void)hipEventDestroy(c.infer_done);
@@ -106,7 +126,11 @@ struct EvalBufs {
   void *p0 = nullptr, *p1 = nullptr, *t1 = nullptr, *sc = nullptr;
   float* pooled = nullptr;
   float* logits = nullptr;
+  float* ws = nullptr;  // split-reduction partials of the forward convs
+  size_t ws_floats = 0;
 };
+
+static ConvGeom conv_geom(const Net& net, const Geo& g, int ci, int n);
 
 static long long max_act_elems(const Net& net, const Geo& g, int lo, int hi) {
   long long m = 0;
@@ -129,6 +153,13 @@ static void plan_eval(Arena& a, const Net& net, const Geo& g, int lo, int hi, in
   b.sc = a.take_bytes(m * es);
   b.pooled = a.take<float>((size_t)cap * 512);
   b.logits = a.take<float>((size_t)cap * net.n_classes);
+  size_t ws = 16;
+  for (size_t i = 0; i < net.conv.size(); ++i)
+    if (net.conv[i].stage >= lo && net.conv[i].stage <= hi)
+      for (int n : {cap, 1})
+        ws = std::max(ws, conv_split_workspace_floats(net.dt, conv_geom(net, g, (int)i, n), false));
+  b.ws_floats = ws;
+  b.ws = a.take<float>(ws);
 }
 
 static ConvGeom conv_geom(const Net& net, const Geo& g, int ci, int n) {
@@ -145,6 +176,7 @@ static ConvGeom conv_geom(const Net& net, const Geo& g, int ci, int n) {
   cg.pad = c.pad;
   cg.P = g.oh[ci];
   cg.Q = g.ow[ci];
+  cg.C0 = c.cin;
   return cg;
 }
 
@@ -169,7 +201,7 @@ static hipError_t eval_forward(const Net& net, const Geo& g, const void* shadow,
       e.shift = fold_shift(net.conv[0].bn);
       e.relu = 1;
       EKYA_HIP(conv_fwd(dt, conv_geom(net, g, 0, n), cur, shadow_at(net, shadow, net.conv[0].sh_krsc),
-                        b.t1, e, st));
+                        b.t1, e, b.ws, b.ws_floats, st));
       void* dst = (hi == 0) ? out : b.p0;
       EKYA_HIP(maxpool_fwd(dt, b.t1, n, g.sh, g.sw, 64, dst, nullptr, st));
       cur = dst;
@@ -186,14 +218,16 @@ static hipError_t eval_forward(const Net& net, const Geo& g, const void* shadow,
         e1.shift = fold_shift(net.conv[bl.c1].bn);
         e1.relu = 1;
         EKYA_HIP(conv_fwd(dt, conv_geom(net, g, bl.c1, n), cur,
-                          shadow_at(net, shadow, net.conv[bl.c1].sh_krsc), b.t1, e1, st));
+                          shadow_at(net, shadow, net.conv[bl.c1].sh_krsc), b.t1, e1, b.ws,
+                          b.ws_floats, st));
         const void* res = cur;
         if (bl.cd >= 0) {
           ConvEpilogue ed;
           ed.scale = fold_scale(net.conv[bl.cd].bn);
           ed.shift = fold_shift(net.conv[bl.cd].bn);
           EKYA_HIP(conv_fwd(dt, conv_geom(net, g, bl.cd, n), cur,
-                            shadow_at(net, shadow, net.conv[bl.cd].sh_krsc), b.sc, ed, st));
+                            shadow_at(net, shadow, net.conv[bl.cd].sh_krsc), b.sc, ed, b.ws,
+                            b.ws_floats, st));
           res = b.sc;
         }
         ConvEpilogue e2;
@@ -202,7 +236,8 @@ static hipError_t eval_forward(const Net& net, const Geo& g, const void* shadow,
         e2.res = res;
         e2.relu = 1;
         EKYA_HIP(conv_fwd(dt, conv_geom(net, g, bl.c2, n), b.t1,
-                          shadow_at(net, shadow, net.conv[bl.c2].sh_krsc), dst, e2, st));
+                          shadow_at(net, shadow, net.conv[bl.c2].sh_krsc), dst, e2, b.ws,
+                          b.ws_floats, st));
         cur = dst;
       }
       if (s == 4) {
@@ -256,6 +291,7 @@ struct TrainJob {
   void* g[6] = {nullptr};      // gradient scratch
   float *pooled = nullptr, *logits = nullptr, *dz = nullptr, *dpooled = nullptr;
   float* ws = nullptr;         // split-K / BatchNorm partials
+  size_t ws_floats = 0;
   float* ce_out = nullptr;     // n_steps x 3
   int32_t* hcount = nullptr;   // epochs
   EvalBufs eval;
@@ -273,6 +309,8 @@ static size_t ws_floats(const TrainJob& j) {
     ConvGeom cg = conv_geom(net, j.geo, (int)i, j.B);
     m = std::max(m, conv_wgrad_workspace_floats(j.dt, cg));
     m = std::max(m, bn_partials_floats((long long)j.B * cg.P * cg.Q, c.cout));
+    m = std::max(m, conv_split_workspace_floats(j.dt, cg, false));
+    if (c.stage > 0) m = std::max(m, conv_split_workspace_floats(j.dt, cg, true));
   }
   return std::max<size_t>(m, 16);
 }
@@ -329,7 +367,8 @@ static void plan_job(Arena& a, TrainJob& j) {
   j.dpooled = a.take<float>((size_t)j.B * 512);
   j.logits = a.take<float>((size_t)j.B * net.n_classes);
   j.dz = a.take<float>((size_t)j.B * net.n_classes);
-  j.ws = a.take<float>(ws_floats(j));
+  j.ws_floats = ws_floats(j);
+  j.ws = a.take<float>(j.ws_floats);
   j.ce_out = a.take<float>((size_t)j.n_steps * 3);
   j.hcount = a.take<int32_t>(j.epochs);
   j.eval_cap = std::max(1, std::min(j.n_h, 256));
@@ -358,7 +397,7 @@ static hipError_t train_forward(TrainJob& j, int nb) {
     if (s == 0) {
       ConvGeom cg = conv_geom(net, j.geo, 0, nb);
       EKYA_HIP(conv_fwd(dt, cg, cur, shadow_at(net, j.shadow, net.conv[0].sh_krsc), j.stem_Z,
-                        ConvEpilogue(), st));
+                        ConvEpilogue(), j.ws, j.ws_floats, st));
       const long long M = (long long)nb * cg.P * cg.Q;
       EKYA_HIP(bn_train(net.conv[0].bn, j.stem_Z, M));
       EKYA_HIP(bn_apply(dt, j.stem_Z, M, 64, mu(net.conv[0].bn), sc(net.conv[0].bn), be(net.conv[0].bn), nullptr, 1,
@@ -377,17 +416,19 @@ static hipError_t train_forward(TrainJob& j, int nb) {
       const long long M = (long long)nb * g1.P * g1.Q;
       const int C = net.conv[b.c1].cout;
       EKYA_HIP(conv_fwd(dt, g1, t.X, shadow_at(net, j.shadow, net.conv[b.c1].sh_krsc), t.Z1,
-                        ConvEpilogue(), st));
+                        ConvEpilogue(), j.ws, j.ws_floats, st));
       EKYA_HIP(bn_train(net.conv[b.c1].bn, t.Z1, M));
       EKYA_HIP(bn_apply(dt, t.Z1, M, C, mu(net.conv[b.c1].bn), sc(net.conv[b.c1].bn), be(net.conv[b.c1].bn), nullptr, 1,
                         t.A1, st));
       EKYA_HIP(conv_fwd(dt, conv_geom(net, j.geo, b.c2, nb), t.A1,
-                        shadow_at(net, j.shadow, net.conv[b.c2].sh_krsc), t.Z2, ConvEpilogue(), st));
+                        shadow_at(net, j.shadow, net.conv[b.c2].sh_krsc), t.Z2, ConvEpilogue(), j.ws,
+                        j.ws_floats, st));
       EKYA_HIP(bn_train(net.conv[b.c2].bn, t.Z2, M));
       const void* res = t.X;
       if (b.cd >= 0) {
         EKYA_HIP(conv_fwd(dt, conv_geom(net, j.geo, b.cd, nb), t.X,
-                          shadow_at(net, j.shadow, net.conv[b.cd].sh_krsc), t.Zd, ConvEpilogue(), st));
+                          shadow_at(net, j.shadow, net.conv[b.cd].sh_krsc), t.Zd, ConvEpilogue(),
+                          j.ws, j.ws_floats, st));
         EKYA_HIP(bn_train(net.conv[b.cd].bn, t.Zd, M));
         EKYA_HIP(bn_apply(dt, t.Zd, M, C, mu(net.conv[b.cd].bn), sc(net.conv[b.cd].bn), be(net.conv[b.cd].bn), nullptr, 0,
                           j.g[0], st));
@@ -434,7 +475,7 @@ static hipError_t train_backward(TrainJob& j, int nb) {
   };
   auto dgrad = [&](int ci, const void* dy, void* dx, const void* res, int n) {
     return conv_dgrad(dt, conv_geom(net, j.geo, ci, n), dy,
-                      shadow_at(net, j.shadow, net.conv[ci].sh_crsk), dx, res, st);
+                      shadow_at(net, j.shadow, net.conv[ci].sh_crsk), dx, res, j.ws, j.ws_floats, st);
   };
   for (int s = 4; s >= j.lowest; --s) {
     if (s == 0) {
@@ -635,11 +676,17 @@ static void destroy_events(TrainJob& j) {
   } while (0)
 
 // --------------------------------------------------------------- retrain
+struct TimerGuard {
+  explicit TimerGuard(Ctx& c) { set_thread_timer(c.timing ? &c.timer : nullptr); }
+  ~TimerGuard() { set_thread_timer(nullptr); }
+};
+
 ekya_status run_retrain(Ctx& c, float* weights, int k, const void* frames, const int32_t* labels,
                         int n_frames, int H, int W, const void* hframes, const int32_t* hlabels,
                         int n_heldout, const ekya_train_opts& o, ekya_retrain_result* res,
                         hipStream_t stream) {
   EKYA_CHECK_HIP(hipSetDevice(c.device));
+  TimerGuard tg(c);
   const int dt = o.precision;
   TrainJob j;
   j.net = &c.net[dt];
@@ -924,6 +971,7 @@ ekya_status run_profile(Ctx& c, const float* weights, const ekya_profile_cfg* cf
 ekya_status run_infer(Ctx& c, const float* weights, const void* frames, int n, int H, int W,
                       int resolution, int precision, int32_t* labels_out, hipStream_t stream) {
   EKYA_CHECK_HIP(hipSetDevice(c.device));
+  TimerGuard tg(c);
   const int dt = precision;
   const Net& net = c.net[dt];
   const Geo geo = Geo::build(net, resolution, resolution);

@@ -2,6 +2,7 @@
 // retraining / profiling / inference jobs.
 #pragma once
 
+#include <map>
 #include <string>
 #include <vector>
 
@@ -49,6 +50,11 @@ struct Tables {
   int n_pack_train[6] = {0};
 };
 
+struct KernelStat {
+  long long launches = 0;
+  double ms = 0.0, flops = 0.0, bytes = 0.0;
+};
+
 struct Ctx {
   int device = 0;
   int n_classes = 0;
@@ -58,7 +64,13 @@ struct Ctx {
   DeviceBuf retrain_ws, infer_ws, profile_ws;
   hipEvent_t infer_done = nullptr;
   std::vector<hipStream_t> streams;  // profiler streams (default priority)
+  bool timing = false;
+  KernelTimer timer;
+  std::map<std::string, KernelStat> stats;
 };
+
+// Read the events of finished timed launches into `stats`.
+hipError_t ctx_collect_timing(Ctx& c);
 
 hipError_t ctx_init(Ctx& c, int device, int n_classes);
 void ctx_free(Ctx& c);
