@@ -758,21 +758,28 @@ size_t conv_split_workspace_floats(int dt, const ConvGeom& g, bool dgrad) {
   return p.splits > 1 ? (size_t)p.splits * npix * g.K : 0;
 }
 
-int conv_wgrad_splits(int dt, const ConvGeom& g) {
+namespace {
+struct WPlan {
+  int bm, bn, splits;
+};
+WPlan plan_wgrad(int dt, const ConvGeom& g) {
+  // 128-row tiles, split the pixel reduction until there are ~1024 blocks
+  // (>= 4 stages per split): measured faster than fewer, longer blocks.
   const long long M = (long long)g.N * g.P * g.Q;
   const int rows = g.R * g.S * g.C;
   const int bn = g.K >= 128 ? 128 : 64;
   const long long tiles = (long long)cdiv(rows, 128) * cdiv(g.K, bn);
-  const long long by_work = cdivl(M, 4LL * wgrad_stage_m(dt));  // >= 4 stages per split
-  long long s = cdivl(1024, tiles);
-  if (s > by_work) s = by_work;
-  if (s < 1) s = 1;
-  if (s > 1024) s = 1024;
-  return (int)s;
+  const long long by_work = std::max(1LL, cdivl(M, 4LL * wgrad_stage_m(dt)));
+  const long long s = std::max(1LL, std::min<long long>(std::min(cdivl(1024, tiles), by_work), 1024));
+  return {128, bn, (int)s};
 }
+}  // namespace
+
+int conv_wgrad_splits(int dt, const ConvGeom& g) { return plan_wgrad(dt, g).splits; }
 
 size_t conv_wgrad_workspace_floats(int dt, const ConvGeom& g) {
-  return (size_t)conv_wgrad_splits(dt, g) * g.K * g.R * g.S * g.C;
+  const WPlan p = plan_wgrad(dt, g);
+  return (size_t)p.splits * g.K * g.R * g.S * g.C;
 }
 
 hipError_t conv_fwd(int dt, const ConvGeom& g, const void* x, const void* w, void* y,
@@ -791,28 +798,32 @@ hipError_t conv_dgrad(int dt, const ConvGeom& g, const void* dy, const void* wt,
 
 hipError_t conv_wgrad(int dt, const ConvGeom& g, const void* x, const void* dy, float* partials,
                       float* dw, int C0, hipStream_t stream) {
-  const int splits = conv_wgrad_splits(dt, g);
+  const WPlan p = plan_wgrad(dt, g);
   const long long M = (long long)g.N * g.P * g.Q;
   const int stage = wgrad_stage_m(dt);
-  const int mps = (int)(cdivl(cdivl(M, splits), stage) * stage);
+  const int mps = (int)(cdivl(cdivl(M, p.splits), stage) * stage);
   const int rows = g.R * g.S * g.C;
-  const int bn = g.K >= 128 ? 128 : 64;
   const Cost cost = conv_cost(g, C0, dtype_size(dt), true);
+  // one split over unpadded channels: the tile writes dw directly
+  const bool direct = p.splits == 1 && C0 == g.C;
+  float* out = direct ? dw : partials;
   hipError_t e;
-  if (dt == DT_F32) {
-    WgradArgs<float> a{g, (const float*)x, (const float*)dy, partials, mps};
-    e = bn == 128 ? launch_gemm<float, WgradPolicy, 128, 128, 4, true>(a, rows, g.K, splits, stream, cost)
-                  : launch_gemm<float, WgradPolicy, 128, 64, 4, true>(a, rows, g.K, splits, stream, cost);
-  } else {
-    WgradArgs<bf16> a{g, (const bf16*)x, (const bf16*)dy, partials, mps};
-    e = bn == 128 ? launch_gemm<bf16, WgradPolicy, 128, 128, 8, true>(a, rows, g.K, splits, stream, cost)
-                  : launch_gemm<bf16, WgradPolicy, 128, 64, 8, true>(a, rows, g.K, splits, stream, cost);
+#define EKYA_WG(T_, KU_, BM_, BN_)                                                              \
+  if (p.bm == BM_ && p.bn == BN_) {                                                            \
+    WgradArgs<T_> a{g, (const T_*)x, (const T_*)dy, out, mps};                                 \
+    e = launch_gemm<T_, WgradPolicy, BM_, BN_, KU_, true>(a, rows, g.K, p.splits, stream, cost); \
   }
-  if (e != hipSuccess) return e;
+  if (dt == DT_F32) {
+    EKYA_WG(float, 4, 128, 128) else EKYA_WG(float, 4, 128, 64) else EKYA_WG(float, 4, 64, 64) else return hipErrorInvalidValue;
+  } else {
+    EKYA_WG(bf16, 8, 128, 128) else EKYA_WG(bf16, 8, 128, 64) else EKYA_WG(bf16, 8, 64, 64) else return hipErrorInvalidValue;
+  }
+#undef EKYA_WG
+  if (e != hipSuccess || direct) return e;
   const long long n = (long long)g.K * g.R * g.S * C0;
   const int blocks = (int)std::min<long long>(cdivl(n, 256), 4096);
-  hipLaunchKernelGGL(wgrad_reduce_kernel, dim3(blocks), dim3(256), 0, stream, partials, splits, g.K,
-                     g.R * g.S, g.C, C0, dw);
+  hipLaunchKernelGGL(wgrad_reduce_kernel, dim3(blocks), dim3(256), 0, stream, partials, p.splits,
+                     g.K, g.R * g.S, g.C, C0, dw);
   return hipGetLastError();
 }
 

@@ -90,17 +90,38 @@ __global__ __launch_bounds__(256) void bn_stats_partial(const T* z, long long M,
   }
 }
 
+// Fixed-order sum over chunks of the two partial rows of channel c: a block
+// handles 64 channels with 4 threads each (thread slice k sums chunks
+// k, k+4, ...), and the four slice sums are added in slice order.
+__device__ __forceinline__ bool chunk_sums(const float* part, int nchunks, int C, double& a,
+                                           double& b) {
+  __shared__ float sa[4][64], sb[4][64];
+  const int lc = threadIdx.x & 63, slice = threadIdx.x >> 6;
+  const int c = blockIdx.x * 64 + lc;
+  float x = 0.f, y = 0.f;
+  if (c < C)
+    for (int k = slice; k < nchunks; k += 4) {
+      x += part[(long long)k * 2 * C + c];
+      y += part[(long long)k * 2 * C + C + c];
+    }
+  sa[slice][lc] = x;
+  sb[slice][lc] = y;
+  __syncthreads();
+  if (slice != 0 || c >= C) return false;
+  a = (double)sa[0][lc] + (double)sa[1][lc] + (double)sa[2][lc] + (double)sa[3][lc];
+  b = (double)sb[0][lc] + (double)sb[1][lc] + (double)sb[2][lc] + (double)sb[3][lc];
+  return true;
+}
+
 template <typename T>
-__global__ void bn_stats_final(const T* z, const float* part, int nchunks, long long M, int C,
-                               const float* gamma, const float* beta, float* rm, float* rv,
-                               float* mean, float* invstd, float* scale, float* shift) {
-  int c = blockIdx.x * blockDim.x + threadIdx.x;
-  if (c >= C) return;
-  double a = 0.0, b = 0.0;
-  for (int k = 0; k < nchunks; ++k) {
-    a += part[(long long)k * 2 * C + c];
-    b += part[(long long)k * 2 * C + C + c];
-  }
+__global__ __launch_bounds__(256) void bn_stats_final(const T* z, const float* part, int nchunks,
+                                                      long long M, int C, const float* gamma,
+                                                      const float* beta, float* rm, float* rv,
+                                                      float* mean, float* invstd, float* scale,
+                                                      float* shift) {
+  double a, b;
+  if (!chunk_sums(part, nchunks, C, a, b)) return;
+  const int c = blockIdx.x * 64 + (threadIdx.x & 63);
   const double Kc = (double)to_f(z[c]);
   const double d = a / (double)M;
   double var = b / (double)M - d * d;
@@ -212,16 +233,12 @@ __global__ __launch_bounds__(256) void bn_bwd_partial(const T* dy, const T* y, c
 }
 
 // coef[3C]: dz = a*g + b + c*(z - mean)
-__global__ void bn_bwd_final(const float* part, int nchunks, long long M, int C,
-                             const float* gamma, const float* invstd, float* dgamma, float* dbeta,
-                             float* coef) {
-  int c = blockIdx.x * blockDim.x + threadIdx.x;
-  if (c >= C) return;
-  double sg = 0.0, sgx = 0.0;
-  for (int k = 0; k < nchunks; ++k) {
-    sg += part[(long long)k * 2 * C + c];
-    sgx += part[(long long)k * 2 * C + C + c];
-  }
+__global__ __launch_bounds__(256) void bn_bwd_final(const float* part, int nchunks, long long M,
+                                                    int C, const float* gamma, const float* invstd,
+                                                    float* dgamma, float* dbeta, float* coef) {
+  double sg, sgx;
+  if (!chunk_sums(part, nchunks, C, sg, sgx)) return;
+  const int c = blockIdx.x * 64 + (threadIdx.x & 63);
   const float is = invstd[c];
   const float db = (float)sg;
   const float dg = (float)(sgx * (double)is);
@@ -361,14 +378,34 @@ __global__ void avgpool_bwd_kernel(const float* df, int N, int HW, int C, T* dx)
 }
 
 // ------------------------------------------------------------- classifier
-__global__ void fc_fwd_kernel(const float* f, const float* W, const float* b, int N, int I, int J,
-                              float* z) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= N * J) return;
-  const int n = i / J, j = i % J;
-  float s = 0.f;
-  for (int k = 0; k < I; ++k) s += f[(long long)n * I + k] * W[(long long)j * I + k];
-  z[i] = s + b[j];
+// One block per row: each thread takes a strided slice of the features for 8
+// classes at a time, then a fixed-order wave and block reduction.
+__global__ __launch_bounds__(256) void fc_fwd_kernel(const float* f, const float* W, const float* b,
+                                                     int N, int I, int J, float* z) {
+  __shared__ float red[4][8];
+  const int n = blockIdx.x, t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const float* fr = f + (long long)n * I;
+  for (int j0 = 0; j0 < J; j0 += 8) {
+    float s[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) s[k] = 0.f;
+    for (int i = t; i < I; i += 256) {
+      const float x = fr[i];
+#pragma unroll
+      for (int k = 0; k < 8; ++k)
+        if (j0 + k < J) s[k] += x * W[(long long)(j0 + k) * I + i];
+    }
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      float v = s[k];
+      for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+      if (lane == 0) red[wave][k] = v;
+    }
+    __syncthreads();
+    if (t < 8 && j0 + t < J)
+      z[(long long)n * J + j0 + t] = ((red[0][t] + red[1][t]) + (red[2][t] + red[3][t])) + b[j0 + t];
+    __syncthreads();
+  }
 }
 
 __global__ __launch_bounds__(256) void softmax_ce_kernel(const float* z, const int32_t* labels,
@@ -567,25 +604,30 @@ __global__ void cast_kernel(const float* src, long long n, T* dst) {
 }
 
 // ------------------------------------------------------- weight repacking
-// tab row: src_off, K, R, S, C0, Cp, krsc_off, crsk_off
+// tab row: src_off, K, R, S, C0, Cp, krsc_off, crsk_off.  Both copies are
+// written in their own element order (coalesced); the [C][R][S][K] copy reads
+// the fp32 master with a stride.
 template <typename T>
 __global__ void pack_conv_kernel(const float* master, const long long* tab, T* shadow) {
   const long long* t = tab + 8 * blockIdx.y;
   const int K = (int)t[1], R = (int)t[2], S = (int)t[3], C0 = (int)t[4], Cp = (int)t[5];
-  const long long n = (long long)K * R * S * Cp;
   const float* src = master + t[0];
   T* krsc = shadow + t[6];
-  T* crsk = t[7] >= 0 ? shadow + t[7] : nullptr;
+  const long long n = (long long)K * R * S * Cp;
   for (long long i = blockIdx.x * (long long)blockDim.x + threadIdx.x; i < n;
        i += (long long)gridDim.x * blockDim.x) {
     const int c = (int)(i % Cp);
-    const long long krs = i / Cp;
-    const float v = c < C0 ? src[krs * C0 + c] : 0.f;
-    krsc[i] = from_f<T>(v);
-    if (crsk && c < C0) {
-      const int s = (int)(krs % S), r = (int)((krs / S) % R), k = (int)(krs / ((long long)R * S));
-      crsk[(((long long)c * R + r) * S + s) * K + k] = from_f<T>(v);
-    }
+    krsc[i] = from_f<T>(c < C0 ? src[(i / Cp) * C0 + c] : 0.f);
+  }
+  if (t[7] < 0) return;
+  T* crsk = shadow + t[7];
+  const long long n2 = (long long)C0 * R * S * K;
+  for (long long i = blockIdx.x * (long long)blockDim.x + threadIdx.x; i < n2;
+       i += (long long)gridDim.x * blockDim.x) {
+    const int k = (int)(i % K);
+    const long long crs = i / K;  // (c * R + r) * S + s
+    const int s = (int)(crs % S), r = (int)((crs / S) % R), c = (int)(crs / ((long long)R * S));
+    crsk[i] = from_f<T>(src[(((long long)k * R + r) * S + s) * C0 + c]);
   }
 }
 
@@ -640,7 +682,7 @@ hipError_t bn_train_stats(int dt, const void* z, long long M, int C, const float
     using T = std::remove_pointer_t<decltype(tp)>;
     hipLaunchKernelGGL(bn_stats_partial<T>, dim3(nch), dim3(256), 0, stream, (const T*)z, M, C,
                        rpc, partials);
-    hipLaunchKernelGGL(bn_stats_final<T>, dim3(cdiv(C, 256)), dim3(256), 0, stream, (const T*)z,
+    hipLaunchKernelGGL(bn_stats_final<T>, dim3(cdiv(C, 64)), dim3(256), 0, stream, (const T*)z,
                        partials, nch, M, C, gamma, beta, rm, rv, mean, invstd, scale, shift);
   });
 }
@@ -676,7 +718,7 @@ hipError_t bn_backward(int dt, const void* dy, const void* y, const void* z, lon
     using T = std::remove_pointer_t<decltype(tp)>;
     hipLaunchKernelGGL(bn_bwd_partial<T>, dim3(nch), dim3(256), 0, stream, (const T*)dy,
                        (const T*)y, (const T*)z, M, C, rpc, mean, partials);
-    hipLaunchKernelGGL(bn_bwd_final, dim3(cdiv(C, 256)), dim3(256), 0, stream, partials, nch, M, C,
+    hipLaunchKernelGGL(bn_bwd_final, dim3(cdiv(C, 64)), dim3(256), 0, stream, partials, nch, M, C,
                        gamma, invstd, dgamma, dbeta, coef);
     hipLaunchKernelGGL(bn_bwd_apply<T>, dim3(grid_for(units)), dim3(256), 0, stream, (const T*)dy,
                        (const T*)y, (const T*)z, units, C, mean, coef, (T*)dz, (T*)g_out);
@@ -731,8 +773,7 @@ hipError_t avgpool_bwd(int dt, const float* df, int N, int HW, int C, void* dx,
 hipError_t fc_fwd(const float* f, const float* W, const float* b, int N, int I, int J, float* z,
                   hipStream_t stream) {
   if (N == 0) return hipSuccess;
-  hipLaunchKernelGGL(fc_fwd_kernel, dim3(cdiv(N * J, 256)), dim3(256), 0, stream, f, W, b, N, I,
-                     J, z);
+  hipLaunchKernelGGL(fc_fwd_kernel, dim3(N), dim3(256), 0, stream, f, W, b, N, I, J, z);
   return hipGetLastError();
 }
 

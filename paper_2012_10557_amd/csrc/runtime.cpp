@@ -371,7 +371,7 @@ static void plan_job(Arena& a, TrainJob& j) {
   j.ws = a.take<float>(j.ws_floats);
   j.ce_out = a.take<float>((size_t)j.n_steps * 3);
   j.hcount = a.take<int32_t>(j.epochs);
-  j.eval_cap = std::max(1, std::min(j.n_h, 256));
+  j.eval_cap = std::max(1, std::min(j.n_h, 512));
   plan_eval(a, net, j.geo, j.lowest, 5, j.eval_cap, j.eval);
   if (j.lowest == 0) j.eval_in = a.take_bytes((size_t)j.eval_cap * in_elems * es);
 }
@@ -713,7 +713,7 @@ ekya_status run_retrain(Ctx& c, float* weights, int k, const void* frames, const
   const size_t es = dtype_size(dt);
   const long long feat = j.geo.stage_in_elems(net, j.lowest);
   j.row_bytes = feat * ((j.lowest == 5) ? 4 : es);
-  const int ccap = 128;  // frames per cache-build chunk
+  const int ccap = 512;  // frames per cache-build chunk
 
   // plan: job buffers + cache + cache-build scratch
   auto plan = [&](Arena& a, void*& cache, int32_t*& d_S, void*& padded, EvalBufs& ceb) {
@@ -861,7 +861,7 @@ ekya_status run_profile(Ctx& c, const float* weights, const ekya_profile_cfg* cf
     std::vector<int32_t> Si(S.begin(), S.begin() + j.n_s);
     job_prepare_host(j, Si, cf.shuffle_seed);
   }
-  const int ccap = 128;
+  const int ccap = 512;
   int32_t* d_S = nullptr;
   void* padded = nullptr;
   EvalBufs ceb;
@@ -976,7 +976,7 @@ ekya_status run_infer(Ctx& c, const float* weights, const void* frames, int n, i
   const Net& net = c.net[dt];
   const Geo geo = Geo::build(net, resolution, resolution);
   const size_t es = dtype_size(dt);
-  const int cap = 256;
+  const int cap = 512;
   float *master = nullptr, *fold = nullptr;
   void *shadow = nullptr, *padded = nullptr;
   EvalBufs eb;
