@@ -4,10 +4,10 @@
  * The library runs, on one gfx950 GPU, the data-parallel hot path of Ekya
  * (Bhardwaj et al., "Ekya: Continuous Learning of Video Analytics Models on
  * Edge Compute Servers"): retraining the last k stages of a ResNet18 frame
- * classifier on a uniformly subsampled window of labelled frames (sections 3.2
+ * classifier on a uniformly subsampled window of labelled frames (sections 3.1
  * and 4.3), micro-profiling many such retraining configurations for a few
  * epochs on small subsets (section 4.3, "Micro-profiling design"), and
- * batched inference at a configured resolution (sections 1 and 3.2,
+ * batched inference at a configured resolution (sections 1 and 3.1,
  * inference configurations).
  *
  * Conventions shared by every call
@@ -62,7 +62,7 @@ typedef enum { EKYA_FP32 = 0, EKYA_BF16 = 1 } ekya_precision;
 typedef struct ekya_ctx ekya_ctx;
 
 /* Retraining configuration (the paper's retraining configuration, section
- * 3.2: layers to retrain, data fraction, epochs, batch size; learning rate
+ * 3.1: layers to retrain, data fraction, epochs, batch size; learning rate
  * and momentum of plain SGD). */
 typedef struct {
   double subsample_frac; /* (0, 1]: round-half-up(frac * n_frames), at least 1, frames are used */
@@ -103,6 +103,7 @@ typedef struct {
   int n_train;
   float heldout_acc[EKYA_MAX_EPOCHS];   /* accuracy after each epoch */
   float epoch_seconds[EKYA_MAX_EPOCHS]; /* GPU time of each epoch */
+  float epoch_loss[EKYA_MAX_EPOCHS];    /* mean training loss over the epoch's steps */
   float heldout_acc_final;
 } ekya_profile_result;
 
@@ -120,7 +121,7 @@ const char* ekya_status_str(ekya_status s);
 const char* ekya_last_error(const ekya_ctx* ctx);
 
 /* ------------------------------------------------------------ retrain
- * Retrain the last k_trainable stages (sections 3.2 and 4.3).
+ * Retrain the last k_trainable stages (sections 3.1 and 4.3).
  *  weights        device fp32, canonical layout, read and updated in place:
  *                 parameters and running statistics of trainable stages
  *                 change; frozen stages stay bitwise unchanged.
@@ -161,7 +162,7 @@ ekya_status ekya_profile(ekya_ctx* ctx, const float* weights, const ekya_profile
 /* ------------------------------------------------------------ infer
  * Classify n frames (device, [n, H, W, 3]) after resizing them bilinearly
  * (half-pixel centres, no antialiasing) to resolution x resolution (the
- * inference configuration's resolution, section 3.2); eval-mode BatchNorm.
+ * inference configuration's resolution, section 3.1); eval-mode BatchNorm.
  * labels_out: device int32 [n] (lowest class index wins ties).  weights:
  * device fp32 canonical, read only.  Asynchronous on `stream`: the caller
  * synchronises before reading labels_out.  Frame sampling (every k-th frame)

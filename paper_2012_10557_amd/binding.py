@@ -60,6 +60,7 @@ class ProfileResult(ctypes.Structure):
     _fields_ = [("status", ctypes.c_int), ("n_train", ctypes.c_int),
                 ("heldout_acc", ctypes.c_float * EKYA_MAX_EPOCHS),
                 ("epoch_seconds", ctypes.c_float * EKYA_MAX_EPOCHS),
+                ("epoch_loss", ctypes.c_float * EKYA_MAX_EPOCHS),
                 ("heldout_acc_final", ctypes.c_float)]
 
 
@@ -273,7 +274,8 @@ def ekya_profile(ctx, weights, cfgs: Sequence[dict], frames, labels, heldout_fra
         r = res[i]
         e = c["epochs"]
         out.append({"status": r.status, "n_train": r.n_train, "heldout_acc": list(r.heldout_acc[:e]),
-                    "epoch_seconds": list(r.epoch_seconds[:e]), "heldout_acc_final": r.heldout_acc_final})
+                    "epoch_seconds": list(r.epoch_seconds[:e]), "epoch_loss": list(r.epoch_loss[:e]),
+                    "heldout_acc_final": r.heldout_acc_final})
     return out
 
 

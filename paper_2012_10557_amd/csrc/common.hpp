@@ -35,6 +35,10 @@ template <typename T> union Unit {
 
 __device__ __forceinline__ uint4 zero_unit() { return make_uint4(0u, 0u, 0u, 0u); }
 
+// max(v, 0) that keeps a NaN input NaN (fmaxf would return 0), so that a
+// non-finite input reaches the loss and is reported.
+__device__ __forceinline__ float relu_nan(float v) { return v < 0.f ? 0.f : v; }
+
 // D += A * B on one 16x16 output tile; `a` and `b` are one 16-byte unit each
 // (k-contiguous).  For bf16 the unit is the whole k-chunk of one
 // v_mfma_f32_16x16x32_bf16; for fp32 the four floats feed four

@@ -210,7 +210,7 @@ struct FwdPolicy {
     }
     if (e.relu) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) v[i] = fmaxf(v[i], 0.0f);
+      for (int i = 0; i < 4; ++i) v[i] = relu_nan(v[i]);
     }
     store4<T>(a.y + off, v);
   }
@@ -546,7 +546,7 @@ __global__ void split_reduce_kernel(const float* part, int splits, long long npi
     }
     if (e.relu) {
 #pragma unroll
-      for (int k = 0; k < 4; ++k) v[k] = fmaxf(v[k], 0.f);
+      for (int k = 0; k < 4; ++k) v[k] = relu_nan(v[k]);
     }
     store4<T>(y + off, v);
   }
@@ -564,6 +564,343 @@ __global__ void wgrad_reduce_kernel(const float* part, int splits, int K, int RS
     for (int z = 0; z < splits; ++z) s += part[z * stride + src];
     dw[i] = s;
   }
+}
+
+// ------------------------------------------------- direct-to-LDS main loop
+// bf16 forward and data-gradient GEMMs whose reduction runs in 64-element
+// stages that never straddle a filter tap (C, resp. K, a multiple of 64).
+// Operands go from global memory straight into LDS with
+// global_load_lds_dwordx4 (16 bytes per lane; lane i's unit lands at the
+// instruction's LDS base + 16 i), through an NST-deep ring of stages.  A stage
+// holds BM A-rows then BN B-rows of 8 units (64 elements) each; unit u of row
+// r sits at slot u ^ (r & 7), so that one instruction fills 8 whole rows
+// (8 lanes read one 128-byte line) and the MFMA fragment reads (lane = 16-row
+// index + 16 * k-unit) hit distinct banks.  Lanes whose row or tap lies
+// outside the operand read a zero unit instead.
+typedef __attribute__((address_space(3))) void lds_void;
+
+__device__ __align__(16) uint4 g_zero_unit[1];
+
+__device__ __forceinline__ void dma16(const void* src, uint4* lds_dst) {
+  const uint32_t m0 = (uint32_t)(uintptr_t)(lds_void*)lds_dst;
+  // inline asm: the compiler would otherwise make every later LDS read wait
+  // for all outstanding loads; completion is tracked with explicit vmcnt waits
+  asm volatile("global_load_lds_dwordx4 %0, off" ::"v"(src), "{m0}"(m0) : "memory");
+}
+
+// Barrier without __syncthreads' fence (which would wait for every
+// outstanding load); the vmcnt wait before it orders the LDS writes.
+__device__ __forceinline__ void stage_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+template <int N> __device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  // gfx9 encoding: vmcnt[3:0], expcnt[6:4], lgkmcnt[11:8], vmcnt[5:4] at [15:14]
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// Workgroups are dispatched round-robin over the 8 XCDs (each with its own
+// L2); give every XCD a contiguous range of tiles, rows of the output fastest,
+// so the blocks sharing a column panel of the B operand share an L2.
+__device__ __forceinline__ int xcd_tile(int L, int total) {
+  const int x = L & 7, k = L >> 3;
+  return x * (total >> 3) + min(x, total & 7) + k;
+}
+
+struct DmaFwdArgs {
+  ConvGeom g;
+  const bf16* x;
+  const bf16* w;  // [K][R][S][C]
+  bf16* y;
+  ConvEpilogue epi;
+  SplitOut so;
+  int tiles_m, tiles_n;
+};
+
+template <int BM, int BN>
+struct DmaFwdOp {
+  static constexpr int GA = BM / 8, IPW = (BM + BN) / 32;  // row octets per wave
+  using Args = DmaFwdArgs;
+  int s_begin, s_end;
+  long long Ktot;
+  const bf16* ptr[IPW];
+  int h0[IPW], w0[IPW];
+  bool ok[IPW];
+  int tr, ts, tc;
+
+  __device__ void init(const Args& a, int m0, int n0, int split, int wave, int lane) {
+    const ConvGeom& g = a.g;
+    Ktot = (long long)g.R * g.S * g.C;
+    const int ns = (int)(Ktot / 64);
+    s_begin = min(ns, split * a.so.stages_per_split);
+    s_end = min(ns, s_begin + a.so.stages_per_split);
+    const int npix = g.N * g.P * g.Q;
+    const int r8 = lane >> 3, u = (lane & 7) ^ r8;
+#pragma unroll
+    for (int j = 0; j < IPW; ++j) {
+      const int oct = wave + 4 * j;
+      if (oct < GA) {
+        const int row = m0 + oct * 8 + r8;
+        ok[j] = row < g.K;
+        ptr[j] = a.w + (ok[j] ? row : 0) * Ktot + u * 8;
+        h0[j] = w0[j] = 0;
+      } else {
+        const int pix = n0 + (oct - GA) * 8 + r8;
+        ok[j] = pix < npix;
+        const int pp = ok[j] ? pix : 0;
+        const int n = pp / (g.P * g.Q), rem = pp % (g.P * g.Q);
+        const int p = rem / g.Q, q = rem % g.Q;
+        h0[j] = p * g.stride - g.pad;
+        w0[j] = q * g.stride - g.pad;
+        ptr[j] = a.x + (long long)n * g.H * g.W * g.C + u * 8;
+      }
+    }
+    const int k0 = s_begin * 64;
+    const int rs = k0 / g.C;
+    tc = k0 - rs * g.C;
+    tr = rs / g.S;
+    ts = rs - tr * g.S;
+  }
+  __device__ void issue(const Args& a, int st, uint4* slot, int wave) {
+    const ConvGeom& g = a.g;
+    const long long k0 = (long long)st * 64;
+#pragma unroll
+    for (int j = 0; j < IPW; ++j) {
+      const int oct = wave + 4 * j;
+      const bf16* src;
+      bool in;
+      if (oct < GA) {
+        src = ptr[j] + k0;
+        in = ok[j];
+      } else {
+        const int h = h0[j] + tr, w = w0[j] + ts;
+        in = ok[j] && (unsigned)h < (unsigned)g.H && (unsigned)w < (unsigned)g.W;
+        src = ptr[j] + ((long long)h * g.W + w) * g.C + tc;
+      }
+      dma16(in ? (const void*)src : (const void*)g_zero_unit, slot + oct * 64);
+    }
+    tc += 64;
+    if (tc >= g.C) {
+      tc = 0;
+      if (++ts == g.S) {
+        ts = 0;
+        ++tr;
+      }
+    }
+  }
+  __device__ void out4(const Args& a, int row, int col, float (&v)[4]) {
+    const ConvGeom& g = a.g;
+    const int npix = g.N * g.P * g.Q;
+    if (row >= g.K || col >= npix) return;
+    const long long off = (long long)col * g.K + row;
+    if (a.so.splits > 1) {
+      float* dst = a.so.part + (long long)blockIdx.y * npix * g.K + off;
+      *reinterpret_cast<float4*>(dst) = make_float4(v[0], v[1], v[2], v[3]);
+      return;
+    }
+    const ConvEpilogue& e = a.epi;
+    if (e.scale) {
+      const float4 s = *reinterpret_cast<const float4*>(e.scale + row);
+      v[0] *= s.x; v[1] *= s.y; v[2] *= s.z; v[3] *= s.w;
+    }
+    if (e.shift) {
+      const float4 s = *reinterpret_cast<const float4*>(e.shift + row);
+      v[0] += s.x; v[1] += s.y; v[2] += s.z; v[3] += s.w;
+    }
+    if (e.res) {
+      float r[4];
+      load4<bf16>(reinterpret_cast<const bf16*>(e.res) + off, r);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) v[i] += r[i];
+    }
+    if (e.relu) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) v[i] = relu_nan(v[i]);
+    }
+    store4<bf16>(a.y + off, v);
+  }
+};
+
+struct DmaDgradArgs {
+  ConvGeom g;
+  const bf16* dy;
+  const bf16* wt;  // [C][R][S][K]
+  bf16* dx;
+  const bf16* res;
+  SplitOut so;
+  int tiles_m, tiles_n;
+};
+
+// dx[pix][c] = sum_(r,s,k) wt[c][r][s][k] dy(pix; r,s,k), stride 1 or 2.
+template <int BM, int BN>
+struct DmaDgradOp {
+  static constexpr int GA = BM / 8, IPW = (BM + BN) / 32;
+  using Args = DmaDgradArgs;
+  int s_begin, s_end;
+  long long Ktot;
+  const bf16* ptr[IPW];
+  int hp[IPW], wp[IPW];  // input pixel + pad
+  bool ok[IPW];
+  int tr, ts, tk;
+
+  __device__ void init(const Args& a, int m0, int n0, int split, int wave, int lane) {
+    const ConvGeom& g = a.g;
+    Ktot = (long long)g.R * g.S * g.K;
+    const int ns = (int)(Ktot / 64);
+    s_begin = min(ns, split * a.so.stages_per_split);
+    s_end = min(ns, s_begin + a.so.stages_per_split);
+    const int npix = g.N * g.H * g.W;
+    const int r8 = lane >> 3, u = (lane & 7) ^ r8;
+#pragma unroll
+    for (int j = 0; j < IPW; ++j) {
+      const int oct = wave + 4 * j;
+      if (oct < GA) {
+        const int row = m0 + oct * 8 + r8;
+        ok[j] = row < g.C;
+        ptr[j] = a.wt + (ok[j] ? row : 0) * Ktot + u * 8;
+        hp[j] = wp[j] = 0;
+      } else {
+        const int pix = n0 + (oct - GA) * 8 + r8;
+        ok[j] = pix < npix;
+        const int pp = ok[j] ? pix : 0;
+        const int n = pp / (g.H * g.W), rem = pp % (g.H * g.W);
+        hp[j] = rem / g.W + g.pad;
+        wp[j] = rem % g.W + g.pad;
+        ptr[j] = a.dy + (long long)n * g.P * g.Q * g.K + u * 8;
+      }
+    }
+    const int k0 = s_begin * 64;
+    const int rs = k0 / g.K;
+    tk = k0 - rs * g.K;
+    tr = rs / g.S;
+    ts = rs - tr * g.S;
+  }
+  __device__ void issue(const Args& a, int st, uint4* slot, int wave) {
+    const ConvGeom& g = a.g;
+    const long long k0 = (long long)st * 64;
+    const int sh = g.stride == 2 ? 1 : 0;
+#pragma unroll
+    for (int j = 0; j < IPW; ++j) {
+      const int oct = wave + 4 * j;
+      const bf16* src;
+      bool in;
+      if (oct < GA) {
+        src = ptr[j] + k0;
+        in = ok[j];
+      } else {
+        const int h = hp[j] - tr, w = wp[j] - ts;
+        const int p = h >> sh, q = w >> sh;
+        in = ok[j] && h >= 0 && w >= 0 && ((h | w) & sh) == 0 && p < g.P && q < g.Q;
+        src = ptr[j] + ((long long)p * g.Q + q) * g.K + tk;
+      }
+      dma16(in ? (const void*)src : (const void*)g_zero_unit, slot + oct * 64);
+    }
+    tk += 64;
+    if (tk >= g.K) {
+      tk = 0;
+      if (++ts == g.S) {
+        ts = 0;
+        ++tr;
+      }
+    }
+  }
+  __device__ void out4(const Args& a, int row, int col, float (&v)[4]) {
+    const ConvGeom& g = a.g;
+    const int npix = g.N * g.H * g.W;
+    if (row >= g.C || col >= npix) return;
+    const long long off = (long long)col * g.C + row;
+    if (a.so.splits > 1) {
+      float* dst = a.so.part + (long long)blockIdx.y * npix * g.C + off;
+      *reinterpret_cast<float4*>(dst) = make_float4(v[0], v[1], v[2], v[3]);
+      return;
+    }
+    if (a.res) {
+      float r[4];
+      load4<bf16>(a.res + off, r);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) v[i] += r[i];
+    }
+    store4<bf16>(a.dx + off, v);
+  }
+};
+
+// 4 waves as WGM x (4 / WGM); each wave owns a (BM/WGM) x (BN*WGM/4) block of
+// 16x16 MFMA tiles.  Stage st waits for its own loads (vmcnt), a barrier makes
+// every wave's loads visible and retires the slot read in the previous
+// iteration, which then receives stage st + NST - 1.
+template <int BM, int BN, int WGM, int NST, class Op>
+__global__ __launch_bounds__(NT) void gemm_dma_kernel(typename Op::Args a) {
+  constexpr int WGN = 4 / WGM;
+  static_assert((BM + BN) % 32 == 0, "row octets split over 4 waves");
+  constexpr int LPS = Op::IPW;            // loads per lane per stage
+  constexpr int SU = (BM + BN) * 8;       // 16-byte units per stage
+  constexpr int WM = BM / WGM, WN = BN / WGN, TI = WM / 16, TJ = WN / 16;
+  __shared__ uint4 smem[NST * SU];
+
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wm = wave / WGN, wn = wave % WGN;
+  const int t = xcd_tile(blockIdx.x, a.tiles_m * a.tiles_n);
+  const int m0 = (t % a.tiles_m) * BM, n0 = (t / a.tiles_m) * BN;
+  // lane's unit within a 16-row fragment: row fr, k-unit kf * 4 + fkc
+  const int fr = lane & 15, fkc = lane >> 4;
+  const int off0 = fr * 8 + (fkc ^ (fr & 7));
+  const int off1 = fr * 8 + ((4 + fkc) ^ (fr & 7));
+
+  Op op;
+  op.init(a, m0, n0, blockIdx.y, wave, lane);
+  const int s0 = op.s_begin, s1 = op.s_end;
+
+  f32x4 acc[TI][TJ];
+#pragma unroll
+  for (int i = 0; i < TI; ++i)
+#pragma unroll
+    for (int j = 0; j < TJ; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+#pragma unroll
+  for (int p = 0; p < NST - 1; ++p)
+    if (s0 + p < s1) op.issue(a, s0 + p, smem + p * SU, wave);
+
+  int slot = 0;
+  for (int st = s0; st < s1; ++st) {
+    if (st + NST - 2 < s1)
+      wait_vmcnt<LPS * (NST - 2)>();
+    else
+      wait_vmcnt<0>();
+    stage_barrier();
+    if (st + NST - 1 < s1) {
+      const int nslot = slot == 0 ? NST - 1 : slot - 1;
+      op.issue(a, st + NST - 1, smem + nslot * SU, wave);
+    }
+    const uint4* As = smem + slot * SU + (wm * WM) * 8;
+    const uint4* Bs = smem + slot * SU + (BM + wn * WN) * 8;
+#pragma unroll
+    for (int kf = 0; kf < 2; ++kf) {
+      const int off = kf == 0 ? off0 : off1;
+      uint4 fa[TI], fb[TJ];
+#pragma unroll
+      for (int i = 0; i < TI; ++i) fa[i] = As[i * 128 + off];
+#pragma unroll
+      for (int j = 0; j < TJ; ++j) fb[j] = Bs[j * 128 + off];
+#pragma unroll
+      for (int i = 0; i < TI; ++i)
+#pragma unroll
+        for (int j = 0; j < TJ; ++j) mma_unit(acc[i][j], fa[i], fb[j], (bf16*)nullptr);
+    }
+    if (++slot == NST) slot = 0;
+  }
+
+  const int lr = lane & 15, lg = lane >> 4;
+#pragma unroll
+  for (int i = 0; i < TI; ++i)
+#pragma unroll
+    for (int j = 0; j < TJ; ++j) {
+      float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
+      op.out4(a, m0 + wm * WM + i * 16 + 4 * lg, n0 + wn * WN + j * 16 + lr, v);
+    }
 }
 
 // -------------------------------------------------------------- launching
@@ -673,12 +1010,106 @@ hipError_t split_finish(const float* part, int splits, long long npix, int C, co
   return hipGetLastError();
 }
 
+// Direct-to-LDS GEMM planning: (BM, BN, blocks per CU) candidates, the first
+// that fills the chip twice over without splitting, else 128-row tiles with
+// the reduction split until ~400 blocks (>= 4 stages per split).
+struct DmaPlan {
+  int bm, bn, splits, sps;
+};
+
+DmaPlan plan_dma(int rows, long long cols, int ns, bool allow_split) {
+  struct Cand {
+    int bm, bn, per_cu;
+  };
+  const Cand big[2] = {{128, 128, 2}, {128, 64, 3}};
+  const Cand narrow[2] = {{64, 256, 2}, {64, 128, 3}};
+  const Cand* c = rows <= 64 ? narrow : big;
+  for (int i = 0; i < 2; ++i) {
+    const long long tiles = (long long)cdiv(rows, c[i].bm) * cdivl(cols, c[i].bn);
+    if (tiles >= 2LL * 256 * c[i].per_cu) return {c[i].bm, c[i].bn, 1, ns};
+  }
+  const long long tiles1 = (long long)cdiv(rows, c[1].bm) * cdivl(cols, c[1].bn);
+  if (tiles1 >= 512 || !allow_split) return {c[1].bm, c[1].bn, 1, ns};
+  const long long tiles0 = (long long)cdiv(rows, c[0].bm) * cdivl(cols, c[0].bn);
+  int s = (int)std::min<long long>(cdivl(400, tiles0), std::max(1, ns / 4));
+  s = std::max(1, std::min(s, 16));
+  const int sps = cdiv(ns, s);
+  return {c[0].bm, c[0].bn, cdiv(ns, sps), sps};
+}
+
+template <int BM, int BN, int WGM, template <int, int> class OpT>
+hipError_t launch_dma(typename OpT<BM, BN>::Args a, long long cols, int rows, hipStream_t stream,
+                      Cost cost, const char* name) {
+  a.tiles_m = cdiv(rows, BM);
+  a.tiles_n = (int)cdivl(cols, BN);
+  dim3 grid(a.tiles_m * a.tiles_n, a.so.splits);
+  KernelTimer* t = t_timer;
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  if (t) {
+    e0 = t->take();
+    e1 = t->take();
+    EKYA_HIP(hipEventRecord(e0, stream));
+  }
+  hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, WGM, 2, OpT<BM, BN>>), grid, dim3(NT), 0, stream, a);
+  hipError_t e = hipGetLastError();
+  if (t && e == hipSuccess) {
+    EKYA_HIP(hipEventRecord(e1, stream));
+    t->recs.push_back({std::string(name) + "<bf16," + std::to_string(BM) + "," +
+                           std::to_string(BN) + ",dma>",
+                       cost.flops, cost.bytes, e0, e1});
+  }
+  return e;
+}
+
+template <template <int, int> class OpT, class Args>
+hipError_t dispatch_dma(Args a, const DmaPlan& p, long long cols, int rows, hipStream_t stream,
+                        Cost cost, const char* name) {
+  if (p.bm == 128 && p.bn == 128) return launch_dma<128, 128, 2, OpT>(a, cols, rows, stream, cost, name);
+  if (p.bm == 128 && p.bn == 64) return launch_dma<128, 64, 2, OpT>(a, cols, rows, stream, cost, name);
+  if (p.bm == 64 && p.bn == 256) return launch_dma<64, 256, 1, OpT>(a, cols, rows, stream, cost, name);
+  if (p.bm == 64 && p.bn == 128) return launch_dma<64, 128, 1, OpT>(a, cols, rows, stream, cost, name);
+  return hipErrorInvalidValue;
+}
+
+// bf16 forward with C % 64 == 0 on the direct-to-LDS path.
+hipError_t conv_fwd_dma(const ConvGeom& g, const void* x, const void* w, void* y,
+                        const ConvEpilogue& epi, float* ws, size_t ws_floats, hipStream_t stream) {
+  const int ns = g.R * g.S * g.C / 64;
+  const long long npix = (long long)g.N * g.P * g.Q;
+  DmaPlan p = plan_dma(g.K, npix, ns, ws != nullptr);
+  if (p.splits > 1 && (size_t)p.splits * npix * g.K > ws_floats) p = {p.bm, p.bn, 1, ns};
+  DmaFwdArgs a{g, (const bf16*)x, (const bf16*)w, (bf16*)y, epi, SplitOut{ws, p.splits, p.sps}, 0, 0};
+  hipError_t e = dispatch_dma<DmaFwdOp>(a, p, npix, g.K, stream,
+                                       conv_cost(g, g.C0 ? g.C0 : g.C, sizeof(bf16), false),
+                                       "conv_fwd");
+  if (e != hipSuccess || p.splits <= 1) return e;
+  return split_finish<bf16>(ws, p.splits, npix, g.K, epi, y, stream);
+}
+
+// bf16 data gradient with K % 64 == 0 on the direct-to-LDS path.
+hipError_t conv_dgrad_dma(const ConvGeom& g, const void* dy, const void* wt, void* dx,
+                          const void* res, float* ws, size_t ws_floats, hipStream_t stream) {
+  const int ns = g.R * g.S * g.K / 64;
+  const long long npix = (long long)g.N * g.H * g.W;
+  DmaPlan p = plan_dma(g.C, npix, ns, ws != nullptr);
+  if (p.splits > 1 && (size_t)p.splits * npix * g.C > ws_floats) p = {p.bm, p.bn, 1, ns};
+  DmaDgradArgs a{g, (const bf16*)dy, (const bf16*)wt, (bf16*)dx, (const bf16*)res,
+                 SplitOut{ws, p.splits, p.sps}, 0, 0};
+  hipError_t e = dispatch_dma<DmaDgradOp>(a, p, npix, g.C, stream,
+                                         conv_cost(g, g.C, sizeof(bf16), false), "conv_dgrad");
+  if (e != hipSuccess || p.splits <= 1) return e;
+  ConvEpilogue ep;
+  ep.res = res;
+  return split_finish<bf16>(ws, p.splits, npix, g.C, ep, dx, stream);
+}
+
 constexpr int KU_MAIN = 8;
 
 template <typename T>
 hipError_t conv_fwd_t(const ConvGeom& g, const void* x, const void* w, void* y,
                       const ConvEpilogue& epi, float* ws, size_t ws_floats, hipStream_t stream) {
   constexpr int E = Elt<T>::E;
+  if (sizeof(T) == 2 && g.C % 64 == 0) return conv_fwd_dma(g, x, w, y, epi, ws, ws_floats, stream);
   const bool ut = g.C % (KU_MAIN * E) == 0;
   const int ns = cdiv(g.R * g.S * g.C, KU_MAIN * E);
   const long long npix = (long long)g.N * g.P * g.Q;
@@ -710,6 +1141,7 @@ hipError_t conv_dgrad_t(const ConvGeom& g, const void* dy, const void* wt, void*
                         const void* res, float* ws, size_t ws_floats, hipStream_t stream) {
   constexpr int E = Elt<T>::E;
   if (g.K % (KU_MAIN * E) != 0 || (g.stride != 1 && g.stride != 2)) return hipErrorInvalidValue;
+  if (sizeof(T) == 2) return conv_dgrad_dma(g, dy, wt, dx, res, ws, ws_floats, stream);
   const int ns = cdiv(g.R * g.S * g.K, KU_MAIN * E);
   const long long npix = (long long)g.N * g.H * g.W;
   Plan p = plan_tiles(g.C, (int)npix, ns, ws != nullptr);
@@ -745,6 +1177,16 @@ KernelTimer* thread_timer() { return t_timer; }
 
 size_t conv_split_workspace_floats(int dt, const ConvGeom& g, bool dgrad) {
   const int E = dtype_vec(dt);
+  if (dt == DT_BF16 && dgrad) {
+    const long long npix = (long long)g.N * g.H * g.W;
+    const DmaPlan p = plan_dma(g.C, npix, g.R * g.S * g.K / 64, true);
+    return p.splits > 1 ? (size_t)p.splits * npix * g.C : 0;
+  }
+  if (dt == DT_BF16 && g.C % 64 == 0) {
+    const long long npix = (long long)g.N * g.P * g.Q;
+    const DmaPlan p = plan_dma(g.K, npix, g.R * g.S * g.C / 64, true);
+    return p.splits > 1 ? (size_t)p.splits * npix * g.K : 0;
+  }
   if (dgrad) {
     const int ns = cdiv(g.R * g.S * g.K, KU_MAIN * E);
     const long long npix = (long long)g.N * g.H * g.W;

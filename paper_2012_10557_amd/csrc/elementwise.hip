@@ -156,7 +156,7 @@ __global__ void bn_apply_kernel(const T* z, long long units, int C, const float*
       // (z - mean) * scale + beta: no cancellation when invstd is large
       float t = (v[i] - mean[c0 + i]) * scale[c0 + i] + beta[c0 + i];
       if (res) t += r[i];
-      if (relu) t = fmaxf(t, 0.f);
+      if (relu) t = relu_nan(t);
       v[i] = t;
     }
     reinterpret_cast<uint4*>(y)[u] = f_to_unit<T>(v);

@@ -5,7 +5,7 @@
 // BatchNorm, ReLU and 3x3/2 max pooling; four stages of two BasicBlocks
 // (widths 64/128/256/512, stride 2 entering stages 2-4 with a 1x1/2
 // projection shortcut); global average pooling; an affine classifier.
-// Stages (the unit of freezing, section 3.2): 0 stem, 1-4 layer1-4, 5 fc.
+// Stages (the unit of freezing, section 3.1): 0 stem, 1-4 layer1-4, 5 fc.
 //
 // Parameter offsets follow the canonical flat layout (torchvision state_dict
 // order without num_batches_tracked).  Inside the library conv weights sit at

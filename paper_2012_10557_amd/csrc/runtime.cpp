@@ -1,6 +1,6 @@
 // Retraining, micro-profiling and inference jobs.
 //
-// Retraining of the last k stages (sections 3.2 and 4.3):
+// Retraining of the last k stages (sections 3.1 and 4.3):
 //   1. draw the uniform training subset S of the window (host, seeded);
 //   2. run the frozen stages once per frame of S and of the held-out set, in
 //      eval mode, into the feature cache (stages below the lowest trainable
@@ -153,10 +153,12 @@ static void plan_eval(Arena& a, const Net& net, const Geo& g, int lo, int hi, in
   b.sc = a.take_bytes(m * es);
   b.pooled = a.take<float>((size_t)cap * 512);
   b.logits = a.take<float>((size_t)cap * net.n_classes);
+  // split-reduction scratch for every frame count a call may use, so that a
+  // convolution's plan never depends on how large this scratch happens to be
   size_t ws = 16;
   for (size_t i = 0; i < net.conv.size(); ++i)
     if (net.conv[i].stage >= lo && net.conv[i].stage <= hi)
-      for (int n : {cap, 1})
+      for (int n = 1; n <= cap; ++n)
         ws = std::max(ws, conv_split_workspace_floats(net.dt, conv_geom(net, g, (int)i, n), false));
   b.ws_floats = ws;
   b.ws = a.take<float>(ws);
@@ -306,11 +308,14 @@ static size_t ws_floats(const TrainJob& j) {
   for (size_t i = 0; i < net.conv.size(); ++i) {
     const ConvL& c = net.conv[i];
     if (c.stage < j.lowest || c.stage > 4) continue;
-    ConvGeom cg = conv_geom(net, j.geo, (int)i, j.B);
-    m = std::max(m, conv_wgrad_workspace_floats(j.dt, cg));
-    m = std::max(m, bn_partials_floats((long long)j.B * cg.P * cg.Q, c.cout));
-    m = std::max(m, conv_split_workspace_floats(j.dt, cg, false));
-    if (c.stage > 0) m = std::max(m, conv_split_workspace_floats(j.dt, cg, true));
+    // every batch size up to B (the last batch of an epoch may be partial)
+    for (int n = 1; n <= j.B; ++n) {
+      ConvGeom cg = conv_geom(net, j.geo, (int)i, n);
+      m = std::max(m, conv_wgrad_workspace_floats(j.dt, cg));
+      m = std::max(m, bn_partials_floats((long long)n * cg.P * cg.Q, c.cout));
+      m = std::max(m, conv_split_workspace_floats(j.dt, cg, false));
+      if (c.stage > 0) m = std::max(m, conv_split_workspace_floats(j.dt, cg, true));
+    }
   }
   return std::max<size_t>(m, 16);
 }
@@ -952,9 +957,13 @@ ekya_status run_profile(Ctx& c, const float* weights, const ekya_profile_cfg* cf
     } else {
       o.status = r.status;
       o.n_train = j.n_s;
+      const int spe = (j.n_s + j.B - 1) / j.B;
       for (int ep = 0; ep < j.epochs; ++ep) {
         o.heldout_acc[ep] = n_heldout ? (float)r.hc[ep] / (float)n_heldout : 0.f;
         o.epoch_seconds[ep] = r.secs[ep];
+        double l = 0.0;
+        for (int s = 0; s < spe; ++s) l += r.ce[3 * (ep * spe + s)];
+        o.epoch_loss[ep] = (float)(l / spe);
       }
       o.heldout_acc_final = o.heldout_acc[j.epochs - 1];
       if (r.status != EKYA_OK && overall == EKYA_OK) {
