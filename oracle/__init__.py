@@ -16,9 +16,9 @@ against the definitions by eye:
 * `resnet18` - the ResNet18 edge classifier (He et al., "Deep residual
                learning", the paper's reference for ResNet), torchvision topology,
                split into the stages whose freezing the paper uses as a cost
-               knob (section 3.2).
+               knob (section 3.1).
 * `ekya`     - retraining of the last k stages on a subsampled window with
-               held-out accuracy after every epoch (sections 3.2 and 4.3),
+               held-out accuracy after every epoch (sections 3.1 and 4.3),
                the micro-profiler's sweep over configurations, and inference
                at a chosen resolution (section 1, inference configurations).
 """

@@ -1,6 +1,6 @@
 """Retraining, micro-profiling and inference as the paper defines them.
 
-Retraining (sections 2.2 and 3.2): continue training the edge classifier on
+Retraining (sections 2.2 and 3.1): continue training the edge classifier on
 the current window's labelled frames.  The retraining configuration fixes the
 number of trainable stages k (the rest is frozen), the fraction of the
 window's data used, the number of epochs, the learning rate and the batch
@@ -13,7 +13,7 @@ uniform random subset of the window for a few epochs and reports its held-out
 accuracy after every epoch; its GPU time per epoch is what the scheduler
 scales.  Accuracy-curve extrapolation is a separate later step.
 
-Inference (section 1 and 3.2, inference configurations): frames sampled from
+Inference (sections 1 and 3.1, inference configurations): frames sampled from
 the stream are downsized to the configured resolution and classified.
 
 Frozen-prefix reuse: stages below the lowest trainable one never change, so

@@ -12,7 +12,7 @@ cites for the network's size in section 6.6):
   pool   : global average pool (no parameters)
   fc     : affine classifier with bias
 
-Retraining "fewer layers" / "freezing more layers" (section 3.2) is read as
+Retraining "fewer layers" / "freezing more layers" (section 3.1) is read as
 training the last k stages of [stem, layer1, layer2, layer3, layer4, fc]:
 k = 1 trains fc, k = 2 trains layer4 and fc, ..., k = 6 trains everything.
 Frozen stages always run BatchNorm in eval mode; trainable stages run it in
