@@ -903,6 +903,162 @@ __global__ __launch_bounds__(NT) void gemm_dma_kernel(typename Op::Args a) {
     }
 }
 
+// ------------------------------------------- direct-to-LDS weight gradient
+// bf16 D[rsc][k] = sum_pix x(pix; r,s,c) dy[pix][k] with C and K multiples of
+// 64.  A tile's rows are BM channels of one tap.  A stage is 64 pixels: 64
+// gathered input-pixel rows of BM channels (zero where the tap falls in the
+// padding), then 64 rows of BN output-gradient channels, both pixel-major as
+// in memory and loaded by global_load_lds_dwordx4; 32-byte segment s of
+// pixel row p is stored at s ^ (p mod segments-per-row).  The MFMA operands
+// need 8 consecutive pixels of one channel per lane: ds_read_b64_tr_b16
+// reads a 4-pixel x 16-channel block per 16-lane group (member m supplies
+// the address of pixel m / 4, channels 4 (m % 4) .. +3) and hands lane i the
+// 4 pixels of channel i; two such reads make one operand.
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ uint2 lds_read_tr16(const char* p) {
+  v4i16 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) v4i16*)(__attribute__((address_space(3))) char*)p);
+  return __builtin_bit_cast(uint2, v);
+}
+
+struct WgDmaArgs {
+  ConvGeom g;
+  const bf16* x;
+  const bf16* dy;
+  float* out;       // [split][K][R*S*C], or dw itself with one split
+  int m_per_split;  // pixels per split, a multiple of 64
+  int tiles_m, tiles_n;
+};
+
+template <int BM, int BN>
+__global__ __launch_bounds__(NT) void wgrad_dma_kernel(WgDmaArgs a) {
+  constexpr int NST = 2;
+  constexpr int UA = BM / 8, UB = BN / 8;     // 16-byte units per pixel row
+  constexpr int RA = 64 / UA, RB = 64 / UB;   // pixel rows per DMA instruction
+  constexpr int IA = 64 / RA, IB = 64 / RB;   // DMA instructions per stage
+  constexpr int LPS = (IA + IB) / 4, LA = IA / 4;
+  static_assert(IA % 4 == 0 && IB % 4 == 0, "instructions split over 4 waves");
+  constexpr int SA = BM / 16, SB = BN / 16;   // 32-byte segments per row
+  constexpr int STAGE_BYTES = 64 * (BM + BN) * 2;
+  constexpr int WM = BM / 2, WN = BN / 2, TI = WM / 16, TJ = WN / 16;
+  __shared__ __align__(16) char smem[NST * STAGE_BYTES];
+
+  const ConvGeom& g = a.g;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wm = wave >> 1, wn = wave & 1;
+  const int t = xcd_tile(blockIdx.x, a.tiles_m * a.tiles_n);
+  const int m0 = (t % a.tiles_m) * BM, n0 = (t / a.tiles_m) * BN;
+  const int rs = m0 / g.C, c0 = m0 - rs * g.C;
+  const int tr = rs / g.S, ts = rs - tr * g.S;
+  const int M = g.N * g.P * g.Q, PQ = g.P * g.Q;
+  const int mb = blockIdx.y * a.m_per_split;
+  const int me = min(M, mb + a.m_per_split);
+  const int ns = me > mb ? (me - mb + 63) / 64 : 0;
+
+  // A rows of this lane advance by 64 pixels per stage: (n, p, q) is stepped
+  int an[LA], ap[LA], aq[LA], am[LA];
+  const int dq = 64 % g.Q, dp = (64 / g.Q) % g.P, dn = 64 / PQ;
+#pragma unroll
+  for (int j = 0; j < LA; ++j) {
+    const int pr = (wave + 4 * j) * RA + lane / UA;
+    am[j] = mb + pr;
+    const int m = am[j] < M ? am[j] : 0;
+    an[j] = m / PQ;
+    const int rem = m - an[j] * PQ;
+    ap[j] = rem / g.Q;
+    aq[j] = rem - ap[j] * g.Q;
+  }
+  auto issue = [&](int st, char* slot) {
+#pragma unroll
+    for (int j = 0; j < LPS; ++j) {
+      const int ins = wave + 4 * j;
+      if (j < LA) {
+        const int pr = ins * RA + lane / UA, sl = lane % UA;
+        const int u = 2 * ((sl >> 1) ^ (pr % SA)) + (sl & 1);
+        const int h = ap[j] * g.stride - g.pad + tr, w = aq[j] * g.stride - g.pad + ts;
+        const bool in = am[j] < me && (unsigned)h < (unsigned)g.H && (unsigned)w < (unsigned)g.W;
+        const bf16* src = a.x + (((long long)an[j] * g.H + h) * g.W + w) * g.C + c0 + u * 8;
+        dma16(in ? (const void*)src : (const void*)g_zero_unit,
+              reinterpret_cast<uint4*>(slot + ins * 1024));
+        am[j] += 64;
+        aq[j] += dq;
+        int cy = aq[j] >= g.Q;
+        aq[j] -= cy ? g.Q : 0;
+        ap[j] += dp + cy;
+        cy = ap[j] >= g.P;
+        ap[j] -= cy ? g.P : 0;
+        an[j] += dn + cy;
+      } else {
+        const int ib = ins - IA;
+        const int pr = ib * RB + lane / UB, sl = lane % UB;
+        const int u = 2 * ((sl >> 1) ^ (pr % SB)) + (sl & 1);
+        const int m = mb + st * 64 + pr;
+        const void* src = m < me ? (const void*)(a.dy + (long long)m * g.K + n0 + u * 8)
+                                 : (const void*)g_zero_unit;
+        dma16(src, reinterpret_cast<uint4*>(slot + 64 * BM * 2 + ib * 1024));
+      }
+    }
+  };
+
+  f32x4 acc[TI][TJ];
+#pragma unroll
+  for (int i = 0; i < TI; ++i)
+#pragma unroll
+    for (int j = 0; j < TJ; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  if (ns > 0) issue(0, smem);
+  const int gq = lane >> 4, jr = (lane & 15) >> 2, qd = lane & 3;
+  int slot = 0;
+  for (int st = 0; st < ns; ++st) {
+    wait_vmcnt<0>();
+    stage_barrier();
+    if (st + 1 < ns) issue(st + 1, smem + (slot ^ 1) * STAGE_BYTES);
+    const char* As = smem + slot * STAGE_BYTES;
+    const char* Bs = As + 64 * BM * 2;
+#pragma unroll
+    for (int kf = 0; kf < 2; ++kf) {
+      uint4 fa[TI], fb[TJ];
+#pragma unroll
+      for (int half = 0; half < 2; ++half) {
+        const int pr = kf * 32 + gq * 8 + half * 4 + jr;
+#pragma unroll
+        for (int i = 0; i < TI; ++i) {
+          const int ch = wm * WM + i * 16 + 4 * qd;
+          const uint2 v = lds_read_tr16(As + pr * (BM * 2) + (((ch >> 4) ^ (pr % SA)) * 32) +
+                                        (ch & 15) * 2);
+          if (half == 0) { fa[i].x = v.x; fa[i].y = v.y; } else { fa[i].z = v.x; fa[i].w = v.y; }
+        }
+#pragma unroll
+        for (int j = 0; j < TJ; ++j) {
+          const int ch = wn * WN + j * 16 + 4 * qd;
+          const uint2 v = lds_read_tr16(Bs + pr * (BN * 2) + (((ch >> 4) ^ (pr % SB)) * 32) +
+                                        (ch & 15) * 2);
+          if (half == 0) { fb[j].x = v.x; fb[j].y = v.y; } else { fb[j].z = v.x; fb[j].w = v.y; }
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < TI; ++i)
+#pragma unroll
+        for (int j = 0; j < TJ; ++j) mma_unit(acc[i][j], fa[i], fb[j], (bf16*)nullptr);
+    }
+    slot ^= 1;
+  }
+
+  const int RSC = g.R * g.S * g.C;
+  const int lr = lane & 15, lg = lane >> 4;
+#pragma unroll
+  for (int i = 0; i < TI; ++i)
+#pragma unroll
+    for (int j = 0; j < TJ; ++j) {
+      const int row = m0 + wm * WM + i * 16 + 4 * lg, col = n0 + wn * WN + j * 16 + lr;
+      float* dst = a.out + ((long long)blockIdx.y * g.K + col) * RSC + row;
+      *reinterpret_cast<float4*>(dst) =
+          make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+    }
+}
+
 // -------------------------------------------------------------- launching
 thread_local KernelTimer* t_timer = nullptr;
 
@@ -1201,9 +1357,59 @@ size_t conv_split_workspace_floats(int dt, const ConvGeom& g, bool dgrad) {
 }
 
 namespace {
+// Direct-to-LDS weight-gradient plan: 64 x 128 tiles (64 x 64 when K is not a
+// multiple of 128), the pixel reduction split until ~576 blocks, keeping
+// >= 2 stages of 64 pixels per split.
+struct WgDmaPlan {
+  int bn, splits, mps;
+};
+bool wgrad_dma_ok(int dt, const ConvGeom& g) { return dt == DT_BF16 && g.C % 64 == 0 && g.K % 64 == 0; }
+WgDmaPlan plan_wgrad_dma(const ConvGeom& g) {
+  const long long M = (long long)g.N * g.P * g.Q;
+  const int bn = g.K % 128 == 0 ? 128 : 64;
+  const long long tiles = (long long)(g.R * g.S * g.C / 64) * (g.K / bn);
+  const long long stages = std::max(1LL, cdivl(M, 64));
+  long long s = std::min(cdivl(576, tiles), std::max(1LL, stages / 2));
+  s = std::max(1LL, std::min(s, 64LL));
+  const long long mps = cdivl(cdivl(M, s), 64) * 64;
+  return {bn, (int)cdivl(M, mps), (int)mps};
+}
 struct WPlan {
   int bm, bn, splits;
 };
+
+hipError_t conv_wgrad_dma(const ConvGeom& g, const void* x, const void* dy, float* partials,
+                          float* dw, hipStream_t stream) {
+  const WgDmaPlan p = plan_wgrad_dma(g);
+  WgDmaArgs a{g, (const bf16*)x, (const bf16*)dy, p.splits > 1 ? partials : dw, p.mps, 0, 0};
+  a.tiles_m = g.R * g.S * g.C / 64;
+  a.tiles_n = g.K / p.bn;
+  const Cost cost = conv_cost(g, g.C, sizeof(bf16), true);
+  KernelTimer* t = t_timer;
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  if (t) {
+    e0 = t->take();
+    e1 = t->take();
+    EKYA_HIP(hipEventRecord(e0, stream));
+  }
+  const dim3 grid(a.tiles_m * a.tiles_n, p.splits);
+  if (p.bn == 128)
+    hipLaunchKernelGGL((wgrad_dma_kernel<64, 128>), grid, dim3(NT), 0, stream, a);
+  else
+    hipLaunchKernelGGL((wgrad_dma_kernel<64, 64>), grid, dim3(NT), 0, stream, a);
+  hipError_t e = hipGetLastError();
+  if (t && e == hipSuccess) {
+    EKYA_HIP(hipEventRecord(e1, stream));
+    t->recs.push_back({std::string("conv_wgrad<bf16,64,") + std::to_string(p.bn) + ",dma>",
+                       cost.flops, cost.bytes, e0, e1});
+  }
+  if (e != hipSuccess || p.splits == 1) return e;
+  const long long n = (long long)g.K * g.R * g.S * g.C;
+  const int blocks = (int)std::min<long long>(cdivl(n, 256), 4096);
+  hipLaunchKernelGGL(wgrad_reduce_kernel, dim3(blocks), dim3(256), 0, stream, partials, p.splits,
+                     g.K, g.R * g.S, g.C, g.C, dw);
+  return hipGetLastError();
+}
 WPlan plan_wgrad(int dt, const ConvGeom& g) {
   // 128-row tiles, split the pixel reduction until there are ~1024 blocks
   // (>= 4 stages per split): measured faster than fewer, longer blocks.
@@ -1217,9 +1423,15 @@ WPlan plan_wgrad(int dt, const ConvGeom& g) {
 }
 }  // namespace
 
-int conv_wgrad_splits(int dt, const ConvGeom& g) { return plan_wgrad(dt, g).splits; }
+int conv_wgrad_splits(int dt, const ConvGeom& g) {
+  return wgrad_dma_ok(dt, g) ? plan_wgrad_dma(g).splits : plan_wgrad(dt, g).splits;
+}
 
 size_t conv_wgrad_workspace_floats(int dt, const ConvGeom& g) {
+  if (wgrad_dma_ok(dt, g)) {
+    const WgDmaPlan q = plan_wgrad_dma(g);
+    return q.splits > 1 ? (size_t)q.splits * g.K * g.R * g.S * g.C : 0;
+  }
   const WPlan p = plan_wgrad(dt, g);
   return (size_t)p.splits * g.K * g.R * g.S * g.C;
 }
@@ -1240,6 +1452,7 @@ hipError_t conv_dgrad(int dt, const ConvGeom& g, const void* dy, const void* wt,
 
 hipError_t conv_wgrad(int dt, const ConvGeom& g, const void* x, const void* dy, float* partials,
                       float* dw, int C0, hipStream_t stream) {
+  if (wgrad_dma_ok(dt, g) && C0 == g.C) return conv_wgrad_dma(g, x, dy, partials, dw, stream);
   const WPlan p = plan_wgrad(dt, g);
   const long long M = (long long)g.N * g.P * g.Q;
   const int stage = wgrad_stage_m(dt);

@@ -27,6 +27,18 @@ template <typename T> __device__ __forceinline__ uint4 f_to_unit(const float* v)
   return x.u;
 }
 
+// E per-channel floats p[c0 .. c0+E) (c0 a multiple of E) as 16-byte loads.
+template <int E> __device__ __forceinline__ void chan_load(const float* p, int c0, float (&v)[E]) {
+#pragma unroll
+  for (int i = 0; i < E; i += 4) {
+    const float4 t = *reinterpret_cast<const float4*>(p + c0 + i);
+    v[i] = t.x;
+    v[i + 1] = t.y;
+    v[i + 2] = t.z;
+    v[i + 3] = t.w;
+  }
+}
+
 inline int grid_for(long long n, int per_block = 256, int cap = 8192) {
   long long b = cdivl(n, per_block);
   if (b < 1) b = 1;
@@ -35,8 +47,8 @@ inline int grid_for(long long n, int per_block = 256, int cap = 8192) {
 
 // Chunking of the M rows for per-channel reductions.
 inline int bn_chunks(long long M) {
-  long long c = cdivl(M, 64);
-  if (c > 1024) c = 1024;
+  long long c = cdivl(M, 16);
+  if (c > 2048) c = 2048;
   if (c < 1) c = 1;
   return (int)c;
 }
@@ -148,13 +160,16 @@ __global__ void bn_apply_kernel(const T* z, long long units, int C, const float*
   for (long long u = blockIdx.x * (long long)blockDim.x + threadIdx.x; u < units;
        u += (long long)gridDim.x * blockDim.x) {
     const int c0 = (int)((u * E) % C);
-    float v[E], r[E];
+    float v[E], r[E], mu[E], sc[E], be[E];
     unit_to_f<T>(reinterpret_cast<const uint4*>(z)[u], v);
     if (res) unit_to_f<T>(reinterpret_cast<const uint4*>(res)[u], r);
+    chan_load<E>(mean, c0, mu);
+    chan_load<E>(scale, c0, sc);
+    chan_load<E>(beta, c0, be);
 #pragma unroll
     for (int i = 0; i < E; ++i) {
       // (z - mean) * scale + beta: no cancellation when invstd is large
-      float t = (v[i] - mean[c0 + i]) * scale[c0 + i] + beta[c0 + i];
+      float t = (v[i] - mu[i]) * sc[i] + be[i];
       if (res) t += r[i];
       if (relu) t = relu_nan(t);
       v[i] = t;
@@ -267,12 +282,13 @@ __global__ void bn_bwd_apply(const T* dy, const T* y, const T* z, long long unit
       for (int i = 0; i < E; ++i) g[i] = yy[i] > 0.f ? g[i] : 0.f;
     }
     if (g_out) reinterpret_cast<uint4*>(g_out)[u] = f_to_unit<T>(g);
-    float o[E];
+    float o[E], ca[E], cb[E], cc[E], mu[E];
+    chan_load<E>(coef, c0, ca);
+    chan_load<E>(coef + C, c0, cb);
+    chan_load<E>(coef + 2 * C, c0, cc);
+    chan_load<E>(mean, c0, mu);
 #pragma unroll
-    for (int i = 0; i < E; ++i) {
-      const int c = c0 + i;
-      o[i] = coef[c] * g[i] + coef[C + c] + coef[2 * C + c] * (zz[i] - mean[c]);
-    }
+    for (int i = 0; i < E; ++i) o[i] = ca[i] * g[i] + cb[i] + cc[i] * (zz[i] - mu[i]);
     reinterpret_cast<uint4*>(dz)[u] = f_to_unit<T>(o);
   }
 }
@@ -607,27 +623,42 @@ __global__ void cast_kernel(const float* src, long long n, T* dst) {
 // tab row: src_off, K, R, S, C0, Cp, krsc_off, crsk_off.  Both copies are
 // written in their own element order (coalesced); the [C][R][S][K] copy reads
 // the fp32 master with a stride.
+// One 64 x 64 tile (output channels k x input channels c) of one tap (r, s)
+// of a conv per iteration: the fp32 master tile is read once along c, the
+// [K][R][S][Cp] copy written along c and, through LDS, the [C][R][S][K] copy
+// along k -- every global access coalesced.
+// tab row: master offset, K, R, S, C0, Cp, krsc offset, crsk offset (-1: none)
 template <typename T>
-__global__ void pack_conv_kernel(const float* master, const long long* tab, T* shadow) {
+__global__ __launch_bounds__(256) void pack_conv_kernel(const float* master, const long long* tab,
+                                                        T* shadow) {
   const long long* t = tab + 8 * blockIdx.y;
-  const int K = (int)t[1], R = (int)t[2], S = (int)t[3], C0 = (int)t[4], Cp = (int)t[5];
+  const int K = (int)t[1], RS = (int)(t[2] * t[3]), C0 = (int)t[4], Cp = (int)t[5];
   const float* src = master + t[0];
   T* krsc = shadow + t[6];
-  const long long n = (long long)K * R * S * Cp;
-  for (long long i = blockIdx.x * (long long)blockDim.x + threadIdx.x; i < n;
-       i += (long long)gridDim.x * blockDim.x) {
-    const int c = (int)(i % Cp);
-    krsc[i] = from_f<T>(c < C0 ? src[(i / Cp) * C0 + c] : 0.f);
-  }
-  if (t[7] < 0) return;
-  T* crsk = shadow + t[7];
-  const long long n2 = (long long)C0 * R * S * K;
-  for (long long i = blockIdx.x * (long long)blockDim.x + threadIdx.x; i < n2;
-       i += (long long)gridDim.x * blockDim.x) {
-    const int k = (int)(i % K);
-    const long long crs = i / K;  // (c * R + r) * S + s
-    const int s = (int)(crs % S), r = (int)((crs / S) % R), c = (int)(crs / ((long long)R * S));
-    crsk[i] = from_f<T>(src[(((long long)k * R + r) * S + s) * C0 + c]);
+  T* crsk = t[7] >= 0 ? shadow + t[7] : nullptr;
+  const int tk = cdiv(K, 64), tc = cdiv(Cp, 64);
+  const int ntiles = RS * tk * tc;
+  const int cc = threadIdx.x & 63, kr = threadIdx.x >> 6;
+  __shared__ float tile[64][65];
+  for (int bt = blockIdx.x; bt < ntiles; bt += gridDim.x) {
+    const int rs = bt / (tk * tc), rem = bt % (tk * tc);
+    const int k0 = (rem / tc) * 64, c0 = (rem % tc) * 64;
+#pragma unroll 4
+    for (int i = 0; i < 16; ++i) {
+      const int k = k0 + kr + 4 * i, c = c0 + cc;
+      const float v = (k < K && c < C0) ? src[((long long)k * RS + rs) * C0 + c] : 0.f;
+      tile[kr + 4 * i][cc] = v;
+      if (k < K && c < Cp) krsc[((long long)k * RS + rs) * Cp + c] = from_f<T>(v);
+    }
+    if (crsk) {
+      __syncthreads();
+#pragma unroll 4
+      for (int i = 0; i < 16; ++i) {
+        const int c = c0 + kr + 4 * i, k = k0 + cc;
+        if (c < C0 && k < K) crsk[((long long)c * RS + rs) * K + k] = from_f<T>(tile[cc][kr + 4 * i]);
+      }
+    }
+    __syncthreads();
   }
 }
 
