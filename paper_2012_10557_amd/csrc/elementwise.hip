@@ -103,16 +103,19 @@ __global__ __launch_bounds__(256) void bn_stats_partial(const T* z, long long M,
 }
 
 // Fixed-order sum over chunks of the two partial rows of channel c: a block
-// handles 64 channels with 4 threads each (thread slice k sums chunks
-// k, k+4, ...), and the four slice sums are added in slice order.
+// handles 16 channels with 16 threads each (thread slice k sums chunks k,
+// k+16, ...; 16 consecutive channels per load, so each read is 64 bytes), and
+// the 16 slice sums are added in slice order in double.  Returns true for the
+// one thread per channel that holds the totals.
+constexpr int FIN_CH = 16;
 __device__ __forceinline__ bool chunk_sums(const float* part, int nchunks, int C, double& a,
                                            double& b) {
-  __shared__ float sa[4][64], sb[4][64];
-  const int lc = threadIdx.x & 63, slice = threadIdx.x >> 6;
-  const int c = blockIdx.x * 64 + lc;
+  __shared__ float sa[16][FIN_CH], sb[16][FIN_CH];
+  const int lc = threadIdx.x & (FIN_CH - 1), slice = threadIdx.x / FIN_CH;
+  const int c = blockIdx.x * FIN_CH + lc;
   float x = 0.f, y = 0.f;
   if (c < C)
-    for (int k = slice; k < nchunks; k += 4) {
+    for (int k = slice; k < nchunks; k += 16) {
       x += part[(long long)k * 2 * C + c];
       y += part[(long long)k * 2 * C + C + c];
     }
@@ -120,8 +123,13 @@ __device__ __forceinline__ bool chunk_sums(const float* part, int nchunks, int C
   sb[slice][lc] = y;
   __syncthreads();
   if (slice != 0 || c >= C) return false;
-  a = (double)sa[0][lc] + (double)sa[1][lc] + (double)sa[2][lc] + (double)sa[3][lc];
-  b = (double)sb[0][lc] + (double)sb[1][lc] + (double)sb[2][lc] + (double)sb[3][lc];
+  a = 0.0;
+  b = 0.0;
+#pragma unroll
+  for (int k = 0; k < 16; ++k) {
+    a += (double)sa[k][lc];
+    b += (double)sb[k][lc];
+  }
   return true;
 }
 
@@ -133,7 +141,7 @@ __global__ __launch_bounds__(256) void bn_stats_final(const T* z, const float* p
                                                       float* shift) {
   double a, b;
   if (!chunk_sums(part, nchunks, C, a, b)) return;
-  const int c = blockIdx.x * 64 + (threadIdx.x & 63);
+  const int c = blockIdx.x * FIN_CH + (threadIdx.x & (FIN_CH - 1));
   const double Kc = (double)to_f(z[c]);
   const double d = a / (double)M;
   double var = b / (double)M - d * d;
@@ -253,7 +261,7 @@ __global__ __launch_bounds__(256) void bn_bwd_final(const float* part, int nchun
                                                     float* dgamma, float* dbeta, float* coef) {
   double sg, sgx;
   if (!chunk_sums(part, nchunks, C, sg, sgx)) return;
-  const int c = blockIdx.x * 64 + (threadIdx.x & 63);
+  const int c = blockIdx.x * FIN_CH + (threadIdx.x & (FIN_CH - 1));
   const float is = invstd[c];
   const float db = (float)sg;
   const float dg = (float)(sgx * (double)is);
@@ -713,7 +721,7 @@ hipError_t bn_train_stats(int dt, const void* z, long long M, int C, const float
     using T = std::remove_pointer_t<decltype(tp)>;
     hipLaunchKernelGGL(bn_stats_partial<T>, dim3(nch), dim3(256), 0, stream, (const T*)z, M, C,
                        rpc, partials);
-    hipLaunchKernelGGL(bn_stats_final<T>, dim3(cdiv(C, 64)), dim3(256), 0, stream, (const T*)z,
+    hipLaunchKernelGGL(bn_stats_final<T>, dim3(cdiv(C, FIN_CH)), dim3(256), 0, stream, (const T*)z,
                        partials, nch, M, C, gamma, beta, rm, rv, mean, invstd, scale, shift);
   });
 }
@@ -749,7 +757,7 @@ hipError_t bn_backward(int dt, const void* dy, const void* y, const void* z, lon
     using T = std::remove_pointer_t<decltype(tp)>;
     hipLaunchKernelGGL(bn_bwd_partial<T>, dim3(nch), dim3(256), 0, stream, (const T*)dy,
                        (const T*)y, (const T*)z, M, C, rpc, mean, partials);
-    hipLaunchKernelGGL(bn_bwd_final, dim3(cdiv(C, 64)), dim3(256), 0, stream, partials, nch, M, C,
+    hipLaunchKernelGGL(bn_bwd_final, dim3(cdiv(C, FIN_CH)), dim3(256), 0, stream, partials, nch, M, C,
                        gamma, invstd, dgamma, dbeta, coef);
     hipLaunchKernelGGL(bn_bwd_apply<T>, dim3(grid_for(units)), dim3(256), 0, stream, (const T*)dy,
                        (const T*)y, (const T*)z, units, C, mean, coef, (T*)dz, (T*)g_out);
