@@ -40,6 +40,31 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
+def kernel_source_digest():
+    """sha256 of the sources that define the GEMM kernels."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("conv.hip", "common.hpp", "kernels.hpp"):
+        with open(os.path.join(ROOT, "paper_2012_10557_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(kernel):
+    """HBM bytes per launch of `kernel` from the rocprofv3 FETCH_SIZE / WRITE_SIZE
+    passes recorded in profiles/traffic.json (scaled by a plain copy's
+    counts), or None if they were taken on another kernel or other sources."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    try:
+        with open(path) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("kernel") != kernel or t.get("kernel_source_sha256") != kernel_source_digest():
+        return None
+    return int(t["fetch_bytes_per_launch"] + t["write_bytes_per_launch"])
+
+
 def cpu_baseline(sample_frames=200, sample_heldout=40):
     """The oracle, as it stands, on a bounded sample of the same workload:
     a 200-frame window at 30% (60 training frames), 40 held-out frames,
@@ -76,6 +101,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--infer-frames", type=int, default=2000)
+    ap.add_argument("--no-infer", action="store_true", help="skip the inference img/s measurement")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -139,7 +165,9 @@ def main():
     gemm_ms = sum(s["total_ms"] for s in stats)
     gemm_flops = sum(s["flops"] for s in stats)
     roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
-                "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                "traffic": measured_traffic(dom["name"]),
+                "algorithmic_bytes_per_launch": round(dom["bytes"] / dom["launches"]),
                 "kernel": dom["name"], "launches_per_step": dom["launches"],
                 "avg_launch_us": round(avg_ms * 1e3, 2),
                 "flops_per_launch": dom["flops"] / dom["launches"],
@@ -150,7 +178,7 @@ def main():
     infer = {}
     nf = min(args.infer_frames, frames.shape[0])
     sub = frames[:nf].contiguous()
-    for r in (224, 160, 112):
+    for r in (() if args.no_infer else (224, 160, 112)):
         lab = binding.ekya_infer(ctx, w0, sub, r)
         torch.cuda.synchronize()
         ti = time.perf_counter()
