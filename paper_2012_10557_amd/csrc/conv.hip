@@ -1059,6 +1059,125 @@ __global__ __launch_bounds__(NT) void wgrad_dma_kernel(WgDmaArgs a) {
     }
 }
 
+// ------------------------------------------------------------- image stem
+// bf16 7x7 / stride 2 / pad 3 convolution of 3-channel frames (stored with
+// channels padded to 8) into 64 channels, for output rows up to 112 wide.
+// A block of 8 waves computes 8 output rows (one per wave) x the full row
+// width x all 64 channels.  The 21 input rows it needs (8 x 2 + 5)
+// are staged in LDS once, keeping channels 0..3 of each pixel (8 bytes;
+// channel 3 is the zero pad), and the filter as [64][7][8 taps][4] with the
+// 8th tap zero.  One MFMA k-step covers one filter row r: 8 taps x 4 channels
+// = 32 products, so a lane's 16-byte operand is 2 adjacent taps x 4 channels
+// -- 2 adjacent input pixels in the staged row, contiguous -- and 7 k-steps
+// cover the filter (224 products per output, against 392 with 8 stored
+// channels).  Global reads are batched 8 per thread before their LDS writes.
+constexpr int STEM_QMAX = 112, STEM_TQ = 7, STEM_PATCH_W = 2 * STEM_TQ * 16 + 6;
+constexpr int STEM_ROWS = 8, STEM_IN_ROWS = 2 * STEM_ROWS + 5;
+constexpr int STEM_WROW = 232;  // 224 filter entries per channel + 8 (bank spread)
+
+constexpr int STEM_NT = 512;
+__global__ __launch_bounds__(STEM_NT) void stem_kernel(const bf16* x, const bf16* wk, bf16* y,
+                                                  ConvEpilogue epi, int N, int H, int W, int P,
+                                                  int Q) {
+  __shared__ __align__(16) uint2 patch[STEM_IN_ROWS * STEM_PATCH_W];  // 4 channels per pixel
+  __shared__ __align__(16) bf16 wl[64 * STEM_WROW];
+  const int blocks_per_img = cdiv(P, STEM_ROWS);
+  const int n = blockIdx.x / blocks_per_img, p0 = (blockIdx.x % blocks_per_img) * STEM_ROWS;
+  const int tq = cdiv(Q, 16);
+  const int pw = 2 * tq * 16 + 6;
+  // filter: wk is [64][7][7][8]; keep channels 0..3, tap 7 zero
+  for (int i0 = threadIdx.x; i0 < 64 * 7 * 8; i0 += 8 * STEM_NT) {
+    uint2 v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int i = i0 + u * STEM_NT, k = i / 56, r = (i % 56) / 8, sp = i % 8;
+      v[u] = (i < 64 * 56 && sp < 7) ? *reinterpret_cast<const uint2*>(wk + ((k * 7 + r) * 7 + sp) * 8)
+                                     : make_uint2(0u, 0u);
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int i = i0 + u * STEM_NT;
+      if (i < 64 * 56)
+        *reinterpret_cast<uint2*>(wl + (i / 56) * STEM_WROW + ((i % 56) / 8) * 32 + (i % 8) * 4) = v[u];
+    }
+  }
+  // input rows 2 p0 - 3 .. 2 p0 + 17, columns -3 .. pw - 4 (zero outside the frame)
+  const bf16* img = x + (long long)n * H * W * 8;
+  const int total = STEM_IN_ROWS * pw;
+  for (int i0 = threadIdx.x; i0 < total; i0 += 8 * STEM_NT) {
+    uint2 v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int i = i0 + u * STEM_NT, pr = i / pw, pc = i % pw;
+      const int h = 2 * p0 - 3 + pr, w = pc - 3;
+      v[u] = (i < total && (unsigned)h < (unsigned)H && (unsigned)w < (unsigned)W)
+                 ? *reinterpret_cast<const uint2*>(img + ((long long)h * W + w) * 8)
+                 : make_uint2(0u, 0u);
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int i = i0 + u * STEM_NT;
+      if (i < total) patch[(i / pw) * STEM_PATCH_W + i % pw] = v[u];
+    }
+  }
+  __syncthreads();
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lr = lane & 15, kc = lane >> 4;
+  {
+    const int lp = wave;  // output row within the block
+    const int p = p0 + lp;
+    if (p >= P) return;
+    f32x4 acc[4][STEM_TQ];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int t = 0; t < STEM_TQ; ++t) acc[i][t] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll 1
+    for (int r = 0; r < 7; ++r) {
+      uint4 fa[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        fa[i] = *reinterpret_cast<const uint4*>(wl + (i * 16 + lr) * STEM_WROW + r * 32 + kc * 8);
+      const uint2* prow = patch + (2 * lp + r) * STEM_PATCH_W;
+#pragma unroll
+      for (int t = 0; t < STEM_TQ; ++t) {
+        if (t < tq) {
+          // output column q = 16 t + lr reads input columns 2 q - 3 + 2 kc, +1
+          const uint4 fb = *reinterpret_cast<const uint4*>(prow + 2 * (t * 16 + lr) + 2 * kc);
+#pragma unroll
+          for (int i = 0; i < 4; ++i) mma_unit(acc[i][t], fa[i], fb, (bf16*)nullptr);
+        }
+      }
+    }
+    const int lg = lane >> 4;
+#pragma unroll
+    for (int t = 0; t < STEM_TQ; ++t) {
+      const int q = t * 16 + lr;
+      if (t >= tq || q >= Q) continue;
+      bf16* dst = y + (((long long)n * P + p) * Q + q) * 64;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int k = i * 16 + 4 * lg;
+        float v[4] = {acc[i][t][0], acc[i][t][1], acc[i][t][2], acc[i][t][3]};
+        if (epi.scale) {
+          const float4 s4 = *reinterpret_cast<const float4*>(epi.scale + k);
+          v[0] *= s4.x; v[1] *= s4.y; v[2] *= s4.z; v[3] *= s4.w;
+        }
+        if (epi.shift) {
+          const float4 b4 = *reinterpret_cast<const float4*>(epi.shift + k);
+          v[0] += b4.x; v[1] += b4.y; v[2] += b4.z; v[3] += b4.w;
+        }
+        if (epi.relu) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] = relu_nan(v[e]);
+        }
+        store4<bf16>(dst + k, v);
+      }
+    }
+  }
+}
+
 // -------------------------------------------------------------- launching
 thread_local KernelTimer* t_timer = nullptr;
 
@@ -1266,6 +1385,25 @@ hipError_t conv_fwd_t(const ConvGeom& g, const void* x, const void* w, void* y,
                       const ConvEpilogue& epi, float* ws, size_t ws_floats, hipStream_t stream) {
   constexpr int E = Elt<T>::E;
   if (sizeof(T) == 2 && g.C % 64 == 0) return conv_fwd_dma(g, x, w, y, epi, ws, ws_floats, stream);
+  if (sizeof(T) == 2 && g.C == 8 && g.C0 == 3 && g.K == 64 && g.R == 7 && g.S == 7 && g.stride == 2 &&
+      g.pad == 3 && g.Q <= STEM_QMAX && g.N > 0) {
+    const Cost cost = conv_cost(g, 3, sizeof(bf16), false);
+    KernelTimer* t = t_timer;
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    if (t) {
+      e0 = t->take();
+      e1 = t->take();
+      EKYA_HIP(hipEventRecord(e0, stream));
+    }
+    hipLaunchKernelGGL(stem_kernel, dim3(g.N * cdiv(g.P, STEM_ROWS)), dim3(STEM_NT), 0, stream, (const bf16*)x,
+                       (const bf16*)w, (bf16*)y, epi, g.N, g.H, g.W, g.P, g.Q);
+    hipError_t e = hipGetLastError();
+    if (t && e == hipSuccess) {
+      EKYA_HIP(hipEventRecord(e1, stream));
+      t->recs.push_back({"conv_fwd<bf16,stem7x7>", cost.flops, cost.bytes, e0, e1});
+    }
+    return e;
+  }
   const bool ut = g.C % (KU_MAIN * E) == 0;
   const int ns = cdiv(g.R * g.S * g.C, KU_MAIN * E);
   const long long npix = (long long)g.N * g.P * g.Q;

@@ -17,6 +17,7 @@ PRECS = ["f32", "bf16"]
 CONV_CASES = [
     (2, 64, 64, 3, 64, 7, 2, 3),      # stem
     (1, 37, 41, 3, 64, 7, 2, 3),      # stem, odd size
+    (1, 224, 224, 3, 64, 7, 2, 3),    # stem at full width (112 output columns)
     (2, 16, 16, 64, 64, 3, 1, 1),     # layer1
     (3, 13, 11, 64, 64, 3, 1, 1),     # layer1, ragged
     (2, 16, 16, 64, 128, 3, 2, 1),    # layer2.0.conv1
