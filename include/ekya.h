@@ -176,7 +176,9 @@ ekya_status ekya_infer(ekya_ctx* ctx, const float* weights, const void* frames, 
  * broken down by GEMM kernel.  ekya_set_kernel_timing(ctx, 1) clears the
  * statistics and makes later ekya_retrain / ekya_infer calls on this context
  * bracket every convolution GEMM launch with two HIP events on the launch's
- * stream (0 turns it off; statistics are kept).  ekya_kernel_timing reads
+ * stream (0 turns it off; statistics are kept).  While timing is on, work
+ * the library would otherwise overlap on a second stream (weight gradients)
+ * runs on the job's stream, so each kernel is timed alone.  ekya_kernel_timing reads
  * entry `index` (0-based; waits for the recorded launches to finish): kernel
  * name into name (NUL-terminated, truncated to name_cap), launch count, summed
  * event time in ms, summed algorithmic flops (2*N*P*Q*K*R*S*C) and bytes

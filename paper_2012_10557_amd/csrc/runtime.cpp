@@ -291,9 +291,21 @@ struct TrainJob {
   uint8_t* stem_arg = nullptr;
   std::vector<BlockAct> acts;  // per block of the network (only trainable ones set)
   void* g[6] = {nullptr};      // gradient scratch
+  // weight gradients run on st2 while st continues down the data-gradient
+  // chain; dz of conv2 / conv1 / downsample per block parity (double
+  // buffered so st2 may lag one block), st2's own split scratch, and events
+  hipStream_t st2 = nullptr;
+  void* gz2[2] = {nullptr}, *gz1[2] = {nullptr}, *gzd[2] = {nullptr};
+  float* ws2 = nullptr;
+  size_t ws2_floats = 0;
+  static constexpr int kForks = 40;
+  hipEvent_t fork[kForks] = {nullptr};
+  hipEvent_t joined[kForks] = {nullptr};
   float *pooled = nullptr, *logits = nullptr, *dz = nullptr, *dpooled = nullptr;
-  float* ws = nullptr;         // split-K / BatchNorm partials
+  float* ws = nullptr;         // split-K partials
   size_t ws_floats = 0;
+  float* bn_ws = nullptr;      // BatchNorm partials
+  size_t bn_ws_floats = 0;
   float* ce_out = nullptr;     // n_steps x 3
   int32_t* hcount = nullptr;   // epochs
   EvalBufs eval;
@@ -318,6 +330,19 @@ static size_t ws_floats(const TrainJob& j) {
     }
   }
   return std::max<size_t>(m, 16);
+}
+
+// Split scratch of the weight gradients (their own, used on st2).
+static size_t wgrad_ws_floats(const TrainJob& j) {
+  const Net& net = *j.net;
+  size_t m = 16;
+  for (size_t i = 0; i < net.conv.size(); ++i) {
+    const ConvL& c = net.conv[i];
+    if (c.stage < j.lowest || c.stage > 4) continue;
+    for (int n = 1; n <= j.B; ++n)
+      m = std::max(m, conv_wgrad_workspace_floats(j.dt, conv_geom(net, j.geo, (int)i, n)));
+  }
+  return m;
 }
 
 static long long train_max_elems(const TrainJob& j) {
@@ -366,14 +391,32 @@ static void plan_job(Arena& a, TrainJob& j) {
     }
   }
   const long long gmax = train_max_elems(j) * j.B;
-  if (j.lowest <= 4)
+  if (j.lowest <= 4) {
     for (int i = 0; i < 6; ++i) j.g[i] = a.take_bytes(gmax * es);
+    for (int p = 0; p < 2; ++p) {
+      j.gz2[p] = a.take_bytes(gmax * es);
+      j.gz1[p] = a.take_bytes(gmax * es);
+      j.gzd[p] = a.take_bytes(gmax * es);
+    }
+    j.ws2_floats = wgrad_ws_floats(j);
+    j.ws2 = a.take<float>(j.ws2_floats);
+  }
   j.pooled = a.take<float>((size_t)j.B * 512);
   j.dpooled = a.take<float>((size_t)j.B * 512);
   j.logits = a.take<float>((size_t)j.B * net.n_classes);
   j.dz = a.take<float>((size_t)j.B * net.n_classes);
   j.ws_floats = ws_floats(j);
   j.ws = a.take<float>(j.ws_floats);
+  j.bn_ws_floats = 16;
+  for (size_t i = 0; i < net.conv.size(); ++i) {
+    const ConvL& c = net.conv[i];
+    if (c.stage < j.lowest || c.stage > 4) continue;
+    for (int n = 1; n <= j.B; ++n) {
+      const ConvGeom cg = conv_geom(net, j.geo, (int)i, n);
+      j.bn_ws_floats = std::max(j.bn_ws_floats, bn_partials_floats((long long)n * cg.P * cg.Q, c.cout));
+    }
+  }
+  j.bn_ws = a.take<float>(j.bn_ws_floats);
   j.ce_out = a.take<float>((size_t)j.n_steps * 3);
   j.hcount = a.take<int32_t>(j.epochs);
   j.eval_cap = std::max(1, std::min(j.n_h, 512));
@@ -392,7 +435,7 @@ static hipError_t train_forward(TrainJob& j, int nb) {
     const BnL& b = net.bn[bi];
     return bn_train_stats(dt, z, M, b.C, j.master + b.g, j.master + b.b, j.master + b.rm,
                           j.master + b.rv, bnp(j.bn_mean, b), bnp(j.bn_invstd, b),
-                          bnp(j.bn_scale, b), bnp(j.bn_shift, b), j.ws, st);
+                          bnp(j.bn_scale, b), bnp(j.bn_shift, b), j.bn_ws, st);
   };
   auto mu = [&](int bi) { return bnp(j.bn_mean, net.bn[bi]); };
   auto sc = [&](int bi) { return bnp(j.bn_scale, net.bn[bi]); };
@@ -464,31 +507,50 @@ static hipError_t train_backward(TrainJob& j, int nb) {
   void* dout = j.g[1];
   void* dnext = j.g[2];
   void* gG = j.g[3];
-  void* gZ = j.g[4];
   void* gA = j.g[5];
-  void* gZd = j.g[0];
   EKYA_HIP(avgpool_bwd(dt, j.dpooled, nb, j.geo.lh[4] * j.geo.lw[4], 512, dout, st));
   auto bn_bwd = [&](int bi, const void* dy, const void* ymask, const void* z, long long M, void* dz,
                     void* gout) {
     const BnL& b = net.bn[bi];
     return bn_backward(dt, dy, ymask, z, M, b.C, j.master + b.g, bnp(j.bn_mean, b),
-                       bnp(j.bn_invstd, b), j.grad + b.g, j.grad + b.b, dz, gout, j.ws, st);
+                       bnp(j.bn_invstd, b), j.grad + b.g, j.grad + b.b, dz, gout, j.bn_ws, st);
   };
-  auto wgrad = [&](int ci, const void* x, const void* dy, int n) {
+  // Weight gradients go to st2 after a fork event on st; st records no
+  // dependency on them until it reuses a dz buffer (two blocks later) or
+  // reaches the end of the backward pass.
+  int nf = 0;
+  int last_join[2] = {-1, -1};  // per buffer parity: join event of its last reader
+  auto wgrad_async = [&](int ci, const void* x, const void* dy, int parity) -> hipError_t {
+    if (nf >= TrainJob::kForks) return hipErrorInvalidValue;
     const ConvL& c = net.conv[ci];
-    return conv_wgrad(dt, conv_geom(net, j.geo, ci, n), x, dy, j.ws, j.grad + c.off, c.cin, st);
+    EKYA_HIP(hipEventRecord(j.fork[nf], st));
+    EKYA_HIP(hipStreamWaitEvent(j.st2, j.fork[nf], 0));
+    EKYA_HIP(conv_wgrad(dt, conv_geom(net, j.geo, ci, nb), x, dy, j.ws2, j.grad + c.off, c.cin,
+                        j.st2));
+    EKYA_HIP(hipEventRecord(j.joined[nf], j.st2));
+    last_join[parity] = nf;
+    ++nf;
+    return hipSuccess;
+  };
+  auto reuse = [&](int parity) -> hipError_t {  // st may overwrite this parity's dz buffers
+    if (last_join[parity] >= 0) EKYA_HIP(hipStreamWaitEvent(st, j.joined[last_join[parity]], 0));
+    last_join[parity] = -1;
+    return hipSuccess;
   };
   auto dgrad = [&](int ci, const void* dy, void* dx, const void* res, int n) {
     return conv_dgrad(dt, conv_geom(net, j.geo, ci, n), dy,
                       shadow_at(net, j.shadow, net.conv[ci].sh_crsk), dx, res, j.ws, j.ws_floats, st);
   };
+  int blk_count = 0;
   for (int s = 4; s >= j.lowest; --s) {
     if (s == 0) {
       // stem: max-pool backward, BN + ReLU backward, weight gradient
+      const int par = blk_count & 1;
+      EKYA_HIP(reuse(par));
       EKYA_HIP(maxpool_bwd(dt, dout, j.stem_arg, nb, j.geo.sh, j.geo.sw, 64, gA, st));
       const long long M = (long long)nb * j.geo.sh * j.geo.sw;
-      EKYA_HIP(bn_bwd(net.conv[0].bn, gA, j.stem_A, j.stem_Z, M, gZ, nullptr));
-      EKYA_HIP(wgrad(0, j.x0, gZ, nb));
+      EKYA_HIP(bn_bwd(net.conv[0].bn, gA, j.stem_A, j.stem_Z, M, j.gz1[par], nullptr));
+      EKYA_HIP(wgrad_async(0, j.x0, j.gz1[par], par));
       break;
     }
     int first_bi = -1;
@@ -498,28 +560,36 @@ static hipError_t train_backward(TrainJob& j, int nb) {
       const BlockL& b = net.blk[bi];
       if (b.stage != s) continue;
       BlockAct& t = j.acts[bi];
+      const int par = blk_count++ & 1;
+      EKYA_HIP(reuse(par));
+      void* gZ2 = j.gz2[par];
+      void* gZ1 = j.gz1[par];
+      void* gZd = j.gzd[par];
       const bool need_dx = !(s == j.lowest && bi == first_bi);
       ConvGeom g1 = conv_geom(net, j.geo, b.c1, nb);
       const long long M = (long long)nb * g1.P * g1.Q;
       // g = dOut * [OUT > 0]; BN2 backward
-      EKYA_HIP(bn_bwd(net.conv[b.c2].bn, dout, t.OUT, t.Z2, M, gZ, gG));
+      EKYA_HIP(bn_bwd(net.conv[b.c2].bn, dout, t.OUT, t.Z2, M, gZ2, gG));
       const void* dx_sc = gG;
       if (b.cd >= 0) {
         EKYA_HIP(bn_bwd(net.conv[b.cd].bn, gG, nullptr, t.Zd, M, gZd, nullptr));
-        EKYA_HIP(wgrad(b.cd, t.X, gZd, nb));
+        EKYA_HIP(wgrad_async(b.cd, t.X, gZd, par));
         if (need_dx) EKYA_HIP(dgrad(b.cd, gZd, dnext, nullptr, nb));
         dx_sc = dnext;
       }
-      EKYA_HIP(wgrad(b.c2, t.A1, gZ, nb));
-      EKYA_HIP(dgrad(b.c2, gZ, gA, nullptr, nb));
-      EKYA_HIP(bn_bwd(net.conv[b.c1].bn, gA, t.A1, t.Z1, M, gZ, nullptr));
-      EKYA_HIP(wgrad(b.c1, t.X, gZ, nb));
+      EKYA_HIP(wgrad_async(b.c2, t.A1, gZ2, par));
+      EKYA_HIP(dgrad(b.c2, gZ2, gA, nullptr, nb));
+      EKYA_HIP(bn_bwd(net.conv[b.c1].bn, gA, t.A1, t.Z1, M, gZ1, nullptr));
+      EKYA_HIP(wgrad_async(b.c1, t.X, gZ1, par));
       if (need_dx) {
-        EKYA_HIP(dgrad(b.c1, gZ, dnext, dx_sc, nb));
+        EKYA_HIP(dgrad(b.c1, gZ1, dnext, dx_sc, nb));
         std::swap(dout, dnext);
       }
     }
   }
+  // every weight gradient must be complete before the optimizer step
+  EKYA_HIP(reuse(0));
+  EKYA_HIP(reuse(1));
   return hipSuccess;
 }
 
@@ -661,6 +731,10 @@ static hipError_t job_collect(TrainJob& j, JobResult& r) {
 
 static hipError_t create_events(TrainJob& j) {
   for (int e = 0; e <= j.epochs; ++e) EKYA_HIP(hipEventCreate(&j.ev[e]));
+  for (int i = 0; i < TrainJob::kForks; ++i) {
+    EKYA_HIP(hipEventCreateWithFlags(&j.fork[i], hipEventDisableTiming));
+    EKYA_HIP(hipEventCreateWithFlags(&j.joined[i], hipEventDisableTiming));
+  }
   return hipSuccess;
 }
 static void destroy_events(TrainJob& j) {
@@ -669,6 +743,11 @@ static void destroy_events(TrainJob& j) {
       (void)hipEventDestroy(j.ev[e]);
       j.ev[e] = nullptr;
     }
+  for (int i = 0; i < TrainJob::kForks; ++i) {
+    if (j.fork[i]) (void)hipEventDestroy(j.fork[i]);
+    if (j.joined[i]) (void)hipEventDestroy(j.joined[i]);
+    j.fork[i] = j.joined[i] = nullptr;
+  }
 }
 
 #define EKYA_CHECK_HIP(expr)                                   \
@@ -705,6 +784,13 @@ ekya_status run_retrain(Ctx& c, float* weights, int k, const void* frames, const
   j.lr = o.lr;
   j.mu = o.momentum;
   j.st = stream;
+  // library-owned side stream (default priority) for the weight gradients
+  if (c.streams.empty()) {
+    hipStream_t s2;
+    EKYA_CHECK_HIP(hipStreamCreateWithFlags(&s2, hipStreamNonBlocking));
+    c.streams.push_back(s2);
+  }
+  j.st2 = c.timing ? stream : c.streams[0];  // per-kernel timing runs serially
   j.weights = weights;
   j.frames = frames;
   j.labels = labels;
@@ -813,8 +899,8 @@ ekya_status run_profile(Ctx& c, const float* weights, const ekya_profile_cfg* cf
   for (int i = 0; i < n_cfgs; ++i)
     n_max = std::max(n_max, subset_count(n_frames, cfgs[i].subsample_frac));
   const std::vector<int32_t> S = partial_shuffle(n_frames, n_max, subsample_seed);
-  // streams: one per candidate, created on first use
-  while ((int)c.streams.size() < n_cfgs + 1) {
+  // streams: per candidate a main and a side stream, plus one for the caches
+  while ((int)c.streams.size() < 2 * n_cfgs + 1) {
     hipStream_t s;
     EKYA_CHECK_HIP(hipStreamCreateWithFlags(&s, hipStreamNonBlocking));
     c.streams.push_back(s);
@@ -856,6 +942,7 @@ ekya_status run_profile(Ctx& c, const float* weights, const ekya_profile_cfg* cf
     j.lr = cf.lr;
     j.mu = cf.momentum;
     j.st = c.streams[i];
+    j.st2 = c.timing ? j.st : c.streams[n_cfgs + 1 + i];
     j.weights = weights;
     j.frames = frames;
     j.labels = labels;
