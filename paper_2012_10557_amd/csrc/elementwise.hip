@@ -508,6 +508,196 @@ __global__ void fc_bwd_x_kernel(const float* dz, const float* W, int N, int I, i
   df[t] = s;
 }
 
+// ----------------------------------------------------- fused classifier head
+// Forward: one block per sample: pooled[n][c] = mean over the HW pixels of
+// x[n] (or the given features f when x is null), then the logits as in
+// fc_fwd_kernel.  Backward: one launch for softmax cross-entropy, the
+// classifier's weight and bias gradients and the average-pool backward.
+// Every block recomputes the (6-wide) softmax rows it needs from the logits,
+// so no intermediate dz array or extra launch is needed.
+template <typename T>
+__global__ __launch_bounds__(256) void head_fwd_kernel(const T* x, int HW, const float* fin,
+                                                       const float* W, const float* b, int I,
+                                                       int J, float* pooled, float* z) {
+  constexpr int E = Elt<T>::E;
+  __shared__ float fl[2048];
+  __shared__ float red[4][8];
+  __shared__ float ps[4][2048];
+  const int n = blockIdx.x, t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  if (x) {
+    // thread: one 16-byte unit of channels x one of 4 pixel slices; slices
+    // added in order
+    const int units = I / E;
+    for (int u = t % 64; u < units; u += 64) {
+      float acc[E];
+#pragma unroll
+      for (int e = 0; e < E; ++e) acc[e] = 0.f;
+      for (int k = wave; k < HW; k += 4) {
+        float v[E];
+        unit_to_f<T>(*reinterpret_cast<const uint4*>(x + ((long long)n * HW + k) * I + u * E), v);
+#pragma unroll
+        for (int e = 0; e < E; ++e) acc[e] += v[e];
+      }
+#pragma unroll
+      for (int e = 0; e < E; ++e) ps[wave][u * E + e] = acc[e];
+    }
+    __syncthreads();
+    for (int i = t; i < I; i += 256) {
+      const float v = (((ps[0][i] + ps[1][i]) + ps[2][i]) + ps[3][i]) / (float)HW;
+      pooled[(long long)n * I + i] = v;
+      fl[i] = v;
+    }
+  } else {
+    for (int i = t; i < I; i += 256) fl[i] = fin[(long long)n * I + i];
+  }
+  __syncthreads();
+  for (int j0 = 0; j0 < J; j0 += 8) {
+    float s[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) s[k] = 0.f;
+    for (int i = t; i < I; i += 256) {
+      const float xv = fl[i];
+#pragma unroll
+      for (int k = 0; k < 8; ++k)
+        if (j0 + k < J) s[k] += xv * W[(long long)(j0 + k) * I + i];
+    }
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      float v = s[k];
+      for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+      if (lane == 0) red[wave][k] = v;
+    }
+    __syncthreads();
+    if (t < 8 && j0 + t < J)
+      z[(long long)n * J + j0 + t] = ((red[0][t] + red[1][t]) + (red[2][t] + red[3][t])) + b[j0 + t];
+    __syncthreads();
+  }
+}
+
+// Softmax cross-entropy gradient of one row: dz[j] = (softmax_j - [j == y]) / N;
+// returns false (dz = 0) for a label outside [0, J).
+__device__ __forceinline__ bool ce_row(const float* zr, int y, int J, int N, float* dz, float& loss,
+                                       int& correct) {
+  if (y < 0 || y >= J) {
+    for (int j = 0; j < J; ++j) dz[j] = 0.f;
+    loss = 0.f;
+    correct = 0;
+    return false;
+  }
+  float m = zr[0];
+  int am = 0;
+  for (int j = 1; j < J; ++j)
+    if (zr[j] > m) {
+      m = zr[j];
+      am = j;
+    }
+  float se = 0.f;
+  for (int j = 0; j < J; ++j) se += expf(zr[j] - m);
+  const float lse = m + logf(se);
+  loss = lse - zr[y];
+  correct = (am == y);
+  for (int j = 0; j < J; ++j) dz[j] = (expf(zr[j] - lse) - (j == y ? 1.f : 0.f)) / (float)N;
+  return true;
+}
+
+constexpr int HEAD_JMAX = 16;  // classes handled by the fused backward (else the separate kernels)
+constexpr int HEAD_WB = 8;     // blocks of 64 features for the weight gradient (I = 512)
+
+template <typename T>
+__global__ __launch_bounds__(256) void head_bwd_kernel(const float* z, const int32_t* labels,
+                                                       const int32_t* idx, int N, int J,
+                                                       const float* f, const float* W, int I,
+                                                       float* dW, float* db, T* dout, int HW,
+                                                       float* out) {
+  constexpr int E = Elt<T>::E;
+  const int t = threadIdx.x;
+  __shared__ float rdz[256][HEAD_JMAX];
+  __shared__ float rl[256];
+  __shared__ int rc[256], rb[256];
+  float dz[HEAD_JMAX];
+  if (blockIdx.x < (unsigned)HEAD_WB) {
+    // weight gradient for features i = 64 b + t % 64; samples in 4 slices of
+    // each 256-row chunk, the slices added in order
+    __shared__ float part[4][HEAD_JMAX][64];
+    const int il = t & 63, sl = t >> 6;
+    const int i = blockIdx.x * 64 + il;
+    float acc[HEAD_JMAX], dbs[HEAD_JMAX], L = 0.f;
+    int C = 0, bad = 0;
+#pragma unroll
+    for (int j = 0; j < HEAD_JMAX; ++j) acc[j] = dbs[j] = 0.f;
+    for (int n0 = 0; n0 < N; n0 += 256) {
+      const int cnt = min(256, N - n0);
+      __syncthreads();
+      if (t < cnt) {
+        float l;
+        int c;
+        const bool ok = ce_row(z + (long long)(n0 + t) * J, labels[idx ? idx[n0 + t] : n0 + t], J,
+                               N, dz, l, c);
+        for (int j = 0; j < J; ++j) rdz[t][j] = dz[j];
+        rl[t] = l;
+        rc[t] = c;
+        rb[t] = (!ok || !isfinite(l)) ? 1 : 0;
+      }
+      __syncthreads();
+      const int per = (cnt + 3) / 4;
+      for (int k = sl * per; k < min(cnt, (sl + 1) * per); ++k) {
+        const float fv = i < I ? f[(long long)(n0 + k) * I + i] : 0.f;
+#pragma unroll
+        for (int j = 0; j < HEAD_JMAX; ++j)
+          if (j < J) acc[j] += rdz[k][j] * fv;
+      }
+      if (blockIdx.x == 0 && t == 0)
+        for (int k = 0; k < cnt; ++k) {
+          L += rl[k];
+          C += rc[k];
+          bad |= rb[k];
+          for (int j = 0; j < J; ++j) dbs[j] += rdz[k][j];
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < HEAD_JMAX; ++j) part[sl][j][il] = acc[j];
+    __syncthreads();
+    if (sl == 0 && i < I)
+      for (int j = 0; j < J; ++j)
+        dW[(long long)j * I + i] = ((part[0][j][il] + part[1][j][il]) + part[2][j][il]) + part[3][j][il];
+    if (blockIdx.x == 0 && t == 0) {
+      for (int j = 0; j < J; ++j) db[j] = dbs[j];
+      out[0] = L / (float)N;
+      out[1] = (float)C;
+      out[2] = (float)bad;
+    }
+    return;
+  }
+  if (!dout) return;
+  // average-pool backward of d pooled = dz W: dout[n][p][c] = (sum_j dz_j W[j][c]) / HW.
+  // A block covers 256 / (I / E) samples; their softmax rows are computed once.
+  const int units = I / E, spb = 256 / units;
+  const int nb0 = (blockIdx.x - HEAD_WB) * spb;
+  if (t < spb && nb0 + t < N) {
+    float l;
+    int c;
+    ce_row(z + (long long)(nb0 + t) * J, labels[idx ? idx[nb0 + t] : nb0 + t], J, N, dz, l, c);
+    for (int j = 0; j < J; ++j) rdz[t][j] = dz[j];
+  }
+  __syncthreads();
+  const int sn = t / units, u = t % units, n = nb0 + sn;
+  if (sn >= spb || n >= N) return;
+  const float inv = 1.f / (float)HW;
+  float d[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) d[e] = 0.f;
+  for (int j = 0; j < J; ++j) {
+    const float w = rdz[sn][j];
+#pragma unroll
+    for (int e = 0; e < E; ++e) d[e] += w * W[(long long)j * I + u * E + e];
+  }
+#pragma unroll
+  for (int e = 0; e < E; ++e) d[e] *= inv;
+  const uint4 v = f_to_unit<T>(d);
+  for (int p = 0; p < HW; ++p)
+    reinterpret_cast<uint4*>(dout + ((long long)n * HW + p) * I)[u] = v;
+}
+
 __global__ __launch_bounds__(256) void count_correct_kernel(const float* z, const int32_t* labels,
                                                             int N, int J, int32_t* count) {
   __shared__ int sc[256];
@@ -832,6 +1022,34 @@ hipError_t fc_bwd(const float* dz, const float* f, const float* W, int N, int I,
                        W, N, I, J, df);
   }
   return hipGetLastError();
+}
+
+hipError_t head_forward(int dt, const void* x, int HW, const float* f, const float* W,
+                        const float* b, int N, int I, int J, float* pooled, float* z,
+                        hipStream_t stream) {
+  if (N == 0) return hipSuccess;
+  if (I > 2048 || I % dtype_vec(dt) != 0) return hipErrorInvalidValue;
+  return by_type(dt, [&](auto* tp) {
+    using T = std::remove_pointer_t<decltype(tp)>;
+    hipLaunchKernelGGL(head_fwd_kernel<T>, dim3(N), dim3(256), 0, stream, (const T*)x, HW, f, W, b,
+                       I, J, pooled, z);
+  });
+}
+
+bool head_backward_fused(int J, int I) { return J <= HEAD_JMAX && I <= 64 * HEAD_WB; }
+
+hipError_t head_backward(int dt, const float* z, const int32_t* labels, const int32_t* idx, int N,
+                         int J, const float* f, const float* W, int I, float* dW, float* db,
+                         void* dout, int HW, float* out, hipStream_t stream) {
+  if (!head_backward_fused(J, I) || I % dtype_vec(dt) != 0 || 256 % (I / dtype_vec(dt)) != 0)
+    return hipErrorInvalidValue;
+  const int spb = 256 / (I / dtype_vec(dt));
+  const int dblocks = dout ? cdiv(N, spb) : 0;
+  return by_type(dt, [&](auto* tp) {
+    using T = std::remove_pointer_t<decltype(tp)>;
+    hipLaunchKernelGGL(head_bwd_kernel<T>, dim3(HEAD_WB + dblocks), dim3(256), 0, stream, z,
+                       labels, idx, N, J, f, W, I, dW, db, (T*)dout, HW, out);
+  });
 }
 
 hipError_t count_correct(const float* z, const int32_t* labels, int N, int J, int32_t* count,

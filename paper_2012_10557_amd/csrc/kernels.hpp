@@ -113,6 +113,19 @@ hipError_t softmax_ce(const float* z, const int32_t* labels, const int32_t* idx,
 // dW[J, I] = dz^T f, db = column sums of dz, df = dz W (df may be null).
 hipError_t fc_bwd(const float* dz, const float* f, const float* Wt, int N, int I, int J, float* dW,
                   float* db, float* df, hipStream_t stream);
+// Fused classifier head.  Forward: pooled[N, I] (fp32) = mean over HW pixels
+// of x[N, HW, I] (x null: features f are used and pooled is not written),
+// z = pooled W^T + b.  Backward (J <= 16, I <= 512; head_backward_fused):
+// softmax cross-entropy of z with labels (through idx when non-null) as in
+// softmax_ce (out[0..2]), dW = dz^T f, db = column sums of dz and, when dout
+// is non-null, dout[N, HW, I] = (dz W) / HW.
+hipError_t head_forward(int dt, const void* x, int HW, const float* f, const float* W,
+                        const float* b, int N, int I, int J, float* pooled, float* z,
+                        hipStream_t stream);
+bool head_backward_fused(int J, int I);
+hipError_t head_backward(int dt, const float* z, const int32_t* labels, const int32_t* idx, int N,
+                         int J, const float* f, const float* W, int I, float* dW, float* db,
+                         void* dout, int HW, float* out, hipStream_t stream);
 // Count of rows whose argmax matches the label, accumulated into *count.
 hipError_t count_correct(const float* z, const int32_t* labels, int N, int J, int32_t* count,
                          hipStream_t stream);

@@ -486,29 +486,38 @@ static hipError_t train_forward(TrainJob& j, int nb) {
                         st));
       cur = t.OUT;
     }
-    if (s == 4) {
-      EKYA_HIP(avgpool_fwd(dt, cur, nb, j.geo.lh[4] * j.geo.lw[4], 512, j.pooled, st));
-      cur = j.pooled;
-    }
+    if (s == 4)  // average pool + classifier in one kernel
+      return head_forward(dt, cur, j.geo.lh[4] * j.geo.lw[4], nullptr, j.master + net.fc_w,
+                          j.master + net.fc_b, nb, 512, net.n_classes, j.pooled, j.logits, st);
   }
-  const float* f = (j.lowest == 5) ? reinterpret_cast<const float*>(j.x0) : j.pooled;
-  return fc_fwd(f, j.master + net.fc_w, j.master + net.fc_b, nb, 512, net.n_classes, j.logits, st);
+  return head_forward(dt, nullptr, 0, reinterpret_cast<const float*>(j.x0), j.master + net.fc_w,
+                      j.master + net.fc_b, nb, 512, net.n_classes, nullptr, j.logits, st);
 }
 
-// Backward of stages 5..lowest from dz (already in j.dz); gradients land in j.grad.
-static hipError_t train_backward(TrainJob& j, int nb) {
+// Loss of the batch (labels through fid, loss / correct / flag into ce) and
+// backward of stages 5..lowest; gradients land in j.grad.
+static hipError_t train_backward(TrainJob& j, int nb, const int32_t* fid, float* ce) {
   const Net& net = *j.net;
   const int dt = j.dt;
   hipStream_t st = j.st;
   const float* f = (j.lowest == 5) ? reinterpret_cast<const float*>(j.x0) : j.pooled;
-  EKYA_HIP(fc_bwd(j.dz, f, j.master + net.fc_w, nb, 512, net.n_classes, j.grad + net.fc_w,
-                  j.grad + net.fc_b, j.lowest == 5 ? nullptr : j.dpooled, st));
-  if (j.lowest == 5) return hipSuccess;
   void* dout = j.g[1];
   void* dnext = j.g[2];
   void* gG = j.g[3];
   void* gA = j.g[5];
-  EKYA_HIP(avgpool_bwd(dt, j.dpooled, nb, j.geo.lh[4] * j.geo.lw[4], 512, dout, st));
+  const int hw = j.geo.lh[4] * j.geo.lw[4];
+  if (head_backward_fused(net.n_classes, 512)) {
+    // softmax cross-entropy, classifier gradients and average-pool backward
+    EKYA_HIP(head_backward(dt, j.logits, j.labels, fid, nb, net.n_classes, f, j.master + net.fc_w,
+                           512, j.grad + net.fc_w, j.grad + net.fc_b,
+                           j.lowest == 5 ? nullptr : dout, hw, ce, st));
+  } else {
+    EKYA_HIP(softmax_ce(j.logits, j.labels, fid, nb, net.n_classes, j.dz, ce, st));
+    EKYA_HIP(fc_bwd(j.dz, f, j.master + net.fc_w, nb, 512, net.n_classes, j.grad + net.fc_w,
+                    j.grad + net.fc_b, j.lowest == 5 ? nullptr : j.dpooled, st));
+    if (j.lowest < 5) EKYA_HIP(avgpool_bwd(dt, j.dpooled, nb, hw, 512, dout, st));
+  }
+  if (j.lowest == 5) return hipSuccess;
   auto bn_bwd = [&](int bi, const void* dy, const void* ymask, const void* z, long long M, void* dz,
                     void* gout) {
     const BnL& b = net.bn[bi];
@@ -654,9 +663,7 @@ static hipError_t job_epochs(TrainJob& j) {
       else
         EKYA_HIP(gather_rows(j.cache, ord, nb, j.row_bytes, j.x0, j.st));
       EKYA_HIP(train_forward(j, nb));
-      EKYA_HIP(softmax_ce(j.logits, j.labels, fid, nb, net.n_classes, j.dz, j.ce_out + 3 * step,
-                          j.st));
-      EKYA_HIP(train_backward(j, nb));
+      EKYA_HIP(train_backward(j, nb, fid, j.ce_out + 3 * step));
       EKYA_HIP(sgd_momentum(j.master + tb, j.mom + tb, j.grad + tb, net.total - tb, j.lr, j.mu,
                             j.st));
       EKYA_HIP(pack_conv_weights(j.dt, j.master, t.pack_train[j.lowest],
