@@ -378,9 +378,8 @@ ekya_status ekya_op_batchnorm_train(int precision, const void* z, long long M, i
   float* ss = tmp.get<float>(2 * (size_t)C);
   hipError_t e = (part && ss) ? hipSuccess : hipErrorOutOfMemory;
   if (e == hipSuccess)
-    e = ekya::bn_train_stats(precision, z, M, C, gamma, beta, running_mean, running_var, mean_out,
-                             invstd_out, ss, ss + C, part, st);
-  if (e == hipSuccess) e = ekya::bn_apply(precision, z, M, C, mean_out, ss, beta, nullptr, relu, y, st);
+    e = ekya::bn_train_forward(precision, z, M, C, gamma, beta, running_mean, running_var,
+                               mean_out, invstd_out, ss, ss + C, nullptr, relu, y, part, st);
   return sync_status(st, e);
 }
 

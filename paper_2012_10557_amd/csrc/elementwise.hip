@@ -186,6 +186,243 @@ __global__ void bn_apply_kernel(const T* z, long long units, int C, const float*
   }
 }
 
+// ------------------------------------------- BN, small batches: two launches
+// For up to BN_FOLD_MAX_CHUNKS chunks of BN_FOLD_ROWS rows and C a multiple of
+// 64: a partial kernel writes per (chunk, 64-channel group) sums, and each
+// block of the apply kernel first reduces the chunk sums of its own 64
+// channels, in one fixed order (so every block derives the same per-channel
+// coefficients), then applies them to its rows.  This replaces the separate
+// per-channel final kernel of the general path.
+constexpr int BN_FOLD_ROWS = 128;
+constexpr int BN_FOLD_MAX_CHUNKS = 64;
+constexpr int BN_GROUP = 64;
+
+inline bool bn_fold_ok(long long M, int C) {
+  return C % BN_GROUP == 0 && cdivl(M, BN_FOLD_ROWS) <= BN_FOLD_MAX_CHUNKS;
+}
+
+// Per (chunk, group) sums of two per-element quantities, added in a fixed
+// order.  Forward: d = z - K with the shift K[c] = z[0][c]; s1 = sum d,
+// s2 = sum d^2.  Backward: g = dy [* (y > 0)]; s1 = sum g, s2 = sum g (z - mean).
+template <typename T, bool BWD>
+__global__ __launch_bounds__(256) void bn_group_partial(const T* z, const T* dy, const T* y,
+                                                        const float* mean, long long M, int C,
+                                                        float* part) {
+  constexpr int E = Elt<T>::E, UG = BN_GROUP / E, RI = 256 / UG;
+  const int t = threadIdx.x, u = t % UG, rs = t / UG;
+  const int c0 = blockIdx.y * BN_GROUP + u * E;
+  const long long r0 = (long long)blockIdx.x * BN_FOLD_ROWS;
+  const long long r1 = std::min<long long>(M, r0 + BN_FOLD_ROWS);
+  float s1[E], s2[E], K[E];
+#pragma unroll
+  for (int i = 0; i < E; ++i) s1[i] = s2[i] = 0.f;
+  if (BWD)
+    chan_load<E>(mean, c0, K);
+  else
+    unit_to_f<T>(*reinterpret_cast<const uint4*>(z + c0), K);
+  for (long long r = r0 + rs; r < r1; r += RI) {
+    const long long off = r * C + c0;
+    float v[E];
+    unit_to_f<T>(*reinterpret_cast<const uint4*>(z + off), v);
+    if (BWD) {
+      float g[E];
+      unit_to_f<T>(*reinterpret_cast<const uint4*>(dy + off), g);
+      if (y) {
+        float yy[E];
+        unit_to_f<T>(*reinterpret_cast<const uint4*>(y + off), yy);
+#pragma unroll
+        for (int i = 0; i < E; ++i) g[i] = yy[i] > 0.f ? g[i] : 0.f;
+      }
+#pragma unroll
+      for (int i = 0; i < E; ++i) {
+        s1[i] += g[i];
+        s2[i] += g[i] * (v[i] - K[i]);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < E; ++i) {
+        const float d = v[i] - K[i];
+        s1[i] += d;
+        s2[i] += d * d;
+      }
+    }
+  }
+  __shared__ float sh[2][256 * E];
+#pragma unroll
+  for (int i = 0; i < E; ++i) {
+    sh[0][t * E + i] = s1[i];
+    sh[1][t * E + i] = s2[i];
+  }
+  __syncthreads();
+  if (t < BN_GROUP) {
+    float a = 0.f, b = 0.f;
+    for (int k = 0; k < RI; ++k) {  // row slices in order
+      a += sh[0][k * BN_GROUP + t];
+      b += sh[1][k * BN_GROUP + t];
+    }
+    const int c = blockIdx.y * BN_GROUP + t;
+    part[(long long)blockIdx.x * 2 * C + c] = a;
+    part[(long long)blockIdx.x * 2 * C + C + c] = b;
+    // the forward shift, after the chunk rows, for the apply kernel
+    if (!BWD && blockIdx.x == 0) part[(long long)gridDim.x * 2 * C + c] = to_f(z[c]);
+  }
+}
+
+// Totals of the two partial rows for channel c = 64 blockIdx.y + threadIdx.x % 64:
+// four slices of chunks (k = slice, slice + 4, ...) in float, the slices added
+// in order in double.  True for the thread (one per channel) that holds them.
+__device__ __forceinline__ bool group_sums(const float* part, int nch, int C, double& a,
+                                           double& b) {
+  __shared__ float sa[4][BN_GROUP], sb[4][BN_GROUP];
+  const int lc = threadIdx.x % BN_GROUP, sl = threadIdx.x / BN_GROUP;
+  const int c = blockIdx.y * BN_GROUP + lc;
+  float x = 0.f, y = 0.f;
+  for (int k = sl; k < nch; k += 4) {
+    x += part[(long long)k * 2 * C + c];
+    y += part[(long long)k * 2 * C + C + c];
+  }
+  sa[sl][lc] = x;
+  sb[sl][lc] = y;
+  __syncthreads();
+  if (sl != 0) return false;
+  a = (((double)sa[0][lc] + (double)sa[1][lc]) + (double)sa[2][lc]) + (double)sa[3][lc];
+  b = (((double)sb[0][lc] + (double)sb[1][lc]) + (double)sb[2][lc]) + (double)sb[3][lc];
+  return true;
+}
+
+// Statistics from the group partials (and the shift stored after them), then
+// y = relu?((z - mean) scale + beta [+ res]) on rows [blockIdx.x rpb, +rpb) of the block's 64 channels.  Blocks
+// with blockIdx.x == 0 publish mean / invstd / scale / shift and update the
+// running statistics.
+template <typename T>
+__global__ __launch_bounds__(256) void bn_fold_apply(const T* z, const float* part, int nch,
+                                                     long long M, int C, long long rpb,
+                                                     const float* gamma, const float* beta,
+                                                     float* rm, float* rv, float* mean,
+                                                     float* invstd, float* scale, float* shift,
+                                                     const T* res, int relu, T* y) {
+  constexpr int E = Elt<T>::E, UG = BN_GROUP / E, RI = 256 / UG;
+  __shared__ float cf[3][BN_GROUP];
+  const int t = threadIdx.x;
+  double a, b;
+  if (group_sums(part, nch, C, a, b)) {
+    const int c = blockIdx.y * BN_GROUP + t;
+    const double Kc = (double)part[(long long)nch * 2 * C + c];
+    const double d = a / (double)M;
+    double var = b / (double)M - d * d;
+    if (var < 0.0) var = 0.0;
+    const float mu = (float)(Kc + d);
+    const float is = (float)(1.0 / sqrt(var + (double)BN_EPS));
+    const float sc = gamma[c] * is;
+    cf[0][t] = mu;
+    cf[1][t] = sc;
+    cf[2][t] = beta[c];
+    if (blockIdx.x == 0) {
+      mean[c] = mu;
+      invstd[c] = is;
+      scale[c] = sc;
+      shift[c] = beta[c] - mu * sc;
+      if (rm) {
+        const double unb = M > 1 ? var * (double)M / (double)(M - 1) : var;
+        rm[c] = (1.f - BN_MOMENTUM) * rm[c] + BN_MOMENTUM * mu;
+        rv[c] = (1.f - BN_MOMENTUM) * rv[c] + BN_MOMENTUM * (float)unb;
+      }
+    }
+  }
+  __syncthreads();
+  const int u = t % UG, rs = t / UG;
+  float mu[E], sc[E], be[E];
+#pragma unroll
+  for (int i = 0; i < E; ++i) {
+    mu[i] = cf[0][u * E + i];
+    sc[i] = cf[1][u * E + i];
+    be[i] = cf[2][u * E + i];
+  }
+  const long long r0 = blockIdx.x * rpb, r1 = std::min<long long>(M, r0 + rpb);
+  const int c0 = blockIdx.y * BN_GROUP + u * E;
+  for (long long r = r0 + rs; r < r1; r += RI) {
+    const long long off = r * C + c0;
+    float v[E], q[E];
+    unit_to_f<T>(*reinterpret_cast<const uint4*>(z + off), v);
+    if (res) unit_to_f<T>(*reinterpret_cast<const uint4*>(res + off), q);
+#pragma unroll
+    for (int i = 0; i < E; ++i) {
+      float o = (v[i] - mu[i]) * sc[i] + be[i];
+      if (res) o += q[i];
+      if (relu) o = relu_nan(o);
+      v[i] = o;
+    }
+    *reinterpret_cast<uint4*>(y + off) = f_to_unit<T>(v);
+  }
+}
+
+// Backward coefficients from the group partials (dz = a g + b + c (z - mean)),
+// then dz (and g if g_out) on the block's rows; blocks with blockIdx.x == 0
+// publish dgamma / dbeta.
+template <typename T>
+__global__ __launch_bounds__(256) void bn_bwd_fold_apply(const T* dy, const T* y, const T* z,
+                                                         const float* part, int nch, long long M,
+                                                         int C, long long rpb,
+                                                         const float* gamma, const float* mean,
+                                                         const float* invstd, float* dgamma,
+                                                         float* dbeta, T* dz, T* g_out) {
+  constexpr int E = Elt<T>::E, UG = BN_GROUP / E, RI = 256 / UG;
+  __shared__ float cf[4][BN_GROUP];
+  const int t = threadIdx.x;
+  double sg, sgx;
+  if (group_sums(part, nch, C, sg, sgx)) {
+    const int c = blockIdx.y * BN_GROUP + t;
+    const float is = invstd[c];
+    const float db = (float)sg;
+    const float dg = (float)(sgx * (double)is);
+    const float a = gamma[c] * is;
+    cf[0][t] = a;
+    cf[1][t] = -a * db / (float)M;
+    cf[2][t] = -a * is * dg / (float)M;
+    cf[3][t] = mean[c];
+    if (blockIdx.x == 0) {
+      dbeta[c] = db;
+      dgamma[c] = dg;
+    }
+  }
+  __syncthreads();
+  const int u = t % UG, rs = t / UG;
+  float ca[E], cb[E], cc[E], mu[E];
+#pragma unroll
+  for (int i = 0; i < E; ++i) {
+    ca[i] = cf[0][u * E + i];
+    cb[i] = cf[1][u * E + i];
+    cc[i] = cf[2][u * E + i];
+    mu[i] = cf[3][u * E + i];
+  }
+  const long long r0 = blockIdx.x * rpb, r1 = std::min<long long>(M, r0 + rpb);
+  const int c0 = blockIdx.y * BN_GROUP + u * E;
+  for (long long r = r0 + rs; r < r1; r += RI) {
+    const long long off = r * C + c0;
+    float g[E], zz[E], o[E];
+    unit_to_f<T>(*reinterpret_cast<const uint4*>(dy + off), g);
+    unit_to_f<T>(*reinterpret_cast<const uint4*>(z + off), zz);
+    if (y) {
+      float yy[E];
+      unit_to_f<T>(*reinterpret_cast<const uint4*>(y + off), yy);
+#pragma unroll
+      for (int i = 0; i < E; ++i) g[i] = yy[i] > 0.f ? g[i] : 0.f;
+    }
+    if (g_out) *reinterpret_cast<uint4*>(g_out + off) = f_to_unit<T>(g);
+#pragma unroll
+    for (int i = 0; i < E; ++i) o[i] = ca[i] * g[i] + cb[i] + cc[i] * (zz[i] - mu[i]);
+    *reinterpret_cast<uint4*>(dz + off) = f_to_unit<T>(o);
+  }
+}
+
+// Rows per block of the fold apply kernels: about 512 blocks over the
+// groups, a whole number of row slices each.
+inline long long bn_fold_rpb(long long M, int C, int dt) {
+  const int ri = 256 / (BN_GROUP / dtype_vec(dt));
+  const long long target = std::max(1, 512 / (C / BN_GROUP));
+  return ri * cdivl(cdivl(M, target), ri);
+}
+
 // tab row: gamma_off, beta_off, rm_off, rv_off, C, out_off
 __global__ void bn_fold_kernel(const float* p, const long long* tab, float* out) {
   const long long* t = tab + 6 * blockIdx.x;
@@ -916,6 +1153,30 @@ hipError_t bn_train_stats(int dt, const void* z, long long M, int C, const float
   });
 }
 
+hipError_t bn_train_forward(int dt, const void* z, long long M, int C, const float* gamma,
+                            const float* beta, float* rm, float* rv, float* mean, float* invstd,
+                            float* scale, float* shift, const void* res, int relu, void* y,
+                            float* partials, hipStream_t stream) {
+  if (M == 0) return hipSuccess;
+  if (!bn_fold_ok(M, C)) {
+    hipError_t e = bn_train_stats(dt, z, M, C, gamma, beta, rm, rv, mean, invstd, scale, shift,
+                                  partials, stream);
+    if (e != hipSuccess) return e;
+    return bn_apply(dt, z, M, C, mean, scale, beta, res, relu, y, stream);
+  }
+  const int nch = (int)cdivl(M, BN_FOLD_ROWS), groups = C / BN_GROUP;
+  const long long rpb = bn_fold_rpb(M, C, dt);
+  return by_type(dt, [&](auto* tp) {
+    using T = std::remove_pointer_t<decltype(tp)>;
+    hipLaunchKernelGGL((bn_group_partial<T, false>), dim3(nch, groups), dim3(256), 0, stream,
+                       (const T*)z, (const T*)nullptr, (const T*)nullptr, (const float*)nullptr, M,
+                       C, partials);
+    hipLaunchKernelGGL(bn_fold_apply<T>, dim3((unsigned)cdivl(M, rpb), groups), dim3(256), 0,
+                       stream, (const T*)z, partials, nch, M, C, rpb, gamma, beta, rm, rv, mean,
+                       invstd, scale, shift, (const T*)res, relu, (T*)y);
+  });
+}
+
 hipError_t bn_apply(int dt, const void* z, long long M, int C, const float* mean,
                     const float* scale, const float* beta, const void* res, int relu, void* y,
                     hipStream_t stream) {
@@ -939,6 +1200,18 @@ hipError_t bn_backward(int dt, const void* dy, const void* y, const void* z, lon
                        const float* gamma, const float* mean, const float* invstd, float* dgamma,
                        float* dbeta, void* dz, void* g_out, float* partials, hipStream_t stream) {
   if (M == 0) return hipSuccess;
+  if (bn_fold_ok(M, C)) {
+    const int nf = (int)cdivl(M, BN_FOLD_ROWS), groups = C / BN_GROUP;
+    const long long rpb = bn_fold_rpb(M, C, dt);
+    return by_type(dt, [&](auto* tp) {
+      using T = std::remove_pointer_t<decltype(tp)>;
+      hipLaunchKernelGGL((bn_group_partial<T, true>), dim3(nf, groups), dim3(256), 0, stream,
+                         (const T*)z, (const T*)dy, (const T*)y, mean, M, C, partials);
+      hipLaunchKernelGGL(bn_bwd_fold_apply<T>, dim3((unsigned)cdivl(M, rpb), groups), dim3(256), 0,
+                         stream, (const T*)dy, (const T*)y, (const T*)z, partials, nf, M, C, rpb,
+                         gamma, mean, invstd, dgamma, dbeta, (T*)dz, (T*)g_out);
+    });
+  }
   const int nch = bn_chunks(M);
   const long long rpc = cdivl(M, nch);
   float* coef = partials + (size_t)nch * 2 * C;

@@ -74,6 +74,12 @@ size_t bn_partials_floats(long long M, int C);
 hipError_t bn_train_stats(int dt, const void* z, long long M, int C, const float* gamma,
                           const float* beta, float* rm, float* rv, float* mean, float* invstd,
                           float* scale, float* shift, float* partials, hipStream_t stream);
+// bn_train_stats followed by bn_apply: y = relu?((z - mean)*scale + beta + res).
+// Two launches when M is at most 64 chunks of 128 rows and C a multiple of 64.
+hipError_t bn_train_forward(int dt, const void* z, long long M, int C, const float* gamma,
+                            const float* beta, float* rm, float* rv, float* mean, float* invstd,
+                            float* scale, float* shift, const void* res, int relu, void* y,
+                            float* partials, hipStream_t stream);
 // y = (z - mean)*scale + beta (+ res) (ReLU), elementwise over [M, C].
 hipError_t bn_apply(int dt, const void* z, long long M, int C, const float* mean,
                     const float* scale, const float* beta, const void* res, int relu, void* y,

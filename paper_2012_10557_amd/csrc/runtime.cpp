@@ -431,15 +431,13 @@ static hipError_t train_forward(TrainJob& j, int nb) {
   const Net& net = *j.net;
   const int dt = j.dt;
   hipStream_t st = j.st;
-  auto bn_train = [&](int bi, const void* z, long long M) {
+  // train-mode BN (statistics, running-statistic update, apply) of layer bi
+  auto bn_train = [&](int bi, const void* z, long long M, const void* res, int relu, void* y) {
     const BnL& b = net.bn[bi];
-    return bn_train_stats(dt, z, M, b.C, j.master + b.g, j.master + b.b, j.master + b.rm,
-                          j.master + b.rv, bnp(j.bn_mean, b), bnp(j.bn_invstd, b),
-                          bnp(j.bn_scale, b), bnp(j.bn_shift, b), j.bn_ws, st);
+    return bn_train_forward(dt, z, M, b.C, j.master + b.g, j.master + b.b, j.master + b.rm,
+                            j.master + b.rv, bnp(j.bn_mean, b), bnp(j.bn_invstd, b),
+                            bnp(j.bn_scale, b), bnp(j.bn_shift, b), res, relu, y, j.bn_ws, st);
   };
-  auto mu = [&](int bi) { return bnp(j.bn_mean, net.bn[bi]); };
-  auto sc = [&](int bi) { return bnp(j.bn_scale, net.bn[bi]); };
-  auto be = [&](int bi) { return j.master + net.bn[bi].b; };
   const void* cur = j.x0;
   for (int s = j.lowest; s <= 4; ++s) {
     if (s == 0) {
@@ -447,9 +445,7 @@ static hipError_t train_forward(TrainJob& j, int nb) {
       EKYA_HIP(conv_fwd(dt, cg, cur, shadow_at(net, j.shadow, net.conv[0].sh_krsc), j.stem_Z,
                         ConvEpilogue(), j.ws, j.ws_floats, st));
       const long long M = (long long)nb * cg.P * cg.Q;
-      EKYA_HIP(bn_train(net.conv[0].bn, j.stem_Z, M));
-      EKYA_HIP(bn_apply(dt, j.stem_Z, M, 64, mu(net.conv[0].bn), sc(net.conv[0].bn), be(net.conv[0].bn), nullptr, 1,
-                        j.stem_A, st));
+      EKYA_HIP(bn_train(net.conv[0].bn, j.stem_Z, M, nullptr, 1, j.stem_A));
       void* xm = j.acts[0].X;
       EKYA_HIP(maxpool_fwd(dt, j.stem_A, nb, j.geo.sh, j.geo.sw, 64, xm, j.stem_arg, st));
       cur = xm;
@@ -462,28 +458,21 @@ static hipError_t train_forward(TrainJob& j, int nb) {
       t.X = const_cast<void*>(cur);
       ConvGeom g1 = conv_geom(net, j.geo, b.c1, nb);
       const long long M = (long long)nb * g1.P * g1.Q;
-      const int C = net.conv[b.c1].cout;
       EKYA_HIP(conv_fwd(dt, g1, t.X, shadow_at(net, j.shadow, net.conv[b.c1].sh_krsc), t.Z1,
                         ConvEpilogue(), j.ws, j.ws_floats, st));
-      EKYA_HIP(bn_train(net.conv[b.c1].bn, t.Z1, M));
-      EKYA_HIP(bn_apply(dt, t.Z1, M, C, mu(net.conv[b.c1].bn), sc(net.conv[b.c1].bn), be(net.conv[b.c1].bn), nullptr, 1,
-                        t.A1, st));
+      EKYA_HIP(bn_train(net.conv[b.c1].bn, t.Z1, M, nullptr, 1, t.A1));
       EKYA_HIP(conv_fwd(dt, conv_geom(net, j.geo, b.c2, nb), t.A1,
                         shadow_at(net, j.shadow, net.conv[b.c2].sh_krsc), t.Z2, ConvEpilogue(), j.ws,
                         j.ws_floats, st));
-      EKYA_HIP(bn_train(net.conv[b.c2].bn, t.Z2, M));
       const void* res = t.X;
-      if (b.cd >= 0) {
+      if (b.cd >= 0) {  // projection shortcut: its BN output is the residual
         EKYA_HIP(conv_fwd(dt, conv_geom(net, j.geo, b.cd, nb), t.X,
                           shadow_at(net, j.shadow, net.conv[b.cd].sh_krsc), t.Zd, ConvEpilogue(),
                           j.ws, j.ws_floats, st));
-        EKYA_HIP(bn_train(net.conv[b.cd].bn, t.Zd, M));
-        EKYA_HIP(bn_apply(dt, t.Zd, M, C, mu(net.conv[b.cd].bn), sc(net.conv[b.cd].bn), be(net.conv[b.cd].bn), nullptr, 0,
-                          j.g[0], st));
+        EKYA_HIP(bn_train(net.conv[b.cd].bn, t.Zd, M, nullptr, 0, j.g[0]));
         res = j.g[0];
       }
-      EKYA_HIP(bn_apply(dt, t.Z2, M, C, mu(net.conv[b.c2].bn), sc(net.conv[b.c2].bn), be(net.conv[b.c2].bn), res, 1, t.OUT,
-                        st));
+      EKYA_HIP(bn_train(net.conv[b.c2].bn, t.Z2, M, res, 1, t.OUT));
       cur = t.OUT;
     }
     if (s == 4)  // average pool + classifier in one kernel
