@@ -769,9 +769,21 @@ __global__ __launch_bounds__(256) void head_fwd_kernel(const T* x, int HW, const
       float acc[E];
 #pragma unroll
       for (int e = 0; e < E; ++e) acc[e] = 0.f;
-      for (int k = wave; k < HW; k += 4) {
+      const T* xp = x + (long long)n * HW * I + u * E;
+      int k = wave;
+      for (; k + 12 < HW; k += 16) {  // four pixels' loads in flight, added in pixel order
+        float v[4][E];
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          unit_to_f<T>(*reinterpret_cast<const uint4*>(xp + (long long)(k + 4 * q) * I), v[q]);
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+#pragma unroll
+          for (int e = 0; e < E; ++e) acc[e] += v[q][e];
+      }
+      for (; k < HW; k += 4) {
         float v[E];
-        unit_to_f<T>(*reinterpret_cast<const uint4*>(x + ((long long)n * HW + k) * I + u * E), v);
+        unit_to_f<T>(*reinterpret_cast<const uint4*>(xp + (long long)k * I), v);
 #pragma unroll
         for (int e = 0; e < E; ++e) acc[e] += v[e];
       }
@@ -811,35 +823,53 @@ __global__ __launch_bounds__(256) void head_fwd_kernel(const T* x, int HW, const
   }
 }
 
-// Softmax cross-entropy gradient of one row: dz[j] = (softmax_j - [j == y]) / N;
-// returns false (dz = 0) for a label outside [0, J).
-__device__ __forceinline__ bool ce_row(const float* zr, int y, int J, int N, float* dz, float& loss,
-                                       int& correct) {
+constexpr int HEAD_JMAX = 16;  // classes handled by the fused backward (else the separate kernels)
+constexpr int HEAD_WB = 8;     // blocks of 64 features for the weight gradient (I = 512)
+constexpr int HEAD_PC = 8;     // pixels per block of the pooled-feature gradient
+
+// Softmax cross-entropy gradient of one row (J <= HEAD_JMAX): dz[j] =
+// (softmax_j - [j == y]) / N, zero for j >= J; false (dz = 0) for a label
+// outside [0, J).  The logits are loaded up front.
+__device__ __forceinline__ bool ce_row(const float* zr, int y, int J, int N,
+                                       float (&dz)[HEAD_JMAX], float& loss, int& correct) {
+  float v[HEAD_JMAX];
+#pragma unroll
+  for (int j = 0; j < HEAD_JMAX; ++j) v[j] = j < J ? zr[j] : 0.f;
   if (y < 0 || y >= J) {
-    for (int j = 0; j < J; ++j) dz[j] = 0.f;
+#pragma unroll
+    for (int j = 0; j < HEAD_JMAX; ++j) dz[j] = 0.f;
     loss = 0.f;
     correct = 0;
     return false;
   }
-  float m = zr[0];
+  float m = v[0], vy = v[0];
   int am = 0;
-  for (int j = 1; j < J; ++j)
-    if (zr[j] > m) {
-      m = zr[j];
+#pragma unroll
+  for (int j = 1; j < HEAD_JMAX; ++j) {
+    if (j < J && v[j] > m) {
+      m = v[j];
       am = j;
     }
+    if (j == y) vy = v[j];
+  }
   float se = 0.f;
-  for (int j = 0; j < J; ++j) se += expf(zr[j] - m);
+#pragma unroll
+  for (int j = 0; j < HEAD_JMAX; ++j)
+    if (j < J) se += expf(v[j] - m);
   const float lse = m + logf(se);
-  loss = lse - zr[y];
+  loss = lse - vy;
   correct = (am == y);
-  for (int j = 0; j < J; ++j) dz[j] = (expf(zr[j] - lse) - (j == y ? 1.f : 0.f)) / (float)N;
+#pragma unroll
+  for (int j = 0; j < HEAD_JMAX; ++j)
+    dz[j] = j < J ? (expf(v[j] - lse) - (j == y ? 1.f : 0.f)) / (float)N : 0.f;
   return true;
 }
 
-constexpr int HEAD_JMAX = 16;  // classes handled by the fused backward (else the separate kernels)
-constexpr int HEAD_WB = 8;     // blocks of 64 features for the weight gradient (I = 512)
-
+// Blocks [0, HEAD_WB): classifier gradients dW (64 features per block) and,
+// in block 0, db / mean loss / correct count / non-finite flag.  Blocks
+// after: the pooled-feature gradient spread over the HW pixels,
+// dout[n][p][c] = (sum_j dz_j W[j][c]) / HW, one sample and HEAD_PC pixels
+// per block.
 template <typename T>
 __global__ __launch_bounds__(256) void head_bwd_kernel(const float* z, const int32_t* labels,
                                                        const int32_t* idx, int N, int J,
@@ -853,15 +883,15 @@ __global__ __launch_bounds__(256) void head_bwd_kernel(const float* z, const int
   __shared__ int rc[256], rb[256];
   float dz[HEAD_JMAX];
   if (blockIdx.x < (unsigned)HEAD_WB) {
-    // weight gradient for features i = 64 b + t % 64; samples in 4 slices of
-    // each 256-row chunk, the slices added in order
+    // features i = 64 b + t % 64; samples of each 256-row chunk in 4 slices,
+    // the slices added in order
     __shared__ float part[4][HEAD_JMAX][64];
     const int il = t & 63, sl = t >> 6;
     const int i = blockIdx.x * 64 + il;
-    float acc[HEAD_JMAX], dbs[HEAD_JMAX], L = 0.f;
+    float acc[HEAD_JMAX], dsum = 0.f, L = 0.f;
     int C = 0, bad = 0;
 #pragma unroll
-    for (int j = 0; j < HEAD_JMAX; ++j) acc[j] = dbs[j] = 0.f;
+    for (int j = 0; j < HEAD_JMAX; ++j) acc[j] = 0.f;
     for (int n0 = 0; n0 < N; n0 += 256) {
       const int cnt = min(256, N - n0);
       __syncthreads();
@@ -870,26 +900,38 @@ __global__ __launch_bounds__(256) void head_bwd_kernel(const float* z, const int
         int c;
         const bool ok = ce_row(z + (long long)(n0 + t) * J, labels[idx ? idx[n0 + t] : n0 + t], J,
                                N, dz, l, c);
-        for (int j = 0; j < J; ++j) rdz[t][j] = dz[j];
+#pragma unroll
+        for (int j = 0; j < HEAD_JMAX; ++j) rdz[t][j] = dz[j];
         rl[t] = l;
         rc[t] = c;
         rb[t] = (!ok || !isfinite(l)) ? 1 : 0;
       }
       __syncthreads();
       const int per = (cnt + 3) / 4;
-      for (int k = sl * per; k < min(cnt, (sl + 1) * per); ++k) {
-        const float fv = i < I ? f[(long long)(n0 + k) * I + i] : 0.f;
+      const int k0 = sl * per, k1 = min(cnt, k0 + per);
+      for (int k = k0; k < k1; k += 8) {  // eight samples' features loaded up front
+        float fv[8];
 #pragma unroll
-        for (int j = 0; j < HEAD_JMAX; ++j)
-          if (j < J) acc[j] += rdz[k][j] * fv;
+        for (int q = 0; q < 8; ++q)
+          fv[q] = (k + q < k1 && i < I) ? f[(long long)(n0 + k + q) * I + i] : 0.f;
+#pragma unroll
+        for (int q = 0; q < 8; ++q)
+          if (k + q < k1)
+#pragma unroll
+            for (int j = 0; j < HEAD_JMAX; ++j)
+              if (j < J) acc[j] += rdz[k + q][j] * fv[q];
       }
-      if (blockIdx.x == 0 && t == 0)
-        for (int k = 0; k < cnt; ++k) {
-          L += rl[k];
-          C += rc[k];
-          bad |= rb[k];
-          for (int j = 0; j < J; ++j) dbs[j] += rdz[k][j];
+      if (blockIdx.x == 0) {  // sample sums in sample order, one quantity per wave
+        if (t < J) {
+          for (int k = 0; k < cnt; ++k) dsum += rdz[k][t];
+        } else if (t == 64) {
+          for (int k = 0; k < cnt; ++k) L += rl[k];
+        } else if (t == 128) {
+          for (int k = 0; k < cnt; ++k) C += rc[k];
+        } else if (t == 192) {
+          for (int k = 0; k < cnt; ++k) bad |= rb[k];
         }
+      }
     }
 #pragma unroll
     for (int j = 0; j < HEAD_JMAX; ++j) part[sl][j][il] = acc[j];
@@ -897,41 +939,45 @@ __global__ __launch_bounds__(256) void head_bwd_kernel(const float* z, const int
     if (sl == 0 && i < I)
       for (int j = 0; j < J; ++j)
         dW[(long long)j * I + i] = ((part[0][j][il] + part[1][j][il]) + part[2][j][il]) + part[3][j][il];
-    if (blockIdx.x == 0 && t == 0) {
-      for (int j = 0; j < J; ++j) db[j] = dbs[j];
-      out[0] = L / (float)N;
-      out[1] = (float)C;
-      out[2] = (float)bad;
+    if (blockIdx.x == 0) {
+      if (t < J) db[t] = dsum;
+      if (t == 64) out[0] = L / (float)N;
+      if (t == 128) out[1] = (float)C;
+      if (t == 192) out[2] = (float)bad;
     }
     return;
   }
   if (!dout) return;
-  // average-pool backward of d pooled = dz W: dout[n][p][c] = (sum_j dz_j W[j][c]) / HW.
-  // A block covers 256 / (I / E) samples; their softmax rows are computed once.
-  const int units = I / E, spb = 256 / units;
-  const int nb0 = (blockIdx.x - HEAD_WB) * spb;
-  if (t < spb && nb0 + t < N) {
+  const int nchunk = (HW + HEAD_PC - 1) / HEAD_PC;
+  const int bb = blockIdx.x - HEAD_WB, n = bb / nchunk, pc = bb % nchunk;
+  if (n >= N) return;
+  if (t == 0) {
     float l;
     int c;
-    ce_row(z + (long long)(nb0 + t) * J, labels[idx ? idx[nb0 + t] : nb0 + t], J, N, dz, l, c);
-    for (int j = 0; j < J; ++j) rdz[t][j] = dz[j];
+    ce_row(z + (long long)n * J, labels[idx ? idx[n] : n], J, N, dz, l, c);
+#pragma unroll
+    for (int j = 0; j < HEAD_JMAX; ++j) rdz[0][j] = dz[j];
   }
   __syncthreads();
-  const int sn = t / units, u = t % units, n = nb0 + sn;
-  if (sn >= spb || n >= N) return;
+  const int units = I / E, u = t % units, ps = t / units, nsl = 256 / units;
   const float inv = 1.f / (float)HW;
   float d[E];
 #pragma unroll
   for (int e = 0; e < E; ++e) d[e] = 0.f;
-  for (int j = 0; j < J; ++j) {
-    const float w = rdz[sn][j];
 #pragma unroll
-    for (int e = 0; e < E; ++e) d[e] += w * W[(long long)j * I + u * E + e];
-  }
+  for (int j = 0; j < HEAD_JMAX; ++j)
+    if (j < J) {
+      const float w = rdz[0][j];
+      float wv[E];
+      chan_load<E>(W + (long long)j * I, u * E, wv);
+#pragma unroll
+      for (int e = 0; e < E; ++e) d[e] += w * wv[e];
+    }
 #pragma unroll
   for (int e = 0; e < E; ++e) d[e] *= inv;
   const uint4 v = f_to_unit<T>(d);
-  for (int p = 0; p < HW; ++p)
+  const int p1 = min(HW, (pc + 1) * HEAD_PC);
+  for (int p = pc * HEAD_PC + ps; p < p1; p += nsl)
     reinterpret_cast<uint4*>(dout + ((long long)n * HW + p) * I)[u] = v;
 }
 
@@ -1316,8 +1362,7 @@ hipError_t head_backward(int dt, const float* z, const int32_t* labels, const in
                          void* dout, int HW, float* out, hipStream_t stream) {
   if (!head_backward_fused(J, I) || I % dtype_vec(dt) != 0 || 256 % (I / dtype_vec(dt)) != 0)
     return hipErrorInvalidValue;
-  const int spb = 256 / (I / dtype_vec(dt));
-  const int dblocks = dout ? cdiv(N, spb) : 0;
+  const int dblocks = dout ? N * cdiv(HW, HEAD_PC) : 0;
   return by_type(dt, [&](auto* tp) {
     using T = std::remove_pointer_t<decltype(tp)>;
     hipLaunchKernelGGL(head_bwd_kernel<T>, dim3(HEAD_WB + dblocks), dim3(256), 0, stream, z,
