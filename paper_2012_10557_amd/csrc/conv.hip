@@ -628,15 +628,23 @@ struct DmaFwdOp {
   long long Ktot;
   const bf16* ptr[IPW];
   int h0[IPW], w0[IPW];
+  int rowoff[IPW];  // input pixel (h0, w0) within its image, in elements (may be negative)
   bool ok[IPW];
   int tr, ts, tc;
+  int split;
 
-  __device__ void init(const Args& a, int m0, int n0, int split, int wave, int lane) {
+  // reduction stages [s0, s1) of a split: 64-element steps of R*S*C
+  static __device__ void stage_range(const Args& a, int split, int& s0, int& s1) {
+    const int ns = a.g.R * a.g.S * a.g.C / 64;
+    s0 = min(ns, split * a.so.stages_per_split);
+    s1 = min(ns, s0 + a.so.stages_per_split);
+  }
+
+  __device__ void init(const Args& a, int m0, int n0, int split_, int wave, int lane) {
     const ConvGeom& g = a.g;
+    split = split_;
     Ktot = (long long)g.R * g.S * g.C;
-    const int ns = (int)(Ktot / 64);
-    s_begin = min(ns, split * a.so.stages_per_split);
-    s_end = min(ns, s_begin + a.so.stages_per_split);
+    stage_range(a, split, s_begin, s_end);
     const int npix = g.N * g.P * g.Q;
     const int r8 = lane >> 3, u = (lane & 7) ^ r8;
 #pragma unroll
@@ -646,7 +654,7 @@ struct DmaFwdOp {
         const int row = m0 + oct * 8 + r8;
         ok[j] = row < g.K;
         ptr[j] = a.w + (ok[j] ? row : 0) * Ktot + u * 8;
-        h0[j] = w0[j] = 0;
+        h0[j] = w0[j] = rowoff[j] = 0;
       } else {
         const int pix = n0 + (oct - GA) * 8 + r8;
         ok[j] = pix < npix;
@@ -655,6 +663,7 @@ struct DmaFwdOp {
         const int p = rem / g.Q, q = rem % g.Q;
         h0[j] = p * g.stride - g.pad;
         w0[j] = q * g.stride - g.pad;
+        rowoff[j] = (h0[j] * g.W + w0[j]) * g.C;
         ptr[j] = a.x + (long long)n * g.H * g.W * g.C + u * 8;
       }
     }
@@ -664,23 +673,24 @@ struct DmaFwdOp {
     tr = rs / g.S;
     ts = rs - tr * g.S;
   }
-  __device__ void issue(const Args& a, int st, uint4* slot, int wave) {
+  // Per load: two adds and two unsigned compares for the padding test, one
+  // 32-bit offset; the tap's part (tr W + ts) C + tc is wave-uniform.
+  __device__ void issue(const Args& a, int st, uint4* slot, int wave, const void* zero) {
     const ConvGeom& g = a.g;
     const long long k0 = (long long)st * 64;
+    const int tap = (tr * g.W + ts) * g.C + tc;
 #pragma unroll
     for (int j = 0; j < IPW; ++j) {
       const int oct = wave + 4 * j;
-      const bf16* src;
-      bool in;
+      const void* src;
       if (oct < GA) {
-        src = ptr[j] + k0;
-        in = ok[j];
+        src = ok[j] ? (const void*)(ptr[j] + k0) : zero;
       } else {
         const int h = h0[j] + tr, w = w0[j] + ts;
-        in = ok[j] && (unsigned)h < (unsigned)g.H && (unsigned)w < (unsigned)g.W;
-        src = ptr[j] + ((long long)h * g.W + w) * g.C + tc;
+        const bool in = ok[j] && (unsigned)h < (unsigned)g.H && (unsigned)w < (unsigned)g.W;
+        src = in ? (const void*)(ptr[j] + (rowoff[j] + tap)) : zero;
       }
-      dma16(in ? (const void*)src : (const void*)g_zero_unit, slot + oct * 64);
+      dma16(src, slot + oct * 64);
     }
     tc += 64;
     if (tc >= g.C) {
@@ -697,7 +707,7 @@ struct DmaFwdOp {
     if (row >= g.K || col >= npix) return;
     const long long off = (long long)col * g.K + row;
     if (a.so.splits > 1) {
-      float* dst = a.so.part + (long long)blockIdx.y * npix * g.K + off;
+      float* dst = a.so.part + (long long)split * npix * g.K + off;
       *reinterpret_cast<float4*>(dst) = make_float4(v[0], v[1], v[2], v[3]);
       return;
     }
@@ -743,15 +753,23 @@ struct DmaDgradOp {
   long long Ktot;
   const bf16* ptr[IPW];
   int hp[IPW], wp[IPW];  // input pixel + pad
+  int rowoff[IPW];       // stride 1: output-gradient pixel (hp, wp), in elements
   bool ok[IPW];
   int tr, ts, tk;
+  int split;
 
-  __device__ void init(const Args& a, int m0, int n0, int split, int wave, int lane) {
+  // reduction stages [s0, s1) of a split: 64-element steps of R*S*K
+  static __device__ void stage_range(const Args& a, int split, int& s0, int& s1) {
+    const int ns = a.g.R * a.g.S * a.g.K / 64;
+    s0 = min(ns, split * a.so.stages_per_split);
+    s1 = min(ns, s0 + a.so.stages_per_split);
+  }
+
+  __device__ void init(const Args& a, int m0, int n0, int split_, int wave, int lane) {
     const ConvGeom& g = a.g;
+    split = split_;
     Ktot = (long long)g.R * g.S * g.K;
-    const int ns = (int)(Ktot / 64);
-    s_begin = min(ns, split * a.so.stages_per_split);
-    s_end = min(ns, s_begin + a.so.stages_per_split);
+    stage_range(a, split, s_begin, s_end);
     const int npix = g.N * g.H * g.W;
     const int r8 = lane >> 3, u = (lane & 7) ^ r8;
 #pragma unroll
@@ -761,7 +779,7 @@ struct DmaDgradOp {
         const int row = m0 + oct * 8 + r8;
         ok[j] = row < g.C;
         ptr[j] = a.wt + (ok[j] ? row : 0) * Ktot + u * 8;
-        hp[j] = wp[j] = 0;
+        hp[j] = wp[j] = rowoff[j] = 0;
       } else {
         const int pix = n0 + (oct - GA) * 8 + r8;
         ok[j] = pix < npix;
@@ -769,6 +787,7 @@ struct DmaDgradOp {
         const int n = pp / (g.H * g.W), rem = pp % (g.H * g.W);
         hp[j] = rem / g.W + g.pad;
         wp[j] = rem % g.W + g.pad;
+        rowoff[j] = (hp[j] * g.Q + wp[j]) * g.K;
         ptr[j] = a.dy + (long long)n * g.P * g.Q * g.K + u * 8;
       }
     }
@@ -778,25 +797,30 @@ struct DmaDgradOp {
     tr = rs / g.S;
     ts = rs - tr * g.S;
   }
-  __device__ void issue(const Args& a, int st, uint4* slot, int wave) {
+  // Stride 1: output-gradient pixel (hp - tr, wp - ts), the lane's row offset
+  // plus a wave-uniform one; stride 2: (h / 2, w / 2) for even h and w.
+  __device__ void issue(const Args& a, int st, uint4* slot, int wave, const void* zero) {
     const ConvGeom& g = a.g;
     const long long k0 = (long long)st * 64;
-    const int sh = g.stride == 2 ? 1 : 0;
+    const int tap = tk - (tr * g.Q + ts) * g.K;
 #pragma unroll
     for (int j = 0; j < IPW; ++j) {
       const int oct = wave + 4 * j;
-      const bf16* src;
-      bool in;
+      const void* src;
       if (oct < GA) {
-        src = ptr[j] + k0;
-        in = ok[j];
+        src = ok[j] ? (const void*)(ptr[j] + k0) : zero;
       } else {
         const int h = hp[j] - tr, w = wp[j] - ts;
-        const int p = h >> sh, q = w >> sh;
-        in = ok[j] && h >= 0 && w >= 0 && ((h | w) & sh) == 0 && p < g.P && q < g.Q;
-        src = ptr[j] + ((long long)p * g.Q + q) * g.K + tk;
+        if (g.stride == 1) {
+          const bool in = ok[j] && (unsigned)h < (unsigned)g.P && (unsigned)w < (unsigned)g.Q;
+          src = in ? (const void*)(ptr[j] + (rowoff[j] + tap)) : zero;
+        } else {
+          const int p = h >> 1, q = w >> 1;
+          const bool in = ok[j] && h >= 0 && w >= 0 && ((h | w) & 1) == 0 && p < g.P && q < g.Q;
+          src = in ? (const void*)(ptr[j] + ((p * g.Q + q) * g.K + tk)) : zero;
+        }
       }
-      dma16(in ? (const void*)src : (const void*)g_zero_unit, slot + oct * 64);
+      dma16(src, slot + oct * 64);
     }
     tk += 64;
     if (tk >= g.K) {
@@ -813,7 +837,7 @@ struct DmaDgradOp {
     if (row >= g.C || col >= npix) return;
     const long long off = (long long)col * g.C + row;
     if (a.so.splits > 1) {
-      float* dst = a.so.part + (long long)blockIdx.y * npix * g.C + off;
+      float* dst = a.so.part + (long long)split * npix * g.C + off;
       *reinterpret_cast<float4*>(dst) = make_float4(v[0], v[1], v[2], v[3]);
       return;
     }
@@ -843,7 +867,11 @@ __global__ __launch_bounds__(NT) void gemm_dma_kernel(typename Op::Args a) {
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wm = wave / WGN, wn = wave % WGN;
-  const int t = xcd_tile(blockIdx.x, a.tiles_m * a.tiles_n);
+  // one-dimensional grid of (split, tile) items, split-major, each XCD a
+  // contiguous range: the blocks of an XCD share one slice of the reduction
+  const int tiles = a.tiles_m * a.tiles_n;
+  const int item = xcd_tile(blockIdx.x, tiles * a.so.splits);
+  const int split = item / tiles, t = item - split * tiles;
   const int m0 = (t % a.tiles_m) * BM, n0 = (t / a.tiles_m) * BN;
   // lane's unit within a 16-row fragment: row fr, k-unit kf * 4 + fkc
   const int fr = lane & 15, fkc = lane >> 4;
@@ -851,8 +879,10 @@ __global__ __launch_bounds__(NT) void gemm_dma_kernel(typename Op::Args a) {
   const int off1 = fr * 8 + ((4 + fkc) ^ (fr & 7));
 
   Op op;
-  op.init(a, m0, n0, blockIdx.y, wave, lane);
+  op.init(a, m0, n0, split, wave, lane);
   const int s0 = op.s_begin, s1 = op.s_end;
+  const void* zero = g_zero_unit;
+  asm volatile("" : "+s"(zero));  // keep it in registers rather than re-deriving it per load
 
   f32x4 acc[TI][TJ];
 #pragma unroll
@@ -862,7 +892,7 @@ __global__ __launch_bounds__(NT) void gemm_dma_kernel(typename Op::Args a) {
 
 #pragma unroll
   for (int p = 0; p < NST - 1; ++p)
-    if (s0 + p < s1) op.issue(a, s0 + p, smem + p * SU, wave);
+    if (s0 + p < s1) op.issue(a, s0 + p, smem + p * SU, wave, zero);
 
   int slot = 0;
   for (int st = s0; st < s1; ++st) {
@@ -873,7 +903,7 @@ __global__ __launch_bounds__(NT) void gemm_dma_kernel(typename Op::Args a) {
     stage_barrier();
     if (st + NST - 1 < s1) {
       const int nslot = slot == 0 ? NST - 1 : slot - 1;
-      op.issue(a, st + NST - 1, smem + nslot * SU, wave);
+      op.issue(a, st + NST - 1, smem + nslot * SU, wave, zero);
     }
     const uint4* As = smem + slot * SU + (wm * WM) * 8;
     const uint4* Bs = smem + slot * SU + (BM + wn * WN) * 8;
@@ -900,6 +930,108 @@ __global__ __launch_bounds__(NT) void gemm_dma_kernel(typename Op::Args a) {
     for (int j = 0; j < TJ; ++j) {
       float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
       op.out4(a, m0 + wm * WM + i * 16 + 4 * lg, n0 + wn * WN + j * 16 + lr, v);
+    }
+}
+
+// Warp-specialised variant for BM = 256 rows: WGM x WGN compute waves (each a
+// 64 x 64 block of 16x16 MFMA tiles, two per SIMD) and four loader waves.  The
+// loader waves keep the copies of the next NST - 1 stages in flight (the
+// CU's vector-memory path, not the MFMAs, is what a wave issuing its own
+// copies waits on); the compute waves only read LDS fragments and issue
+// MFMAs.  One barrier per stage: before it the loaders have waited for stage
+// st + 1 and the compute waves have finished reading stage st, whose slot the
+// loaders refill after it.  Every wave executes the same barriers.
+constexpr int WS_LOADERS = 4;
+
+template <int BM, int BN, int NST, class Op>
+__global__ __launch_bounds__((BM / 64) * (BN / 64) * 64 + WS_LOADERS * 64) void gemm_ws_kernel(
+    typename Op::Args a) {
+  constexpr int WGN = BN / 64, CW = (BM / 64) * WGN;
+  constexpr int LPS = Op::IPW;            // copies per loader lane per stage
+  constexpr int SU = (BM + BN) * 8;       // 16-byte units per stage
+  static_assert(LPS * (NST - 2) < 64, "vmcnt range");
+  __shared__ uint4 smem[NST * SU];
+
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int tiles = a.tiles_m * a.tiles_n;
+  const int item = xcd_tile(blockIdx.x, tiles * a.so.splits);
+  const int split = item / tiles, t = item - split * tiles;
+  const int m0 = (t % a.tiles_m) * BM, n0 = (t / a.tiles_m) * BN;
+  int s0, s1;
+  Op::stage_range(a, split, s0, s1);
+
+  // The two roles run separate loops (their registers are never live
+  // together) with the same barrier count: one before the loop, one per stage.
+  if (wave >= CW) {
+    const int lw = wave - CW;
+    Op op;
+    op.init(a, m0, n0, split, lw, lane);
+    const void* zero = g_zero_unit;
+    asm volatile("" : "+s"(zero));
+#pragma unroll
+    for (int p = 0; p < NST - 1; ++p)
+      if (s0 + p < s1) op.issue(a, s0 + p, smem + p * SU, lw, zero);
+    if (s0 + NST - 2 < s1)
+      wait_vmcnt<LPS * (NST - 2)>();
+    else
+      wait_vmcnt<0>();
+    stage_barrier();
+    int slot = 0;
+    for (int st = s0; st < s1; ++st) {
+      if (st + NST - 1 < s1) {
+        const int nslot = slot == 0 ? NST - 1 : slot - 1;
+        op.issue(a, st + NST - 1, smem + nslot * SU, lw, zero);
+        wait_vmcnt<LPS * (NST - 2)>();  // stage st + 1 has landed
+      } else {
+        wait_vmcnt<0>();
+      }
+      stage_barrier();
+      if (++slot == NST) slot = 0;
+    }
+    return;
+  }
+
+  const int wm = wave / WGN, wn = wave % WGN;
+  const int fr = lane & 15, fkc = lane >> 4;
+  const int off0 = fr * 8 + (fkc ^ (fr & 7));
+  const int off1 = fr * 8 + ((4 + fkc) ^ (fr & 7));
+  f32x4 acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  stage_barrier();
+  int slot = 0;
+  for (int st = s0; st < s1; ++st) {
+    const uint4* As = smem + slot * SU + (wm * 64) * 8;
+    const uint4* Bs = smem + slot * SU + (BM + wn * 64) * 8;
+#pragma unroll
+    for (int kf = 0; kf < 2; ++kf) {
+      const int off = kf == 0 ? off0 : off1;
+      uint4 fa[4], fb[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) fa[i] = As[i * 128 + off];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) fb[j] = Bs[j * 128 + off];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) mma_unit(acc[i][j], fa[i], fb[j], (bf16*)nullptr);
+    }
+    stage_barrier();
+    if (++slot == NST) slot = 0;
+  }
+
+  Op op;
+  op.split = split;
+  const int lr = lane & 15, lg = lane >> 4;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
+      op.out4(a, m0 + wm * 64 + i * 16 + 4 * lg, n0 + wn * 64 + j * 16 + lr, v);
     }
 }
 
@@ -1293,6 +1425,16 @@ struct DmaPlan {
 };
 
 DmaPlan plan_dma(int rows, long long cols, int ns, bool allow_split) {
+  if (rows % 256 == 0 && ns >= 8) {
+    // warp-specialised 256 x 128 tiles, one block per CU: split the
+    // reduction until the blocks about fill the chip once (>= 4 stages each)
+    const long long tiles = (long long)(rows / 256) * cdivl(cols, 128);
+    if (tiles >= 256 || !allow_split) return {256, 128, 1, ns};
+    int s = (int)std::min<long long>(256 / tiles, 16);
+    s = std::max(1, std::min(s, std::max(1, ns / 4)));
+    const int sps = cdiv(ns, s);
+    return {256, 128, cdiv(ns, sps), sps};
+  }
   struct Cand {
     int bm, bn, per_cu;
   };
@@ -1317,7 +1459,7 @@ hipError_t launch_dma(typename OpT<BM, BN>::Args a, long long cols, int rows, hi
                       Cost cost, const char* name) {
   a.tiles_m = cdiv(rows, BM);
   a.tiles_n = (int)cdivl(cols, BN);
-  dim3 grid(a.tiles_m * a.tiles_n, a.so.splits);
+  dim3 grid(a.tiles_m * a.tiles_n * a.so.splits);
   KernelTimer* t = t_timer;
   hipEvent_t e0 = nullptr, e1 = nullptr;
   if (t) {
@@ -1336,9 +1478,36 @@ hipError_t launch_dma(typename OpT<BM, BN>::Args a, long long cols, int rows, hi
   return e;
 }
 
+template <int BM, int BN, template <int, int> class OpT>
+hipError_t launch_ws(typename OpT<BM, BN>::Args a, long long cols, int rows, hipStream_t stream,
+                     Cost cost, const char* name) {
+  constexpr int NST = 3;
+  a.tiles_m = cdiv(rows, BM);
+  a.tiles_n = (int)cdivl(cols, BN);
+  dim3 grid(a.tiles_m * a.tiles_n * a.so.splits);
+  KernelTimer* t = t_timer;
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  if (t) {
+    e0 = t->take();
+    e1 = t->take();
+    EKYA_HIP(hipEventRecord(e0, stream));
+  }
+  hipLaunchKernelGGL((gemm_ws_kernel<BM, BN, NST, OpT<BM, BN>>), grid,
+                     dim3((BM / 64) * (BN / 64) * 64 + WS_LOADERS * 64), 0, stream, a);
+  hipError_t e = hipGetLastError();
+  if (t && e == hipSuccess) {
+    EKYA_HIP(hipEventRecord(e1, stream));
+    t->recs.push_back({std::string(name) + "<bf16," + std::to_string(BM) + "," +
+                           std::to_string(BN) + ",ws>",
+                       cost.flops, cost.bytes, e0, e1});
+  }
+  return e;
+}
+
 template <template <int, int> class OpT, class Args>
 hipError_t dispatch_dma(Args a, const DmaPlan& p, long long cols, int rows, hipStream_t stream,
                         Cost cost, const char* name) {
+  if (p.bm == 256 && p.bn == 128) return launch_ws<256, 128, OpT>(a, cols, rows, stream, cost, name);
   if (p.bm == 128 && p.bn == 128) return launch_dma<128, 128, 2, OpT>(a, cols, rows, stream, cost, name);
   if (p.bm == 128 && p.bn == 64) return launch_dma<128, 64, 2, OpT>(a, cols, rows, stream, cost, name);
   if (p.bm == 64 && p.bn == 256) return launch_dma<64, 256, 1, OpT>(a, cols, rows, stream, cost, name);
