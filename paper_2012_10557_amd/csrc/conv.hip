@@ -1061,6 +1061,7 @@ struct WgDmaArgs {
   float* out;       // [split][K][R*S*C], or dw itself with one split
   int m_per_split;  // pixels per split, a multiple of 64
   int tiles_m, tiles_n;
+  int splits;
 };
 
 template <int BM, int BN>
@@ -1186,6 +1187,174 @@ __global__ __launch_bounds__(NT) void wgrad_dma_kernel(WgDmaArgs a) {
     for (int j = 0; j < TJ; ++j) {
       const int row = m0 + wm * WM + i * 16 + 4 * lg, col = n0 + wn * WN + j * 16 + lr;
       float* dst = a.out + ((long long)blockIdx.y * g.K + col) * RSC + row;
+      *reinterpret_cast<float4*>(dst) =
+          make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+    }
+}
+
+// Warp-specialised weight gradient for BM = 256 rows (channels of one filter
+// tap, so C % 256 == 0) x BN output channels: four loader waves gather the
+// stage's 64 input-pixel rows and 64 output-gradient rows (same LDS layout as
+// above) NST - 1 stages ahead; the compute waves (64 x 64 each) read the
+// operands with LDS transpose reads and issue the MFMAs.  A loader lane keeps
+// its input pixel as (n, p, q) plus a 32-bit element offset, stepped by 64
+// pixels per stage.  Barriers as in gemm_ws_kernel.
+template <int BM, int BN, int NST>
+__global__ __launch_bounds__((BM / 64) * (BN / 64) * 64 + WS_LOADERS * 64) void wgrad_ws_kernel(
+    WgDmaArgs a) {
+  constexpr int WGN = BN / 64, CW = (BM / 64) * WGN;
+  constexpr int UA = BM / 8, UB = BN / 8;     // 16-byte units per pixel row
+  constexpr int RA = 64 / UA, RB = 64 / UB;   // pixel rows per copy instruction
+  constexpr int IA = 64 / RA, IB = 64 / RB;   // copy instructions per stage
+  constexpr int LPS = (IA + IB) / 4, LA = IA / 4;
+  static_assert(IA % 4 == 0 && IB % 4 == 0, "instructions split over 4 loader waves");
+  static_assert(LPS * (NST - 2) < 64, "vmcnt range");
+  constexpr int SA = BM / 16, SB = BN / 16;   // 32-byte segments per row
+  constexpr int STAGE_BYTES = 64 * (BM + BN) * 2;
+  __shared__ __align__(16) char smem[NST * STAGE_BYTES];
+
+  const ConvGeom& g = a.g;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int tiles = a.tiles_m * a.tiles_n;
+  const int item = xcd_tile(blockIdx.x, tiles * a.splits);
+  const int split = item / tiles, t = item - split * tiles;
+  const int m0 = (t % a.tiles_m) * BM, n0 = (t / a.tiles_m) * BN;
+  const int M = g.N * g.P * g.Q;
+  const int mb = split * a.m_per_split;
+  const int me = min(M, mb + a.m_per_split);
+  const int ns = me > mb ? (me - mb + 63) / 64 : 0;
+
+  if (wave >= CW) {
+    const int lw = wave - CW;
+    const void* zero = g_zero_unit;
+    asm volatile("" : "+s"(zero));
+    const int rs = m0 / g.C, c0 = m0 - rs * g.C;
+    const int tr = rs / g.S, ts = rs - tr * g.S;
+    const int PQ = g.P * g.Q;
+    const int dq = 64 % g.Q, dp = (64 / g.Q) % g.P, dn = 64 / PQ;
+    const int sC = g.stride * g.C, sWC = g.stride * g.W * g.C, HWC = g.H * g.W * g.C;
+    int am[LA], pp[LA], qq[LA], xo[LA];
+#pragma unroll
+    for (int j = 0; j < LA; ++j) {
+      const int pr = (lw + 4 * j) * RA + lane / UA;
+      am[j] = mb + pr;
+      const int m = am[j] < M ? am[j] : 0;
+      const int n = m / PQ, rem = m - n * PQ;
+      pp[j] = rem / g.Q;
+      qq[j] = rem - pp[j] * g.Q;
+      // element offset of input pixel (n, p stride - pad + tr, q stride - pad + ts), channel c0
+      xo[j] = n * HWC + ((pp[j] * g.stride - g.pad + tr) * g.W + qq[j] * g.stride - g.pad + ts) * g.C + c0;
+    }
+    auto issue = [&](int st, char* slot) {
+#pragma unroll
+      for (int j = 0; j < LPS; ++j) {
+        const int ins = lw + 4 * j;
+        if (j < LA) {
+          const int pr = ins * RA + lane / UA, sl = lane % UA;
+          const int u = 2 * ((sl >> 1) ^ (pr % SA)) + (sl & 1);
+          const int h = pp[j] * g.stride - g.pad + tr, w = qq[j] * g.stride - g.pad + ts;
+          const bool in = am[j] < me && (unsigned)h < (unsigned)g.H && (unsigned)w < (unsigned)g.W;
+          dma16(in ? (const void*)(a.x + xo[j] + u * 8) : zero,
+                reinterpret_cast<uint4*>(slot + ins * 1024));
+          am[j] += 64;
+          qq[j] += dq;
+          xo[j] += dq * sC;
+          if (qq[j] >= g.Q) {
+            qq[j] -= g.Q;
+            ++pp[j];
+            xo[j] += sWC - g.Q * sC;
+          }
+          pp[j] += dp;
+          xo[j] += dp * sWC;
+          if (pp[j] >= g.P) {
+            pp[j] -= g.P;
+            xo[j] += HWC - g.P * sWC;
+          }
+          xo[j] += dn * HWC;
+        } else {
+          const int ib = ins - IA;
+          const int pr = ib * RB + lane / UB, sl = lane % UB;
+          const int u = 2 * ((sl >> 1) ^ (pr % SB)) + (sl & 1);
+          const int m = mb + st * 64 + pr;
+          dma16(m < me ? (const void*)(a.dy + m * g.K + n0 + u * 8) : zero,
+                reinterpret_cast<uint4*>(slot + 64 * BM * 2 + ib * 1024));
+        }
+      }
+    };
+#pragma unroll
+    for (int p = 0; p < NST - 1; ++p)
+      if (p < ns) issue(p, smem + p * STAGE_BYTES);
+    if (NST - 2 < ns)
+      wait_vmcnt<LPS * (NST - 2)>();
+    else
+      wait_vmcnt<0>();
+    stage_barrier();
+    int slot = 0;
+    for (int st = 0; st < ns; ++st) {
+      if (st + NST - 1 < ns) {
+        const int nslot = slot == 0 ? NST - 1 : slot - 1;
+        issue(st + NST - 1, smem + nslot * STAGE_BYTES);
+        wait_vmcnt<LPS * (NST - 2)>();  // stage st + 1 has landed
+      } else {
+        wait_vmcnt<0>();
+      }
+      stage_barrier();
+      if (++slot == NST) slot = 0;
+    }
+    return;
+  }
+
+  const int wm = wave / WGN, wn = wave % WGN;
+  const int gq = lane >> 4, jr = (lane & 15) >> 2, qd = lane & 3;
+  f32x4 acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  stage_barrier();
+  int slot = 0;
+  for (int st = 0; st < ns; ++st) {
+    const char* As = smem + slot * STAGE_BYTES;
+    const char* Bs = As + 64 * BM * 2;
+#pragma unroll
+    for (int kf = 0; kf < 2; ++kf) {
+      uint4 fa[4], fb[4];
+#pragma unroll
+      for (int half = 0; half < 2; ++half) {
+        const int pr = kf * 32 + gq * 8 + half * 4 + jr;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int ch = wm * 64 + i * 16 + 4 * qd;
+          const uint2 v = lds_read_tr16(As + pr * (BM * 2) + (((ch >> 4) ^ (pr % SA)) * 32) +
+                                        (ch & 15) * 2);
+          if (half == 0) { fa[i].x = v.x; fa[i].y = v.y; } else { fa[i].z = v.x; fa[i].w = v.y; }
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int ch = wn * 64 + j * 16 + 4 * qd;
+          const uint2 v = lds_read_tr16(Bs + pr * (BN * 2) + (((ch >> 4) ^ (pr % SB)) * 32) +
+                                        (ch & 15) * 2);
+          if (half == 0) { fb[j].x = v.x; fb[j].y = v.y; } else { fb[j].z = v.x; fb[j].w = v.y; }
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) mma_unit(acc[i][j], fa[i], fb[j], (bf16*)nullptr);
+    }
+    stage_barrier();
+    if (++slot == NST) slot = 0;
+  }
+
+  const int RSC = g.R * g.S * g.C;
+  const int lr = lane & 15, lg = lane >> 4;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int row = m0 + wm * 64 + i * 16 + 4 * lg, col = n0 + wn * 64 + j * 16 + lr;
+      float* dst = a.out + ((long long)split * g.K + col) * RSC + row;
       *reinterpret_cast<float4*>(dst) =
           make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
     }
@@ -1668,18 +1837,30 @@ namespace {
 // multiple of 128), the pixel reduction split until ~576 blocks, keeping
 // >= 2 stages of 64 pixels per split.
 struct WgDmaPlan {
-  int bn, splits, mps;
+  int bm, bn, splits, mps;
 };
 bool wgrad_dma_ok(int dt, const ConvGeom& g) { return dt == DT_BF16 && g.C % 64 == 0 && g.K % 64 == 0; }
 WgDmaPlan plan_wgrad_dma(const ConvGeom& g) {
   const long long M = (long long)g.N * g.P * g.Q;
+  const long long stages = std::max(1LL, cdivl(M, 64));
+  const long long ws_tiles = (long long)(g.R * g.S * g.C / 256) * (g.K / 128);
+  if (g.C % 256 == 0 && g.K % 128 == 0 && ws_tiles >= 16 && stages >= 128 &&
+      (long long)g.N * g.H * g.W * g.C < (1LL << 31) && M * g.K < (1LL << 31)) {
+    // warp-specialised 256 x 128 tiles, one block per CU, for long pixel
+    // reductions (shorter ones run faster as the smaller blocks below, which
+    // also share CUs with the data-gradient chain): about one block per CU in
+    // total, >= 4 stages per split
+    long long s = std::min(std::max(1LL, 256 / ws_tiles), std::max(1LL, stages / 4));
+    s = std::min(s, 64LL);
+    const long long mps = cdivl(cdivl(M, s), 64) * 64;
+    return {256, 128, (int)cdivl(M, mps), (int)mps};
+  }
   const int bn = g.K % 128 == 0 ? 128 : 64;
   const long long tiles = (long long)(g.R * g.S * g.C / 64) * (g.K / bn);
-  const long long stages = std::max(1LL, cdivl(M, 64));
   long long s = std::min(cdivl(576, tiles), std::max(1LL, stages / 2));
   s = std::max(1LL, std::min(s, 64LL));
   const long long mps = cdivl(cdivl(M, s), 64) * 64;
-  return {bn, (int)cdivl(M, mps), (int)mps};
+  return {64, bn, (int)cdivl(M, mps), (int)mps};
 }
 struct WPlan {
   int bm, bn, splits;
@@ -1688,8 +1869,9 @@ struct WPlan {
 hipError_t conv_wgrad_dma(const ConvGeom& g, const void* x, const void* dy, float* partials,
                           float* dw, hipStream_t stream) {
   const WgDmaPlan p = plan_wgrad_dma(g);
-  WgDmaArgs a{g, (const bf16*)x, (const bf16*)dy, p.splits > 1 ? partials : dw, p.mps, 0, 0};
-  a.tiles_m = g.R * g.S * g.C / 64;
+  WgDmaArgs a{g, (const bf16*)x, (const bf16*)dy, p.splits > 1 ? partials : dw, p.mps, 0, 0,
+              p.splits};
+  a.tiles_m = g.R * g.S * g.C / p.bm;
   a.tiles_n = g.K / p.bn;
   const Cost cost = conv_cost(g, g.C, sizeof(bf16), true);
   KernelTimer* t = t_timer;
@@ -1700,14 +1882,18 @@ hipError_t conv_wgrad_dma(const ConvGeom& g, const void* x, const void* dy, floa
     EKYA_HIP(hipEventRecord(e0, stream));
   }
   const dim3 grid(a.tiles_m * a.tiles_n, p.splits);
-  if (p.bn == 128)
+  if (p.bm == 256)
+    hipLaunchKernelGGL((wgrad_ws_kernel<256, 128, 3>), dim3(a.tiles_m * a.tiles_n * p.splits),
+                       dim3(8 * 64 + WS_LOADERS * 64), 0, stream, a);
+  else if (p.bn == 128)
     hipLaunchKernelGGL((wgrad_dma_kernel<64, 128>), grid, dim3(NT), 0, stream, a);
   else
     hipLaunchKernelGGL((wgrad_dma_kernel<64, 64>), grid, dim3(NT), 0, stream, a);
   hipError_t e = hipGetLastError();
   if (t && e == hipSuccess) {
     EKYA_HIP(hipEventRecord(e1, stream));
-    t->recs.push_back({std::string("conv_wgrad<bf16,64,") + std::to_string(p.bn) + ",dma>",
+    t->recs.push_back({std::string("conv_wgrad<bf16,") + std::to_string(p.bm) + "," +
+                           std::to_string(p.bn) + (p.bm == 256 ? ",ws>" : ",dma>"),
                        cost.flops, cost.bytes, e0, e1});
   }
   if (e != hipSuccess || p.splits == 1) return e;

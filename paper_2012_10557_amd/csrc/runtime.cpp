@@ -521,6 +521,8 @@ static hipError_t train_backward(TrainJob& j, int nb, const int32_t* fid, float*
   auto wgrad_async = [&](int ci, const void* x, const void* dy, int parity) -> hipError_t {
     if (nf >= TrainJob::kForks) return hipErrorInvalidValue;
     const ConvL& c = net.conv[ci];
+    if (j.st2 == st)
+      return conv_wgrad(dt, conv_geom(net, j.geo, ci, nb), x, dy, j.ws2, j.grad + c.off, c.cin, st);
     EKYA_HIP(hipEventRecord(j.fork[nf], st));
     EKYA_HIP(hipStreamWaitEvent(j.st2, j.fork[nf], 0));
     EKYA_HIP(conv_wgrad(dt, conv_geom(net, j.geo, ci, nb), x, dy, j.ws2, j.grad + c.off, c.cin,

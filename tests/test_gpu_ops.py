@@ -28,6 +28,9 @@ CONV_CASES = [
     (2, 14, 14, 256, 512, 1, 2, 0),   # layer4.0.downsample
     (2, 7, 7, 512, 512, 3, 1, 1),     # layer4
     (4, 56, 56, 64, 64, 3, 1, 1),     # layer1 at 224 px, many tiles
+    (44, 14, 14, 256, 256, 3, 1, 1),  # layer3, 68 pixel tiles (ragged), split reductions,
+                                      # 135 weight-gradient pixel stages
+    (168, 14, 14, 256, 512, 3, 2, 1), # layer4.0.conv1, strided, 129 weight-gradient pixel stages
 ]
 
 
