@@ -1866,11 +1866,12 @@ struct WPlan {
   int bm, bn, splits;
 };
 
+// dw == nullptr: leave the split partials (one split included) in `partials`.
 hipError_t conv_wgrad_dma(const ConvGeom& g, const void* x, const void* dy, float* partials,
                           float* dw, hipStream_t stream) {
   const WgDmaPlan p = plan_wgrad_dma(g);
-  WgDmaArgs a{g, (const bf16*)x, (const bf16*)dy, p.splits > 1 ? partials : dw, p.mps, 0, 0,
-              p.splits};
+  WgDmaArgs a{g, (const bf16*)x, (const bf16*)dy, (p.splits > 1 || !dw) ? partials : dw, p.mps,
+              0, 0, p.splits};
   a.tiles_m = g.R * g.S * g.C / p.bm;
   a.tiles_n = g.K / p.bn;
   const Cost cost = conv_cost(g, g.C, sizeof(bf16), true);
@@ -1896,7 +1897,7 @@ hipError_t conv_wgrad_dma(const ConvGeom& g, const void* x, const void* dy, floa
                            std::to_string(p.bn) + (p.bm == 256 ? ",ws>" : ",dma>"),
                        cost.flops, cost.bytes, e0, e1});
   }
-  if (e != hipSuccess || p.splits == 1) return e;
+  if (e != hipSuccess || p.splits == 1 || !dw) return e;
   const long long n = (long long)g.K * g.R * g.S * g.C;
   const int blocks = (int)std::min<long long>(cdivl(n, 256), 4096);
   hipLaunchKernelGGL(wgrad_reduce_kernel, dim3(blocks), dim3(256), 0, stream, partials, p.splits,
@@ -1918,6 +1919,22 @@ WPlan plan_wgrad(int dt, const ConvGeom& g) {
 
 int conv_wgrad_splits(int dt, const ConvGeom& g) {
   return wgrad_dma_ok(dt, g) ? plan_wgrad_dma(g).splits : plan_wgrad(dt, g).splits;
+}
+
+bool conv_wgrad_partials_ok(int dt, const ConvGeom& g) {
+  return wgrad_dma_ok(dt, g) && (g.C0 == 0 || g.C0 == g.C);
+}
+
+size_t conv_wgrad_partials_floats(int dt, const ConvGeom& g) {
+  if (!conv_wgrad_partials_ok(dt, g)) return 0;
+  return (size_t)plan_wgrad_dma(g).splits * g.K * g.R * g.S * g.C;
+}
+
+hipError_t conv_wgrad_partials(int dt, const ConvGeom& g, const void* x, const void* dy,
+                               float* partials, int* splits, hipStream_t stream) {
+  if (!conv_wgrad_partials_ok(dt, g) || !partials) return hipErrorInvalidValue;
+  *splits = plan_wgrad_dma(g).splits;
+  return conv_wgrad_dma(g, x, dy, partials, nullptr, stream);
 }
 
 size_t conv_wgrad_workspace_floats(int dt, const ConvGeom& g) {

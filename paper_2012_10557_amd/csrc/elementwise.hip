@@ -1143,6 +1143,83 @@ __global__ __launch_bounds__(256) void pack_conv_kernel(const float* master, con
   }
 }
 
+// Momentum SGD of one convolution's weights from its weight-gradient split
+// partials, and its low-precision copies.  A block takes 16 output x 64 input
+// channels of one filter tap, 4 elements per thread: g = sum of the splits in
+// split order (as the separate reduction adds them), loads four splits ahead;
+// v = mu v + g, w = w - lr v on the fp32 [K][RS][C] master, then the
+// [K][RS][C] copy directly and the [C][RS][K] copy through an LDS transpose.
+constexpr int UPD_K = 16;
+template <typename T>
+__global__ __launch_bounds__(256) void conv_update_kernel(const float* part, int splits, int K,
+                                                          int RS, int C, float* w, float* v,
+                                                          float lr, float mu, T* krsc, T* crsk) {
+  const int tk = K / UPD_K, tc = C / 64;
+  const int ntiles = RS * tk * tc;
+  const long long stride = (long long)K * RS * C;
+  const int cc = threadIdx.x & 63, kr = threadIdx.x >> 6;
+  __shared__ float tile[UPD_K][65];
+  for (int bt = blockIdx.x; bt < ntiles; bt += gridDim.x) {
+    const int rs = bt / (tk * tc), rem = bt % (tk * tc);
+    const int k0 = (rem / tc) * UPD_K, c0 = (rem % tc) * 64;
+    int o[4];
+    float g[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      o[i] = ((k0 + kr + 4 * i) * RS + rs) * C + c0 + cc;
+      g[i] = 0.f;
+    }
+    for (int sp = 0; sp < splits; sp += 4) {
+      float t[4][4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) t[q][i] = sp + q < splits ? part[(sp + q) * stride + o[i]] : 0.f;
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if (sp + q < splits) g[i] += t[q][i];
+    }
+    float vv[4], ww[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      vv[i] = v[o[i]];
+      ww[i] = w[o[i]];
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float vn = mu * vv[i] + g[i];
+      const float wn = ww[i] - lr * vn;
+      v[o[i]] = vn;
+      w[o[i]] = wn;
+      krsc[o[i]] = from_f<T>(wn);
+      tile[kr + 4 * i][cc] = wn;
+    }
+    __syncthreads();
+    // [C][RS][K]: thread -> input channel c0 + t / 4, output channels 4 (t % 4) .. + 3
+    const int c = c0 + (threadIdx.x >> 2), kq = (threadIdx.x & 3) * 4;
+    T* dst = crsk + ((long long)c * RS + rs) * K + k0 + kq;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) dst[i] = from_f<T>(tile[kq + i][c - c0]);
+    __syncthreads();
+  }
+}
+
+// SGD with momentum over the ranges (offset, length) of a table, one range per
+// blockIdx.y.
+__global__ void sgd_ranges_kernel(float* w, float* v, const float* g, const long long* tab,
+                                  float lr, float mu) {
+  const long long off = tab[2 * blockIdx.y], n = tab[2 * blockIdx.y + 1];
+  for (long long i = blockIdx.x * (long long)blockDim.x + threadIdx.x; i < n;
+       i += (long long)gridDim.x * blockDim.x) {
+    const long long o = off + i;
+    const float vn = mu * v[o] + g[o];
+    v[o] = vn;
+    w[o] = w[o] - lr * vn;
+  }
+}
+
 // tab row: off, K, C, R, S
 __global__ void permute_kernel(const float* src, float* dst, const long long* tab, int ntab,
                                long long total, int to_internal) {
@@ -1436,6 +1513,27 @@ hipError_t pack_conv_weights(int dt, const float* master, const long long* tab, 
     hipLaunchKernelGGL(pack_conv_kernel<T>, dim3(256, n), dim3(256), 0, stream, master, tab,
                        (T*)shadow);
   });
+}
+
+hipError_t conv_weight_update(int dt, const float* part, int splits, int K, int RS, int C,
+                              float* w, float* v, float lr, float mu, void* krsc, void* crsk,
+                              hipStream_t stream) {
+  if (K % 64 != 0 || C % 64 != 0 || splits < 1 || (long long)K * RS * C >= (1LL << 31))
+    return hipErrorInvalidValue;
+  const int ntiles = RS * (K / UPD_K) * (C / 64);
+  return by_type(dt, [&](auto* tp) {
+    using T = std::remove_pointer_t<decltype(tp)>;
+    hipLaunchKernelGGL(conv_update_kernel<T>, dim3(std::min(ntiles, 4096)), dim3(256), 0, stream,
+                       part, splits, K, RS, C, w, v, lr, mu, (T*)krsc, (T*)crsk);
+  });
+}
+
+hipError_t sgd_momentum_ranges(float* w, float* v, const float* g, const long long* tab, int n,
+                               long long max_len, float lr, float mu, hipStream_t stream) {
+  if (n == 0 || max_len == 0) return hipSuccess;
+  hipLaunchKernelGGL(sgd_ranges_kernel, dim3(grid_for(max_len, 256, 1024), n), dim3(256), 0, stream,
+                     w, v, g, tab, lr, mu);
+  return hipGetLastError();
 }
 
 hipError_t permute_weights(const float* src, float* dst, const long long* tab, int n,

@@ -64,6 +64,12 @@ size_t conv_wgrad_workspace_floats(int dt, const ConvGeom& g);
 // dy x im2col(x); deterministic split-K through `partials`.
 hipError_t conv_wgrad(int dt, const ConvGeom& g, const void* x, const void* dy, float* partials,
                       float* dw, int C0, hipStream_t stream);
+// The weight gradient left as fp32 split partials [splits][K][R][S][C] (one
+// split included) for conv_weight_update: bf16 with C and K multiples of 64.
+bool conv_wgrad_partials_ok(int dt, const ConvGeom& g);
+size_t conv_wgrad_partials_floats(int dt, const ConvGeom& g);
+hipError_t conv_wgrad_partials(int dt, const ConvGeom& g, const void* x, const void* dy,
+                               float* partials, int* splits, hipStream_t stream);
 
 // ---------------------------------------------------------------- BatchNorm
 // Per-channel statistics of z[M, C] (NHWC rows).  Writes mean and 1/sqrt(var+eps)
@@ -141,6 +147,15 @@ hipError_t argmax_rows(const float* z, int N, int J, int32_t* out, hipStream_t s
 // v = mu v + g; w = w - lr v over n floats.
 hipError_t sgd_momentum(float* w, float* v, const float* g, long long n, float lr, float mu,
                         hipStream_t stream);
+// The same over n (offset, length) rows of tab; max_len bounds the lengths.
+hipError_t sgd_momentum_ranges(float* w, float* v, const float* g, const long long* tab, int n,
+                               long long max_len, float lr, float mu, hipStream_t stream);
+// One convolution's momentum step from its weight-gradient split partials
+// (summed in split order): v = mu v + g, w = w - lr v on the fp32 [K][RS][C]
+// master, then its [K][RS][C] and [C][RS][K] low-precision copies.
+hipError_t conv_weight_update(int dt, const float* part, int splits, int K, int RS, int C,
+                              float* w, float* v, float lr, float mu, void* krsc, void* crsk,
+                              hipStream_t stream);
 
 // ---------------------------------------------------------- data movement
 // dst row i = src row idx[i] (idx null: row i), rows of `row_bytes` (multiple of 16).

@@ -52,6 +52,40 @@ void DeviceBuf::release() {
   cap = 0;
 }
 
+// Convolutions whose momentum step runs right after their weight gradient
+// (conv_weight_update from the split partials); the others' gradients go
+// through the gradient buffer and the step-end SGD.
+static bool fused_update(const Net& net, const ConvL& c) {
+  ConvGeom g;
+  g.C = c.cin_pad;
+  g.K = c.cout;
+  return c.cin == c.cin_pad && conv_wgrad_partials_ok(net.dt, g);
+}
+
+// (offset, length) ranges of the trainable parameters from stage lo on that
+// the step-end SGD updates: everything but the fused convolutions' weights.
+static std::vector<long long> sgd_rest_table(const Net& net, int lo, long long* max_len) {
+  std::vector<std::pair<long long, long long>> skip;
+  for (const ConvL& c : net.conv)
+    if (c.stage >= lo && c.stage <= 4 && fused_update(net, c))
+      skip.push_back({c.off, c.off + (long long)c.cout * c.R * c.S * c.cin});
+  std::sort(skip.begin(), skip.end());
+  std::vector<long long> t;
+  long long pos = net.stage_begin[lo];
+  *max_len = 0;
+  auto emit = [&](long long a, long long b) {
+    if (b <= a) return;
+    t.insert(t.end(), {a, b - a});
+    *max_len = std::max(*max_len, b - a);
+  };
+  for (auto& r : skip) {
+    emit(pos, r.first);
+    pos = std::max(pos, r.second);
+  }
+  emit(pos, net.total);
+  return t;
+}
+
 // ----------------------------------------------------------------- tables
 static hipError_t upload_tables(const Net& net, Tables& t) {
   std::vector<long long> all;
@@ -68,6 +102,12 @@ static hipError_t upload_tables(const Net& net, Tables& t) {
     put(net.fold_table(lo, 5), &t.fold_train[lo], &t.n_fold_train[lo], 6);
     put(net.pack_table(0, lo - 1, false), &t.pack_frozen[lo], &t.n_pack_frozen[lo], 8);
     put(net.pack_table(lo, 4, true), &t.pack_train[lo], &t.n_pack_train[lo], 8);
+    put(sgd_rest_table(net, lo, &t.sgd_rest_max[lo]), &t.sgd_rest[lo], &t.n_sgd_rest[lo], 2);
+    std::vector<long long> pr;
+    for (const ConvL& c : net.conv)
+      if (c.stage >= lo && c.stage <= 4 && !fused_update(net, c))
+        pr.insert(pr.end(), {c.off, c.cout, c.R, c.S, c.cin, c.cin_pad, c.sh_krsc, c.sh_crsk});
+    put(pr, &t.pack_rest[lo], &t.n_pack_rest[lo], 8);
   }
   EKYA_HIP(t.buf.ensure(all.size() * sizeof(long long) + 16));
   EKYA_HIP(hipMemcpy(t.buf.p, all.data(), all.size() * sizeof(long long), hipMemcpyHostToDevice));
@@ -185,6 +225,9 @@ static ConvGeom conv_geom(const Net& net, const Geo& g, int ci, int n) {
 static inline const char* shadow_at(const Net& net, const void* shadow, long long off) {
   return reinterpret_cast<const char*>(shadow) + off * (long long)dtype_size(net.dt);
 }
+static inline void* shadow_at(const Net& net, void* shadow, long long off) {
+  return reinterpret_cast<char*>(shadow) + off * (long long)dtype_size(net.dt);
+}
 
 // Run stages lo..hi in eval mode (BatchNorm folded into the conv epilogue) on
 // n frames.  Output: hi <= 3: the stage's output tensor; hi == 4: the pooled
@@ -301,6 +344,7 @@ struct TrainJob {
   static constexpr int kForks = 40;
   hipEvent_t fork[kForks] = {nullptr};
   hipEvent_t joined[kForks] = {nullptr};
+  hipEvent_t dgdone[kForks] = {nullptr};  // data gradient queued: its weight copy may change
   float *pooled = nullptr, *logits = nullptr, *dz = nullptr, *dpooled = nullptr;
   float* ws = nullptr;         // split-K partials
   size_t ws_floats = 0;
@@ -339,8 +383,11 @@ static size_t wgrad_ws_floats(const TrainJob& j) {
   for (size_t i = 0; i < net.conv.size(); ++i) {
     const ConvL& c = net.conv[i];
     if (c.stage < j.lowest || c.stage > 4) continue;
-    for (int n = 1; n <= j.B; ++n)
-      m = std::max(m, conv_wgrad_workspace_floats(j.dt, conv_geom(net, j.geo, (int)i, n)));
+    for (int n = 1; n <= j.B; ++n) {
+      const ConvGeom cg = conv_geom(net, j.geo, (int)i, n);
+      m = std::max(m, fused_update(net, c) ? conv_wgrad_partials_floats(j.dt, cg)
+                                           : conv_wgrad_workspace_floats(j.dt, cg));
+    }
   }
   return m;
 }
@@ -515,20 +562,48 @@ static hipError_t train_backward(TrainJob& j, int nb, const int32_t* fid, float*
   };
   // Weight gradients go to st2 after a fork event on st; st records no
   // dependency on them until it reuses a dz buffer (two blocks later) or
-  // reaches the end of the backward pass.
+  // reaches the end of the backward pass.  A fused convolution leaves its
+  // gradient as split partials in ws2, and its momentum step (which rewrites
+  // the weight copy its data gradient reads) follows on st2 once st has
+  // queued that data gradient (wgrad_finish after the dgrad call).
   int nf = 0;
   int last_join[2] = {-1, -1};  // per buffer parity: join event of its last reader
-  auto wgrad_async = [&](int ci, const void* x, const void* dy, int parity) -> hipError_t {
+  int pending = -1, pending_splits = 0;
+  const bool two = j.st2 != st;
+  auto wgrad_start = [&](int ci, const void* x, const void* dy) -> hipError_t {
     if (nf >= TrainJob::kForks) return hipErrorInvalidValue;
     const ConvL& c = net.conv[ci];
-    if (j.st2 == st)
-      return conv_wgrad(dt, conv_geom(net, j.geo, ci, nb), x, dy, j.ws2, j.grad + c.off, c.cin, st);
-    EKYA_HIP(hipEventRecord(j.fork[nf], st));
-    EKYA_HIP(hipStreamWaitEvent(j.st2, j.fork[nf], 0));
-    EKYA_HIP(conv_wgrad(dt, conv_geom(net, j.geo, ci, nb), x, dy, j.ws2, j.grad + c.off, c.cin,
-                        j.st2));
-    EKYA_HIP(hipEventRecord(j.joined[nf], j.st2));
-    last_join[parity] = nf;
+    const ConvGeom cg = conv_geom(net, j.geo, ci, nb);
+    if (two) {
+      EKYA_HIP(hipEventRecord(j.fork[nf], st));
+      EKYA_HIP(hipStreamWaitEvent(j.st2, j.fork[nf], 0));
+    }
+    if (fused_update(net, c)) {
+      EKYA_HIP(conv_wgrad_partials(dt, cg, x, dy, j.ws2, &pending_splits, j.st2));
+      pending = ci;
+    } else {
+      EKYA_HIP(conv_wgrad(dt, cg, x, dy, j.ws2, j.grad + c.off, c.cin, j.st2));
+      pending = -1;
+    }
+    return hipSuccess;
+  };
+  auto wgrad_finish = [&](int ci, bool after_dgrad, int parity) -> hipError_t {
+    if (pending == ci) {
+      const ConvL& c = net.conv[ci];
+      if (two && after_dgrad) {
+        EKYA_HIP(hipEventRecord(j.dgdone[nf], st));
+        EKYA_HIP(hipStreamWaitEvent(j.st2, j.dgdone[nf], 0));
+      }
+      EKYA_HIP(conv_weight_update(dt, j.ws2, pending_splits, c.cout, c.R * c.S, c.cin,
+                                  j.master + c.off, j.mom + c.off, j.lr, j.mu,
+                                  shadow_at(net, j.shadow, c.sh_krsc),
+                                  shadow_at(net, j.shadow, c.sh_crsk), j.st2));
+      pending = -1;
+    }
+    if (two) {
+      EKYA_HIP(hipEventRecord(j.joined[nf], j.st2));
+      last_join[parity] = nf;
+    }
     ++nf;
     return hipSuccess;
   };
@@ -550,7 +625,8 @@ static hipError_t train_backward(TrainJob& j, int nb, const int32_t* fid, float*
       EKYA_HIP(maxpool_bwd(dt, dout, j.stem_arg, nb, j.geo.sh, j.geo.sw, 64, gA, st));
       const long long M = (long long)nb * j.geo.sh * j.geo.sw;
       EKYA_HIP(bn_bwd(net.conv[0].bn, gA, j.stem_A, j.stem_Z, M, j.gz1[par], nullptr));
-      EKYA_HIP(wgrad_async(0, j.x0, j.gz1[par], par));
+      EKYA_HIP(wgrad_start(0, j.x0, j.gz1[par]));
+      EKYA_HIP(wgrad_finish(0, false, par));
       break;
     }
     int first_bi = -1;
@@ -573,18 +649,19 @@ static hipError_t train_backward(TrainJob& j, int nb, const int32_t* fid, float*
       const void* dx_sc = gG;
       if (b.cd >= 0) {
         EKYA_HIP(bn_bwd(net.conv[b.cd].bn, gG, nullptr, t.Zd, M, gZd, nullptr));
-        EKYA_HIP(wgrad_async(b.cd, t.X, gZd, par));
+        EKYA_HIP(wgrad_start(b.cd, t.X, gZd));
         if (need_dx) EKYA_HIP(dgrad(b.cd, gZd, dnext, nullptr, nb));
+        EKYA_HIP(wgrad_finish(b.cd, need_dx, par));
         dx_sc = dnext;
       }
-      EKYA_HIP(wgrad_async(b.c2, t.A1, gZ2, par));
+      EKYA_HIP(wgrad_start(b.c2, t.A1, gZ2));
       EKYA_HIP(dgrad(b.c2, gZ2, gA, nullptr, nb));
+      EKYA_HIP(wgrad_finish(b.c2, true, par));
       EKYA_HIP(bn_bwd(net.conv[b.c1].bn, gA, t.A1, t.Z1, M, gZ1, nullptr));
-      EKYA_HIP(wgrad_async(b.c1, t.X, gZ1, par));
-      if (need_dx) {
-        EKYA_HIP(dgrad(b.c1, gZ1, dnext, dx_sc, nb));
-        std::swap(dout, dnext);
-      }
+      EKYA_HIP(wgrad_start(b.c1, t.X, gZ1));
+      if (need_dx) EKYA_HIP(dgrad(b.c1, gZ1, dnext, dx_sc, nb));
+      EKYA_HIP(wgrad_finish(b.c1, need_dx, par));
+      if (need_dx) std::swap(dout, dnext);
     }
   }
   // every weight gradient must be complete before the optimizer step
@@ -639,7 +716,6 @@ static hipError_t job_epochs(TrainJob& j) {
   const Net& net = *j.net;
   const Tables& t = *j.tabs;
   const size_t es = dtype_size(j.dt);
-  const long long tb = net.stage_begin[j.lowest];
   const long long fbytes = (long long)j.geo.H * j.geo.W * 3 * es;
   int step = 0;
   EKYA_HIP(hipEventRecord(j.ev[0], j.st));
@@ -655,10 +731,13 @@ static hipError_t job_epochs(TrainJob& j) {
         EKYA_HIP(gather_rows(j.cache, ord, nb, j.row_bytes, j.x0, j.st));
       EKYA_HIP(train_forward(j, nb));
       EKYA_HIP(train_backward(j, nb, fid, j.ce_out + 3 * step));
-      EKYA_HIP(sgd_momentum(j.master + tb, j.mom + tb, j.grad + tb, net.total - tb, j.lr, j.mu,
-                            j.st));
-      EKYA_HIP(pack_conv_weights(j.dt, j.master, t.pack_train[j.lowest],
-                                 t.n_pack_train[j.lowest], j.shadow, j.st));
+      // the parameters without a fused update (BatchNorm, classifier, and
+      // convolutions outside conv_weight_update's reach)
+      EKYA_HIP(sgd_momentum_ranges(j.master, j.mom, j.grad, t.sgd_rest[j.lowest],
+                                   t.n_sgd_rest[j.lowest], t.sgd_rest_max[j.lowest], j.lr, j.mu,
+                                   j.st));
+      EKYA_HIP(pack_conv_weights(j.dt, j.master, t.pack_rest[j.lowest], t.n_pack_rest[j.lowest],
+                                 j.shadow, j.st));
       ++step;
     }
     // held-out accuracy in eval mode with the current running statistics
@@ -732,6 +811,7 @@ static hipError_t create_events(TrainJob& j) {
   for (int i = 0; i < TrainJob::kForks; ++i) {
     EKYA_HIP(hipEventCreateWithFlags(&j.fork[i], hipEventDisableTiming));
     EKYA_HIP(hipEventCreateWithFlags(&j.joined[i], hipEventDisableTiming));
+    EKYA_HIP(hipEventCreateWithFlags(&j.dgdone[i], hipEventDisableTiming));
   }
   return hipSuccess;
 }
@@ -744,7 +824,8 @@ static void destroy_events(TrainJob& j) {
   for (int i = 0; i < TrainJob::kForks; ++i) {
     if (j.fork[i]) (void)hipEventDestroy(j.fork[i]);
     if (j.joined[i]) (void)hipEventDestroy(j.joined[i]);
-    j.fork[i] = j.joined[i] = nullptr;
+    if (j.dgdone[i]) (void)hipEventDestroy(j.dgdone[i]);
+    j.fork[i] = j.joined[i] = j.dgdone[i] = nullptr;
   }
 }
 

@@ -48,6 +48,13 @@ struct Tables {
   int n_pack_frozen[6] = {0};
   const long long* pack_train[6] = {nullptr};
   int n_pack_train[6] = {0};
+  // step-end SGD ranges (offset, length) and repacking of the parameters
+  // without a fused per-convolution update
+  const long long* sgd_rest[6] = {nullptr};
+  int n_sgd_rest[6] = {0};
+  long long sgd_rest_max[6] = {0};
+  const long long* pack_rest[6] = {nullptr};
+  int n_pack_rest[6] = {0};
 };
 
 struct KernelStat {
