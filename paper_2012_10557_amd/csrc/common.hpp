@@ -39,6 +39,36 @@ __device__ __forceinline__ uint4 zero_unit() { return make_uint4(0u, 0u, 0u, 0u)
 // non-finite input reaches the loss and is reported.
 __device__ __forceinline__ float relu_nan(float v) { return v < 0.f ? 0.f : v; }
 
+// Four consecutive elements as float (8- or 16-byte accesses).
+template <typename T> __device__ __forceinline__ void store4(T* dst, const float (&v)[4]);
+template <> __device__ __forceinline__ void store4<float>(float* dst, const float (&v)[4]) {
+  *reinterpret_cast<float4*>(dst) = make_float4(v[0], v[1], v[2], v[3]);
+}
+template <> __device__ __forceinline__ void store4<bf16>(bf16* dst, const float (&v)[4]) {
+  union {
+    uint2 u;
+    bf16 e[4];
+  } p;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) p.e[i] = (bf16)v[i];
+  *reinterpret_cast<uint2*>(dst) = p.u;
+}
+template <typename T> __device__ __forceinline__ void load4(const T* src, float (&v)[4]);
+template <> __device__ __forceinline__ void load4<float>(const float* src, float (&v)[4]) {
+  float4 t = *reinterpret_cast<const float4*>(src);
+  v[0] = t.x; v[1] = t.y; v[2] = t.z; v[3] = t.w;
+}
+template <> __device__ __forceinline__ void load4<bf16>(const bf16* src, float (&v)[4]) {
+  union {
+    uint2 u;
+    bf16 e[4];
+  } p;
+  p.u = *reinterpret_cast<const uint2*>(src);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) v[i] = (float)p.e[i];
+}
+
+
 // D += A * B on one 16x16 output tile; `a` and `b` are one 16-byte unit each
 // (k-contiguous).  For bf16 the unit is the whole k-chunk of one
 // v_mfma_f32_16x16x32_bf16; for fp32 the four floats feed four

@@ -25,34 +25,6 @@ namespace {
 
 constexpr int NT = 256;
 
-template <typename T> __device__ __forceinline__ void store4(T* dst, const float (&v)[4]);
-template <> __device__ __forceinline__ void store4<float>(float* dst, const float (&v)[4]) {
-  *reinterpret_cast<float4*>(dst) = make_float4(v[0], v[1], v[2], v[3]);
-}
-template <> __device__ __forceinline__ void store4<bf16>(bf16* dst, const float (&v)[4]) {
-  union {
-    uint2 u;
-    bf16 e[4];
-  } p;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) p.e[i] = (bf16)v[i];
-  *reinterpret_cast<uint2*>(dst) = p.u;
-}
-template <typename T> __device__ __forceinline__ void load4(const T* src, float (&v)[4]);
-template <> __device__ __forceinline__ void load4<float>(const float* src, float (&v)[4]) {
-  float4 t = *reinterpret_cast<const float4*>(src);
-  v[0] = t.x; v[1] = t.y; v[2] = t.z; v[3] = t.w;
-}
-template <> __device__ __forceinline__ void load4<bf16>(const bf16* src, float (&v)[4]) {
-  union {
-    uint2 u;
-    bf16 e[4];
-  } p;
-  p.u = *reinterpret_cast<const uint2*>(src);
-#pragma unroll
-  for (int i = 0; i < 4; ++i) v[i] = (float)p.e[i];
-}
-
 __device__ __forceinline__ uint4 ld16(const void* p) { return *reinterpret_cast<const uint4*>(p); }
 
 // Quotient of non-negative a < 2^22 by d > 0, with inv = 1.0f / d.
@@ -1686,7 +1658,8 @@ hipError_t dispatch_dma(Args a, const DmaPlan& p, long long cols, int rows, hipS
 
 // bf16 forward with C % 64 == 0 on the direct-to-LDS path.
 hipError_t conv_fwd_dma(const ConvGeom& g, const void* x, const void* w, void* y,
-                        const ConvEpilogue& epi, float* ws, size_t ws_floats, hipStream_t stream) {
+                        const ConvEpilogue& epi, float* ws, size_t ws_floats, hipStream_t stream,
+                        BnStatsSink* sink) {
   const int ns = g.R * g.S * g.C / 64;
   const long long npix = (long long)g.N * g.P * g.Q;
   DmaPlan p = plan_dma(g.K, npix, ns, ws != nullptr);
@@ -1696,12 +1669,18 @@ hipError_t conv_fwd_dma(const ConvGeom& g, const void* x, const void* w, void* y
                                        conv_cost(g, g.C0 ? g.C0 : g.C, sizeof(bf16), false),
                                        "conv_fwd");
   if (e != hipSuccess || p.splits <= 1) return e;
+  if (sink && !sink->bwd && !epi.scale && !epi.shift && !epi.res && !epi.relu &&
+      bn_fold_path(npix, g.K)) {
+    sink->done = true;
+    return split_reduce_bn(DT_BF16, ws, p.splits, npix, g.K, nullptr, y, *sink, stream);
+  }
   return split_finish<bf16>(ws, p.splits, npix, g.K, epi, y, stream);
 }
 
 // bf16 data gradient with K % 64 == 0 on the direct-to-LDS path.
 hipError_t conv_dgrad_dma(const ConvGeom& g, const void* dy, const void* wt, void* dx,
-                          const void* res, float* ws, size_t ws_floats, hipStream_t stream) {
+                          const void* res, float* ws, size_t ws_floats, hipStream_t stream,
+                          BnStatsSink* sink) {
   const int ns = g.R * g.S * g.K / 64;
   const long long npix = (long long)g.N * g.H * g.W;
   DmaPlan p = plan_dma(g.C, npix, ns, ws != nullptr);
@@ -1711,6 +1690,10 @@ hipError_t conv_dgrad_dma(const ConvGeom& g, const void* dy, const void* wt, voi
   hipError_t e = dispatch_dma<DmaDgradOp>(a, p, npix, g.C, stream,
                                          conv_cost(g, g.C, sizeof(bf16), false), "conv_dgrad");
   if (e != hipSuccess || p.splits <= 1) return e;
+  if (sink && sink->bwd && bn_fold_path(npix, g.C)) {
+    sink->done = true;
+    return split_reduce_bn(DT_BF16, ws, p.splits, npix, g.C, res, dx, *sink, stream);
+  }
   ConvEpilogue ep;
   ep.res = res;
   return split_finish<bf16>(ws, p.splits, npix, g.C, ep, dx, stream);
@@ -1720,9 +1703,11 @@ constexpr int KU_MAIN = 8;
 
 template <typename T>
 hipError_t conv_fwd_t(const ConvGeom& g, const void* x, const void* w, void* y,
-                      const ConvEpilogue& epi, float* ws, size_t ws_floats, hipStream_t stream) {
+                      const ConvEpilogue& epi, float* ws, size_t ws_floats, hipStream_t stream,
+                      BnStatsSink* sink) {
   constexpr int E = Elt<T>::E;
-  if (sizeof(T) == 2 && g.C % 64 == 0) return conv_fwd_dma(g, x, w, y, epi, ws, ws_floats, stream);
+  if (sizeof(T) == 2 && g.C % 64 == 0)
+    return conv_fwd_dma(g, x, w, y, epi, ws, ws_floats, stream, sink);
   if (sizeof(T) == 2 && g.C == 8 && g.C0 == 3 && g.K == 64 && g.R == 7 && g.S == 7 && g.stride == 2 &&
       g.pad == 3 && g.Q <= STEM_QMAX && g.N > 0) {
     const Cost cost = conv_cost(g, 3, sizeof(bf16), false);
@@ -1770,10 +1755,11 @@ hipError_t conv_fwd_t(const ConvGeom& g, const void* x, const void* w, void* y,
 
 template <typename T>
 hipError_t conv_dgrad_t(const ConvGeom& g, const void* dy, const void* wt, void* dx,
-                        const void* res, float* ws, size_t ws_floats, hipStream_t stream) {
+                        const void* res, float* ws, size_t ws_floats, hipStream_t stream,
+                        BnStatsSink* sink) {
   constexpr int E = Elt<T>::E;
   if (g.K % (KU_MAIN * E) != 0 || (g.stride != 1 && g.stride != 2)) return hipErrorInvalidValue;
-  if (sizeof(T) == 2) return conv_dgrad_dma(g, dy, wt, dx, res, ws, ws_floats, stream);
+  if (sizeof(T) == 2) return conv_dgrad_dma(g, dy, wt, dx, res, ws, ws_floats, stream, sink);
   const int ns = cdiv(g.R * g.S * g.K, KU_MAIN * E);
   const long long npix = (long long)g.N * g.H * g.W;
   Plan p = plan_tiles(g.C, (int)npix, ns, ws != nullptr);
@@ -1947,17 +1933,21 @@ size_t conv_wgrad_workspace_floats(int dt, const ConvGeom& g) {
 }
 
 hipError_t conv_fwd(int dt, const ConvGeom& g, const void* x, const void* w, void* y,
-                    const ConvEpilogue& epi, float* ws, size_t ws_floats, hipStream_t stream) {
+                    const ConvEpilogue& epi, float* ws, size_t ws_floats, hipStream_t stream,
+                    BnStatsSink* sink) {
+  if (sink) sink->done = false;
   if (g.N * g.P * g.Q == 0) return hipSuccess;
-  return dt == DT_F32 ? conv_fwd_t<float>(g, x, w, y, epi, ws, ws_floats, stream)
-                      : conv_fwd_t<bf16>(g, x, w, y, epi, ws, ws_floats, stream);
+  return dt == DT_F32 ? conv_fwd_t<float>(g, x, w, y, epi, ws, ws_floats, stream, sink)
+                      : conv_fwd_t<bf16>(g, x, w, y, epi, ws, ws_floats, stream, sink);
 }
 
 hipError_t conv_dgrad(int dt, const ConvGeom& g, const void* dy, const void* wt, void* dx,
-                      const void* res, float* ws, size_t ws_floats, hipStream_t stream) {
+                      const void* res, float* ws, size_t ws_floats, hipStream_t stream,
+                      BnStatsSink* sink) {
+  if (sink) sink->done = false;
   if (g.N * g.H * g.W == 0) return hipSuccess;
-  return dt == DT_F32 ? conv_dgrad_t<float>(g, dy, wt, dx, res, ws, ws_floats, stream)
-                      : conv_dgrad_t<bf16>(g, dy, wt, dx, res, ws, ws_floats, stream);
+  return dt == DT_F32 ? conv_dgrad_t<float>(g, dy, wt, dx, res, ws, ws_floats, stream, sink)
+                      : conv_dgrad_t<bf16>(g, dy, wt, dx, res, ws, ws_floats, stream, sink);
 }
 
 hipError_t conv_wgrad(int dt, const ConvGeom& g, const void* x, const void* dy, float* partials,

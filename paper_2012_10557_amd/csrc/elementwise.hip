@@ -201,31 +201,33 @@ inline bool bn_fold_ok(long long M, int C) {
   return C % BN_GROUP == 0 && cdivl(M, BN_FOLD_ROWS) <= BN_FOLD_MAX_CHUNKS;
 }
 
-// Per (chunk, group) sums of two per-element quantities, added in a fixed
-// order.  Forward: d = z - K with the shift K[c] = z[0][c]; s1 = sum d,
-// s2 = sum d^2.  Backward: g = dy [* (y > 0)]; s1 = sum g, s2 = sum g (z - mean).
+// Per (chunk, 64-channel group) partials, in a fixed order.  Forward: the
+// chunk's sum S1 and its squared deviations from the chunk mean M2 (rows kept
+// in registers for the second pass).  Backward: g = dy [* (y > 0)];
+// S1 = sum g, S2 = sum g (z - mean).  Row slices are added in slice order.
 template <typename T, bool BWD>
 __global__ __launch_bounds__(256) void bn_group_partial(const T* z, const T* dy, const T* y,
                                                         const float* mean, long long M, int C,
                                                         float* part) {
-  constexpr int E = Elt<T>::E, UG = BN_GROUP / E, RI = 256 / UG;
+  constexpr int E = Elt<T>::E, UG = BN_GROUP / E, RI = 256 / UG, RPT = BN_FOLD_ROWS / RI;
   const int t = threadIdx.x, u = t % UG, rs = t / UG;
   const int c0 = blockIdx.y * BN_GROUP + u * E;
   const long long r0 = (long long)blockIdx.x * BN_FOLD_ROWS;
-  const long long r1 = std::min<long long>(M, r0 + BN_FOLD_ROWS);
-  float s1[E], s2[E], K[E];
+  __shared__ float sh[2][256 * E];
+  __shared__ float smean[BN_GROUP];
+  float s1[E], s2[E];
 #pragma unroll
   for (int i = 0; i < E; ++i) s1[i] = s2[i] = 0.f;
-  if (BWD)
-    chan_load<E>(mean, c0, K);
-  else
-    unit_to_f<T>(*reinterpret_cast<const uint4*>(z + c0), K);
-  for (long long r = r0 + rs; r < r1; r += RI) {
-    const long long off = r * C + c0;
-    float v[E];
-    unit_to_f<T>(*reinterpret_cast<const uint4*>(z + off), v);
-    if (BWD) {
-      float g[E];
+  if constexpr (BWD) {
+    float mu[E];
+    chan_load<E>(mean, c0, mu);
+#pragma unroll
+    for (int q = 0; q < RPT; ++q) {
+      const long long r = r0 + rs + (long long)RI * q;
+      if (r >= M) break;
+      const long long off = r * C + c0;
+      float v[E], g[E];
+      unit_to_f<T>(*reinterpret_cast<const uint4*>(z + off), v);
       unit_to_f<T>(*reinterpret_cast<const uint4*>(dy + off), g);
       if (y) {
         float yy[E];
@@ -236,18 +238,42 @@ __global__ __launch_bounds__(256) void bn_group_partial(const T* z, const T* dy,
 #pragma unroll
       for (int i = 0; i < E; ++i) {
         s1[i] += g[i];
-        s2[i] += g[i] * (v[i] - K[i]);
+        s2[i] += g[i] * (v[i] - mu[i]);
       }
-    } else {
+    }
+  } else {
+    float v[RPT][E];
+    const int nk = (int)std::min<long long>(BN_FOLD_ROWS, M - r0);
 #pragma unroll
-      for (int i = 0; i < E; ++i) {
-        const float d = v[i] - K[i];
-        s1[i] += d;
-        s2[i] += d * d;
+    for (int q = 0; q < RPT; ++q) {
+      const long long r = r0 + rs + (long long)RI * q;
+      if (r < M) {
+        unit_to_f<T>(*reinterpret_cast<const uint4*>(z + r * C + c0), v[q]);
+#pragma unroll
+        for (int i = 0; i < E; ++i) s1[i] += v[q][i];
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < E; ++i) sh[0][t * E + i] = s1[i];
+    __syncthreads();
+    if (t < BN_GROUP) {
+      float a = 0.f;
+      for (int k = 0; k < RI; ++k) a += sh[0][k * BN_GROUP + t];
+      smean[t] = a / (float)nk;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < RPT; ++q) {
+      const long long r = r0 + rs + (long long)RI * q;
+      if (r < M) {
+#pragma unroll
+        for (int i = 0; i < E; ++i) {
+          const float d = v[q][i] - smean[u * E + i];
+          s2[i] += d * d;
+        }
       }
     }
   }
-  __shared__ float sh[2][256 * E];
 #pragma unroll
   for (int i = 0; i < E; ++i) {
     sh[0][t * E + i] = s1[i];
@@ -263,9 +289,40 @@ __global__ __launch_bounds__(256) void bn_group_partial(const T* z, const T* dy,
     const int c = blockIdx.y * BN_GROUP + t;
     part[(long long)blockIdx.x * 2 * C + c] = a;
     part[(long long)blockIdx.x * 2 * C + C + c] = b;
-    // the forward shift, after the chunk rows, for the apply kernel
-    if (!BWD && blockIdx.x == 0) part[(long long)gridDim.x * 2 * C + c] = to_f(z[c]);
   }
+}
+
+// Mean and biased variance of channel c = 64 blockIdx.y + threadIdx.x % 64
+// over M rows from forward chunk partials (S1, M2): Chan's combination in
+// double, M2 = sum_k [M2_k + n_k (S1_k / n_k - mean)^2], four slices of chunks
+// (k = slice, slice + 4, ...) added in slice order.  The same in every block;
+// true for the thread (one per channel) that holds the result.
+__device__ __forceinline__ bool group_stats(const float* part, int nch, long long M, int C,
+                                            double& mean, double& var) {
+  __shared__ double sa[4][BN_GROUP];
+  __shared__ double smu[BN_GROUP];
+  const int lc = threadIdx.x % BN_GROUP, sl = threadIdx.x / BN_GROUP;
+  const int c = blockIdx.y * BN_GROUP + lc;
+  double x = 0.0;
+  for (int k = sl; k < nch; k += 4) x += (double)part[(long long)k * 2 * C + c];
+  sa[sl][lc] = x;
+  __syncthreads();
+  if (sl == 0) smu[lc] = (((sa[0][lc] + sa[1][lc]) + sa[2][lc]) + sa[3][lc]) / (double)M;
+  __syncthreads();
+  const double mu = smu[lc];
+  double y = 0.0;
+  for (int k = sl; k < nch; k += 4) {
+    const double nk = (double)std::min<long long>(BN_FOLD_ROWS, M - (long long)k * BN_FOLD_ROWS);
+    const double d = (double)part[(long long)k * 2 * C + c] / nk - mu;
+    y += (double)part[(long long)k * 2 * C + C + c] + nk * d * d;
+  }
+  __syncthreads();
+  sa[sl][lc] = y;
+  __syncthreads();
+  if (sl != 0) return false;
+  mean = mu;
+  var = (((sa[0][lc] + sa[1][lc]) + sa[2][lc]) + sa[3][lc]) / (double)M;
+  return true;
 }
 
 // Totals of the two partial rows for channel c = 64 blockIdx.y + threadIdx.x % 64:
@@ -290,8 +347,8 @@ __device__ __forceinline__ bool group_sums(const float* part, int nch, int C, do
   return true;
 }
 
-// Statistics from the group partials (and the shift stored after them), then
-// y = relu?((z - mean) scale + beta [+ res]) on rows [blockIdx.x rpb, +rpb) of the block's 64 channels.  Blocks
+// Statistics from the group partials, then y = relu?((z - mean) scale + beta
+// [+ res]) on rows [blockIdx.x rpb, +rpb) of the block's 64 channels.  Blocks
 // with blockIdx.x == 0 publish mean / invstd / scale / shift and update the
 // running statistics.
 template <typename T>
@@ -304,14 +361,10 @@ __global__ __launch_bounds__(256) void bn_fold_apply(const T* z, const float* pa
   constexpr int E = Elt<T>::E, UG = BN_GROUP / E, RI = 256 / UG;
   __shared__ float cf[3][BN_GROUP];
   const int t = threadIdx.x;
-  double a, b;
-  if (group_sums(part, nch, C, a, b)) {
+  double mean_d, var;
+  if (group_stats(part, nch, M, C, mean_d, var)) {
     const int c = blockIdx.y * BN_GROUP + t;
-    const double Kc = (double)part[(long long)nch * 2 * C + c];
-    const double d = a / (double)M;
-    double var = b / (double)M - d * d;
-    if (var < 0.0) var = 0.0;
-    const float mu = (float)(Kc + d);
+    const float mu = (float)mean_d;
     const float is = (float)(1.0 / sqrt(var + (double)BN_EPS));
     const float sc = gamma[c] * is;
     cf[0][t] = mu;
@@ -412,6 +465,142 @@ __global__ __launch_bounds__(256) void bn_bwd_fold_apply(const T* dy, const T* y
 #pragma unroll
     for (int i = 0; i < E; ++i) o[i] = ca[i] * g[i] + cb[i] + cc[i] * (zz[i] - mu[i]);
     *reinterpret_cast<uint4*>(dz + off) = f_to_unit<T>(o);
+  }
+}
+
+// Sum of split-K partials [split][M][C] in split order (+ res), stored in T,
+// with the BatchNorm chunk partials of the stored values for the two-launch
+// path: one block per chunk of BN_FOLD_ROWS rows and 64 channels, 1024
+// threads = 64 row slices x 16 four-channel units (two rows each), partials
+// loaded four splits ahead.  Forward: (S1, M2) as bn_group_partial;
+// backward: g = out [* (ymask > 0)], (sum g, sum g (z - mean)).
+// Sum over the 64 row slices of channel column c (sh[k * 64 + c], k < 64) in a
+// fixed order: 16 groups of 4 consecutive slices (all 1024 threads), then
+// the 16 group sums; the result in red[c] for c < 64.
+__device__ __forceinline__ void slice_sum64(const float* sh, float* grp, float* red) {
+  const int t = threadIdx.x, c = t & 63, gi = t >> 6;
+  const float* p = sh + (gi * 4) * BN_GROUP + c;
+  grp[gi * BN_GROUP + c] = ((p[0] + p[BN_GROUP]) + p[2 * BN_GROUP]) + p[3 * BN_GROUP];
+  __syncthreads();
+  if (t < BN_GROUP) {
+    float a = 0.f;
+#pragma unroll
+    for (int k = 0; k < 16; ++k) a += grp[k * BN_GROUP + t];
+    red[t] = a;
+  }
+  __syncthreads();
+}
+
+constexpr int SBN_SLICES = 64, SBN_RPT = BN_FOLD_ROWS / SBN_SLICES;
+template <typename T, bool BWD>
+__global__ __launch_bounds__(1024) void split_bn_kernel(const float* part, int splits, long long M,
+                                                        int C, const T* res, T* out,
+                                                        const T* ymask, const T* z,
+                                                        const float* mean, float* bnp) {
+  const int t = threadIdx.x, u = t & 15, rs = t >> 4;
+  const int c0 = blockIdx.y * BN_GROUP + u * 4;
+  const long long r0 = (long long)blockIdx.x * BN_FOLD_ROWS;
+  const long long stride = M * C;
+  __shared__ float sh[2][1024 * 4];
+  __shared__ float grp[16 * BN_GROUP];
+  __shared__ float red[2][BN_GROUP];
+  bool ok[SBN_RPT];
+  long long off[SBN_RPT];
+  float v[SBN_RPT][4];
+#pragma unroll
+  for (int q = 0; q < SBN_RPT; ++q) {
+    const long long r = r0 + rs + (long long)SBN_SLICES * q;
+    ok[q] = r < M;
+    off[q] = (ok[q] ? r : 0) * C + c0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) v[q][i] = 0.f;
+  }
+  for (int sp = 0; sp < splits; sp += 4) {
+    float4 p[4][SBN_RPT];
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+#pragma unroll
+      for (int q = 0; q < SBN_RPT; ++q)
+        p[k][q] = (sp + k < splits && ok[q])
+                      ? *reinterpret_cast<const float4*>(part + (sp + k) * stride + off[q])
+                      : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      if (sp + k < splits)
+#pragma unroll
+        for (int q = 0; q < SBN_RPT; ++q) {  // split order per element
+          v[q][0] += p[k][q].x;
+          v[q][1] += p[k][q].y;
+          v[q][2] += p[k][q].z;
+          v[q][3] += p[k][q].w;
+        }
+  }
+  float s1[4] = {0.f, 0.f, 0.f, 0.f}, s2[4] = {0.f, 0.f, 0.f, 0.f}, mu[4];
+  if (BWD) chan_load<4>(mean, c0, mu);
+#pragma unroll
+  for (int q = 0; q < SBN_RPT; ++q) {
+    if (!ok[q]) continue;
+    if (res) {
+      float rr[4];
+      load4<T>(res + off[q], rr);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) v[q][i] += rr[i];
+    }
+    store4<T>(out + off[q], v[q]);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) v[q][i] = to_f(from_f<T>(v[q][i]));  // the stored values
+    if (BWD) {
+      float zz[4], g[4] = {v[q][0], v[q][1], v[q][2], v[q][3]};
+      load4<T>(z + off[q], zz);
+      if (ymask) {
+        float yy[4];
+        load4<T>(ymask + off[q], yy);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) g[i] = yy[i] > 0.f ? g[i] : 0.f;
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        s1[i] += g[i];
+        s2[i] += g[i] * (zz[i] - mu[i]);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) s1[i] += v[q][i];
+    }
+  }
+  if (!BWD) {
+    const int nk = (int)std::min<long long>(BN_FOLD_ROWS, M - r0);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) sh[0][t * 4 + i] = s1[i];
+    __syncthreads();
+    slice_sum64(sh[0], grp, red[0]);
+#pragma unroll
+    for (int q = 0; q < SBN_RPT; ++q) {
+      if (!ok[q]) continue;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float d = v[q][i] - red[0][u * 4 + i] / (float)nk;
+        s2[i] += d * d;
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) sh[1][t * 4 + i] = s2[i];
+    __syncthreads();
+    slice_sum64(sh[1], grp, red[1]);
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      sh[0][t * 4 + i] = s1[i];
+      sh[1][t * 4 + i] = s2[i];
+    }
+    __syncthreads();
+    slice_sum64(sh[0], grp, red[0]);
+    slice_sum64(sh[1], grp, red[1]);
+  }
+  if (t < BN_GROUP) {
+    const int c = blockIdx.y * BN_GROUP + t;
+    bnp[(long long)blockIdx.x * 2 * C + c] = red[0][t];
+    bnp[(long long)blockIdx.x * 2 * C + C + c] = red[1][t];
   }
 }
 
@@ -1276,10 +1465,33 @@ hipError_t bn_train_stats(int dt, const void* z, long long M, int C, const float
   });
 }
 
+bool bn_fold_path(long long M, int C) { return bn_fold_ok(M, C); }
+
+hipError_t split_reduce_bn(int dt, const float* part, int splits, long long M, int C,
+                           const void* res, void* out, const BnStatsSink& sink,
+                           hipStream_t stream) {
+  if (M == 0) return hipSuccess;
+  if (!bn_fold_ok(M, C) || splits < 1 || !sink.part ||
+      (sink.bwd && (!sink.z || !sink.mean)))
+    return hipErrorInvalidValue;
+  const dim3 grid((unsigned)cdivl(M, BN_FOLD_ROWS), C / BN_GROUP);
+  return by_type(dt, [&](auto* tp) {
+    using T = std::remove_pointer_t<decltype(tp)>;
+    if (sink.bwd)
+      hipLaunchKernelGGL((split_bn_kernel<T, true>), grid, dim3(1024), 0, stream, part, splits, M,
+                         C, (const T*)res, (T*)out, (const T*)sink.ymask, (const T*)sink.z,
+                         sink.mean, sink.part);
+    else
+      hipLaunchKernelGGL((split_bn_kernel<T, false>), grid, dim3(1024), 0, stream, part, splits, M,
+                         C, (const T*)res, (T*)out, (const T*)nullptr, (const T*)nullptr,
+                         (const float*)nullptr, sink.part);
+  });
+}
+
 hipError_t bn_train_forward(int dt, const void* z, long long M, int C, const float* gamma,
                             const float* beta, float* rm, float* rv, float* mean, float* invstd,
                             float* scale, float* shift, const void* res, int relu, void* y,
-                            float* partials, hipStream_t stream) {
+                            float* partials, hipStream_t stream, bool partials_ready) {
   if (M == 0) return hipSuccess;
   if (!bn_fold_ok(M, C)) {
     hipError_t e = bn_train_stats(dt, z, M, C, gamma, beta, rm, rv, mean, invstd, scale, shift,
@@ -1291,9 +1503,10 @@ hipError_t bn_train_forward(int dt, const void* z, long long M, int C, const flo
   const long long rpb = bn_fold_rpb(M, C, dt);
   return by_type(dt, [&](auto* tp) {
     using T = std::remove_pointer_t<decltype(tp)>;
-    hipLaunchKernelGGL((bn_group_partial<T, false>), dim3(nch, groups), dim3(256), 0, stream,
-                       (const T*)z, (const T*)nullptr, (const T*)nullptr, (const float*)nullptr, M,
-                       C, partials);
+    if (!partials_ready)
+      hipLaunchKernelGGL((bn_group_partial<T, false>), dim3(nch, groups), dim3(256), 0, stream,
+                         (const T*)z, (const T*)nullptr, (const T*)nullptr, (const float*)nullptr,
+                         M, C, partials);
     hipLaunchKernelGGL(bn_fold_apply<T>, dim3((unsigned)cdivl(M, rpb), groups), dim3(256), 0,
                        stream, (const T*)z, partials, nch, M, C, rpb, gamma, beta, rm, rv, mean,
                        invstd, scale, shift, (const T*)res, relu, (T*)y);
@@ -1321,15 +1534,17 @@ hipError_t bn_fold(const float* params, const long long* tab, int n, float* out,
 
 hipError_t bn_backward(int dt, const void* dy, const void* y, const void* z, long long M, int C,
                        const float* gamma, const float* mean, const float* invstd, float* dgamma,
-                       float* dbeta, void* dz, void* g_out, float* partials, hipStream_t stream) {
+                       float* dbeta, void* dz, void* g_out, float* partials, hipStream_t stream,
+                       bool partials_ready) {
   if (M == 0) return hipSuccess;
   if (bn_fold_ok(M, C)) {
     const int nf = (int)cdivl(M, BN_FOLD_ROWS), groups = C / BN_GROUP;
     const long long rpb = bn_fold_rpb(M, C, dt);
     return by_type(dt, [&](auto* tp) {
       using T = std::remove_pointer_t<decltype(tp)>;
-      hipLaunchKernelGGL((bn_group_partial<T, true>), dim3(nf, groups), dim3(256), 0, stream,
-                         (const T*)z, (const T*)dy, (const T*)y, mean, M, C, partials);
+      if (!partials_ready)
+        hipLaunchKernelGGL((bn_group_partial<T, true>), dim3(nf, groups), dim3(256), 0, stream,
+                           (const T*)z, (const T*)dy, (const T*)y, mean, M, C, partials);
       hipLaunchKernelGGL(bn_bwd_fold_apply<T>, dim3((unsigned)cdivl(M, rpb), groups), dim3(256), 0,
                          stream, (const T*)dy, (const T*)y, (const T*)z, partials, nf, M, C, rpb,
                          gamma, mean, invstd, dgamma, dbeta, (T*)dz, (T*)g_out);

@@ -47,15 +47,32 @@ struct ConvEpilogue {
   int relu = 0;
 };
 
+// BatchNorm chunk partials for the two-launch BatchNorm path, produced while
+// a split convolution's partials are reduced (bf16 direct-to-LDS path, empty
+// forward epilogue, M within bn_fold_path).  `done` reports whether they were;
+// otherwise the caller computes them.  Forward: statistics of the output.
+// Backward (bwd): of g = out * [ymask > 0] (no mask when null) against z and
+// mean, as bn_backward's first pass.
+struct BnStatsSink {
+  float* part = nullptr;  // bn_partials_floats(M, C)
+  bool bwd = false;
+  const void* ymask = nullptr;
+  const void* z = nullptr;
+  const float* mean = nullptr;
+  bool done = false;
+};
+
 // y[N,P,Q,K] = conv(x[N,H,W,C], w[K,R,S,C]) with the epilogue.  `ws` (fp32,
 // ws_floats) holds split-reduction partials when the output has too few tiles
 // (conv_split_workspace_floats tells how much; null or too small: no split).
 hipError_t conv_fwd(int dt, const ConvGeom& g, const void* x, const void* w_krsc, void* y,
-                    const ConvEpilogue& epi, float* ws, size_t ws_floats, hipStream_t stream);
+                    const ConvEpilogue& epi, float* ws, size_t ws_floats, hipStream_t stream,
+                    BnStatsSink* sink = nullptr);
 // dx[N,H,W,C] = conv-transpose of dy[N,P,Q,K] with wT[C,R,S,K] (+ res[N,H,W,C]).
 // Needs K a multiple of 64 (bf16) / 32 (fp32) and stride 1 or 2.
 hipError_t conv_dgrad(int dt, const ConvGeom& g, const void* dy, const void* w_crsk, void* dx,
-                      const void* res, float* ws, size_t ws_floats, hipStream_t stream);
+                      const void* res, float* ws, size_t ws_floats, hipStream_t stream,
+                      BnStatsSink* sink = nullptr);
 size_t conv_split_workspace_floats(int dt, const ConvGeom& g, bool dgrad);
 // Split count and partial-buffer size (floats) the weight gradient will use.
 int conv_wgrad_splits(int dt, const ConvGeom& g);
@@ -77,15 +94,25 @@ hipError_t conv_wgrad_partials(int dt, const ConvGeom& g, const void* x, const v
 // with momentum 0.1 and the unbiased variance.  Also writes scale = gamma*invstd,
 // shift = beta - mean*scale.  `partials` needs bn_partials_floats(M, C).
 size_t bn_partials_floats(long long M, int C);
+// True when BatchNorm over [M, C] takes the two-launch path (partials per
+// 128-row chunk and 64 channels, reduced inside the apply kernels).
+bool bn_fold_path(long long M, int C);
+// Sum of split partials [splits][M][C] in split order (+ res) into out (dt),
+// with the chunk partials the sink asks for (bn_fold_path(M, C) must hold).
+hipError_t split_reduce_bn(int dt, const float* part, int splits, long long M, int C,
+                           const void* res, void* out, const BnStatsSink& sink,
+                           hipStream_t stream);
 hipError_t bn_train_stats(int dt, const void* z, long long M, int C, const float* gamma,
                           const float* beta, float* rm, float* rv, float* mean, float* invstd,
                           float* scale, float* shift, float* partials, hipStream_t stream);
 // bn_train_stats followed by bn_apply: y = relu?((z - mean)*scale + beta + res).
 // Two launches when M is at most 64 chunks of 128 rows and C a multiple of 64.
+// partials_ready: `partials` already holds the chunk partials of z (from a
+// BnStatsSink).
 hipError_t bn_train_forward(int dt, const void* z, long long M, int C, const float* gamma,
                             const float* beta, float* rm, float* rv, float* mean, float* invstd,
                             float* scale, float* shift, const void* res, int relu, void* y,
-                            float* partials, hipStream_t stream);
+                            float* partials, hipStream_t stream, bool partials_ready = false);
 // y = (z - mean)*scale + beta (+ res) (ReLU), elementwise over [M, C].
 hipError_t bn_apply(int dt, const void* z, long long M, int C, const float* mean,
                     const float* scale, const float* beta, const void* res, int relu, void* y,
@@ -99,9 +126,11 @@ hipError_t bn_fold(const float* params, const long long* tab, int n, float* out,
 // g = dy * [y > 0]; dgamma = sum g*xhat; dbeta = sum g;
 // dz = gamma*invstd*(g - dbeta/M - xhat*dgamma/M).  Writes dgamma/dbeta and
 // dz; when g_out != null also writes g.
+// partials_ready: as for bn_train_forward.
 hipError_t bn_backward(int dt, const void* dy, const void* y, const void* z, long long M, int C,
                        const float* gamma, const float* mean, const float* invstd, float* dgamma,
-                       float* dbeta, void* dz, void* g_out, float* partials, hipStream_t stream);
+                       float* dbeta, void* dz, void* g_out, float* partials, hipStream_t stream,
+                       bool partials_ready = false);
 
 // ------------------------------------------------------------------ pooling
 hipError_t maxpool_fwd(int dt, const void* x, int N, int H, int W, int C, void* y, uint8_t* arg,

@@ -479,20 +479,25 @@ static hipError_t train_forward(TrainJob& j, int nb) {
   const int dt = j.dt;
   hipStream_t st = j.st;
   // train-mode BN (statistics, running-statistic update, apply) of layer bi
-  auto bn_train = [&](int bi, const void* z, long long M, const void* res, int relu, void* y) {
+  // (ready: the convolution producing z left its chunk statistics in bn_ws)
+  auto bn_train = [&](int bi, const void* z, long long M, const void* res, int relu, void* y,
+                      bool ready) {
     const BnL& b = net.bn[bi];
     return bn_train_forward(dt, z, M, b.C, j.master + b.g, j.master + b.b, j.master + b.rm,
                             j.master + b.rv, bnp(j.bn_mean, b), bnp(j.bn_invstd, b),
-                            bnp(j.bn_scale, b), bnp(j.bn_shift, b), res, relu, y, j.bn_ws, st);
+                            bnp(j.bn_scale, b), bnp(j.bn_shift, b), res, relu, y, j.bn_ws, st,
+                            ready);
   };
+  BnStatsSink sk;
+  sk.part = j.bn_ws;
   const void* cur = j.x0;
   for (int s = j.lowest; s <= 4; ++s) {
     if (s == 0) {
       ConvGeom cg = conv_geom(net, j.geo, 0, nb);
       EKYA_HIP(conv_fwd(dt, cg, cur, shadow_at(net, j.shadow, net.conv[0].sh_krsc), j.stem_Z,
-                        ConvEpilogue(), j.ws, j.ws_floats, st));
+                        ConvEpilogue(), j.ws, j.ws_floats, st, &sk));
       const long long M = (long long)nb * cg.P * cg.Q;
-      EKYA_HIP(bn_train(net.conv[0].bn, j.stem_Z, M, nullptr, 1, j.stem_A));
+      EKYA_HIP(bn_train(net.conv[0].bn, j.stem_Z, M, nullptr, 1, j.stem_A, sk.done));
       void* xm = j.acts[0].X;
       EKYA_HIP(maxpool_fwd(dt, j.stem_A, nb, j.geo.sh, j.geo.sw, 64, xm, j.stem_arg, st));
       cur = xm;
@@ -506,20 +511,20 @@ static hipError_t train_forward(TrainJob& j, int nb) {
       ConvGeom g1 = conv_geom(net, j.geo, b.c1, nb);
       const long long M = (long long)nb * g1.P * g1.Q;
       EKYA_HIP(conv_fwd(dt, g1, t.X, shadow_at(net, j.shadow, net.conv[b.c1].sh_krsc), t.Z1,
-                        ConvEpilogue(), j.ws, j.ws_floats, st));
-      EKYA_HIP(bn_train(net.conv[b.c1].bn, t.Z1, M, nullptr, 1, t.A1));
-      EKYA_HIP(conv_fwd(dt, conv_geom(net, j.geo, b.c2, nb), t.A1,
-                        shadow_at(net, j.shadow, net.conv[b.c2].sh_krsc), t.Z2, ConvEpilogue(), j.ws,
-                        j.ws_floats, st));
+                        ConvEpilogue(), j.ws, j.ws_floats, st, &sk));
+      EKYA_HIP(bn_train(net.conv[b.c1].bn, t.Z1, M, nullptr, 1, t.A1, sk.done));
       const void* res = t.X;
       if (b.cd >= 0) {  // projection shortcut: its BN output is the residual
         EKYA_HIP(conv_fwd(dt, conv_geom(net, j.geo, b.cd, nb), t.X,
                           shadow_at(net, j.shadow, net.conv[b.cd].sh_krsc), t.Zd, ConvEpilogue(),
-                          j.ws, j.ws_floats, st));
-        EKYA_HIP(bn_train(net.conv[b.cd].bn, t.Zd, M, nullptr, 0, j.g[0]));
+                          j.ws, j.ws_floats, st, &sk));
+        EKYA_HIP(bn_train(net.conv[b.cd].bn, t.Zd, M, nullptr, 0, j.g[0], sk.done));
         res = j.g[0];
       }
-      EKYA_HIP(bn_train(net.conv[b.c2].bn, t.Z2, M, res, 1, t.OUT));
+      EKYA_HIP(conv_fwd(dt, conv_geom(net, j.geo, b.c2, nb), t.A1,
+                        shadow_at(net, j.shadow, net.conv[b.c2].sh_krsc), t.Z2, ConvEpilogue(), j.ws,
+                        j.ws_floats, st, &sk));
+      EKYA_HIP(bn_train(net.conv[b.c2].bn, t.Z2, M, res, 1, t.OUT, sk.done));
       cur = t.OUT;
     }
     if (s == 4)  // average pool + classifier in one kernel
@@ -554,11 +559,23 @@ static hipError_t train_backward(TrainJob& j, int nb, const int32_t* fid, float*
     if (j.lowest < 5) EKYA_HIP(avgpool_bwd(dt, j.dpooled, nb, hw, 512, dout, st));
   }
   if (j.lowest == 5) return hipSuccess;
+  // (ready: the data gradient producing dy left the chunk statistics in bn_ws)
   auto bn_bwd = [&](int bi, const void* dy, const void* ymask, const void* z, long long M, void* dz,
-                    void* gout) {
+                    void* gout, bool ready) {
     const BnL& b = net.bn[bi];
     return bn_backward(dt, dy, ymask, z, M, b.C, j.master + b.g, bnp(j.bn_mean, b),
-                       bnp(j.bn_invstd, b), j.grad + b.g, j.grad + b.b, dz, gout, j.bn_ws, st);
+                       bnp(j.bn_invstd, b), j.grad + b.g, j.grad + b.b, dz, gout, j.bn_ws, st,
+                       ready);
+  };
+  // statistics sink of the BatchNorm whose dy a data gradient produces
+  auto sink_for = [&](int bni, const void* ymask, const void* z) {
+    BnStatsSink k;
+    k.part = j.bn_ws;
+    k.bwd = true;
+    k.ymask = ymask;
+    k.z = z;
+    k.mean = bnp(j.bn_mean, net.bn[bni]);
+    return k;
   };
   // Weight gradients go to st2 after a fork event on st; st records no
   // dependency on them until it reuses a dz buffer (two blocks later) or
@@ -612,10 +629,13 @@ static hipError_t train_backward(TrainJob& j, int nb, const int32_t* fid, float*
     last_join[parity] = -1;
     return hipSuccess;
   };
-  auto dgrad = [&](int ci, const void* dy, void* dx, const void* res, int n) {
+  auto dgrad = [&](int ci, const void* dy, void* dx, const void* res, int n,
+                   BnStatsSink* sink) {
     return conv_dgrad(dt, conv_geom(net, j.geo, ci, n), dy,
-                      shadow_at(net, j.shadow, net.conv[ci].sh_crsk), dx, res, j.ws, j.ws_floats, st);
+                      shadow_at(net, j.shadow, net.conv[ci].sh_crsk), dx, res, j.ws, j.ws_floats, st,
+                      sink);
   };
+  bool dout_ready = false;  // statistics of the next block's conv2 BatchNorm are in bn_ws
   int blk_count = 0;
   for (int s = 4; s >= j.lowest; --s) {
     if (s == 0) {
@@ -624,7 +644,7 @@ static hipError_t train_backward(TrainJob& j, int nb, const int32_t* fid, float*
       EKYA_HIP(reuse(par));
       EKYA_HIP(maxpool_bwd(dt, dout, j.stem_arg, nb, j.geo.sh, j.geo.sw, 64, gA, st));
       const long long M = (long long)nb * j.geo.sh * j.geo.sw;
-      EKYA_HIP(bn_bwd(net.conv[0].bn, gA, j.stem_A, j.stem_Z, M, j.gz1[par], nullptr));
+      EKYA_HIP(bn_bwd(net.conv[0].bn, gA, j.stem_A, j.stem_Z, M, j.gz1[par], nullptr, false));
       EKYA_HIP(wgrad_start(0, j.x0, j.gz1[par]));
       EKYA_HIP(wgrad_finish(0, false, par));
       break;
@@ -645,21 +665,34 @@ static hipError_t train_backward(TrainJob& j, int nb, const int32_t* fid, float*
       ConvGeom g1 = conv_geom(net, j.geo, b.c1, nb);
       const long long M = (long long)nb * g1.P * g1.Q;
       // g = dOut * [OUT > 0]; BN2 backward
-      EKYA_HIP(bn_bwd(net.conv[b.c2].bn, dout, t.OUT, t.Z2, M, gZ2, gG));
+      EKYA_HIP(bn_bwd(net.conv[b.c2].bn, dout, t.OUT, t.Z2, M, gZ2, gG, dout_ready));
+      dout_ready = false;
       const void* dx_sc = gG;
       if (b.cd >= 0) {
-        EKYA_HIP(bn_bwd(net.conv[b.cd].bn, gG, nullptr, t.Zd, M, gZd, nullptr));
+        EKYA_HIP(bn_bwd(net.conv[b.cd].bn, gG, nullptr, t.Zd, M, gZd, nullptr, false));
         EKYA_HIP(wgrad_start(b.cd, t.X, gZd));
-        if (need_dx) EKYA_HIP(dgrad(b.cd, gZd, dnext, nullptr, nb));
+        if (need_dx) EKYA_HIP(dgrad(b.cd, gZd, dnext, nullptr, nb, nullptr));
         EKYA_HIP(wgrad_finish(b.cd, need_dx, par));
         dx_sc = dnext;
       }
       EKYA_HIP(wgrad_start(b.c2, t.A1, gZ2));
-      EKYA_HIP(dgrad(b.c2, gZ2, gA, nullptr, nb));
+      BnStatsSink sk1 = sink_for(net.conv[b.c1].bn, t.A1, t.Z1);
+      EKYA_HIP(dgrad(b.c2, gZ2, gA, nullptr, nb, &sk1));
       EKYA_HIP(wgrad_finish(b.c2, true, par));
-      EKYA_HIP(bn_bwd(net.conv[b.c1].bn, gA, t.A1, t.Z1, M, gZ1, nullptr));
+      EKYA_HIP(bn_bwd(net.conv[b.c1].bn, gA, t.A1, t.Z1, M, gZ1, nullptr, sk1.done));
       EKYA_HIP(wgrad_start(b.c1, t.X, gZ1));
-      if (need_dx) EKYA_HIP(dgrad(b.c1, gZ1, dnext, dx_sc, nb));
+      if (need_dx) {
+        // dOut of the block processed next (bi - 1): its conv2 BatchNorm's statistics
+        BnStatsSink skn;
+        BnStatsSink* psk = nullptr;
+        if (bi > 0 && net.blk[bi - 1].stage >= j.lowest) {
+          const BlockL& nbk = net.blk[bi - 1];
+          skn = sink_for(net.conv[nbk.c2].bn, j.acts[bi - 1].OUT, j.acts[bi - 1].Z2);
+          psk = &skn;
+        }
+        EKYA_HIP(dgrad(b.c1, gZ1, dnext, dx_sc, nb, psk));
+        dout_ready = psk && psk->done;
+      }
       EKYA_HIP(wgrad_finish(b.c1, need_dx, par));
       if (need_dx) std::swap(dout, dnext);
     }
