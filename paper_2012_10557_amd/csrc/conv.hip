@@ -905,8 +905,8 @@ __global__ __launch_bounds__(NT) void gemm_dma_kernel(typename Op::Args a) {
     }
 }
 
-// Warp-specialised variant for BM = 256 rows: WGM x WGN compute waves (each a
-// 64 x 64 block of 16x16 MFMA tiles, two per SIMD) and four loader waves.  The
+// Warp-specialised variant: (BM / WTM) x (BN / WTN) compute waves (each a
+// WTM x WTN block of 16x16 MFMA tiles) and four loader waves.  The
 // loader waves keep the copies of the next NST - 1 stages in flight (the
 // CU's vector-memory path, not the MFMAs, is what a wave issuing its own
 // copies waits on); the compute waves only read LDS fragments and issue
@@ -915,10 +915,11 @@ __global__ __launch_bounds__(NT) void gemm_dma_kernel(typename Op::Args a) {
 // loaders refill after it.  Every wave executes the same barriers.
 constexpr int WS_LOADERS = 4;
 
-template <int BM, int BN, int NST, class Op>
-__global__ __launch_bounds__((BM / 64) * (BN / 64) * 64 + WS_LOADERS * 64) void gemm_ws_kernel(
+template <int BM, int BN, int WTM, int WTN, int NST, class Op>
+__global__ __launch_bounds__((BM / WTM) * (BN / WTN) * 64 + WS_LOADERS * 64) void gemm_ws_kernel(
     typename Op::Args a) {
-  constexpr int WGN = BN / 64, CW = (BM / 64) * WGN;
+  constexpr int WGN = BN / WTN, CW = (BM / WTM) * WGN;
+  constexpr int TI = WTM / 16, TJ = WTN / 16;
   constexpr int LPS = Op::IPW;            // copies per loader lane per stage
   constexpr int SU = (BM + BN) * 8;       // 16-byte units per stage
   static_assert(LPS * (NST - 2) < 64, "vmcnt range");
@@ -968,28 +969,28 @@ __global__ __launch_bounds__((BM / 64) * (BN / 64) * 64 + WS_LOADERS * 64) void 
   const int fr = lane & 15, fkc = lane >> 4;
   const int off0 = fr * 8 + (fkc ^ (fr & 7));
   const int off1 = fr * 8 + ((4 + fkc) ^ (fr & 7));
-  f32x4 acc[4][4];
+  f32x4 acc[TI][TJ];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < TI; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < TJ; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
   stage_barrier();
   int slot = 0;
   for (int st = s0; st < s1; ++st) {
-    const uint4* As = smem + slot * SU + (wm * 64) * 8;
-    const uint4* Bs = smem + slot * SU + (BM + wn * 64) * 8;
+    const uint4* As = smem + slot * SU + (wm * WTM) * 8;
+    const uint4* Bs = smem + slot * SU + (BM + wn * WTN) * 8;
 #pragma unroll
     for (int kf = 0; kf < 2; ++kf) {
       const int off = kf == 0 ? off0 : off1;
-      uint4 fa[4], fb[4];
+      uint4 fa[TI], fb[TJ];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) fa[i] = As[i * 128 + off];
+      for (int i = 0; i < TI; ++i) fa[i] = As[i * 128 + off];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) fb[j] = Bs[j * 128 + off];
+      for (int j = 0; j < TJ; ++j) fb[j] = Bs[j * 128 + off];
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < TI; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) mma_unit(acc[i][j], fa[i], fb[j], (bf16*)nullptr);
+        for (int j = 0; j < TJ; ++j) mma_unit(acc[i][j], fa[i], fb[j], (bf16*)nullptr);
     }
     stage_barrier();
     if (++slot == NST) slot = 0;
@@ -999,11 +1000,11 @@ __global__ __launch_bounds__((BM / 64) * (BN / 64) * 64 + WS_LOADERS * 64) void 
   op.split = split;
   const int lr = lane & 15, lg = lane >> 4;
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < TI; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < TJ; ++j) {
       float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
-      op.out4(a, m0 + wm * 64 + i * 16 + 4 * lg, n0 + wn * 64 + j * 16 + lr, v);
+      op.out4(a, m0 + wm * WTM + i * 16 + 4 * lg, n0 + wn * WTN + j * 16 + lr, v);
     }
 }
 
@@ -1563,18 +1564,23 @@ hipError_t split_finish(const float* part, int splits, long long npix, int C, co
 // the reduction split until ~400 blocks (>= 4 stages per split).
 struct DmaPlan {
   int bm, bn, splits, sps;
+  bool ws = false;  // warp-specialised kernel (always for bm = 256)
 };
 
 DmaPlan plan_dma(int rows, long long cols, int ns, bool allow_split) {
   if (rows % 256 == 0 && ns >= 8) {
     // warp-specialised 256 x 128 tiles, one block per CU: split the
-    // reduction until the blocks about fill the chip once (>= 4 stages each)
+    // reduction until the blocks about fill the chip once (>= 4 stages
+    // each) -- unless 128 x 64 tiles already give half a chip of blocks
+    // without splitting, which saves the fp32 partials' round trip
     const long long tiles = (long long)(rows / 256) * cdivl(cols, 128);
-    if (tiles >= 256 || !allow_split) return {256, 128, 1, ns};
+    if (tiles >= 256 || !allow_split) return {256, 128, 1, ns, true};
+    const long long small = (long long)(rows / 128) * cdivl(cols, 64);
+    if (small >= 128) return {128, 64, 1, ns, true};
     int s = (int)std::min<long long>(256 / tiles, 16);
     s = std::max(1, std::min(s, std::max(1, ns / 4)));
     const int sps = cdiv(ns, s);
-    return {256, 128, cdiv(ns, sps), sps};
+    return {256, 128, cdiv(ns, sps), sps, true};
   }
   struct Cand {
     int bm, bn, per_cu;
@@ -1619,10 +1625,9 @@ hipError_t launch_dma(typename OpT<BM, BN>::Args a, long long cols, int rows, hi
   return e;
 }
 
-template <int BM, int BN, template <int, int> class OpT>
+template <int BM, int BN, int WTM, int WTN, int NST, template <int, int> class OpT>
 hipError_t launch_ws(typename OpT<BM, BN>::Args a, long long cols, int rows, hipStream_t stream,
                      Cost cost, const char* name) {
-  constexpr int NST = 3;
   a.tiles_m = cdiv(rows, BM);
   a.tiles_n = (int)cdivl(cols, BN);
   dim3 grid(a.tiles_m * a.tiles_n * a.so.splits);
@@ -1633,8 +1638,8 @@ hipError_t launch_ws(typename OpT<BM, BN>::Args a, long long cols, int rows, hip
     e1 = t->take();
     EKYA_HIP(hipEventRecord(e0, stream));
   }
-  hipLaunchKernelGGL((gemm_ws_kernel<BM, BN, NST, OpT<BM, BN>>), grid,
-                     dim3((BM / 64) * (BN / 64) * 64 + WS_LOADERS * 64), 0, stream, a);
+  hipLaunchKernelGGL((gemm_ws_kernel<BM, BN, WTM, WTN, NST, OpT<BM, BN>>), grid,
+                     dim3((BM / WTM) * (BN / WTN) * 64 + WS_LOADERS * 64), 0, stream, a);
   hipError_t e = hipGetLastError();
   if (t && e == hipSuccess) {
     EKYA_HIP(hipEventRecord(e1, stream));
@@ -1648,7 +1653,10 @@ hipError_t launch_ws(typename OpT<BM, BN>::Args a, long long cols, int rows, hip
 template <template <int, int> class OpT, class Args>
 hipError_t dispatch_dma(Args a, const DmaPlan& p, long long cols, int rows, hipStream_t stream,
                         Cost cost, const char* name) {
-  if (p.bm == 256 && p.bn == 128) return launch_ws<256, 128, OpT>(a, cols, rows, stream, cost, name);
+  if (p.bm == 256 && p.bn == 128)
+    return launch_ws<256, 128, 64, 64, 3, OpT>(a, cols, rows, stream, cost, name);
+  if (p.bm == 128 && p.bn == 64 && p.ws)
+    return launch_ws<128, 64, 32, 64, 4, OpT>(a, cols, rows, stream, cost, name);
   if (p.bm == 128 && p.bn == 128) return launch_dma<128, 128, 2, OpT>(a, cols, rows, stream, cost, name);
   if (p.bm == 128 && p.bn == 64) return launch_dma<128, 64, 2, OpT>(a, cols, rows, stream, cost, name);
   if (p.bm == 64 && p.bn == 256) return launch_dma<64, 256, 1, OpT>(a, cols, rows, stream, cost, name);
@@ -1663,7 +1671,7 @@ hipError_t conv_fwd_dma(const ConvGeom& g, const void* x, const void* w, void* y
   const int ns = g.R * g.S * g.C / 64;
   const long long npix = (long long)g.N * g.P * g.Q;
   DmaPlan p = plan_dma(g.K, npix, ns, ws != nullptr);
-  if (p.splits > 1 && (size_t)p.splits * npix * g.K > ws_floats) p = {p.bm, p.bn, 1, ns};
+  if (p.splits > 1 && (size_t)p.splits * npix * g.K > ws_floats) p = {p.bm, p.bn, 1, ns, p.ws};
   DmaFwdArgs a{g, (const bf16*)x, (const bf16*)w, (bf16*)y, epi, SplitOut{ws, p.splits, p.sps}, 0, 0};
   hipError_t e = dispatch_dma<DmaFwdOp>(a, p, npix, g.K, stream,
                                        conv_cost(g, g.C0 ? g.C0 : g.C, sizeof(bf16), false),
@@ -1684,7 +1692,7 @@ hipError_t conv_dgrad_dma(const ConvGeom& g, const void* dy, const void* wt, voi
   const int ns = g.R * g.S * g.K / 64;
   const long long npix = (long long)g.N * g.H * g.W;
   DmaPlan p = plan_dma(g.C, npix, ns, ws != nullptr);
-  if (p.splits > 1 && (size_t)p.splits * npix * g.C > ws_floats) p = {p.bm, p.bn, 1, ns};
+  if (p.splits > 1 && (size_t)p.splits * npix * g.C > ws_floats) p = {p.bm, p.bn, 1, ns, p.ws};
   DmaDgradArgs a{g, (const bf16*)dy, (const bf16*)wt, (bf16*)dx, (const bf16*)res,
                  SplitOut{ws, p.splits, p.sps}, 0, 0};
   hipError_t e = dispatch_dma<DmaDgradOp>(a, p, npix, g.C, stream,
