@@ -1568,15 +1568,20 @@ struct DmaPlan {
 };
 
 DmaPlan plan_dma(int rows, long long cols, int ns, bool allow_split) {
+  // warp-specialised 128 x 256 tiles for 128 rows when they fill the chip
+  // without a split and the reduction is long enough (>= 16 stages) to
+  // amortise the pipeline fill
+  if (rows == 128 && ns >= 16 && cdivl(cols, 256) >= 256) return {128, 256, 1, ns, true};
   if (rows % 256 == 0 && ns >= 8) {
     // warp-specialised 256 x 128 tiles, one block per CU: split the
     // reduction until the blocks about fill the chip once (>= 4 stages
-    // each) -- unless 128 x 64 tiles already give half a chip of blocks
-    // without splitting, which saves the fp32 partials' round trip
+    // each) -- unless that would take a split of >= 2 and 128 x 64 tiles
+    // already give half a chip of blocks without one, which saves the fp32
+    // partials' round trip
     const long long tiles = (long long)(rows / 256) * cdivl(cols, 128);
     if (tiles >= 256 || !allow_split) return {256, 128, 1, ns, true};
     const long long small = (long long)(rows / 128) * cdivl(cols, 64);
-    if (small >= 128) return {128, 64, 1, ns, true};
+    if (tiles < 128 && small >= 128) return {128, 64, 1, ns, true};
     int s = (int)std::min<long long>(256 / tiles, 16);
     s = std::max(1, std::min(s, std::max(1, ns / 4)));
     const int sps = cdiv(ns, s);
@@ -1657,6 +1662,8 @@ hipError_t dispatch_dma(Args a, const DmaPlan& p, long long cols, int rows, hipS
     return launch_ws<256, 128, 64, 64, 3, OpT>(a, cols, rows, stream, cost, name);
   if (p.bm == 128 && p.bn == 64 && p.ws)
     return launch_ws<128, 64, 32, 64, 4, OpT>(a, cols, rows, stream, cost, name);
+  if (p.bm == 128 && p.bn == 256 && p.ws)
+    return launch_ws<128, 256, 64, 64, 3, OpT>(a, cols, rows, stream, cost, name);
   if (p.bm == 128 && p.bn == 128) return launch_dma<128, 128, 2, OpT>(a, cols, rows, stream, cost, name);
   if (p.bm == 128 && p.bn == 64) return launch_dma<128, 64, 2, OpT>(a, cols, rows, stream, cost, name);
   if (p.bm == 64 && p.bn == 256) return launch_dma<64, 256, 1, OpT>(a, cols, rows, stream, cost, name);

@@ -31,6 +31,8 @@ CONV_CASES = [
     (44, 14, 14, 256, 256, 3, 1, 1),  # layer3, 68 pixel tiles (ragged), split reductions,
                                       # 135 weight-gradient pixel stages
     (168, 14, 14, 256, 512, 3, 2, 1), # layer4.0.conv1, strided, 129 weight-gradient pixel stages
+    (22, 56, 56, 64, 64, 3, 1, 1),    # layer1, 270 tiles of 64 x 256 (ragged)
+    (84, 28, 28, 128, 128, 3, 1, 1),  # layer2, 258 tiles of 128 x 256 (ragged)
 ]
 
 
