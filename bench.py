@@ -102,6 +102,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--infer-frames", type=int, default=2000)
     ap.add_argument("--no-infer", action="store_true", help="skip the inference img/s measurement")
+    ap.add_argument("--timing-all-steps", action="store_true",
+                    help="per-kernel timing (serial schedule) on every step, so that a profiler "
+                         "run of this command measures the kernels as the roofline does")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -134,6 +137,8 @@ def main():
         return binding.ekya_retrain(ctx, weights, w["k"], frames, labels, hframes, hlabels, w["frac"],
                                     w["epochs"], w["lr"], w["momentum"], w["batch"], w["seed"])
 
+    if args.timing_all_steps:
+        binding.ekya_set_kernel_timing(ctx, True)
     for i in range(args.warmup):
         out = step()
         log(f"warmup {i}: {out['epoch_seconds']} acc {out['heldout_acc']}")
@@ -150,6 +155,7 @@ def main():
         f"prefix {out['prefix_seconds'] * 1e3:.2f} ms, epochs {[round(x * 1e3, 2) for x in out['epoch_seconds']]} ms")
 
     # one instrumented step: per-kernel event timing on the library's stream
+    # (the weight gradients then run on the job's stream, each kernel alone)
     binding.ekya_set_kernel_timing(ctx, True)
     step()
     stats = binding.ekya_kernel_timing(ctx)

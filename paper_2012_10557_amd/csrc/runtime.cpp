@@ -902,7 +902,8 @@ ekya_status run_retrain(Ctx& c, float* weights, int k, const void* frames, const
     EKYA_CHECK_HIP(hipStreamCreateWithFlags(&s2, hipStreamNonBlocking));
     c.streams.push_back(s2);
   }
-  j.st2 = c.timing ? stream : c.streams[0];  // per-kernel timing runs serially
+  // per-kernel timing runs serially, so each timed kernel runs alone
+  j.st2 = c.timing ? stream : c.streams[0];
   j.weights = weights;
   j.frames = frames;
   j.labels = labels;
