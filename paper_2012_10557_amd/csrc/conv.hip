@@ -1350,9 +1350,12 @@ constexpr int STEM_ROWS = 8, STEM_IN_ROWS = 2 * STEM_ROWS + 5;
 constexpr int STEM_WROW = 232;  // 224 filter entries per channel + 8 (bank spread)
 
 constexpr int STEM_NT = 512;
-__global__ __launch_bounds__(STEM_NT) void stem_kernel(const bf16* x, const bf16* wk, bf16* y,
-                                                  ConvEpilogue epi, int N, int H, int W, int P,
-                                                  int Q) {
+// RAW: x is [.][H][W][3] frames (image n at idx[n] when idx != null) read
+// with three 2-byte loads per pixel, instead of the 8-channel padded input.
+template <bool RAW>
+__global__ __launch_bounds__(STEM_NT) void stem_kernel(const bf16* x, const int32_t* idx,
+                                                  const bf16* wk, bf16* y, ConvEpilogue epi,
+                                                  int N, int H, int W, int P, int Q) {
   __shared__ __align__(16) uint2 patch[STEM_IN_ROWS * STEM_PATCH_W];  // 4 channels per pixel
   __shared__ __align__(16) bf16 wl[64 * STEM_WROW];
   const int blocks_per_img = cdiv(P, STEM_ROWS);
@@ -1376,7 +1379,8 @@ __global__ __launch_bounds__(STEM_NT) void stem_kernel(const bf16* x, const bf16
     }
   }
   // input rows 2 p0 - 3 .. 2 p0 + 17, columns -3 .. pw - 4 (zero outside the frame)
-  const bf16* img = x + (long long)n * H * W * 8;
+  const long long img_n = (RAW && idx) ? idx[n] : n;
+  const bf16* img = x + img_n * H * W * (RAW ? 3 : 8);
   const int total = STEM_IN_ROWS * pw;
   for (int i0 = threadIdx.x; i0 < total; i0 += 8 * STEM_NT) {
     uint2 v[8];
@@ -1384,9 +1388,16 @@ __global__ __launch_bounds__(STEM_NT) void stem_kernel(const bf16* x, const bf16
     for (int u = 0; u < 8; ++u) {
       const int i = i0 + u * STEM_NT, pr = i / pw, pc = i % pw;
       const int h = 2 * p0 - 3 + pr, w = pc - 3;
-      v[u] = (i < total && (unsigned)h < (unsigned)H && (unsigned)w < (unsigned)W)
-                 ? *reinterpret_cast<const uint2*>(img + ((long long)h * W + w) * 8)
-                 : make_uint2(0u, 0u);
+      const bool in = i < total && (unsigned)h < (unsigned)H && (unsigned)w < (unsigned)W;
+      if (RAW) {
+        const unsigned short* px =
+            reinterpret_cast<const unsigned short*>(img + ((long long)h * W + w) * 3);
+        v[u] = in ? make_uint2((unsigned)px[0] | ((unsigned)px[1] << 16), (unsigned)px[2])
+                  : make_uint2(0u, 0u);
+      } else {
+        v[u] = in ? *reinterpret_cast<const uint2*>(img + ((long long)h * W + w) * 8)
+                  : make_uint2(0u, 0u);
+      }
     }
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
@@ -1733,8 +1744,9 @@ hipError_t conv_fwd_t(const ConvGeom& g, const void* x, const void* w, void* y,
       e1 = t->take();
       EKYA_HIP(hipEventRecord(e0, stream));
     }
-    hipLaunchKernelGGL(stem_kernel, dim3(g.N * cdiv(g.P, STEM_ROWS)), dim3(STEM_NT), 0, stream, (const bf16*)x,
-                       (const bf16*)w, (bf16*)y, epi, g.N, g.H, g.W, g.P, g.Q);
+    hipLaunchKernelGGL(stem_kernel<false>, dim3(g.N * cdiv(g.P, STEM_ROWS)), dim3(STEM_NT), 0,
+                       stream, (const bf16*)x, (const int32_t*)nullptr, (const bf16*)w, (bf16*)y,
+                       epi, g.N, g.H, g.W, g.P, g.Q);
     hipError_t e = hipGetLastError();
     if (t && e == hipSuccess) {
       EKYA_HIP(hipEventRecord(e1, stream));
@@ -1945,6 +1957,34 @@ size_t conv_wgrad_workspace_floats(int dt, const ConvGeom& g) {
   }
   const WPlan p = plan_wgrad(dt, g);
   return (size_t)p.splits * g.K * g.R * g.S * g.C;
+}
+
+bool stem_frames_ok(int dt, const ConvGeom& g) {
+  return dt == DT_BF16 && g.C == 8 && (g.C0 == 0 || g.C0 == 3) && g.K == 64 && g.R == 7 &&
+         g.S == 7 && g.stride == 2 && g.pad == 3 && g.Q <= STEM_QMAX && g.Q >= 1;
+}
+
+hipError_t stem_fwd_frames(int dt, const ConvGeom& g, const void* frames, const int32_t* idx,
+                           const void* w, void* y, const ConvEpilogue& epi, hipStream_t stream) {
+  if (!stem_frames_ok(dt, g)) return hipErrorInvalidValue;
+  if (g.N == 0) return hipSuccess;
+  const Cost cost = conv_cost(g, 3, sizeof(bf16), false);
+  KernelTimer* t = t_timer;
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  if (t) {
+    e0 = t->take();
+    e1 = t->take();
+    EKYA_HIP(hipEventRecord(e0, stream));
+  }
+  hipLaunchKernelGGL(stem_kernel<true>, dim3(g.N * cdiv(g.P, STEM_ROWS)), dim3(STEM_NT), 0, stream,
+                     (const bf16*)frames, idx, (const bf16*)w, (bf16*)y, epi, g.N, g.H, g.W, g.P,
+                     g.Q);
+  hipError_t e = hipGetLastError();
+  if (t && e == hipSuccess) {
+    EKYA_HIP(hipEventRecord(e1, stream));
+    t->recs.push_back({"conv_fwd<bf16,stem7x7,frames>", cost.flops, cost.bytes, e0, e1});
+  }
+  return e;
 }
 
 hipError_t conv_fwd(int dt, const ConvGeom& g, const void* x, const void* w, void* y,

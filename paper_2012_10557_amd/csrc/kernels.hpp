@@ -68,6 +68,13 @@ struct BnStatsSink {
 hipError_t conv_fwd(int dt, const ConvGeom& g, const void* x, const void* w_krsc, void* y,
                     const ConvEpilogue& epi, float* ws, size_t ws_floats, hipStream_t stream,
                     BnStatsSink* sink = nullptr);
+// The 7x7/2 stem reading [.][H][W][3] frames directly (image n at idx[n] when
+// idx != null) in place of the padded input; g is the padded-input geometry
+// (C = 8).  bf16 with Q <= 112 only (stem_frames_ok).
+bool stem_frames_ok(int dt, const ConvGeom& g);
+hipError_t stem_fwd_frames(int dt, const ConvGeom& g, const void* frames, const int32_t* idx,
+                           const void* w_krsc, void* y, const ConvEpilogue& epi,
+                           hipStream_t stream);
 // dx[N,H,W,C] = conv-transpose of dy[N,P,Q,K] with wT[C,R,S,K] (+ res[N,H,W,C]).
 // Needs K a multiple of 64 (bf16) / 32 (fp32) and stride 1 or 2.
 hipError_t conv_dgrad(int dt, const ConvGeom& g, const void* dy, const void* w_crsk, void* dx,

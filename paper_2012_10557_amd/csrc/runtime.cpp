@@ -232,9 +232,12 @@ static inline void* shadow_at(const Net& net, void* shadow, long long off) {
 // Run stages lo..hi in eval mode (BatchNorm folded into the conv epilogue) on
 // n frames.  Output: hi <= 3: the stage's output tensor; hi == 4: the pooled
 // fp32 features [n, 512]; hi == 5: fp32 logits [n, classes].
+// raw: x (stage 0 only) is [.][H][W][3] frames, image i at raw_idx[i] when
+// raw_idx != null, read directly by the stem (stem_frames_ok).
 static hipError_t eval_forward(const Net& net, const Geo& g, const void* shadow, const float* fold,
                                const float* master, int lo, int hi, const void* x, int n,
-                               EvalBufs& b, void* out, hipStream_t st) {
+                               EvalBufs& b, void* out, hipStream_t st, bool raw = false,
+                               const int32_t* raw_idx = nullptr) {
   const int dt = net.dt;
   const void* cur = x;
   auto fold_scale = [&](int bi) { return fold + 2 * net.bn[bi].st; };
@@ -245,8 +248,13 @@ static hipError_t eval_forward(const Net& net, const Geo& g, const void* shadow,
       e.scale = fold_scale(net.conv[0].bn);
       e.shift = fold_shift(net.conv[0].bn);
       e.relu = 1;
-      EKYA_HIP(conv_fwd(dt, conv_geom(net, g, 0, n), cur, shadow_at(net, shadow, net.conv[0].sh_krsc),
-                        b.t1, e, b.ws, b.ws_floats, st));
+      if (raw)
+        EKYA_HIP(stem_fwd_frames(dt, conv_geom(net, g, 0, n), cur, raw_idx,
+                                 shadow_at(net, shadow, net.conv[0].sh_krsc), b.t1, e, st));
+      else
+        EKYA_HIP(conv_fwd(dt, conv_geom(net, g, 0, n), cur,
+                          shadow_at(net, shadow, net.conv[0].sh_krsc), b.t1, e, b.ws, b.ws_floats,
+                          st));
       void* dst = (hi == 0) ? out : b.p0;
       EKYA_HIP(maxpool_fwd(dt, b.t1, n, g.sh, g.sw, 64, dst, nullptr, st));
       cur = dst;
@@ -715,9 +723,14 @@ static hipError_t build_cache(const Net& net, const Geo& g, const void* shadow, 
   for (int i0 = 0; i0 < n; i0 += cap) {
     const int cnt = std::min(cap, n - i0);
     const void* src = d_idx ? frames : reinterpret_cast<const char*>(frames) + i0 * fbytes;
+    void* out = reinterpret_cast<char*>(cache) + (row0 + i0) * row_bytes;
+    if (stem_frames_ok(net.dt, conv_geom(net, g, 0, cnt))) {  // the stem reads the frames
+      EKYA_HIP(eval_forward(net, g, shadow, fold, master, 0, lowest - 1, src, cnt, eb, out, st,
+                            true, d_idx ? d_idx + i0 : nullptr));
+      continue;
+    }
     EKYA_HIP(frames_to_padded(net.dt, src, d_idx ? d_idx + i0 : nullptr, cnt, g.H, g.W,
                               net.conv[0].cin_pad, padded, st));
-    void* out = reinterpret_cast<char*>(cache) + (row0 + i0) * row_bytes;
     EKYA_HIP(eval_forward(net, g, shadow, fold, master, 0, lowest - 1, padded, cnt, eb, out, st));
   }
   return hipSuccess;
@@ -1214,13 +1227,19 @@ ekya_status run_infer(Ctx& c, const float* weights, const void* frames, int n, i
     for (int i0 = 0; i0 < n; i0 += cap) {
       const int cnt = std::min(cap, n - i0);
       const void* src = reinterpret_cast<const char*>(frames) + i0 * fbytes;
-      if (resolution == H && resolution == W)
-        EKYA_HIP(frames_to_padded(dt, src, nullptr, cnt, H, W, net.conv[0].cin_pad, padded, stream));
-      else
-        EKYA_HIP(resize_to_padded(dt, src, cnt, H, W, resolution, net.conv[0].cin_pad, padded,
-                                  stream));
-      EKYA_HIP(eval_forward(net, geo, shadow, fold, master, 0, 5, padded, cnt, eb, eb.logits,
-                            stream));
+      if (resolution == H && resolution == W && stem_frames_ok(dt, conv_geom(net, geo, 0, cnt))) {
+        EKYA_HIP(eval_forward(net, geo, shadow, fold, master, 0, 5, src, cnt, eb, eb.logits,
+                              stream, true));  // the stem reads the frames
+      } else {
+        if (resolution == H && resolution == W)
+          EKYA_HIP(frames_to_padded(dt, src, nullptr, cnt, H, W, net.conv[0].cin_pad, padded,
+                                    stream));
+        else
+          EKYA_HIP(resize_to_padded(dt, src, cnt, H, W, resolution, net.conv[0].cin_pad, padded,
+                                    stream));
+        EKYA_HIP(eval_forward(net, geo, shadow, fold, master, 0, 5, padded, cnt, eb, eb.logits,
+                              stream));
+      }
       EKYA_HIP(argmax_rows(eb.logits, cnt, net.n_classes, labels_out + i0, stream));
     }
     EKYA_HIP(hipEventRecord(c.infer_done, stream));
