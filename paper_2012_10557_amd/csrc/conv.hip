@@ -42,6 +42,23 @@ struct SplitOut {
   int stages_per_split;
 };
 
+// BatchNorm chunk partials an unsplit GEMM leaves from its epilogue (part
+// null: none); see wave_epilogue.
+struct BnEpi {
+  float* part = nullptr;
+  const bf16* ymask = nullptr;
+  const bf16* z = nullptr;
+  const float* mean = nullptr;
+  int bwd = 0;
+};
+
+// Stores v as bf16 and leaves the stored (rounded) values in v.
+__device__ __forceinline__ void store4_keep(bf16* dst, float (&v)[4]) {
+  store4<bf16>(dst, v);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) v[i] = (float)(bf16)v[i];
+}
+
 // ------------------------------------------------------------------ forward
 template <typename T> struct FwdArgs {
   ConvGeom g;
@@ -590,6 +607,7 @@ struct DmaFwdArgs {
   ConvEpilogue epi;
   SplitOut so;
   int tiles_m, tiles_n;
+  BnEpi bn;
 };
 
 template <int BM, int BN>
@@ -673,15 +691,18 @@ struct DmaFwdOp {
       }
     }
   }
-  __device__ void out4(const Args& a, int row, int col, float (&v)[4]) {
+  static __device__ int chans(const Args& a) { return a.g.K; }
+  static __device__ int pixels(const Args& a) { return a.g.N * a.g.P * a.g.Q; }
+  // True when it stored bf16 outputs (then v holds the stored values).
+  __device__ bool out4(const Args& a, int row, int col, float (&v)[4]) {
     const ConvGeom& g = a.g;
     const int npix = g.N * g.P * g.Q;
-    if (row >= g.K || col >= npix) return;
+    if (row >= g.K || col >= npix) return false;
     const long long off = (long long)col * g.K + row;
     if (a.so.splits > 1) {
       float* dst = a.so.part + (long long)split * npix * g.K + off;
       *reinterpret_cast<float4*>(dst) = make_float4(v[0], v[1], v[2], v[3]);
-      return;
+      return false;
     }
     const ConvEpilogue& e = a.epi;
     if (e.scale) {
@@ -702,7 +723,8 @@ struct DmaFwdOp {
 #pragma unroll
       for (int i = 0; i < 4; ++i) v[i] = relu_nan(v[i]);
     }
-    store4<bf16>(a.y + off, v);
+    store4_keep(a.y + off, v);
+    return true;
   }
 };
 
@@ -714,6 +736,7 @@ struct DmaDgradArgs {
   const bf16* res;
   SplitOut so;
   int tiles_m, tiles_n;
+  BnEpi bn;
 };
 
 // dx[pix][c] = sum_(r,s,k) wt[c][r][s][k] dy(pix; r,s,k), stride 1 or 2.
@@ -803,15 +826,17 @@ struct DmaDgradOp {
       }
     }
   }
-  __device__ void out4(const Args& a, int row, int col, float (&v)[4]) {
+  static __device__ int chans(const Args& a) { return a.g.C; }
+  static __device__ int pixels(const Args& a) { return a.g.N * a.g.H * a.g.W; }
+  __device__ bool out4(const Args& a, int row, int col, float (&v)[4]) {
     const ConvGeom& g = a.g;
     const int npix = g.N * g.H * g.W;
-    if (row >= g.C || col >= npix) return;
+    if (row >= g.C || col >= npix) return false;
     const long long off = (long long)col * g.C + row;
     if (a.so.splits > 1) {
       float* dst = a.so.part + (long long)split * npix * g.C + off;
       *reinterpret_cast<float4*>(dst) = make_float4(v[0], v[1], v[2], v[3]);
-      return;
+      return false;
     }
     if (a.res) {
       float r[4];
@@ -819,15 +844,166 @@ struct DmaDgradOp {
 #pragma unroll
       for (int i = 0; i < 4; ++i) v[i] += r[i];
     }
-    store4<bf16>(a.dx + off, v);
+    store4_keep(a.dx + off, v);
+    return true;
   }
 };
+
+// Four bf16 (8 bytes) to float.
+__device__ __forceinline__ void unpack4(uint2 u, float (&v)[4]) {
+  v[0] = __uint_as_float(u.x << 16);
+  v[1] = __uint_as_float(u.x & 0xffff0000u);
+  v[2] = __uint_as_float(u.y << 16);
+  v[3] = __uint_as_float(u.y & 0xffff0000u);
+}
+
+// x of the lane n places lower in the same 16-lane row (DPP row_ror:n).
+template <int N> __device__ __forceinline__ float row_ror(float x) {
+  static_assert(N >= 1 && N <= 15, "row_ror range");
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x120 + N, 0xF, 0xF,
+                                                    false));
+}
+
+// Sum over the 16 lanes of a row (lanes 16 r .. 16 r + 15): adding the value
+// rotated by 8, 4, 2, 1 lanes pairs the same two partial sums in both lanes
+// of each pair, so every lane of the row ends with the same value.
+__device__ __forceinline__ float row_sum16(float x) {
+  x += row_ror<8>(x);
+  x += row_ror<4>(x);
+  x += row_ror<2>(x);
+  x += row_ror<1>(x);
+  return x;
+}
+
+// Output of one wave's TI x TJ fragments: channels row0 + 16 i + 4 (lane / 16)
+// + 0..3 at pixel col0 + 16 j + lane % 16.  In the BNS variant with
+// a.bn.part set (TJ = 4, so the wave covers the 64 pixels [col0, col0 + 64):
+// BatchNorm chunk col0 / 64 of 64 rows) it also writes that chunk's per-channel partials of the stored
+// values, in the layout of the standalone BatchNorm kernels (row pair k:
+// first sums, then second sums, C each).  Forward: the sum and the squared
+// deviations from the chunk mean.  Backward, with g = out [* (ymask > 0)]:
+// sum g and sum g (z - mean).  A lane adds its own fragments in order, then
+// the 16 lanes of a row (one channel's pixels) are combined by row_sum16.
+template <int TI, int TJ, bool BNS, class Op>
+__device__ __forceinline__ void wave_epilogue(const typename Op::Args& a, Op& op,
+                                              f32x4 (&acc)[TI][TJ], int row0, int col0,
+                                              int lane) {
+  const int lr = lane & 15, lg = lane >> 4;
+  if constexpr (BNS && TJ == 4) {
+    if (a.bn.part) {
+      const int C = Op::chans(a), npix = Op::pixels(a);
+      // backward: the BatchNorm input z and the ReLU mask of the lane's
+      // outputs, loaded before the stores (clamped in range; out-of-range
+      // outputs are excluded below).  The loads are issued as inline asm and
+      // waited for explicitly: loads the compiler tracks anywhere in this
+      // kernel make it add full vmcnt waits to the loader waves' copy loop.
+      uint2 zr[TI][TJ], yr[TI][TJ];
+      if (a.bn.bwd) {
+        const bf16* ym = a.bn.ymask ? a.bn.ymask : a.bn.z;
+#pragma unroll
+        for (int i = 0; i < TI; ++i)
+#pragma unroll
+          for (int j = 0; j < TJ; ++j) {
+            const int row = min(row0 + i * 16 + 4 * lg, C - 4);
+            const int col = min(col0 + j * 16 + lr, npix - 1);
+            const long long off = (long long)col * C + row;
+            asm volatile("global_load_dwordx2 %0, %1, off" : "=v"(zr[i][j]) : "v"(a.bn.z + off)
+                         : "memory");
+            asm volatile("global_load_dwordx2 %0, %1, off" : "=v"(yr[i][j]) : "v"(ym + off)
+                         : "memory");
+          }
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+#pragma unroll
+        for (int i = 0; i < TI; ++i)
+#pragma unroll
+          for (int j = 0; j < TJ; ++j) {
+            asm volatile("" : "+v"(zr[i][j]));
+            asm volatile("" : "+v"(yr[i][j]));
+            if (!a.bn.ymask) yr[i][j] = make_uint2(0x3f803f80u, 0x3f803f80u);  // 1.0 each
+          }
+      }
+      // store, keeping the stored values in acc
+#pragma unroll
+      for (int i = 0; i < TI; ++i)
+#pragma unroll
+        for (int j = 0; j < TJ; ++j) {
+          float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
+          op.out4(a, row0 + i * 16 + 4 * lg, col0 + j * 16 + lr, v);
+          acc[i][j] = f32x4{v[0], v[1], v[2], v[3]};
+        }
+      if (col0 >= npix) return;
+      float* p = a.bn.part + (long long)(col0 / 64) * 2 * C;
+      const float nk = (float)min(64, npix - col0);
+#pragma unroll
+      for (int i = 0; i < TI; ++i) {
+        const int row = row0 + i * 16 + 4 * lg;
+        if (!a.bn.bwd) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            float x = 0.f;
+#pragma unroll
+            for (int j = 0; j < TJ; ++j) x += col0 + j * 16 + lr < npix ? acc[i][j][e] : 0.f;
+            const float s1 = row_sum16(x);
+            const float mu = s1 / nk;
+            float y = 0.f;
+#pragma unroll
+            for (int j = 0; j < TJ; ++j) {
+              const float d = acc[i][j][e] - mu;
+              y += col0 + j * 16 + lr < npix ? d * d : 0.f;
+            }
+            const float s2 = row_sum16(y);
+            if (lr == 0 && row < C) {
+              p[row + e] = s1;
+              p[C + row + e] = s2;
+            }
+          }
+        } else {
+          float mu[4] = {0.f, 0.f, 0.f, 0.f};
+          if (row < C) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) mu[e] = a.bn.mean[row + e];
+          }
+          float x[4] = {0.f, 0.f, 0.f, 0.f}, y[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int j = 0; j < TJ; ++j) {
+            const bool in = row < C && col0 + j * 16 + lr < npix;
+            float zz[4], yy[4];
+            unpack4(zr[i][j], zz);
+            unpack4(yr[i][j], yy);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const float g = (in && yy[e] > 0.f) ? acc[i][j][e] : 0.f;
+              x[e] += g;
+              y[e] += g * (zz[e] - mu[e]);
+            }
+          }
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float s1 = row_sum16(x[e]), s2 = row_sum16(y[e]);
+            if (lr == 0 && row < C) {
+              p[row + e] = s1;
+              p[C + row + e] = s2;
+            }
+          }
+        }
+      }
+      return;
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < TI; ++i)
+#pragma unroll
+    for (int j = 0; j < TJ; ++j) {
+      float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
+      op.out4(a, row0 + i * 16 + 4 * lg, col0 + j * 16 + lr, v);
+    }
+}
 
 // 4 waves as WGM x (4 / WGM); each wave owns a (BM/WGM) x (BN*WGM/4) block of
 // 16x16 MFMA tiles.  Stage st waits for its own loads (vmcnt), a barrier makes
 // every wave's loads visible and retires the slot read in the previous
 // iteration, which then receives stage st + NST - 1.
-template <int BM, int BN, int WGM, int NST, class Op>
+template <int BM, int BN, int WGM, int NST, class Op, bool BNS = false>
 __global__ __launch_bounds__(NT) void gemm_dma_kernel(typename Op::Args a) {
   constexpr int WGN = 4 / WGM;
   static_assert((BM + BN) % 32 == 0, "row octets split over 4 waves");
@@ -895,14 +1071,7 @@ __global__ __launch_bounds__(NT) void gemm_dma_kernel(typename Op::Args a) {
     if (++slot == NST) slot = 0;
   }
 
-  const int lr = lane & 15, lg = lane >> 4;
-#pragma unroll
-  for (int i = 0; i < TI; ++i)
-#pragma unroll
-    for (int j = 0; j < TJ; ++j) {
-      float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
-      op.out4(a, m0 + wm * WM + i * 16 + 4 * lg, n0 + wn * WN + j * 16 + lr, v);
-    }
+  wave_epilogue<TI, TJ, BNS>(a, op, acc, m0 + wm * WM, n0 + wn * WN, lane);
 }
 
 // Warp-specialised variant: (BM / WTM) x (BN / WTN) compute waves (each a
@@ -915,7 +1084,7 @@ __global__ __launch_bounds__(NT) void gemm_dma_kernel(typename Op::Args a) {
 // loaders refill after it.  Every wave executes the same barriers.
 constexpr int WS_LOADERS = 4;
 
-template <int BM, int BN, int WTM, int WTN, int NST, class Op>
+template <int BM, int BN, int WTM, int WTN, int NST, class Op, bool BNS = false>
 __global__ __launch_bounds__((BM / WTM) * (BN / WTN) * 64 + WS_LOADERS * 64) void gemm_ws_kernel(
     typename Op::Args a) {
   constexpr int WGN = BN / WTN, CW = (BM / WTM) * WGN;
@@ -998,14 +1167,7 @@ __global__ __launch_bounds__((BM / WTM) * (BN / WTN) * 64 + WS_LOADERS * 64) voi
 
   Op op;
   op.split = split;
-  const int lr = lane & 15, lg = lane >> 4;
-#pragma unroll
-  for (int i = 0; i < TI; ++i)
-#pragma unroll
-    for (int j = 0; j < TJ; ++j) {
-      float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
-      op.out4(a, m0 + wm * WTM + i * 16 + 4 * lg, n0 + wn * WTN + j * 16 + lr, v);
-    }
+  wave_epilogue<TI, TJ, BNS>(a, op, acc, m0 + wm * WTM, n0 + wn * WTN, lane);
 }
 
 // ------------------------------------------- direct-to-LDS weight gradient
@@ -1630,7 +1792,18 @@ hipError_t launch_dma(typename OpT<BM, BN>::Args a, long long cols, int rows, hi
     e1 = t->take();
     EKYA_HIP(hipEventRecord(e0, stream));
   }
-  hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, WGM, 2, OpT<BM, BN>>), grid, dim3(NT), 0, stream, a);
+  // the BatchNorm-statistics variant exists for 128 x 128 tiles (64 pixels per wave)
+  if constexpr (BM == 128 && BN == 128 && WGM == 2) {
+    if (a.bn.part)
+      hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, WGM, 2, OpT<BM, BN>, true>), grid, dim3(NT), 0,
+                         stream, a);
+    else
+      hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, WGM, 2, OpT<BM, BN>>), grid, dim3(NT), 0, stream,
+                         a);
+  } else {
+    if (a.bn.part) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, WGM, 2, OpT<BM, BN>>), grid, dim3(NT), 0, stream, a);
+  }
   hipError_t e = hipGetLastError();
   if (t && e == hipSuccess) {
     EKYA_HIP(hipEventRecord(e1, stream));
@@ -1654,8 +1827,20 @@ hipError_t launch_ws(typename OpT<BM, BN>::Args a, long long cols, int rows, hip
     e1 = t->take();
     EKYA_HIP(hipEventRecord(e0, stream));
   }
-  hipLaunchKernelGGL((gemm_ws_kernel<BM, BN, WTM, WTN, NST, OpT<BM, BN>>), grid,
-                     dim3((BM / WTM) * (BN / WTN) * 64 + WS_LOADERS * 64), 0, stream, a);
+  const dim3 block((BM / WTM) * (BN / WTN) * 64 + WS_LOADERS * 64);
+  // the BatchNorm-statistics variant exists for 128 x 64 tiles (64 pixels per wave)
+  if constexpr (BM == 128 && BN == 64 && WTN == 64) {
+    if (a.bn.part)
+      hipLaunchKernelGGL((gemm_ws_kernel<BM, BN, WTM, WTN, NST, OpT<BM, BN>, true>), grid, block,
+                         0, stream, a);
+    else
+      hipLaunchKernelGGL((gemm_ws_kernel<BM, BN, WTM, WTN, NST, OpT<BM, BN>>), grid, block, 0,
+                         stream, a);
+  } else {
+    if (a.bn.part) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((gemm_ws_kernel<BM, BN, WTM, WTN, NST, OpT<BM, BN>>), grid, block, 0,
+                       stream, a);
+  }
   hipError_t e = hipGetLastError();
   if (t && e == hipSuccess) {
     EKYA_HIP(hipEventRecord(e1, stream));
@@ -1682,6 +1867,12 @@ hipError_t dispatch_dma(Args a, const DmaPlan& p, long long cols, int rows, hipS
   return hipErrorInvalidValue;
 }
 
+// Whether the kernel dispatch_dma runs for an unsplit plan has a variant that
+// leaves BatchNorm chunk statistics (launch_ws / launch_dma).
+bool plan_bn_epilogue(const DmaPlan& p) {
+  return p.splits == 1 && p.bm == 128 && ((p.bn == 64 && p.ws) || (p.bn == 128 && !p.ws));
+}
+
 // bf16 forward with C % 64 == 0 on the direct-to-LDS path.
 hipError_t conv_fwd_dma(const ConvGeom& g, const void* x, const void* w, void* y,
                         const ConvEpilogue& epi, float* ws, size_t ws_floats, hipStream_t stream,
@@ -1691,13 +1882,21 @@ hipError_t conv_fwd_dma(const ConvGeom& g, const void* x, const void* w, void* y
   DmaPlan p = plan_dma(g.K, npix, ns, ws != nullptr);
   if (p.splits > 1 && (size_t)p.splits * npix * g.K > ws_floats) p = {p.bm, p.bn, 1, ns, p.ws};
   DmaFwdArgs a{g, (const bf16*)x, (const bf16*)w, (bf16*)y, epi, SplitOut{ws, p.splits, p.sps}, 0, 0};
+  const bool plain = !epi.scale && !epi.shift && !epi.res && !epi.relu;
+  const bool bn_epi = sink && !sink->bwd && sink->part && plain && plan_bn_epilogue(p) &&
+                      bn_fold_path(npix, g.K);
+  if (bn_epi) a.bn.part = sink->part;
   hipError_t e = dispatch_dma<DmaFwdOp>(a, p, npix, g.K, stream,
                                        conv_cost(g, g.C0 ? g.C0 : g.C, sizeof(bf16), false),
                                        "conv_fwd");
-  if (e != hipSuccess || p.splits <= 1) return e;
-  if (sink && !sink->bwd && !epi.scale && !epi.shift && !epi.res && !epi.relu &&
-      bn_fold_path(npix, g.K)) {
+  if (e == hipSuccess && bn_epi) {
     sink->done = true;
+    sink->rows = 64;
+  }
+  if (e != hipSuccess || p.splits <= 1) return e;
+  if (sink && !sink->bwd && plain && bn_fold_path(npix, g.K)) {
+    sink->done = true;
+    sink->rows = 128;
     return split_reduce_bn(DT_BF16, ws, p.splits, npix, g.K, nullptr, y, *sink, stream);
   }
   return split_finish<bf16>(ws, p.splits, npix, g.K, epi, y, stream);
@@ -1713,11 +1912,25 @@ hipError_t conv_dgrad_dma(const ConvGeom& g, const void* dy, const void* wt, voi
   if (p.splits > 1 && (size_t)p.splits * npix * g.C > ws_floats) p = {p.bm, p.bn, 1, ns, p.ws};
   DmaDgradArgs a{g, (const bf16*)dy, (const bf16*)wt, (bf16*)dx, (const bf16*)res,
                  SplitOut{ws, p.splits, p.sps}, 0, 0};
+  const bool bn_epi = sink && sink->bwd && sink->part && sink->z && sink->mean &&
+                      plan_bn_epilogue(p) && bn_fold_path(npix, g.C);
+  if (bn_epi) {
+    a.bn.part = sink->part;
+    a.bn.ymask = (const bf16*)sink->ymask;
+    a.bn.z = (const bf16*)sink->z;
+    a.bn.mean = sink->mean;
+    a.bn.bwd = 1;
+  }
   hipError_t e = dispatch_dma<DmaDgradOp>(a, p, npix, g.C, stream,
                                          conv_cost(g, g.C, sizeof(bf16), false), "conv_dgrad");
+  if (e == hipSuccess && bn_epi) {
+    sink->done = true;
+    sink->rows = 64;
+  }
   if (e != hipSuccess || p.splits <= 1) return e;
   if (sink && sink->bwd && bn_fold_path(npix, g.C)) {
     sink->done = true;
+    sink->rows = 128;
     return split_reduce_bn(DT_BF16, ws, p.splits, npix, g.C, res, dx, *sink, stream);
   }
   ConvEpilogue ep;

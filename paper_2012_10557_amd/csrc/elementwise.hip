@@ -293,12 +293,13 @@ __global__ __launch_bounds__(256) void bn_group_partial(const T* z, const T* dy,
 }
 
 // Mean and biased variance of channel c = 64 blockIdx.y + threadIdx.x % 64
-// over M rows from forward chunk partials (S1, M2): Chan's combination in
+// over M rows from forward partials (S1, M2) of chunks of `crows` rows
+// (the last one ragged): Chan's combination in
 // double, M2 = sum_k [M2_k + n_k (S1_k / n_k - mean)^2], four slices of chunks
 // (k = slice, slice + 4, ...) added in slice order.  The same in every block;
 // true for the thread (one per channel) that holds the result.
-__device__ __forceinline__ bool group_stats(const float* part, int nch, long long M, int C,
-                                            double& mean, double& var) {
+__device__ __forceinline__ bool group_stats(const float* part, int nch, int crows, long long M,
+                                            int C, double& mean, double& var) {
   __shared__ double sa[4][BN_GROUP];
   __shared__ double smu[BN_GROUP];
   const int lc = threadIdx.x % BN_GROUP, sl = threadIdx.x / BN_GROUP;
@@ -312,7 +313,7 @@ __device__ __forceinline__ bool group_stats(const float* part, int nch, long lon
   const double mu = smu[lc];
   double y = 0.0;
   for (int k = sl; k < nch; k += 4) {
-    const double nk = (double)std::min<long long>(BN_FOLD_ROWS, M - (long long)k * BN_FOLD_ROWS);
+    const double nk = (double)std::min<long long>(crows, M - (long long)k * crows);
     const double d = (double)part[(long long)k * 2 * C + c] / nk - mu;
     y += (double)part[(long long)k * 2 * C + C + c] + nk * d * d;
   }
@@ -353,7 +354,7 @@ __device__ __forceinline__ bool group_sums(const float* part, int nch, int C, do
 // running statistics.
 template <typename T>
 __global__ __launch_bounds__(256) void bn_fold_apply(const T* z, const float* part, int nch,
-                                                     long long M, int C, long long rpb,
+                                                     int crows, long long M, int C, long long rpb,
                                                      const float* gamma, const float* beta,
                                                      float* rm, float* rv, float* mean,
                                                      float* invstd, float* scale, float* shift,
@@ -362,7 +363,7 @@ __global__ __launch_bounds__(256) void bn_fold_apply(const T* z, const float* pa
   __shared__ float cf[3][BN_GROUP];
   const int t = threadIdx.x;
   double mean_d, var;
-  if (group_stats(part, nch, M, C, mean_d, var)) {
+  if (group_stats(part, nch, crows, M, C, mean_d, var)) {
     const int c = blockIdx.y * BN_GROUP + t;
     const float mu = (float)mean_d;
     const float is = (float)(1.0 / sqrt(var + (double)BN_EPS));
@@ -1491,24 +1492,27 @@ hipError_t split_reduce_bn(int dt, const float* part, int splits, long long M, i
 hipError_t bn_train_forward(int dt, const void* z, long long M, int C, const float* gamma,
                             const float* beta, float* rm, float* rv, float* mean, float* invstd,
                             float* scale, float* shift, const void* res, int relu, void* y,
-                            float* partials, hipStream_t stream, bool partials_ready) {
+                            float* partials, hipStream_t stream, int ready_rows) {
   if (M == 0) return hipSuccess;
+  if (ready_rows != 0 && ((ready_rows != 64 && ready_rows != BN_FOLD_ROWS) || !bn_fold_ok(M, C)))
+    return hipErrorInvalidValue;
   if (!bn_fold_ok(M, C)) {
     hipError_t e = bn_train_stats(dt, z, M, C, gamma, beta, rm, rv, mean, invstd, scale, shift,
                                   partials, stream);
     if (e != hipSuccess) return e;
     return bn_apply(dt, z, M, C, mean, scale, beta, res, relu, y, stream);
   }
-  const int nch = (int)cdivl(M, BN_FOLD_ROWS), groups = C / BN_GROUP;
+  const int crows = ready_rows ? ready_rows : BN_FOLD_ROWS;
+  const int nch = (int)cdivl(M, crows), groups = C / BN_GROUP;
   const long long rpb = bn_fold_rpb(M, C, dt);
   return by_type(dt, [&](auto* tp) {
     using T = std::remove_pointer_t<decltype(tp)>;
-    if (!partials_ready)
+    if (!ready_rows)
       hipLaunchKernelGGL((bn_group_partial<T, false>), dim3(nch, groups), dim3(256), 0, stream,
                          (const T*)z, (const T*)nullptr, (const T*)nullptr, (const float*)nullptr,
                          M, C, partials);
     hipLaunchKernelGGL(bn_fold_apply<T>, dim3((unsigned)cdivl(M, rpb), groups), dim3(256), 0,
-                       stream, (const T*)z, partials, nch, M, C, rpb, gamma, beta, rm, rv, mean,
+                       stream, (const T*)z, partials, nch, crows, M, C, rpb, gamma, beta, rm, rv, mean,
                        invstd, scale, shift, (const T*)res, relu, (T*)y);
   });
 }
@@ -1535,14 +1539,16 @@ hipError_t bn_fold(const float* params, const long long* tab, int n, float* out,
 hipError_t bn_backward(int dt, const void* dy, const void* y, const void* z, long long M, int C,
                        const float* gamma, const float* mean, const float* invstd, float* dgamma,
                        float* dbeta, void* dz, void* g_out, float* partials, hipStream_t stream,
-                       bool partials_ready) {
+                       int ready_rows) {
   if (M == 0) return hipSuccess;
+  if (ready_rows != 0 && ((ready_rows != 64 && ready_rows != BN_FOLD_ROWS) || !bn_fold_ok(M, C)))
+    return hipErrorInvalidValue;
   if (bn_fold_ok(M, C)) {
-    const int nf = (int)cdivl(M, BN_FOLD_ROWS), groups = C / BN_GROUP;
+    const int nf = (int)cdivl(M, ready_rows ? ready_rows : BN_FOLD_ROWS), groups = C / BN_GROUP;
     const long long rpb = bn_fold_rpb(M, C, dt);
     return by_type(dt, [&](auto* tp) {
       using T = std::remove_pointer_t<decltype(tp)>;
-      if (!partials_ready)
+      if (!ready_rows)
         hipLaunchKernelGGL((bn_group_partial<T, true>), dim3(nf, groups), dim3(256), 0, stream,
                            (const T*)z, (const T*)dy, (const T*)y, mean, M, C, partials);
       hipLaunchKernelGGL(bn_bwd_fold_apply<T>, dim3((unsigned)cdivl(M, rpb), groups), dim3(256), 0,

@@ -47,10 +47,12 @@ struct ConvEpilogue {
   int relu = 0;
 };
 
-// BatchNorm chunk partials for the two-launch BatchNorm path, produced while
-// a split convolution's partials are reduced (bf16 direct-to-LDS path, empty
-// forward epilogue, M within bn_fold_path).  `done` reports whether they were;
-// otherwise the caller computes them.  Forward: statistics of the output.
+// BatchNorm chunk partials for the two-launch BatchNorm path, produced by a
+// convolution on the bf16 direct-to-LDS path (empty forward epilogue, M
+// within bn_fold_path): in the epilogue of an unsplit GEMM whose waves each
+// cover 64 output pixels (chunks of 64 rows), or while a split GEMM's
+// partials are reduced (chunks of 128 rows).  `done` reports whether they
+// were; otherwise the caller computes them.  Forward: statistics of the output.
 // Backward (bwd): of g = out * [ymask > 0] (no mask when null) against z and
 // mean, as bn_backward's first pass.
 struct BnStatsSink {
@@ -60,6 +62,7 @@ struct BnStatsSink {
   const void* z = nullptr;
   const float* mean = nullptr;
   bool done = false;
+  int rows = 0;  // rows per chunk of the partials when done (64 or 128)
 };
 
 // y[N,P,Q,K] = conv(x[N,H,W,C], w[K,R,S,C]) with the epilogue.  `ws` (fp32,
@@ -114,12 +117,12 @@ hipError_t bn_train_stats(int dt, const void* z, long long M, int C, const float
                           float* scale, float* shift, float* partials, hipStream_t stream);
 // bn_train_stats followed by bn_apply: y = relu?((z - mean)*scale + beta + res).
 // Two launches when M is at most 64 chunks of 128 rows and C a multiple of 64.
-// partials_ready: `partials` already holds the chunk partials of z (from a
-// BnStatsSink).
+// ready_rows > 0: `partials` already holds the chunk partials of z in chunks
+// of that many rows (64 or 128, from a BnStatsSink).
 hipError_t bn_train_forward(int dt, const void* z, long long M, int C, const float* gamma,
                             const float* beta, float* rm, float* rv, float* mean, float* invstd,
                             float* scale, float* shift, const void* res, int relu, void* y,
-                            float* partials, hipStream_t stream, bool partials_ready = false);
+                            float* partials, hipStream_t stream, int ready_rows = 0);
 // y = (z - mean)*scale + beta (+ res) (ReLU), elementwise over [M, C].
 hipError_t bn_apply(int dt, const void* z, long long M, int C, const float* mean,
                     const float* scale, const float* beta, const void* res, int relu, void* y,
@@ -133,11 +136,11 @@ hipError_t bn_fold(const float* params, const long long* tab, int n, float* out,
 // g = dy * [y > 0]; dgamma = sum g*xhat; dbeta = sum g;
 // dz = gamma*invstd*(g - dbeta/M - xhat*dgamma/M).  Writes dgamma/dbeta and
 // dz; when g_out != null also writes g.
-// partials_ready: as for bn_train_forward.
+// ready_rows: as for bn_train_forward.
 hipError_t bn_backward(int dt, const void* dy, const void* y, const void* z, long long M, int C,
                        const float* gamma, const float* mean, const float* invstd, float* dgamma,
                        float* dbeta, void* dz, void* g_out, float* partials, hipStream_t stream,
-                       bool partials_ready = false);
+                       int ready_rows = 0);
 
 // ------------------------------------------------------------------ pooling
 hipError_t maxpool_fwd(int dt, const void* x, int N, int H, int W, int C, void* y, uint8_t* arg,

@@ -487,9 +487,10 @@ static hipError_t train_forward(TrainJob& j, int nb) {
   const int dt = j.dt;
   hipStream_t st = j.st;
   // train-mode BN (statistics, running-statistic update, apply) of layer bi
-  // (ready: the convolution producing z left its chunk statistics in bn_ws)
+  // (ready > 0: the convolution producing z left its chunk statistics in
+  // bn_ws, in chunks of that many rows)
   auto bn_train = [&](int bi, const void* z, long long M, const void* res, int relu, void* y,
-                      bool ready) {
+                      int ready) {
     const BnL& b = net.bn[bi];
     return bn_train_forward(dt, z, M, b.C, j.master + b.g, j.master + b.b, j.master + b.rm,
                             j.master + b.rv, bnp(j.bn_mean, b), bnp(j.bn_invstd, b),
@@ -505,7 +506,7 @@ static hipError_t train_forward(TrainJob& j, int nb) {
       EKYA_HIP(conv_fwd(dt, cg, cur, shadow_at(net, j.shadow, net.conv[0].sh_krsc), j.stem_Z,
                         ConvEpilogue(), j.ws, j.ws_floats, st, &sk));
       const long long M = (long long)nb * cg.P * cg.Q;
-      EKYA_HIP(bn_train(net.conv[0].bn, j.stem_Z, M, nullptr, 1, j.stem_A, sk.done));
+      EKYA_HIP(bn_train(net.conv[0].bn, j.stem_Z, M, nullptr, 1, j.stem_A, sk.done ? sk.rows : 0));
       void* xm = j.acts[0].X;
       EKYA_HIP(maxpool_fwd(dt, j.stem_A, nb, j.geo.sh, j.geo.sw, 64, xm, j.stem_arg, st));
       cur = xm;
@@ -520,19 +521,19 @@ static hipError_t train_forward(TrainJob& j, int nb) {
       const long long M = (long long)nb * g1.P * g1.Q;
       EKYA_HIP(conv_fwd(dt, g1, t.X, shadow_at(net, j.shadow, net.conv[b.c1].sh_krsc), t.Z1,
                         ConvEpilogue(), j.ws, j.ws_floats, st, &sk));
-      EKYA_HIP(bn_train(net.conv[b.c1].bn, t.Z1, M, nullptr, 1, t.A1, sk.done));
+      EKYA_HIP(bn_train(net.conv[b.c1].bn, t.Z1, M, nullptr, 1, t.A1, sk.done ? sk.rows : 0));
       const void* res = t.X;
       if (b.cd >= 0) {  // projection shortcut: its BN output is the residual
         EKYA_HIP(conv_fwd(dt, conv_geom(net, j.geo, b.cd, nb), t.X,
                           shadow_at(net, j.shadow, net.conv[b.cd].sh_krsc), t.Zd, ConvEpilogue(),
                           j.ws, j.ws_floats, st, &sk));
-        EKYA_HIP(bn_train(net.conv[b.cd].bn, t.Zd, M, nullptr, 0, j.g[0], sk.done));
+        EKYA_HIP(bn_train(net.conv[b.cd].bn, t.Zd, M, nullptr, 0, j.g[0], sk.done ? sk.rows : 0));
         res = j.g[0];
       }
       EKYA_HIP(conv_fwd(dt, conv_geom(net, j.geo, b.c2, nb), t.A1,
                         shadow_at(net, j.shadow, net.conv[b.c2].sh_krsc), t.Z2, ConvEpilogue(), j.ws,
                         j.ws_floats, st, &sk));
-      EKYA_HIP(bn_train(net.conv[b.c2].bn, t.Z2, M, res, 1, t.OUT, sk.done));
+      EKYA_HIP(bn_train(net.conv[b.c2].bn, t.Z2, M, res, 1, t.OUT, sk.done ? sk.rows : 0));
       cur = t.OUT;
     }
     if (s == 4)  // average pool + classifier in one kernel
@@ -567,9 +568,10 @@ static hipError_t train_backward(TrainJob& j, int nb, const int32_t* fid, float*
     if (j.lowest < 5) EKYA_HIP(avgpool_bwd(dt, j.dpooled, nb, hw, 512, dout, st));
   }
   if (j.lowest == 5) return hipSuccess;
-  // (ready: the data gradient producing dy left the chunk statistics in bn_ws)
+  // (ready > 0: the data gradient producing dy left the chunk statistics in
+  // bn_ws, in chunks of that many rows)
   auto bn_bwd = [&](int bi, const void* dy, const void* ymask, const void* z, long long M, void* dz,
-                    void* gout, bool ready) {
+                    void* gout, int ready) {
     const BnL& b = net.bn[bi];
     return bn_backward(dt, dy, ymask, z, M, b.C, j.master + b.g, bnp(j.bn_mean, b),
                        bnp(j.bn_invstd, b), j.grad + b.g, j.grad + b.b, dz, gout, j.bn_ws, st,
@@ -643,7 +645,7 @@ static hipError_t train_backward(TrainJob& j, int nb, const int32_t* fid, float*
                       shadow_at(net, j.shadow, net.conv[ci].sh_crsk), dx, res, j.ws, j.ws_floats, st,
                       sink);
   };
-  bool dout_ready = false;  // statistics of the next block's conv2 BatchNorm are in bn_ws
+  int dout_ready = 0;  // statistics of the next block's conv2 BatchNorm are in bn_ws (chunk rows)
   int blk_count = 0;
   for (int s = 4; s >= j.lowest; --s) {
     if (s == 0) {
@@ -652,7 +654,7 @@ static hipError_t train_backward(TrainJob& j, int nb, const int32_t* fid, float*
       EKYA_HIP(reuse(par));
       EKYA_HIP(maxpool_bwd(dt, dout, j.stem_arg, nb, j.geo.sh, j.geo.sw, 64, gA, st));
       const long long M = (long long)nb * j.geo.sh * j.geo.sw;
-      EKYA_HIP(bn_bwd(net.conv[0].bn, gA, j.stem_A, j.stem_Z, M, j.gz1[par], nullptr, false));
+      EKYA_HIP(bn_bwd(net.conv[0].bn, gA, j.stem_A, j.stem_Z, M, j.gz1[par], nullptr, 0));
       EKYA_HIP(wgrad_start(0, j.x0, j.gz1[par]));
       EKYA_HIP(wgrad_finish(0, false, par));
       break;
@@ -674,10 +676,10 @@ static hipError_t train_backward(TrainJob& j, int nb, const int32_t* fid, float*
       const long long M = (long long)nb * g1.P * g1.Q;
       // g = dOut * [OUT > 0]; BN2 backward
       EKYA_HIP(bn_bwd(net.conv[b.c2].bn, dout, t.OUT, t.Z2, M, gZ2, gG, dout_ready));
-      dout_ready = false;
+      dout_ready = 0;
       const void* dx_sc = gG;
       if (b.cd >= 0) {
-        EKYA_HIP(bn_bwd(net.conv[b.cd].bn, gG, nullptr, t.Zd, M, gZd, nullptr, false));
+        EKYA_HIP(bn_bwd(net.conv[b.cd].bn, gG, nullptr, t.Zd, M, gZd, nullptr, 0));
         EKYA_HIP(wgrad_start(b.cd, t.X, gZd));
         if (need_dx) EKYA_HIP(dgrad(b.cd, gZd, dnext, nullptr, nb, nullptr));
         EKYA_HIP(wgrad_finish(b.cd, need_dx, par));
@@ -687,7 +689,7 @@ static hipError_t train_backward(TrainJob& j, int nb, const int32_t* fid, float*
       BnStatsSink sk1 = sink_for(net.conv[b.c1].bn, t.A1, t.Z1);
       EKYA_HIP(dgrad(b.c2, gZ2, gA, nullptr, nb, &sk1));
       EKYA_HIP(wgrad_finish(b.c2, true, par));
-      EKYA_HIP(bn_bwd(net.conv[b.c1].bn, gA, t.A1, t.Z1, M, gZ1, nullptr, sk1.done));
+      EKYA_HIP(bn_bwd(net.conv[b.c1].bn, gA, t.A1, t.Z1, M, gZ1, nullptr, sk1.done ? sk1.rows : 0));
       EKYA_HIP(wgrad_start(b.c1, t.X, gZ1));
       if (need_dx) {
         // dOut of the block processed next (bi - 1): its conv2 BatchNorm's statistics
@@ -699,7 +701,7 @@ static hipError_t train_backward(TrainJob& j, int nb, const int32_t* fid, float*
           psk = &skn;
         }
         EKYA_HIP(dgrad(b.c1, gZ1, dnext, dx_sc, nb, psk));
-        dout_ready = psk && psk->done;
+        dout_ready = (psk && psk->done) ? psk->rows : 0;
       }
       EKYA_HIP(wgrad_finish(b.c1, need_dx, par));
       if (need_dx) std::swap(dout, dnext);

@@ -26,9 +26,12 @@ def ctx():
     binding.ekya_destroy(c)
 
 
-@pytest.mark.parametrize("k,n", [(1, 40), (2, 40)])
+@pytest.mark.parametrize("k,n", [(1, 40), (2, 40), (2, 64)])
 def test_bf16_one_step_224_matches_oracle(ctx, k, n):
-    """n frames at 224 px, one batch, one SGD step from identical state.
+    """n frames at 224 px, one batch, one SGD step from identical state (at
+    n = 40 the layer4 convolutions split their reduction and BatchNorm
+    statistics come from the split reduction; at n = 64, the retraining
+    batch, they run unsplit and the GEMM epilogues leave the statistics).
     Within 2e-2 of the oracle: the step loss, the BatchNorm running-statistic
     updates (batch statistics of the activations) and the classifier update.
     Conv and BatchNorm parameter updates of the trainable stages go through
