@@ -293,51 +293,74 @@ __global__ __launch_bounds__(256) void bn_group_partial(const T* z, const T* dy,
 }
 
 // Mean and biased variance of channel c = 64 blockIdx.y + threadIdx.x % 64
-// over M rows from forward partials (S1, M2) of chunks of `crows` rows
-// (the last one ragged): Chan's combination in
-// double, M2 = sum_k [M2_k + n_k (S1_k / n_k - mean)^2], four slices of chunks
-// (k = slice, slice + 4, ...) added in slice order.  The same in every block;
-// true for the thread (one per channel) that holds the result.
+// over M rows from forward partials (S1_k, M2_k) of chunks of `crows` rows
+// (the last one ragged), in one pass in double: S = sum S1_k and
+// Q = sum [M2_k + S1_k^2 / n_k] (the chunk's sum of squares), mean = S / M,
+// var = (Q - S^2 / M) / M.  Four slices of chunks (k = slice, slice + 4, ...)
+// are added in slice order; a slice loads GS_BATCH chunks before adding them
+// in k order, so the loads overlap.  The same in every block; true for the
+// thread (one per channel) that holds the result.
+constexpr int GS_BATCH = 8;
 __device__ __forceinline__ bool group_stats(const float* part, int nch, int crows, long long M,
                                             int C, double& mean, double& var) {
-  __shared__ double sa[4][BN_GROUP];
-  __shared__ double smu[BN_GROUP];
+  __shared__ double sa[4][BN_GROUP], sb[4][BN_GROUP];
   const int lc = threadIdx.x % BN_GROUP, sl = threadIdx.x / BN_GROUP;
   const int c = blockIdx.y * BN_GROUP + lc;
-  double x = 0.0;
-  for (int k = sl; k < nch; k += 4) x += (double)part[(long long)k * 2 * C + c];
-  sa[sl][lc] = x;
-  __syncthreads();
-  if (sl == 0) smu[lc] = (((sa[0][lc] + sa[1][lc]) + sa[2][lc]) + sa[3][lc]) / (double)M;
-  __syncthreads();
-  const double mu = smu[lc];
-  double y = 0.0;
-  for (int k = sl; k < nch; k += 4) {
-    const double nk = (double)std::min<long long>(crows, M - (long long)k * crows);
-    const double d = (double)part[(long long)k * 2 * C + c] / nk - mu;
-    y += (double)part[(long long)k * 2 * C + C + c] + nk * d * d;
+  double x = 0.0, y = 0.0;
+  for (int k0 = sl; k0 < nch; k0 += 4 * GS_BATCH) {
+    float v1[GS_BATCH], v2[GS_BATCH];
+#pragma unroll
+    for (int u = 0; u < GS_BATCH; ++u) {
+      const int k = k0 + 4 * u;
+      v1[u] = k < nch ? part[(long long)k * 2 * C + c] : 0.f;
+      v2[u] = k < nch ? part[(long long)k * 2 * C + C + c] : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < GS_BATCH; ++u) {
+      const int k = k0 + 4 * u;
+      if (k < nch) {
+        const double nk = (double)std::min<long long>(crows, M - (long long)k * crows);
+        const double s1 = (double)v1[u];
+        x += s1;
+        y += (double)v2[u] + s1 * s1 / nk;
+      }
+    }
   }
-  __syncthreads();
-  sa[sl][lc] = y;
+  sa[sl][lc] = x;
+  sb[sl][lc] = y;
   __syncthreads();
   if (sl != 0) return false;
-  mean = mu;
-  var = (((sa[0][lc] + sa[1][lc]) + sa[2][lc]) + sa[3][lc]) / (double)M;
+  const double S = ((sa[0][lc] + sa[1][lc]) + sa[2][lc]) + sa[3][lc];
+  const double Q = ((sb[0][lc] + sb[1][lc]) + sb[2][lc]) + sb[3][lc];
+  mean = S / (double)M;
+  var = std::max(0.0, (Q - S * mean) / (double)M);
   return true;
 }
 
 // Totals of the two partial rows for channel c = 64 blockIdx.y + threadIdx.x % 64:
-// four slices of chunks (k = slice, slice + 4, ...) in float, the slices added
-// in order in double.  True for the thread (one per channel) that holds them.
+// four slices of chunks (k = slice, slice + 4, ...) in float, loaded in
+// batches as in group_stats, the slices added in order in double.  True for
+// the thread (one per channel) that holds them.
 __device__ __forceinline__ bool group_sums(const float* part, int nch, int C, double& a,
                                            double& b) {
   __shared__ float sa[4][BN_GROUP], sb[4][BN_GROUP];
   const int lc = threadIdx.x % BN_GROUP, sl = threadIdx.x / BN_GROUP;
   const int c = blockIdx.y * BN_GROUP + lc;
   float x = 0.f, y = 0.f;
-  for (int k = sl; k < nch; k += 4) {
-    x += part[(long long)k * 2 * C + c];
-    y += part[(long long)k * 2 * C + C + c];
+  for (int k0 = sl; k0 < nch; k0 += 4 * GS_BATCH) {
+    float v1[GS_BATCH], v2[GS_BATCH];
+#pragma unroll
+    for (int u = 0; u < GS_BATCH; ++u) {
+      const int k = k0 + 4 * u;
+      v1[u] = k < nch ? part[(long long)k * 2 * C + c] : 0.f;
+      v2[u] = k < nch ? part[(long long)k * 2 * C + C + c] : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < GS_BATCH; ++u)
+      if (k0 + 4 * u < nch) {
+        x += v1[u];
+        y += v2[u];
+      }
   }
   sa[sl][lc] = x;
   sb[sl][lc] = y;
