@@ -376,6 +376,8 @@ static size_t ws_floats(const TrainJob& j) {
     for (int n = 1; n <= j.B; ++n) {
       ConvGeom cg = conv_geom(net, j.geo, (int)i, n);
       m = std::max(m, conv_wgrad_workspace_floats(j.dt, cg));
+      // the last weight gradients of a step run on the main stream in ws
+      if (fused_update(net, c)) m = std::max(m, conv_wgrad_partials_floats(j.dt, cg));
       m = std::max(m, bn_partials_floats((long long)n * cg.P * cg.Q, c.cout));
       m = std::max(m, conv_split_workspace_floats(j.dt, cg, false));
       if (c.stage > 0) m = std::max(m, conv_split_workspace_floats(j.dt, cg, true));
@@ -593,41 +595,49 @@ static hipError_t train_backward(TrainJob& j, int nb, const int32_t* fid, float*
   // gradient as split partials in ws2, and its momentum step (which rewrites
   // the weight copy its data gradient reads) follows on st2 once st has
   // queued that data gradient (wgrad_finish after the dgrad call).
+  // A weight gradient with no data gradient after it on st (the last block,
+  // the stem) runs on st itself with st's scratch ws (`main`): st has no
+  // other work left, and it saves the cross-stream event waits.
   int nf = 0;
   int last_join[2] = {-1, -1};  // per buffer parity: join event of its last reader
   int pending = -1, pending_splits = 0;
+  bool pending_main = false;
   const bool two = j.st2 != st;
-  auto wgrad_start = [&](int ci, const void* x, const void* dy) -> hipError_t {
+  auto wgrad_start = [&](int ci, const void* x, const void* dy, bool main) -> hipError_t {
     if (nf >= TrainJob::kForks) return hipErrorInvalidValue;
     const ConvL& c = net.conv[ci];
     const ConvGeom cg = conv_geom(net, j.geo, ci, nb);
-    if (two) {
+    hipStream_t ws = main ? st : j.st2;
+    float* scratch = main ? j.ws : j.ws2;
+    if (two && !main) {
       EKYA_HIP(hipEventRecord(j.fork[nf], st));
       EKYA_HIP(hipStreamWaitEvent(j.st2, j.fork[nf], 0));
     }
+    pending_main = main;
     if (fused_update(net, c)) {
-      EKYA_HIP(conv_wgrad_partials(dt, cg, x, dy, j.ws2, &pending_splits, j.st2));
+      EKYA_HIP(conv_wgrad_partials(dt, cg, x, dy, scratch, &pending_splits, ws));
       pending = ci;
     } else {
-      EKYA_HIP(conv_wgrad(dt, cg, x, dy, j.ws2, j.grad + c.off, c.cin, j.st2));
+      EKYA_HIP(conv_wgrad(dt, cg, x, dy, scratch, j.grad + c.off, c.cin, ws));
       pending = -1;
     }
     return hipSuccess;
   };
   auto wgrad_finish = [&](int ci, bool after_dgrad, int parity) -> hipError_t {
+    hipStream_t ws = pending_main ? st : j.st2;
     if (pending == ci) {
       const ConvL& c = net.conv[ci];
-      if (two && after_dgrad) {
+      if (two && after_dgrad && !pending_main) {
         EKYA_HIP(hipEventRecord(j.dgdone[nf], st));
         EKYA_HIP(hipStreamWaitEvent(j.st2, j.dgdone[nf], 0));
       }
-      EKYA_HIP(conv_weight_update(dt, j.ws2, pending_splits, c.cout, c.R * c.S, c.cin,
-                                  j.master + c.off, j.mom + c.off, j.lr, j.mu,
+      EKYA_HIP(conv_weight_update(dt, pending_main ? j.ws : j.ws2, pending_splits, c.cout,
+                                  c.R * c.S, c.cin, j.master + c.off, j.mom + c.off, j.lr, j.mu,
                                   shadow_at(net, j.shadow, c.sh_krsc),
-                                  shadow_at(net, j.shadow, c.sh_crsk), j.st2));
+                                  shadow_at(net, j.shadow, c.sh_crsk), ws));
       pending = -1;
     }
-    if (two) {
+    if (two && !pending_main) {
       EKYA_HIP(hipEventRecord(j.joined[nf], j.st2));
       last_join[parity] = nf;
     }
@@ -655,7 +665,7 @@ static hipError_t train_backward(TrainJob& j, int nb, const int32_t* fid, float*
       EKYA_HIP(maxpool_bwd(dt, dout, j.stem_arg, nb, j.geo.sh, j.geo.sw, 64, gA, st));
       const long long M = (long long)nb * j.geo.sh * j.geo.sw;
       EKYA_HIP(bn_bwd(net.conv[0].bn, gA, j.stem_A, j.stem_Z, M, j.gz1[par], nullptr, 0));
-      EKYA_HIP(wgrad_start(0, j.x0, j.gz1[par]));
+      EKYA_HIP(wgrad_start(0, j.x0, j.gz1[par], true));
       EKYA_HIP(wgrad_finish(0, false, par));
       break;
     }
@@ -680,17 +690,17 @@ static hipError_t train_backward(TrainJob& j, int nb, const int32_t* fid, float*
       const void* dx_sc = gG;
       if (b.cd >= 0) {
         EKYA_HIP(bn_bwd(net.conv[b.cd].bn, gG, nullptr, t.Zd, M, gZd, nullptr, 0));
-        EKYA_HIP(wgrad_start(b.cd, t.X, gZd));
+        EKYA_HIP(wgrad_start(b.cd, t.X, gZd, false));
         if (need_dx) EKYA_HIP(dgrad(b.cd, gZd, dnext, nullptr, nb, nullptr));
         EKYA_HIP(wgrad_finish(b.cd, need_dx, par));
         dx_sc = dnext;
       }
-      EKYA_HIP(wgrad_start(b.c2, t.A1, gZ2));
+      EKYA_HIP(wgrad_start(b.c2, t.A1, gZ2, false));
       BnStatsSink sk1 = sink_for(net.conv[b.c1].bn, t.A1, t.Z1);
       EKYA_HIP(dgrad(b.c2, gZ2, gA, nullptr, nb, &sk1));
       EKYA_HIP(wgrad_finish(b.c2, true, par));
       EKYA_HIP(bn_bwd(net.conv[b.c1].bn, gA, t.A1, t.Z1, M, gZ1, nullptr, sk1.done ? sk1.rows : 0));
-      EKYA_HIP(wgrad_start(b.c1, t.X, gZ1));
+      EKYA_HIP(wgrad_start(b.c1, t.X, gZ1, !need_dx));
       if (need_dx) {
         // dOut of the block processed next (bi - 1): its conv2 BatchNorm's statistics
         BnStatsSink skn;
