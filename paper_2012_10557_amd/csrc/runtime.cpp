@@ -358,6 +358,7 @@ struct TrainJob {
   size_t ws_floats = 0;
   float* bn_ws = nullptr;      // BatchNorm partials
   size_t bn_ws_floats = 0;
+  float* bn_ws2 = nullptr;     // BatchNorm partials of work on st2 (projection shortcuts)
   float* ce_out = nullptr;     // n_steps x 3
   int32_t* hcount = nullptr;   // epochs
   EvalBufs eval;
@@ -455,7 +456,8 @@ static void plan_job(Arena& a, TrainJob& j) {
       j.gz1[p] = a.take_bytes(gmax * es);
       j.gzd[p] = a.take_bytes(gmax * es);
     }
-    j.ws2_floats = wgrad_ws_floats(j);
+    // st2 also runs the projection-shortcut convolutions of the forward pass
+    j.ws2_floats = std::max(wgrad_ws_floats(j), ws_floats(j));
     j.ws2 = a.take<float>(j.ws2_floats);
   }
   j.pooled = a.take<float>((size_t)j.B * 512);
@@ -474,6 +476,7 @@ static void plan_job(Arena& a, TrainJob& j) {
     }
   }
   j.bn_ws = a.take<float>(j.bn_ws_floats);
+  j.bn_ws2 = a.take<float>(j.bn_ws_floats);
   j.ce_out = a.take<float>((size_t)j.n_steps * 3);
   j.hcount = a.take<int32_t>(j.epochs);
   j.eval_cap = std::max(1, std::min(j.n_h, 512));
@@ -489,18 +492,29 @@ static hipError_t train_forward(TrainJob& j, int nb) {
   const int dt = j.dt;
   hipStream_t st = j.st;
   // train-mode BN (statistics, running-statistic update, apply) of layer bi
-  // (ready > 0: the convolution producing z left its chunk statistics in
-  // bn_ws, in chunks of that many rows)
-  auto bn_train = [&](int bi, const void* z, long long M, const void* res, int relu, void* y,
-                      int ready) {
+  // on stream q with partial scratch part (ready > 0: the convolution
+  // producing z left its chunk statistics there, in chunks of that many rows)
+  auto bn_train_on = [&](int bi, const void* z, long long M, const void* res, int relu, void* y,
+                         int ready, float* part, hipStream_t q) {
     const BnL& b = net.bn[bi];
     return bn_train_forward(dt, z, M, b.C, j.master + b.g, j.master + b.b, j.master + b.rm,
                             j.master + b.rv, bnp(j.bn_mean, b), bnp(j.bn_invstd, b),
-                            bnp(j.bn_scale, b), bnp(j.bn_shift, b), res, relu, y, j.bn_ws, st,
-                            ready);
+                            bnp(j.bn_scale, b), bnp(j.bn_shift, b), res, relu, y, part, q, ready);
   };
+  auto bn_train = [&](int bi, const void* z, long long M, const void* res, int relu, void* y,
+                      int ready) { return bn_train_on(bi, z, M, res, relu, y, ready, j.bn_ws, st); };
   BnStatsSink sk;
   sk.part = j.bn_ws;
+  // A projection shortcut (convolution + BatchNorm, BatchNorm partials in
+  // bn_ws2) runs on st2 beside the block's main branch, with st2's split
+  // scratch; st waits for it before the second BatchNorm, which adds it.
+  // Events from the top of the fork arrays (the backward pass uses them from
+  // the bottom).  With one stream it runs between the first convolution and
+  // its BatchNorm.
+  const bool two = j.st2 != st;
+  BnStatsSink skd;
+  skd.part = j.bn_ws2;
+  int fi = TrainJob::kForks - 1;
   const void* cur = j.x0;
   for (int s = j.lowest; s <= 4; ++s) {
     if (s == 0) {
@@ -521,20 +535,35 @@ static hipError_t train_forward(TrainJob& j, int nb) {
       t.X = const_cast<void*>(cur);
       ConvGeom g1 = conv_geom(net, j.geo, b.c1, nb);
       const long long M = (long long)nb * g1.P * g1.Q;
+      const void* res = t.X;
+      int joined = -1;
+      const bool side = b.cd >= 0 && two;
+      if (side) {  // the block input is ready: fork before queueing the main branch
+        if (fi < TrainJob::kForks / 2) return hipErrorInvalidValue;
+        EKYA_HIP(hipEventRecord(j.fork[fi], st));
+      }
       EKYA_HIP(conv_fwd(dt, g1, t.X, shadow_at(net, j.shadow, net.conv[b.c1].sh_krsc), t.Z1,
                         ConvEpilogue(), j.ws, j.ws_floats, st, &sk));
-      EKYA_HIP(bn_train(net.conv[b.c1].bn, t.Z1, M, nullptr, 1, t.A1, sk.done ? sk.rows : 0));
-      const void* res = t.X;
+      const int ready1 = sk.done ? sk.rows : 0;
       if (b.cd >= 0) {  // projection shortcut: its BN output is the residual
+        hipStream_t q = side ? j.st2 : st;
+        if (side) EKYA_HIP(hipStreamWaitEvent(q, j.fork[fi], 0));
         EKYA_HIP(conv_fwd(dt, conv_geom(net, j.geo, b.cd, nb), t.X,
                           shadow_at(net, j.shadow, net.conv[b.cd].sh_krsc), t.Zd, ConvEpilogue(),
-                          j.ws, j.ws_floats, st, &sk));
-        EKYA_HIP(bn_train(net.conv[b.cd].bn, t.Zd, M, nullptr, 0, j.g[0], sk.done ? sk.rows : 0));
+                          side ? j.ws2 : j.ws, side ? j.ws2_floats : j.ws_floats, q, &skd));
+        EKYA_HIP(bn_train_on(net.conv[b.cd].bn, t.Zd, M, nullptr, 0, j.g[0],
+                             skd.done ? skd.rows : 0, j.bn_ws2, q));
+        if (side) {
+          EKYA_HIP(hipEventRecord(j.joined[fi], q));
+          joined = fi--;
+        }
         res = j.g[0];
       }
+      EKYA_HIP(bn_train(net.conv[b.c1].bn, t.Z1, M, nullptr, 1, t.A1, ready1));
       EKYA_HIP(conv_fwd(dt, conv_geom(net, j.geo, b.c2, nb), t.A1,
                         shadow_at(net, j.shadow, net.conv[b.c2].sh_krsc), t.Z2, ConvEpilogue(), j.ws,
                         j.ws_floats, st, &sk));
+      if (joined >= 0) EKYA_HIP(hipStreamWaitEvent(st, j.joined[joined], 0));
       EKYA_HIP(bn_train(net.conv[b.c2].bn, t.Z2, M, res, 1, t.OUT, sk.done ? sk.rows : 0));
       cur = t.OUT;
     }
