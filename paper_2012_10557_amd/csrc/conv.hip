@@ -1512,43 +1512,67 @@ constexpr int STEM_ROWS = 8, STEM_IN_ROWS = 2 * STEM_ROWS + 5;
 constexpr int STEM_WROW = 232;  // 224 filter entries per channel + 8 (bank spread)
 
 constexpr int STEM_NT = 512;
+
+// The eval-mode stem followed by the 3x3 / stride 2 / pad 1 max pool (POOL):
+// a block produces 4 pool rows (4 b .. 4 b + 3) of one image from the 9 stem
+// rows 8 b - 1 .. 8 b + 7 (9 waves, one row each; rows outside the image are
+// skipped).  After the epilogue each wave takes, for every pool column c,
+// the maximum over stem columns 2 c - 1, 2 c, 2 c + 1 (the neighbouring
+// columns come from the adjacent lanes of a 16-lane row, and for column
+// 16 t - 1 from lane 15 of block t - 1, by DPP rotations), rounds it to bf16
+// and writes the 56-column row to LDS, over the staged input; the block then
+// takes the maximum over the 3 stem rows of each pool row.  Maxima skip NaNs
+// (start from -inf and take greater values), as the separate max pool does;
+// rounding is monotone, so the result equals pooling the rounded stem output.
+constexpr int SP_QMAX = STEM_QMAX / 2;  // pool columns
+__device__ __forceinline__ float gt_max(float m, float v) { return v > m ? v : m; }
+
 // RAW: x is [.][H][W][3] frames (image n at idx[n] when idx != null) read
 // with three 2-byte loads per pixel, instead of the 8-channel padded input.
-template <bool RAW>
-__global__ __launch_bounds__(STEM_NT) void stem_kernel(const bf16* x, const int32_t* idx,
-                                                  const bf16* wk, bf16* y, ConvEpilogue epi,
-                                                  int N, int H, int W, int P, int Q) {
-  __shared__ __align__(16) uint2 patch[STEM_IN_ROWS * STEM_PATCH_W];  // 4 channels per pixel
-  __shared__ __align__(16) bf16 wl[64 * STEM_WROW];
-  const int blocks_per_img = cdiv(P, STEM_ROWS);
-  const int n = blockIdx.x / blocks_per_img, p0 = (blockIdx.x % blocks_per_img) * STEM_ROWS;
+template <bool RAW, bool POOL = false>
+__global__ __launch_bounds__(STEM_NT + (POOL ? 64 : 0)) void stem_kernel(
+    const bf16* x, const int32_t* idx, const bf16* wk, bf16* y, ConvEpilogue epi, int N, int H,
+    int W, int P, int Q) {
+  constexpr int ROWS = POOL ? STEM_ROWS + 1 : STEM_ROWS, NT = ROWS * 64;
+  constexpr int IN_ROWS = 2 * ROWS + 5;
+  constexpr int PATCH_BYTES = IN_ROWS * STEM_PATCH_W * 8, W_BYTES = 64 * STEM_WROW * 2;
+  constexpr int POOL_BYTES = POOL ? ROWS * SP_QMAX * 64 * 2 : 0;
+  constexpr int LDS_BYTES = PATCH_BYTES + W_BYTES > POOL_BYTES ? PATCH_BYTES + W_BYTES : POOL_BYTES;
+  static_assert(PATCH_BYTES % 16 == 0, "filter alignment");
+  __shared__ __align__(16) char lds[LDS_BYTES];
+  uint2* patch = reinterpret_cast<uint2*>(lds);                // 4 channels per pixel
+  bf16* wl = reinterpret_cast<bf16*>(lds + PATCH_BYTES);
+  const int PP = (P - 1) / 2 + 1, PQ = (Q - 1) / 2 + 1;  // pool output (POOL)
+  const int blocks_per_img = POOL ? cdiv(PP, 4) : cdiv(P, STEM_ROWS);
+  const int n = blockIdx.x / blocks_per_img, bq = blockIdx.x % blocks_per_img;
+  const int p0 = POOL ? 8 * bq - 1 : bq * STEM_ROWS;  // first stem row of the block
   const int tq = cdiv(Q, 16);
   const int pw = 2 * tq * 16 + 6;
   // filter: wk is [64][7][7][8]; keep channels 0..3, tap 7 zero
-  for (int i0 = threadIdx.x; i0 < 64 * 7 * 8; i0 += 8 * STEM_NT) {
+  for (int i0 = threadIdx.x; i0 < 64 * 7 * 8; i0 += 8 * NT) {
     uint2 v[8];
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
-      const int i = i0 + u * STEM_NT, k = i / 56, r = (i % 56) / 8, sp = i % 8;
+      const int i = i0 + u * NT, k = i / 56, r = (i % 56) / 8, sp = i % 8;
       v[u] = (i < 64 * 56 && sp < 7) ? *reinterpret_cast<const uint2*>(wk + ((k * 7 + r) * 7 + sp) * 8)
                                      : make_uint2(0u, 0u);
     }
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
-      const int i = i0 + u * STEM_NT;
+      const int i = i0 + u * NT;
       if (i < 64 * 56)
         *reinterpret_cast<uint2*>(wl + (i / 56) * STEM_WROW + ((i % 56) / 8) * 32 + (i % 8) * 4) = v[u];
     }
   }
-  // input rows 2 p0 - 3 .. 2 p0 + 17, columns -3 .. pw - 4 (zero outside the frame)
+  // input rows 2 p0 - 3 .. 2 p0 + 2 ROWS + 1, columns -3 .. pw - 4 (zero outside the frame)
   const long long img_n = (RAW && idx) ? idx[n] : n;
   const bf16* img = x + img_n * H * W * (RAW ? 3 : 8);
-  const int total = STEM_IN_ROWS * pw;
-  for (int i0 = threadIdx.x; i0 < total; i0 += 8 * STEM_NT) {
+  const int total = IN_ROWS * pw;
+  for (int i0 = threadIdx.x; i0 < total; i0 += 8 * NT) {
     uint2 v[8];
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
-      const int i = i0 + u * STEM_NT, pr = i / pw, pc = i % pw;
+      const int i = i0 + u * NT, pr = i / pw, pc = i % pw;
       const int h = 2 * p0 - 3 + pr, w = pc - 3;
       const bool in = i < total && (unsigned)h < (unsigned)H && (unsigned)w < (unsigned)W;
       if (RAW) {
@@ -1563,7 +1587,7 @@ __global__ __launch_bounds__(STEM_NT) void stem_kernel(const bf16* x, const int3
     }
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
-      const int i = i0 + u * STEM_NT;
+      const int i = i0 + u * NT;
       if (i < total) patch[(i / pw) * STEM_PATCH_W + i % pw] = v[u];
     }
   }
@@ -1574,14 +1598,15 @@ __global__ __launch_bounds__(STEM_NT) void stem_kernel(const bf16* x, const int3
   {
     const int lp = wave;  // output row within the block
     const int p = p0 + lp;
-    if (p >= P) return;
+    const bool row_ok = p >= 0 && p < P;
+    if (!POOL && !row_ok) return;
     f32x4 acc[4][STEM_TQ];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int t = 0; t < STEM_TQ; ++t) acc[i][t] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll 1
-    for (int r = 0; r < 7; ++r) {
+    for (int r = 0; r < (row_ok ? 7 : 0); ++r) {
       uint4 fa[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i)
@@ -1598,6 +1623,82 @@ __global__ __launch_bounds__(STEM_NT) void stem_kernel(const bf16* x, const int3
       }
     }
     const int lg = lane >> 4;
+    if constexpr (POOL) {
+      __syncthreads();  // the staged input is dead: LDS now takes the pooled rows
+      bf16* prow = reinterpret_cast<bf16*>(lds) + lp * (SP_QMAX * 64);
+      float prev[4][4];  // epilogue values of column block t - 1
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) prev[i][e] = -INFINITY;
+#pragma unroll
+      for (int t = 0; t < STEM_TQ; ++t) {
+        if (!row_ok || t >= tq) continue;  // wave-uniform
+        const int q = t * 16 + lr;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int k = i * 16 + 4 * lg;
+          float v[4] = {acc[i][t][0], acc[i][t][1], acc[i][t][2], acc[i][t][3]};
+          if (epi.scale) {
+            const float4 s4 = *reinterpret_cast<const float4*>(epi.scale + k);
+            v[0] *= s4.x; v[1] *= s4.y; v[2] *= s4.z; v[3] *= s4.w;
+          }
+          if (epi.shift) {
+            const float4 b4 = *reinterpret_cast<const float4*>(epi.shift + k);
+            v[0] += b4.x; v[1] += b4.y; v[2] += b4.z; v[3] += b4.w;
+          }
+          if (epi.relu) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[e] = relu_nan(v[e]);
+          }
+          float m[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            // every lane evaluates all three rotations, then selects
+            const float lsame = row_ror<1>(v[e]), lprev = row_ror<1>(prev[i][e]);
+            const float right = row_ror<15>(v[e]);
+            const float left = lr == 0 ? lprev : lsame;
+            float b = gt_max(-INFINITY, v[e]);
+            if (q >= 1) b = gt_max(b, left);
+            if (q + 1 < Q) b = gt_max(b, right);
+            m[e] = b;
+            prev[i][e] = v[e];
+          }
+          if ((lr & 1) == 0 && q < Q) store4<bf16>(prow + (q >> 1) * 64 + k, m);
+        }
+      }
+      __syncthreads();
+      // pool row 4 bq + m0 = max over stem rows p0 + 2 m0 .. + 2 (local rows)
+      const int units = 4 * PQ * 8;
+      for (int u = threadIdx.x; u < units; u += NT) {
+        const int m0 = u / (PQ * 8), rem = u % (PQ * 8), c = rem / 8, cu = rem % 8;
+        const int pr = 4 * bq + m0;
+        if (pr >= PP) continue;
+        float best[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) best[e] = -INFINITY;
+#pragma unroll
+        for (int d = 0; d < 3; ++d) {
+          const int lrow = 2 * m0 + d, sp = p0 + lrow;
+          if (sp < 0 || sp >= P) continue;
+          const uint4 w4 = *reinterpret_cast<const uint4*>(reinterpret_cast<const bf16*>(lds) +
+                                                           (lrow * SP_QMAX + c) * 64 + cu * 8);
+          float f0[4], f1[4];
+          unpack4(make_uint2(w4.x, w4.y), f0);
+          unpack4(make_uint2(w4.z, w4.w), f1);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            best[e] = gt_max(best[e], f0[e]);
+            best[4 + e] = gt_max(best[4 + e], f1[e]);
+          }
+        }
+        bf16* dst = y + (((long long)n * PP + pr) * PQ + c) * 64 + cu * 8;
+        float lo4[4] = {best[0], best[1], best[2], best[3]}, hi4[4] = {best[4], best[5], best[6], best[7]};
+        store4<bf16>(dst, lo4);
+        store4<bf16>(dst + 4, hi4);
+      }
+      return;
+    }
 #pragma unroll
     for (int t = 0; t < STEM_TQ; ++t) {
       const int q = t * 16 + lr;
@@ -2170,6 +2271,41 @@ size_t conv_wgrad_workspace_floats(int dt, const ConvGeom& g) {
   }
   const WPlan p = plan_wgrad(dt, g);
   return (size_t)p.splits * g.K * g.R * g.S * g.C;
+}
+
+bool stem_pool_ok(int dt, const ConvGeom& g) {
+  return dt == DT_BF16 && g.C == 8 && (g.C0 == 0 || g.C0 == 3) && g.K == 64 && g.R == 7 &&
+         g.S == 7 && g.stride == 2 && g.pad == 3 && g.Q <= STEM_QMAX && g.Q >= 1 && g.P >= 1;
+}
+
+hipError_t stem_pool_fwd(int dt, const ConvGeom& g, const void* x, bool raw, const int32_t* idx,
+                         const void* w, void* y, const ConvEpilogue& epi, hipStream_t stream) {
+  if (!stem_pool_ok(dt, g)) return hipErrorInvalidValue;
+  if (g.N == 0) return hipSuccess;
+  const int PP = (g.P - 1) / 2 + 1;
+  const Cost cost = conv_cost(g, 3, sizeof(bf16), false);
+  KernelTimer* t = t_timer;
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  if (t) {
+    e0 = t->take();
+    e1 = t->take();
+    EKYA_HIP(hipEventRecord(e0, stream));
+  }
+  const dim3 grid(g.N * cdiv(PP, 4)), block(STEM_NT + 64);
+  if (raw)
+    hipLaunchKernelGGL((stem_kernel<true, true>), grid, block, 0, stream, (const bf16*)x, idx,
+                       (const bf16*)w, (bf16*)y, epi, g.N, g.H, g.W, g.P, g.Q);
+  else
+    hipLaunchKernelGGL((stem_kernel<false, true>), grid, block, 0, stream, (const bf16*)x,
+                       (const int32_t*)nullptr, (const bf16*)w, (bf16*)y, epi, g.N, g.H, g.W,
+                       g.P, g.Q);
+  hipError_t e = hipGetLastError();
+  if (t && e == hipSuccess) {
+    EKYA_HIP(hipEventRecord(e1, stream));
+    t->recs.push_back({raw ? "conv_fwd<bf16,stem7x7+pool,frames>" : "conv_fwd<bf16,stem7x7+pool>",
+                       cost.flops, cost.bytes, e0, e1});
+  }
+  return e;
 }
 
 bool stem_frames_ok(int dt, const ConvGeom& g) {

@@ -75,6 +75,14 @@ hipError_t conv_fwd(int dt, const ConvGeom& g, const void* x, const void* w_krsc
 // idx != null) in place of the padded input; g is the padded-input geometry
 // (C = 8).  bf16 with Q <= 112 only (stem_frames_ok).
 bool stem_frames_ok(int dt, const ConvGeom& g);
+// The stem (epilogue as given, e.g. folded BatchNorm + ReLU) followed by the
+// 3x3 / stride 2 / pad 1 max pool, in one kernel: y is [N][(P-1)/2+1][(Q-1)/2+1][64].
+// x is the padded input, or with `raw` the 3-channel frames as in
+// stem_fwd_frames.  bf16 with Q <= 112 only (stem_pool_ok).
+bool stem_pool_ok(int dt, const ConvGeom& g);
+hipError_t stem_pool_fwd(int dt, const ConvGeom& g, const void* x, bool raw, const int32_t* idx,
+                         const void* w_krsc, void* y, const ConvEpilogue& epi,
+                         hipStream_t stream);
 hipError_t stem_fwd_frames(int dt, const ConvGeom& g, const void* frames, const int32_t* idx,
                            const void* w_krsc, void* y, const ConvEpilogue& epi,
                            hipStream_t stream);

@@ -248,14 +248,20 @@ static hipError_t eval_forward(const Net& net, const Geo& g, const void* shadow,
       e.scale = fold_scale(net.conv[0].bn);
       e.shift = fold_shift(net.conv[0].bn);
       e.relu = 1;
-      if (raw)
-        EKYA_HIP(stem_fwd_frames(dt, conv_geom(net, g, 0, n), cur, raw_idx,
-                                 shadow_at(net, shadow, net.conv[0].sh_krsc), b.t1, e, st));
-      else
-        EKYA_HIP(conv_fwd(dt, conv_geom(net, g, 0, n), cur,
-                          shadow_at(net, shadow, net.conv[0].sh_krsc), b.t1, e, b.ws, b.ws_floats,
-                          st));
       void* dst = (hi == 0) ? out : b.p0;
+      const ConvGeom cg = conv_geom(net, g, 0, n);
+      if (stem_pool_ok(dt, cg)) {  // stem and max pool in one kernel
+        EKYA_HIP(stem_pool_fwd(dt, cg, cur, raw, raw_idx,
+                               shadow_at(net, shadow, net.conv[0].sh_krsc), dst, e, st));
+        cur = dst;
+        continue;
+      }
+      if (raw)
+        EKYA_HIP(stem_fwd_frames(dt, cg, cur, raw_idx, shadow_at(net, shadow, net.conv[0].sh_krsc),
+                                 b.t1, e, st));
+      else
+        EKYA_HIP(conv_fwd(dt, cg, cur, shadow_at(net, shadow, net.conv[0].sh_krsc), b.t1, e, b.ws,
+                          b.ws_floats, st));
       EKYA_HIP(maxpool_fwd(dt, b.t1, n, g.sh, g.sw, 64, dst, nullptr, st));
       cur = dst;
     } else if (s <= 4) {
