@@ -358,7 +358,6 @@ struct TrainJob {
   static constexpr int kForks = 40;
   hipEvent_t fork[kForks] = {nullptr};
   hipEvent_t joined[kForks] = {nullptr};
-  hipEvent_t dgdone[kForks] = {nullptr};  // data gradient queued: its weight copy may change
   float *pooled = nullptr, *logits = nullptr, *dz = nullptr, *dpooled = nullptr;
   float* ws = nullptr;         // split-K partials
   size_t ws_floats = 0;
@@ -624,59 +623,71 @@ static hipError_t train_backward(TrainJob& j, int nb, const int32_t* fid, float*
     k.mean = bnp(j.bn_mean, net.bn[bni]);
     return k;
   };
-  // Weight gradients go to st2 after a fork event on st; st records no
-  // dependency on them until it reuses a dz buffer (two blocks later) or
-  // reaches the end of the backward pass.  A fused convolution leaves its
-  // gradient as split partials in ws2, and its momentum step (which rewrites
-  // the weight copy its data gradient reads) follows on st2 once st has
-  // queued that data gradient (wgrad_finish after the dgrad call).
-  // A weight gradient with no data gradient after it on st (the last block,
-  // the stem) runs on st itself with st's scratch ws (`main`): st has no
-  // other work left, and it saves the cross-stream event waits.
-  int nf = 0;
+  // Weight gradients run on st2.  A fused convolution leaves its gradient as
+  // split partials in ws2; its momentum step rewrites the weight copy that
+  // the convolution's own data gradient (on st) reads, so when that data
+  // gradient comes later the step is deferred to the next fork (or the end
+  // of the pass) -- before the next weight gradient overwrites ws2.  A fork
+  // is an event recorded on st that st2 waits for; every event recorded on
+  // st costs st a bubble, so there is one fork per group of weight gradients
+  // whose inputs are ready (a block's conv2 and shortcut, then its conv1).
+  // st waits for st2 only before it reuses a dz buffer parity (two blocks
+  // later) and at the end.  A weight gradient with no data gradient after it
+  // on st (the last block, the stem) runs on st itself with st's scratch ws
+  // (`main`).  With one stream (st2 == st) the same order runs serially.
+  int nf = 0, nj = 0;
   int last_join[2] = {-1, -1};  // per buffer parity: join event of its last reader
-  int pending = -1, pending_splits = 0;
-  bool pending_main = false;
+  int deferred = -1, deferred_splits = 0;
   const bool two = j.st2 != st;
-  auto wgrad_start = [&](int ci, const void* x, const void* dy, bool main) -> hipError_t {
-    if (nf >= TrainJob::kForks) return hipErrorInvalidValue;
+  auto update = [&](int ci, const float* part, int splits, hipStream_t q) {
     const ConvL& c = net.conv[ci];
-    const ConvGeom cg = conv_geom(net, j.geo, ci, nb);
-    hipStream_t ws = main ? st : j.st2;
-    float* scratch = main ? j.ws : j.ws2;
-    if (two && !main) {
+    return conv_weight_update(dt, part, splits, c.cout, c.R * c.S, c.cin, j.master + c.off,
+                              j.mom + c.off, j.lr, j.mu, shadow_at(net, j.shadow, c.sh_krsc),
+                              shadow_at(net, j.shadow, c.sh_crsk), q);
+  };
+  // st2 waits for everything queued on st so far (the forward pass uses the
+  // top half of the event arrays); a deferred momentum step follows on st2
+  auto fork = [&]() -> hipError_t {
+    if (two) {
+      if (nf >= TrainJob::kForks / 2) return hipErrorInvalidValue;
       EKYA_HIP(hipEventRecord(j.fork[nf], st));
       EKYA_HIP(hipStreamWaitEvent(j.st2, j.fork[nf], 0));
+      ++nf;
     }
-    pending_main = main;
-    if (fused_update(net, c)) {
-      EKYA_HIP(conv_wgrad_partials(dt, cg, x, dy, scratch, &pending_splits, ws));
-      pending = ci;
-    } else {
-      EKYA_HIP(conv_wgrad(dt, cg, x, dy, scratch, j.grad + c.off, c.cin, ws));
-      pending = -1;
+    if (deferred >= 0) {
+      EKYA_HIP(update(deferred, j.ws2, deferred_splits, j.st2));
+      deferred = -1;
     }
     return hipSuccess;
   };
-  auto wgrad_finish = [&](int ci, bool after_dgrad, int parity) -> hipError_t {
-    hipStream_t ws = pending_main ? st : j.st2;
-    if (pending == ci) {
-      const ConvL& c = net.conv[ci];
-      if (two && after_dgrad && !pending_main) {
-        EKYA_HIP(hipEventRecord(j.dgdone[nf], st));
-        EKYA_HIP(hipStreamWaitEvent(j.st2, j.dgdone[nf], 0));
+  // weight gradient of conv ci from x and dy (queued on st before the last
+  // fork unless main); dgrad_after: its data gradient is queued on st later
+  auto wgrad = [&](int ci, const void* x, const void* dy, bool main,
+                   bool dgrad_after) -> hipError_t {
+    const ConvL& c = net.conv[ci];
+    const ConvGeom cg = conv_geom(net, j.geo, ci, nb);
+    hipStream_t q = main ? st : j.st2;
+    float* scratch = main ? j.ws : j.ws2;
+    if (!main && deferred >= 0) EKYA_HIP(fork());  // ws2 still holds the deferred partials
+    if (fused_update(net, c)) {
+      int splits = 0;
+      EKYA_HIP(conv_wgrad_partials(dt, cg, x, dy, scratch, &splits, q));
+      if (!main && dgrad_after) {
+        deferred = ci;
+        deferred_splits = splits;
+      } else {
+        EKYA_HIP(update(ci, scratch, splits, q));
       }
-      EKYA_HIP(conv_weight_update(dt, pending_main ? j.ws : j.ws2, pending_splits, c.cout,
-                                  c.R * c.S, c.cin, j.master + c.off, j.mom + c.off, j.lr, j.mu,
-                                  shadow_at(net, j.shadow, c.sh_krsc),
-                                  shadow_at(net, j.shadow, c.sh_crsk), ws));
-      pending = -1;
+    } else {
+      EKYA_HIP(conv_wgrad(dt, cg, x, dy, scratch, j.grad + c.off, c.cin, q));
     }
-    if (two && !pending_main) {
-      EKYA_HIP(hipEventRecord(j.joined[nf], j.st2));
-      last_join[parity] = nf;
-    }
-    ++nf;
+    return hipSuccess;
+  };
+  auto join = [&](int parity) -> hipError_t {  // st2 has queued every reader of this parity
+    if (!two) return hipSuccess;
+    if (nj >= TrainJob::kForks / 2) return hipErrorInvalidValue;
+    EKYA_HIP(hipEventRecord(j.joined[nj], j.st2));
+    last_join[parity] = nj++;
     return hipSuccess;
   };
   auto reuse = [&](int parity) -> hipError_t {  // st may overwrite this parity's dz buffers
@@ -700,8 +711,7 @@ static hipError_t train_backward(TrainJob& j, int nb, const int32_t* fid, float*
       EKYA_HIP(maxpool_bwd(dt, dout, j.stem_arg, nb, j.geo.sh, j.geo.sw, 64, gA, st));
       const long long M = (long long)nb * j.geo.sh * j.geo.sw;
       EKYA_HIP(bn_bwd(net.conv[0].bn, gA, j.stem_A, j.stem_Z, M, j.gz1[par], nullptr, 0));
-      EKYA_HIP(wgrad_start(0, j.x0, j.gz1[par], true));
-      EKYA_HIP(wgrad_finish(0, false, par));
+      EKYA_HIP(wgrad(0, j.x0, j.gz1[par], true, false));
       break;
     }
     int first_bi = -1;
@@ -719,24 +729,23 @@ static hipError_t train_backward(TrainJob& j, int nb, const int32_t* fid, float*
       const bool need_dx = !(s == j.lowest && bi == first_bi);
       ConvGeom g1 = conv_geom(net, j.geo, b.c1, nb);
       const long long M = (long long)nb * g1.P * g1.Q;
-      // g = dOut * [OUT > 0]; BN2 backward
+      // g = dOut * [OUT > 0]; BN2 backward (and the shortcut's BN backward)
       EKYA_HIP(bn_bwd(net.conv[b.c2].bn, dout, t.OUT, t.Z2, M, gZ2, gG, dout_ready));
       dout_ready = 0;
+      if (b.cd >= 0) EKYA_HIP(bn_bwd(net.conv[b.cd].bn, gG, nullptr, t.Zd, M, gZd, nullptr, 0));
+      // After each fork the data-gradient work is queued on st before the
+      // weight-gradient work on st2, so the critical chain is dispatched first.
+      EKYA_HIP(fork());
       const void* dx_sc = gG;
-      if (b.cd >= 0) {
-        EKYA_HIP(bn_bwd(net.conv[b.cd].bn, gG, nullptr, t.Zd, M, gZd, nullptr, 0));
-        EKYA_HIP(wgrad_start(b.cd, t.X, gZd, false));
-        if (need_dx) EKYA_HIP(dgrad(b.cd, gZd, dnext, nullptr, nb, nullptr));
-        EKYA_HIP(wgrad_finish(b.cd, need_dx, par));
-        dx_sc = dnext;
-      }
-      EKYA_HIP(wgrad_start(b.c2, t.A1, gZ2, false));
+      if (b.cd >= 0 && need_dx) EKYA_HIP(dgrad(b.cd, gZd, dnext, nullptr, nb, nullptr));
+      if (b.cd >= 0) dx_sc = dnext;
       BnStatsSink sk1 = sink_for(net.conv[b.c1].bn, t.A1, t.Z1);
       EKYA_HIP(dgrad(b.c2, gZ2, gA, nullptr, nb, &sk1));
-      EKYA_HIP(wgrad_finish(b.c2, true, par));
+      if (b.cd >= 0) EKYA_HIP(wgrad(b.cd, t.X, gZd, false, need_dx));
+      EKYA_HIP(wgrad(b.c2, t.A1, gZ2, false, true));
       EKYA_HIP(bn_bwd(net.conv[b.c1].bn, gA, t.A1, t.Z1, M, gZ1, nullptr, sk1.done ? sk1.rows : 0));
-      EKYA_HIP(wgrad_start(b.c1, t.X, gZ1, !need_dx));
       if (need_dx) {
+        EKYA_HIP(fork());
         // dOut of the block processed next (bi - 1): its conv2 BatchNorm's statistics
         BnStatsSink skn;
         BnStatsSink* psk = nullptr;
@@ -748,13 +757,20 @@ static hipError_t train_backward(TrainJob& j, int nb, const int32_t* fid, float*
         EKYA_HIP(dgrad(b.c1, gZ1, dnext, dx_sc, nb, psk));
         dout_ready = (psk && psk->done) ? psk->rows : 0;
       }
-      EKYA_HIP(wgrad_finish(b.c1, need_dx, par));
+      EKYA_HIP(wgrad(b.c1, t.X, gZ1, !need_dx, need_dx));
+      EKYA_HIP(join(par));
       if (need_dx) std::swap(dout, dnext);
     }
   }
-  // every weight gradient must be complete before the optimizer step
-  EKYA_HIP(reuse(0));
-  EKYA_HIP(reuse(1));
+  // every weight gradient must be complete before the optimizer step: st
+  // waits for all of st2's work, then runs a still-deferred momentum step
+  if (two) {
+    if (nj >= TrainJob::kForks / 2) return hipErrorInvalidValue;
+    EKYA_HIP(hipEventRecord(j.joined[nj], j.st2));
+    EKYA_HIP(hipStreamWaitEvent(st, j.joined[nj], 0));
+    ++nj;
+  }
+  if (deferred >= 0) EKYA_HIP(update(deferred, j.ws2, deferred_splits, st));
   return hipSuccess;
 }
 
@@ -904,7 +920,6 @@ static hipError_t create_events(TrainJob& j) {
   for (int i = 0; i < TrainJob::kForks; ++i) {
     EKYA_HIP(hipEventCreateWithFlags(&j.fork[i], hipEventDisableTiming));
     EKYA_HIP(hipEventCreateWithFlags(&j.joined[i], hipEventDisableTiming));
-    EKYA_HIP(hipEventCreateWithFlags(&j.dgdone[i], hipEventDisableTiming));
   }
   return hipSuccess;
 }
@@ -917,8 +932,7 @@ static void destroy_events(TrainJob& j) {
   for (int i = 0; i < TrainJob::kForks; ++i) {
     if (j.fork[i]) (void)hipEventDestroy(j.fork[i]);
     if (j.joined[i]) (void)hipEventDestroy(j.joined[i]);
-    if (j.dgdone[i]) (void)hipEventDestroy(j.dgdone[i]);
-    j.fork[i] = j.joined[i] = j.dgdone[i] = nullptr;
+    j.fork[i] = j.joined[i] = nullptr;
   }
 }
 
