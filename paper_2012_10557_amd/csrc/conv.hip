@@ -1612,13 +1612,18 @@ __global__ __launch_bounds__(STEM_NT + (POOL ? 64 : 0)) void stem_kernel(
       for (int i = 0; i < 4; ++i)
         fa[i] = *reinterpret_cast<const uint4*>(wl + (i * 16 + lr) * STEM_WROW + r * 32 + kc * 8);
       const uint2* prow = patch + (2 * lp + r) * STEM_PATCH_W;
+      // output column q = 16 t + lr reads input columns 2 q - 3 + 2 kc, +1; all
+      // seven fragments are read first (in bounds of the staged row for every
+      // t) so the LDS latency is paid once per filter row
+      uint4 fb[STEM_TQ];
+#pragma unroll
+      for (int t = 0; t < STEM_TQ; ++t)
+        fb[t] = *reinterpret_cast<const uint4*>(prow + 2 * (t * 16 + lr) + 2 * kc);
 #pragma unroll
       for (int t = 0; t < STEM_TQ; ++t) {
         if (t < tq) {
-          // output column q = 16 t + lr reads input columns 2 q - 3 + 2 kc, +1
-          const uint4 fb = *reinterpret_cast<const uint4*>(prow + 2 * (t * 16 + lr) + 2 * kc);
 #pragma unroll
-          for (int i = 0; i < 4; ++i) mma_unit(acc[i][t], fa[i], fb, (bf16*)nullptr);
+          for (int i = 0; i < 4; ++i) mma_unit(acc[i][t], fa[i], fb[t], (bf16*)nullptr);
         }
       }
     }
