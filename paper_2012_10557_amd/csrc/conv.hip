@@ -2135,7 +2135,7 @@ hipEvent_t KernelTimer::take() {
     return e;
   }
   hipEvent_t e = nullptr;
-  (void)hipEventCreate(&e);
+  (void)hipEventCreateWithFlags(&e, hipEventDisableSystemFence);  // device-local timing only
   return e;
 }
 void set_thread_timer(KernelTimer* t) { t_timer = t; }

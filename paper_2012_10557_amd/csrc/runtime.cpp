@@ -915,11 +915,16 @@ static hipError_t job_collect(TrainJob& j, JobResult& r) {
   return hipSuccess;
 }
 
+// Every event here orders work between streams of this device (or times it);
+// the host reads results only after a stream synchronisation.  Without the
+// system-scope fence a recorded event costs its stream a shorter bubble.
 static hipError_t create_events(TrainJob& j) {
-  for (int e = 0; e <= j.epochs; ++e) EKYA_HIP(hipEventCreate(&j.ev[e]));
+  for (int e = 0; e <= j.epochs; ++e)
+    EKYA_HIP(hipEventCreateWithFlags(&j.ev[e], hipEventDisableSystemFence));
   for (int i = 0; i < TrainJob::kForks; ++i) {
-    EKYA_HIP(hipEventCreateWithFlags(&j.fork[i], hipEventDisableTiming));
-    EKYA_HIP(hipEventCreateWithFlags(&j.joined[i], hipEventDisableTiming));
+    EKYA_HIP(hipEventCreateWithFlags(&j.fork[i], hipEventDisableTiming | hipEventDisableSystemFence));
+    EKYA_HIP(
+        hipEventCreateWithFlags(&j.joined[i], hipEventDisableTiming | hipEventDisableSystemFence));
   }
   return hipSuccess;
 }
@@ -1020,8 +1025,8 @@ ekya_status run_retrain(Ctx& c, float* weights, int k, const void* frames, const
 
   EKYA_CHECK_HIP(create_events(j));
   hipEvent_t p0 = nullptr, p1 = nullptr;
-  EKYA_CHECK_HIP(hipEventCreate(&p0));
-  EKYA_CHECK_HIP(hipEventCreate(&p1));
+  EKYA_CHECK_HIP(hipEventCreateWithFlags(&p0, hipEventDisableSystemFence));
+  EKYA_CHECK_HIP(hipEventCreateWithFlags(&p1, hipEventDisableSystemFence));
   auto run = [&]() -> hipError_t {
     EKYA_HIP(job_setup(j));
     EKYA_HIP(hipEventRecord(p0, stream));
