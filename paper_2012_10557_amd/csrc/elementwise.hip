@@ -292,21 +292,35 @@ __global__ __launch_bounds__(256) void bn_group_partial(const T* z, const T* dy,
   }
 }
 
+// Count, mean and sum of squared deviations (n, m, q) of one channel merged
+// with those of another set of rows (Chan, Golub and LeVeque's pairwise
+// update): stable in float, where the one-pass sum of squares would need
+// double.  The weight nb / (n + nb) uses the hardware reciprocal (about one
+// ulp).  A set with no rows leaves the state unchanged.
+__device__ __forceinline__ void stats_merge(float& n, float& m, float& q, float nb, float mb,
+                                            float qb) {
+  if (nb == 0.f) return;
+  const float nn = n + nb, d = mb - m, f = nb * __builtin_amdgcn_rcpf(nn);
+  m += d * f;
+  q += qb + d * d * n * f;
+  n = nn;
+}
+
 // Mean and biased variance of channel c = 64 blockIdx.y + threadIdx.x % 64
 // over M rows from forward partials (S1_k, M2_k) of chunks of `crows` rows
-// (the last one ragged), in one pass in double: S = sum S1_k and
-// Q = sum [M2_k + S1_k^2 / n_k] (the chunk's sum of squares), mean = S / M,
-// var = (Q - S^2 / M) / M.  Four slices of chunks (k = slice, slice + 4, ...)
-// are added in slice order; a slice loads GS_BATCH chunks before adding them
-// in k order, so the loads overlap.  The same in every block; true for the
-// thread (one per channel) that holds the result.
+// (the last one ragged): chunk k contributes n_k rows of mean S1_k / n_k and
+// squared deviations M2_k, merged by stats_merge.  Four slices of chunks
+// (k = slice, slice + 4, ...) are merged in k order, then the slices in
+// slice order; a slice loads GS_BATCH chunks before merging them, so the
+// loads overlap.  The same in every block; true for the thread (one per
+// channel) that holds the result.
 constexpr int GS_BATCH = 8;
 __device__ __forceinline__ bool group_stats(const float* part, int nch, int crows, long long M,
                                             int C, double& mean, double& var) {
-  __shared__ double sa[4][BN_GROUP], sb[4][BN_GROUP];
+  __shared__ float sn[4][BN_GROUP], sm[4][BN_GROUP], sq[4][BN_GROUP];
   const int lc = threadIdx.x % BN_GROUP, sl = threadIdx.x / BN_GROUP;
   const int c = blockIdx.y * BN_GROUP + lc;
-  double x = 0.0, y = 0.0;
+  float n = 0.f, m = 0.f, q = 0.f;
   for (int k0 = sl; k0 < nch; k0 += 4 * GS_BATCH) {
     float v1[GS_BATCH], v2[GS_BATCH];
 #pragma unroll
@@ -319,21 +333,20 @@ __device__ __forceinline__ bool group_stats(const float* part, int nch, int crow
     for (int u = 0; u < GS_BATCH; ++u) {
       const int k = k0 + 4 * u;
       if (k < nch) {
-        const double nk = (double)std::min<long long>(crows, M - (long long)k * crows);
-        const double s1 = (double)v1[u];
-        x += s1;
-        y += (double)v2[u] + s1 * s1 / nk;
+        const float nk = (float)std::min<long long>(crows, M - (long long)k * crows);
+        stats_merge(n, m, q, nk, v1[u] * __builtin_amdgcn_rcpf(nk), v2[u]);
       }
     }
   }
-  sa[sl][lc] = x;
-  sb[sl][lc] = y;
+  sn[sl][lc] = n;
+  sm[sl][lc] = m;
+  sq[sl][lc] = q;
   __syncthreads();
   if (sl != 0) return false;
-  const double S = ((sa[0][lc] + sa[1][lc]) + sa[2][lc]) + sa[3][lc];
-  const double Q = ((sb[0][lc] + sb[1][lc]) + sb[2][lc]) + sb[3][lc];
-  mean = S / (double)M;
-  var = std::max(0.0, (Q - S * mean) / (double)M);
+#pragma unroll
+  for (int k = 1; k < 4; ++k) stats_merge(n, m, q, sn[k][lc], sm[k][lc], sq[k][lc]);
+  mean = (double)m;
+  var = M > 0 ? std::max(0.0, (double)q / (double)M) : 0.0;
   return true;
 }
 
