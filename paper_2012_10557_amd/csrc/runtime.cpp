@@ -631,8 +631,10 @@ static hipError_t train_backward(TrainJob& j, int nb, const int32_t* fid, float*
   // is an event recorded on st that st2 waits for; every event recorded on
   // st costs st a bubble, so there is one fork per group of weight gradients
   // whose inputs are ready (a block's conv2 and shortcut, then its conv1).
-  // st waits for st2 only before it reuses a dz buffer parity (two blocks
-  // later) and at the end.  A weight gradient with no data gradient after it
+  // The lowest block (no data gradient of its input) forks once more after
+  // its conv2 data gradient, so that conv2's momentum step overlaps the end
+  // of the pass.  st waits for st2 only before it reuses a dz buffer parity
+  // (two blocks later) and at the end.  A weight gradient with no data gradient after it
   // on st (the last block, the stem) runs on st itself with st's scratch ws
   // (`main`).  With one stream (st2 == st) the same order runs serially.
   int nf = 0, nj = 0;
@@ -756,6 +758,10 @@ static hipError_t train_backward(TrainJob& j, int nb, const int32_t* fid, float*
         }
         EKYA_HIP(dgrad(b.c1, gZ1, dnext, dx_sc, nb, psk));
         dout_ready = (psk && psk->done) ? psk->rows : 0;
+      } else if (deferred >= 0) {
+        // no later work on st reads the conv2 weights: the deferred momentum
+        // step runs on st2 beside this block's remaining work on st
+        EKYA_HIP(fork());
       }
       EKYA_HIP(wgrad(b.c1, t.X, gZ1, !need_dx, need_dx));
       EKYA_HIP(join(par));
