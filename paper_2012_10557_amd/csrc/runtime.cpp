@@ -358,6 +358,9 @@ struct TrainJob {
   static constexpr int kForks = 40;
   hipEvent_t fork[kForks] = {nullptr};
   hipEvent_t joined[kForks] = {nullptr};
+  // joined[] index of the end-of-backward join that st has not waited for
+  // yet (-1: none); see settle()
+  int pending_join = -1;
   float *pooled = nullptr, *logits = nullptr, *dz = nullptr, *dpooled = nullptr;
   float* ws = nullptr;         // split-K partials
   size_t ws_floats = 0;
@@ -664,6 +667,7 @@ static hipError_t train_backward(TrainJob& j, int nb, const int32_t* fid, float*
   };
   // weight gradient of conv ci from x and dy (queued on st before the last
   // fork unless main); dgrad_after: its data gradient is queued on st later
+  bool st2_grad = false;  // st2 wrote a weight gradient that the optimizer step reads
   auto wgrad = [&](int ci, const void* x, const void* dy, bool main,
                    bool dgrad_after) -> hipError_t {
     const ConvL& c = net.conv[ci];
@@ -682,6 +686,7 @@ static hipError_t train_backward(TrainJob& j, int nb, const int32_t* fid, float*
       }
     } else {
       EKYA_HIP(conv_wgrad(dt, cg, x, dy, scratch, j.grad + c.off, c.cin, q));
+      if (!main && two) st2_grad = true;
     }
     return hipSuccess;
   };
@@ -768,15 +773,28 @@ static hipError_t train_backward(TrainJob& j, int nb, const int32_t* fid, float*
       if (need_dx) std::swap(dout, dnext);
     }
   }
-  // every weight gradient must be complete before the optimizer step: st
-  // waits for all of st2's work, then runs a still-deferred momentum step
+  // The end join.  st waits for it here when what follows on st needs st2's
+  // results (a still-deferred momentum step, or a weight gradient for the
+  // optimizer step); otherwise st runs the optimizer step of the remaining
+  // parameters first and waits in settle() before anything that reads the
+  // convolution weights or buffers st2 read.
   if (two) {
     if (nj >= TrainJob::kForks / 2) return hipErrorInvalidValue;
     EKYA_HIP(hipEventRecord(j.joined[nj], j.st2));
-    EKYA_HIP(hipStreamWaitEvent(st, j.joined[nj], 0));
+    if (deferred >= 0 || st2_grad)
+      EKYA_HIP(hipStreamWaitEvent(st, j.joined[nj], 0));
+    else
+      j.pending_join = nj;
     ++nj;
   }
   if (deferred >= 0) EKYA_HIP(update(deferred, j.ws2, deferred_splits, st));
+  return hipSuccess;
+}
+
+// st waits for the pending end-of-backward join, if any.
+static hipError_t settle(TrainJob& j) {
+  if (j.pending_join >= 0) EKYA_HIP(hipStreamWaitEvent(j.st, j.joined[j.pending_join], 0));
+  j.pending_join = -1;
   return hipSuccess;
 }
 
@@ -839,6 +857,7 @@ static hipError_t job_epochs(TrainJob& j) {
       const int nb = std::min(j.B, j.n_s - b0);
       const int32_t* ord = j.d_order + (size_t)e * j.n_s + b0;
       const int32_t* fid = j.d_fidx + (size_t)e * j.n_s + b0;
+      EKYA_HIP(settle(j));  // the gather overwrites the input st2 read
       if (j.lowest == 0)
         EKYA_HIP(frames_to_padded(j.dt, j.frames, fid, nb, j.geo.H, j.geo.W, net.conv[0].cin_pad,
                                   j.x0, j.st));
@@ -855,6 +874,7 @@ static hipError_t job_epochs(TrainJob& j) {
                                  j.shadow, j.st));
       ++step;
     }
+    EKYA_HIP(settle(j));
     // held-out accuracy in eval mode with the current running statistics
     EKYA_HIP(bn_fold(j.master, t.fold_train[j.lowest], t.n_fold_train[j.lowest], j.fold, j.st));
     for (int h0 = 0; h0 < j.n_h; h0 += j.eval_cap) {
