@@ -978,36 +978,37 @@ __global__ void fc_bwd_x_kernel(const float* dz, const float* W, int N, int I, i
 // classifier's weight and bias gradients and the average-pool backward.
 // Every block recomputes the (6-wide) softmax rows it needs from the logits,
 // so no intermediate dz array or extra launch is needed.
-template <typename T>
-__global__ __launch_bounds__(256) void head_fwd_kernel(const T* x, int HW, const float* fin,
-                                                       const float* W, const float* b, int I,
-                                                       int J, float* pooled, float* z) {
+template <typename T, int NW, int IMAX>
+__global__ __launch_bounds__(NW * 64) void head_fwd_kernel(const T* x, int HW, const float* fin,
+                                                           const float* W, const float* b, int I,
+                                                           int J, float* pooled, float* z) {
   constexpr int E = Elt<T>::E;
-  __shared__ float fl[2048];
-  __shared__ float red[4][8];
-  __shared__ float ps[4][2048];
+  __shared__ float fl[IMAX];
+  __shared__ float red[NW][8];
+  __shared__ float ps[NW][IMAX];
   const int n = blockIdx.x, t = threadIdx.x, lane = t & 63, wave = t >> 6;
   if (x) {
-    // thread: one 16-byte unit of channels x one of 4 pixel slices; slices
-    // added in order
+    // thread: one 16-byte unit of channels x one of NW pixel slices (pixels
+    // wave, wave + NW, ...), four pixels' loads in flight, added in pixel
+    // order; the slices added in order
     const int units = I / E;
-    for (int u = t % 64; u < units; u += 64) {
+    for (int u = lane; u < units; u += 64) {
       float acc[E];
 #pragma unroll
       for (int e = 0; e < E; ++e) acc[e] = 0.f;
       const T* xp = x + (long long)n * HW * I + u * E;
       int k = wave;
-      for (; k + 12 < HW; k += 16) {  // four pixels' loads in flight, added in pixel order
+      for (; k + 3 * NW < HW; k += 4 * NW) {
         float v[4][E];
 #pragma unroll
         for (int q = 0; q < 4; ++q)
-          unit_to_f<T>(*reinterpret_cast<const uint4*>(xp + (long long)(k + 4 * q) * I), v[q]);
+          unit_to_f<T>(*reinterpret_cast<const uint4*>(xp + (long long)(k + q * NW) * I), v[q]);
 #pragma unroll
         for (int q = 0; q < 4; ++q)
 #pragma unroll
           for (int e = 0; e < E; ++e) acc[e] += v[q][e];
       }
-      for (; k < HW; k += 4) {
+      for (; k < HW; k += NW) {
         float v[E];
         unit_to_f<T>(*reinterpret_cast<const uint4*>(xp + (long long)k * I), v);
 #pragma unroll
@@ -1017,20 +1018,23 @@ __global__ __launch_bounds__(256) void head_fwd_kernel(const T* x, int HW, const
       for (int e = 0; e < E; ++e) ps[wave][u * E + e] = acc[e];
     }
     __syncthreads();
-    for (int i = t; i < I; i += 256) {
-      const float v = (((ps[0][i] + ps[1][i]) + ps[2][i]) + ps[3][i]) / (float)HW;
+    for (int i = t; i < I; i += NW * 64) {
+      float v = ps[0][i];
+#pragma unroll
+      for (int w = 1; w < NW; ++w) v += ps[w][i];
+      v /= (float)HW;
       pooled[(long long)n * I + i] = v;
       fl[i] = v;
     }
   } else {
-    for (int i = t; i < I; i += 256) fl[i] = fin[(long long)n * I + i];
+    for (int i = t; i < I; i += NW * 64) fl[i] = fin[(long long)n * I + i];
   }
   __syncthreads();
   for (int j0 = 0; j0 < J; j0 += 8) {
     float s[8];
 #pragma unroll
     for (int k = 0; k < 8; ++k) s[k] = 0.f;
-    for (int i = t; i < I; i += 256) {
+    for (int i = t; i < I; i += NW * 64) {
       const float xv = fl[i];
 #pragma unroll
       for (int k = 0; k < 8; ++k)
@@ -1043,8 +1047,12 @@ __global__ __launch_bounds__(256) void head_fwd_kernel(const T* x, int HW, const
       if (lane == 0) red[wave][k] = v;
     }
     __syncthreads();
-    if (t < 8 && j0 + t < J)
-      z[(long long)n * J + j0 + t] = ((red[0][t] + red[1][t]) + (red[2][t] + red[3][t])) + b[j0 + t];
+    if (t < 8 && j0 + t < J) {
+      float v = red[0][t];
+#pragma unroll
+      for (int w = 1; w < NW; ++w) v += red[w][t];
+      z[(long long)n * J + j0 + t] = v + b[j0 + t];
+    }
     __syncthreads();
   }
 }
@@ -1684,8 +1692,12 @@ hipError_t head_forward(int dt, const void* x, int HW, const float* f, const flo
   if (I > 2048 || I % dtype_vec(dt) != 0) return hipErrorInvalidValue;
   return by_type(dt, [&](auto* tp) {
     using T = std::remove_pointer_t<decltype(tp)>;
-    hipLaunchKernelGGL(head_fwd_kernel<T>, dim3(N), dim3(256), 0, stream, (const T*)x, HW, f, W, b,
-                       I, J, pooled, z);
+    if (I <= 512)  // ResNet18's 512 features: 16 waves per sample
+      hipLaunchKernelGGL((head_fwd_kernel<T, 16, 512>), dim3(N), dim3(1024), 0, stream,
+                         (const T*)x, HW, f, W, b, I, J, pooled, z);
+    else
+      hipLaunchKernelGGL((head_fwd_kernel<T, 4, 2048>), dim3(N), dim3(256), 0, stream,
+                         (const T*)x, HW, f, W, b, I, J, pooled, z);
   });
 }
 
