@@ -65,9 +65,9 @@ def measured_traffic(kernel):
     return int(t["fetch_bytes_per_launch"] + t["write_bytes_per_launch"])
 
 
-def cpu_baseline(sample_frames=200, sample_heldout=40):
+def cpu_baseline(sample_frames=300, sample_heldout=60):
     """The oracle, as it stands, on a bounded sample of the same workload:
-    a 200-frame window at 30% (60 training frames), 40 held-out frames,
+    a 300-frame window at 30% (90 training frames), 60 held-out frames,
     k = 2, 5 epochs, batch 64, 224 px (about 10-30 s on a many-core host)."""
     import numpy as np
     from threadpoolctl import threadpool_info
