@@ -127,6 +127,29 @@ def test_batchnorm_train_forward(prec, M, C, relu):
     torch.cuda.synchronize()
 
 
+@pytest.mark.parametrize("M", [3136, 64 * 7 * 7 + 5])
+def test_batchnorm_large_mean_small_spread(M):
+    """Mean 2000x the standard deviation, fp32, a ragged last chunk: the
+    chunk statistics must be combined without cancellation (the variance
+    from sums of squares would lose every digit here)."""
+    import torch
+    C = 128
+    rs = _rng(M + 7)
+    z = rounded(40.0 + 0.02 * rs.standard_normal((M, C)), "f32")
+    g = np.ones(C, np.float32)
+    b = np.zeros(C, np.float32)
+    from paper_2012_10557_amd import binding
+    rm, rv = to_dev(np.zeros(C, np.float32)), to_dev(np.ones(C, np.float32))
+    y, mean, invstd = binding.ekya_op_batchnorm_train(to_dev(z, "f32"), to_dev(g), to_dev(b), rm, rv,
+                                                      relu=False)
+    yr, (xhat, istd, mu, var, m) = nn.batchnorm_train(z.reshape(M, 1, 1, C), g.astype(np.float64),
+                                                      b.astype(np.float64))
+    assert rel_err(as_np(mean), mu) <= 1e-6
+    assert rel_err(as_np(invstd), istd) <= 1e-3
+    assert rel_err(as_np(y), yr.reshape(M, C)) <= 1e-3
+    torch.cuda.synchronize()
+
+
 @pytest.mark.parametrize("prec", PRECS)
 @pytest.mark.parametrize("M,C", BN_CASES[:4])
 @pytest.mark.parametrize("mask", [False, True])
