@@ -1104,12 +1104,24 @@ __device__ __forceinline__ bool ce_row(const float* zr, int y, int J, int N,
 // after: the pooled-feature gradient spread over the HW pixels,
 // dout[n][p][c] = (sum_j dz_j W[j][c]) / HW, one sample and HEAD_PC pixels
 // per block.
-template <typename T>
+// BNP: the pooled-feature gradient blocks instead cover 64-row chunks x 64
+// channels of dout (rows n HW + p) and also leave the backward BatchNorm
+// partials of the block output's BatchNorm in `bp.part` (chunk k: sum g and
+// sum g (z - mean), g = dout * [ymask > 0], as bn_group_partial in 64-row
+// chunks), so that BatchNorm's backward needs no partials pass.
+struct HeadBnArgs {
+  const void* ymask;
+  const void* z;
+  const float* mean;
+  float* part;
+};
+
+template <typename T, bool BNP>
 __global__ __launch_bounds__(256) void head_bwd_kernel(const float* z, const int32_t* labels,
                                                        const int32_t* idx, int N, int J,
                                                        const float* f, const float* W, int I,
                                                        float* dW, float* db, T* dout, int HW,
-                                                       float* out) {
+                                                       float* out, HeadBnArgs bp) {
   constexpr int E = Elt<T>::E;
   const int t = threadIdx.x;
   __shared__ float rdz[256][HEAD_JMAX];
@@ -1182,6 +1194,88 @@ __global__ __launch_bounds__(256) void head_bwd_kernel(const float* z, const int
     return;
   }
   if (!dout) return;
+  if constexpr (BNP) {
+    constexpr int UG = BN_GROUP / E, RI = 256 / UG, RPT = 64 / RI;
+    const int G = I / BN_GROUP;
+    const long long Mr = (long long)N * HW;
+    const int bb = blockIdx.x - HEAD_WB, k = bb / G, cg = bb % G;
+    const long long r0 = (long long)k * 64, r1 = std::min<long long>(Mr, r0 + 64);
+    if (r0 >= Mr) return;
+    const int u = t % UG, rs = t / UG, c0 = cg * BN_GROUP + u * E;
+    const T* ymask = reinterpret_cast<const T*>(bp.ymask);
+    const T* zb = reinterpret_cast<const T*>(bp.z);
+    // the rows' ReLU mask and BatchNorm input, loaded before the softmax rows
+    uint4 ym[RPT], zr[RPT];
+#pragma unroll
+    for (int q = 0; q < RPT; ++q) {
+      const long long r = r0 + rs + (long long)RI * q;
+      if (r < r1) {
+        ym[q] = *reinterpret_cast<const uint4*>(ymask + r * I + c0);
+        zr[q] = *reinterpret_cast<const uint4*>(zb + r * I + c0);
+      }
+    }
+    const int n_lo = (int)(r0 / HW), nsm = (int)((r1 - 1) / HW) - n_lo + 1;  // <= 64 samples
+    if (t < nsm) {
+      float l;
+      int c;
+      const int n = n_lo + t;
+      ce_row(z + (long long)n * J, labels[idx ? idx[n] : n], J, N, dz, l, c);
+#pragma unroll
+      for (int j = 0; j < HEAD_JMAX; ++j) rdz[t][j] = dz[j];
+    }
+    __syncthreads();
+    __shared__ float dp[64][BN_GROUP];
+    const float inv = 1.f / (float)HW;
+    for (int i = t; i < nsm * BN_GROUP; i += 256) {
+      const int sm = i / BN_GROUP, c = i % BN_GROUP;
+      float d = 0.f;
+      for (int j = 0; j < J; ++j) d += rdz[sm][j] * W[(long long)j * I + cg * BN_GROUP + c];
+      dp[sm][c] = d * inv;
+    }
+    __syncthreads();
+    float mu[E], s1[E], s2[E];
+    chan_load<E>(bp.mean, c0, mu);
+#pragma unroll
+    for (int e = 0; e < E; ++e) s1[e] = s2[e] = 0.f;
+#pragma unroll
+    for (int q = 0; q < RPT; ++q) {
+      const long long r = r0 + rs + (long long)RI * q;
+      if (r < r1) {
+        const int sm = (int)(r / HW) - n_lo;
+        float d[E], gs[E], yv[E], zv[E];
+#pragma unroll
+        for (int e = 0; e < E; ++e) d[e] = dp[sm][u * E + e];
+        const uint4 v = f_to_unit<T>(d);
+        *reinterpret_cast<uint4*>(dout + r * I + c0) = v;
+        unit_to_f<T>(v, gs);
+        unit_to_f<T>(ym[q], yv);
+        unit_to_f<T>(zr[q], zv);
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          const float g = yv[e] > 0.f ? gs[e] : 0.f;
+          s1[e] += g;
+          s2[e] += g * (zv[e] - mu[e]);
+        }
+      }
+    }
+    __shared__ float red[2][RI][BN_GROUP];  // row slices added in slice order
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      red[0][rs][u * E + e] = s1[e];
+      red[1][rs][u * E + e] = s2[e];
+    }
+    __syncthreads();
+    if (t < BN_GROUP) {
+      float a = 0.f, b = 0.f;
+      for (int q = 0; q < RI; ++q) {
+        a += red[0][q][t];
+        b += red[1][q][t];
+      }
+      bp.part[(long long)k * 2 * I + cg * BN_GROUP + t] = a;
+      bp.part[(long long)k * 2 * I + I + cg * BN_GROUP + t] = b;
+    }
+    return;
+  }
   const int nchunk = (HW + HEAD_PC - 1) / HEAD_PC;
   const int bb = blockIdx.x - HEAD_WB, n = bb / nchunk, pc = bb % nchunk;
   if (n >= N) return;
@@ -1705,15 +1799,28 @@ bool head_backward_fused(int J, int I) { return J <= HEAD_JMAX && I <= 64 * HEAD
 
 hipError_t head_backward(int dt, const float* z, const int32_t* labels, const int32_t* idx, int N,
                          int J, const float* f, const float* W, int I, float* dW, float* db,
-                         void* dout, int HW, float* out, hipStream_t stream) {
+                         void* dout, int HW, float* out, hipStream_t stream, HeadBnSink* bn) {
+  if (bn) bn->rows = 0;
   if (!head_backward_fused(J, I) || I % dtype_vec(dt) != 0 || 256 % (I / dtype_vec(dt)) != 0)
     return hipErrorInvalidValue;
-  const int dblocks = dout ? N * cdiv(HW, HEAD_PC) : 0;
-  return by_type(dt, [&](auto* tp) {
+  const long long Mr = (long long)N * HW;
+  const bool bnp = dout && bn && bn->ymask && bn->z && bn->mean && bn->part && Mr > 0 &&
+                   bn_fold_ok(Mr, I);
+  const int dblocks =
+      !dout ? 0 : bnp ? (int)cdivl(Mr, 64) * (I / BN_GROUP) : N * cdiv(HW, HEAD_PC);
+  const HeadBnArgs ha = bnp ? HeadBnArgs{bn->ymask, bn->z, bn->mean, bn->part}
+                            : HeadBnArgs{nullptr, nullptr, nullptr, nullptr};
+  hipError_t e = by_type(dt, [&](auto* tp) {
     using T = std::remove_pointer_t<decltype(tp)>;
-    hipLaunchKernelGGL(head_bwd_kernel<T>, dim3(HEAD_WB + dblocks), dim3(256), 0, stream, z,
-                       labels, idx, N, J, f, W, I, dW, db, (T*)dout, HW, out);
+    if (bnp)
+      hipLaunchKernelGGL((head_bwd_kernel<T, true>), dim3(HEAD_WB + dblocks), dim3(256), 0, stream,
+                         z, labels, idx, N, J, f, W, I, dW, db, (T*)dout, HW, out, ha);
+    else
+      hipLaunchKernelGGL((head_bwd_kernel<T, false>), dim3(HEAD_WB + dblocks), dim3(256), 0,
+                         stream, z, labels, idx, N, J, f, W, I, dW, db, (T*)dout, HW, out, ha);
   });
+  if (e == hipSuccess && bnp) bn->rows = 64;
+  return e;
 }
 
 hipError_t count_correct(const float* z, const int32_t* labels, int N, int J, int32_t* count,

@@ -181,10 +181,22 @@ hipError_t fc_bwd(const float* dz, const float* f, const float* Wt, int N, int I
 hipError_t head_forward(int dt, const void* x, int HW, const float* f, const float* W,
                         const float* b, int N, int I, int J, float* pooled, float* z,
                         hipStream_t stream);
+// bn (with dout): the BatchNorm whose output (ReLU mask ymask, input z,
+// batch mean) dout is the gradient of; when the fused path can, the launch
+// also leaves that BatchNorm's backward chunk partials in bn->part and sets
+// bn->rows (64: pass it to bn_backward as ready_rows), else rows = 0.
+struct HeadBnSink {
+  const void* ymask = nullptr;
+  const void* z = nullptr;
+  const float* mean = nullptr;
+  float* part = nullptr;
+  int rows = 0;
+};
 bool head_backward_fused(int J, int I);
 hipError_t head_backward(int dt, const float* z, const int32_t* labels, const int32_t* idx, int N,
                          int J, const float* f, const float* W, int I, float* dW, float* db,
-                         void* dout, int HW, float* out, hipStream_t stream);
+                         void* dout, int HW, float* out, hipStream_t stream,
+                         HeadBnSink* bn = nullptr);
 // Count of rows whose argmax matches the label, accumulated into *count.
 hipError_t count_correct(const float* z, const int32_t* labels, int N, int J, int32_t* count,
                          hipStream_t stream);

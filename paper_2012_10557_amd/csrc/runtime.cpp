@@ -595,11 +595,22 @@ static hipError_t train_backward(TrainJob& j, int nb, const int32_t* fid, float*
   void* gG = j.g[3];
   void* gA = j.g[5];
   const int hw = j.geo.lh[4] * j.geo.lw[4];
+  int head_ready = 0;  // rows per chunk of the last BatchNorm's backward partials in bn_ws
   if (head_backward_fused(net.n_classes, 512)) {
     // softmax cross-entropy, classifier gradients and average-pool backward
+    // (with the backward partials of the last block's output BatchNorm)
+    HeadBnSink hb;
+    if (j.lowest < 5) {
+      const size_t lb = net.blk.size() - 1;
+      hb.ymask = j.acts[lb].OUT;
+      hb.z = j.acts[lb].Z2;
+      hb.mean = bnp(j.bn_mean, net.bn[net.conv[net.blk[lb].c2].bn]);
+      hb.part = j.bn_ws;
+    }
     EKYA_HIP(head_backward(dt, j.logits, j.labels, fid, nb, net.n_classes, f, j.master + net.fc_w,
                            512, j.grad + net.fc_w, j.grad + net.fc_b,
-                           j.lowest == 5 ? nullptr : dout, hw, ce, st));
+                           j.lowest == 5 ? nullptr : dout, hw, ce, st, &hb));
+    head_ready = hb.rows;
   } else {
     EKYA_HIP(softmax_ce(j.logits, j.labels, fid, nb, net.n_classes, j.dz, ce, st));
     EKYA_HIP(fc_bwd(j.dz, f, j.master + net.fc_w, nb, 512, net.n_classes, j.grad + net.fc_w,
@@ -708,7 +719,7 @@ static hipError_t train_backward(TrainJob& j, int nb, const int32_t* fid, float*
                       shadow_at(net, j.shadow, net.conv[ci].sh_crsk), dx, res, j.ws, j.ws_floats, st,
                       sink);
   };
-  int dout_ready = 0;  // statistics of the next block's conv2 BatchNorm are in bn_ws (chunk rows)
+  int dout_ready = head_ready;  // statistics of the next block's conv2 BatchNorm are in bn_ws (chunk rows)
   int blk_count = 0;
   for (int s = 4; s >= j.lowest; --s) {
     if (s == 0) {
