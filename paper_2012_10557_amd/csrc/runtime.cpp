@@ -487,7 +487,17 @@ static void plan_job(Arena& a, TrainJob& j) {
   j.bn_ws2 = a.take<float>(j.bn_ws_floats);
   j.ce_out = a.take<float>((size_t)j.n_steps * 3);
   j.hcount = a.take<int32_t>(j.epochs);
-  j.eval_cap = std::max(1, std::min(j.n_h, 512));
+  // Held-out chunks: at most 512 frames; when the lowest trainable stage has
+  // >= 256 channels its convolutions take 256 x 128 tiles one per CU, so a
+  // chunk is cut to the frames whose tiles fill the 256 CUs once (400 frames
+  // at 224 px would take 308 tiles: two rounds, the second one a fifth full).
+  int cap = 512;
+  if (j.lowest >= 1 && j.lowest <= 4) {
+    const long long ch = 64LL << (j.lowest - 1);
+    const long long hw = (long long)j.geo.lh[j.lowest] * j.geo.lw[j.lowest];
+    if (ch >= 256 && hw > 0) cap = (int)std::max(1LL, std::min(512LL, 256LL * 128 / (hw * (ch / 256))));
+  }
+  j.eval_cap = std::max(1, std::min(j.n_h, cap));
   plan_eval(a, net, j.geo, j.lowest, 5, j.eval_cap, j.eval);
   if (j.lowest == 0) j.eval_in = a.take_bytes((size_t)j.eval_cap * in_elems * es);
 }
@@ -818,8 +828,11 @@ static hipError_t build_cache(const Net& net, const Geo& g, const void* shadow, 
                               hipStream_t st) {
   const size_t es = dtype_size(net.dt);
   const long long fbytes = (long long)g.H * g.W * 3 * es;
-  for (int i0 = 0; i0 < n; i0 += cap) {
-    const int cnt = std::min(cap, n - i0);
+  // equal chunks of at most cap frames (600 frames: 2 x 300, not 512 + 88,
+  // whose short tail costs the big-tile convolutions a nearly empty round)
+  const int per = n > 0 ? cdiv(n, cdiv(n, cap)) : cap;
+  for (int i0 = 0; i0 < n; i0 += per) {
+    const int cnt = std::min(per, n - i0);
     const void* src = d_idx ? frames : reinterpret_cast<const char*>(frames) + i0 * fbytes;
     void* out = reinterpret_cast<char*>(cache) + (row0 + i0) * row_bytes;
     if (stem_frames_ok(net.dt, conv_geom(net, g, 0, cnt))) {  // the stem reads the frames
