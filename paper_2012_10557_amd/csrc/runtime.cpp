@@ -1340,8 +1340,9 @@ ekya_status run_infer(Ctx& c, const float* weights, const void* frames, int n, i
     EKYA_HIP(bn_fold(master, t.fold_all, t.n_fold_all, fold, stream));
     EKYA_HIP(pack_conv_weights(dt, master, t.pack_all, t.n_pack_all, shadow, stream));
     const long long fbytes = (long long)H * W * 3 * es;
-    for (int i0 = 0; i0 < n; i0 += cap) {
-      const int cnt = std::min(cap, n - i0);
+    const int per = n > 0 ? cdiv(n, cdiv(n, cap)) : cap;  // equal chunks (2000: 4 x 500)
+    for (int i0 = 0; i0 < n; i0 += per) {
+      const int cnt = std::min(per, n - i0);
       const void* src = reinterpret_cast<const char*>(frames) + i0 * fbytes;
       if (resolution == H && resolution == W && stem_frames_ok(dt, conv_geom(net, geo, 0, cnt))) {
         EKYA_HIP(eval_forward(net, geo, shadow, fold, master, 0, 5, src, cnt, eb, eb.logits,
