@@ -80,7 +80,8 @@ typedef struct {
   int n_steps;                          /* SGD steps taken */
   float heldout_acc_final;              /* held-out accuracy after the last epoch */
   float heldout_acc[EKYA_MAX_EPOCHS];   /* held-out accuracy after each epoch */
-  float epoch_seconds[EKYA_MAX_EPOCHS]; /* GPU time of each epoch (training + held-out eval) */
+  float epoch_seconds[EKYA_MAX_EPOCHS]; /* GPU time of each epoch's training steps (the held-out
+                                          evaluation after it overlaps the next epoch) */
   float epoch_loss[EKYA_MAX_EPOCHS];    /* mean training loss over the epoch's steps */
   float prefix_seconds;                 /* GPU time of the frozen-prefix cache build */
   float* step_loss;                     /* host, optional: receives per-step losses */

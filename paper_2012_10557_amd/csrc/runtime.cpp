@@ -152,6 +152,8 @@ void ctx_free(Ctx& c) {
   c.timer.pool.clear();
   for (hipStream_t s : c.streams) (void)hipStreamDestroy(s);
   c.streams.clear();
+  if (c.eval_stream) (void)hipStreamDestroy(c.eval_stream);
+  c.eval_stream = nullptr;
   if (c.infer_done) (void)hipEventDestroy(c.infer_done);
   c.infer_done = nullptr;
   c.retrain_ws.release();
@@ -352,6 +354,13 @@ struct TrainJob {
   // chain; dz of conv2 / conv1 / downsample per block parity (double
   // buffered so st2 may lag one block), st2's own split scratch, and events
   hipStream_t st2 = nullptr;
+  // retraining only: each epoch's held-out evaluation runs on st3 beside the
+  // next epoch, from snapshots of the weights it reads; fork / done events
+  hipStream_t st3 = nullptr;
+  void* shadow_snap = nullptr;
+  float* master_snap = nullptr;
+  hipEvent_t ev_eval_fork = nullptr, ev_eval_done = nullptr;
+  bool eval_pending = false;
   void* gz2[2] = {nullptr}, *gz1[2] = {nullptr}, *gzd[2] = {nullptr};
   float* ws2 = nullptr;
   size_t ws2_floats = 0;
@@ -425,6 +434,10 @@ static void plan_job(Arena& a, TrainJob& j) {
   j.mom = a.take<float>(net.total);
   (void)tb;
   j.shadow = a.take_bytes(net.shadow_elems * es);
+  if (j.st3) {
+    j.shadow_snap = a.take_bytes(net.shadow_elems * es);
+    j.master_snap = a.take<float>(net.total);
+  }
   j.bn_mean = a.take<float>(net.bn_channels);
   j.bn_invstd = a.take<float>(net.bn_channels);
   j.bn_scale = a.take<float>(net.bn_channels);
@@ -899,26 +912,49 @@ static hipError_t job_epochs(TrainJob& j) {
       ++step;
     }
     EKYA_HIP(settle(j));
+    // the previous evaluation still reads the folded BatchNorm and its buffers
+    if (j.eval_pending) EKYA_HIP(hipStreamWaitEvent(j.st, j.ev_eval_done, 0));
+    j.eval_pending = false;
     // held-out accuracy in eval mode with the current running statistics
     EKYA_HIP(bn_fold(j.master, t.fold_train[j.lowest], t.n_fold_train[j.lowest], j.fold, j.st));
+    hipStream_t qe = j.st;
+    const void* esh = j.shadow;
+    const float* ems = j.master;
+    if (j.st3 && j.n_h > 0) {  // on st3 from this epoch's weights, beside the next epoch
+      EKYA_HIP(hipMemcpyAsync(j.shadow_snap, j.shadow, net.shadow_elems * es,
+                              hipMemcpyDeviceToDevice, j.st));
+      EKYA_HIP(hipMemcpyAsync(j.master_snap, j.master, net.total * sizeof(float),
+                              hipMemcpyDeviceToDevice, j.st));
+      EKYA_HIP(hipEventRecord(j.ev_eval_fork, j.st));
+      EKYA_HIP(hipStreamWaitEvent(j.st3, j.ev_eval_fork, 0));
+      qe = j.st3;
+      esh = j.shadow_snap;
+      ems = j.master_snap;
+    }
     for (int h0 = 0; h0 < j.n_h; h0 += j.eval_cap) {
       const int cnt = std::min(j.eval_cap, j.n_h - h0);
       const void* in;
       if (j.lowest == 0) {
         EKYA_HIP(frames_to_padded(j.dt, reinterpret_cast<const char*>(j.hframes) + h0 * fbytes,
                                   nullptr, cnt, j.geo.H, j.geo.W, net.conv[0].cin_pad, j.eval_in,
-                                  j.st));
+                                  qe));
         in = j.eval_in;
       } else {
         in = reinterpret_cast<const char*>(j.hcache) + (long long)h0 * j.row_bytes;
       }
-      EKYA_HIP(eval_forward(net, j.geo, j.shadow, j.fold, j.master, j.lowest, 5, in, cnt, j.eval,
-                            j.eval.logits, j.st));
+      EKYA_HIP(eval_forward(net, j.geo, esh, j.fold, ems, j.lowest, 5, in, cnt, j.eval,
+                            j.eval.logits, qe));
       EKYA_HIP(count_correct(j.eval.logits, j.hlabels + h0, cnt, net.n_classes, j.hcount + e,
-                             j.st));
+                             qe));
+    }
+    if (qe != j.st) {
+      EKYA_HIP(hipEventRecord(j.ev_eval_done, qe));
+      j.eval_pending = true;
     }
     EKYA_HIP(hipEventRecord(j.ev[e + 1], j.st));
   }
+  if (j.eval_pending) EKYA_HIP(hipStreamWaitEvent(j.st, j.ev_eval_done, 0));
+  j.eval_pending = false;
   return hipSuccess;
 }
 
@@ -971,6 +1007,10 @@ static hipError_t job_collect(TrainJob& j, JobResult& r) {
 static hipError_t create_events(TrainJob& j) {
   for (int e = 0; e <= j.epochs; ++e)
     EKYA_HIP(hipEventCreateWithFlags(&j.ev[e], hipEventDisableSystemFence));
+  if (j.st3) {
+    EKYA_HIP(hipEventCreateWithFlags(&j.ev_eval_fork, hipEventDisableTiming | hipEventDisableSystemFence));
+    EKYA_HIP(hipEventCreateWithFlags(&j.ev_eval_done, hipEventDisableTiming | hipEventDisableSystemFence));
+  }
   for (int i = 0; i < TrainJob::kForks; ++i) {
     EKYA_HIP(hipEventCreateWithFlags(&j.fork[i], hipEventDisableTiming | hipEventDisableSystemFence));
     EKYA_HIP(
@@ -979,6 +1019,9 @@ static hipError_t create_events(TrainJob& j) {
   return hipSuccess;
 }
 static void destroy_events(TrainJob& j) {
+  if (j.ev_eval_fork) (void)hipEventDestroy(j.ev_eval_fork);
+  if (j.ev_eval_done) (void)hipEventDestroy(j.ev_eval_done);
+  j.ev_eval_fork = j.ev_eval_done = nullptr;
   for (int e = 0; e <= EKYA_MAX_EPOCHS; ++e)
     if (j.ev[e]) {
       (void)hipEventDestroy(j.ev[e]);
@@ -1033,6 +1076,10 @@ ekya_status run_retrain(Ctx& c, float* weights, int k, const void* frames, const
   }
   // per-kernel timing runs serially, so each timed kernel runs alone
   j.st2 = c.timing ? stream : c.streams[0];
+  if (!c.timing) {
+    if (!c.eval_stream) EKYA_CHECK_HIP(hipStreamCreateWithFlags(&c.eval_stream, hipStreamNonBlocking));
+    j.st3 = c.eval_stream;
+  }
   j.weights = weights;
   j.frames = frames;
   j.labels = labels;

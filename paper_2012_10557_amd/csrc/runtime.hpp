@@ -71,6 +71,7 @@ struct Ctx {
   DeviceBuf retrain_ws, infer_ws, profile_ws;
   hipEvent_t infer_done = nullptr;
   std::vector<hipStream_t> streams;  // profiler streams (default priority)
+  hipStream_t eval_stream = nullptr;  // retraining's held-out evaluation (default priority)
   bool timing = false;
   KernelTimer timer;
   std::map<std::string, KernelStat> stats;
