@@ -578,9 +578,14 @@ __device__ __forceinline__ void dma16(const void* src, uint4* lds_dst) {
 }
 
 // Barrier without __syncthreads' fence (which would wait for every
-// outstanding load); the vmcnt wait before it orders the LDS writes.
+// outstanding global load); the vmcnt wait before it orders the LDS writes.
+// The wave's own LDS reads are completed first: right after the barrier
+// another wave may refill the slot they read.  (Left to itself the compiler
+// sinks the last MFMAs of a stage, and the waits for their operands, below
+// the barrier, so a slot could be overwritten while reads of it were still in
+// flight -- harmless on an idle GPU, wrong results under contention.)
 __device__ __forceinline__ void stage_barrier() {
-  asm volatile("" ::: "memory");
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
 }
