@@ -15,8 +15,11 @@
  *    data_ptr()); pointers marked "host" are CPU memory.  The caller owns every
  *    buffer and keeps it alive until the call returns (synchronous calls) or
  *    until `stream` has been synchronised (asynchronous calls).
- *  - The library owns only the memory behind an ekya_ctx (workspace arenas,
- *    frozen-prefix feature caches, internal streams and events).
+ *  - The library owns only the memory behind an ekya_ctx: one workspace arena
+ *    (every device buffer a call needs -- activations, gradients, optimizer
+ *    state, frozen-prefix feature caches -- is planned inside it), internal
+ *    streams and events.  Calls on one context run in turn on the GPU: each
+ *    call's work is ordered after the previous call's.
  *  - Arguments are validated before any GPU work; on failure nothing is
  *    launched and the status names the problem (see ekya_last_error).
  *  - A context is used by one host thread at a time.
@@ -49,7 +52,7 @@ extern "C" {
 typedef enum {
   EKYA_OK = 0,
   EKYA_ERR_INVALID_ARG = 1, /* a pointer, size or option is out of range */
-  EKYA_ERR_NOMEM = 2,       /* device memory for the workspace could not be obtained */
+  EKYA_ERR_NOMEM = 2,       /* the workspace could not be allocated, or a fixed one is too small */
   EKYA_ERR_HIP = 3,         /* a HIP runtime call or kernel launch failed */
   EKYA_ERR_NONFINITE = 4,   /* a training loss became NaN or infinite */
   EKYA_ERR_UNSUPPORTED = 5  /* valid request this build does not implement */
@@ -80,8 +83,12 @@ typedef struct {
   int n_steps;                          /* SGD steps taken */
   float heldout_acc_final;              /* held-out accuracy after the last epoch */
   float heldout_acc[EKYA_MAX_EPOCHS];   /* held-out accuracy after each epoch */
-  float epoch_seconds[EKYA_MAX_EPOCHS]; /* GPU time of each epoch's training steps (the held-out
-                                          evaluation after it overlaps the next epoch) */
+  float epoch_seconds[EKYA_MAX_EPOCHS]; /* GPU time of each epoch's training steps, from the
+                                          epoch's first step to the end of its last (both the
+                                          data- and the weight-gradient streams) */
+  float eval_seconds[EKYA_MAX_EPOCHS];  /* GPU time of the held-out evaluation after each epoch
+                                          (it runs on its own stream beside the next epoch's
+                                          steps, so the two overlap) */
   float epoch_loss[EKYA_MAX_EPOCHS];    /* mean training loss over the epoch's steps */
   float prefix_seconds;                 /* GPU time of the frozen-prefix cache build */
   float* step_loss;                     /* host, optional: receives per-step losses */
@@ -103,7 +110,10 @@ typedef struct {
   int status;                           /* ekya_status of this candidate */
   int n_train;
   float heldout_acc[EKYA_MAX_EPOCHS];   /* accuracy after each epoch */
-  float epoch_seconds[EKYA_MAX_EPOCHS]; /* GPU time of each epoch */
+  float epoch_seconds[EKYA_MAX_EPOCHS]; /* GPU time of each epoch's training steps (as in
+                                          ekya_retrain_result) */
+  float eval_seconds[EKYA_MAX_EPOCHS];  /* GPU time of the held-out evaluation after each epoch
+                                          (on the candidate's own stream, after the steps) */
   float epoch_loss[EKYA_MAX_EPOCHS];    /* mean training loss over the epoch's steps */
   float heldout_acc_final;
 } ekya_profile_result;
@@ -111,8 +121,18 @@ typedef struct {
 /* ------------------------------------------------------------ context */
 
 /* Create a context on HIP device `hip_device` for a ResNet18 with
- * `n_classes` (1 .. 1024) outputs.  *out is set on success. */
-ekya_status ekya_create(ekya_ctx** out, int hip_device, int n_classes);
+ * `n_classes` (1 .. 1024) outputs.  *out is set on success.
+ *  workspace_bytes > 0: the context allocates one device arena of exactly
+ *    that size here and never allocates device memory afterwards; a call
+ *    whose buffers do not fit returns EKYA_ERR_NOMEM before queueing any GPU
+ *    work (size it with ekya_*_workspace below).
+ *  workspace_bytes == 0: the arena is sized by the calls themselves; a call
+ *    that needs more than the arena holds waits (on the host) for the
+ *    context's previous call to finish and replaces the arena before it
+ *    queues any work -- releasing device memory may wait for the whole
+ *    device, so concurrent work elsewhere on the GPU is delayed once.
+ * EKYA_ERR_NOMEM if the arena cannot be allocated. */
+ekya_status ekya_create(ekya_ctx** out, int hip_device, int n_classes, size_t workspace_bytes);
 /* Release everything the context owns (synchronises its streams first). */
 void ekya_destroy(ekya_ctx* ctx);
 /* Length in floats of the canonical weight array for `n_classes`. */
@@ -120,6 +140,18 @@ size_t ekya_weights_count(int n_classes);
 const char* ekya_status_str(ekya_status s);
 /* Message of the last failure on this context ("" if none). */
 const char* ekya_last_error(const ekya_ctx* ctx);
+
+/* Workspace bytes (for ekya_create) that one call with these arguments
+ * plans; host-only computations that need no GPU.  0 if an argument is
+ * invalid (the matching call would return EKYA_ERR_INVALID_ARG).  The
+ * arena is reused call after call, so a context serving several kinds of
+ * call needs the largest of their sizes.  Inference needs the same
+ * workspace for any number of frames. */
+size_t ekya_retrain_workspace(int n_classes, int k_trainable, int n_frames, int H, int W,
+                              int n_heldout, const ekya_train_opts* opts);
+size_t ekya_profile_workspace(int n_classes, const ekya_profile_cfg* cfgs, int n_cfgs,
+                              int n_frames, int H, int W, int n_heldout, int precision);
+size_t ekya_infer_workspace(int n_classes, int resolution, int precision);
 
 /* ------------------------------------------------------------ retrain
  * Retrain the last k_trainable stages (sections 3.1 and 4.3).

@@ -44,6 +44,7 @@ class RetrainResult(ctypes.Structure):
                 ("heldout_acc_final", ctypes.c_float),
                 ("heldout_acc", ctypes.c_float * EKYA_MAX_EPOCHS),
                 ("epoch_seconds", ctypes.c_float * EKYA_MAX_EPOCHS),
+                ("eval_seconds", ctypes.c_float * EKYA_MAX_EPOCHS),
                 ("epoch_loss", ctypes.c_float * EKYA_MAX_EPOCHS),
                 ("prefix_seconds", ctypes.c_float),
                 ("step_loss", ctypes.POINTER(ctypes.c_float)),
@@ -60,6 +61,7 @@ class ProfileResult(ctypes.Structure):
     _fields_ = [("status", ctypes.c_int), ("n_train", ctypes.c_int),
                 ("heldout_acc", ctypes.c_float * EKYA_MAX_EPOCHS),
                 ("epoch_seconds", ctypes.c_float * EKYA_MAX_EPOCHS),
+                ("eval_seconds", ctypes.c_float * EKYA_MAX_EPOCHS),
                 ("epoch_loss", ctypes.c_float * EKYA_MAX_EPOCHS),
                 ("heldout_acc_final", ctypes.c_float)]
 
@@ -71,11 +73,15 @@ _F = ctypes.c_float
 
 # name -> (restype, argtypes)
 _SIGS = {
-    "ekya_create": (_I, [ctypes.POINTER(_P), _I, _I]),
+    "ekya_create": (_I, [ctypes.POINTER(_P), _I, _I, ctypes.c_size_t]),
     "ekya_destroy": (None, [_P]),
     "ekya_weights_count": (ctypes.c_size_t, [_I]),
     "ekya_status_str": (ctypes.c_char_p, [_I]),
     "ekya_last_error": (ctypes.c_char_p, [_P]),
+    "ekya_retrain_workspace": (ctypes.c_size_t, [_I, _I, _I, _I, _I, _I, ctypes.POINTER(TrainOpts)]),
+    "ekya_profile_workspace": (ctypes.c_size_t, [_I, ctypes.POINTER(ProfileCfg), _I, _I, _I, _I, _I,
+                                                 _I]),
+    "ekya_infer_workspace": (ctypes.c_size_t, [_I, _I, _I]),
     "ekya_retrain": (_I, [_P, _P, _I, _P, _P, _I, _I, _I, _P, _P, _I, ctypes.POINTER(TrainOpts),
                           ctypes.POINTER(RetrainResult), _P]),
     "ekya_profile": (_I, [_P, _P, ctypes.POINTER(ProfileCfg), _I, _P, _P, _I, _I, _I, _P, _P, _I,
@@ -167,11 +173,38 @@ def _stream(stream=None):
 
 
 # ------------------------------------------------------------ context
-def ekya_create(device: int = 0, n_classes: int = 6):
+def ekya_create(device: int = 0, n_classes: int = 6, workspace_bytes: int = 0):
     lib = load()
     h = ctypes.c_void_p()
-    _check(lib.ekya_create(ctypes.byref(h), device, n_classes))
+    _check(lib.ekya_create(ctypes.byref(h), device, n_classes, workspace_bytes))
     return h
+
+
+def _profile_cfgs(cfgs: Sequence[dict]):
+    arr = (ProfileCfg * len(cfgs))()
+    for i, c in enumerate(cfgs):
+        arr[i] = ProfileCfg(c["k"], c["subsample_frac"], c["epochs"], c.get("lr", 0.01),
+                            c.get("momentum", 0.9), c.get("batch", 64), c.get("seed", 0))
+    return arr
+
+
+def ekya_retrain_workspace(n_classes: int, k_trainable: int, n_frames: int, H: int, W: int,
+                           n_heldout: int, subsample_frac: float, epochs: int, lr: float,
+                           momentum: float = 0.9, batch: int = 64, seed: int = 0,
+                           precision: int = EKYA_BF16) -> int:
+    opts = TrainOpts(subsample_frac, epochs, lr, momentum, batch, seed, precision)
+    return int(load().ekya_retrain_workspace(n_classes, k_trainable, n_frames, H, W, n_heldout,
+                                             ctypes.byref(opts)))
+
+
+def ekya_profile_workspace(n_classes: int, cfgs: Sequence[dict], n_frames: int, H: int, W: int,
+                           n_heldout: int, precision: int = EKYA_BF16) -> int:
+    return int(load().ekya_profile_workspace(n_classes, _profile_cfgs(cfgs), len(cfgs), n_frames, H,
+                                             W, n_heldout, precision))
+
+
+def ekya_infer_workspace(n_classes: int, resolution: int, precision: int = EKYA_BF16) -> int:
+    return int(load().ekya_infer_workspace(n_classes, resolution, precision))
 
 
 def ekya_destroy(ctx) -> None:
@@ -247,6 +280,7 @@ def ekya_retrain(ctx, weights, k_trainable: int, frames, labels, heldout_frames,
     out = {"n_train": res.n_train, "n_epochs": ne, "n_steps": res.n_steps,
            "heldout_acc_final": res.heldout_acc_final,
            "heldout_acc": list(res.heldout_acc[:ne]), "epoch_seconds": list(res.epoch_seconds[:ne]),
+           "eval_seconds": list(res.eval_seconds[:ne]),
            "epoch_loss": list(res.epoch_loss[:ne]), "prefix_seconds": res.prefix_seconds}
     if buf is not None:
         out["step_loss"] = list(buf[:res.n_steps])
@@ -259,10 +293,7 @@ def ekya_profile(ctx, weights, cfgs: Sequence[dict], frames, labels, heldout_fra
     lib = load()
     prec = _precision(frames)
     n, H, W, _ = frames.shape
-    arr = (ProfileCfg * len(cfgs))()
-    for i, c in enumerate(cfgs):
-        arr[i] = ProfileCfg(c["k"], c["subsample_frac"], c["epochs"], c.get("lr", 0.01),
-                            c.get("momentum", 0.9), c.get("batch", 64), c.get("seed", 0))
+    arr = _profile_cfgs(cfgs)
     res = (ProfileResult * len(cfgs))()
     st = lib.ekya_profile(ctx, _dev(weights, torch.float32), arr, len(cfgs), _dev(frames),
                           _dev(labels, torch.int32), n, H, W, _dev(heldout_frames, frames.dtype),
@@ -274,7 +305,8 @@ def ekya_profile(ctx, weights, cfgs: Sequence[dict], frames, labels, heldout_fra
         r = res[i]
         e = c["epochs"]
         out.append({"status": r.status, "n_train": r.n_train, "heldout_acc": list(r.heldout_acc[:e]),
-                    "epoch_seconds": list(r.epoch_seconds[:e]), "epoch_loss": list(r.epoch_loss[:e]),
+                    "epoch_seconds": list(r.epoch_seconds[:e]), "eval_seconds": list(r.eval_seconds[:e]),
+                    "epoch_loss": list(r.epoch_loss[:e]),
                     "heldout_acc_final": r.heldout_acc_final})
     return out
 

@@ -66,7 +66,7 @@ const char* ekya_last_error(const ekya_ctx* ctx) {
   return ctx ? ctx->c.err.c_str() : g_noctx_err.c_str();
 }
 
-ekya_status ekya_create(ekya_ctx** out, int hip_device, int n_classes) {
+ekya_status ekya_create(ekya_ctx** out, int hip_device, int n_classes, size_t workspace_bytes) {
   if (!out) return fail(nullptr, EKYA_ERR_INVALID_ARG, "out is null");
   *out = nullptr;
   if (n_classes < 1 || n_classes > 1024)
@@ -78,7 +78,7 @@ ekya_status ekya_create(ekya_ctx** out, int hip_device, int n_classes) {
     return fail(nullptr, EKYA_ERR_INVALID_ARG, "hip_device out of range");
   ekya_ctx* c = new (std::nothrow) ekya_ctx();
   if (!c) return fail(nullptr, EKYA_ERR_NOMEM, "host allocation failed");
-  hipError_t e = ekya::ctx_init(c->c, hip_device, n_classes);
+  hipError_t e = ekya::ctx_init(c->c, hip_device, n_classes, workspace_bytes);
   if (e != hipSuccess) {
     ekya::ctx_free(c->c);
     delete c;
@@ -108,13 +108,10 @@ static ekya_status check_train(ekya_ctx* ctx, int k, double frac, int epochs, fl
   return EKYA_OK;
 }
 
-ekya_status ekya_retrain(ekya_ctx* ctx, float* weights, int k_trainable, const void* frames,
-                         const int32_t* labels, int n_frames, int H, int W,
-                         const void* heldout_frames, const int32_t* heldout_labels, int n_heldout,
-                         const ekya_train_opts* opts, ekya_retrain_result* result, void* stream) {
-  if (!ctx) return fail(nullptr, EKYA_ERR_INVALID_ARG, "ctx is null");
-  if (!weights || !frames || !labels || !heldout_frames || !heldout_labels || !opts || !result)
-    return fail(ctx, EKYA_ERR_INVALID_ARG, "null pointer argument");
+// Sizes and options of a retraining call (pointers checked by the caller).
+static ekya_status check_retrain_args(ekya_ctx* ctx, int k, int n_frames, int H, int W,
+                                      int n_heldout, const ekya_train_opts* opts) {
+  if (!opts) return fail(ctx, EKYA_ERR_INVALID_ARG, "opts is null");
   if (n_frames < 1 || n_frames > (1 << 24))
     return fail(ctx, EKYA_ERR_INVALID_ARG, "n_frames must be in [1, 2^24]");
   if (n_heldout < 1 || n_heldout > (1 << 24))
@@ -122,8 +119,18 @@ ekya_status ekya_retrain(ekya_ctx* ctx, float* weights, int k_trainable, const v
   if (ekya_status s = check_frames(ctx, H, W)) return s;
   if (!valid_precision(opts->precision))
     return fail(ctx, EKYA_ERR_INVALID_ARG, "precision must be EKYA_FP32 or EKYA_BF16");
-  if (ekya_status s = check_train(ctx, k_trainable, opts->subsample_frac, opts->epochs, opts->lr,
-                                  opts->momentum, opts->batch))
+  return check_train(ctx, k, opts->subsample_frac, opts->epochs, opts->lr, opts->momentum,
+                     opts->batch);
+}
+
+ekya_status ekya_retrain(ekya_ctx* ctx, float* weights, int k_trainable, const void* frames,
+                         const int32_t* labels, int n_frames, int H, int W,
+                         const void* heldout_frames, const int32_t* heldout_labels, int n_heldout,
+                         const ekya_train_opts* opts, ekya_retrain_result* result, void* stream) {
+  if (!ctx) return fail(nullptr, EKYA_ERR_INVALID_ARG, "ctx is null");
+  if (!weights || !frames || !labels || !heldout_frames || !heldout_labels || !opts || !result)
+    return fail(ctx, EKYA_ERR_INVALID_ARG, "null pointer argument");
+  if (ekya_status s = check_retrain_args(ctx, k_trainable, n_frames, H, W, n_heldout, opts))
     return s;
   if (result->step_loss_capacity < 0 || (result->step_loss_capacity > 0 && !result->step_loss))
     return fail(ctx, EKYA_ERR_INVALID_ARG, "step_loss capacity without a buffer");
@@ -133,14 +140,19 @@ ekya_status ekya_retrain(ekya_ctx* ctx, float* weights, int k_trainable, const v
                            (hipStream_t)stream);
 }
 
-ekya_status ekya_profile(ekya_ctx* ctx, const float* weights, const ekya_profile_cfg* cfgs,
-                         int n_cfgs, const void* frames, const int32_t* labels, int n_frames,
-                         int H, int W, const void* heldout_frames, const int32_t* heldout_labels,
-                         int n_heldout, uint64_t subsample_seed, int precision, int concurrent,
-                         ekya_profile_result* results) {
-  if (!ctx) return fail(nullptr, EKYA_ERR_INVALID_ARG, "ctx is null");
-  if (!weights || !cfgs || !frames || !labels || !heldout_frames || !heldout_labels || !results)
-    return fail(ctx, EKYA_ERR_INVALID_ARG, "null pointer argument");
+size_t ekya_retrain_workspace(int n_classes, int k_trainable, int n_frames, int H, int W,
+                              int n_heldout, const ekya_train_opts* opts) {
+  if (n_classes < 1 || n_classes > 1024 ||
+      check_retrain_args(nullptr, k_trainable, n_frames, H, W, n_heldout, opts) != EKYA_OK)
+    return 0;
+  const ekya::Net net = ekya::Net::build(n_classes, opts->precision);
+  return ekya::retrain_workspace_bytes(net, k_trainable, n_frames, H, W, n_heldout, *opts);
+}
+
+// Sizes and candidates of a profiling call (pointers checked by the caller).
+static ekya_status check_profile_args(ekya_ctx* ctx, const ekya_profile_cfg* cfgs, int n_cfgs,
+                                      int n_frames, int H, int W, int n_heldout, int precision) {
+  if (!cfgs) return fail(ctx, EKYA_ERR_INVALID_ARG, "cfgs is null");
   if (n_cfgs < 1 || n_cfgs > 256) return fail(ctx, EKYA_ERR_INVALID_ARG, "n_cfgs must be in [1, 256]");
   if (n_frames < 1 || n_frames > (1 << 24))
     return fail(ctx, EKYA_ERR_INVALID_ARG, "n_frames must be in [1, 2^24]");
@@ -155,10 +167,32 @@ ekya_status ekya_profile(ekya_ctx* ctx, const float* weights, const ekya_profile
                                     c.batch))
       return s;
   }
+  return EKYA_OK;
+}
+
+ekya_status ekya_profile(ekya_ctx* ctx, const float* weights, const ekya_profile_cfg* cfgs,
+                         int n_cfgs, const void* frames, const int32_t* labels, int n_frames,
+                         int H, int W, const void* heldout_frames, const int32_t* heldout_labels,
+                         int n_heldout, uint64_t subsample_seed, int precision, int concurrent,
+                         ekya_profile_result* results) {
+  if (!ctx) return fail(nullptr, EKYA_ERR_INVALID_ARG, "ctx is null");
+  if (!weights || !cfgs || !frames || !labels || !heldout_frames || !heldout_labels || !results)
+    return fail(ctx, EKYA_ERR_INVALID_ARG, "null pointer argument");
+  if (ekya_status s = check_profile_args(ctx, cfgs, n_cfgs, n_frames, H, W, n_heldout, precision))
+    return s;
   ctx->c.err.clear();
   return ekya::run_profile(ctx->c, weights, cfgs, n_cfgs, frames, labels, n_frames, H, W,
                            heldout_frames, heldout_labels, n_heldout, subsample_seed, precision,
                            concurrent, results);
+}
+
+size_t ekya_profile_workspace(int n_classes, const ekya_profile_cfg* cfgs, int n_cfgs,
+                              int n_frames, int H, int W, int n_heldout, int precision) {
+  if (n_classes < 1 || n_classes > 1024 ||
+      check_profile_args(nullptr, cfgs, n_cfgs, n_frames, H, W, n_heldout, precision) != EKYA_OK)
+    return 0;
+  const ekya::Net net = ekya::Net::build(n_classes, precision);
+  return ekya::profile_workspace_bytes(net, cfgs, n_cfgs, n_frames, H, W, n_heldout);
 }
 
 ekya_status ekya_infer(ekya_ctx* ctx, const float* weights, const void* frames, int n, int H,
@@ -175,6 +209,14 @@ ekya_status ekya_infer(ekya_ctx* ctx, const float* weights, const void* frames, 
   ctx->c.err.clear();
   return ekya::run_infer(ctx->c, weights, frames, n, H, W, resolution, precision, labels_out,
                          (hipStream_t)stream);
+}
+
+size_t ekya_infer_workspace(int n_classes, int resolution, int precision) {
+  if (n_classes < 1 || n_classes > 1024 || resolution < 32 || resolution > 4096 ||
+      !valid_precision(precision))
+    return 0;
+  const ekya::Net net = ekya::Net::build(n_classes, precision);
+  return ekya::infer_workspace_bytes(net, resolution);
 }
 
 ekya_status ekya_set_kernel_timing(ekya_ctx* ctx, int enable) {

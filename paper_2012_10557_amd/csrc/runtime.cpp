@@ -26,23 +26,14 @@
 
 namespace ekya {
 
-hipError_t DeviceBuf::ensure(size_t bytes) {
-  if (bytes <= cap) return hipSuccess;
-  if (p) {
-    hipError_t e = hipDeviceSynchronize();
-    if (e != hipSuccess) return e;
-    e = hipFree(p);
-    if (e != hipSuccess) return e;
-    p = nullptr;
-    cap = 0;
-  }
-  size_t want = bytes + bytes / 8 + (1 << 20);
-  hipError_t e = hipMalloc(&p, want);
+hipError_t DeviceBuf::alloc(size_t bytes) {
+  release();
+  hipError_t e = hipMalloc(&p, std::max<size_t>(bytes, 256));
   if (e != hipSuccess) {
     p = nullptr;
     return e;
   }
-  cap = want;
+  cap = std::max<size_t>(bytes, 256);
   return hipSuccess;
 }
 
@@ -109,13 +100,13 @@ static hipError_t upload_tables(const Net& net, Tables& t) {
         pr.insert(pr.end(), {c.off, c.cout, c.R, c.S, c.cin, c.cin_pad, c.sh_krsc, c.sh_crsk});
     put(pr, &t.pack_rest[lo], &t.n_pack_rest[lo], 8);
   }
-  EKYA_HIP(t.buf.ensure(all.size() * sizeof(long long) + 16));
+  EKYA_HIP(t.buf.alloc(all.size() * sizeof(long long) + 16));
   EKYA_HIP(hipMemcpy(t.buf.p, all.data(), all.size() * sizeof(long long), hipMemcpyHostToDevice));
   for (auto& f : fix) *f.first = reinterpret_cast<const long long*>(t.buf.p) + f.second;
   return hipSuccess;
 }
 
-hipError_t ctx_init(Ctx& c, int device, int n_classes) {
+hipError_t ctx_init(Ctx& c, int device, int n_classes, size_t workspace_bytes) {
   c.device = device;
   c.n_classes = n_classes;
   EKYA_HIP(hipSetDevice(device));
@@ -123,8 +114,37 @@ hipError_t ctx_init(Ctx& c, int device, int n_classes) {
     c.net[dt] = Net::build(n_classes, dt);
     EKYA_HIP(upload_tables(c.net[dt], c.tabs[dt]));
   }
-  EKYA_HIP(hipEventCreateWithFlags(&c.infer_done, hipEventDisableTiming));
+  EKYA_HIP(hipEventCreateWithFlags(&c.last_done, hipEventDisableTiming));
+  if (workspace_bytes > 0) {
+    EKYA_HIP(c.ws.alloc(workspace_bytes));
+    c.fixed_ws = true;
+  }
   return hipSuccess;
+}
+
+// Give the call `need` bytes of arena and order `stream` after the
+// context's previous call.  On failure nothing has been queued.
+static ekya_status acquire_workspace(Ctx& c, size_t need, hipStream_t stream) {
+  if (need > c.ws.cap) {
+    if (c.fixed_ws) {
+      c.err = "workspace of " + std::to_string(c.ws.cap) + " bytes is too small: the call needs " +
+              std::to_string(need) + " bytes";
+      return EKYA_ERR_NOMEM;
+    }
+    // grow mode: the previous call must be done with the old arena
+    hipError_t e = hipEventSynchronize(c.last_done);
+    if (e == hipSuccess) e = c.ws.alloc(need + need / 8 + (1 << 20));
+    if (e != hipSuccess) {
+      c.err = std::string("workspace of ") + std::to_string(need) + " bytes: " + hipGetErrorString(e);
+      return e == hipErrorOutOfMemory ? EKYA_ERR_NOMEM : EKYA_ERR_HIP;
+    }
+  }
+  hipError_t e = hipStreamWaitEvent(stream, c.last_done, 0);
+  if (e != hipSuccess) {
+    c.err = std::string("HIP error: ") + hipGetErrorString(e);
+    return EKYA_ERR_HIP;
+  }
+  return EKYA_OK;
 }
 
 hipError_t ctx_collect_timing(Ctx& c) {
@@ -154,11 +174,9 @@ void ctx_free(Ctx& c) {
   c.streams.clear();
   if (c.eval_stream) (void)hipStreamDestroy(c.eval_stream);
   c.eval_stream = nullptr;
-  if (c.infer_done) (void)hipEventDestroy(c.infer_done);
-  c.infer_done = nullptr;
-  c.retrain_ws.release();
-  c.infer_ws.release();
-  c.profile_ws.release();
+  if (c.last_done) (void)hipEventDestroy(c.last_done);
+  c.last_done = nullptr;
+  c.ws.release();
   for (auto& t : c.tabs) t.buf.release();
 }
 
@@ -357,6 +375,7 @@ struct TrainJob {
   // retraining only: each epoch's held-out evaluation runs on st3 beside the
   // next epoch, from snapshots of the weights it reads; fork / done events
   hipStream_t st3 = nullptr;
+  bool eval_overlap = false;  // planned with the snapshot buffers st3 reads
   void* shadow_snap = nullptr;
   float* master_snap = nullptr;
   hipEvent_t ev_eval_fork = nullptr, ev_eval_done = nullptr;
@@ -364,7 +383,10 @@ struct TrainJob {
   void* gz2[2] = {nullptr}, *gz1[2] = {nullptr}, *gzd[2] = {nullptr};
   float* ws2 = nullptr;
   size_t ws2_floats = 0;
-  static constexpr int kForks = 40;
+  // The backward pass records at most three forks per residual block (eight
+  // blocks at full depth) plus the end join, the forward pass one per
+  // projection shortcut; each half of the arrays holds more than that.
+  static constexpr int kForks = 64;
   hipEvent_t fork[kForks] = {nullptr};
   hipEvent_t joined[kForks] = {nullptr};
   // joined[] index of the end-of-backward join that st has not waited for
@@ -381,8 +403,15 @@ struct TrainJob {
   EvalBufs eval;
   int eval_cap = 0;
   void* eval_in = nullptr;     // padded frames for held-out eval when lowest == 0
+  // ev[e]: start of epoch e on st (ev[epochs]: end of the loop); ev_tr[e]:
+  // end of epoch e's training steps (both streams); ev_e0/ev_e1[e]: around
+  // epoch e's held-out evaluation on the stream that runs it
   hipEvent_t ev[EKYA_MAX_EPOCHS + 1] = {nullptr};
+  hipEvent_t ev_tr[EKYA_MAX_EPOCHS] = {nullptr};
+  hipEvent_t ev_e0[EKYA_MAX_EPOCHS] = {nullptr}, ev_e1[EKYA_MAX_EPOCHS] = {nullptr};
 };
+
+static_assert(3 * 8 + 1 <= TrainJob::kForks / 2, "fork events for a full-depth backward pass");
 
 static size_t ws_floats(const TrainJob& j) {
   const Net& net = *j.net;
@@ -434,7 +463,7 @@ static void plan_job(Arena& a, TrainJob& j) {
   j.mom = a.take<float>(net.total);
   (void)tb;
   j.shadow = a.take_bytes(net.shadow_elems * es);
-  if (j.st3) {
+  if (j.eval_overlap) {
     j.shadow_snap = a.take_bytes(net.shadow_elems * es);
     j.master_snap = a.take<float>(net.total);
   }
@@ -912,6 +941,7 @@ static hipError_t job_epochs(TrainJob& j) {
       ++step;
     }
     EKYA_HIP(settle(j));
+    EKYA_HIP(hipEventRecord(j.ev_tr[e], j.st));
     // the previous evaluation still reads the folded BatchNorm and its buffers
     if (j.eval_pending) EKYA_HIP(hipStreamWaitEvent(j.st, j.ev_eval_done, 0));
     j.eval_pending = false;
@@ -931,6 +961,7 @@ static hipError_t job_epochs(TrainJob& j) {
       esh = j.shadow_snap;
       ems = j.master_snap;
     }
+    EKYA_HIP(hipEventRecord(j.ev_e0[e], qe));
     for (int h0 = 0; h0 < j.n_h; h0 += j.eval_cap) {
       const int cnt = std::min(j.eval_cap, j.n_h - h0);
       const void* in;
@@ -947,6 +978,7 @@ static hipError_t job_epochs(TrainJob& j) {
       EKYA_HIP(count_correct(j.eval.logits, j.hlabels + h0, cnt, net.n_classes, j.hcount + e,
                              qe));
     }
+    EKYA_HIP(hipEventRecord(j.ev_e1[e], qe));
     if (qe != j.st) {
       EKYA_HIP(hipEventRecord(j.ev_eval_done, qe));
       j.eval_pending = true;
@@ -974,7 +1006,8 @@ static void job_prepare_host(TrainJob& j, const std::vector<int32_t>& S, uint64_
 struct JobResult {
   std::vector<float> ce;       // n_steps x 3
   std::vector<int32_t> hc;     // epochs
-  std::vector<float> secs;     // epochs
+  std::vector<float> secs;     // epochs: training steps
+  std::vector<float> esecs;    // epochs: held-out evaluation
   ekya_status status = EKYA_OK;
 };
 
@@ -982,6 +1015,7 @@ static hipError_t job_collect(TrainJob& j, JobResult& r) {
   r.ce.resize((size_t)j.n_steps * 3);
   r.hc.resize(j.epochs);
   r.secs.resize(j.epochs);
+  r.esecs.resize(j.epochs);
   EKYA_HIP(hipMemcpyAsync(r.ce.data(), j.ce_out, r.ce.size() * sizeof(float), hipMemcpyDeviceToHost,
                           j.st));
   EKYA_HIP(hipMemcpyAsync(r.hc.data(), j.hcount, r.hc.size() * sizeof(int32_t),
@@ -989,8 +1023,11 @@ static hipError_t job_collect(TrainJob& j, JobResult& r) {
   EKYA_HIP(hipStreamSynchronize(j.st));
   for (int e = 0; e < j.epochs; ++e) {
     float ms = 0.f;
-    EKYA_HIP(hipEventElapsedTime(&ms, j.ev[e], j.ev[e + 1]));
+    EKYA_HIP(hipEventElapsedTime(&ms, j.ev[e], j.ev_tr[e]));
     r.secs[e] = ms * 1e-3f;
+    ms = 0.f;
+    if (j.n_h > 0) EKYA_HIP(hipEventElapsedTime(&ms, j.ev_e0[e], j.ev_e1[e]));
+    r.esecs[e] = ms * 1e-3f;
   }
   r.status = EKYA_OK;
   for (int s = 0; s < j.n_steps; ++s)
@@ -1007,6 +1044,11 @@ static hipError_t job_collect(TrainJob& j, JobResult& r) {
 static hipError_t create_events(TrainJob& j) {
   for (int e = 0; e <= j.epochs; ++e)
     EKYA_HIP(hipEventCreateWithFlags(&j.ev[e], hipEventDisableSystemFence));
+  for (int e = 0; e < j.epochs; ++e) {
+    EKYA_HIP(hipEventCreateWithFlags(&j.ev_tr[e], hipEventDisableSystemFence));
+    EKYA_HIP(hipEventCreateWithFlags(&j.ev_e0[e], hipEventDisableSystemFence));
+    EKYA_HIP(hipEventCreateWithFlags(&j.ev_e1[e], hipEventDisableSystemFence));
+  }
   if (j.st3) {
     EKYA_HIP(hipEventCreateWithFlags(&j.ev_eval_fork, hipEventDisableTiming | hipEventDisableSystemFence));
     EKYA_HIP(hipEventCreateWithFlags(&j.ev_eval_done, hipEventDisableTiming | hipEventDisableSystemFence));
@@ -1027,6 +1069,12 @@ static void destroy_events(TrainJob& j) {
       (void)hipEventDestroy(j.ev[e]);
       j.ev[e] = nullptr;
     }
+  for (hipEvent_t* a : {j.ev_tr, j.ev_e0, j.ev_e1})
+    for (int e = 0; e < EKYA_MAX_EPOCHS; ++e)
+      if (a[e]) {
+        (void)hipEventDestroy(a[e]);
+        a[e] = nullptr;
+      }
   for (int i = 0; i < TrainJob::kForks; ++i) {
     if (j.fork[i]) (void)hipEventDestroy(j.fork[i]);
     if (j.joined[i]) (void)hipEventDestroy(j.joined[i]);
@@ -1049,6 +1097,60 @@ struct TimerGuard {
   ~TimerGuard() { set_thread_timer(nullptr); }
 };
 
+// Retraining job shape from the call's arguments (host only).
+static void config_retrain(TrainJob& j, const Net& net, int k, int n_frames, int H, int W,
+                           int n_heldout, const ekya_train_opts& o, bool eval_overlap) {
+  j.net = &net;
+  j.geo = Geo::build(net, H, W);
+  j.dt = o.precision;
+  j.k = k;
+  j.lowest = 6 - k;
+  j.B = o.batch;
+  j.epochs = o.epochs;
+  j.lr = o.lr;
+  j.mu = o.momentum;
+  j.n_h = n_heldout;
+  j.n_s = subset_count(n_frames, o.subsample_frac);
+  j.n_steps = j.epochs * cdiv(j.n_s, j.B);
+  j.eval_overlap = eval_overlap;
+  const long long feat = j.geo.stage_in_elems(net, j.lowest);
+  j.row_bytes = feat * ((j.lowest == 5) ? 4 : (long long)dtype_size(j.dt));
+}
+
+// Frames per chunk of a frozen-prefix cache build.
+static constexpr int kCacheChunk = 512;
+
+struct RetrainBufs {
+  void* cache = nullptr;  // training rows, then held-out rows
+  int32_t* d_S = nullptr;
+  void* padded = nullptr;
+  EvalBufs ceb;
+};
+
+// Job buffers, the feature cache and its build scratch.
+static void plan_retrain(Arena& a, TrainJob& j, RetrainBufs& r) {
+  const Net& net = *j.net;
+  plan_job(a, j);
+  r = RetrainBufs();
+  if (j.lowest >= 1) {
+    r.cache = a.take_bytes((size_t)(j.n_s + j.n_h) * j.row_bytes);
+    r.d_S = a.take<int32_t>(j.n_s);
+    r.padded = a.take_bytes((size_t)kCacheChunk * j.geo.H * j.geo.W * net.conv[0].cin_pad *
+                            dtype_size(j.dt));
+    plan_eval(a, net, j.geo, 0, j.lowest - 1, kCacheChunk, r.ceb);
+  }
+}
+
+size_t retrain_workspace_bytes(const Net& net, int k, int n_frames, int H, int W, int n_heldout,
+                               const ekya_train_opts& o) {
+  TrainJob j;
+  config_retrain(j, net, k, n_frames, H, W, n_heldout, o, true);
+  RetrainBufs r;
+  Arena a;
+  plan_retrain(a, j, r);
+  return a.used;
+}
+
 ekya_status run_retrain(Ctx& c, float* weights, int k, const void* frames, const int32_t* labels,
                         int n_frames, int H, int W, const void* hframes, const int32_t* hlabels,
                         int n_heldout, const ekya_train_opts& o, ekya_retrain_result* res,
@@ -1056,27 +1158,27 @@ ekya_status run_retrain(Ctx& c, float* weights, int k, const void* frames, const
   EKYA_CHECK_HIP(hipSetDevice(c.device));
   TimerGuard tg(c);
   const int dt = o.precision;
+  const Net& net = c.net[dt];
   TrainJob j;
-  j.net = &c.net[dt];
+  // per-kernel timing runs serially, so each timed kernel runs alone; otherwise
+  // each epoch's held-out evaluation overlaps the next epoch on st3
+  config_retrain(j, net, k, n_frames, H, W, n_heldout, o, !c.timing);
+  RetrainBufs rb;
+  {
+    Arena meas;
+    plan_retrain(meas, j, rb);
+    if (ekya_status s = acquire_workspace(c, meas.used, stream)) return s;
+  }
   j.tabs = &c.tabs[dt];
-  j.geo = Geo::build(*j.net, H, W);
-  j.dt = dt;
-  j.k = k;
-  j.lowest = 6 - k;
-  j.B = o.batch;
-  j.epochs = o.epochs;
-  j.lr = o.lr;
-  j.mu = o.momentum;
   j.st = stream;
-  // library-owned side stream (default priority) for the weight gradients
+  // library-owned side streams (default priority): weight gradients, held-out evaluation
   if (c.streams.empty()) {
     hipStream_t s2;
     EKYA_CHECK_HIP(hipStreamCreateWithFlags(&s2, hipStreamNonBlocking));
     c.streams.push_back(s2);
   }
-  // per-kernel timing runs serially, so each timed kernel runs alone
   j.st2 = c.timing ? stream : c.streams[0];
-  if (!c.timing) {
+  if (j.eval_overlap) {
     if (!c.eval_stream) EKYA_CHECK_HIP(hipStreamCreateWithFlags(&c.eval_stream, hipStreamNonBlocking));
     j.st3 = c.eval_stream;
   }
@@ -1085,38 +1187,16 @@ ekya_status run_retrain(Ctx& c, float* weights, int k, const void* frames, const
   j.labels = labels;
   j.hframes = hframes;
   j.hlabels = hlabels;
-  j.n_h = n_heldout;
   std::vector<int32_t> S = training_subset(n_frames, o.subsample_frac, o.seed);
-  j.n_s = (int)S.size();
   job_prepare_host(j, S, o.seed);
-  const Net& net = *j.net;
-  const size_t es = dtype_size(dt);
-  const long long feat = j.geo.stage_in_elems(net, j.lowest);
-  j.row_bytes = feat * ((j.lowest == 5) ? 4 : es);
-  const int ccap = 512;  // frames per cache-build chunk
-
-  // plan: job buffers + cache + cache-build scratch
-  auto plan = [&](Arena& a, void*& cache, int32_t*& d_S, void*& padded, EvalBufs& ceb) {
-    plan_job(a, j);
-    cache = nullptr;
-    d_S = nullptr;
-    padded = nullptr;
-    if (j.lowest >= 1) {
-      cache = a.take_bytes((size_t)(j.n_s + j.n_h) * j.row_bytes);
-      d_S = a.take<int32_t>(j.n_s);
-      padded = a.take_bytes((size_t)ccap * j.geo.H * j.geo.W * net.conv[0].cin_pad * es);
-      plan_eval(a, net, j.geo, 0, j.lowest - 1, ccap, ceb);
-    }
-  };
-  Arena meas;
-  void *cache, *padded;
-  int32_t* d_S;
-  EvalBufs ceb;
-  plan(meas, cache, d_S, padded, ceb);
-  EKYA_CHECK_HIP(c.retrain_ws.ensure(meas.used));
   Arena real;
-  real.base = reinterpret_cast<char*>(c.retrain_ws.p);
-  plan(real, cache, d_S, padded, ceb);
+  real.base = reinterpret_cast<char*>(c.ws.p);
+  plan_retrain(real, j, rb);
+  void* cache = rb.cache;
+  int32_t* d_S = rb.d_S;
+  void* padded = rb.padded;
+  EvalBufs& ceb = rb.ceb;
+  const int ccap = kCacheChunk;
   j.cache = cache;
   j.hcache = cache ? reinterpret_cast<char*>(cache) + (long long)j.n_s * j.row_bytes : nullptr;
 
@@ -1143,6 +1223,7 @@ ekya_status run_retrain(Ctx& c, float* weights, int k, const void* frames, const
     return hipSuccess;
   };
   hipError_t he = run();
+  (void)hipEventRecord(c.last_done, stream);  // after whatever was queued
   JobResult r;
   if (he == hipSuccess) he = job_collect(j, r);
   float pms = 0.f;
@@ -1160,6 +1241,7 @@ ekya_status run_retrain(Ctx& c, float* weights, int k, const void* frames, const
   for (int e = 0; e < j.epochs; ++e) {
     res->heldout_acc[e] = j.n_h ? (float)r.hc[e] / (float)j.n_h : 0.f;
     res->epoch_seconds[e] = r.secs[e];
+    res->eval_seconds[e] = r.esecs[e];
     double l = 0.0;
     for (int s = 0; s < spe; ++s) l += r.ce[3 * (e * spe + s)];
     res->epoch_loss[e] = (float)(l / spe);
@@ -1173,6 +1255,89 @@ ekya_status run_retrain(Ctx& c, float* weights, int k, const void* frames, const
 }
 
 // --------------------------------------------------------------- profile
+// A frozen-prefix feature cache shared by the candidates of one depth.
+struct CacheInfo {
+  int lowest;
+  int n_rows_s;  // training rows (prefix of the shared draw) held
+  long long row_bytes;
+  void* p;
+};
+
+struct ProfilePlan {
+  std::vector<TrainJob> jobs;
+  std::vector<CacheInfo> caches;
+  int n_max = 0;  // frames of the shared draw
+  int32_t* d_S = nullptr;
+  void* padded = nullptr;
+  EvalBufs ceb;
+  float *pmaster = nullptr, *pfold = nullptr;
+  void* pshadow = nullptr;
+};
+
+// Candidate jobs and per-depth caches from the call's arguments (host only).
+static void config_profile(ProfilePlan& pp, const Net& net, const ekya_profile_cfg* cfgs, int n_cfgs,
+                           int n_frames, int H, int W, int n_heldout) {
+  const Geo geo = Geo::build(net, H, W);
+  const size_t es = dtype_size(net.dt);
+  pp.n_max = 0;
+  for (int i = 0; i < n_cfgs; ++i)
+    pp.n_max = std::max(pp.n_max, subset_count(n_frames, cfgs[i].subsample_frac));
+  pp.caches.clear();
+  for (int i = 0; i < n_cfgs; ++i) {
+    const int lo = 6 - cfgs[i].k_trainable;
+    if (lo == 0) continue;
+    const int ns = subset_count(n_frames, cfgs[i].subsample_frac);
+    bool found = false;
+    for (auto& ci : pp.caches)
+      if (ci.lowest == lo) {
+        ci.n_rows_s = std::max(ci.n_rows_s, ns);
+        found = true;
+      }
+    if (!found)
+      pp.caches.push_back({lo, ns, geo.stage_in_elems(net, lo) * (long long)((lo == 5) ? 4 : es), nullptr});
+  }
+  pp.jobs.assign(n_cfgs, TrainJob());
+  for (int i = 0; i < n_cfgs; ++i) {
+    TrainJob& j = pp.jobs[i];
+    const ekya_profile_cfg& cf = cfgs[i];
+    j.net = &net;
+    j.geo = geo;
+    j.dt = net.dt;
+    j.k = cf.k_trainable;
+    j.lowest = 6 - cf.k_trainable;
+    j.B = cf.batch;
+    j.epochs = cf.epochs;
+    j.lr = cf.lr;
+    j.mu = cf.momentum;
+    j.n_h = n_heldout;
+    j.n_s = subset_count(n_frames, cf.subsample_frac);
+    j.n_steps = j.epochs * cdiv(j.n_s, j.B);
+  }
+}
+
+static void plan_profile(Arena& a, ProfilePlan& pp, int n_heldout, int H, int W) {
+  const Net& net = *pp.jobs[0].net;
+  const Geo& geo = pp.jobs[0].geo;
+  const size_t es = dtype_size(net.dt);
+  for (auto& j : pp.jobs) plan_job(a, j);
+  for (auto& ci : pp.caches) ci.p = a.take_bytes((size_t)(ci.n_rows_s + n_heldout) * ci.row_bytes);
+  pp.d_S = a.take<int32_t>(std::max(1, pp.n_max));
+  pp.padded = a.take_bytes((size_t)kCacheChunk * H * W * net.conv[0].cin_pad * es);
+  plan_eval(a, net, geo, 0, 4, kCacheChunk, pp.ceb);
+  pp.pmaster = a.take<float>(net.total);
+  pp.pfold = a.take<float>(2 * net.bn_channels);
+  pp.pshadow = a.take_bytes(net.shadow_elems * es);
+}
+
+size_t profile_workspace_bytes(const Net& net, const ekya_profile_cfg* cfgs, int n_cfgs,
+                               int n_frames, int H, int W, int n_heldout) {
+  ProfilePlan pp;
+  config_profile(pp, net, cfgs, n_cfgs, n_frames, H, W, n_heldout);
+  Arena a;
+  plan_profile(a, pp, n_heldout, H, W);
+  return a.used;
+}
+
 ekya_status run_profile(Ctx& c, const float* weights, const ekya_profile_cfg* cfgs, int n_cfgs,
                         const void* frames, const int32_t* labels, int n_frames, int H, int W,
                         const void* hframes, const int32_t* hlabels, int n_heldout,
@@ -1182,12 +1347,8 @@ ekya_status run_profile(Ctx& c, const float* weights, const ekya_profile_cfg* cf
   const int dt = precision;
   const Net& net = c.net[dt];
   const Geo geo = Geo::build(net, H, W);
-  const size_t es = dtype_size(dt);
-  // one shared draw; each candidate uses a prefix of it
-  int n_max = 0;
-  for (int i = 0; i < n_cfgs; ++i)
-    n_max = std::max(n_max, subset_count(n_frames, cfgs[i].subsample_frac));
-  const std::vector<int32_t> S = partial_shuffle(n_frames, n_max, subsample_seed);
+  ProfilePlan pp;
+  config_profile(pp, net, cfgs, n_cfgs, n_frames, H, W, n_heldout);
   // streams: per candidate a main and a side stream, plus one for the caches
   while ((int)c.streams.size() < 2 * n_cfgs + 1) {
     hipStream_t s;
@@ -1195,41 +1356,19 @@ ekya_status run_profile(Ctx& c, const float* weights, const ekya_profile_cfg* cf
     c.streams.push_back(s);
   }
   hipStream_t s0 = c.streams[n_cfgs];
-  // caches per distinct lowest stage >= 1, over the n_max frames + held-out
-  struct CacheInfo {
-    int lowest;
-    int n_rows_s;  // training rows (prefix of S) held
-    long long row_bytes;
-    void* p;
-  };
-  std::vector<CacheInfo> caches;
-  for (int i = 0; i < n_cfgs; ++i) {
-    const int lo = 6 - cfgs[i].k_trainable;
-    if (lo == 0) continue;
-    const int ns = subset_count(n_frames, cfgs[i].subsample_frac);
-    bool found = false;
-    for (auto& ci : caches)
-      if (ci.lowest == lo) {
-        ci.n_rows_s = std::max(ci.n_rows_s, ns);
-        found = true;
-      }
-    if (!found)
-      caches.push_back({lo, ns, geo.stage_in_elems(net, lo) * (long long)((lo == 5) ? 4 : es), nullptr});
+  {
+    Arena meas;
+    plan_profile(meas, pp, n_heldout, H, W);
+    if (ekya_status s = acquire_workspace(c, meas.used, s0)) return s;
   }
-  std::vector<TrainJob> jobs(n_cfgs);
+  // one shared draw; each candidate uses a prefix of it
+  const int n_max = pp.n_max;
+  const std::vector<int32_t> S = partial_shuffle(n_frames, n_max, subsample_seed);
+  std::vector<TrainJob>& jobs = pp.jobs;
+  std::vector<CacheInfo>& caches = pp.caches;
   for (int i = 0; i < n_cfgs; ++i) {
     TrainJob& j = jobs[i];
-    const ekya_profile_cfg& cf = cfgs[i];
-    j.net = &net;
     j.tabs = &c.tabs[dt];
-    j.geo = geo;
-    j.dt = dt;
-    j.k = cf.k_trainable;
-    j.lowest = 6 - cf.k_trainable;
-    j.B = cf.batch;
-    j.epochs = cf.epochs;
-    j.lr = cf.lr;
-    j.mu = cf.momentum;
     j.st = c.streams[i];
     j.st2 = c.timing ? j.st : c.streams[n_cfgs + 1 + i];
     j.weights = weights;
@@ -1237,35 +1376,19 @@ ekya_status run_profile(Ctx& c, const float* weights, const ekya_profile_cfg* cf
     j.labels = labels;
     j.hframes = hframes;
     j.hlabels = hlabels;
-    j.n_h = n_heldout;
-    j.n_s = subset_count(n_frames, cf.subsample_frac);
     std::vector<int32_t> Si(S.begin(), S.begin() + j.n_s);
-    job_prepare_host(j, Si, cf.shuffle_seed);
+    job_prepare_host(j, Si, cfgs[i].shuffle_seed);
   }
-  const int ccap = 512;
-  int32_t* d_S = nullptr;
-  void* padded = nullptr;
-  EvalBufs ceb;
-  float *pmaster = nullptr, *pfold = nullptr;
-  void* pshadow = nullptr;
-  auto plan = [&](Arena& a) {
-    for (auto& j : jobs) plan_job(a, j);
-    for (auto& ci : caches) {
-      ci.p = a.take_bytes((size_t)(ci.n_rows_s + n_heldout) * ci.row_bytes);
-    }
-    d_S = a.take<int32_t>(std::max(1, n_max));
-    padded = a.take_bytes((size_t)ccap * H * W * net.conv[0].cin_pad * es);
-    plan_eval(a, net, geo, 0, 4, ccap, ceb);
-    pmaster = a.take<float>(net.total);
-    pfold = a.take<float>(2 * net.bn_channels);
-    pshadow = a.take_bytes(net.shadow_elems * es);
-  };
-  Arena meas;
-  plan(meas);
-  EKYA_CHECK_HIP(c.profile_ws.ensure(meas.used));
+  const int ccap = kCacheChunk;
   Arena real;
-  real.base = reinterpret_cast<char*>(c.profile_ws.p);
-  plan(real);
+  real.base = reinterpret_cast<char*>(c.ws.p);
+  plan_profile(real, pp, n_heldout, H, W);
+  int32_t* d_S = pp.d_S;
+  void* padded = pp.padded;
+  EvalBufs& ceb = pp.ceb;
+  float* pmaster = pp.pmaster;
+  float* pfold = pp.pfold;
+  void* pshadow = pp.pshadow;
 
   // caches: the frozen prefix of the starting weights, built once per depth on s0
   const Tables& t = c.tabs[dt];
@@ -1337,6 +1460,7 @@ ekya_status run_profile(Ctx& c, const float* weights, const ekya_profile_cfg* cf
       for (int ep = 0; ep < j.epochs; ++ep) {
         o.heldout_acc[ep] = n_heldout ? (float)r.hc[ep] / (float)n_heldout : 0.f;
         o.epoch_seconds[ep] = r.secs[ep];
+        o.eval_seconds[ep] = r.esecs[ep];
         double l = 0.0;
         for (int s = 0; s < spe; ++s) l += r.ce[3 * (ep * spe + s)];
         o.epoch_loss[ep] = (float)(l / spe);
@@ -1349,10 +1473,41 @@ ekya_status run_profile(Ctx& c, const float* weights, const ekya_profile_cfg* cf
     }
     destroy_events(j);
   }
+  // every candidate's streams are idle before the next call reuses the arena
+  for (const TrainJob& j : jobs) {
+    (void)hipStreamSynchronize(j.st);
+    (void)hipStreamSynchronize(j.st2);
+  }
+  (void)hipEventRecord(c.last_done, s0);
   return overall;
 }
 
 // ----------------------------------------------------------------- infer
+// Frames per chunk of batched inference.
+static constexpr int kInferChunk = 512;
+
+struct InferBufs {
+  float *master = nullptr, *fold = nullptr;
+  void *shadow = nullptr, *padded = nullptr;
+  EvalBufs eb;
+};
+
+static void plan_infer(Arena& a, const Net& net, const Geo& geo, int resolution, InferBufs& b) {
+  const size_t es = dtype_size(net.dt);
+  b.master = a.take<float>(net.total);
+  b.fold = a.take<float>(2 * net.bn_channels);
+  b.shadow = a.take_bytes(net.shadow_elems * es);
+  b.padded = a.take_bytes((size_t)kInferChunk * resolution * resolution * net.conv[0].cin_pad * es);
+  plan_eval(a, net, geo, 0, 5, kInferChunk, b.eb);
+}
+
+size_t infer_workspace_bytes(const Net& net, int resolution) {
+  InferBufs b;
+  Arena a;
+  plan_infer(a, net, Geo::build(net, resolution, resolution), resolution, b);
+  return a.used;
+}
+
 ekya_status run_infer(Ctx& c, const float* weights, const void* frames, int n, int H, int W,
                       int resolution, int precision, int32_t* labels_out, hipStream_t stream) {
   EKYA_CHECK_HIP(hipSetDevice(c.device));
@@ -1361,26 +1516,21 @@ ekya_status run_infer(Ctx& c, const float* weights, const void* frames, int n, i
   const Net& net = c.net[dt];
   const Geo geo = Geo::build(net, resolution, resolution);
   const size_t es = dtype_size(dt);
-  const int cap = 512;
-  float *master = nullptr, *fold = nullptr;
-  void *shadow = nullptr, *padded = nullptr;
-  EvalBufs eb;
-  auto plan = [&](Arena& a) {
-    master = a.take<float>(net.total);
-    fold = a.take<float>(2 * net.bn_channels);
-    shadow = a.take_bytes(net.shadow_elems * es);
-    padded = a.take_bytes((size_t)cap * resolution * resolution * net.conv[0].cin_pad * es);
-    plan_eval(a, net, geo, 0, 5, cap, eb);
-  };
-  Arena meas;
-  plan(meas);
-  // the previous inference call may still be using the workspace
-  EKYA_CHECK_HIP(hipStreamWaitEvent(stream, c.infer_done, 0));
-  if (meas.used > c.infer_ws.cap) EKYA_CHECK_HIP(hipEventSynchronize(c.infer_done));
-  EKYA_CHECK_HIP(c.infer_ws.ensure(meas.used));
+  const int cap = kInferChunk;
+  InferBufs ib;
+  {
+    Arena meas;
+    plan_infer(meas, net, geo, resolution, ib);
+    if (ekya_status s = acquire_workspace(c, meas.used, stream)) return s;
+  }
   Arena real;
-  real.base = reinterpret_cast<char*>(c.infer_ws.p);
-  plan(real);
+  real.base = reinterpret_cast<char*>(c.ws.p);
+  plan_infer(real, net, geo, resolution, ib);
+  float* master = ib.master;
+  float* fold = ib.fold;
+  void* shadow = ib.shadow;
+  void* padded = ib.padded;
+  EvalBufs& eb = ib.eb;
   const Tables& t = c.tabs[dt];
   auto run = [&]() -> hipError_t {
     EKYA_HIP(permute_weights(weights, master, t.permute, t.n_permute, net.total, 1, stream));
@@ -1406,10 +1556,11 @@ ekya_status run_infer(Ctx& c, const float* weights, const void* frames, int n, i
       }
       EKYA_HIP(argmax_rows(eb.logits, cnt, net.n_classes, labels_out + i0, stream));
     }
-    EKYA_HIP(hipEventRecord(c.infer_done, stream));
     return hipSuccess;
   };
-  EKYA_CHECK_HIP(run());
+  hipError_t he = run();
+  (void)hipEventRecord(c.last_done, stream);  // after whatever was queued
+  EKYA_CHECK_HIP(he);
   return EKYA_OK;
 }
 

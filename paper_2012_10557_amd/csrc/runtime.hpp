@@ -12,11 +12,11 @@
 
 namespace ekya {
 
-// Growable device buffer owned by the context.
+// Device buffer owned by the context.
 struct DeviceBuf {
   void* p = nullptr;
   size_t cap = 0;
-  hipError_t ensure(size_t bytes);
+  hipError_t alloc(size_t bytes);  // exactly `bytes` (releases what it held)
   void release();
 };
 
@@ -68,8 +68,16 @@ struct Ctx {
   std::string err;
   Net net[2];
   Tables tabs[2];
-  DeviceBuf retrain_ws, infer_ws, profile_ws;
-  hipEvent_t infer_done = nullptr;
+  // The workspace arena every call plans its device buffers in.  With
+  // fixed_ws it was allocated once at creation and is never replaced; a call
+  // that needs more fails before queueing any work.  Otherwise a call that
+  // needs more replaces it before queueing any work, after the context's
+  // previous call has finished.
+  DeviceBuf ws;
+  bool fixed_ws = false;
+  // Recorded after the last work of every call that used the arena; the next
+  // call's stream waits for it (calls on one context run in turn on the GPU).
+  hipEvent_t last_done = nullptr;
   std::vector<hipStream_t> streams;  // profiler streams (default priority)
   hipStream_t eval_stream = nullptr;  // retraining's held-out evaluation (default priority)
   bool timing = false;
@@ -80,7 +88,15 @@ struct Ctx {
 // Read the events of finished timed launches into `stats`.
 hipError_t ctx_collect_timing(Ctx& c);
 
-hipError_t ctx_init(Ctx& c, int device, int n_classes);
+hipError_t ctx_init(Ctx& c, int device, int n_classes, size_t workspace_bytes);
+
+// Bytes of workspace arena a call with these arguments plans (host only;
+// arguments already validated).
+size_t retrain_workspace_bytes(const Net& net, int k, int n_frames, int H, int W, int n_heldout,
+                               const ekya_train_opts& o);
+size_t profile_workspace_bytes(const Net& net, const ekya_profile_cfg* cfgs, int n_cfgs,
+                               int n_frames, int H, int W, int n_heldout);
+size_t infer_workspace_bytes(const Net& net, int resolution);
 void ctx_free(Ctx& c);
 
 ekya_status run_retrain(Ctx& c, float* weights, int k, const void* frames, const int32_t* labels,
