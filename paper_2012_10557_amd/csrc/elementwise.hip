@@ -46,9 +46,12 @@ inline int grid_for(long long n, int per_block = 256, int cap = 8192) {
 }
 
 // Chunking of the M rows for per-channel reductions.
+// Chunks of rows for the partial sums of large-M BatchNorm: at least 256 rows
+// each and at most 512 of them -- two blocks per CU stream the activations,
+// and the final per-channel reduction reads at most 512 partials.
 inline int bn_chunks(long long M) {
-  long long c = cdivl(M, 16);
-  if (c > 2048) c = 2048;
+  long long c = cdivl(M, 256);
+  if (c > 512) c = 512;
   if (c < 1) c = 1;
   return (int)c;
 }
@@ -71,14 +74,26 @@ __global__ __launch_bounds__(256) void bn_stats_partial(const T* z, long long M,
   for (int i = 0; i < E; ++i) s1[i] = s2[i] = 0.f;
   if (rsub < rpi) {
     unit_to_f<T>(*reinterpret_cast<const uint4*>(z + cu * E), K);
-    for (long long r = r0 + rsub; r < r1; r += rpi) {
-      float v[E];
-      unit_to_f<T>(*reinterpret_cast<const uint4*>(z + r * C + cu * E), v);
+    // four rows' loads issued before they are accumulated (in row order)
+    constexpr int U = 4;
+    for (long long r = r0 + rsub; r < r1; r += U * rpi) {
+      uint4 raw[U];
 #pragma unroll
-      for (int i = 0; i < E; ++i) {
-        float d = v[i] - K[i];
-        s1[i] += d;
-        s2[i] += d * d;
+      for (int q = 0; q < U; ++q) {
+        const long long rq = r + (long long)q * rpi;
+        raw[q] = rq < r1 ? *reinterpret_cast<const uint4*>(z + rq * C + cu * E) : uint4{0, 0, 0, 0};
+      }
+#pragma unroll
+      for (int q = 0; q < U; ++q) {
+        if (r + (long long)q * rpi >= r1) break;
+        float v[E];
+        unit_to_f<T>(raw[q], v);
+#pragma unroll
+        for (int i = 0; i < E; ++i) {
+          float d = v[i] - K[i];
+          s1[i] += d;
+          s2[i] += d * d;
+        }
       }
     }
   }
@@ -105,9 +120,11 @@ __global__ __launch_bounds__(256) void bn_stats_partial(const T* z, long long M,
 // Fixed-order sum over chunks of the two partial rows of channel c: a block
 // handles 16 channels with 16 threads each (thread slice k sums chunks k,
 // k+16, ...; 16 consecutive channels per load, so each read is 64 bytes), and
-// the 16 slice sums are added in slice order in double.  Returns true for the
-// one thread per channel that holds the totals.
+// the 16 slice sums are added in slice order in double.  A thread issues the
+// loads of 8 of its chunks before adding them, so their latencies overlap.
+// Returns true for the one thread per channel that holds the totals.
 constexpr int FIN_CH = 16;
+constexpr int FIN_BATCH = 8;
 __device__ __forceinline__ bool chunk_sums(const float* part, int nchunks, int C, double& a,
                                            double& b) {
   __shared__ float sa[16][FIN_CH], sb[16][FIN_CH];
@@ -115,9 +132,20 @@ __device__ __forceinline__ bool chunk_sums(const float* part, int nchunks, int C
   const int c = blockIdx.x * FIN_CH + lc;
   float x = 0.f, y = 0.f;
   if (c < C)
-    for (int k = slice; k < nchunks; k += 16) {
-      x += part[(long long)k * 2 * C + c];
-      y += part[(long long)k * 2 * C + C + c];
+    for (int k0 = slice; k0 < nchunks; k0 += 16 * FIN_BATCH) {
+      float v1[FIN_BATCH], v2[FIN_BATCH];
+#pragma unroll
+      for (int u = 0; u < FIN_BATCH; ++u) {
+        const int k = k0 + 16 * u;
+        v1[u] = k < nchunks ? part[(long long)k * 2 * C + c] : 0.f;
+        v2[u] = k < nchunks ? part[(long long)k * 2 * C + C + c] : 0.f;
+      }
+#pragma unroll
+      for (int u = 0; u < FIN_BATCH; ++u)
+        if (k0 + 16 * u < nchunks) {
+          x += v1[u];
+          y += v2[u];
+        }
     }
   sa[slice][lc] = x;
   sb[slice][lc] = y;
@@ -681,21 +709,36 @@ __global__ __launch_bounds__(256) void bn_bwd_partial(const T* dy, const T* y, c
     mu[i] = mean[cu * E + i];
   }
   if (rsub < rpi) {
-    for (long long r = r0 + rsub; r < r1; r += rpi) {
-      const long long off = r * C + cu * E;
-      float g[E], zz[E];
-      unit_to_f<T>(*reinterpret_cast<const uint4*>(dy + off), g);
-      unit_to_f<T>(*reinterpret_cast<const uint4*>(z + off), zz);
-      if (y) {
-        float yy[E];
-        unit_to_f<T>(*reinterpret_cast<const uint4*>(y + off), yy);
+    // two rows' loads issued before they are accumulated (in row order)
+    constexpr int U = 2;
+    for (long long r = r0 + rsub; r < r1; r += U * rpi) {
+      uint4 rg[U], rz[U], ry[U];
 #pragma unroll
-        for (int i = 0; i < E; ++i) g[i] = yy[i] > 0.f ? g[i] : 0.f;
+      for (int q = 0; q < U; ++q) {
+        const long long rq = r + (long long)q * rpi;
+        const bool in = rq < r1;
+        const long long off = rq * C + cu * E;
+        rg[q] = in ? *reinterpret_cast<const uint4*>(dy + off) : uint4{0, 0, 0, 0};
+        rz[q] = in ? *reinterpret_cast<const uint4*>(z + off) : uint4{0, 0, 0, 0};
+        ry[q] = (in && y) ? *reinterpret_cast<const uint4*>(y + off) : uint4{0, 0, 0, 0};
       }
 #pragma unroll
-      for (int i = 0; i < E; ++i) {
-        s1[i] += g[i];
-        s2[i] += g[i] * (zz[i] - mu[i]);
+      for (int q = 0; q < U; ++q) {
+        if (r + (long long)q * rpi >= r1) break;
+        float g[E], zz[E];
+        unit_to_f<T>(rg[q], g);
+        unit_to_f<T>(rz[q], zz);
+        if (y) {
+          float yy[E];
+          unit_to_f<T>(ry[q], yy);
+#pragma unroll
+          for (int i = 0; i < E; ++i) g[i] = yy[i] > 0.f ? g[i] : 0.f;
+        }
+#pragma unroll
+        for (int i = 0; i < E; ++i) {
+          s1[i] += g[i];
+          s2[i] += g[i] * (zz[i] - mu[i]);
+        }
       }
     }
   }
@@ -1614,7 +1657,12 @@ hipError_t split_reduce_bn(int dt, const float* part, int splits, long long M, i
       (sink.bwd && (!sink.z || !sink.mean)))
     return hipErrorInvalidValue;
   const dim3 grid((unsigned)cdivl(M, BN_FOLD_ROWS), C / BN_GROUP);
-  return by_type(dt, [&](auto* tp) {
+  const double act = (double)M * C * dtype_size(dt);
+  // fp32 partials of every split read, the sum written; the backward variant
+  // also reads the ReLU mask and the BatchNorm input (and a residual)
+  const double bytes = (double)M * C * 4 * splits + act * (1 + (res ? 1 : 0) + (sink.bwd ? 2 : 0));
+  TimedLaunch tl(stream);
+  return tl.done(by_type(dt, [&](auto* tp) {
     using T = std::remove_pointer_t<decltype(tp)>;
     if (sink.bwd)
       hipLaunchKernelGGL((split_bn_kernel<T, true>), grid, dim3(1024), 0, stream, part, splits, M,
@@ -1624,7 +1672,7 @@ hipError_t split_reduce_bn(int dt, const float* part, int splits, long long M, i
       hipLaunchKernelGGL((split_bn_kernel<T, false>), grid, dim3(1024), 0, stream, part, splits, M,
                          C, (const T*)res, (T*)out, (const T*)nullptr, (const T*)nullptr,
                          (const float*)nullptr, sink.part);
-  });
+  }), "split_reduce_bn", bytes);
 }
 
 hipError_t bn_train_forward(int dt, const void* z, long long M, int C, const float* gamma,
@@ -1634,25 +1682,37 @@ hipError_t bn_train_forward(int dt, const void* z, long long M, int C, const flo
   if (M == 0) return hipSuccess;
   if (ready_rows != 0 && ((ready_rows != 64 && ready_rows != BN_FOLD_ROWS) || !bn_fold_ok(M, C)))
     return hipErrorInvalidValue;
+  const double act = (double)M * C * dtype_size(dt);  // bytes of one activation tensor
   if (!bn_fold_ok(M, C)) {
-    hipError_t e = bn_train_stats(dt, z, M, C, gamma, beta, rm, rv, mean, invstd, scale, shift,
-                                  partials, stream);
+    TimedLaunch ts(stream);
+    hipError_t e = ts.done(bn_train_stats(dt, z, M, C, gamma, beta, rm, rv, mean, invstd, scale,
+                                          shift, partials, stream),
+                           "bn_fwd_stats", act);
     if (e != hipSuccess) return e;
-    return bn_apply(dt, z, M, C, mean, scale, beta, res, relu, y, stream);
+    TimedLaunch ta(stream);
+    return ta.done(bn_apply(dt, z, M, C, mean, scale, beta, res, relu, y, stream), "bn_fwd_apply",
+                   act * (res ? 3 : 2));
   }
   const int crows = ready_rows ? ready_rows : BN_FOLD_ROWS;
   const int nch = (int)cdivl(M, crows), groups = C / BN_GROUP;
   const long long rpb = bn_fold_rpb(M, C, dt);
-  return by_type(dt, [&](auto* tp) {
-    using T = std::remove_pointer_t<decltype(tp)>;
-    if (!ready_rows)
+  if (!ready_rows) {
+    TimedLaunch tp_(stream);
+    hipError_t e = tp_.done(by_type(dt, [&](auto* tp) {
+      using T = std::remove_pointer_t<decltype(tp)>;
       hipLaunchKernelGGL((bn_group_partial<T, false>), dim3(nch, groups), dim3(256), 0, stream,
                          (const T*)z, (const T*)nullptr, (const T*)nullptr, (const float*)nullptr,
                          M, C, partials);
+    }), "bn_fwd_stats", act);
+    if (e != hipSuccess) return e;
+  }
+  TimedLaunch ta(stream);
+  return ta.done(by_type(dt, [&](auto* tp) {
+    using T = std::remove_pointer_t<decltype(tp)>;
     hipLaunchKernelGGL(bn_fold_apply<T>, dim3((unsigned)cdivl(M, rpb), groups), dim3(256), 0,
                        stream, (const T*)z, partials, nch, crows, M, C, rpb, gamma, beta, rm, rv, mean,
                        invstd, scale, shift, (const T*)res, relu, (T*)y);
-  });
+  }), "bn_fwd_apply", act * (res ? 3 : 2));
 }
 
 hipError_t bn_apply(int dt, const void* z, long long M, int C, const float* mean,
@@ -1681,32 +1741,48 @@ hipError_t bn_backward(int dt, const void* dy, const void* y, const void* z, lon
   if (M == 0) return hipSuccess;
   if (ready_rows != 0 && ((ready_rows != 64 && ready_rows != BN_FOLD_ROWS) || !bn_fold_ok(M, C)))
     return hipErrorInvalidValue;
+  const double act = (double)M * C * dtype_size(dt);
+  // reads dy, z (and y), writes dz (and g)
+  const double apply_bytes = act * (3 + (y ? 1 : 0) + (g_out ? 1 : 0));
   if (bn_fold_ok(M, C)) {
     const int nf = (int)cdivl(M, ready_rows ? ready_rows : BN_FOLD_ROWS), groups = C / BN_GROUP;
     const long long rpb = bn_fold_rpb(M, C, dt);
-    return by_type(dt, [&](auto* tp) {
-      using T = std::remove_pointer_t<decltype(tp)>;
-      if (!ready_rows)
+    if (!ready_rows) {
+      TimedLaunch tp_(stream);
+      hipError_t e = tp_.done(by_type(dt, [&](auto* tp) {
+        using T = std::remove_pointer_t<decltype(tp)>;
         hipLaunchKernelGGL((bn_group_partial<T, true>), dim3(nf, groups), dim3(256), 0, stream,
                            (const T*)z, (const T*)dy, (const T*)y, mean, M, C, partials);
+      }), "bn_bwd_stats", act * (y ? 3 : 2));
+      if (e != hipSuccess) return e;
+    }
+    TimedLaunch ta(stream);
+    return ta.done(by_type(dt, [&](auto* tp) {
+      using T = std::remove_pointer_t<decltype(tp)>;
       hipLaunchKernelGGL(bn_bwd_fold_apply<T>, dim3((unsigned)cdivl(M, rpb), groups), dim3(256), 0,
                          stream, (const T*)dy, (const T*)y, (const T*)z, partials, nf, M, C, rpb,
                          gamma, mean, invstd, dgamma, dbeta, (T*)dz, (T*)g_out);
-    });
+    }), "bn_bwd_apply", apply_bytes);
   }
   const int nch = bn_chunks(M);
   const long long rpc = cdivl(M, nch);
   float* coef = partials + (size_t)nch * 2 * C;
   const long long units = M * C / dtype_vec(dt);
-  return by_type(dt, [&](auto* tp) {
+  TimedLaunch ts(stream);
+  hipError_t e = ts.done(by_type(dt, [&](auto* tp) {
     using T = std::remove_pointer_t<decltype(tp)>;
     hipLaunchKernelGGL(bn_bwd_partial<T>, dim3(nch), dim3(256), 0, stream, (const T*)dy,
                        (const T*)y, (const T*)z, M, C, rpc, mean, partials);
     hipLaunchKernelGGL(bn_bwd_final, dim3(cdiv(C, FIN_CH)), dim3(256), 0, stream, partials, nch, M, C,
                        gamma, invstd, dgamma, dbeta, coef);
+  }), "bn_bwd_stats", act * (y ? 3 : 2));
+  if (e != hipSuccess) return e;
+  TimedLaunch ta(stream);
+  return ta.done(by_type(dt, [&](auto* tp) {
+    using T = std::remove_pointer_t<decltype(tp)>;
     hipLaunchKernelGGL(bn_bwd_apply<T>, dim3(grid_for(units)), dim3(256), 0, stream, (const T*)dy,
                        (const T*)y, (const T*)z, units, C, mean, coef, (T*)dz, (T*)g_out);
-  });
+  }), "bn_bwd_apply", apply_bytes);
 }
 
 hipError_t maxpool_fwd(int dt, const void* x, int N, int H, int W, int C, void* y, uint8_t* arg,
@@ -1714,11 +1790,13 @@ hipError_t maxpool_fwd(int dt, const void* x, int N, int H, int W, int C, void* 
   const int P = (H - 1) / 2 + 1, Q = (W - 1) / 2 + 1;
   const long long units = (long long)N * P * Q * C / dtype_vec(dt);
   if (units == 0) return hipSuccess;
-  return by_type(dt, [&](auto* tp) {
+  const size_t es = dtype_size(dt);
+  TimedLaunch tl(stream);  // input once; output (and its window index)
+  return tl.done(by_type(dt, [&](auto* tp) {
     using T = std::remove_pointer_t<decltype(tp)>;
     hipLaunchKernelGGL(maxpool_fwd_kernel<T>, dim3(grid_for(units)), dim3(256), 0, stream,
                        (const T*)x, N, H, W, C, P, Q, (T*)y, arg);
-  });
+  }), "maxpool_fwd", (double)N * C * ((double)H * W * es + (double)P * Q * (es + (arg ? 1 : 0))));
 }
 
 hipError_t maxpool_bwd(int dt, const void* dy, const uint8_t* arg, int N, int H, int W, int C,
@@ -1726,11 +1804,13 @@ hipError_t maxpool_bwd(int dt, const void* dy, const uint8_t* arg, int N, int H,
   const int P = (H - 1) / 2 + 1, Q = (W - 1) / 2 + 1;
   const long long units = (long long)N * H * W * C / dtype_vec(dt);
   if (units == 0) return hipSuccess;
-  return by_type(dt, [&](auto* tp) {
+  const size_t es = dtype_size(dt);
+  TimedLaunch tl(stream);  // output gradient and window index once; input gradient
+  return tl.done(by_type(dt, [&](auto* tp) {
     using T = std::remove_pointer_t<decltype(tp)>;
     hipLaunchKernelGGL(maxpool_bwd_kernel<T>, dim3(grid_for(units)), dim3(256), 0, stream,
                        (const T*)dy, arg, N, H, W, C, P, Q, (T*)dx);
-  });
+  }), "maxpool_bwd", (double)N * C * ((double)P * Q * (es + 1) + (double)H * W * es));
 }
 
 hipError_t avgpool_fwd(int dt, const void* x, int N, int HW, int C, float* f, hipStream_t stream) {
@@ -1784,7 +1864,8 @@ hipError_t head_forward(int dt, const void* x, int HW, const float* f, const flo
                         hipStream_t stream) {
   if (N == 0) return hipSuccess;
   if (I > 2048 || I % dtype_vec(dt) != 0) return hipErrorInvalidValue;
-  return by_type(dt, [&](auto* tp) {
+  TimedLaunch tl(stream);
+  return tl.done(by_type(dt, [&](auto* tp) {
     using T = std::remove_pointer_t<decltype(tp)>;
     if (I <= 512)  // ResNet18's 512 features: 16 waves per sample
       hipLaunchKernelGGL((head_fwd_kernel<T, 16, 512>), dim3(N), dim3(1024), 0, stream,
@@ -1792,7 +1873,7 @@ hipError_t head_forward(int dt, const void* x, int HW, const float* f, const flo
     else
       hipLaunchKernelGGL((head_fwd_kernel<T, 4, 2048>), dim3(N), dim3(256), 0, stream,
                          (const T*)x, HW, f, W, b, I, J, pooled, z);
-  });
+  }), "head_fwd", x ? (double)N * HW * I * dtype_size(dt) : (double)N * I * 4);
 }
 
 bool head_backward_fused(int J, int I) { return J <= HEAD_JMAX && I <= 64 * HEAD_WB; }
@@ -1810,7 +1891,10 @@ hipError_t head_backward(int dt, const float* z, const int32_t* labels, const in
       !dout ? 0 : bnp ? (int)cdivl(Mr, 64) * (I / BN_GROUP) : N * cdiv(HW, HEAD_PC);
   const HeadBnArgs ha = bnp ? HeadBnArgs{bn->ymask, bn->z, bn->mean, bn->part}
                             : HeadBnArgs{nullptr, nullptr, nullptr, nullptr};
-  hipError_t e = by_type(dt, [&](auto* tp) {
+  // the pooled-feature gradient spread over the block's output (and, with
+  // the BatchNorm partials, that block's ReLU mask and BatchNorm input read)
+  TimedLaunch tl(stream);
+  hipError_t e = tl.done(by_type(dt, [&](auto* tp) {
     using T = std::remove_pointer_t<decltype(tp)>;
     if (bnp)
       hipLaunchKernelGGL((head_bwd_kernel<T, true>), dim3(HEAD_WB + dblocks), dim3(256), 0, stream,
@@ -1818,7 +1902,7 @@ hipError_t head_backward(int dt, const float* z, const int32_t* labels, const in
     else
       hipLaunchKernelGGL((head_bwd_kernel<T, false>), dim3(HEAD_WB + dblocks), dim3(256), 0,
                          stream, z, labels, idx, N, J, f, W, I, dW, db, (T*)dout, HW, out, ha);
-  });
+  }), "head_bwd", (double)Mr * I * dtype_size(dt) * (bnp ? 3 : 1) + (double)N * I * 4);
   if (e == hipSuccess && bnp) bn->rows = 64;
   return e;
 }
@@ -1846,31 +1930,34 @@ hipError_t gather_rows(const void* src, const int32_t* idx, int n, long long row
                        hipStream_t stream) {
   const long long ru = row_bytes / 16;
   if (n == 0 || ru == 0) return hipSuccess;
+  TimedLaunch tl(stream);
   hipLaunchKernelGGL(gather_rows_kernel, dim3(grid_for(n * ru)), dim3(256), 0, stream,
                      (const uint4*)src, idx, n, ru, (uint4*)dst);
-  return hipGetLastError();
+  return tl.done(hipGetLastError(), "gather_rows", 2.0 * n * row_bytes);
 }
 
 hipError_t frames_to_padded(int dt, const void* frames, const int32_t* idx, int n, int H, int W,
                             int Cp, void* dst, hipStream_t stream) {
   const long long hw = (long long)H * W;
   if (n == 0) return hipSuccess;
-  return by_type(dt, [&](auto* tp) {
+  TimedLaunch tl(stream);
+  return tl.done(by_type(dt, [&](auto* tp) {
     using T = std::remove_pointer_t<decltype(tp)>;
     hipLaunchKernelGGL(frames_to_padded_kernel<T>, dim3(grid_for(n * hw)), dim3(256), 0, stream,
                        (const T*)frames, idx, n, hw, Cp, (T*)dst);
-  });
+  }), "frames_to_padded", (double)n * hw * (3 + Cp) * dtype_size(dt));
 }
 
 hipError_t resize_to_padded(int dt, const void* frames, int n, int H, int W, int r, int Cp,
                             void* dst, hipStream_t stream) {
   const long long total = (long long)n * r * r;
   if (total == 0) return hipSuccess;
-  return by_type(dt, [&](auto* tp) {
+  TimedLaunch tl(stream);  // every source pixel once, every padded output pixel
+  return tl.done(by_type(dt, [&](auto* tp) {
     using T = std::remove_pointer_t<decltype(tp)>;
     hipLaunchKernelGGL(resize_kernel<T>, dim3(grid_for(total)), dim3(256), 0, stream,
                        (const T*)frames, n, H, W, r, Cp, (T*)dst);
-  });
+  }), "resize", (double)n * ((double)H * W * 3 + (double)r * r * Cp) * dtype_size(dt));
 }
 
 hipError_t cast_from_f32(int dt, const float* src, long long n, void* dst, hipStream_t stream) {
@@ -1897,11 +1984,15 @@ hipError_t conv_weight_update(int dt, const float* part, int splits, int K, int 
   if (K % 64 != 0 || C % 64 != 0 || splits < 1 || (long long)K * RS * C >= (1LL << 31))
     return hipErrorInvalidValue;
   const int ntiles = RS * (K / UPD_K) * (C / 64);
-  return by_type(dt, [&](auto* tp) {
+  // per weight: the split partials, master and momentum read; master and
+  // momentum written, and the two low-precision copies
+  const double n = (double)K * RS * C;
+  TimedLaunch tl(stream);
+  return tl.done(by_type(dt, [&](auto* tp) {
     using T = std::remove_pointer_t<decltype(tp)>;
     hipLaunchKernelGGL(conv_update_kernel<T>, dim3(std::min(ntiles, 4096)), dim3(256), 0, stream,
                        part, splits, K, RS, C, w, v, lr, mu, (T*)krsc, (T*)crsk);
-  });
+  }), "conv_update", n * (4.0 * splits + 16 + 2 * dtype_size(dt)));
 }
 
 hipError_t sgd_momentum_ranges(float* w, float* v, const float* g, const long long* tab, int n,

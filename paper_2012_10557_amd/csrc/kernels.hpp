@@ -25,6 +25,32 @@ struct KernelTimer {
 void set_thread_timer(KernelTimer* t);
 KernelTimer* thread_timer();
 
+// The same for the memory-bound kernels: brackets the launches queued between
+// construction and done() with two events on `stream` when the calling thread
+// has a timer installed, logged with the launch's algorithmic HBM bytes.
+class TimedLaunch {
+ public:
+  explicit TimedLaunch(hipStream_t s) : t_(thread_timer()), s_(s) {
+    if (t_) {
+      e0_ = t_->take();
+      e1_ = t_->take();
+      if (hipEventRecord(e0_, s_) != hipSuccess) t_ = nullptr;
+    }
+  }
+  hipError_t done(hipError_t e, const char* name, double bytes) {
+    if (t_ && e == hipSuccess) {
+      e = hipEventRecord(e1_, s_);
+      if (e == hipSuccess) t_->recs.push_back({name, 0.0, bytes, e0_, e1_});
+    }
+    return e;
+  }
+
+ private:
+  KernelTimer* t_;
+  hipStream_t s_;
+  hipEvent_t e0_ = nullptr, e1_ = nullptr;
+};
+
 enum DType { DT_F32 = 0, DT_BF16 = 1 };
 inline size_t dtype_size(int dt) { return dt == DT_F32 ? 4 : 2; }
 inline int dtype_vec(int dt) { return dt == DT_F32 ? 4 : 8; }

@@ -1,7 +1,22 @@
-"""bf16 path at the 224 px retraining shape (ResNet18, layer4 and fc
-trainable) against the fp64 CPU oracle: one SGD step from identical state
-(every trainable tensor's update within 2e-2), and the full 2000-frame window
-(held-out accuracy within one percentage point of the stored oracle run)."""
+"""bf16 path at 224 px against the fp64 CPU oracle: one SGD step from
+identical state at every trainable depth (k = 1, 2 with the oracle run here;
+k = 3 and 6 at batch 32 and 128 against stored oracle runs), the 2000-frame
+layer4+fc windows (an easy one that saturates and a hard one that does not:
+every epoch's held-out accuracy within one percentage point), and a short
+full-depth run shaped like the full-depth workload (batch 128, every stage
+trainable, BatchNorm in train mode).
+
+What is gated at the fixed bf16 tolerance 2e-2: the step loss, the BatchNorm
+running statistics (batch statistics of the activations) and the classifier
+update.  Convolution and BatchNorm-affine updates are weight gradients summed
+over thousands of pixels whose operands are all stored in bf16; rounding the
+operands alone moves them by several percent of the tensor's largest update,
+and ReLU / max-pool branch decisions taken within rounding of their branch
+point move single channels further.  They are gated by the root-mean-square
+error of the update (sampled positions) within BF16_GRAD_RMS of its
+root-mean-square, and printed with their largest error.  Stored runs come
+from tests/golden/make_*_golden.py (oracle only)."""
+import gzip
 import json
 import os
 
@@ -15,7 +30,9 @@ from tests.gpu_util import TOL, as_np, rounded, to_dev
 
 pytestmark = pytest.mark.gpu
 
-GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "retrain_224_k2.json")
+HERE = os.path.join(os.path.dirname(__file__), "golden")
+GOLDEN = os.path.join(HERE, "retrain_224_k2.json")
+BF16_GRAD_RMS = 0.1
 
 
 @pytest.fixture(scope="module")
@@ -26,23 +43,41 @@ def ctx():
     binding.ekya_destroy(c)
 
 
+def _rms_errors(got, ref, w0, names):
+    """Per tensor: (rms error of the update / rms of the oracle's update,
+    largest error / largest oracle update)."""
+    net = ResNet18(6)
+    G, R, W0 = net.unpack(got), net.unpack(ref), net.unpack(np.asarray(w0, dtype=np.float64))
+    out = {}
+    for n in names:
+        dr, dg = R[n] - W0[n], G[n] - W0[n]
+        rms = float(np.sqrt(np.mean((dg - dr) ** 2)) / max(np.sqrt(np.mean(dr * dr)), 1e-30))
+        out[n] = (rms, float(np.abs(dg - dr).max() / max(np.abs(dr).max(), 1e-30)))
+    return out
+
+
+def _gate_updates(strict, loose):
+    """strict: name -> error (fixed 2e-2); loose: name -> (rms err, max err)."""
+    for n, e in strict.items():
+        print(f"  {n:40s} err {e:.3e}  (gate {TOL['bf16']:.0e})")
+    for n, (r, m) in loose.items():
+        print(f"  {n:40s} rms err {r:.3e}  (gate {BF16_GRAD_RMS:.0e})  max err {m:.3e}")
+    bad = {n: e for n, e in strict.items() if e > TOL["bf16"]}
+    assert not bad, bad
+    bad = {n: r for n, (r, _) in loose.items() if r > BF16_GRAD_RMS}
+    assert not bad, bad
+
+
 @pytest.mark.parametrize("k,n", [(1, 40), (2, 40), (2, 64)])
 def test_bf16_one_step_224_matches_oracle(ctx, k, n):
     """n frames at 224 px, one batch, one SGD step from identical state (at
     n = 40 the layer4 convolutions split their reduction and BatchNorm
     statistics come from the split reduction; at n = 64, the retraining
-    batch, they run unsplit and the GEMM epilogues leave the statistics).
-    Within 2e-2 of the oracle: the step loss, the BatchNorm running-statistic
-    updates (batch statistics of the activations) and the classifier update.
-    Conv and BatchNorm parameter updates of the trainable stages go through
-    ReLU branch decisions that bf16 rounding flips for thousands of elements
-    (see tests/margins.py), so each is bounded by max(2e-2, 3 x the largest
-    error of an independent bf16-storage implementation over four in-batch
-    orders); frozen stages are bitwise unchanged."""
+    batch, they run unsplit and the GEMM epilogues leave the statistics);
+    frozen stages bitwise unchanged."""
     import torch
     from paper_2012_10557_amd import binding
     from tests.test_gpu_retrain import _update_errors
-    from tests.torch_probe import probe_spread
     w0 = kaiming_resnet18_weights(seed=0)
     win = make_window(WindowSpec(n, 8, 224, 224, drift="shift", seed=4))
     fr, hf = rounded(win["frames"], "bf16"), rounded(win["heldout_frames"], "bf16")
@@ -54,46 +89,104 @@ def test_bf16_one_step_224_matches_oracle(ctx, k, n):
                                1.0, 1, lr, 0.9, n, 0, step_losses=True)
     ref = oracle.retrain(w0, k, fr, win["labels"], hf, win["heldout_labels"], 1.0, 1, lr, 0.9, n, 0)
     assert out["n_steps"] == 1
+    print(f"loss {out['step_loss'][0]:.6f} oracle {ref.losses[0]:.6f}")
     assert abs(out["step_loss"][0] - ref.losses[0]) <= TOL["bf16"] * abs(ref.losses[0])
     net = ResNet18(6)
     lo = len(STAGES) - k
     names = [nm for nm, _ in net.spec if net.stage_of[nm] >= lo]
     got = as_np(w)
-    errs = _update_errors(got, ref.weights, w0, names)
-    strict = [nm for nm in names if nm.startswith("fc.") or net.is_running_stat(nm)]
-    bad = {nm: errs[nm] for nm in strict if errs[nm] > TOL["bf16"]}
-    assert not bad, bad
-    loose = [nm for nm in names if nm not in strict]
-    if loose:
-        probe = probe_spread(w0, k, dict(win, frames=fr), 1.0, lr, 0.9, n, 0, ref.weights, loose,
-                             bf16=True)
-        bad = {nm: (errs[nm], probe[nm]) for nm in loose if errs[nm] > max(TOL["bf16"], 3 * probe[nm])}
-        assert not bad, bad
+    strict_names = [nm for nm in names if nm.startswith("fc.") or net.is_running_stat(nm)]
+    strict = {nm: e for nm, e in _update_errors(got, ref.weights, w0, strict_names).items()}
+    loose = _rms_errors(got, ref.weights, w0, [nm for nm in names if nm not in strict_names])
+    _gate_updates(strict, loose)
     G, W0 = net.unpack(got), net.unpack(w0.astype(np.float64))
     for nm, _ in net.spec:
         if net.stage_of[nm] < lo:
             np.testing.assert_array_equal(G[nm], W0[nm])
 
 
-def test_bf16_window_accuracy_within_1pp_of_oracle(ctx):
-    """The 2000-frame 224 px window at 30% (600 frames), 5 epochs of batch 64:
-    held-out accuracy after the last epoch within 1 percentage point of the
-    stored oracle run, and the first epoch's mean loss within 2e-2."""
+@pytest.fixture(scope="module")
+def onestep():
+    with gzip.open(os.path.join(HERE, "onestep_224.json.gz"), "rt") as f:
+        return json.load(f)
+
+
+@pytest.mark.parametrize("k,n", [(3, 32), (3, 128), (6, 32), (6, 128)])
+def test_bf16_one_step_at_depth_matches_stored_oracle(ctx, onestep, k, n):
+    """One SGD step of layer3+ (k = 3) and of every stage (k = 6: the stem's
+    BatchNorm, ReLU and max-pool backward, layer1-2 in train mode) at 224 px
+    in bf16, at batch 32 and 128 (the full-depth workload's batch: the fused
+    per-convolution momentum steps, deferred across blocks on the second
+    stream, and the GEMM-epilogue BatchNorm statistics).  Against the stored
+    oracle step: loss, every running statistic and the classifier within 2e-2;
+    the other tensors' updates at their stored positions (rms, normalised by
+    the stored rms of the whole tensor's update); frozen stages bitwise."""
     import torch
     from paper_2012_10557_amd import binding
-    with open(GOLDEN) as f:
-        g = json.load(f)
-    c = g["case"]
-    win = make_window(WindowSpec(c["n_frames"], c["n_heldout"], c["px"], c["px"], drift=c["drift"],
-                                 seed=c["window_seed"]))
-    w = torch.tensor(kaiming_resnet18_weights(seed=c["weights_seed"]), device="cuda")
-    out = binding.ekya_retrain(ctx, w, c["k"], to_dev(win["frames"], "bf16"),
+    c0 = onestep["common"]
+    case = next(e for e in onestep["cases"] if e["k"] == k and e["n"] == n)
+    w0 = kaiming_resnet18_weights(seed=c0["weights_seed"])
+    win = make_window(WindowSpec(n, c0["n_heldout"], c0["px"], c0["px"], drift=c0["drift"],
+                                 seed=c0["window_seed"]))
+    w = torch.tensor(w0, device="cuda")
+    out = binding.ekya_retrain(ctx, w, k, to_dev(win["frames"], "bf16"),
                                torch.tensor(win["labels"], device="cuda"),
                                to_dev(win["heldout_frames"], "bf16"),
                                torch.tensor(win["heldout_labels"], device="cuda"),
-                               c["frac"], c["epochs"], c["lr"], c["momentum"], c["batch"], c["seed"])
+                               1.0, 1, c0["lr"], c0["momentum"], n, c0["seed"], step_losses=True)
+    assert out["n_steps"] == 1
+    print(f"k={k} n={n}: loss {out['step_loss'][0]:.6f} oracle {case['loss']:.6f}")
+    assert abs(out["step_loss"][0] - case["loss"]) <= TOL["bf16"] * abs(case["loss"])
+    net = ResNet18(6)
+    G, W0 = net.unpack(as_np(w)), net.unpack(w0.astype(np.float64))
+    strict = {}
+    for nm, vals in case["full"].items():
+        ref = np.asarray(vals).reshape(W0[nm].shape)
+        dr = ref - W0[nm]
+        strict[nm] = float(np.abs((G[nm] - W0[nm]) - dr).max() / max(np.abs(dr).max(), 1e-30))
+    loose = {}
+    for nm, smp in case["sampled"].items():
+        pos = np.asarray(smp["pos"])
+        dg = G[nm].reshape(-1)[pos] - W0[nm].reshape(-1)[pos]
+        dr = np.asarray(smp["w1"]) - W0[nm].reshape(-1)[pos]
+        loose[nm] = (float(np.sqrt(np.mean((dg - dr) ** 2)) / max(smp["rms_update"], 1e-30)),
+                     float(np.abs(dg - dr).max() / max(smp["max_abs_update"], 1e-30)))
+    _gate_updates(strict, loose)
+    lo = len(STAGES) - k
+    for nm, _ in net.spec:
+        if net.stage_of[nm] < lo:
+            np.testing.assert_array_equal(G[nm], W0[nm])
+
+
+def _window_run(ctx, c):
+    import torch
+    from paper_2012_10557_amd import binding
+    win = make_window(WindowSpec(c["n_frames"], c["n_heldout"], c["px"], c["px"], drift=c["drift"],
+                                 seed=c["window_seed"], noise_std=c.get("noise", 0.3)))
+    w = torch.tensor(kaiming_resnet18_weights(seed=c["weights_seed"]), device="cuda")
+    return binding.ekya_retrain(ctx, w, c["k"], to_dev(win["frames"], "bf16"),
+                                torch.tensor(win["labels"], device="cuda"),
+                                to_dev(win["heldout_frames"], "bf16"),
+                                torch.tensor(win["heldout_labels"], device="cuda"),
+                                c["frac"], c["epochs"], c["lr"], c["momentum"], c["batch"], c["seed"])
+
+
+@pytest.mark.parametrize("name", ["retrain_224_k2.json", "retrain_224_k2_hard.json",
+                                  "retrain_224_k6.json"])
+def test_bf16_window_follows_oracle(ctx, name):
+    """Whole retraining jobs against stored oracle runs: the 2000-frame window
+    at 30% (600 frames), layer4+fc, 5 epochs of batch 64 -- with noise 0.3 it
+    saturates by epoch 3, with noise 3.0 and a drift it does not -- and a
+    full-depth job (every stage, batch 128, 256 frames, 2 epochs).  Held-out
+    accuracy after every epoch within one percentage point (4 of 400
+    frames); the first epoch's mean loss within 2e-2."""
+    with open(os.path.join(HERE, name)) as f:
+        g = json.load(f)
+    c = g["case"]
+    out = _window_run(ctx, c)
     assert out["n_train"] == g["n_train"]
-    print("gpu", out["heldout_acc"], out["epoch_loss"])
-    print("oracle", g["heldout_acc"], g["epoch_loss"])
-    assert abs(out["heldout_acc_final"] - g["heldout_acc"][-1]) <= 0.01
+    print("gpu   ", out["heldout_acc"], [round(x, 5) for x in out["epoch_loss"]])
+    print("oracle", g["heldout_acc"], [round(x, 5) for x in g["epoch_loss"]])
+    for a, b in zip(out["heldout_acc"], g["heldout_acc"]):
+        assert abs(a - b) <= 0.01 + 1e-6, (out["heldout_acc"], g["heldout_acc"])
     assert abs(out["epoch_loss"][0] - g["epoch_loss"][0]) <= TOL["bf16"] * abs(g["epoch_loss"][0])

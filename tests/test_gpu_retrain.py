@@ -67,9 +67,31 @@ def test_tiny_fc_only_fp32_matches_oracle(ctx):
 # ReLU input and max-pool top-2 gap of the trainable stages at least MARGIN
 # (in RMS units) away from its branch point -- no decision that fp32 rounding
 # could flip (see tests/margins.py).
-STRICT = [(64, 2, 16, 0.5, 8, 12, 1), (64, 3, 16, 0.5, 8, 62, 1), (224, 2, 2, 1.0, 2, 26, 0)]
+STRICT = [(64, 2, 16, 0.5, 8, 12, 1), (64, 3, 16, 0.5, 8, 62, 1), (224, 2, 2, 1.0, 2, 26, 0),
+          # every stage trainable: stem BatchNorm and max-pool backward, layer1-4
+          (32, 6, 8, 0.5, 4, 1, 1), (40, 6, 4, 0.5, 2, 9, 1), (48, 6, 6, 0.5, 3, 17, 0)]
 MARGIN = 1e-5
 SHUFFLE_SEED = 7
+
+
+# An adaptive bound is 3 x the probe's spread; a spread that large means the
+# run is dominated by branch decisions and the comparison says little.
+ADAPTIVE_CAP = 0.1
+
+
+def assert_adaptive(errs, probe, floor):
+    """Each tensor's error within the fixed floor, or else within 3 x the
+    probe's spread -- and then only if that bound stays within ADAPTIVE_CAP.
+    Every tensor's (error, bound) is printed."""
+    for n in errs:
+        bound = max(floor, 3 * probe[n])
+        print(f"  {n:40s} err {errs[n]:.3e}  bound {bound:.3e}  (probe {probe[n]:.3e})")
+    over = {n: e for n, e in errs.items() if e > floor}
+    wide = {n: 3 * probe[n] for n in over if 3 * probe[n] > ADAPTIVE_CAP}
+    assert not wide, f"error above {floor:.0e} where the probe's spread is too wide to bound it: {wide}"
+    bad = {n: (e, 3 * probe[n]) for n, e in over.items() if e > 3 * probe[n]}
+    assert not bad, bad
+    print(f"  {len(errs) - len(over)} of {len(errs)} tensors within the fixed {floor:.0e}")
 
 
 def _update_errors(got, ref, w0, names):
@@ -85,7 +107,8 @@ def _update_errors(got, ref, w0, names):
     return out
 
 
-@pytest.mark.parametrize("case", STRICT, ids=["64px-k2", "64px-k3", "224px-k2"])
+@pytest.mark.parametrize("case", STRICT, ids=["64px-k2", "64px-k3", "224px-k2", "32px-k6-b4",
+                                              "40px-k6-b2", "48px-k6-b3"])
 def test_fp32_one_step_matches_oracle_strict(ctx, case):
     """fp32, one SGD step of the last k stages with BatchNorm in train mode:
     every trainable tensor's update (parameters and running statistics) within
@@ -117,6 +140,8 @@ def test_fp32_one_step_matches_oracle_strict(ctx, case):
     got = as_np(w)
     errs = _update_errors(got, ref.weights, w0, names)
     worst = max(errs, key=errs.get)
+    print(f"{len(names)} tensors, worst {worst} {errs[worst]:.2e} (gate {TOL['f32']:.0e}), "
+          f"decision margin {margin:.2e}")
     assert errs[worst] <= TOL["f32"], (worst, errs[worst])
     G, W0 = net.unpack(got), net.unpack(w0.astype(np.float64))
     for n, _ in net.spec:
@@ -150,8 +175,7 @@ def test_deeper_fp32_retrain_matches_oracle(ctx, k):
     names = [n for n, _ in net.spec if net.stage_of[n] >= len(STAGES) - k]
     probe = probe_spread(w0, k, win, 0.5, 0.05, 0.9, 8, 7, ref.weights, names)
     errs = _update_errors(as_np(w), ref.weights, w0, names)
-    bad = {n: (e, probe[n]) for n, e in errs.items() if e > max(TOL["f32"], 3 * probe[n])}
-    assert not bad, bad
+    assert_adaptive(errs, probe, TOL["f32"])
 
 
 @pytest.mark.parametrize("prec", ["f32", "bf16"])
