@@ -45,6 +45,23 @@ ekya_status ekya_op_batchnorm_train(int precision, const void* z, long long M, i
                                     const float* gamma, const float* beta, float* running_mean,
                                     float* running_var, int relu, void* y, float* mean_out,
                                     float* invstd_out, void* stream);
+/* ekya_op_batchnorm_train for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): same arguments, kernels and results (bitwise), but it calls no
+ * hipMalloc / hipFree and does not synchronise -- the work is queued on
+ * `stream` and the caller synchronises.  Its scratch (partial sums, scale and
+ * shift) is one static device array per GPU of 512*2*2048 + 5*2048 floats
+ * (about 8.4 MB), enough for every M and C <= 2048; a request that would
+ * need more returns EKYA_ERR_INVALID_ARG.  The first call on a device looks
+ * up the array's address (make it outside graph capture).  Every call on one
+ * GPU shares that array, so calls that overlap on one GPU (different
+ * streams without ordering between them) race; nothing in it needs to start
+ * at zero. */
+ekya_status ekya_op_batchnorm_train_noalloc(int precision, const void* z, long long M, int C,
+                                            const float* gamma, const float* beta,
+                                            float* running_mean, float* running_var, int relu,
+                                            void* y, float* mean_out, float* invstd_out,
+                                            void* stream);
 /* Backward of ekya_op_batchnorm_train: g = dy * [y_relu > 0] (no mask when
  * y_relu is null); dbeta = sum g, dgamma = sum g*xhat,
  * dz = gamma*invstd/M*(M*g - dbeta - xhat*dgamma). */

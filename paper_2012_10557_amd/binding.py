@@ -97,6 +97,7 @@ _SIGS = {
     "ekya_op_conv2d_dgrad": (_I, [_I, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _I, _P, _P]),
     "ekya_op_conv2d_wgrad": (_I, [_I, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _I, _P, _P]),
     "ekya_op_batchnorm_train": (_I, [_I, _P, _LL, _I, _P, _P, _P, _P, _I, _P, _P, _P, _P]),
+    "ekya_op_batchnorm_train_noalloc": (_I, [_I, _P, _LL, _I, _P, _P, _P, _P, _I, _P, _P, _P, _P]),
     "ekya_op_batchnorm_backward": (_I, [_I, _P, _P, _P, _LL, _I, _P, _P, _P, _P, _P, _P, _P]),
     "ekya_op_maxpool": (_I, [_I, _P, _I, _I, _I, _I, _P, _P, _P]),
     "ekya_op_maxpool_backward": (_I, [_I, _P, _P, _I, _I, _I, _I, _P, _P]),
@@ -372,6 +373,23 @@ def ekya_op_batchnorm_train(z, gamma, beta, running_mean=None, running_var=None,
                                        _dev(beta, torch.float32), _dev(running_mean, torch.float32),
                                        _dev(running_var, torch.float32), int(relu), _dev(y),
                                        _dev(mean), _dev(invstd), _stream()))
+    return y, mean, invstd
+
+
+def ekya_op_batchnorm_train_noalloc(z, gamma, beta, running_mean=None, running_var=None,
+                                    relu=False, y=None, mean=None, invstd=None, stream=None):
+    """Asynchronous on the stream; outputs may be passed in (no allocation in the library)."""
+    torch = _torch()
+    C = z.shape[-1]
+    M = z.numel() // C
+    y = torch.empty_like(z) if y is None else y
+    mean = torch.empty(C, dtype=torch.float32, device=z.device) if mean is None else mean
+    invstd = torch.empty_like(mean) if invstd is None else invstd
+    _op(load().ekya_op_batchnorm_train_noalloc(_precision(z), _dev(z), M, C, _dev(gamma, torch.float32),
+                                               _dev(beta, torch.float32),
+                                               _dev(running_mean, torch.float32),
+                                               _dev(running_var, torch.float32), int(relu), _dev(y),
+                                               _dev(mean), _dev(invstd), _stream(stream)))
     return y, mean, invstd
 
 

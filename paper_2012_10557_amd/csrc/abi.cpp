@@ -5,6 +5,7 @@
 #include <cstdio>
 #include <cstring>
 #include <iterator>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -423,6 +424,67 @@ ekya_status ekya_op_batchnorm_train(int precision, const void* z, long long M, i
     e = ekya::bn_train_forward(precision, z, M, C, gamma, beta, running_mean, running_var,
                                mean_out, invstd_out, ss, ss + C, nullptr, relu, y, part, st);
   return sync_status(st, e);
+}
+
+// ---------------------------------------------- BatchNorm without allocation
+// Device scratch of ekya_op_batchnorm_train_noalloc: the BatchNorm partial
+// sums (bn_partials_floats(M, C), largest at 512 chunks of 2 x 2048
+// channels plus 3 x 2048) followed by the per-channel scale and shift
+// (2 x 2048).  Each GPU the library runs on holds its own copy until the
+// process ends.  In host code only the address from hipGetSymbolAddress is
+// used (the array's name is a host-side stand-in).
+constexpr size_t kBnScratchFloats = 512 * 2 * 2048 + 3 * 2048 + 2 * 2048;
+static __device__ __align__(256) float scratch[kBnScratchFloats];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+float* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of `scratch` on the current device, looked up once per device.
+hipError_t scratch_on_current_device(float** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch_ptr[dev] = reinterpret_cast<float*>(p);
+  }
+  *out = g_scratch_ptr[dev];
+  return hipSuccess;
+}
+
+}  // namespace
+
+ekya_status ekya_op_batchnorm_train_noalloc(int precision, const void* z, long long M, int C,
+                                            const float* gamma, const float* beta,
+                                            float* running_mean, float* running_var, int relu,
+                                            void* y, float* mean_out, float* invstd_out,
+                                            void* stream) {
+  if (!valid_precision(precision) || !z || !gamma || !beta || !y || !mean_out || !invstd_out ||
+      M < 1 || !chan_ok(precision, C, false) || C > 2048 ||
+      (running_mean == nullptr) != (running_var == nullptr))
+    return fail(nullptr, EKYA_ERR_INVALID_ARG, "invalid batchnorm_train_noalloc arguments");
+  const size_t part = ekya::bn_partials_floats(M, C);
+  if (part + 2 * (size_t)C > kBnScratchFloats)
+    return fail(nullptr, EKYA_ERR_INVALID_ARG,
+                "batchnorm_train_noalloc: M and C need more scratch than the static " +
+                    std::to_string(kBnScratchFloats) + " floats");
+  float* sp = nullptr;
+  hipError_t e = scratch_on_current_device(&sp);
+  if (e != hipSuccess) return hip_status(e);
+  hipStream_t st = (hipStream_t)stream;
+  // every partial is written before it is read, so nothing needs clearing
+  float* ss = sp + part;
+  e = ekya::bn_train_forward(precision, z, M, C, gamma, beta, running_mean, running_var, mean_out,
+                             invstd_out, ss, ss + C, nullptr, relu, y, sp, st);
+  if (e == hipSuccess) e = hipGetLastError();
+  return hip_status(e);
 }
 
 ekya_status ekya_op_batchnorm_backward(int precision, const void* dy, const void* y_relu,
