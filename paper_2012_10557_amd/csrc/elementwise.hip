@@ -1630,7 +1630,16 @@ hipError_t by_type(int dt, F&& f) {
 
 }  // namespace
 
-size_t bn_partials_floats(long long M, int C) { return (size_t)bn_chunks(M) * 2 * C + 3 * C; }
+// Room for every chunking that writes partials of an M x C BatchNorm: the
+// large-M path (bn_chunks), and -- where the two-launch path applies (at most
+// BN_FOLD_MAX_CHUNKS chunks of BN_FOLD_ROWS rows) -- the 128-row chunks of its
+// partial kernel and the 64-row chunks GEMM epilogues and the classifier-head
+// backward leave; plus the per-channel coefficients of the large-M backward.
+size_t bn_partials_floats(long long M, int C) {
+  long long ch = bn_chunks(M);
+  if (bn_fold_ok(M, C)) ch = std::max(ch, cdivl(M, 64));
+  return (size_t)ch * 2 * C + 3 * C;
+}
 
 hipError_t bn_train_stats(int dt, const void* z, long long M, int C, const float* gamma,
                           const float* beta, float* rm, float* rv, float* mean, float* invstd,

@@ -9,13 +9,19 @@ trainable, BatchNorm in train mode).
 What is gated at the fixed bf16 tolerance 2e-2: the step loss, the BatchNorm
 running statistics (batch statistics of the activations) and the classifier
 update.  Convolution and BatchNorm-affine updates are weight gradients summed
-over thousands of pixels whose operands are all stored in bf16; rounding the
-operands alone moves them by several percent of the tensor's largest update,
-and ReLU / max-pool branch decisions taken within rounding of their branch
-point move single channels further.  They are gated by the root-mean-square
-error of the update (sampled positions) within BF16_GRAD_RMS of its
-root-mean-square, and printed with their largest error.  Stored runs come
-from tests/golden/make_*_golden.py (oracle only)."""
+over thousands of pixels whose operands (activations and their gradients)
+are stored in bf16; the BatchNorm backward projects each channel's gradient
+onto what is left after removing its mean and its correlation with the
+normalised input, so these sums are small residues of large terms, and the
+rounding of the stored operands alone moves them by 5-50% (root mean square,
+largest in the stem and layer1 after a full-depth backward pass).  An
+independent implementation that stores the same tensors in bf16
+(tests/torch_probe.py, torch on the CPU) shows the same errors against the
+fp64 oracle, and agrees with the oracle to 0.4% when it keeps fp32.  Each of
+these tensors is therefore gated by its root-mean-square update error within
+max(2e-2, 1.5 x that probe's error on the same positions), and every error is
+printed.  Stored runs come from tests/golden/make_*_golden.py (oracle
+only)."""
 import gzip
 import json
 import os
@@ -32,7 +38,8 @@ pytestmark = pytest.mark.gpu
 
 HERE = os.path.join(os.path.dirname(__file__), "golden")
 GOLDEN = os.path.join(HERE, "retrain_224_k2.json")
-BF16_GRAD_RMS = 0.1
+BF16_GRAD_RMS = 2e-2
+PROBE_FACTOR = 1.5
 
 
 @pytest.fixture(scope="module")
@@ -56,15 +63,25 @@ def _rms_errors(got, ref, w0, names):
     return out
 
 
-def _gate_updates(strict, loose):
-    """strict: name -> error (fixed 2e-2); loose: name -> (rms err, max err)."""
+def _probe_weights(w0, k, frames_bf16, labels, n, lr, mu, seed):
+    """Weights after the same step from the bf16-storage torch probe."""
+    from tests.torch_probe import torch_retrain
+    win = {"frames": frames_bf16, "labels": labels}
+    return torch_retrain(w0, k, win, 1.0, lr, mu, n, seed, None, True, 1)[0]
+
+
+def _gate_updates(strict, loose, probe):
+    """strict: name -> error (fixed 2e-2); loose: name -> (rms err, max err);
+    probe: name -> the bf16 probe's rms error on the same positions."""
     for n, e in strict.items():
         print(f"  {n:40s} err {e:.3e}  (gate {TOL['bf16']:.0e})")
+    bound = {n: max(BF16_GRAD_RMS, PROBE_FACTOR * probe[n]) for n in loose}
     for n, (r, m) in loose.items():
-        print(f"  {n:40s} rms err {r:.3e}  (gate {BF16_GRAD_RMS:.0e})  max err {m:.3e}")
+        print(f"  {n:40s} rms err {r:.3e}  bound {bound[n]:.3e}  (bf16 probe {probe[n]:.3e})  "
+              f"max err {m:.3e}")
     bad = {n: e for n, e in strict.items() if e > TOL["bf16"]}
     assert not bad, bad
-    bad = {n: r for n, (r, _) in loose.items() if r > BF16_GRAD_RMS}
+    bad = {n: (r, bound[n]) for n, (r, _) in loose.items() if r > bound[n]}
     assert not bad, bad
 
 
@@ -97,8 +114,14 @@ def test_bf16_one_step_224_matches_oracle(ctx, k, n):
     got = as_np(w)
     strict_names = [nm for nm in names if nm.startswith("fc.") or net.is_running_stat(nm)]
     strict = {nm: e for nm, e in _update_errors(got, ref.weights, w0, strict_names).items()}
-    loose = _rms_errors(got, ref.weights, w0, [nm for nm in names if nm not in strict_names])
-    _gate_updates(strict, loose)
+    loose_names = [nm for nm in names if nm not in strict_names]
+    loose = _rms_errors(got, ref.weights, w0, loose_names)
+    if loose_names:
+        pw = _probe_weights(w0, k, fr, win["labels"], n, lr, 0.9, 0)
+        probe = {nm: r for nm, (r, _) in _rms_errors(pw, ref.weights, w0, loose_names).items()}
+    else:
+        probe = {}
+    _gate_updates(strict, loose, probe)
     G, W0 = net.unpack(got), net.unpack(w0.astype(np.float64))
     for nm, _ in net.spec:
         if net.stage_of[nm] < lo:
@@ -144,14 +167,19 @@ def test_bf16_one_step_at_depth_matches_stored_oracle(ctx, onestep, k, n):
         ref = np.asarray(vals).reshape(W0[nm].shape)
         dr = ref - W0[nm]
         strict[nm] = float(np.abs((G[nm] - W0[nm]) - dr).max() / max(np.abs(dr).max(), 1e-30))
-    loose = {}
+    frames = rounded(win["frames"], "bf16")
+    PW = net.unpack(_probe_weights(w0, k, frames, win["labels"], n, c0["lr"], c0["momentum"],
+                                   c0["seed"]))
+    loose, probe = {}, {}
     for nm, smp in case["sampled"].items():
         pos = np.asarray(smp["pos"])
-        dg = G[nm].reshape(-1)[pos] - W0[nm].reshape(-1)[pos]
         dr = np.asarray(smp["w1"]) - W0[nm].reshape(-1)[pos]
+        dg = G[nm].reshape(-1)[pos] - W0[nm].reshape(-1)[pos]
+        dp = PW[nm].reshape(-1)[pos] - W0[nm].reshape(-1)[pos]
         loose[nm] = (float(np.sqrt(np.mean((dg - dr) ** 2)) / max(smp["rms_update"], 1e-30)),
                      float(np.abs(dg - dr).max() / max(smp["max_abs_update"], 1e-30)))
-    _gate_updates(strict, loose)
+        probe[nm] = float(np.sqrt(np.mean((dp - dr) ** 2)) / max(smp["rms_update"], 1e-30))
+    _gate_updates(strict, loose, probe)
     lo = len(STAGES) - k
     for nm, _ in net.spec:
         if net.stage_of[nm] < lo:
