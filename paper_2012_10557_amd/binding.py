@@ -66,6 +66,31 @@ class ProfileResult(ctypes.Structure):
                 ("heldout_acc_final", ctypes.c_float)]
 
 
+class Curve(ctypes.Structure):
+    _fields_ = [("b0", ctypes.c_double), ("b1", ctypes.c_double), ("b2", ctypes.c_double),
+                ("rss", ctypes.c_double)]
+
+
+class InferCfg(ctypes.Structure):
+    _fields_ = [("cost", ctypes.c_double), ("factor", ctypes.c_double)]
+
+
+class TrainCfg(ctypes.Structure):
+    _fields_ = [("acc_after", ctypes.c_double), ("gpu_seconds", ctypes.c_double)]
+
+
+class VideoIn(ctypes.Structure):
+    _fields_ = [("acc_now", ctypes.c_double), ("infer", ctypes.POINTER(InferCfg)),
+                ("n_infer", ctypes.c_int), ("train", ctypes.POINTER(TrainCfg)),
+                ("n_train", ctypes.c_int)]
+
+
+class ScheduleOut(ctypes.Structure):
+    _fields_ = [("alloc", ctypes.POINTER(ctypes.c_double)), ("infer_choice", ctypes.POINTER(ctypes.c_int)),
+                ("train_choice", ctypes.POINTER(ctypes.c_int)),
+                ("video_accuracy", ctypes.POINTER(ctypes.c_double)), ("accuracy", ctypes.c_double)]
+
+
 _P = ctypes.c_void_p
 _I = ctypes.c_int
 _LL = ctypes.c_longlong
@@ -93,6 +118,14 @@ _SIGS = {
                                 ctypes.POINTER(ctypes.c_double)]),
     "ekya_training_subset": (_I, [_I, ctypes.c_double, ctypes.c_uint64, _P, _I]),
     "ekya_epoch_order": (_I, [_I, ctypes.c_uint64, _I, _P]),
+    "ekya_nnls": (_I, [_P, _I, _I, _P, _P, _P]),
+    "ekya_fit_accuracy_curve": (_I, [_P, _P, _I, ctypes.POINTER(Curve)]),
+    "ekya_curve_accuracy": (ctypes.c_double, [ctypes.POINTER(Curve), ctypes.c_double]),
+    "ekya_extrapolate": (_I, [ctypes.POINTER(ProfileCfg), ctypes.POINTER(ProfileResult), _I, _I,
+                              ctypes.POINTER(Curve), ctypes.POINTER(ctypes.c_double),
+                              ctypes.POINTER(ctypes.c_double)]),
+    "ekya_thief_schedule": (_I, [ctypes.POINTER(VideoIn), _I, ctypes.c_double, ctypes.c_double,
+                                 ctypes.c_double, ctypes.c_double, ctypes.POINTER(ScheduleOut)]),
     "ekya_op_conv2d": (_I, [_I, _P, _I, _I, _I, _I, _P, _I, _I, _I, _I, _I, _P, _P]),
     "ekya_op_conv2d_dgrad": (_I, [_I, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _I, _P, _P]),
     "ekya_op_conv2d_wgrad": (_I, [_I, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _I, _P, _P]),
@@ -488,3 +521,65 @@ def ekya_op_resize(frames, r: int):
     out = torch.empty(n, r, r, 3, dtype=frames.dtype, device=frames.device)
     _op(load().ekya_op_resize(_precision(frames), _dev(frames), n, H, W, r, _dev(out), _stream()))
     return out
+
+
+# ---------------------------------------------------- scheduling layer (host)
+def ekya_nnls(A, b):
+    """(x, ||Ax - b||) of min ||Ax - b||, x >= 0 (numpy arrays)."""
+    import numpy as np
+    A = np.ascontiguousarray(A, dtype=np.float64)
+    b = np.ascontiguousarray(b, dtype=np.float64)
+    m, n = A.shape
+    x = np.zeros(n)
+    r = ctypes.c_double()
+    _op(load().ekya_nnls(A.ctypes.data, m, n, b.ctypes.data, x.ctypes.data, ctypes.byref(r)))
+    return x, r.value
+
+
+def ekya_fit_accuracy_curve(x, acc):
+    import numpy as np
+    x = np.ascontiguousarray(x, dtype=np.float64)
+    acc = np.ascontiguousarray(acc, dtype=np.float64)
+    c = Curve()
+    _op(load().ekya_fit_accuracy_curve(x.ctypes.data, acc.ctypes.data, x.size, ctypes.byref(c)))
+    return c
+
+
+def ekya_curve_accuracy(c, x: float) -> float:
+    return float(load().ekya_curve_accuracy(ctypes.byref(c), x))
+
+
+def ekya_extrapolate(cfg: dict, result: dict, n_frames: int, epochs_target: int):
+    """(curve, accuracy, gpu_seconds) for a candidate dict and its ekya_profile result dict."""
+    pc = ProfileCfg(cfg["k"], cfg["subsample_frac"], cfg["epochs"], cfg.get("lr", 0.01),
+                    cfg.get("momentum", 0.9), cfg.get("batch", 64), cfg.get("seed", 0))
+    pr = ProfileResult()
+    pr.status = result.get("status", 0)
+    pr.n_train = result["n_train"]
+    for e in range(cfg["epochs"]):
+        pr.heldout_acc[e] = result["heldout_acc"][e]
+        pr.epoch_seconds[e] = result["epoch_seconds"][e]
+    c = Curve()
+    acc, sec = ctypes.c_double(), ctypes.c_double()
+    _op(load().ekya_extrapolate(ctypes.byref(pc), ctypes.byref(pr), n_frames, epochs_target,
+                                ctypes.byref(c), ctypes.byref(acc), ctypes.byref(sec)))
+    return c, acc.value, sec.value
+
+
+def ekya_thief_schedule(videos, n_gpus: float, delta: float, window_s: float, a_min: float) -> dict:
+    """videos: list of dicts {acc_now, infer: [(cost, factor)], train: [(acc_after, gpu_seconds)]}."""
+    keep = []
+    arr = (VideoIn * len(videos))()
+    for i, v in enumerate(videos):
+        inf = (InferCfg * len(v["infer"]))(*[InferCfg(c, f) for c, f in v["infer"]])
+        tr = (TrainCfg * max(1, len(v["train"])))(*[TrainCfg(a, g) for a, g in v["train"]])
+        keep += [inf, tr]
+        arr[i] = VideoIn(v["acc_now"], inf, len(v["infer"]), tr, len(v["train"]))
+    nv = len(videos)
+    alloc = (ctypes.c_double * (2 * nv))()
+    ic, tc = (ctypes.c_int * nv)(), (ctypes.c_int * nv)()
+    va = (ctypes.c_double * nv)()
+    out = ScheduleOut(alloc, ic, tc, va, 0.0)
+    _op(load().ekya_thief_schedule(arr, nv, n_gpus, delta, window_s, a_min, ctypes.byref(out)))
+    return {"alloc": list(alloc), "infer_choice": list(ic), "train_choice": list(tc),
+            "video_accuracy": list(va), "accuracy": out.accuracy}

@@ -15,7 +15,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libekya.so")
-SOURCES = ["conv.hip", "elementwise.hip", "net.cpp", "rng.cpp", "runtime.cpp", "abi.cpp"]
+SOURCES = ["conv.hip", "elementwise.hip", "net.cpp", "rng.cpp", "runtime.cpp", "curve.cpp", "sched.cpp",
+           "abi.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-result",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]

@@ -12,6 +12,8 @@
 
 #include "../../include/ekya.h"
 #include "../../include/ekya_ops.h"
+#include "../../include/ekya_sched.h"
+#include "curve.hpp"
 #include "rng.hpp"
 #include "runtime.hpp"
 
@@ -575,6 +577,109 @@ ekya_status ekya_op_resize(int precision, const void* frames, int n, int H, int 
     return fail(nullptr, EKYA_ERR_INVALID_ARG, "invalid resize arguments");
   hipStream_t st = (hipStream_t)stream;
   return sync_status(st, ekya::resize_to_padded(precision, frames, n, H, W, r, 3, out, st));
+}
+
+}  // extern "C"
+
+// ------------------------------------------------------ scheduling layer
+extern "C" {
+
+ekya_status ekya_nnls(const double* A, int m, int n, const double* b, double* x, double* rnorm) {
+  if (!A || !b || !x || m < 1 || n < 1 || m > 4096 || n > 4096 || (long long)m * n > (1LL << 22))
+    return fail(nullptr, EKYA_ERR_INVALID_ARG, "invalid nnls arguments");
+  for (long long i = 0; i < (long long)m * n; ++i)
+    if (!std::isfinite(A[i])) return fail(nullptr, EKYA_ERR_INVALID_ARG, "nnls: A is not finite");
+  for (int i = 0; i < m; ++i)
+    if (!std::isfinite(b[i])) return fail(nullptr, EKYA_ERR_INVALID_ARG, "nnls: b is not finite");
+  if (!ekya::nnls(A, m, n, b, x, rnorm))
+    return fail(nullptr, EKYA_ERR_UNSUPPORTED, "nnls: singular least-squares subproblem");
+  return EKYA_OK;
+}
+
+ekya_status ekya_fit_accuracy_curve(const double* x, const double* acc, int n, ekya_curve* out) {
+  if (!x || !acc || !out || n < 1 || n > 4096)
+    return fail(nullptr, EKYA_ERR_INVALID_ARG, "invalid curve-fit arguments");
+  for (int i = 0; i < n; ++i)
+    if (!(x[i] > 0.0) || !std::isfinite(x[i]) || !(acc[i] >= 0.0 && acc[i] <= 1.0))
+      return fail(nullptr, EKYA_ERR_INVALID_ARG, "curve fit: need x > 0 and accuracy in [0, 1]");
+  ekya::Curve c;
+  if (!ekya::fit_accuracy_curve(x, acc, n, &c))
+    return fail(nullptr, EKYA_ERR_INVALID_ARG, "curve fit failed");
+  *out = ekya_curve{c.b0, c.b1, c.b2, c.rss};
+  return EKYA_OK;
+}
+
+double ekya_curve_accuracy(const ekya_curve* c, double x) {
+  if (!c) return 0.0;
+  ekya::Curve k;
+  k.b0 = c->b0;
+  k.b1 = c->b1;
+  k.b2 = c->b2;
+  return ekya::curve_accuracy(k, x);
+}
+
+ekya_status ekya_extrapolate(const ekya_profile_cfg* cfg, const ekya_profile_result* res,
+                             int n_frames, int epochs_target, ekya_curve* curve, double* acc_out,
+                             double* gpu_seconds_out) {
+  if (!cfg || !res || n_frames < 1 || epochs_target < 1 || cfg->epochs < 1 ||
+      cfg->epochs > EKYA_MAX_EPOCHS || cfg->batch < 1 || res->n_train < 1 ||
+      res->n_train > n_frames || res->status != EKYA_OK)
+    return fail(nullptr, EKYA_ERR_INVALID_ARG, "invalid extrapolation arguments");
+  const double f = (double)res->n_train / n_frames;
+  double xs[EKYA_MAX_EPOCHS], acc[EKYA_MAX_EPOCHS], sec = 0.0;
+  for (int e = 0; e < cfg->epochs; ++e) {
+    xs[e] = (e + 1) * f;
+    acc[e] = res->heldout_acc[e];
+    sec += res->epoch_seconds[e];
+  }
+  ekya_curve c;
+  if (ekya_status s = ekya_fit_accuracy_curve(xs, acc, cfg->epochs, &c)) return s;
+  const long long steps_sub = (res->n_train + cfg->batch - 1) / cfg->batch;
+  const long long steps_full = ((long long)n_frames + cfg->batch - 1) / cfg->batch;
+  if (curve) *curve = c;
+  if (acc_out) *acc_out = ekya_curve_accuracy(&c, (double)epochs_target);
+  if (gpu_seconds_out)
+    *gpu_seconds_out = sec / cfg->epochs * (double)steps_full / (double)steps_sub * epochs_target;
+  return EKYA_OK;
+}
+
+ekya_status ekya_thief_schedule(const ekya_video* videos, int n_videos, double n_gpus, double delta,
+                                double window_s, double a_min, ekya_schedule* out) {
+  if (!videos || !out || !out->alloc || !out->infer_choice || !out->train_choice ||
+      !out->video_accuracy || n_videos < 1 || n_videos > 1024 || !(delta > 0.0) ||
+      !(n_gpus > 0.0) || !(window_s > 0.0) || !std::isfinite(a_min))
+    return fail(nullptr, EKYA_ERR_INVALID_ARG, "invalid scheduler arguments");
+  const double qd = n_gpus / delta;
+  const long long quanta = std::llround(qd);
+  if (std::fabs(qd - (double)quanta) > 1e-9 * std::max(1.0, qd) || quanta < 1 || quanta > 4096)
+    return fail(nullptr, EKYA_ERR_INVALID_ARG, "n_gpus must be a whole number (1..4096) of quanta");
+  std::vector<ekya::SchedVideo> vs(n_videos);
+  for (int v = 0; v < n_videos; ++v) {
+    const ekya_video& in = videos[v];
+    if (in.n_infer < 1 || !in.infer || in.n_train < 0 || (in.n_train > 0 && !in.train) ||
+        !std::isfinite(in.acc_now))
+      return fail(nullptr, EKYA_ERR_INVALID_ARG, "scheduler: a stream needs inference configurations");
+    vs[v].acc_now = in.acc_now;
+    for (int i = 0; i < in.n_infer; ++i) {
+      if (!(in.infer[i].cost > 0.0) || !std::isfinite(in.infer[i].factor))
+        return fail(nullptr, EKYA_ERR_INVALID_ARG, "scheduler: inference cost must be > 0");
+      vs[v].infer.push_back({in.infer[i].cost, in.infer[i].factor});
+    }
+    for (int i = 0; i < in.n_train; ++i) {
+      if (!(in.train[i].gpu_seconds >= 0.0) || !std::isfinite(in.train[i].acc_after))
+        return fail(nullptr, EKYA_ERR_INVALID_ARG, "scheduler: retraining cost must be >= 0");
+      vs[v].train.push_back({in.train[i].acc_after, in.train[i].gpu_seconds});
+    }
+  }
+  const ekya::SchedResult r = ekya::thief_schedule(vs, (int)quanta, delta, window_s, a_min);
+  for (int j = 0; j < 2 * n_videos; ++j) out->alloc[j] = r.quanta[j] * delta;
+  for (int v = 0; v < n_videos; ++v) {
+    out->infer_choice[v] = r.infer_choice[v];
+    out->train_choice[v] = r.train_choice[v];
+    out->video_accuracy[v] = r.video_accuracy[v];
+  }
+  out->accuracy = r.accuracy;
+  return EKYA_OK;
 }
 
 }  // extern "C"

@@ -105,3 +105,36 @@ def test_one_candidate_per_depth_follows_oracle(sweeps):
         assert got["n_train"] == ref["n_train"]
         assert abs(got["epoch_loss"][0] - ref["epoch_loss"][0]) <= TOL["bf16"] * abs(ref["epoch_loss"][0])
         assert abs(got["heldout_acc"][0] - ref["heldout_acc"][0]) <= 0.01 + 1e-6
+
+
+def test_profiles_feed_extrapolation_and_the_scheduler(sweeps):
+    """The micro-profiler's output drives the scheduling layer (sections 4.2
+    and 4.3): every 2-epoch candidate's per-epoch accuracies and times are
+    extrapolated to a 10-epoch retraining on the whole window (library equal
+    to the oracle on the same float32 numbers), and the extrapolations are
+    the retraining configurations of two streams that the thief scheduler
+    splits 1 GPU between (library equal to the oracle)."""
+    from oracle import curve, scheduler as S
+    from paper_2012_10557_amd import binding
+    f32 = lambda v: [float(np.float32(x)) for x in v]
+    train = []
+    for cfg, res in zip(sweep_configs(), sweeps["sequential"]):
+        if cfg["epochs"] != 2:
+            continue
+        c, acc, sec = binding.ekya_extrapolate(cfg, res, 4000, 10)
+        co, acco, seco = curve.extrapolate(f32(res["heldout_acc"]), f32(res["epoch_seconds"]),
+                                           res["n_train"], 4000, cfg["batch"], 10)
+        print(f"k={cfg['k']} {cfg['subsample_frac']:.0%}: acc {res['heldout_acc']} -> {acc:.3f} "
+              f"after 10 epochs on the window, {sec * 1e3:.1f} GPU-ms")
+        assert abs(acc - acco) < 1e-7 and abs(sec - seco) <= 1e-9 * seco
+        assert 0.0 <= acc <= 1.0 and sec > 0.0
+        train.append((acc, sec))
+    videos = [{"acc_now": 0.4, "infer": [(0.5, 1.0), (0.25, 0.8)], "train": train},
+              {"acc_now": 0.6, "infer": [(0.5, 1.0), (0.25, 0.8)], "train": train[::-1]}]
+    got = binding.ekya_thief_schedule(videos, 1.0, 0.05, 1.0, 0.3)
+    ref = S.thief_schedule([S.Video(v["acc_now"], [S.InferConfig(c, q) for c, q in v["infer"]],
+                                    [S.TrainConfig(a, g) for a, g in v["train"]]) for v in videos],
+                           1.0, 0.05, 1.0, 0.3)
+    print("schedule", got)
+    assert got["alloc"] == ref.alloc and got["train_choice"] == ref.train_choice
+    assert abs(got["accuracy"] - ref.accuracy) < 1e-15
