@@ -353,6 +353,71 @@ def run_extras(binding, torch, d, w0):
                            "workload": "3600 frames at 224 px beside layer3+ retraining "
                                        "(10% of 3600 frames, 5 epochs, batch 128)"}
     log(f"joint: {out['joint_window']}")
+
+    # the same joint window on complementary CU ranges, the GPU split in
+    # steps of 0.1 (the scheduler's quantum): inference on [0, s), the
+    # retraining job's streams on [s, 1); each alone on its range, then both
+    def retrain_on(stream):
+        t = time.perf_counter()
+        binding.ekya_retrain(ctx, w0.clone(), 3, r3, l3, d["hf"], d["hl"], 0.1, 5, 0.01, 0.9, 128,
+                             0, stream=stream)
+        return time.perf_counter() - t
+
+    def infer_on(stream):
+        t = time.perf_counter()
+        binding.ekya_infer(ictx, w0, inf, 224, labels_out=lab, stream=stream)
+        stream.synchronize()
+        return inf.shape[0] / (time.perf_counter() - t)
+
+    shares = []
+    for i in range(1, 10):
+        s = i / 10
+        si, st = binding.CuStream(0, 0.0, s), binding.CuStream(0, s, 1.0 - s)
+        binding.ekya_set_cu_partition(ctx, s, 1.0 - s)
+        infer_on(si)
+        rate_alone = infer_on(si)
+        retrain_on(st)
+        wall_alone = retrain_on(st)
+        box = {}
+        th = threading.Thread(target=lambda: box.update(t=retrain_on(st)))
+        th.start()
+        rate_joint = infer_on(si)
+        th.join()
+        shares.append({"infer_share": s, "infer_cus": si.cu_count(), "retrain_cus": st.cu_count(),
+                       "infer_img_per_s_alone": round(rate_alone, 1),
+                       "infer_img_per_s_joint": round(rate_joint, 1),
+                       "retrain_wall_s_alone": round(wall_alone, 4),
+                       "retrain_wall_s_joint": round(box["t"], 4)})
+        si.destroy()
+        st.destroy()
+        log(f"cu share: {shares[-1]}")
+    binding.ekya_set_cu_partition(ctx, 0.0, 1.0)
+    out["cu_shares"] = {"workload": out["joint_window"]["workload"], "splits": shares}
+
+    # hot reload: one load of the model (prepared inference weights) and the
+    # cost of publishing a checkpoint after every epoch of the retraining job
+    model = binding.ekya_model_create(0, 6, binding.EKYA_BF16)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    with torch.cuda.stream(s_tr):
+        binding.ekya_model_load(model, w0, stream=s_tr)
+        e0.record(s_tr)
+        for _ in range(10):
+            binding.ekya_model_load(model, w0, stream=s_tr)
+        e1.record(s_tr)
+    s_tr.synchronize()
+    load_ms = e0.elapsed_time(e1) / 10
+    retrain_on(s_tr)
+    plain = min(retrain_on(s_tr) for _ in range(3))
+    binding.ekya_set_checkpoint(ctx, model, 1)
+    published = min(retrain_on(s_tr) for _ in range(3))
+    binding.ekya_set_checkpoint(ctx, None, 0)
+    out["hot_reload"] = {"model_load_ms": round(load_ms, 4),
+                         "retrain_wall_s": round(plain, 4),
+                         "retrain_wall_s_checkpoint_every_epoch": round(published, 4),
+                         "workload": "layer3+ retraining (10% of 3600 frames, 5 epochs, batch 128); "
+                                     "bf16 ResNet18 weights"}
+    log(f"hot reload: {out['hot_reload']}")
+    binding.ekya_model_destroy(model)
     binding.ekya_destroy(ictx)
     binding.ekya_destroy(ctx)
     return out

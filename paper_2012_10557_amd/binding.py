@@ -126,6 +126,19 @@ _SIGS = {
                               ctypes.POINTER(ctypes.c_double)]),
     "ekya_thief_schedule": (_I, [ctypes.POINTER(VideoIn), _I, ctypes.c_double, ctypes.c_double,
                                  ctypes.c_double, ctypes.c_double, ctypes.POINTER(ScheduleOut)]),
+    "ekya_partition_mask": (_I, [_I, _I, _I, ctypes.c_double, ctypes.c_double, _P, _I]),
+    "ekya_stream_create": (_I, [_I, ctypes.c_double, ctypes.c_double, ctypes.POINTER(_P)]),
+    "ekya_stream_destroy": (_I, [_P]),
+    "ekya_stream_cu_count": (_I, [_P]),
+    "ekya_set_cu_partition": (_I, [_P, ctypes.c_double, ctypes.c_double]),
+    "ekya_cu_ids": (_I, [_I, _P, _P]),
+    "ekya_model_create": (_I, [ctypes.POINTER(_P), _I, _I, _I]),
+    "ekya_model_destroy": (None, [_P]),
+    "ekya_model_load": (_I, [_P, _P, _P, ctypes.POINTER(ctypes.c_uint64)]),
+    "ekya_model_export": (_I, [_P, _P, _P, ctypes.POINTER(ctypes.c_uint64)]),
+    "ekya_model_version": (ctypes.c_uint64, [_P]),
+    "ekya_infer_model": (_I, [_P, _P, _P, _I, _I, _I, _I, _P, _P, ctypes.POINTER(ctypes.c_uint64)]),
+    "ekya_set_checkpoint": (_I, [_P, _P, _I]),
     "ekya_op_conv2d": (_I, [_I, _P, _I, _I, _I, _I, _P, _I, _I, _I, _I, _I, _P, _P]),
     "ekya_op_conv2d_dgrad": (_I, [_I, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _I, _P, _P]),
     "ekya_op_conv2d_wgrad": (_I, [_I, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _I, _P, _P]),
@@ -356,6 +369,108 @@ def ekya_infer(ctx, weights, frames, resolution: int, labels_out=None, stream=No
                         _precision(frames), _dev(labels_out, torch.int32), _stream(stream))
     _check(st, ctx)
     return labels_out
+
+
+# ------------------------------------------------- CU shares and hot reload
+def ekya_partition_mask(n_cu: int, n_xcd: int, n_se: int, cu_begin: float, cu_share: float):
+    """(CU count, mask words) of a CU range (host only); raises on invalid input."""
+    import numpy as np
+    words = np.zeros(max(1, (n_cu + 31) // 32), dtype=np.uint32)
+    n = load().ekya_partition_mask(n_cu, n_xcd, n_se, cu_begin, cu_share, words.ctypes.data,
+                                   words.size)
+    if n < 0:
+        raise ValueError("invalid CU range")
+    return n, words
+
+
+class CuStream:
+    """A HIP stream restricted to a CU range; .stream is a torch ExternalStream."""
+
+    def __init__(self, device: int, cu_begin: float, cu_share: float):
+        torch = _torch()
+        h = ctypes.c_void_p()
+        _check(load().ekya_stream_create(device, cu_begin, cu_share, ctypes.byref(h)))
+        self.handle = h
+        self.stream = torch.cuda.ExternalStream(h.value, device=torch.device("cuda", device))
+
+    @property
+    def cuda_stream(self):
+        return self.handle.value
+
+    def synchronize(self):
+        self.stream.synchronize()
+
+    def cu_count(self) -> int:
+        return int(load().ekya_stream_cu_count(self.handle))
+
+    def destroy(self):
+        if self.handle is not None and self.handle.value:
+            self.stream.synchronize()
+            _check(load().ekya_stream_destroy(self.handle))
+        self.handle = None
+
+
+def ekya_stream_cu_count(stream) -> int:
+    return int(load().ekya_stream_cu_count(_stream(stream)))
+
+
+def ekya_set_cu_partition(ctx, cu_begin: float, cu_share: float) -> None:
+    _check(load().ekya_set_cu_partition(ctx, cu_begin, cu_share), ctx)
+
+
+def ekya_cu_ids(n_workgroups: int, stream=None):
+    """int32 view of the compute-unit id each of n one-wavefront workgroups ran on."""
+    torch = _torch()
+    out = torch.zeros(n_workgroups, dtype=torch.int32, device="cuda")
+    _check(load().ekya_cu_ids(n_workgroups, _dev(out), _stream(stream)))
+    return out
+
+
+def ekya_model_create(device: int = 0, n_classes: int = 6, precision: int = EKYA_BF16):
+    h = ctypes.c_void_p()
+    _check(load().ekya_model_create(ctypes.byref(h), device, n_classes, precision))
+    return h
+
+
+def ekya_model_destroy(model) -> None:
+    load().ekya_model_destroy(model)
+
+
+def ekya_model_load(model, weights, stream=None) -> int:
+    torch = _torch()
+    v = ctypes.c_uint64()
+    _check(load().ekya_model_load(model, _dev(weights, torch.float32), _stream(stream),
+                                  ctypes.byref(v)))
+    return int(v.value)
+
+
+def ekya_model_export(model, weights_out, stream=None) -> int:
+    torch = _torch()
+    v = ctypes.c_uint64()
+    _check(load().ekya_model_export(model, _dev(weights_out, torch.float32), _stream(stream),
+                                    ctypes.byref(v)))
+    return int(v.value)
+
+
+def ekya_model_version(model) -> int:
+    return int(load().ekya_model_version(model))
+
+
+def ekya_infer_model(ctx, model, frames, resolution: int, labels_out=None, stream=None):
+    """(labels_out, version of the weights used); asynchronous on the stream."""
+    torch = _torch()
+    n, H, W, _ = frames.shape
+    if labels_out is None:
+        labels_out = torch.empty(n, dtype=torch.int32, device=frames.device)
+    v = ctypes.c_uint64()
+    _check(load().ekya_infer_model(ctx, model, _dev(frames), n, H, W, resolution,
+                                   _dev(labels_out, torch.int32), _stream(stream), ctypes.byref(v)),
+           ctx)
+    return labels_out, int(v.value)
+
+
+def ekya_set_checkpoint(ctx, model, every_epochs: int = 1) -> None:
+    _check(load().ekya_set_checkpoint(ctx, model, every_epochs), ctx)
 
 
 # ----------------------------------------------------------------- ops

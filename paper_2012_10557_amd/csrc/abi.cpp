@@ -11,6 +11,7 @@
 #include <vector>
 
 #include "../../include/ekya.h"
+#include "../../include/ekya_joint.h"
 #include "../../include/ekya_ops.h"
 #include "../../include/ekya_sched.h"
 #include "curve.hpp"
@@ -19,6 +20,10 @@
 
 struct ekya_ctx {
   ekya::Ctx c;
+};
+
+struct ekya_model {
+  ekya::Model m;
 };
 
 namespace {
@@ -137,6 +142,9 @@ ekya_status ekya_retrain(ekya_ctx* ctx, float* weights, int k_trainable, const v
     return s;
   if (result->step_loss_capacity < 0 || (result->step_loss_capacity > 0 && !result->step_loss))
     return fail(ctx, EKYA_ERR_INVALID_ARG, "step_loss capacity without a buffer");
+  if (ctx->c.ckpt && ctx->c.ckpt->dt != opts->precision)
+    return fail(ctx, EKYA_ERR_INVALID_ARG,
+                "the checkpoint model's precision differs from the retraining precision");
   ctx->c.err.clear();
   return ekya::run_retrain(ctx->c, weights, k_trainable, frames, labels, n_frames, H, W,
                            heldout_frames, heldout_labels, n_heldout, *opts, result,
@@ -679,6 +687,182 @@ ekya_status ekya_thief_schedule(const ekya_video* videos, int n_videos, double n
     out->video_accuracy[v] = r.video_accuracy[v];
   }
   out->accuracy = r.accuracy;
+  return EKYA_OK;
+}
+
+}  // extern "C"
+
+// ------------------------------------------------------- joint inference and retraining
+namespace {
+
+bool valid_range(double begin, double share) {
+  return begin >= 0.0 && begin < 1.0 && share > 0.0 && begin + share <= 1.0 + 1e-9;
+}
+
+}  // namespace
+
+extern "C" {
+
+int ekya_partition_mask(int n_cu, int n_xcd, int n_se, double cu_begin, double cu_share,
+                        uint32_t* mask_out, int words) {
+  if (n_cu > (1 << 16) || n_xcd > (1 << 10) || n_se > (1 << 10)) return -1;
+  return ekya::partition_mask(n_cu, n_xcd, n_se, cu_begin, cu_share, mask_out, words);
+}
+
+ekya_status ekya_stream_create(int hip_device, double cu_begin, double cu_share,
+                               void** stream_out) {
+  if (!stream_out) return fail(nullptr, EKYA_ERR_INVALID_ARG, "stream_out is null");
+  *stream_out = nullptr;
+  if (!valid_range(cu_begin, cu_share))
+    return fail(nullptr, EKYA_ERR_INVALID_ARG,
+                "CU range must satisfy 0 <= cu_begin < 1, cu_share > 0, cu_begin + cu_share <= 1");
+  int n = 0;
+  if (hipGetDeviceCount(&n) != hipSuccess || n == 0)
+    return fail(nullptr, EKYA_ERR_HIP, "no HIP device available");
+  if (hip_device < 0 || hip_device >= n)
+    return fail(nullptr, EKYA_ERR_INVALID_ARG, "hip_device out of range");
+  std::vector<uint32_t> mask;
+  int count = 0;
+  hipError_t e = ekya::device_partition_mask(hip_device, cu_begin, cu_share, mask, &count);
+  if (e != hipSuccess)
+    return fail(nullptr, EKYA_ERR_INVALID_ARG, "the CU range selects no row of CUs");
+  int prev = 0;
+  if (hipGetDevice(&prev) != hipSuccess) prev = hip_device;
+  hipStream_t st = nullptr;
+  e = hipSetDevice(hip_device);
+  if (e == hipSuccess) e = ekya::create_masked_stream(mask, &st);
+  (void)hipSetDevice(prev);
+  if (e != hipSuccess) return hip_status(e);
+  *stream_out = st;
+  return EKYA_OK;
+}
+
+ekya_status ekya_stream_destroy(void* stream) {
+  if (!stream) return fail(nullptr, EKYA_ERR_INVALID_ARG, "stream is null");
+  return hip_status(hipStreamDestroy((hipStream_t)stream));
+}
+
+int ekya_stream_cu_count(void* stream) {
+  hipDevice_t dev = 0;
+  if (hipStreamGetDevice((hipStream_t)stream, &dev) != hipSuccess) return -1;
+  int n_cu = 0;
+  if (hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    return -1;
+  // sized for either reading of the size argument (words or bits)
+  std::vector<uint32_t> mask((size_t)32 * ((n_cu + 31) / 32), 0u);
+  if (hipExtStreamGetCUMask((hipStream_t)stream, (uint32_t)mask.size(), mask.data()) != hipSuccess)
+    return -1;
+  int c = 0;
+  for (int i = 0; i < n_cu; ++i) c += (mask[i / 32] >> (i % 32)) & 1u;
+  return c;
+}
+
+ekya_status ekya_set_cu_partition(ekya_ctx* ctx, double cu_begin, double cu_share) {
+  if (!ctx) return fail(nullptr, EKYA_ERR_INVALID_ARG, "ctx is null");
+  if (!valid_range(cu_begin, cu_share))
+    return fail(ctx, EKYA_ERR_INVALID_ARG,
+                "CU range must satisfy 0 <= cu_begin < 1, cu_share > 0, cu_begin + cu_share <= 1");
+  std::vector<uint32_t> mask;
+  const bool whole = cu_begin == 0.0 && cu_share >= 1.0;
+  if (!whole) {
+    int count = 0;
+    if (ekya::device_partition_mask(ctx->c.device, cu_begin, cu_share, mask, &count) != hipSuccess)
+      return fail(ctx, EKYA_ERR_INVALID_ARG, "the CU range selects no row of CUs");
+  }
+  hipError_t e = ekya::ctx_reset_streams(ctx->c);
+  if (e != hipSuccess) return fail(ctx, EKYA_ERR_HIP, std::string("HIP error: ") + hipGetErrorString(e));
+  ctx->c.cu_mask = mask;
+  return EKYA_OK;
+}
+
+ekya_status ekya_cu_ids(int n_workgroups, uint32_t* ids_out, void* stream) {
+  if (n_workgroups < 1 || n_workgroups > (1 << 20))
+    return fail(nullptr, EKYA_ERR_INVALID_ARG, "n_workgroups must be in [1, 2^20]");
+  if (!ids_out) return fail(nullptr, EKYA_ERR_INVALID_ARG, "ids_out is null");
+  return hip_status(ekya::cu_ids(n_workgroups, ids_out, (hipStream_t)stream));
+}
+
+ekya_status ekya_model_create(ekya_model** out, int hip_device, int n_classes, int precision) {
+  if (!out) return fail(nullptr, EKYA_ERR_INVALID_ARG, "out is null");
+  *out = nullptr;
+  if (n_classes < 1 || n_classes > 1024)
+    return fail(nullptr, EKYA_ERR_INVALID_ARG, "n_classes must be in [1, 1024]");
+  if (!valid_precision(precision))
+    return fail(nullptr, EKYA_ERR_INVALID_ARG, "precision must be EKYA_FP32 or EKYA_BF16");
+  int n = 0;
+  if (hipGetDeviceCount(&n) != hipSuccess || n == 0)
+    return fail(nullptr, EKYA_ERR_HIP, "no HIP device available");
+  if (hip_device < 0 || hip_device >= n)
+    return fail(nullptr, EKYA_ERR_INVALID_ARG, "hip_device out of range");
+  ekya_model* m = new (std::nothrow) ekya_model();
+  if (!m) return fail(nullptr, EKYA_ERR_NOMEM, "host allocation failed");
+  hipError_t e = ekya::model_init(m->m, hip_device, n_classes, precision);
+  if (e != hipSuccess) {
+    ekya::model_free(m->m);
+    delete m;
+    return hip_status(e);
+  }
+  *out = m;
+  return EKYA_OK;
+}
+
+void ekya_model_destroy(ekya_model* m) {
+  if (!m) return;
+  ekya::model_free(m->m);
+  delete m;
+}
+
+ekya_status ekya_model_load(ekya_model* m, const float* weights, void* stream,
+                            uint64_t* version_out) {
+  if (!m || !weights) return fail(nullptr, EKYA_ERR_INVALID_ARG, "null pointer argument");
+  return hip_status(ekya::model_load(m->m, weights, nullptr, (hipStream_t)stream, version_out));
+}
+
+ekya_status ekya_model_export(ekya_model* m, float* weights_out, void* stream,
+                              uint64_t* version_out) {
+  if (!m || !weights_out) return fail(nullptr, EKYA_ERR_INVALID_ARG, "null pointer argument");
+  bool empty = false;
+  hipError_t e = ekya::model_export(m->m, weights_out, (hipStream_t)stream, version_out, &empty);
+  if (empty) return fail(nullptr, EKYA_ERR_INVALID_ARG, "the model has no published weights");
+  return hip_status(e);
+}
+
+uint64_t ekya_model_version(ekya_model* m) {
+  if (!m) return 0;
+  std::lock_guard<std::mutex> lk(m->m.mu);
+  return m->m.current < 0 ? 0 : m->m.slot[m->m.current].version;
+}
+
+ekya_status ekya_infer_model(ekya_ctx* ctx, ekya_model* m, const void* frames, int n, int H, int W,
+                             int resolution, int32_t* labels_out, void* stream,
+                             uint64_t* version_out) {
+  if (!ctx) return fail(nullptr, EKYA_ERR_INVALID_ARG, "ctx is null");
+  if (!m) return fail(ctx, EKYA_ERR_INVALID_ARG, "model is null");
+  if (n < 0 || n > (1 << 26)) return fail(ctx, EKYA_ERR_INVALID_ARG, "n must be in [0, 2^26]");
+  if (m->m.device != ctx->c.device || m->m.n_classes != ctx->c.n_classes)
+    return fail(ctx, EKYA_ERR_INVALID_ARG, "the model's device or class count differs from the context's");
+  if (ekya_model_version(m) == 0)
+    return fail(ctx, EKYA_ERR_INVALID_ARG, "the model has no published weights (call ekya_model_load first)");
+  if (n == 0) return EKYA_OK;
+  if (!frames || !labels_out) return fail(ctx, EKYA_ERR_INVALID_ARG, "null pointer argument");
+  if (ekya_status s = check_frames(ctx, H, W)) return s;
+  if (resolution < 32 || resolution > 4096)
+    return fail(ctx, EKYA_ERR_INVALID_ARG, "resolution must be in [32, 4096]");
+  ctx->c.err.clear();
+  return ekya::run_infer_model(ctx->c, m->m, frames, n, H, W, resolution, labels_out,
+                               (hipStream_t)stream, version_out);
+}
+
+ekya_status ekya_set_checkpoint(ekya_ctx* ctx, ekya_model* m, int every_epochs) {
+  if (!ctx) return fail(nullptr, EKYA_ERR_INVALID_ARG, "ctx is null");
+  if (m) {
+    if (every_epochs < 1) return fail(ctx, EKYA_ERR_INVALID_ARG, "every_epochs must be >= 1");
+    if (m->m.device != ctx->c.device || m->m.n_classes != ctx->c.n_classes)
+      return fail(ctx, EKYA_ERR_INVALID_ARG,
+                  "the model's device or class count differs from the context's");
+  }
+  ctx->c.ckpt = m ? &m->m : nullptr;
+  ctx->c.ckpt_every = m ? every_epochs : 0;
   return EKYA_OK;
 }
 

@@ -2019,4 +2019,26 @@ hipError_t permute_weights(const float* src, float* dst, const long long* tab, i
   return hipGetLastError();
 }
 
+// Hardware registers read with s_getreg_b32 (hwreg(id, offset, size) is
+// id | offset << 6 | (size - 1) << 11): HW_ID (4) holds the CU in bits 11:8,
+// the shader array in bit 12 and the shader engine in bits 14:13; XCC_ID (20)
+// the die in bits 3:0.
+__global__ void __launch_bounds__(64) cu_ids_kernel(uint32_t* out, int n) {
+  const uint32_t hw = __builtin_amdgcn_s_getreg(4 | (0 << 6) | (31 << 11));
+  const uint32_t xcc = __builtin_amdgcn_s_getreg(20 | (0 << 6) | (3 << 11));
+  // stay resident for about 20 us (wall clock at 100 MHz, at most 2^20
+  // polls) so that the workgroups spread over every CU the queue may use
+  const uint64_t t0 = wall_clock64();
+  for (int i = 0; i < (1 << 20) && wall_clock64() - t0 < 2000; ++i) __builtin_amdgcn_s_sleep(1);
+  if (threadIdx.x == 0 && (int)blockIdx.x < n)
+    out[blockIdx.x] = (xcc & 15u) << 10 | ((hw >> 12) & 1u) << 8 | ((hw >> 13) & 3u) << 4 |
+                      ((hw >> 8) & 15u);
+}
+
+hipError_t cu_ids(int n, uint32_t* out, hipStream_t stream) {
+  if (n < 1 || n > (1 << 20)) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(cu_ids_kernel, dim3(n), dim3(64), 0, stream, out, n);
+  return hipGetLastError();
+}
+
 }  // namespace ekya

@@ -267,4 +267,9 @@ hipError_t pack_conv_weights(int dt, const float* master, const long long* tab, 
 hipError_t permute_weights(const float* src, float* dst, const long long* tab, int n,
                            long long total, int to_internal, hipStream_t stream);
 
+// ------------------------------------------------------------- diagnostics
+// n one-wavefront workgroups; workgroup i writes the compute unit it ran on,
+// (xcd << 10) | (shader array << 8) | (shader engine << 4) | cu, to out[i].
+hipError_t cu_ids(int n, uint32_t* out, hipStream_t stream);
+
 }  // namespace ekya

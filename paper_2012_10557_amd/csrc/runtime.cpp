@@ -180,6 +180,92 @@ void ctx_free(Ctx& c) {
   for (auto& t : c.tabs) t.buf.release();
 }
 
+// A stream of the context's own (default priority), restricted to the
+// context's CU partition when it has one.
+static hipError_t ctx_stream(const Ctx& c, hipStream_t* s) {
+  if (c.cu_mask.empty()) return hipStreamCreateWithFlags(s, hipStreamNonBlocking);
+  return create_masked_stream(c.cu_mask, s);
+}
+
+hipError_t ctx_reset_streams(Ctx& c) {
+  EKYA_HIP(hipSetDevice(c.device));
+  EKYA_HIP(hipEventSynchronize(c.last_done));
+  for (hipStream_t s : c.streams) EKYA_HIP(hipStreamSynchronize(s));
+  if (c.eval_stream) EKYA_HIP(hipStreamSynchronize(c.eval_stream));
+  for (hipStream_t s : c.streams) (void)hipStreamDestroy(s);
+  c.streams.clear();
+  if (c.eval_stream) (void)hipStreamDestroy(c.eval_stream);
+  c.eval_stream = nullptr;
+  return hipSuccess;
+}
+
+// ------------------------------------------------------------ CU shares
+// The amdgpu driver deals CU-mask bits to the dies first, then to the
+// shader engines of a die, then to the CUs of an engine: bit b is CU
+// b / (X S) of engine (b / X) mod S on die b mod X (X dies, S engines, R CUs
+// per die).  A share is counted in groups of one CU per die; group
+// g = k S + s takes CU k of engine s on every die, so a run of groups spreads
+// over the engines of every die as evenly as whole groups allow.  Where
+// R = X S (the CUs per engine equal the dies, as on MI355X: 8 dies of 4
+// engines of 8 CUs) the CU index k is rotated to (j + s + k) mod X for die j:
+// the bits of a group then also fall in X different blocks of R bits, so a
+// die-by-die numbering (bit b on die b / R) would still give every die one
+// CU per group.  Otherwise the group of row r puts die j on bit
+// j R + (r + j) mod R, one CU per die under either numbering.  Disjoint group
+// ranges give disjoint bits.
+int partition_mask(int n_cu, int n_xcd, int n_se, double begin, double share, uint32_t* mask,
+                   int words) {
+  if (n_cu < 1 || n_xcd < 1 || n_se < 1 || n_cu % n_xcd != 0 || !mask ||
+      words < (n_cu + 31) / 32)
+    return -1;
+  if (!(begin >= 0.0 && begin < 1.0) || !(share > 0.0) || begin + share > 1.0 + 1e-9) return -1;
+  const int X = n_xcd, R = n_cu / n_xcd;
+  const int g0 = (int)std::lround(begin * R);
+  const int g1 = std::min(R, (int)std::lround((begin + share) * R));
+  if (g1 <= g0) return -1;
+  std::fill(mask, mask + words, 0u);
+  const bool engines = R % n_se == 0 && R / n_se == X;
+  for (int g = g0; g < g1; ++g)
+    for (int j = 0; j < X; ++j) {
+      int b;
+      if (engines) {
+        const int S = n_se, k = g / S, s = g % S;
+        b = X * S * ((j + s + k) % X) + X * s + j;
+      } else {
+        b = j * R + (g + j) % R;
+      }
+      mask[b / 32] |= 1u << (b % 32);
+    }
+  return (g1 - g0) * X;
+}
+
+// Shader engines per die: 4 on the CDNA3 and CDNA4 dies.
+static constexpr int kEnginesPerXcd = 4;
+
+hipError_t device_partition_mask(int device, double begin, double share,
+                                 std::vector<uint32_t>& mask, int* count) {
+  int n_cu = 0, n_xcd = 1;
+  EKYA_HIP(hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, device));
+  if (hipDeviceGetAttribute(&n_xcd, hipDeviceAttributeNumberOfXccs, device) != hipSuccess ||
+      n_xcd < 1 || n_cu % n_xcd != 0)
+    n_xcd = 1;
+  mask.assign((n_cu + 31) / 32, 0u);
+  *count = partition_mask(n_cu, n_xcd, kEnginesPerXcd, begin, share, mask.data(),
+                          (int)mask.size());
+  return *count > 0 ? hipSuccess : hipErrorInvalidValue;
+}
+
+// hipExtStreamCreateWithCUMask's size argument counts mask words in the
+// runtime (its documentation calls it the size of the bit array): the mask
+// is passed zero-padded to 32 times its words, which reads the same mask
+// under either reading and ignores bits past the device's CUs.
+hipError_t create_masked_stream(const std::vector<uint32_t>& mask, hipStream_t* s) {
+  std::vector<uint32_t> padded(mask.size() * 32, 0u);
+  std::copy(mask.begin(), mask.end(), padded.begin());
+  return hipExtStreamCreateWithCUMask(s, (uint32_t)padded.size(), padded.data());
+}
+
+
 // --------------------------------------------------------- eval forward
 // Buffers for running stages in eval mode on up to `cap` frames.
 struct EvalBufs {
@@ -409,6 +495,9 @@ struct TrainJob {
   hipEvent_t ev[EKYA_MAX_EPOCHS + 1] = {nullptr};
   hipEvent_t ev_tr[EKYA_MAX_EPOCHS] = {nullptr};
   hipEvent_t ev_e0[EKYA_MAX_EPOCHS] = {nullptr}, ev_e1[EKYA_MAX_EPOCHS] = {nullptr};
+  // retraining only: publish the weights into ckpt every ckpt_every epochs
+  Model* ckpt = nullptr;
+  int ckpt_every = 0;
 };
 
 static_assert(3 * 8 + 1 <= TrainJob::kForks / 2, "fork events for a full-depth backward pass");
@@ -947,6 +1036,8 @@ static hipError_t job_epochs(TrainJob& j) {
     j.eval_pending = false;
     // held-out accuracy in eval mode with the current running statistics
     EKYA_HIP(bn_fold(j.master, t.fold_train[j.lowest], t.n_fold_train[j.lowest], j.fold, j.st));
+    if (j.ckpt && ((e + 1) % j.ckpt_every == 0 || e + 1 == j.epochs))
+      EKYA_HIP(model_load(*j.ckpt, nullptr, j.master, j.st, nullptr));
     hipStream_t qe = j.st;
     const void* esh = j.shadow;
     const float* ems = j.master;
@@ -1174,14 +1265,16 @@ ekya_status run_retrain(Ctx& c, float* weights, int k, const void* frames, const
   // library-owned side streams (default priority): weight gradients, held-out evaluation
   if (c.streams.empty()) {
     hipStream_t s2;
-    EKYA_CHECK_HIP(hipStreamCreateWithFlags(&s2, hipStreamNonBlocking));
+    EKYA_CHECK_HIP(ctx_stream(c, &s2));
     c.streams.push_back(s2);
   }
   j.st2 = c.timing ? stream : c.streams[0];
   if (j.eval_overlap) {
-    if (!c.eval_stream) EKYA_CHECK_HIP(hipStreamCreateWithFlags(&c.eval_stream, hipStreamNonBlocking));
+    if (!c.eval_stream) EKYA_CHECK_HIP(ctx_stream(c, &c.eval_stream));
     j.st3 = c.eval_stream;
   }
+  j.ckpt = c.ckpt;
+  j.ckpt_every = c.ckpt_every;
   j.weights = weights;
   j.frames = frames;
   j.labels = labels;
@@ -1352,7 +1445,7 @@ ekya_status run_profile(Ctx& c, const float* weights, const ekya_profile_cfg* cf
   // streams: per candidate a main and a side stream, plus one for the caches
   while ((int)c.streams.size() < 2 * n_cfgs + 1) {
     hipStream_t s;
-    EKYA_CHECK_HIP(hipStreamCreateWithFlags(&s, hipStreamNonBlocking));
+    EKYA_CHECK_HIP(ctx_stream(c, &s));
     c.streams.push_back(s);
   }
   hipStream_t s0 = c.streams[n_cfgs];
@@ -1492,11 +1585,16 @@ struct InferBufs {
   EvalBufs eb;
 };
 
-static void plan_infer(Arena& a, const Net& net, const Geo& geo, int resolution, InferBufs& b) {
+// own_weights: the call prepares the weights in its arena (ekya_infer);
+// otherwise they come from a prepared model.
+static void plan_infer(Arena& a, const Net& net, const Geo& geo, int resolution, InferBufs& b,
+                       bool own_weights = true) {
   const size_t es = dtype_size(net.dt);
-  b.master = a.take<float>(net.total);
-  b.fold = a.take<float>(2 * net.bn_channels);
-  b.shadow = a.take_bytes(net.shadow_elems * es);
+  if (own_weights) {
+    b.master = a.take<float>(net.total);
+    b.fold = a.take<float>(2 * net.bn_channels);
+    b.shadow = a.take_bytes(net.shadow_elems * es);
+  }
   b.padded = a.take_bytes((size_t)kInferChunk * resolution * resolution * net.conv[0].cin_pad * es);
   plan_eval(a, net, geo, 0, 5, kInferChunk, b.eb);
 }
@@ -1508,6 +1606,46 @@ size_t infer_workspace_bytes(const Net& net, int resolution) {
   return a.used;
 }
 
+// Inference weights from internal-layout fp32 weights: folded eval-mode
+// BatchNorm and the low-precision convolution weights.
+static hipError_t prepare_inference(const Net& net, const Tables& t, const float* master,
+                                    float* fold, void* shadow, hipStream_t stream) {
+  EKYA_HIP(bn_fold(master, t.fold_all, t.n_fold_all, fold, stream));
+  EKYA_HIP(pack_conv_weights(net.dt, master, t.pack_all, t.n_pack_all, shadow, stream));
+  return hipSuccess;
+}
+
+// Classify n frames with prepared weights, chunk by chunk.
+static hipError_t infer_frames(const Net& net, const Geo& geo, const float* master,
+                               const float* fold, const void* shadow, const void* frames, int n,
+                               int H, int W, int resolution, int32_t* labels_out, InferBufs& ib,
+                               hipStream_t stream) {
+  const size_t es = dtype_size(net.dt);
+  const int cap = kInferChunk;
+  EvalBufs& eb = ib.eb;
+  const long long fbytes = (long long)H * W * 3 * es;
+  const int per = n > 0 ? cdiv(n, cdiv(n, cap)) : cap;  // equal chunks (2000: 4 x 500)
+  for (int i0 = 0; i0 < n; i0 += per) {
+    const int cnt = std::min(per, n - i0);
+    const void* src = reinterpret_cast<const char*>(frames) + i0 * fbytes;
+    if (resolution == H && resolution == W && stem_frames_ok(net.dt, conv_geom(net, geo, 0, cnt))) {
+      EKYA_HIP(eval_forward(net, geo, shadow, fold, master, 0, 5, src, cnt, eb, eb.logits, stream,
+                            true));  // the stem reads the frames
+    } else {
+      if (resolution == H && resolution == W)
+        EKYA_HIP(frames_to_padded(net.dt, src, nullptr, cnt, H, W, net.conv[0].cin_pad, ib.padded,
+                                  stream));
+      else
+        EKYA_HIP(resize_to_padded(net.dt, src, cnt, H, W, resolution, net.conv[0].cin_pad,
+                                  ib.padded, stream));
+      EKYA_HIP(eval_forward(net, geo, shadow, fold, master, 0, 5, ib.padded, cnt, eb, eb.logits,
+                            stream));
+    }
+    EKYA_HIP(argmax_rows(eb.logits, cnt, net.n_classes, labels_out + i0, stream));
+  }
+  return hipSuccess;
+}
+
 ekya_status run_infer(Ctx& c, const float* weights, const void* frames, int n, int H, int W,
                       int resolution, int precision, int32_t* labels_out, hipStream_t stream) {
   EKYA_CHECK_HIP(hipSetDevice(c.device));
@@ -1515,8 +1653,6 @@ ekya_status run_infer(Ctx& c, const float* weights, const void* frames, int n, i
   const int dt = precision;
   const Net& net = c.net[dt];
   const Geo geo = Geo::build(net, resolution, resolution);
-  const size_t es = dtype_size(dt);
-  const int cap = kInferChunk;
   InferBufs ib;
   {
     Arena meas;
@@ -1526,40 +1662,154 @@ ekya_status run_infer(Ctx& c, const float* weights, const void* frames, int n, i
   Arena real;
   real.base = reinterpret_cast<char*>(c.ws.p);
   plan_infer(real, net, geo, resolution, ib);
-  float* master = ib.master;
-  float* fold = ib.fold;
-  void* shadow = ib.shadow;
-  void* padded = ib.padded;
-  EvalBufs& eb = ib.eb;
   const Tables& t = c.tabs[dt];
   auto run = [&]() -> hipError_t {
-    EKYA_HIP(permute_weights(weights, master, t.permute, t.n_permute, net.total, 1, stream));
-    EKYA_HIP(bn_fold(master, t.fold_all, t.n_fold_all, fold, stream));
-    EKYA_HIP(pack_conv_weights(dt, master, t.pack_all, t.n_pack_all, shadow, stream));
-    const long long fbytes = (long long)H * W * 3 * es;
-    const int per = n > 0 ? cdiv(n, cdiv(n, cap)) : cap;  // equal chunks (2000: 4 x 500)
-    for (int i0 = 0; i0 < n; i0 += per) {
-      const int cnt = std::min(per, n - i0);
-      const void* src = reinterpret_cast<const char*>(frames) + i0 * fbytes;
-      if (resolution == H && resolution == W && stem_frames_ok(dt, conv_geom(net, geo, 0, cnt))) {
-        EKYA_HIP(eval_forward(net, geo, shadow, fold, master, 0, 5, src, cnt, eb, eb.logits,
-                              stream, true));  // the stem reads the frames
-      } else {
-        if (resolution == H && resolution == W)
-          EKYA_HIP(frames_to_padded(dt, src, nullptr, cnt, H, W, net.conv[0].cin_pad, padded,
-                                    stream));
-        else
-          EKYA_HIP(resize_to_padded(dt, src, cnt, H, W, resolution, net.conv[0].cin_pad, padded,
-                                    stream));
-        EKYA_HIP(eval_forward(net, geo, shadow, fold, master, 0, 5, padded, cnt, eb, eb.logits,
-                              stream));
-      }
-      EKYA_HIP(argmax_rows(eb.logits, cnt, net.n_classes, labels_out + i0, stream));
-    }
-    return hipSuccess;
+    EKYA_HIP(permute_weights(weights, ib.master, t.permute, t.n_permute, net.total, 1, stream));
+    EKYA_HIP(prepare_inference(net, t, ib.master, ib.fold, ib.shadow, stream));
+    return infer_frames(net, geo, ib.master, ib.fold, ib.shadow, frames, n, H, W, resolution,
+                        labels_out, ib, stream);
   };
   hipError_t he = run();
   (void)hipEventRecord(c.last_done, stream);  // after whatever was queued
+  EKYA_CHECK_HIP(he);
+  return EKYA_OK;
+}
+
+// ------------------------------------------------------------ hot reload
+hipError_t model_init(Model& m, int device, int n_classes, int dt) {
+  m.device = device;
+  m.n_classes = n_classes;
+  m.dt = dt;
+  EKYA_HIP(hipSetDevice(device));
+  m.net = Net::build(n_classes, dt);
+  EKYA_HIP(upload_tables(m.net, m.tabs));
+  Arena a;
+  for (int i = 0; i < 2; ++i) {
+    a.take<float>(m.net.total);
+    a.take<float>(2 * m.net.bn_channels);
+    a.take_bytes(m.net.shadow_elems * dtype_size(dt));
+  }
+  EKYA_HIP(m.mem.alloc(a.used));
+  Arena r;
+  r.base = reinterpret_cast<char*>(m.mem.p);
+  for (ModelSlot& sl : m.slot) {
+    sl.master = r.take<float>(m.net.total);
+    sl.fold = r.take<float>(2 * m.net.bn_channels);
+    sl.shadow = r.take_bytes(m.net.shadow_elems * dtype_size(dt));
+    EKYA_HIP(hipEventCreateWithFlags(&sl.ready, hipEventDisableTiming));
+  }
+  return hipSuccess;
+}
+
+void model_free(Model& m) {
+  (void)hipSetDevice(m.device);
+  for (ModelSlot& sl : m.slot) {
+    if (sl.ready) (void)hipEventSynchronize(sl.ready);
+    for (auto& u : sl.uses) {
+      (void)hipEventSynchronize(u.second);
+      (void)hipEventDestroy(u.second);
+    }
+    sl.uses.clear();
+    if (sl.ready) (void)hipEventDestroy(sl.ready);
+    sl.ready = nullptr;
+  }
+  for (hipEvent_t e : m.pool) (void)hipEventDestroy(e);
+  m.pool.clear();
+  m.mem.release();
+  m.tabs.buf.release();
+}
+
+// Record that the call just queued on `stream` read slot s (caller holds mu).
+static hipError_t model_note_use(Model& m, int s, hipStream_t stream) {
+  ModelSlot& sl = m.slot[s];
+  for (auto& u : sl.uses)
+    if (u.first == stream) return hipEventRecord(u.second, stream);
+  hipEvent_t e;
+  if (!m.pool.empty()) {
+    e = m.pool.back();
+    m.pool.pop_back();
+  } else {
+    EKYA_HIP(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+  }
+  sl.uses.push_back({stream, e});
+  return hipEventRecord(e, stream);
+}
+
+hipError_t model_load(Model& m, const float* canonical, const float* internal, hipStream_t stream,
+                      uint64_t* version) {
+  std::lock_guard<std::mutex> lk(m.mu);
+  EKYA_HIP(hipSetDevice(m.device));
+  const int s = m.current < 0 ? 0 : 1 - m.current;
+  ModelSlot& sl = m.slot[s];
+  // the calls still reading this slot finish before it is overwritten
+  for (auto& u : sl.uses) EKYA_HIP(hipStreamWaitEvent(stream, u.second, 0));
+  for (auto& u : sl.uses) m.pool.push_back(u.second);
+  sl.uses.clear();
+  if (canonical)
+    EKYA_HIP(permute_weights(canonical, sl.master, m.tabs.permute, m.tabs.n_permute, m.net.total,
+                             1, stream));
+  else
+    EKYA_HIP(hipMemcpyAsync(sl.master, internal, m.net.total * sizeof(float),
+                            hipMemcpyDeviceToDevice, stream));
+  EKYA_HIP(prepare_inference(m.net, m.tabs, sl.master, sl.fold, sl.shadow, stream));
+  EKYA_HIP(hipEventRecord(sl.ready, stream));
+  sl.version = m.next_version++;
+  m.current = s;
+  if (version) *version = sl.version;
+  return hipSuccess;
+}
+
+hipError_t model_export(Model& m, float* canonical_out, hipStream_t stream, uint64_t* version,
+                        bool* empty) {
+  std::lock_guard<std::mutex> lk(m.mu);
+  *empty = m.current < 0;
+  if (*empty) return hipSuccess;
+  EKYA_HIP(hipSetDevice(m.device));
+  ModelSlot& sl = m.slot[m.current];
+  EKYA_HIP(hipStreamWaitEvent(stream, sl.ready, 0));
+  EKYA_HIP(permute_weights(sl.master, canonical_out, m.tabs.permute, m.tabs.n_permute,
+                           m.net.total, 0, stream));
+  EKYA_HIP(model_note_use(m, m.current, stream));
+  if (version) *version = sl.version;
+  return hipSuccess;
+}
+
+ekya_status run_infer_model(Ctx& c, Model& m, const void* frames, int n, int H, int W,
+                            int resolution, int32_t* labels_out, hipStream_t stream,
+                            uint64_t* version) {
+  EKYA_CHECK_HIP(hipSetDevice(c.device));
+  TimerGuard tg(c);
+  const Net& net = c.net[m.dt];
+  const Geo geo = Geo::build(net, resolution, resolution);
+  InferBufs ib;
+  {
+    Arena meas;
+    plan_infer(meas, net, geo, resolution, ib, false);
+    if (ekya_status s = acquire_workspace(c, meas.used, stream)) return s;
+  }
+  Arena real;
+  real.base = reinterpret_cast<char*>(c.ws.p);
+  plan_infer(real, net, geo, resolution, ib, false);
+  hipError_t he;
+  {
+    // the slot is taken, read and marked as read under the lock, so a load
+    // that overwrites it later waits for this call
+    std::lock_guard<std::mutex> lk(m.mu);
+    if (m.current < 0) {
+      c.err = "the model has no published weights (call ekya_model_load first)";
+      return EKYA_ERR_INVALID_ARG;
+    }
+    const int s = m.current;
+    ModelSlot& sl = m.slot[s];
+    he = hipStreamWaitEvent(stream, sl.ready, 0);
+    if (he == hipSuccess)
+      he = infer_frames(net, geo, sl.master, sl.fold, sl.shadow, frames, n, H, W, resolution,
+                        labels_out, ib, stream);
+    const hipError_t hu = model_note_use(m, s, stream);
+    if (he == hipSuccess) he = hu;
+    if (version) *version = sl.version;
+  }
+  (void)hipEventRecord(c.last_done, stream);
   EKYA_CHECK_HIP(he);
   return EKYA_OK;
 }

@@ -3,7 +3,9 @@
 #pragma once
 
 #include <map>
+#include <mutex>
 #include <string>
+#include <utility>
 #include <vector>
 
 #include "../../include/ekya.h"
@@ -57,6 +59,52 @@ struct Tables {
   int n_pack_rest[6] = {0};
 };
 
+// One slot of a prepared inference model: internal-layout fp32 weights,
+// folded eval-mode BatchNorm and the low-precision convolution weights.
+struct ModelSlot {
+  float* master = nullptr;
+  float* fold = nullptr;
+  void* shadow = nullptr;
+  hipEvent_t ready = nullptr;  // recorded after the load that filled the slot
+  // per stream, an event recorded after the latest inference call (or
+  // export) on that stream that read the slot; a load into the slot waits
+  // for all of them
+  std::vector<std::pair<hipStream_t, hipEvent_t>> uses;
+  uint64_t version = 0;
+};
+
+// Double-buffered inference model (hot reload of retrained weights).
+struct Model {
+  int device = 0;
+  int n_classes = 0;
+  int dt = 0;
+  Net net;
+  Tables tabs;
+  DeviceBuf mem;
+  ModelSlot slot[2];
+  int current = -1;  // published slot, -1 before the first load
+  uint64_t next_version = 1;
+  std::vector<hipEvent_t> pool;  // spare use events
+  std::mutex mu;                 // guards everything above after init
+};
+
+hipError_t model_init(Model& m, int device, int n_classes, int dt);
+void model_free(Model& m);
+// Fill the unpublished slot on `stream` from canonical weights (canonical !=
+// null) or from internal-layout fp32 weights (internal), then publish it.
+hipError_t model_load(Model& m, const float* canonical, const float* internal, hipStream_t stream,
+                      uint64_t* version);
+hipError_t model_export(Model& m, float* canonical_out, hipStream_t stream, uint64_t* version,
+                        bool* empty);
+
+// CU mask of a range [begin, begin + share) of a device with n_cu CUs on
+// n_xcd dies of n_se shader engines; returns the CU count or -1.
+int partition_mask(int n_cu, int n_xcd, int n_se, double begin, double share, uint32_t* mask,
+                   int words);
+hipError_t device_partition_mask(int device, double begin, double share,
+                                 std::vector<uint32_t>& mask, int* count);
+hipError_t create_masked_stream(const std::vector<uint32_t>& mask, hipStream_t* s);
+
 struct KernelStat {
   long long launches = 0;
   double ms = 0.0, flops = 0.0, bytes = 0.0;
@@ -80,6 +128,11 @@ struct Ctx {
   hipEvent_t last_done = nullptr;
   std::vector<hipStream_t> streams;  // profiler streams (default priority)
   hipStream_t eval_stream = nullptr;  // retraining's held-out evaluation (default priority)
+  // CU mask of the context's own streams (empty: every CU)
+  std::vector<uint32_t> cu_mask;
+  // checkpointing during retraining: publish into ckpt every ckpt_every epochs
+  Model* ckpt = nullptr;
+  int ckpt_every = 0;
   bool timing = false;
   KernelTimer timer;
   std::map<std::string, KernelStat> stats;
@@ -89,6 +142,9 @@ struct Ctx {
 hipError_t ctx_collect_timing(Ctx& c);
 
 hipError_t ctx_init(Ctx& c, int device, int n_classes, size_t workspace_bytes);
+// Wait for the context's queued work and release its own streams (they are
+// created again, with the current cu_mask, when next needed).
+hipError_t ctx_reset_streams(Ctx& c);
 
 // Bytes of workspace arena a call with these arguments plans (host only;
 // arguments already validated).
@@ -110,5 +166,8 @@ ekya_status run_profile(Ctx& c, const float* weights, const ekya_profile_cfg* cf
                         ekya_profile_result* out);
 ekya_status run_infer(Ctx& c, const float* weights, const void* frames, int n, int H, int W,
                       int resolution, int precision, int32_t* labels_out, hipStream_t stream);
+ekya_status run_infer_model(Ctx& c, Model& m, const void* frames, int n, int H, int W,
+                            int resolution, int32_t* labels_out, hipStream_t stream,
+                            uint64_t* version);
 
 }  // namespace ekya
