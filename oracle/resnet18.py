@@ -10,7 +10,15 @@ cites for the network's size in section 6.6):
            layers 2-4, shortcut = BN(conv 1x1 stride 2) where the shape
            changes, identity otherwise
   pool   : global average pool (no parameters)
-  fc     : affine classifier with bias
+  fc     : affine classifier with bias; or, with `hidden` > 0 neurons in the
+           last hidden layer, Linear(512, hidden), ReLU, Linear(hidden,
+           classes) (torch nn.Sequential names fc.0 and fc.2)
+
+The number of neurons in the last layer is one of the retraining
+configuration's knobs (sections 3.2 and 6.1).  The output layer's width is
+fixed by the classes, so the knob is read as the width of a hidden fully
+connected layer between the pooled features and the classifier, trained with
+the classifier (stage 5); hidden = 0 is the plain affine classifier.
 
 Retraining "fewer layers" / "freezing more layers" (section 3.1) is read as
 training the last k stages of [stem, layer1, layer2, layer3, layer4, fc]:
@@ -33,8 +41,10 @@ STAGES = ("stem", "layer1", "layer2", "layer3", "layer4", "fc")
 
 
 class ResNet18:
-    def __init__(self, n_classes: int = 6, widths=(64, 128, 256, 512), blocks=(2, 2, 2, 2)):
+    def __init__(self, n_classes: int = 6, widths=(64, 128, 256, 512), blocks=(2, 2, 2, 2),
+                 hidden: int = 0):
         self.n_classes = n_classes
+        self.hidden = hidden
         self.widths = tuple(widths)
         self.blocks = tuple(blocks)
         self.spec: List[Tuple[str, Tuple[int, ...]]] = []
@@ -68,8 +78,14 @@ class ResNet18:
                 cfg.append((p, stride, has_ds))
                 cin = w
             self._block_cfg.append(cfg)
-        add("fc.weight", (n_classes, widths[-1]), 5)
-        add("fc.bias", (n_classes,), 5)
+        if hidden:
+            add("fc.0.weight", (hidden, widths[-1]), 5)
+            add("fc.0.bias", (hidden,), 5)
+            add("fc.2.weight", (n_classes, hidden), 5)
+            add("fc.2.bias", (n_classes,), 5)
+        else:
+            add("fc.weight", (n_classes, widths[-1]), 5)
+            add("fc.bias", (n_classes,), 5)
 
     # ----------------------------------------------------------- weights
     def n_weights(self) -> int:
@@ -121,7 +137,11 @@ class ResNet18:
             return y
         if stage == 5:
             tape["fc"] = x
-            return nn.linear(x, P["fc.weight"], P["fc.bias"])
+            if not self.hidden:
+                return nn.linear(x, P["fc.weight"], P["fc.bias"])
+            a = nn.relu(nn.linear(x, P["fc.0.weight"], P["fc.0.bias"]))
+            tape["fc.hidden"] = a
+            return nn.linear(a, P["fc.2.weight"], P["fc.2.bias"])
         for prefix, stride, has_ds in self._block_cfg[stage - 1]:
             x = self._block_forward(P, prefix, x, stride, has_ds, train, tape)
         if stage == 4:
@@ -153,7 +173,14 @@ class ResNet18:
 
         No gradient is sent into the input of stage `lowest` (it is frozen data)."""
         grads: Dict[str, np.ndarray] = {}
-        df, grads["fc.weight"], grads["fc.bias"] = nn.linear_backward(dlogits, tape["fc"], P["fc.weight"])
+        if self.hidden:
+            a = tape["fc.hidden"]
+            da, grads["fc.2.weight"], grads["fc.2.bias"] = nn.linear_backward(dlogits, a, P["fc.2.weight"])
+            df, grads["fc.0.weight"], grads["fc.0.bias"] = nn.linear_backward(
+                nn.relu_backward(da, a), tape["fc"], P["fc.0.weight"])
+        else:
+            df, grads["fc.weight"], grads["fc.bias"] = nn.linear_backward(dlogits, tape["fc"],
+                                                                          P["fc.weight"])
         if lowest == 5:
             return grads
         d = nn.avgpool_backward(df, tape["pool"])

@@ -166,8 +166,10 @@ def make_window(spec: WindowSpec) -> dict:
 
 
 def resnet18_param_spec(n_classes: int = 6, widths=(64, 128, 256, 512),
-                        blocks=(2, 2, 2, 2)) -> List[Tuple[str, Tuple[int, ...], str]]:
-    """(name, shape, kind) in torchvision state_dict order, without num_batches_tracked."""
+                        blocks=(2, 2, 2, 2), hidden: int = 0) -> List[Tuple[str, Tuple[int, ...], str]]:
+    """(name, shape, kind) in torchvision state_dict order, without num_batches_tracked.
+    hidden > 0: the classifier is Linear(512, hidden), ReLU, Linear(hidden,
+    n_classes), named as an nn.Sequential (fc.0, fc.2)."""
     spec: List[Tuple[str, Tuple[int, ...], str]] = []
 
     def bn(prefix: str, c: int):
@@ -191,19 +193,29 @@ def resnet18_param_spec(n_classes: int = 6, widths=(64, 128, 256, 512),
                 spec.append((p + ".downsample.0.weight", (w, cin, 1, 1), "conv"))
                 bn(p + ".downsample.1", w)
             cin = w
-    spec.append(("fc.weight", (n_classes, widths[-1]), "fc_weight"))
-    spec.append(("fc.bias", (n_classes,), "fc_bias"))
+    if hidden:
+        spec.append(("fc.0.weight", (hidden, widths[-1]), "fc_weight"))
+        spec.append(("fc.0.bias", (hidden,), "fc_bias"))
+        spec.append(("fc.2.weight", (n_classes, hidden), "fc_weight"))
+        spec.append(("fc.2.bias", (n_classes,), "fc_bias"))
+    else:
+        spec.append(("fc.weight", (n_classes, widths[-1]), "fc_weight"))
+        spec.append(("fc.bias", (n_classes,), "fc_bias"))
     return spec
 
 
 def kaiming_resnet18_weights(seed: int = 0, n_classes: int = 6, widths=(64, 128, 256, 512),
-                             blocks=(2, 2, 2, 2)) -> np.ndarray:
-    """Flat float32 weights in the canonical order of `resnet18_param_spec`."""
+                             blocks=(2, 2, 2, 2), hidden: int = 0) -> np.ndarray:
+    """Flat float32 weights in the canonical order of `resnet18_param_spec`.
+    Linear layers draw weight and bias from U(-1/sqrt(fan_in), 1/sqrt(fan_in))
+    (torch.nn.Linear's default), fan_in being the layer's input width."""
     parts = []
     fan_in_fc = widths[-1]
-    for idx, (name, shape, kind) in enumerate(resnet18_param_spec(n_classes, widths, blocks)):
+    for idx, (name, shape, kind) in enumerate(resnet18_param_spec(n_classes, widths, blocks, hidden)):
         n = int(np.prod(shape))
         st = _state(seed, TAG_WEIGHTS + idx)
+        if kind == "fc_weight":
+            fan_in_fc = shape[1]
         if kind == "conv":
             std = np.sqrt(2.0 / (shape[0] * shape[2] * shape[3]))
             vals = std * _normal(st, n)

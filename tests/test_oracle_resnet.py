@@ -17,10 +17,10 @@ from synth import WindowSpec, kaiming_resnet18_weights, make_window, resnet18_pa
 TINY = dict(n_classes=3, widths=(4, 8, 8, 8), blocks=(1, 1, 1, 1))
 
 
-def _tiny_weights(seed):
+def _tiny_weights(seed, hidden=0):
     rs = np.random.default_rng(seed)
-    net = ResNet18(**TINY)
-    flat = kaiming_resnet18_weights(seed, **TINY).astype(np.float64)
+    net = ResNet18(**TINY, hidden=hidden)
+    flat = kaiming_resnet18_weights(seed, **TINY, hidden=hidden).astype(np.float64)
     P = net.unpack(flat)
     for name in P:  # non-trivial BN parameters and statistics
         if name.endswith(".weight") and P[name].ndim == 1:
@@ -40,6 +40,77 @@ def _loss(net, P, x_prefix, labels, lowest):
     return nn.softmax_cross_entropy(logits, labels)[0]
 
 
+@pytest.mark.parametrize("hidden", [64, 1024])
+def test_hidden_head_spec(hidden):
+    """A hidden layer of h neurons replaces fc (512 * 6 + 6 parameters) by
+    fc.0 (512 h + h) and fc.2 (6 h + 6), in torch nn.Sequential's names."""
+    net = ResNet18(6, hidden=hidden)
+    gen = resnet18_param_spec(6, hidden=hidden)
+    assert [(n, tuple(s)) for n, s, _ in gen] == net.spec
+    assert net.n_weights() == 11_189_190 - 512 * 6 - 6 + 512 * hidden + hidden + 6 * hidden + 6
+    assert [n for n, _ in net.spec[-4:]] == ["fc.0.weight", "fc.0.bias", "fc.2.weight", "fc.2.bias"]
+    assert all(net.stage_of[n] == 5 for n, _ in net.spec[-4:])
+    w = kaiming_resnet18_weights(0, hidden=hidden)
+    P = net.unpack(w)
+    # torch.nn.Linear's default bounds, 1/sqrt(fan_in)
+    assert np.abs(P["fc.0.weight"]).max() <= 1 / math.sqrt(512)
+    assert np.abs(P["fc.2.weight"]).max() <= 1 / math.sqrt(hidden)
+    assert np.abs(P["fc.2.weight"]).max() > 0.9 / math.sqrt(hidden)
+
+
+def test_identity_hidden_layer_reduces_to_the_plain_classifier():
+    """Pooled features are non-negative (they average ReLU outputs), so a
+    hidden layer of 512 neurons with identity weights and zero bias passes
+    them through unchanged: logits, loss and the output layer's gradient equal
+    the plain classifier's with the same output weights, and the hidden
+    layer's weight gradient is the outer product of the data gradient with
+    the features."""
+    rs = np.random.default_rng(3)
+    f = np.maximum(rs.standard_normal((5, 512)), 0.0)
+    labels = np.array([0, 3, 5, 1, 1])
+    plain, mlp = ResNet18(6), ResNet18(6, hidden=512)
+    W, b = 0.05 * rs.standard_normal((6, 512)), 0.1 * rs.standard_normal(6)
+    P0 = {"fc.weight": W, "fc.bias": b}
+    P1 = {"fc.0.weight": np.eye(512), "fc.0.bias": np.zeros(512), "fc.2.weight": W, "fc.2.bias": b}
+    t0, t1 = {}, {}
+    z0 = plain.stage_forward(P0, 5, f, True, t0)
+    z1 = mlp.stage_forward(P1, 5, f, True, t1)
+    np.testing.assert_array_equal(z0, z1)
+    _, dz, _ = nn.softmax_cross_entropy(z0, labels)
+    g0, g1 = plain.backward(P0, dz, 5, t0), mlp.backward(P1, dz, 5, t1)
+    np.testing.assert_allclose(g1["fc.2.weight"], g0["fc.weight"], rtol=1e-13, atol=1e-16)
+    np.testing.assert_allclose(g1["fc.2.bias"], g0["fc.bias"], rtol=1e-13, atol=1e-16)
+    da = (dz @ W) * (f > 0)
+    np.testing.assert_allclose(g1["fc.0.weight"], da.T @ f, rtol=1e-12, atol=1e-15)
+
+
+def test_hidden_head_matches_torch_sequential():
+    """An independent torch float64 head, nn.Sequential(Linear, ReLU, Linear),
+    on pooled features: logits and every gradient."""
+    rs = np.random.default_rng(4)
+    f = np.maximum(rs.standard_normal((7, 512)), 0.0)
+    labels = np.array([0, 1, 2, 3, 4, 5, 0])
+    h = 96
+    net = ResNet18(6, hidden=h)
+    P = net.unpack(kaiming_resnet18_weights(2, hidden=h).astype(np.float64))
+    tape = {}
+    z = net.stage_forward(P, 5, f, True, tape)
+    _, dz, _ = nn.softmax_cross_entropy(z, labels)
+    g = net.backward(P, dz, 5, tape)
+    head = tnn.Sequential(tnn.Linear(512, h), tnn.ReLU(), tnn.Linear(h, 6)).double()
+    with torch.no_grad():
+        head[0].weight.copy_(torch.tensor(P["fc.0.weight"]))
+        head[0].bias.copy_(torch.tensor(P["fc.0.bias"]))
+        head[2].weight.copy_(torch.tensor(P["fc.2.weight"]))
+        head[2].bias.copy_(torch.tensor(P["fc.2.bias"]))
+    zt = head(torch.tensor(f))
+    F.cross_entropy(zt, torch.tensor(labels, dtype=torch.long)).backward()
+    np.testing.assert_allclose(z, zt.detach().numpy(), rtol=1e-12, atol=1e-14)
+    for name, t in [("fc.0.weight", head[0].weight), ("fc.0.bias", head[0].bias),
+                    ("fc.2.weight", head[2].weight), ("fc.2.bias", head[2].bias)]:
+        np.testing.assert_allclose(g[name], t.grad.numpy(), rtol=1e-10, atol=1e-14)
+
+
 def test_param_spec_agrees_with_generator():
     net = ResNet18(6)
     gen = resnet18_param_spec(6)
@@ -49,9 +120,9 @@ def test_param_spec_agrees_with_generator():
     assert trainable_all == 11_179_590
 
 
-@pytest.mark.parametrize("k", [1, 2, 3, 6])
-def test_tiny_resnet_gradients_match_finite_differences(k):
-    net, P = _tiny_weights(7)
+@pytest.mark.parametrize("k,hidden", [(1, 0), (2, 0), (3, 0), (6, 0), (1, 5), (2, 5), (6, 5)])
+def test_tiny_resnet_gradients_match_finite_differences(k, hidden):
+    net, P = _tiny_weights(7, hidden)
     rs = np.random.default_rng(11)
     x = rs.standard_normal((4, 16, 16, 3))
     labels = np.array([0, 1, 2, 1])
