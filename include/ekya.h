@@ -61,6 +61,7 @@ typedef enum {
 typedef enum { EKYA_FP32 = 0, EKYA_BF16 = 1 } ekya_precision;
 
 #define EKYA_MAX_EPOCHS 64
+#define EKYA_MAX_HIDDEN 4096
 
 typedef struct ekya_ctx ekya_ctx;
 
@@ -133,10 +134,22 @@ typedef struct {
  *    device, so concurrent work elsewhere on the GPU is delayed once.
  * EKYA_ERR_NOMEM if the arena cannot be allocated. */
 ekya_status ekya_create(ekya_ctx** out, int hip_device, int n_classes, size_t workspace_bytes);
+/* A context whose network has a hidden fully connected ReLU layer of
+ * `hidden` neurons (0 .. EKYA_MAX_HIDDEN; 0 is ekya_create) between the pooled
+ * features and the classifier: the number of neurons in the last layer, one
+ * of the knobs of a retraining configuration (sections 3.2 and 6.1).  The
+ * layer belongs to the classifier stage (trained whenever k_trainable >= 1).
+ * Canonical weights then end with fc.0.weight [hidden][512], fc.0.bias
+ * [hidden], fc.2.weight [n_classes][hidden], fc.2.bias [n_classes] (torch
+ * nn.Sequential names) in place of fc.weight and fc.bias; their length is
+ * ekya_weights_count_head(n_classes, hidden). */
+ekya_status ekya_create_head(ekya_ctx** out, int hip_device, int n_classes, int hidden,
+                             size_t workspace_bytes);
 /* Release everything the context owns (synchronises its streams first). */
 void ekya_destroy(ekya_ctx* ctx);
 /* Length in floats of the canonical weight array for `n_classes`. */
 size_t ekya_weights_count(int n_classes);
+size_t ekya_weights_count_head(int n_classes, int hidden);
 const char* ekya_status_str(ekya_status s);
 /* Message of the last failure on this context ("" if none). */
 const char* ekya_last_error(const ekya_ctx* ctx);
@@ -152,6 +165,13 @@ size_t ekya_retrain_workspace(int n_classes, int k_trainable, int n_frames, int 
 size_t ekya_profile_workspace(int n_classes, const ekya_profile_cfg* cfgs, int n_cfgs,
                               int n_frames, int H, int W, int n_heldout, int precision);
 size_t ekya_infer_workspace(int n_classes, int resolution, int precision);
+/* The same for a context made by ekya_create_head with `hidden` neurons. */
+size_t ekya_retrain_workspace_head(int n_classes, int hidden, int k_trainable, int n_frames, int H,
+                                   int W, int n_heldout, const ekya_train_opts* opts);
+size_t ekya_profile_workspace_head(int n_classes, int hidden, const ekya_profile_cfg* cfgs,
+                                   int n_cfgs, int n_frames, int H, int W, int n_heldout,
+                                   int precision);
+size_t ekya_infer_workspace_head(int n_classes, int hidden, int resolution, int precision);
 
 /* ------------------------------------------------------------ retrain
  * Retrain the last k_trainable stages (sections 3.1 and 4.3).

@@ -92,6 +92,9 @@ typedef struct ekya_model ekya_model;
  * its device memory (two slots, about 12 * 11.2 M bytes in bf16) here, none
  * later.  Empty until the first load. */
 ekya_status ekya_model_create(ekya_model** out, int hip_device, int n_classes, int precision);
+/* The same for a network with a hidden classifier layer (ekya_create_head). */
+ekya_status ekya_model_create_head(ekya_model** out, int hip_device, int n_classes, int hidden,
+                                   int precision);
 /* Waits for the model's queued work, then releases it.  A context that
  * checkpoints into it must stop first (ekya_set_checkpoint(ctx, NULL, 0)). */
 void ekya_model_destroy(ekya_model* m);
@@ -122,11 +125,30 @@ uint64_t ekya_model_version(ekya_model* m);
  * published slot when it starts and reports its version in version_out
  * (host, optional).  Labels equal bitwise those of ekya_infer with the
  * canonical weights that were published.  Asynchronous on `stream`.  The
- * model's device, class count and precision must be the context's and the
- * frames'. */
+ * model's device, class count and hidden layer must be the context's, its
+ * precision the frames'. */
 ekya_status ekya_infer_model(ekya_ctx* ctx, ekya_model* m, const void* frames, int n, int H, int W,
                              int resolution, int32_t* labels_out, void* stream,
                              uint64_t* version_out);
+
+/* Batched inference over several video streams, each with its own model
+ * (every stream's model is retrained on its own window, sections 3.1 and
+ * 4.1): frames (device, [sum counts, H, W, 3]) hold counts[i] (host, >= 0)
+ * consecutive frames of stream i, classified with models[i]'s published
+ * weights into labels_out (device int32, same order).  The streams' groups
+ * run on up to 4 streams of the context at once (forked from `stream` and
+ * joined back into it), each with its own buffers; each group takes its
+ * model's slot when the call starts and versions_out[i] (host, optional)
+ * receives its version.  Every model must have published weights and match
+ * the context (device, classes, hidden layer); all share one precision,
+ * the frames'.  Labels equal bitwise those of ekya_infer_model per stream.
+ * Asynchronous on `stream`. */
+ekya_status ekya_infer_models(ekya_ctx* ctx, ekya_model* const* models, int n_models,
+                              const void* frames, const int* counts, int H, int W, int resolution,
+                              int32_t* labels_out, uint64_t* versions_out, void* stream);
+/* Workspace bytes of ekya_infer_models with n_models models (host only). */
+size_t ekya_infer_models_workspace(int n_classes, int hidden, int resolution, int precision,
+                                   int n_models);
 
 /* Checkpointing during retraining: later ekya_retrain calls on ctx publish
  * the weights being trained into m, as ekya_model_load would, on the

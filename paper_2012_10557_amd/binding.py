@@ -99,6 +99,14 @@ _F = ctypes.c_float
 # name -> (restype, argtypes)
 _SIGS = {
     "ekya_create": (_I, [ctypes.POINTER(_P), _I, _I, ctypes.c_size_t]),
+    "ekya_create_head": (_I, [ctypes.POINTER(_P), _I, _I, _I, ctypes.c_size_t]),
+    "ekya_weights_count_head": (ctypes.c_size_t, [_I, _I]),
+    "ekya_retrain_workspace_head": (ctypes.c_size_t, [_I, _I, _I, _I, _I, _I, _I,
+                                                      ctypes.POINTER(TrainOpts)]),
+    "ekya_profile_workspace_head": (ctypes.c_size_t, [_I, _I, ctypes.POINTER(ProfileCfg), _I, _I,
+                                                      _I, _I, _I, _I]),
+    "ekya_infer_workspace_head": (ctypes.c_size_t, [_I, _I, _I, _I]),
+    "ekya_model_create_head": (_I, [ctypes.POINTER(_P), _I, _I, _I, _I]),
     "ekya_destroy": (None, [_P]),
     "ekya_weights_count": (ctypes.c_size_t, [_I]),
     "ekya_status_str": (ctypes.c_char_p, [_I]),
@@ -139,6 +147,8 @@ _SIGS = {
     "ekya_model_version": (ctypes.c_uint64, [_P]),
     "ekya_infer_model": (_I, [_P, _P, _P, _I, _I, _I, _I, _P, _P, ctypes.POINTER(ctypes.c_uint64)]),
     "ekya_set_checkpoint": (_I, [_P, _P, _I]),
+    "ekya_infer_models": (_I, [_P, _P, _I, _P, _P, _I, _I, _I, _P, _P, _P]),
+    "ekya_infer_models_workspace": (ctypes.c_size_t, [_I, _I, _I, _I, _I]),
     "ekya_op_conv2d": (_I, [_I, _P, _I, _I, _I, _I, _P, _I, _I, _I, _I, _I, _P, _P]),
     "ekya_op_conv2d_dgrad": (_I, [_I, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _I, _P, _P]),
     "ekya_op_conv2d_wgrad": (_I, [_I, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _I, _P, _P]),
@@ -220,10 +230,14 @@ def _stream(stream=None):
 
 
 # ------------------------------------------------------------ context
-def ekya_create(device: int = 0, n_classes: int = 6, workspace_bytes: int = 0):
+def ekya_create(device: int = 0, n_classes: int = 6, workspace_bytes: int = 0, hidden: int = 0):
+    """A context; hidden > 0 gives the network a hidden classifier layer."""
     lib = load()
     h = ctypes.c_void_p()
-    _check(lib.ekya_create(ctypes.byref(h), device, n_classes, workspace_bytes))
+    if hidden:
+        _check(lib.ekya_create_head(ctypes.byref(h), device, n_classes, hidden, workspace_bytes))
+    else:
+        _check(lib.ekya_create(ctypes.byref(h), device, n_classes, workspace_bytes))
     return h
 
 
@@ -238,28 +252,29 @@ def _profile_cfgs(cfgs: Sequence[dict]):
 def ekya_retrain_workspace(n_classes: int, k_trainable: int, n_frames: int, H: int, W: int,
                            n_heldout: int, subsample_frac: float, epochs: int, lr: float,
                            momentum: float = 0.9, batch: int = 64, seed: int = 0,
-                           precision: int = EKYA_BF16) -> int:
+                           precision: int = EKYA_BF16, hidden: int = 0) -> int:
     opts = TrainOpts(subsample_frac, epochs, lr, momentum, batch, seed, precision)
-    return int(load().ekya_retrain_workspace(n_classes, k_trainable, n_frames, H, W, n_heldout,
-                                             ctypes.byref(opts)))
+    return int(load().ekya_retrain_workspace_head(n_classes, hidden, k_trainable, n_frames, H, W,
+                                                  n_heldout, ctypes.byref(opts)))
 
 
 def ekya_profile_workspace(n_classes: int, cfgs: Sequence[dict], n_frames: int, H: int, W: int,
-                           n_heldout: int, precision: int = EKYA_BF16) -> int:
-    return int(load().ekya_profile_workspace(n_classes, _profile_cfgs(cfgs), len(cfgs), n_frames, H,
-                                             W, n_heldout, precision))
+                           n_heldout: int, precision: int = EKYA_BF16, hidden: int = 0) -> int:
+    return int(load().ekya_profile_workspace_head(n_classes, hidden, _profile_cfgs(cfgs), len(cfgs),
+                                                  n_frames, H, W, n_heldout, precision))
 
 
-def ekya_infer_workspace(n_classes: int, resolution: int, precision: int = EKYA_BF16) -> int:
-    return int(load().ekya_infer_workspace(n_classes, resolution, precision))
+def ekya_infer_workspace(n_classes: int, resolution: int, precision: int = EKYA_BF16,
+                         hidden: int = 0) -> int:
+    return int(load().ekya_infer_workspace_head(n_classes, hidden, resolution, precision))
 
 
 def ekya_destroy(ctx) -> None:
     load().ekya_destroy(ctx)
 
 
-def ekya_weights_count(n_classes: int = 6) -> int:
-    return int(load().ekya_weights_count(n_classes))
+def ekya_weights_count(n_classes: int = 6, hidden: int = 0) -> int:
+    return int(load().ekya_weights_count_head(n_classes, hidden))
 
 
 def ekya_set_kernel_timing(ctx, enable: bool) -> None:
@@ -426,9 +441,13 @@ def ekya_cu_ids(n_workgroups: int, stream=None):
     return out
 
 
-def ekya_model_create(device: int = 0, n_classes: int = 6, precision: int = EKYA_BF16):
+def ekya_model_create(device: int = 0, n_classes: int = 6, precision: int = EKYA_BF16,
+                      hidden: int = 0):
     h = ctypes.c_void_p()
-    _check(load().ekya_model_create(ctypes.byref(h), device, n_classes, precision))
+    if hidden:
+        _check(load().ekya_model_create_head(ctypes.byref(h), device, n_classes, hidden, precision))
+    else:
+        _check(load().ekya_model_create(ctypes.byref(h), device, n_classes, precision))
     return h
 
 
@@ -467,6 +486,31 @@ def ekya_infer_model(ctx, model, frames, resolution: int, labels_out=None, strea
                                    _dev(labels_out, torch.int32), _stream(stream), ctypes.byref(v)),
            ctx)
     return labels_out, int(v.value)
+
+
+def ekya_infer_models(ctx, models, frames, counts, resolution: int, labels_out=None, stream=None):
+    """(labels_out, versions): frames holds counts[i] consecutive frames of
+    stream i, classified with models[i]; asynchronous on the stream."""
+    import numpy as np
+    torch = _torch()
+    n, H, W, _ = frames.shape
+    if sum(counts) != n:
+        raise ValueError("counts must add up to the number of frames")
+    if labels_out is None:
+        labels_out = torch.empty(n, dtype=torch.int32, device=frames.device)
+    arr = (ctypes.c_void_p * len(models))(*[m.value for m in models])
+    cnt = np.ascontiguousarray(counts, dtype=np.int32)
+    ver = np.zeros(len(models), dtype=np.uint64)
+    _check(load().ekya_infer_models(ctx, arr, len(models), _dev(frames), cnt.ctypes.data, H, W,
+                                    resolution, _dev(labels_out, torch.int32), ver.ctypes.data,
+                                    _stream(stream)), ctx)
+    return labels_out, [int(v) for v in ver]
+
+
+def ekya_infer_models_workspace(n_classes: int, resolution: int, n_models: int,
+                                precision: int = EKYA_BF16, hidden: int = 0) -> int:
+    return int(load().ekya_infer_models_workspace(n_classes, hidden, resolution, precision,
+                                                  n_models))
 
 
 def ekya_set_checkpoint(ctx, model, every_epochs: int = 1) -> None:

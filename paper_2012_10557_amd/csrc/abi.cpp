@@ -53,10 +53,12 @@ ekya_status hip_status(hipError_t e) {
 
 extern "C" {
 
-size_t ekya_weights_count(int n_classes) {
-  if (n_classes < 1 || n_classes > 1024) return 0;
-  return (size_t)ekya::Net::build(n_classes, 0).total;
+size_t ekya_weights_count_head(int n_classes, int hidden) {
+  if (n_classes < 1 || n_classes > 1024 || hidden < 0 || hidden > EKYA_MAX_HIDDEN) return 0;
+  return (size_t)ekya::Net::build(n_classes, 0, hidden).total;
 }
+
+size_t ekya_weights_count(int n_classes) { return ekya_weights_count_head(n_classes, 0); }
 
 const char* ekya_status_str(ekya_status s) {
   switch (s) {
@@ -75,10 +77,17 @@ const char* ekya_last_error(const ekya_ctx* ctx) {
 }
 
 ekya_status ekya_create(ekya_ctx** out, int hip_device, int n_classes, size_t workspace_bytes) {
+  return ekya_create_head(out, hip_device, n_classes, 0, workspace_bytes);
+}
+
+ekya_status ekya_create_head(ekya_ctx** out, int hip_device, int n_classes, int hidden,
+                             size_t workspace_bytes) {
   if (!out) return fail(nullptr, EKYA_ERR_INVALID_ARG, "out is null");
   *out = nullptr;
   if (n_classes < 1 || n_classes > 1024)
     return fail(nullptr, EKYA_ERR_INVALID_ARG, "n_classes must be in [1, 1024]");
+  if (hidden < 0 || hidden > EKYA_MAX_HIDDEN)
+    return fail(nullptr, EKYA_ERR_INVALID_ARG, "hidden must be in [0, EKYA_MAX_HIDDEN]");
   int n = 0;
   if (hipGetDeviceCount(&n) != hipSuccess || n == 0)
     return fail(nullptr, EKYA_ERR_HIP, "no HIP device available");
@@ -86,7 +95,7 @@ ekya_status ekya_create(ekya_ctx** out, int hip_device, int n_classes, size_t wo
     return fail(nullptr, EKYA_ERR_INVALID_ARG, "hip_device out of range");
   ekya_ctx* c = new (std::nothrow) ekya_ctx();
   if (!c) return fail(nullptr, EKYA_ERR_NOMEM, "host allocation failed");
-  hipError_t e = ekya::ctx_init(c->c, hip_device, n_classes, workspace_bytes);
+  hipError_t e = ekya::ctx_init(c->c, hip_device, n_classes, hidden, workspace_bytes);
   if (e != hipSuccess) {
     ekya::ctx_free(c->c);
     delete c;
@@ -151,13 +160,18 @@ ekya_status ekya_retrain(ekya_ctx* ctx, float* weights, int k_trainable, const v
                            (hipStream_t)stream);
 }
 
-size_t ekya_retrain_workspace(int n_classes, int k_trainable, int n_frames, int H, int W,
-                              int n_heldout, const ekya_train_opts* opts) {
-  if (n_classes < 1 || n_classes > 1024 ||
+size_t ekya_retrain_workspace_head(int n_classes, int hidden, int k_trainable, int n_frames, int H,
+                                   int W, int n_heldout, const ekya_train_opts* opts) {
+  if (n_classes < 1 || n_classes > 1024 || hidden < 0 || hidden > EKYA_MAX_HIDDEN ||
       check_retrain_args(nullptr, k_trainable, n_frames, H, W, n_heldout, opts) != EKYA_OK)
     return 0;
-  const ekya::Net net = ekya::Net::build(n_classes, opts->precision);
+  const ekya::Net net = ekya::Net::build(n_classes, opts->precision, hidden);
   return ekya::retrain_workspace_bytes(net, k_trainable, n_frames, H, W, n_heldout, *opts);
+}
+
+size_t ekya_retrain_workspace(int n_classes, int k_trainable, int n_frames, int H, int W,
+                              int n_heldout, const ekya_train_opts* opts) {
+  return ekya_retrain_workspace_head(n_classes, 0, k_trainable, n_frames, H, W, n_heldout, opts);
 }
 
 // Sizes and candidates of a profiling call (pointers checked by the caller).
@@ -197,13 +211,20 @@ ekya_status ekya_profile(ekya_ctx* ctx, const float* weights, const ekya_profile
                            concurrent, results);
 }
 
-size_t ekya_profile_workspace(int n_classes, const ekya_profile_cfg* cfgs, int n_cfgs,
-                              int n_frames, int H, int W, int n_heldout, int precision) {
-  if (n_classes < 1 || n_classes > 1024 ||
+size_t ekya_profile_workspace_head(int n_classes, int hidden, const ekya_profile_cfg* cfgs,
+                                   int n_cfgs, int n_frames, int H, int W, int n_heldout,
+                                   int precision) {
+  if (n_classes < 1 || n_classes > 1024 || hidden < 0 || hidden > EKYA_MAX_HIDDEN ||
       check_profile_args(nullptr, cfgs, n_cfgs, n_frames, H, W, n_heldout, precision) != EKYA_OK)
     return 0;
-  const ekya::Net net = ekya::Net::build(n_classes, precision);
+  const ekya::Net net = ekya::Net::build(n_classes, precision, hidden);
   return ekya::profile_workspace_bytes(net, cfgs, n_cfgs, n_frames, H, W, n_heldout);
+}
+
+size_t ekya_profile_workspace(int n_classes, const ekya_profile_cfg* cfgs, int n_cfgs,
+                              int n_frames, int H, int W, int n_heldout, int precision) {
+  return ekya_profile_workspace_head(n_classes, 0, cfgs, n_cfgs, n_frames, H, W, n_heldout,
+                                     precision);
 }
 
 ekya_status ekya_infer(ekya_ctx* ctx, const float* weights, const void* frames, int n, int H,
@@ -222,12 +243,16 @@ ekya_status ekya_infer(ekya_ctx* ctx, const float* weights, const void* frames, 
                          (hipStream_t)stream);
 }
 
-size_t ekya_infer_workspace(int n_classes, int resolution, int precision) {
-  if (n_classes < 1 || n_classes > 1024 || resolution < 32 || resolution > 4096 ||
-      !valid_precision(precision))
+size_t ekya_infer_workspace_head(int n_classes, int hidden, int resolution, int precision) {
+  if (n_classes < 1 || n_classes > 1024 || hidden < 0 || hidden > EKYA_MAX_HIDDEN ||
+      resolution < 32 || resolution > 4096 || !valid_precision(precision))
     return 0;
-  const ekya::Net net = ekya::Net::build(n_classes, precision);
+  const ekya::Net net = ekya::Net::build(n_classes, precision, hidden);
   return ekya::infer_workspace_bytes(net, resolution);
+}
+
+size_t ekya_infer_workspace(int n_classes, int resolution, int precision) {
+  return ekya_infer_workspace_head(n_classes, 0, resolution, precision);
 }
 
 ekya_status ekya_set_kernel_timing(ekya_ctx* ctx, int enable) {
@@ -783,10 +808,17 @@ ekya_status ekya_cu_ids(int n_workgroups, uint32_t* ids_out, void* stream) {
 }
 
 ekya_status ekya_model_create(ekya_model** out, int hip_device, int n_classes, int precision) {
+  return ekya_model_create_head(out, hip_device, n_classes, 0, precision);
+}
+
+ekya_status ekya_model_create_head(ekya_model** out, int hip_device, int n_classes, int hidden,
+                                   int precision) {
   if (!out) return fail(nullptr, EKYA_ERR_INVALID_ARG, "out is null");
   *out = nullptr;
   if (n_classes < 1 || n_classes > 1024)
     return fail(nullptr, EKYA_ERR_INVALID_ARG, "n_classes must be in [1, 1024]");
+  if (hidden < 0 || hidden > EKYA_MAX_HIDDEN)
+    return fail(nullptr, EKYA_ERR_INVALID_ARG, "hidden must be in [0, EKYA_MAX_HIDDEN]");
   if (!valid_precision(precision))
     return fail(nullptr, EKYA_ERR_INVALID_ARG, "precision must be EKYA_FP32 or EKYA_BF16");
   int n = 0;
@@ -796,7 +828,7 @@ ekya_status ekya_model_create(ekya_model** out, int hip_device, int n_classes, i
     return fail(nullptr, EKYA_ERR_INVALID_ARG, "hip_device out of range");
   ekya_model* m = new (std::nothrow) ekya_model();
   if (!m) return fail(nullptr, EKYA_ERR_NOMEM, "host allocation failed");
-  hipError_t e = ekya::model_init(m->m, hip_device, n_classes, precision);
+  hipError_t e = ekya::model_init(m->m, hip_device, n_classes, hidden, precision);
   if (e != hipSuccess) {
     ekya::model_free(m->m);
     delete m;
@@ -839,8 +871,10 @@ ekya_status ekya_infer_model(ekya_ctx* ctx, ekya_model* m, const void* frames, i
   if (!ctx) return fail(nullptr, EKYA_ERR_INVALID_ARG, "ctx is null");
   if (!m) return fail(ctx, EKYA_ERR_INVALID_ARG, "model is null");
   if (n < 0 || n > (1 << 26)) return fail(ctx, EKYA_ERR_INVALID_ARG, "n must be in [0, 2^26]");
-  if (m->m.device != ctx->c.device || m->m.n_classes != ctx->c.n_classes)
-    return fail(ctx, EKYA_ERR_INVALID_ARG, "the model's device or class count differs from the context's");
+  if (m->m.device != ctx->c.device || m->m.n_classes != ctx->c.n_classes ||
+      m->m.hidden != ctx->c.hidden)
+    return fail(ctx, EKYA_ERR_INVALID_ARG,
+                "the model's device, class count or hidden layer differs from the context's");
   if (ekya_model_version(m) == 0)
     return fail(ctx, EKYA_ERR_INVALID_ARG, "the model has no published weights (call ekya_model_load first)");
   if (n == 0) return EKYA_OK;
@@ -853,13 +887,58 @@ ekya_status ekya_infer_model(ekya_ctx* ctx, ekya_model* m, const void* frames, i
                                (hipStream_t)stream, version_out);
 }
 
+ekya_status ekya_infer_models(ekya_ctx* ctx, ekya_model* const* models, int n_models,
+                              const void* frames, const int* counts, int H, int W, int resolution,
+                              int32_t* labels_out, uint64_t* versions_out, void* stream) {
+  if (!ctx) return fail(nullptr, EKYA_ERR_INVALID_ARG, "ctx is null");
+  if (!models || !counts) return fail(ctx, EKYA_ERR_INVALID_ARG, "null pointer argument");
+  if (n_models < 1 || n_models > 4096)
+    return fail(ctx, EKYA_ERR_INVALID_ARG, "n_models must be in [1, 4096]");
+  long long total = 0;
+  std::vector<ekya::Model*> ms(n_models);
+  for (int i = 0; i < n_models; ++i) {
+    if (!models[i]) return fail(ctx, EKYA_ERR_INVALID_ARG, "a model is null");
+    const ekya::Model& m = models[i]->m;
+    if (m.device != ctx->c.device || m.n_classes != ctx->c.n_classes || m.hidden != ctx->c.hidden)
+      return fail(ctx, EKYA_ERR_INVALID_ARG,
+                  "a model's device, class count or hidden layer differs from the context's");
+    if (m.dt != models[0]->m.dt)
+      return fail(ctx, EKYA_ERR_INVALID_ARG, "the models' precisions differ");
+    if (ekya_model_version(models[i]) == 0)
+      return fail(ctx, EKYA_ERR_INVALID_ARG, "a model has no published weights");
+    if (counts[i] < 0) return fail(ctx, EKYA_ERR_INVALID_ARG, "counts must be >= 0");
+    total += counts[i];
+    ms[i] = &models[i]->m;
+  }
+  if (total > (1 << 26)) return fail(ctx, EKYA_ERR_INVALID_ARG, "more than 2^26 frames");
+  if (total > 0 && (!frames || !labels_out))
+    return fail(ctx, EKYA_ERR_INVALID_ARG, "null pointer argument");
+  if (ekya_status s = check_frames(ctx, H, W)) return s;
+  if (resolution < 32 || resolution > 4096)
+    return fail(ctx, EKYA_ERR_INVALID_ARG, "resolution must be in [32, 4096]");
+  ctx->c.err.clear();
+  return ekya::run_infer_models(ctx->c, ms.data(), n_models, frames, counts, H, W, resolution,
+                                labels_out, versions_out, (hipStream_t)stream);
+}
+
+size_t ekya_infer_models_workspace(int n_classes, int hidden, int resolution, int precision,
+                                   int n_models) {
+  if (n_classes < 1 || n_classes > 1024 || hidden < 0 || hidden > EKYA_MAX_HIDDEN ||
+      resolution < 32 || resolution > 4096 || !valid_precision(precision) || n_models < 1 ||
+      n_models > 4096)
+    return 0;
+  const ekya::Net net = ekya::Net::build(n_classes, precision, hidden);
+  return ekya::infer_models_workspace_bytes(net, resolution, n_models);
+}
+
 ekya_status ekya_set_checkpoint(ekya_ctx* ctx, ekya_model* m, int every_epochs) {
   if (!ctx) return fail(nullptr, EKYA_ERR_INVALID_ARG, "ctx is null");
   if (m) {
     if (every_epochs < 1) return fail(ctx, EKYA_ERR_INVALID_ARG, "every_epochs must be >= 1");
-    if (m->m.device != ctx->c.device || m->m.n_classes != ctx->c.n_classes)
+    if (m->m.device != ctx->c.device || m->m.n_classes != ctx->c.n_classes ||
+        m->m.hidden != ctx->c.hidden)
       return fail(ctx, EKYA_ERR_INVALID_ARG,
-                  "the model's device or class count differs from the context's");
+                  "the model's device, class count or hidden layer differs from the context's");
   }
   ctx->c.ckpt = m ? &m->m : nullptr;
   ctx->c.ckpt_every = m ? every_epochs : 0;

@@ -2019,6 +2019,18 @@ hipError_t permute_weights(const float* src, float* dst, const long long* tab, i
   return hipGetLastError();
 }
 
+__global__ void relu_f32_kernel(float* y, const float* x, const float* mask, long long n) {
+  for (long long i = blockIdx.x * (long long)blockDim.x + threadIdx.x; i < n;
+       i += (long long)gridDim.x * blockDim.x)
+    y[i] = mask ? (mask[i] > 0.f ? x[i] : 0.f) : fmaxf(x[i], 0.f);
+}
+
+hipError_t relu_f32(float* y, const float* x, const float* mask, long long n, hipStream_t stream) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(relu_f32_kernel, dim3(grid_for(n)), dim3(256), 0, stream, y, x, mask, n);
+  return hipGetLastError();
+}
+
 // Hardware registers read with s_getreg_b32 (hwreg(id, offset, size) is
 // id | offset << 6 | (size - 1) << 11): HW_ID (4) holds the CU in bits 11:8,
 // the shader array in bit 12 and the shader engine in bits 14:13; XCC_ID (20)

@@ -227,6 +227,9 @@ hipError_t head_backward(int dt, const float* z, const int32_t* labels, const in
 hipError_t count_correct(const float* z, const int32_t* labels, int N, int J, int32_t* count,
                          hipStream_t stream);
 hipError_t argmax_rows(const float* z, int N, int J, int32_t* out, hipStream_t stream);
+// y = max(x, 0) (mask null) or y = x where mask > 0, else 0 (the ReLU
+// backward through the ReLU's output), over n fp32 values; y may be x.
+hipError_t relu_f32(float* y, const float* x, const float* mask, long long n, hipStream_t stream);
 
 // -------------------------------------------------------------- optimiser
 // v = mu v + g; w = w - lr v over n floats.

@@ -4,10 +4,11 @@
 
 namespace ekya {
 
-Net Net::build(int n_classes, int dt) {
+Net Net::build(int n_classes, int dt, int hidden) {
   Net n;
   n.n_classes = n_classes;
   n.dt = dt;
+  n.hidden = hidden;
   long long off = 0, sh = 0, bnc = 0;
   const int vec = dtype_vec(dt);
 
@@ -68,8 +69,14 @@ Net Net::build(int n_classes, int dt) {
     }
   }
   n.stage_begin[5] = off;
+  if (hidden > 0) {  // fc.0 (hidden x 512), fc.2 (classes x hidden)
+    n.fc1_w = off;
+    off += (long long)hidden * 512;
+    n.fc1_b = off;
+    off += hidden;
+  }
   n.fc_w = off;
-  off += (long long)n_classes * 512;
+  off += (long long)n_classes * n.head_in();
   n.fc_b = off;
   off += n_classes;
   n.stage_begin[6] = off;

@@ -4,7 +4,10 @@
 // paper's ResNet reference), torchvision's ResNet18: a 7x7/2 stem conv with
 // BatchNorm, ReLU and 3x3/2 max pooling; four stages of two BasicBlocks
 // (widths 64/128/256/512, stride 2 entering stages 2-4 with a 1x1/2
-// projection shortcut); global average pooling; an affine classifier.
+// projection shortcut); global average pooling; an affine classifier, or
+// (hidden > 0, the number of neurons in the last layer that retraining
+// configurations vary, sections 3.2 and 6.1) a hidden fully connected ReLU
+// layer of `hidden` neurons and then the classifier.
 // Stages (the unit of freezing, section 3.1): 0 stem, 1-4 layer1-4, 5 fc.
 //
 // Parameter offsets follow the canonical flat layout (torchvision state_dict
@@ -44,13 +47,16 @@ struct Net {
   std::vector<ConvL> conv;
   std::vector<BnL> bn;
   std::vector<BlockL> blk;
-  long long fc_w = 0, fc_b = 0, total = 0;
+  int hidden = 0;                    // neurons of the hidden classifier layer (0: none)
+  long long fc1_w = -1, fc1_b = -1;  // hidden layer [hidden][512], [hidden]
+  long long fc_w = 0, fc_b = 0, total = 0;  // output layer [classes][head_in()], [classes]
   long long stage_begin[7] = {0};  // first parameter offset of each stage; [6] = total
   long long bn_channels = 0;       // sum of C over all BatchNorm layers
   long long shadow_elems = 0;
   int widths[4] = {64, 128, 256, 512};
 
-  static Net build(int n_classes, int dt);
+  static Net build(int n_classes, int dt, int hidden = 0);
+  int head_in() const { return hidden > 0 ? hidden : 512; }
 
   // Host tables for the kernels (see kernels.hpp for row formats).
   std::vector<long long> permute_table() const;              // every tensor

@@ -106,12 +106,13 @@ static hipError_t upload_tables(const Net& net, Tables& t) {
   return hipSuccess;
 }
 
-hipError_t ctx_init(Ctx& c, int device, int n_classes, size_t workspace_bytes) {
+hipError_t ctx_init(Ctx& c, int device, int n_classes, int hidden, size_t workspace_bytes) {
   c.device = device;
   c.n_classes = n_classes;
+  c.hidden = hidden;
   EKYA_HIP(hipSetDevice(device));
   for (int dt = 0; dt < 2; ++dt) {
-    c.net[dt] = Net::build(n_classes, dt);
+    c.net[dt] = Net::build(n_classes, dt, hidden);
     EKYA_HIP(upload_tables(c.net[dt], c.tabs[dt]));
   }
   EKYA_HIP(hipEventCreateWithFlags(&c.last_done, hipEventDisableTiming));
@@ -172,8 +173,16 @@ void ctx_free(Ctx& c) {
   c.timer.pool.clear();
   for (hipStream_t s : c.streams) (void)hipStreamDestroy(s);
   c.streams.clear();
+  for (hipStream_t s : c.lanes) (void)hipStreamDestroy(s);
+  c.lanes.clear();
   if (c.eval_stream) (void)hipStreamDestroy(c.eval_stream);
   c.eval_stream = nullptr;
+  if (c.lane_fork) (void)hipEventDestroy(c.lane_fork);
+  c.lane_fork = nullptr;
+  for (hipEvent_t& e : c.lane_join) {
+    if (e) (void)hipEventDestroy(e);
+    e = nullptr;
+  }
   if (c.last_done) (void)hipEventDestroy(c.last_done);
   c.last_done = nullptr;
   c.ws.release();
@@ -191,9 +200,12 @@ hipError_t ctx_reset_streams(Ctx& c) {
   EKYA_HIP(hipSetDevice(c.device));
   EKYA_HIP(hipEventSynchronize(c.last_done));
   for (hipStream_t s : c.streams) EKYA_HIP(hipStreamSynchronize(s));
+  for (hipStream_t s : c.lanes) EKYA_HIP(hipStreamSynchronize(s));
   if (c.eval_stream) EKYA_HIP(hipStreamSynchronize(c.eval_stream));
   for (hipStream_t s : c.streams) (void)hipStreamDestroy(s);
   c.streams.clear();
+  for (hipStream_t s : c.lanes) (void)hipStreamDestroy(s);
+  c.lanes.clear();
   if (c.eval_stream) (void)hipStreamDestroy(c.eval_stream);
   c.eval_stream = nullptr;
   return hipSuccess;
@@ -271,6 +283,7 @@ hipError_t create_masked_stream(const std::vector<uint32_t>& mask, hipStream_t* 
 struct EvalBufs {
   void *p0 = nullptr, *p1 = nullptr, *t1 = nullptr, *sc = nullptr;
   float* pooled = nullptr;
+  float* hid = nullptr;  // hidden classifier layer's activations
   float* logits = nullptr;
   float* ws = nullptr;  // split-reduction partials of the forward convs
   size_t ws_floats = 0;
@@ -298,6 +311,7 @@ static void plan_eval(Arena& a, const Net& net, const Geo& g, int lo, int hi, in
   b.t1 = a.take_bytes(m * es);
   b.sc = a.take_bytes(m * es);
   b.pooled = a.take<float>((size_t)cap * 512);
+  if (net.hidden > 0) b.hid = a.take<float>((size_t)cap * net.hidden);
   b.logits = a.take<float>((size_t)cap * net.n_classes);
   // split-reduction scratch for every frame count a call may use, so that a
   // convolution's plan never depends on how large this scratch happens to be
@@ -411,8 +425,14 @@ static hipError_t eval_forward(const Net& net, const Geo& g, const void* shadow,
         cur = pd;
       }
     } else {  // s == 5
-      EKYA_HIP(fc_fwd(reinterpret_cast<const float*>(cur), master + net.fc_w, master + net.fc_b, n,
-                      512, net.n_classes, reinterpret_cast<float*>(out), st));
+      const float* f = reinterpret_cast<const float*>(cur);
+      if (net.hidden > 0) {
+        EKYA_HIP(fc_fwd(f, master + net.fc1_w, master + net.fc1_b, n, 512, net.hidden, b.hid, st));
+        EKYA_HIP(relu_f32(b.hid, b.hid, nullptr, (long long)n * net.hidden, st));
+        f = b.hid;
+      }
+      EKYA_HIP(fc_fwd(f, master + net.fc_w, master + net.fc_b, n, net.head_in(), net.n_classes,
+                      reinterpret_cast<float*>(out), st));
     }
   }
   return hipSuccess;
@@ -479,6 +499,7 @@ struct TrainJob {
   // yet (-1: none); see settle()
   int pending_join = -1;
   float *pooled = nullptr, *logits = nullptr, *dz = nullptr, *dpooled = nullptr;
+  float *hid = nullptr, *dhid = nullptr;  // hidden classifier layer: activations, gradient
   float* ws = nullptr;         // split-K partials
   size_t ws_floats = 0;
   float* bn_ws = nullptr;      // BatchNorm partials
@@ -601,6 +622,10 @@ static void plan_job(Arena& a, TrainJob& j) {
   }
   j.pooled = a.take<float>((size_t)j.B * 512);
   j.dpooled = a.take<float>((size_t)j.B * 512);
+  if (net.hidden > 0) {
+    j.hid = a.take<float>((size_t)j.B * net.hidden);
+    j.dhid = a.take<float>((size_t)j.B * net.hidden);
+  }
   j.logits = a.take<float>((size_t)j.B * net.n_classes);
   j.dz = a.take<float>((size_t)j.B * net.n_classes);
   j.ws_floats = ws_floats(j);
@@ -634,6 +659,24 @@ static void plan_job(Arena& a, TrainJob& j) {
 }
 
 static inline float* bnp(float* base, const BnL& b) { return base + b.st; }
+
+// Average pool (x: layer4's output; null: the pooled features in x0) and
+// the classifier: pooled and logits, or with a hidden layer the pooled
+// features, the hidden layer's ReLU activations and the logits.
+static hipError_t train_head_forward(TrainJob& j, int nb, const void* x) {
+  const Net& net = *j.net;
+  const int hw = j.geo.lh[4] * j.geo.lw[4];
+  const float* f = x ? nullptr : reinterpret_cast<const float*>(j.x0);
+  float* pooled = x ? j.pooled : nullptr;
+  if (net.hidden == 0)
+    return head_forward(j.dt, x, hw, f, j.master + net.fc_w, j.master + net.fc_b, nb, 512,
+                        net.n_classes, pooled, j.logits, j.st);
+  EKYA_HIP(head_forward(j.dt, x, hw, f, j.master + net.fc1_w, j.master + net.fc1_b, nb, 512,
+                        net.hidden, pooled, j.hid, j.st));
+  EKYA_HIP(relu_f32(j.hid, j.hid, nullptr, (long long)nb * net.hidden, j.st));
+  return fc_fwd(j.hid, j.master + net.fc_w, j.master + net.fc_b, nb, net.hidden, net.n_classes,
+                j.logits, j.st);
+}
 
 // Train-mode forward of stages lowest..5 on the batch in x0 (nb frames).
 static hipError_t train_forward(TrainJob& j, int nb) {
@@ -717,11 +760,9 @@ static hipError_t train_forward(TrainJob& j, int nb) {
       cur = t.OUT;
     }
     if (s == 4)  // average pool + classifier in one kernel
-      return head_forward(dt, cur, j.geo.lh[4] * j.geo.lw[4], nullptr, j.master + net.fc_w,
-                          j.master + net.fc_b, nb, 512, net.n_classes, j.pooled, j.logits, st);
+      return train_head_forward(j, nb, cur);
   }
-  return head_forward(dt, nullptr, 0, reinterpret_cast<const float*>(j.x0), j.master + net.fc_w,
-                      j.master + net.fc_b, nb, 512, net.n_classes, nullptr, j.logits, st);
+  return train_head_forward(j, nb, nullptr);
 }
 
 // Loss of the batch (labels through fid, loss / correct / flag into ce) and
@@ -737,7 +778,17 @@ static hipError_t train_backward(TrainJob& j, int nb, const int32_t* fid, float*
   void* gA = j.g[5];
   const int hw = j.geo.lh[4] * j.geo.lw[4];
   int head_ready = 0;  // rows per chunk of the last BatchNorm's backward partials in bn_ws
-  if (head_backward_fused(net.n_classes, 512)) {
+  if (net.hidden > 0) {
+    // softmax cross-entropy, the output layer, the hidden layer's ReLU, the
+    // hidden layer, then the average-pool backward
+    EKYA_HIP(softmax_ce(j.logits, j.labels, fid, nb, net.n_classes, j.dz, ce, st));
+    EKYA_HIP(fc_bwd(j.dz, j.hid, j.master + net.fc_w, nb, net.hidden, net.n_classes,
+                    j.grad + net.fc_w, j.grad + net.fc_b, j.dhid, st));
+    EKYA_HIP(relu_f32(j.dhid, j.dhid, j.hid, (long long)nb * net.hidden, st));
+    EKYA_HIP(fc_bwd(j.dhid, f, j.master + net.fc1_w, nb, 512, net.hidden, j.grad + net.fc1_w,
+                    j.grad + net.fc1_b, j.lowest == 5 ? nullptr : j.dpooled, st));
+    if (j.lowest < 5) EKYA_HIP(avgpool_bwd(dt, j.dpooled, nb, hw, 512, dout, st));
+  } else if (head_backward_fused(net.n_classes, 512)) {
     // softmax cross-entropy, classifier gradients and average-pool backward
     // (with the backward partials of the last block's output BatchNorm)
     HeadBnSink hb;
@@ -1676,12 +1727,13 @@ ekya_status run_infer(Ctx& c, const float* weights, const void* frames, int n, i
 }
 
 // ------------------------------------------------------------ hot reload
-hipError_t model_init(Model& m, int device, int n_classes, int dt) {
+hipError_t model_init(Model& m, int device, int n_classes, int hidden, int dt) {
   m.device = device;
   m.n_classes = n_classes;
+  m.hidden = hidden;
   m.dt = dt;
   EKYA_HIP(hipSetDevice(device));
-  m.net = Net::build(n_classes, dt);
+  m.net = Net::build(n_classes, dt, hidden);
   EKYA_HIP(upload_tables(m.net, m.tabs));
   Arena a;
   for (int i = 0; i < 2; ++i) {
@@ -1772,6 +1824,87 @@ hipError_t model_export(Model& m, float* canonical_out, hipStream_t stream, uint
   EKYA_HIP(model_note_use(m, m.current, stream));
   if (version) *version = sl.version;
   return hipSuccess;
+}
+
+// Inference for several streams' models in one call: the frames of model i
+// are counts[i] consecutive frames.  The models' groups run on up to
+// kInferLanes streams of the context (forked from `stream`, joined back),
+// each lane with its own buffers; lane l takes groups l, l + lanes, ...
+static constexpr int kInferLanes = 4;
+
+static_assert(kInferLanes <= (int)(sizeof(Ctx::lane_join) / sizeof(hipEvent_t)),
+              "a join event per lane");
+
+static int infer_lanes(int n_models) { return std::max(1, std::min(n_models, kInferLanes)); }
+
+size_t infer_models_workspace_bytes(const Net& net, int resolution, int n_models) {
+  InferBufs b;
+  Arena a;
+  const Geo g = Geo::build(net, resolution, resolution);
+  for (int l = 0; l < infer_lanes(n_models); ++l) plan_infer(a, net, g, resolution, b, false);
+  return a.used;
+}
+
+ekya_status run_infer_models(Ctx& c, Model* const* models, int n_models, const void* frames,
+                             const int* counts, int H, int W, int resolution, int32_t* labels_out,
+                             uint64_t* versions, hipStream_t stream) {
+  EKYA_CHECK_HIP(hipSetDevice(c.device));
+  TimerGuard tg(c);
+  const int dt = models[0]->dt;
+  const Net& net = c.net[dt];
+  const Geo geo = Geo::build(net, resolution, resolution);
+  const int lanes = infer_lanes(n_models);
+  {
+    Arena meas;
+    InferBufs b;
+    for (int l = 0; l < lanes; ++l) plan_infer(meas, net, geo, resolution, b, false);
+    if (ekya_status s = acquire_workspace(c, meas.used, stream)) return s;
+  }
+  while ((int)c.lanes.size() < lanes) {
+    hipStream_t s;
+    EKYA_CHECK_HIP(ctx_stream(c, &s));
+    c.lanes.push_back(s);
+  }
+  if (!c.lane_fork) {
+    EKYA_CHECK_HIP(hipEventCreateWithFlags(&c.lane_fork, hipEventDisableTiming));
+    for (int l = 0; l < kInferLanes; ++l)
+      EKYA_CHECK_HIP(hipEventCreateWithFlags(&c.lane_join[l], hipEventDisableTiming));
+  }
+  Arena real;
+  real.base = reinterpret_cast<char*>(c.ws.p);
+  std::vector<InferBufs> ib(lanes);
+  for (int l = 0; l < lanes; ++l) plan_infer(real, net, geo, resolution, ib[l], false);
+  const long long fbytes = (long long)H * W * 3 * dtype_size(dt);
+  std::vector<long long> first(n_models + 1, 0);
+  for (int i = 0; i < n_models; ++i) first[i + 1] = first[i] + counts[i];
+  auto run = [&]() -> hipError_t {
+    EKYA_HIP(hipEventRecord(c.lane_fork, stream));
+    for (int l = 0; l < lanes; ++l) EKYA_HIP(hipStreamWaitEvent(c.lanes[l], c.lane_fork, 0));
+    for (int i = 0; i < n_models; ++i) {
+      const int l = i % lanes;
+      hipStream_t q = c.lanes[l];
+      Model& m = *models[i];
+      std::lock_guard<std::mutex> lk(m.mu);  // take, read and mark the slot together
+      const int s = m.current;
+      ModelSlot& sl = m.slot[s];
+      EKYA_HIP(hipStreamWaitEvent(q, sl.ready, 0));
+      if (counts[i] > 0)
+        EKYA_HIP(infer_frames(net, geo, sl.master, sl.fold, sl.shadow,
+                              reinterpret_cast<const char*>(frames) + first[i] * fbytes, counts[i],
+                              H, W, resolution, labels_out + first[i], ib[l], q));
+      EKYA_HIP(model_note_use(m, s, q));
+      if (versions) versions[i] = sl.version;
+    }
+    for (int l = 0; l < lanes; ++l) {
+      EKYA_HIP(hipEventRecord(c.lane_join[l], c.lanes[l]));
+      EKYA_HIP(hipStreamWaitEvent(stream, c.lane_join[l], 0));
+    }
+    return hipSuccess;
+  };
+  hipError_t he = run();
+  (void)hipEventRecord(c.last_done, stream);
+  EKYA_CHECK_HIP(he);
+  return EKYA_OK;
 }
 
 ekya_status run_infer_model(Ctx& c, Model& m, const void* frames, int n, int H, int W,

@@ -77,6 +77,7 @@ struct ModelSlot {
 struct Model {
   int device = 0;
   int n_classes = 0;
+  int hidden = 0;
   int dt = 0;
   Net net;
   Tables tabs;
@@ -88,7 +89,7 @@ struct Model {
   std::mutex mu;                 // guards everything above after init
 };
 
-hipError_t model_init(Model& m, int device, int n_classes, int dt);
+hipError_t model_init(Model& m, int device, int n_classes, int hidden, int dt);
 void model_free(Model& m);
 // Fill the unpublished slot on `stream` from canonical weights (canonical !=
 // null) or from internal-layout fp32 weights (internal), then publish it.
@@ -113,6 +114,7 @@ struct KernelStat {
 struct Ctx {
   int device = 0;
   int n_classes = 0;
+  int hidden = 0;  // neurons of the hidden classifier layer (0: none)
   std::string err;
   Net net[2];
   Tables tabs[2];
@@ -128,6 +130,10 @@ struct Ctx {
   hipEvent_t last_done = nullptr;
   std::vector<hipStream_t> streams;  // profiler streams (default priority)
   hipStream_t eval_stream = nullptr;  // retraining's held-out evaluation (default priority)
+  // inference lanes of ekya_infer_models, and their fork / join events
+  std::vector<hipStream_t> lanes;
+  hipEvent_t lane_fork = nullptr;
+  hipEvent_t lane_join[4] = {nullptr, nullptr, nullptr, nullptr};
   // CU mask of the context's own streams (empty: every CU)
   std::vector<uint32_t> cu_mask;
   // checkpointing during retraining: publish into ckpt every ckpt_every epochs
@@ -141,7 +147,7 @@ struct Ctx {
 // Read the events of finished timed launches into `stats`.
 hipError_t ctx_collect_timing(Ctx& c);
 
-hipError_t ctx_init(Ctx& c, int device, int n_classes, size_t workspace_bytes);
+hipError_t ctx_init(Ctx& c, int device, int n_classes, int hidden, size_t workspace_bytes);
 // Wait for the context's queued work and release its own streams (they are
 // created again, with the current cu_mask, when next needed).
 hipError_t ctx_reset_streams(Ctx& c);
@@ -166,6 +172,10 @@ ekya_status run_profile(Ctx& c, const float* weights, const ekya_profile_cfg* cf
                         ekya_profile_result* out);
 ekya_status run_infer(Ctx& c, const float* weights, const void* frames, int n, int H, int W,
                       int resolution, int precision, int32_t* labels_out, hipStream_t stream);
+size_t infer_models_workspace_bytes(const Net& net, int resolution, int n_models);
+ekya_status run_infer_models(Ctx& c, Model* const* models, int n_models, const void* frames,
+                             const int* counts, int H, int W, int resolution, int32_t* labels_out,
+                             uint64_t* versions, hipStream_t stream);
 ekya_status run_infer_model(Ctx& c, Model& m, const void* frames, int n, int H, int W,
                             int resolution, int32_t* labels_out, hipStream_t stream,
                             uint64_t* version);

@@ -174,7 +174,7 @@ class _Block(tnn.Module):
 
 
 class _TorchResNet18(tnn.Module):
-    def __init__(self, n_classes, widths=(64, 128, 256, 512)):
+    def __init__(self, n_classes, widths=(64, 128, 256, 512), hidden=0):
         super().__init__()
         self.conv1 = tnn.Conv2d(3, widths[0], 7, 2, 3, bias=False)
         self.bn1 = tnn.BatchNorm2d(widths[0])
@@ -183,7 +183,11 @@ class _TorchResNet18(tnn.Module):
             s = 1 if i == 0 else 2
             setattr(self, f"layer{i + 1}", tnn.Sequential(_Block(cin, w, s), _Block(w, w, 1)))
             cin = w
-        self.fc = tnn.Linear(widths[-1], n_classes)
+        if hidden:
+            self.fc = tnn.Sequential(tnn.Linear(widths[-1], hidden), tnn.ReLU(),
+                                     tnn.Linear(hidden, n_classes))
+        else:
+            self.fc = tnn.Linear(widths[-1], n_classes)
 
     def forward(self, x):
         x = F.max_pool2d(F.relu(self.bn1(self.conv1(x))), 3, 2, 1)
@@ -192,8 +196,8 @@ class _TorchResNet18(tnn.Module):
         return self.fc(x.mean(dim=(2, 3)))
 
 
-def _torch_model(flat, n_classes=6):
-    m = _TorchResNet18(n_classes).double()
+def _torch_model(flat, n_classes=6, hidden=0):
+    m = _TorchResNet18(n_classes, hidden=hidden).double()
     sd = m.state_dict()
     names = [n for n in sd if not n.endswith("num_batches_tracked")]
     off = 0

@@ -13,8 +13,8 @@ several in-batch summation orders.
 `bf16=True` stores every module output (activations, and through a custom
 autograd function their gradients) and the conv weights used in a step in
 bfloat16 (round to nearest even), with fp32 arithmetic in between, as the
-library's bf16 path does; logits, pooled features, BatchNorm statistics and
-master weights stay fp32."""
+library's bf16 path does; the classifier (with its hidden layer, if any),
+logits, pooled features, BatchNorm statistics and master weights stay fp32."""
 import numpy as np
 
 from oracle import rng
@@ -37,7 +37,7 @@ def _round_fn():
 
 
 def torch_retrain(w0, k, win, frac, lr, mu, batch, seed, perm_seed=None, bf16=False, epochs=1,
-                  shuffle_seed=None):
+                  shuffle_seed=None, hidden=0):
     """(weights, step losses): the weights (canonical flat, float64) after
     `epochs` epochs of the same retraining job, and the loss of every step;
     perm_seed permutes the samples inside every batch (the same mathematics
@@ -47,10 +47,10 @@ def torch_retrain(w0, k, win, frac, lr, mu, batch, seed, perm_seed=None, bf16=Fa
     import torch.nn.functional as F
 
     from tests.test_oracle_resnet import _torch_model
-    m, names = _torch_model(np.asarray(w0, dtype=np.float64))
+    m, names = _torch_model(np.asarray(w0, dtype=np.float64), hidden=hidden)
     m = m.float()
     m.train()
-    net = ResNet18(6)
+    net = ResNet18(6, hidden=hidden)
     lo = len(STAGES) - k
     trainable = net.trainable_names(k)
     params = dict(m.named_parameters())
@@ -63,6 +63,8 @@ def torch_retrain(w0, k, win, frac, lr, mu, batch, seed, perm_seed=None, bf16=Fa
     if bf16:
         rnd = _round_fn()
         for name, mod in m.named_modules():
+            if name.startswith("fc"):  # the classifier computes in fp32
+                continue
             if isinstance(mod, (torch.nn.Conv2d, torch.nn.BatchNorm2d, torch.nn.ReLU,
                                 torch.nn.MaxPool2d)):
                 mod.register_forward_hook(lambda mod, inp, out: rnd(out))
