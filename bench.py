@@ -73,10 +73,10 @@ def measured_traffic(kernel):
     return int(t["fetch_bytes_per_launch"] + t["write_bytes_per_launch"])
 
 
-def cpu_baseline(n=8, n_heldout=4):
+def cpu_baseline(n=64, n_heldout=8):
     """The oracle, as it stands, on a bounded sample of the headline workload:
-    one SGD step of full-depth retraining on 8 frames of the 224 px drifting
-    window (4 held-out frames evaluated after it), fp64 numpy."""
+    one SGD step of full-depth retraining on 64 frames of the 224 px drifting
+    window (8 held-out frames evaluated after it), fp64 numpy."""
     from threadpoolctl import threadpool_info
 
     from oracle import ekya as oracle
@@ -281,6 +281,31 @@ def run_extras(binding, torch, d, w0):
                              "ms_per_step": round(ms2, 3), "prefix_ms": round(o2["prefix_seconds"] * 1e3, 3),
                              "workload": "layer4+fc, 2000-frame window at 30%, 5 epochs, batch 64"}
     log(f"layer4+fc: {out['layer4_retrain']}")
+
+    # the same job with a hidden classifier layer of 1024 neurons
+    from synth import kaiming_resnet18_weights
+    hctx = binding.ekya_create(0, 6, hidden=1024)
+    wh0 = torch.tensor(kaiming_resnet18_weights(seed=0, hidden=1024), device=w0.device)
+    wh = wh0.clone()
+
+    def step_h():
+        wh.copy_(wh0)
+        return binding.ekya_retrain(hctx, wh, c["k"], d2["fr"], d2["lab"], d2["hf"], d2["hl"],
+                                    c["frac"], c["epochs"], c["lr"], c["momentum"], c["batch"],
+                                    c["seed"])
+    step_h()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(3):
+        oh = step_h()
+    torch.cuda.synchronize()
+    msh = (time.perf_counter() - t0) * 1e3 / 3
+    out["layer4_retrain_hidden1024"] = {
+        "samples_per_s": round(oh["n_train"] * c["epochs"] / (msh * 1e-3), 1),
+        "ms_per_step": round(msh, 3),
+        "workload": "as layer4_retrain, with a 1024-neuron hidden layer before the classifier"}
+    log(f"layer4+fc, hidden 1024: {out['layer4_retrain_hidden1024']}")
+    binding.ekya_destroy(hctx)
     del d2
 
     # inference img/s on 2000 frames of the window
@@ -418,6 +443,26 @@ def run_extras(binding, torch, d, w0):
                                      "bf16 ResNet18 weights"}
     log(f"hot reload: {out['hot_reload']}")
     binding.ekya_model_destroy(model)
+
+    # ten streams, each with its own model, 360 frames each at 224 px in one
+    # call, against the same 3600 frames through one model
+    models = [binding.ekya_model_create(0, 6, binding.EKYA_BF16) for _ in range(10)]
+    for m in models:
+        binding.ekya_model_load(m, w0)
+    counts = [360] * 10
+    lab10, _ = binding.ekya_infer_models(ictx, models, inf, counts, 224)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(3):
+        binding.ekya_infer_models(ictx, models, inf, counts, 224, labels_out=lab10)
+    torch.cuda.synchronize()
+    rate10 = 3 * inf.shape[0] / (time.perf_counter() - t0)
+    out["infer_per_stream_models"] = {"img_per_s": round(rate10, 1),
+                                      "single_model_img_per_s": out["joint_window"]["infer_224_alone_img_per_s"],
+                                      "workload": "10 streams x 360 frames at 224 px, one model per stream"}
+    log(f"per-stream models: {out['infer_per_stream_models']}")
+    for m in models:
+        binding.ekya_model_destroy(m)
     binding.ekya_destroy(ictx)
     binding.ekya_destroy(ctx)
     return out
