@@ -599,7 +599,7 @@ template <int N> __device__ __forceinline__ void wait_vmcnt() {
 // Workgroups are dispatched round-robin over the 8 XCDs (each with its own
 // L2); give every XCD a contiguous range of tiles, rows of the output fastest,
 // so the blocks sharing a column panel of the B operand share an L2.
-__device__ __forceinline__ int xcd_tile(int L, int total) {
+__host__ __device__ __forceinline__ int xcd_tile(int L, int total) {
   const int x = L & 7, k = L >> 3;
   return x * (total >> 3) + min(x, total & 7) + k;
 }
@@ -1330,6 +1330,178 @@ __global__ __launch_bounds__(NT) void wgrad_dma_kernel(WgDmaArgs a) {
       *reinterpret_cast<float4*>(dst) =
           make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
     }
+}
+
+// ----------------------------------- weight gradient of a 3x3 / stride 1 conv
+// All nine taps at once: a block owns 64 input channels x 64 output channels
+// x 9 taps (576 x 64 outputs) and reduces over 8 x 8 patches of output
+// pixels.  A stage is one patch: its 10 x 10 input pixels (the patch grown by
+// the filter's reach, zero outside the image) and its 64 output-gradient
+// pixels (zero outside the image) go to LDS once, and each tap reads the
+// input at its own offset -- one load of the input serves nine taps, where a
+// tap-at-a-time tiling loads it nine times.  Pixel rows of 64 channels
+// (128 bytes) hold four 32-byte segments, segment s of pixel p stored at
+// s ^ (p mod 4); an 8-byte transpose read (ds_read_b64_tr_b16) takes 4
+// pixels x 16 channels per 16-lane group, member m supplying pixel m / 4,
+// channels 4 (m % 4) .. +3, and hands lane i channel i's 4 pixels; two reads
+// make a lane's MFMA operand of 8 pixels (one patch row).  Wave w owns row
+// tiles 9 w .. 9 w + 8 of the 36 (tap t / 4, channels 16 (t % 4) ..) and all 4
+// column tiles; the output-gradient fragments are read once per k-step and
+// used by the nine row tiles.  Every wave issues the same six copies per
+// stage: 16 instructions of input pixels (100 used, 28 zero rows) and 8 of
+// output-gradient pixels.
+struct TapGeom {
+  int tiles_c, tiles_k, splits, pps;  // pps: patches per split
+  int py_n, px_n;                     // patches down / across an image
+  __host__ __device__ int n_patches(int N) const { return N * py_n * px_n; }
+};
+
+constexpr int TAP_IN_PIX = 128;                       // staged input pixel rows (100 used)
+constexpr int TAP_STAGE = (TAP_IN_PIX + 64) * 128;    // bytes per stage
+constexpr int TAP_INS = (TAP_IN_PIX + 64) / 8;        // 1024-byte copies per stage
+constexpr int TAP_LPS = TAP_INS / 4;                  // copies per wave and stage
+
+// Copy slot j (instruction wave + 4 j) of `lane`: slots 0-3 stage input
+// pixel rows, 4-5 output-gradient rows.  sy, sx: the pixel's offset from the
+// patch origin (input rows start one pixel up and left; unused rows get an
+// offset that no patch brings inside the image); off: its element offset in
+// the operand relative to the patch origin's pixel, channel block included.
+// Shared by the kernel and the host-side bounds check.
+struct TapSlot {
+  int sy, sx, off;
+};
+__host__ __device__ inline TapSlot tap_slot(int W, int C, int Q, int K, int c0, int k0, int wave,
+                                            int lane, int j) {
+  const int ins = wave + 4 * j, sl = lane & 7;
+  TapSlot t;
+  if (j < 4) {
+    const int pix = 8 * ins + (lane >> 3);  // < TAP_IN_PIX
+    const int u = 2 * ((sl >> 1) ^ (pix & 3)) + (sl & 1);
+    const int ty = pix / 10, tx = pix - 10 * (pix / 10);
+    t.sy = pix < 100 ? ty - 1 : -(1 << 24);
+    t.sx = tx - 1;
+    t.off = pix < 100 ? (t.sy * W + t.sx) * C + c0 + u * 8 : 0;
+  } else {
+    const int pix = 8 * (ins - TAP_IN_PIX / 8) + (lane >> 3);
+    const int u = 2 * ((sl >> 1) ^ (pix & 3)) + (sl & 1);
+    t.sy = pix >> 3;
+    t.sx = pix & 7;
+    t.off = (t.sy * Q + t.sx) * K + k0 + u * 8;
+  }
+  return t;
+}
+// Whether slot j's pixel of the patch at (py0, px0) lies inside its operand.
+__host__ __device__ inline bool tap_slot_in(const TapSlot& t, int j, int py0, int px0, int H,
+                                            int W, int P, int Q) {
+  if (j < 4)
+    return (unsigned)(py0 + t.sy) < (unsigned)H && (unsigned)(px0 + t.sx) < (unsigned)W;
+  return py0 + t.sy < P && px0 + t.sx < Q;
+}
+
+struct WgTapArgs {
+  ConvGeom g;
+  TapGeom t;
+  const bf16* x;
+  const bf16* dy;
+  float* out;  // [split][K][9 C]
+};
+
+template <int NST>
+__global__ __launch_bounds__(NT, 2) void wgrad_tap_kernel(WgTapArgs a) {
+  __shared__ __align__(16) char smem[NST * TAP_STAGE];
+  const int H = a.g.H, W = a.g.W, C = a.g.C, K = a.g.K, P = a.g.P, Q = a.g.Q, N = a.g.N;
+  const int tiles_c = a.t.tiles_c, px_n = a.t.px_n, per_img = a.t.py_n * a.t.px_n;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int tiles = tiles_c * a.t.tiles_k;
+  const int item = xcd_tile(blockIdx.x, tiles * a.t.splits);
+  const int split = item / tiles, tile = item - split * tiles;
+  const int c0 = (tile % tiles_c) * 64, k0 = (tile / tiles_c) * 64;
+  const int q0 = split * a.t.pps;
+  const int ns = max(0, min(N * per_img, q0 + a.t.pps) - q0);
+  const bf16* const xg = a.x;
+  const bf16* const dyg = a.dy;
+  const void* const zero = g_zero_unit;
+  TapSlot sl[TAP_LPS];
+#pragma unroll
+  for (int j = 0; j < TAP_LPS; ++j) sl[j] = tap_slot(W, C, Q, K, c0, k0, wave, lane, j);
+
+  auto issue = [&](int st, char* slot) {
+    const int q = q0 + st;
+    const int n = q / per_img, rem = q - n * per_img;
+    const int pyi = rem / px_n;
+    const int py0 = 8 * pyi, px0 = 8 * (rem - pyi * px_n);
+    const bf16* xb = xg + ((long long)n * H * W + (long long)py0 * W + px0) * C;
+    const bf16* db = dyg + ((long long)n * P * Q + (long long)py0 * Q + px0) * K;
+#pragma unroll
+    for (int j = 0; j < TAP_LPS; ++j) {
+      const bool in = tap_slot_in(sl[j], j, py0, px0, H, W, P, Q);
+      const void* src = in ? (const void*)((j < 4 ? xb : db) + sl[j].off) : zero;
+      dma16(src, reinterpret_cast<uint4*>(slot + (wave + 4 * j) * 1024));
+    }
+  };
+
+  f32x4 acc[9][4];
+#pragma unroll
+  for (int i = 0; i < 9; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+#pragma unroll
+  for (int st = 0; st < NST - 1; ++st)
+    if (st < ns) issue(st, smem + st * TAP_STAGE);
+  const int gq = lane >> 4, jr = (lane & 15) >> 2, qd = lane & 3;
+  for (int st = 0; st < ns; ++st) {
+    // stage st's copies are the oldest; later stages' may stay in flight
+    if (st + NST - 2 < ns) wait_vmcnt<(NST - 2) * TAP_LPS>(); else wait_vmcnt<0>();
+    stage_barrier();
+    if (st + NST - 1 < ns) issue(st + NST - 1, smem + ((st + NST - 1) % NST) * TAP_STAGE);
+    const char* As = smem + (st % NST) * TAP_STAGE;
+    const char* Bs = As + TAP_IN_PIX * 128;
+#pragma unroll
+    for (int kf = 0; kf < 2; ++kf) {
+      const int py = kf * 4 + gq;  // this lane's patch row
+      uint4 fb[4];
+#pragma unroll
+      for (int half = 0; half < 2; ++half) {
+        const int p = py * 8 + half * 4 + jr;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const uint2 v = lds_read_tr16(Bs + p * 128 + ((j ^ (p & 3)) * 32) + qd * 8);
+          if (half == 0) { fb[j].x = v.x; fb[j].y = v.y; } else { fb[j].z = v.x; fb[j].w = v.y; }
+        }
+      }
+#pragma unroll
+      for (int t = 0; t < 9; ++t) {
+        const int T = 9 * wave + t, tap = T >> 2, cg = T & 3;
+        const int r = tap / 3, s = tap - 3 * (tap / 3);
+        uint4 fa;
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {
+          const int ip = (py + r) * 10 + half * 4 + jr + s;
+          const uint2 v = lds_read_tr16(As + ip * 128 + ((cg ^ (ip & 3)) * 32) + qd * 8);
+          if (half == 0) { fa.x = v.x; fa.y = v.y; } else { fa.z = v.x; fa.w = v.y; }
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) mma_unit(acc[t][j], fa, fb[j], (bf16*)nullptr);
+      }
+    }
+  }
+
+  const long long RSC = 9LL * C;
+  const int lr = lane & 15, lg = lane >> 4;
+#pragma unroll
+  for (int t = 0; t < 9; ++t) {
+    const int T = 9 * wave + t, tap = T >> 2, cg = T & 3;
+    const long long row = (long long)tap * C + c0 + 16 * cg + 4 * lg;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int col = k0 + 16 * j + lr;
+      float* dst = a.out + ((long long)split * K + col) * RSC + row;
+      *reinterpret_cast<float4*>(dst) =
+          make_float4(acc[t][j][0], acc[t][j][1], acc[t][j][2], acc[t][j][3]);
+    }
+  }
 }
 
 // Warp-specialised weight gradient for BM = 256 rows (channels of one filter
@@ -2177,9 +2349,34 @@ namespace {
 // >= 2 stages of 64 pixels per split.
 struct WgDmaPlan {
   int bm, bn, splits, mps;
+  TapGeom tap;  // tap.splits > 0: the all-taps kernel (3x3, stride 1)
 };
 bool wgrad_dma_ok(int dt, const ConvGeom& g) { return dt == DT_BF16 && g.C % 64 == 0 && g.K % 64 == 0; }
+// Blocks the all-taps weight gradient aims for (one per CU).
+constexpr int TAP_TARGET_BLOCKS = 256;
+bool wgrad_tap_ok(const ConvGeom& g) {
+  return g.R == 3 && g.S == 3 && g.stride == 1 && g.pad == 1 && g.P == g.H && g.Q == g.W &&
+         g.C % 64 == 0 && g.K % 64 == 0 && (long long)g.N * g.H * g.W * g.C < (1LL << 40) &&
+         (long long)g.N * g.P * g.Q * g.K < (1LL << 40);
+}
+TapGeom plan_wgrad_tap(const ConvGeom& g) {
+  TapGeom t;
+  t.tiles_c = g.C / 64;
+  t.tiles_k = g.K / 64;
+  t.py_n = (g.P + 7) / 8;
+  t.px_n = (g.Q + 7) / 8;
+  const long long np = (long long)g.N * t.py_n * t.px_n;
+  const long long tiles = (long long)t.tiles_c * t.tiles_k;
+  long long s = std::max(1LL, std::min(np, cdivl(TAP_TARGET_BLOCKS, tiles)));
+  t.pps = (int)cdivl(np, s);
+  t.splits = (int)cdivl(np, t.pps);
+  return t;
+}
 WgDmaPlan plan_wgrad_dma(const ConvGeom& g) {
+  if (wgrad_tap_ok(g)) {
+    const TapGeom t = plan_wgrad_tap(g);
+    return {576, 64, t.splits, 0, t};
+  }
   const long long M = (long long)g.N * g.P * g.Q;
   const long long stages = std::max(1LL, cdivl(M, 64));
   const long long ws_tiles = (long long)(g.R * g.S * g.C / 256) * (g.K / 128);
@@ -2192,14 +2389,14 @@ WgDmaPlan plan_wgrad_dma(const ConvGeom& g) {
     long long s = std::min(std::max(1LL, 256 / ws_tiles), std::max(1LL, stages / 4));
     s = std::min(s, 64LL);
     const long long mps = cdivl(cdivl(M, s), 64) * 64;
-    return {256, 128, (int)cdivl(M, mps), (int)mps};
+    return {256, 128, (int)cdivl(M, mps), (int)mps, TapGeom{}};
   }
   const int bn = g.K % 128 == 0 ? 128 : 64;
   const long long tiles = (long long)(g.R * g.S * g.C / 64) * (g.K / bn);
   long long s = std::min(cdivl(576, tiles), std::max(1LL, stages / 2));
   s = std::max(1LL, std::min(s, 64LL));
   const long long mps = cdivl(cdivl(M, s), 64) * 64;
-  return {64, bn, (int)cdivl(M, mps), (int)mps};
+  return {64, bn, (int)cdivl(M, mps), (int)mps, TapGeom{}};
 }
 struct WPlan {
   int bm, bn, splits;
@@ -2209,8 +2406,8 @@ struct WPlan {
 hipError_t conv_wgrad_dma(const ConvGeom& g, const void* x, const void* dy, float* partials,
                           float* dw, hipStream_t stream) {
   const WgDmaPlan p = plan_wgrad_dma(g);
-  WgDmaArgs a{g, (const bf16*)x, (const bf16*)dy, (p.splits > 1 || !dw) ? partials : dw, p.mps,
-              0, 0, p.splits};
+  float* out = (p.splits > 1 || !dw) ? partials : dw;
+  WgDmaArgs a{g, (const bf16*)x, (const bf16*)dy, out, p.mps, 0, 0, p.splits};
   a.tiles_m = g.R * g.S * g.C / p.bm;
   a.tiles_n = g.K / p.bn;
   const Cost cost = conv_cost(g, g.C, sizeof(bf16), true);
@@ -2222,7 +2419,11 @@ hipError_t conv_wgrad_dma(const ConvGeom& g, const void* x, const void* dy, floa
     EKYA_HIP(hipEventRecord(e0, stream));
   }
   const dim3 grid(a.tiles_m * a.tiles_n, p.splits);
-  if (p.bm == 256)
+  if (p.tap.splits > 0) {
+    const WgTapArgs ta{g, p.tap, (const bf16*)x, (const bf16*)dy, out};
+    hipLaunchKernelGGL((wgrad_tap_kernel<2>),
+                       dim3(p.tap.tiles_c * p.tap.tiles_k * p.tap.splits), dim3(NT), 0, stream, ta);
+  } else if (p.bm == 256)
     hipLaunchKernelGGL((wgrad_ws_kernel<256, 128, 3>), dim3(a.tiles_m * a.tiles_n * p.splits),
                        dim3(8 * 64 + WS_LOADERS * 64), 0, stream, a);
   else if (p.bn == 128)
@@ -2232,8 +2433,10 @@ hipError_t conv_wgrad_dma(const ConvGeom& g, const void* x, const void* dy, floa
   hipError_t e = hipGetLastError();
   if (t && e == hipSuccess) {
     EKYA_HIP(hipEventRecord(e1, stream));
-    t->recs.push_back({std::string("conv_wgrad<bf16,") + std::to_string(p.bm) + "," +
-                           std::to_string(p.bn) + (p.bm == 256 ? ",ws>" : ",dma>"),
+    t->recs.push_back({p.tap.splits > 0 ? std::string("conv_wgrad<bf16,taps9,64>")
+                                         : std::string("conv_wgrad<bf16,") + std::to_string(p.bm) +
+                                               "," + std::to_string(p.bn) +
+                                               (p.bm == 256 ? ",ws>" : ",dma>"),
                        cost.flops, cost.bytes, e0, e1});
   }
   if (e != hipSuccess || p.splits == 1 || !dw) return e;
@@ -2266,7 +2469,8 @@ bool conv_wgrad_partials_ok(int dt, const ConvGeom& g) {
 
 size_t conv_wgrad_partials_floats(int dt, const ConvGeom& g) {
   if (!conv_wgrad_partials_ok(dt, g)) return 0;
-  return (size_t)plan_wgrad_dma(g).splits * g.K * g.R * g.S * g.C;
+  const int s = plan_wgrad_dma(g).splits;
+  return (size_t)(s + conv_update_groups(s)) * g.K * g.R * g.S * g.C;
 }
 
 hipError_t conv_wgrad_partials(int dt, const ConvGeom& g, const void* x, const void* dy,

@@ -1521,6 +1521,8 @@ __global__ __launch_bounds__(256) void pack_conv_kernel(const float* master, con
 // v = mu v + g, w = w - lr v on the fp32 [K][RS][C] master, then the
 // [K][RS][C] copy directly and the [C][RS][K] copy through an LDS transpose.
 constexpr int UPD_K = 16;
+// Splits a split-group pass adds up before the momentum step (above it).
+constexpr int UPD_GROUP = 16;
 template <typename T>
 __global__ __launch_bounds__(256) void conv_update_kernel(const float* part, int splits, int K,
                                                           int RS, int C, float* w, float* v,
@@ -1987,11 +1989,48 @@ hipError_t pack_conv_weights(int dt, const float* master, const long long* tab, 
   });
 }
 
+// out[g][i] = sum of part[s][i] over the splits s of group g (UPD_GROUP
+// consecutive splits, added in split order), four floats per thread.
+__global__ __launch_bounds__(256) void split_group_kernel(const float* part, int splits,
+                                                          long long n, float* out) {
+  const long long n4 = n / 4;
+  const int g = blockIdx.y, s0 = g * UPD_GROUP, s1 = min(splits, s0 + UPD_GROUP);
+  for (long long i = blockIdx.x * 256LL + threadIdx.x; i < n4; i += (long long)gridDim.x * 256) {
+    float4 acc = reinterpret_cast<const float4*>(part + (long long)s0 * n)[i];
+    for (int s = s0 + 1; s < s1; ++s) {
+      const float4 t = reinterpret_cast<const float4*>(part + (long long)s * n)[i];
+      acc.x += t.x;
+      acc.y += t.y;
+      acc.z += t.z;
+      acc.w += t.w;
+    }
+    reinterpret_cast<float4*>(out + (long long)g * n)[i] = acc;
+  }
+}
+
+int conv_update_groups(int splits) { return splits > UPD_GROUP ? cdiv(splits, UPD_GROUP) : 0; }
+
 hipError_t conv_weight_update(int dt, const float* part, int splits, int K, int RS, int C,
                               float* w, float* v, float lr, float mu, void* krsc, void* crsk,
                               hipStream_t stream) {
   if (K % 64 != 0 || C % 64 != 0 || splits < 1 || (long long)K * RS * C >= (1LL << 31))
     return hipErrorInvalidValue;
+  const int groups = conv_update_groups(splits);
+  if (groups > 0) {
+    // many splits (the all-taps weight gradient of small convolutions): add
+    // them in groups first, spread over the whole GPU, into the scratch
+    // after the partials; the momentum step then reads the group sums
+    const long long nw = (long long)K * RS * C;
+    float* sums = const_cast<float*>(part) + (long long)splits * nw;
+    TimedLaunch tg(stream);
+    hipLaunchKernelGGL(split_group_kernel,
+                       dim3((unsigned)std::min<long long>(cdivl(nw / 4, 256), 1024), groups),
+                       dim3(256), 0, stream, part, splits, nw, sums);
+    EKYA_HIP(tg.done(hipGetLastError(), "conv_update_group",
+                     (double)nw * 4.0 * (splits + groups)));
+    part = sums;
+    splits = groups;
+  }
   const int ntiles = RS * (K / UPD_K) * (C / 64);
   // per weight: the split partials, master and momentum read; master and
   // momentum written, and the two low-precision copies

@@ -127,6 +127,8 @@ hipError_t conv_wgrad(int dt, const ConvGeom& g, const void* x, const void* dy, 
                       float* dw, int C0, hipStream_t stream);
 // The weight gradient left as fp32 split partials [splits][K][R][S][C] (one
 // split included) for conv_weight_update: bf16 with C and K multiples of 64.
+// conv_wgrad_partials_floats includes the scratch conv_weight_update needs
+// after the partials.
 bool conv_wgrad_partials_ok(int dt, const ConvGeom& g);
 size_t conv_wgrad_partials_floats(int dt, const ConvGeom& g);
 hipError_t conv_wgrad_partials(int dt, const ConvGeom& g, const void* x, const void* dy,
@@ -239,8 +241,12 @@ hipError_t sgd_momentum(float* w, float* v, const float* g, long long n, float l
 hipError_t sgd_momentum_ranges(float* w, float* v, const float* g, const long long* tab, int n,
                                long long max_len, float lr, float mu, hipStream_t stream);
 // One convolution's momentum step from its weight-gradient split partials
-// (summed in split order): v = mu v + g, w = w - lr v on the fp32 [K][RS][C]
-// master, then its [K][RS][C] and [C][RS][K] low-precision copies.
+// (summed in split order; more than 16 splits are first added in groups of
+// 16, in order, into conv_update_groups(splits) scratch slices right after
+// the partials, which the buffer must hold): v = mu v + g, w = w - lr v on
+// the fp32 [K][RS][C] master, then its [K][RS][C] and [C][RS][K]
+// low-precision copies.
+int conv_update_groups(int splits);
 hipError_t conv_weight_update(int dt, const float* part, int splits, int K, int RS, int C,
                               float* w, float* v, float lr, float mu, void* krsc, void* crsk,
                               hipStream_t stream);
