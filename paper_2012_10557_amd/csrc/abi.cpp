@@ -429,6 +429,7 @@ ekya_status ekya_op_conv2d_wgrad(int precision, const void* x, const void* dy, i
   const void* xp;
   hipError_t e = pad_input(precision, x, N, H, W, C, Cp, tmp, &xp, st);
   ekya::ConvGeom g = make_geom(N, H, W, Cp, K, R, S, stride, pad);
+  g.C0 = C;  // the plan (and so its scratch) depends on the real channel count
   float* part = tmp.get<float>(ekya::conv_wgrad_workspace_floats(precision, g));
   float* krsc = tmp.get<float>((size_t)K * R * S * C);
   long long* tab = tmp.get<long long>(8);

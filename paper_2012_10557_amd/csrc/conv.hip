@@ -1504,6 +1504,175 @@ __global__ __launch_bounds__(NT, 2) void wgrad_tap_kernel(WgTapArgs a) {
   }
 }
 
+// ---------------------------------------------- weight gradient of the stem
+// dw[k][r][s][c] = sum over output pixels of dy[pix][k] * x(2p + r - 3,
+// 2q + s - 3)[c] for the 7x7 / stride 2 / pad 3 stem on frames stored with
+// channels padded to 8 (3 real).  A block owns every output (64 k x 49 taps x
+// channels 0-3, the fourth a zero pad) and reduces over 8 x 8 patches of output
+// pixels.  A stage stages the patch's 22 x 22 input pixels (channels 0-3,
+// 8 bytes, through registers; rows of 24 pixels) and its 64 output-gradient
+// pixels (128-byte rows, direct copies, segments swizzled as in the all-taps
+// kernel).  Taps are taken in 2 x 2 blocks (r and s from 0 to 7; taps 7
+// compute into discarded rows): a 16-row MFMA tile is 4 taps x 4 channels,
+// its transpose read has member m supply pixel m / 4 of tap m % 4, and with
+// rows of 24 pixels the 16 members' 8-byte slots differ modulo 128 bytes
+// (tap offsets 0, 1, 24, 25 plus twice the pixel index), so the read meets no
+// bank conflict.  Wave w owns the 4 tap blocks of filter rows 2w, 2w + 1.
+constexpr int STEM_WG_ROWS = 22, STEM_WG_PITCH = 24;
+constexpr int STEM_WG_X = STEM_WG_ROWS * STEM_WG_PITCH * 8;  // input bytes per stage
+constexpr int STEM_WG_STAGE = STEM_WG_X + 64 * 128;
+
+struct StemWgArgs {
+  ConvGeom g;
+  const bf16* x;   // [N][H][W][8]
+  const bf16* dy;  // [N][P][Q][64]
+  float* out;      // [split][64][49][4]
+  int splits, pps, py_n, px_n;
+};
+
+__global__ __launch_bounds__(NT, 2) void wgrad_stem_kernel(StemWgArgs a) {
+  constexpr int NST = 2;
+  __shared__ __align__(16) char smem[NST * STEM_WG_STAGE];
+  const int H = a.g.H, W = a.g.W, P = a.g.P, Q = a.g.Q, N = a.g.N;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int split = xcd_tile(blockIdx.x, a.splits);
+  const int per_img = a.py_n * a.px_n;
+  const int q0 = split * a.pps;
+  const int ns = max(0, min(N * per_img, q0 + a.pps) - q0);
+  const void* const zero = g_zero_unit;
+  // output-gradient copy slots: instructions wave and wave + 4 of the 8
+  int dsy[2], dsx[2], doff[2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int pix = 8 * (wave + 4 * j) + (lane >> 3), sl = lane & 7;
+    const int u = 2 * ((sl >> 1) ^ (pix & 3)) + (sl & 1);
+    dsy[j] = pix >> 3;
+    dsx[j] = pix & 7;
+    doff[j] = (dsy[j] * Q + dsx[j]) * 64 + u * 8;
+  }
+  auto origin = [&](int st, int& n, int& py0, int& px0) {
+    const int q = q0 + st;
+    n = q / per_img;
+    const int rem = q - n * per_img, pyi = rem / a.px_n;
+    py0 = 8 * pyi;
+    px0 = 8 * (rem - pyi * a.px_n);
+  };
+  // input pixels t and t + 256 of the 22 x 22 region, as registers
+  uint4 xv[2];
+  auto load_x = [&](int st) {
+    int n, py0, px0;
+    origin(st, n, py0, px0);
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int t = threadIdx.x + 256 * h;
+      const int ry = t / STEM_WG_ROWS, rx = t - STEM_WG_ROWS * (t / STEM_WG_ROWS);
+      const int iy = 2 * py0 - 3 + ry, ix = 2 * px0 - 3 + rx;
+      const bool in = t < STEM_WG_ROWS * STEM_WG_ROWS && (unsigned)iy < (unsigned)H &&
+                      (unsigned)ix < (unsigned)W;
+      xv[h] = in ? *reinterpret_cast<const uint4*>(a.x + (((long long)n * H + iy) * W + ix) * 8)
+                 : make_uint4(0u, 0u, 0u, 0u);
+    }
+  };
+  auto store_x = [&](char* slot) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int t = threadIdx.x + 256 * h;
+      if (t < STEM_WG_ROWS * STEM_WG_ROWS) {
+        const int ry = t / STEM_WG_ROWS, rx = t - STEM_WG_ROWS * (t / STEM_WG_ROWS);
+        *reinterpret_cast<uint2*>(slot + (ry * STEM_WG_PITCH + rx) * 8) = make_uint2(xv[h].x, xv[h].y);
+      }
+    }
+  };
+  auto issue_dy = [&](int st, char* slot) {
+    int n, py0, px0;
+    origin(st, n, py0, px0);
+    const bf16* db = a.dy + ((long long)n * P * Q + (long long)py0 * Q + px0) * 64;
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const bool in = py0 + dsy[j] < P && px0 + dsx[j] < Q;
+      dma16(in ? (const void*)(db + doff[j]) : zero,
+            reinterpret_cast<uint4*>(slot + STEM_WG_X + (wave + 4 * j) * 1024));
+    }
+  };
+
+  f32x4 acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  if (ns > 0) {
+    load_x(0);
+    issue_dy(0, smem);
+    wait_vmcnt<0>();
+    store_x(smem);
+  }
+  const int gq = lane >> 4, jr = (lane & 15) >> 2, qd = lane & 3;
+  for (int st = 0; st < ns; ++st) {
+    stage_barrier();  // stage st's input rows (stores) and copies are in LDS
+    const bool next = st + 1 < ns;
+    char* nslot = smem + ((st + 1) % NST) * STEM_WG_STAGE;
+    if (next) {
+      load_x(st + 1);
+      issue_dy(st + 1, nslot);
+    }
+    const char* Xs = smem + (st % NST) * STEM_WG_STAGE;
+    const char* Bs = Xs + STEM_WG_X;
+#pragma unroll
+    for (int kf = 0; kf < 2; ++kf) {
+      const int py = kf * 4 + gq;
+      uint4 fb[4];
+#pragma unroll
+      for (int half = 0; half < 2; ++half) {
+        const int p = py * 8 + half * 4 + jr;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const uint2 v = lds_read_tr16(Bs + p * 128 + ((j ^ (p & 3)) * 32) + qd * 8);
+          if (half == 0) { fb[j].x = v.x; fb[j].y = v.y; } else { fb[j].z = v.x; fb[j].w = v.y; }
+        }
+      }
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        // tap block (filter rows 2 wave, 2 wave + 1; columns 2t, 2t + 1); this
+        // member's tap within it is qd
+        const int r = 2 * wave + (qd >> 1), sc = 2 * t + (qd & 1);
+        uint4 fa;
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {
+          const int px = half * 4 + jr;
+          const uint2 v =
+              lds_read_tr16(Xs + ((2 * py + r) * STEM_WG_PITCH + 2 * px + sc) * 8);
+          if (half == 0) { fa.x = v.x; fa.y = v.y; } else { fa.z = v.x; fa.w = v.y; }
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) mma_unit(acc[t][j], fa, fb[j], (bf16*)nullptr);
+      }
+    }
+    if (next) {
+      wait_vmcnt<0>();
+      store_x(nslot);  // that slot was last read before this stage's barrier
+    }
+  }
+
+  // lane rows 4 lg .. 4 lg + 3 of a tile are tap lg of the block, channels 0-3
+  const int lr = lane & 15, lg = lane >> 4;
+  const int r = 2 * wave + (lg >> 1);
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    const int sc = 2 * t + (lg & 1);
+    if (r < 7 && sc < 7) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int k = 16 * j + lr;
+        float* dst = a.out + (((long long)split * 64 + k) * 49 + r * 7 + sc) * 4;
+        *reinterpret_cast<float4*>(dst) =
+            make_float4(acc[t][j][0], acc[t][j][1], acc[t][j][2], acc[t][j][3]);
+      }
+    }
+  }
+}
+
 // Warp-specialised weight gradient for BM = 256 rows (channels of one filter
 // tap, so C % 256 == 0) x BN output channels: four loader waves gather the
 // stage's 64 input-pixel rows and 64 output-gradient rows (same LDS layout as
@@ -2480,7 +2649,67 @@ hipError_t conv_wgrad_partials(int dt, const ConvGeom& g, const void* x, const v
   return conv_wgrad_dma(g, x, dy, partials, nullptr, stream);
 }
 
+namespace {
+bool stem_wgrad_ok(int dt, const ConvGeom& g, int C0) {
+  return dt == DT_BF16 && g.C == 8 && C0 == 3 && g.K == 64 && g.R == 7 && g.S == 7 &&
+         g.stride == 2 && g.pad == 3 && g.P == (g.H - 1) / 2 + 1 && g.Q == (g.W - 1) / 2 + 1 &&
+         g.P >= 1 && g.Q >= 1 && (long long)g.N * g.H * g.W * 8 < (1LL << 40);
+}
+constexpr int STEM_WG_BLOCKS = 256;
+StemWgArgs plan_stem_wgrad(const ConvGeom& g) {
+  StemWgArgs a{};
+  a.g = g;
+  a.py_n = (g.P + 7) / 8;
+  a.px_n = (g.Q + 7) / 8;
+  const long long np = (long long)g.N * a.py_n * a.px_n;
+  a.pps = (int)cdivl(np, std::min<long long>(np, STEM_WG_BLOCKS));
+  a.splits = (int)cdivl(np, a.pps);
+  return a;
+}
+// stem partials [splits][64][49][4], then their group sums
+size_t stem_wgrad_floats(const ConvGeom& g) {
+  const int s = plan_stem_wgrad(g).splits;
+  return (size_t)(s + conv_update_groups(s)) * 64 * 49 * 4;
+}
+hipError_t stem_wgrad(const ConvGeom& g, const void* x, const void* dy, float* partials, float* dw,
+                      hipStream_t stream) {
+  StemWgArgs a = plan_stem_wgrad(g);
+  a.x = (const bf16*)x;
+  a.dy = (const bf16*)dy;
+  a.out = partials;
+  const Cost cost = conv_cost(g, 3, sizeof(bf16), true);
+  KernelTimer* t = t_timer;
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  if (t) {
+    e0 = t->take();
+    e1 = t->take();
+    EKYA_HIP(hipEventRecord(e0, stream));
+  }
+  hipLaunchKernelGGL(wgrad_stem_kernel, dim3(a.splits), dim3(NT), 0, stream, a);
+  hipError_t e = hipGetLastError();
+  if (t && e == hipSuccess) {
+    EKYA_HIP(hipEventRecord(e1, stream));
+    t->recs.push_back({"conv_wgrad<bf16,stem>", cost.flops, cost.bytes, e0, e1});
+  }
+  EKYA_HIP(e);
+  const long long n = 64LL * 49 * 4;
+  const float* sums = partials;
+  int splits = a.splits;
+  if (conv_update_groups(splits) > 0) {
+    float* gs = partials + (long long)splits * n;
+    EKYA_HIP(split_group_sum(partials, splits, n, gs, stream));
+    sums = gs;
+    splits = conv_update_groups(splits);
+  }
+  const long long nw = 64LL * 49 * 3;
+  hipLaunchKernelGGL(wgrad_reduce_kernel, dim3((int)cdivl(nw, 256)), dim3(256), 0, stream, sums,
+                     splits, 64, 49, 4, 3, dw);
+  return hipGetLastError();
+}
+}  // namespace
+
 size_t conv_wgrad_workspace_floats(int dt, const ConvGeom& g) {
+  if (stem_wgrad_ok(dt, g, g.C0 ? g.C0 : g.C)) return stem_wgrad_floats(g);
   if (wgrad_dma_ok(dt, g)) {
     const WgDmaPlan q = plan_wgrad_dma(g);
     return q.splits > 1 ? (size_t)q.splits * g.K * g.R * g.S * g.C : 0;
@@ -2570,8 +2799,10 @@ hipError_t conv_dgrad(int dt, const ConvGeom& g, const void* dy, const void* wt,
                       : conv_dgrad_t<bf16>(g, dy, wt, dx, res, ws, ws_floats, stream, sink);
 }
 
+
 hipError_t conv_wgrad(int dt, const ConvGeom& g, const void* x, const void* dy, float* partials,
                       float* dw, int C0, hipStream_t stream) {
+  if (stem_wgrad_ok(dt, g, C0)) return stem_wgrad(g, x, dy, partials, dw, stream);
   if (wgrad_dma_ok(dt, g) && C0 == g.C) return conv_wgrad_dma(g, x, dy, partials, dw, stream);
   const WPlan p = plan_wgrad(dt, g);
   const long long M = (long long)g.N * g.P * g.Q;

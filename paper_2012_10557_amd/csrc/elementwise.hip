@@ -2010,6 +2010,16 @@ __global__ __launch_bounds__(256) void split_group_kernel(const float* part, int
 
 int conv_update_groups(int splits) { return splits > UPD_GROUP ? cdiv(splits, UPD_GROUP) : 0; }
 
+hipError_t split_group_sum(const float* part, int splits, long long n, float* out,
+                           hipStream_t stream) {
+  const int groups = conv_update_groups(splits);
+  if (groups == 0 || n % 4 != 0) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(split_group_kernel,
+                     dim3((unsigned)std::min<long long>(cdivl(n / 4, 256), 1024), groups), dim3(256),
+                     0, stream, part, splits, n, out);
+  return hipGetLastError();
+}
+
 hipError_t conv_weight_update(int dt, const float* part, int splits, int K, int RS, int C,
                               float* w, float* v, float lr, float mu, void* krsc, void* crsk,
                               hipStream_t stream) {

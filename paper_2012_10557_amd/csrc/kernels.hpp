@@ -118,7 +118,9 @@ hipError_t conv_dgrad(int dt, const ConvGeom& g, const void* dy, const void* w_c
                       const void* res, float* ws, size_t ws_floats, hipStream_t stream,
                       BnStatsSink* sink = nullptr);
 size_t conv_split_workspace_floats(int dt, const ConvGeom& g, bool dgrad);
-// Split count and partial-buffer size (floats) the weight gradient will use.
+// Split count and partial-buffer size (floats) the weight gradient will use;
+// g.C0 must be the real channel count later passed to conv_wgrad as C0 (the
+// bf16 stem, 3 channels stored as 8, has its own kernel and scratch).
 int conv_wgrad_splits(int dt, const ConvGeom& g);
 size_t conv_wgrad_workspace_floats(int dt, const ConvGeom& g);
 // dw[K,R,S,C0] (fp32, unpadded channel count C0 <= C) = sum over pixels of
@@ -247,6 +249,10 @@ hipError_t sgd_momentum_ranges(float* w, float* v, const float* g, const long lo
 // the fp32 [K][RS][C] master, then its [K][RS][C] and [C][RS][K]
 // low-precision copies.
 int conv_update_groups(int splits);
+// out[g][i] = sum of part[s][i] over the splits of group g (16 consecutive
+// splits, in order), g < conv_update_groups(splits); n a multiple of 4.
+hipError_t split_group_sum(const float* part, int splits, long long n, float* out,
+                           hipStream_t stream);
 hipError_t conv_weight_update(int dt, const float* part, int splits, int K, int RS, int C,
                               float* w, float* v, float lr, float mu, void* krsc, void* crsk,
                               hipStream_t stream);
