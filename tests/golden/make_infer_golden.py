@@ -9,10 +9,14 @@ float32 frames.  Calls only the CPU oracle.
 A randomly initialised network sends every frame to one class (its pooled
 features share a large mean, and the classifier row with the largest
 projection on it wins everywhere), which would make label parity trivial.
-The stored classifier is therefore the initial one with that mean direction
-removed from every row (measured on the oracle's own pooled features of the
-bf16 224 px frames) and scaled so the logits spread over a few units; the
+Each case's stored classifier is therefore the initial one with that mean
+direction removed from every row (measured on the oracle's own pooled
+features of that case) and scaled so the logits spread over a few units; the
 test uses it in place of the initial classifier.
+
+Per frame the file also stores the logits' scale max_j sum_i |W_ji f_i| (f
+the oracle's pooled features): a relative error e in the features moves a
+logit by at most e times that, which bounds where two logits may swap.
 
     python tests/golden/make_infer_golden.py   # writes infer_224.json
 """
@@ -67,17 +71,20 @@ def main():
     for prec, res in c["cases"]:
         feats[(prec, res)] = pooled(P, net, frames_for(prec), res)
         print(prec, res, "pooled", round(time.time() - t0, 1), flush=True)
-    F = feats[("bf16", 224)]
-    mu = F.mean(axis=0)
-    W = P["fc.weight"] - np.outer(P["fc.weight"] @ mu, mu) / (mu @ mu)
-    W *= 3.0 / np.std(F @ W.T)
-    W = W.astype(np.float32).astype(np.float64)   # stored as float32 values
-    b = np.zeros(6)
-    out["fc_weight"] = [[float(v) for v in row] for row in W.astype(np.float32)]
-    out["fc_bias"] = [0.0] * 6
-    for (prec, res), Fc in feats.items():
-        lg = nn.linear(Fc, W, b)
+    out["fc"] = {}
+    out["scale"] = {}
+    for (prec, res), F in feats.items():
+        mu = F.mean(axis=0)
+        W = P["fc.weight"] - np.outer(P["fc.weight"] @ mu, mu) / (mu @ mu)
+        W *= 3.0 / np.std(F @ W.T)
+        W = W.astype(np.float32).astype(np.float64)   # stored as float32 values
+        b = np.zeros(6)
+        out["fc"][f"{prec}_{res}"] = {"weight": [[float(v) for v in row] for row in W.astype(np.float32)],
+                                      "bias": [0.0] * 6}
+        lg = nn.linear(F, W, b)
         out["logits"][f"{prec}_{res}"] = [[float("%.12g" % v) for v in row] for row in lg]
+        out["scale"][f"{prec}_{res}"] = [float("%.12g" % v)
+                                         for v in (np.abs(F) @ np.abs(W).T).max(axis=1)]
         print(prec, res, np.bincount(np.argmax(lg, 1), minlength=6), flush=True)
     out["oracle_seconds"] = round(time.time() - t0, 1)
     with open(os.path.join(HERE, "infer_224.json"), "w") as f:
