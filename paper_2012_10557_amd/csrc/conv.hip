@@ -1504,6 +1504,263 @@ __global__ __launch_bounds__(NT, 2) void wgrad_tap_kernel(WgTapArgs a) {
   }
 }
 
+// ------------------------------------ 3x3 / stride 1 convolution, 64 -> 64
+// out[pix][o] = sum over taps (r, s) and input channels i of
+// A[o][r][s][i] * in(pix + d)[i], d = (r - 1, s - 1) for the forward pass
+// (A: weights [K][R][S][C], in: x) and d = (1 - r, 1 - s) for the data
+// gradient (A: [C][R][S][K], in: dy).  With 64 channels on both sides the
+// whole filter (64 x 576) fits in the compute waves' registers for the
+// block's life: compute wave (wm, wn) of a 2 x 2 grid owns output channels
+// 32 wm .. + 31 (two 16-row MFMA tiles) and patch rows 4 wn .. 4 wn + 3 (two
+// 16-pixel tiles) of an 8 x 8 output patch, and holds its rows' 18 k-steps
+// (9 taps x 2 halves of 32 channels) as MFMA operands (144 registers), so
+// only the patches' inputs stream through LDS, in a ring of C64_NST stages:
+// the patch's 10 x 10 input pixels (13 copies of 8 pixel rows, the last 4
+// rows zero), pixel (ty, tx) of the tile holding 16-byte chunk u at
+// u ^ ((ty + tx) mod 8), so that the 16 lanes of a read (8 consecutive
+// pixels of two tile rows) hit distinct banks; then, with a residual, the
+// patch's 64 residual pixels (8 copies, chunk u of pixel p at u ^ (p mod 8)).
+// A fifth wave does all the copying: it never stores, so its vector-memory
+// count covers copies only and it keeps up to C64_NST - 1 stages in flight
+// (3 x 21 copies: the counter has 6 bits) while waiting for the oldest; the
+// compute waves wait on barriers only, never on their own stores.  MFMA row
+// 4 q + j of tile rt is channel 32 wm + 8 q + 4 rt + j, so a lane's
+// accumulators hold 8 consecutive channels of one pixel (one 16-byte store).
+// Blocks are persistent, one per CU (5 waves of at most 256 registers fill a
+// CU's register file).
+constexpr int C64_IN_COPIES = 13;                   // 104 input pixel rows (100 used)
+constexpr int C64_RES_COPIES = 8;
+constexpr int C64_ROWS = 8 * C64_IN_COPIES;
+constexpr int C64_STAGE = (C64_ROWS + 64) * 128;    // input + residual bytes per stage
+constexpr int C64_NST = 4;
+constexpr int C64_NT = 320;                         // 4 compute waves + 1 copy wave
+constexpr int C64_TARGET_BLOCKS = 256;
+static_assert((C64_NST - 1) * (C64_IN_COPIES + C64_RES_COPIES) <= 63, "vector-memory counter");
+
+struct Conv64Args {
+  ConvGeom g;            // the forward convolution (C == K == 64, 3x3, stride 1, pad 1)
+  const bf16* in;        // x (forward) or dy (data gradient), [N][H][W][64]
+  const bf16* a;         // [64][3][3][64]
+  bf16* out;             // [N][H][W][64]
+  ConvEpilogue epi;      // forward: scale, shift, res, relu; data gradient: res only
+  int pps, py_n, px_n;   // patches per block, patches down / across an image
+};
+
+// Copy j (0 .. 20) of the copy wave: 8 staged pixel rows (lane / 8), 16-byte
+// segment lane % 8.  Input rows (j < C64_IN_COPIES): tile pixel p, image
+// offset (p / 10 - 1, p % 10 - 1) from the patch origin, in range only for
+// p < 100 (sy far out otherwise).  Residual rows: patch pixel p - C64_ROWS,
+// offset (p / 8, p % 8).  `off` is the element offset from the patch
+// origin's first channel, chunk swizzled.
+__host__ __device__ inline TapSlot c64_slot(int W, int lane, int j) {
+  const int pix = 8 * j + (lane >> 3);
+  TapSlot t;
+  int sy, sx, sw;
+  if (pix < C64_ROWS) {
+    sy = pix < 100 ? pix / 10 - 1 : -(1 << 24);
+    sx = pix - 10 * (pix / 10) - 1;
+    sw = (pix / 10 + pix % 10) & 7;
+  } else {
+    sy = (pix - C64_ROWS) >> 3;
+    sx = (pix - C64_ROWS) & 7;
+    sw = sx;
+  }
+  const int u = (lane & 7) ^ sw;
+  t.sy = sy;
+  t.sx = sx;
+  t.off = sy > -(1 << 24) ? (sy * W + sx) * 64 + u * 8 : 0;
+  return t;
+}
+
+// One patch out of ring slot SLOT (the slot is an immediate of every LDS
+// read).  fa: the wave's filter operands; rb[v][h]: the lane's read offset
+// for k-step half h when its column's tap pixel (ty, tx) has
+// ty + tx = b + v mod 8 (b: the lane's own pixel, tap offset 0), chunk
+// swizzle included.  The schedule keeps the reads two k-steps ahead of the
+// MFMAs.
+template <bool DGRAD, int SLOT>
+__device__ __forceinline__ void conv64_patch(const char* smem, const uint4 (&fa)[2][18],
+                                             const int (&rb)[8][2], f32x4 (&acc)[2][2]) {
+#pragma unroll
+  for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+    for (int ct = 0; ct < 2; ++ct) acc[rt][ct] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int ks = 0; ks < 18; ++ks) {
+    const int tap = ks >> 1, r = tap / 3, s = tap % 3, h = ks & 1;
+    uint4 fb[2];
+#pragma unroll
+    for (int ct = 0; ct < 2; ++ct) {
+      // tile pixel offset from the lane's own: forward (2 ct + r) rows and s
+      // columns; data gradient (2 ct + 2 - r) rows and 2 - s columns
+      const int d = DGRAD ? 20 * ct + 22 - 10 * r - s : 20 * ct + 10 * r + s;
+      const int v = DGRAD ? (2 * ct + 4 - r - s) & 7 : (2 * ct + r + s) & 7;
+      fb[ct] = *reinterpret_cast<const uint4*>(smem + SLOT * C64_STAGE + d * 128 + rb[v][h]);
+    }
+#pragma unroll
+    for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+      for (int ct = 0; ct < 2; ++ct) mma_unit(acc[rt][ct], fa[rt][ks], fb[ct], (bf16*)nullptr);
+  }
+  // scheduling groups (0x100: LDS reads, 0x008: MFMAs)
+  __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+  }
+  __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+}
+
+template <int L> __device__ __forceinline__ void c64_wait(int later) {
+  // at most `later` (0 .. C64_NST - 2) stages of L copies still in flight
+  if (later >= 2) wait_vmcnt<2 * L>();
+  else if (later == 1) wait_vmcnt<L>();
+  else wait_vmcnt<0>();
+}
+
+template <bool DGRAD>
+__global__ __launch_bounds__(C64_NT) void conv64_kernel(Conv64Args a) {
+  static_assert(C64_NST == 4, "the compute loop selects among 4 slots; c64_wait covers 2 later stages");
+  __shared__ __align__(16) char smem[C64_NST * C64_STAGE];
+  __shared__ __align__(16) float ss[128];  // forward: scale[64], shift[64]
+  const int H = a.g.H, W = a.g.W, N = a.g.N;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int per_img = a.py_n * a.px_n;
+  const int q0 = xcd_tile(blockIdx.x, gridDim.x) * a.pps;
+  const int ns = max(0, min(N * per_img, q0 + a.pps) - q0);
+  const bool has_res = a.epi.res != nullptr;
+  auto origin = [&](int st, int& n, int& py0, int& px0) {
+    const int q = q0 + st;
+    n = q / per_img;
+    const int rem = q - n * per_img, pyi = rem / a.px_n;
+    py0 = 8 * pyi;
+    px0 = 8 * (rem - pyi * a.px_n);
+  };
+
+  if (wave == 4) {
+    // the copy wave: stages 0 .. C64_NST - 2 ahead, then one more per barrier
+    const bf16* const res = reinterpret_cast<const bf16*>(a.epi.res);
+    const void* const zero = g_zero_unit;
+    auto issue = [&](int st) {
+      int n, py0, px0;
+      origin(st, n, py0, px0);
+      const long long pbase = ((long long)n * H * W + (long long)py0 * W + px0) * 64;
+      char* slot = smem + (st % C64_NST) * C64_STAGE;
+#pragma unroll
+      for (int j = 0; j < C64_IN_COPIES + C64_RES_COPIES; ++j) {
+        if (j >= C64_IN_COPIES && !has_res) break;
+        const TapSlot sl = c64_slot(W, lane, j);
+        const bf16* b = (j < C64_IN_COPIES ? a.in : res) + pbase;
+        const bool in = (unsigned)(py0 + sl.sy) < (unsigned)H && (unsigned)(px0 + sl.sx) < (unsigned)W;
+        dma16(in ? (const void*)(b + sl.off) : zero, reinterpret_cast<uint4*>(slot + j * 1024));
+      }
+    };
+    for (int st = 0; st < min(ns, C64_NST - 1); ++st) issue(st);
+    for (int st = 0; st < ns; ++st) {
+      // stage st has landed once only the later stages issued remain
+      const int later = min(ns - 1 - st, C64_NST - 2);
+      if (has_res) c64_wait<C64_IN_COPIES + C64_RES_COPIES>(later);
+      else c64_wait<C64_IN_COPIES>(later);
+      stage_barrier();
+      // every compute wave is past stage st - 1: refill its slot
+      if (st + C64_NST - 1 < ns) issue(st + C64_NST - 1);
+    }
+    return;
+  }
+
+  const int wm = wave >> 1, wn = wave & 1;
+  // the wave's filter rows as MFMA operands: tile rt, row lane % 16 = 4 q + j
+  // (channel 32 wm + 8 q + 4 rt + j), k-step ks = 2 tap + half: channels
+  // 32 half + 8 (lane / 16) .. + 7 of tap ks / 2
+  const int cq = lane & 15, cu = lane >> 4;
+  uint4 fa[2][18];
+#pragma unroll
+  for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+    for (int ks = 0; ks < 18; ++ks) {
+      const int o = 32 * wm + 8 * (cq >> 2) + 4 * rt + (cq & 3);
+      const int ch = 32 * (ks & 1) + 8 * cu;
+      fa[rt][ks] = *reinterpret_cast<const uint4*>(a.a + ((long long)o * 9 + (ks >> 1)) * 64 + ch);
+    }
+  // the lane's column at tap offset 0: patch pixel (4 wn + (lane % 16) / 8,
+  // lane % 8) = tile pixel (ty0, tx0), ip0 (forward: the tap (0, 0) pixel;
+  // data gradient: two rows and columns before the tap (2, 2) pixel)
+  const int ty0 = 4 * wn + (cq >> 3), tx0 = lane & 7;
+  const int ip0 = ty0 * 10 + tx0;
+  int rb[8][2];
+#pragma unroll
+  for (int v = 0; v < 8; ++v)
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+      rb[v][h] = ip0 * 128 + ((((4 * h + cu) ^ ((ty0 + tx0 + v) & 7))) * 16);
+  // this lane's output channels: c0 .. c0 + 7
+  const int c0 = 32 * wm + 8 * cu;
+  const bool affine = !DGRAD && (a.epi.scale || a.epi.shift);
+  if (affine && threadIdx.x < 128) {
+    const int c = threadIdx.x & 63;
+    const float* src = threadIdx.x < 64 ? a.epi.scale : a.epi.shift;
+    ss[threadIdx.x] = src ? src[c] : (threadIdx.x < 64 ? 1.f : 0.f);
+  }
+  const bool relu = !DGRAD && a.epi.relu;
+  // residual pixel pp = 8 ppy + ppx (ppx = lane % 8): chunk c0 / 8 at
+  // (c0 / 8) ^ ppx
+  const int rr = C64_ROWS * 128 + ty0 * 8 * 128 + tx0 * 128 + (((c0 >> 3) ^ tx0) * 16);
+
+  f32x4 acc[2][2];
+  for (int st = 0; st < ns; ++st) {
+    stage_barrier();
+    const int slot = st % C64_NST;
+    switch (slot) {
+      case 0: conv64_patch<DGRAD, 0>(smem, fa, rb, acc); break;
+      case 1: conv64_patch<DGRAD, 1>(smem, fa, rb, acc); break;
+      case 2: conv64_patch<DGRAD, 2>(smem, fa, rb, acc); break;
+      default: conv64_patch<DGRAD, 3>(smem, fa, rb, acc); break;
+    }
+    const char* X = smem + slot * C64_STAGE;
+    int n, py0, px0;
+    origin(st, n, py0, px0);
+#pragma unroll
+    for (int ct = 0; ct < 2; ++ct) {
+      const int ppy = ty0 + 2 * ct, ppx = tx0;
+      float v[8];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        v[j] = acc[0][ct][j];
+        v[4 + j] = acc[1][ct][j];
+      }
+      if (affine) {
+        const float4* s4 = reinterpret_cast<const float4*>(ss + c0);
+        const float4* h4 = reinterpret_cast<const float4*>(ss + 64 + c0);
+        const float4 sa = s4[0], sb = s4[1], ha = h4[0], hb = h4[1];
+        v[0] = v[0] * sa.x + ha.x; v[1] = v[1] * sa.y + ha.y;
+        v[2] = v[2] * sa.z + ha.z; v[3] = v[3] * sa.w + ha.w;
+        v[4] = v[4] * sb.x + hb.x; v[5] = v[5] * sb.y + hb.y;
+        v[6] = v[6] * sb.z + hb.z; v[7] = v[7] * sb.w + hb.w;
+      }
+      if (has_res) {
+        const uint4 rv = *reinterpret_cast<const uint4*>(X + rr + ct * 16 * 128);
+        const bf16x8 rbv = __builtin_bit_cast(bf16x8, rv);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) v[i] += (float)rbv[i];
+      }
+      if (relu) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) v[i] = relu_nan(v[i]);
+      }
+      const int py = py0 + ppy, px = px0 + ppx;
+      if (py < H && px < W) {
+        bf16x8 ob;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) ob[i] = (bf16)v[i];
+        *reinterpret_cast<uint4*>(a.out + (((long long)n * H + py) * W + px) * 64 + c0) =
+            __builtin_bit_cast(uint4, ob);
+      }
+    }
+  }
+}
+
 // ---------------------------------------------- weight gradient of the stem
 // dw[k][r][s][c] = sum over output pixels of dy[pix][k] * x(2p + r - 3,
 // 2q + s - 3)[c] for the 7x7 / stride 2 / pad 3 stem on frames stored with
@@ -2327,12 +2584,62 @@ bool plan_bn_epilogue(const DmaPlan& p) {
   return p.splits == 1 && p.bm == 128 && ((p.bn == 64 && p.ws) || (p.bn == 128 && !p.ws));
 }
 
+// Filter-resident path: 3x3, stride 1, pad 1, 64 -> 64 channels, bf16.
+bool conv64_ok(const ConvGeom& g) {
+  return g.C == 64 && g.K == 64 && g.R == 3 && g.S == 3 && g.stride == 1 && g.pad == 1 &&
+         g.P == g.H && g.Q == g.W && g.N > 0 && g.H > 0 && g.W > 0 &&
+         (long long)g.N * cdiv(g.H, 8) * cdiv(g.W, 8) < (1LL << 30);
+}
+Conv64Args plan_conv64(const ConvGeom& g) {
+  Conv64Args a{};
+  a.g = g;
+  a.py_n = cdiv(g.H, 8);
+  a.px_n = cdiv(g.W, 8);
+  const long long np = (long long)g.N * a.py_n * a.px_n;
+  a.pps = (int)cdivl(np, std::min<long long>(np, C64_TARGET_BLOCKS));
+  return a;
+}
+int conv64_blocks(const Conv64Args& a) {
+  return (int)cdivl((long long)a.g.N * a.py_n * a.px_n, a.pps);
+}
+// in: x (forward) or dy (data gradient); A: w [K][3][3][C] or wt [C][3][3][K].
+hipError_t conv64(const ConvGeom& g, bool dgrad, const void* in, const void* A, void* out,
+                  const ConvEpilogue& epi, hipStream_t stream) {
+  Conv64Args a = plan_conv64(g);
+  a.in = (const bf16*)in;
+  a.a = (const bf16*)A;
+  a.out = (bf16*)out;
+  a.epi = epi;
+  const Cost cost = conv_cost(g, 64, sizeof(bf16), false);
+  KernelTimer* t = t_timer;
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  if (t) {
+    e0 = t->take();
+    e1 = t->take();
+    EKYA_HIP(hipEventRecord(e0, stream));
+  }
+  const int blocks = conv64_blocks(a);
+  if (dgrad)
+    hipLaunchKernelGGL(conv64_kernel<true>, dim3(blocks), dim3(C64_NT), 0, stream, a);
+  else
+    hipLaunchKernelGGL(conv64_kernel<false>, dim3(blocks), dim3(C64_NT), 0, stream, a);
+  hipError_t e = hipGetLastError();
+  if (t && e == hipSuccess) {
+    EKYA_HIP(hipEventRecord(e1, stream));
+    t->recs.push_back({dgrad ? "conv_dgrad<bf16,c64>" : "conv_fwd<bf16,c64>", cost.flops,
+                       cost.bytes, e0, e1});
+  }
+  return e;
+}
+
 // bf16 forward with C % 64 == 0 on the direct-to-LDS path.
 hipError_t conv_fwd_dma(const ConvGeom& g, const void* x, const void* w, void* y,
                         const ConvEpilogue& epi, float* ws, size_t ws_floats, hipStream_t stream,
                         BnStatsSink* sink) {
   const int ns = g.R * g.S * g.C / 64;
   const long long npix = (long long)g.N * g.P * g.Q;
+  if (conv64_ok(g) && !(sink && !sink->bwd && bn_fold_path(npix, g.K)))
+    return conv64(g, false, x, w, y, epi, stream);
   DmaPlan p = plan_dma(g.K, npix, ns, ws != nullptr);
   if (p.splits > 1 && (size_t)p.splits * npix * g.K > ws_floats) p = {p.bm, p.bn, 1, ns, p.ws};
   DmaFwdArgs a{g, (const bf16*)x, (const bf16*)w, (bf16*)y, epi, SplitOut{ws, p.splits, p.sps}, 0, 0};
@@ -2362,6 +2669,11 @@ hipError_t conv_dgrad_dma(const ConvGeom& g, const void* dy, const void* wt, voi
                           BnStatsSink* sink) {
   const int ns = g.R * g.S * g.K / 64;
   const long long npix = (long long)g.N * g.H * g.W;
+  if (conv64_ok(g) && !(sink && sink->bwd && bn_fold_path(npix, g.C))) {
+    ConvEpilogue ep;
+    ep.res = res;
+    return conv64(g, true, dy, wt, dx, ep, stream);
+  }
   DmaPlan p = plan_dma(g.C, npix, ns, ws != nullptr);
   if (p.splits > 1 && (size_t)p.splits * npix * g.C > ws_floats) p = {p.bm, p.bn, 1, ns, p.ws};
   DmaDgradArgs a{g, (const bf16*)dy, (const bf16*)wt, (bf16*)dx, (const bf16*)res,

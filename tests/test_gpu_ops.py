@@ -35,6 +35,7 @@ CONV_CASES = [
     (84, 28, 28, 128, 128, 3, 1, 1),  # layer2, 258 tiles of 128 x 256 (ragged)
     # frozen-prefix shapes at cache-build batch sizes: more tiles than CUs
     (48, 56, 56, 64, 64, 3, 1, 1),    # layer1, 588 tiles of 64 x 256
+    (60, 20, 20, 64, 64, 3, 1, 1),    # 64 -> 64: two 8 x 8 patches per block, ragged patches
     (168, 28, 28, 128, 128, 3, 1, 1), # layer2, 515 tiles of 128 x 256
     (336, 14, 14, 256, 256, 3, 1, 1), # layer3, 515 tiles of 256 x 128 (ragged)
 ]
