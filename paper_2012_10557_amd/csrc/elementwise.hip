@@ -45,13 +45,16 @@ inline int grid_for(long long n, int per_block = 256, int cap = 8192) {
   return (int)std::min<long long>(b, cap);
 }
 
-// Chunking of the M rows for per-channel reductions.
-// Chunks of rows for the partial sums of large-M BatchNorm: at least 256 rows
-// each and at most 512 of them -- two blocks per CU stream the activations,
-// and the final per-channel reduction reads at most 512 partials.
-inline int bn_chunks(long long M) {
-  long long c = cdivl(M, 256);
-  if (c > 512) c = 512;
+// Chunks of rows for the partial sums of large-M BatchNorm: about
+// BN_CHUNK_ELEMS elements each (at least one row) and at most BN_MAX_CHUNKS
+// of them -- up to four blocks per CU stream the activations, and the final
+// per-channel reduction reads each channel's partials in one round of loads.
+constexpr int BN_MAX_CHUNKS = 1024;
+constexpr long long BN_CHUNK_ELEMS = 16384;
+inline int bn_chunks(long long M, int C) {
+  long long c = cdivl(M * C, BN_CHUNK_ELEMS);
+  if (c > BN_MAX_CHUNKS) c = BN_MAX_CHUNKS;
+  if (c > M) c = M;
   if (c < 1) c = 1;
   return (int)c;
 }
@@ -74,8 +77,8 @@ __global__ __launch_bounds__(256) void bn_stats_partial(const T* z, long long M,
   for (int i = 0; i < E; ++i) s1[i] = s2[i] = 0.f;
   if (rsub < rpi) {
     unit_to_f<T>(*reinterpret_cast<const uint4*>(z + cu * E), K);
-    // four rows' loads issued before they are accumulated (in row order)
-    constexpr int U = 4;
+    // eight rows' loads issued before they are accumulated (in row order)
+    constexpr int U = 8;
     for (long long r = r0 + rsub; r < r1; r += U * rpi) {
       uint4 raw[U];
 #pragma unroll
@@ -118,48 +121,48 @@ __global__ __launch_bounds__(256) void bn_stats_partial(const T* z, long long M,
 }
 
 // Fixed-order sum over chunks of the two partial rows of channel c: a block
-// handles 16 channels with 16 threads each (thread slice k sums chunks k,
-// k+16, ...; 16 consecutive channels per load, so each read is 64 bytes), and
-// the 16 slice sums are added in slice order in double.  A thread issues the
-// loads of 8 of its chunks before adding them, so their latencies overlap.
-// Returns true for the one thread per channel that holds the totals.
-constexpr int FIN_CH = 16;
-constexpr int FIN_BATCH = 8;
+// handles FIN_CH channels with FIN_SL threads each (thread slice k sums chunks
+// k, k + FIN_SL, ... -- at most FIN_PER of them, all loads issued before the
+// adds, so one round of latency), and the slice sums are added in slice order
+// in double.  Returns true for the one thread per channel that holds the
+// totals.
+constexpr int FIN_CH = 4;
+constexpr int FIN_SL = 64;
+constexpr int FIN_PER = BN_MAX_CHUNKS / FIN_SL;
 __device__ __forceinline__ bool chunk_sums(const float* part, int nchunks, int C, double& a,
                                            double& b) {
-  __shared__ float sa[16][FIN_CH], sb[16][FIN_CH];
-  const int lc = threadIdx.x & (FIN_CH - 1), slice = threadIdx.x / FIN_CH;
+  __shared__ float sa[FIN_SL][FIN_CH], sb[FIN_SL][FIN_CH];
+  const int lc = threadIdx.x % FIN_CH, slice = threadIdx.x / FIN_CH;
   const int c = blockIdx.x * FIN_CH + lc;
   float x = 0.f, y = 0.f;
-  if (c < C)
-    for (int k0 = slice; k0 < nchunks; k0 += 16 * FIN_BATCH) {
-      float v1[FIN_BATCH], v2[FIN_BATCH];
+  if (c < C) {
+    float v1[FIN_PER], v2[FIN_PER];
 #pragma unroll
-      for (int u = 0; u < FIN_BATCH; ++u) {
-        const int k = k0 + 16 * u;
-        v1[u] = k < nchunks ? part[(long long)k * 2 * C + c] : 0.f;
-        v2[u] = k < nchunks ? part[(long long)k * 2 * C + C + c] : 0.f;
-      }
-#pragma unroll
-      for (int u = 0; u < FIN_BATCH; ++u)
-        if (k0 + 16 * u < nchunks) {
-          x += v1[u];
-          y += v2[u];
-        }
+    for (int u = 0; u < FIN_PER; ++u) {
+      const int k = slice + FIN_SL * u;
+      v1[u] = k < nchunks ? part[(long long)k * 2 * C + c] : 0.f;
+      v2[u] = k < nchunks ? part[(long long)k * 2 * C + C + c] : 0.f;
     }
+#pragma unroll
+    for (int u = 0; u < FIN_PER; ++u)
+      if (slice + FIN_SL * u < nchunks) {
+        x += v1[u];
+        y += v2[u];
+      }
+  }
   sa[slice][lc] = x;
   sb[slice][lc] = y;
   __syncthreads();
   if (slice != 0 || c >= C) return false;
   a = 0.0;
   b = 0.0;
-#pragma unroll
-  for (int k = 0; k < 16; ++k) {
+  for (int k = 0; k < FIN_SL; ++k) {
     a += (double)sa[k][lc];
     b += (double)sb[k][lc];
   }
   return true;
 }
+static_assert(FIN_CH * FIN_SL == 256, "chunk_sums runs in 256-thread blocks");
 
 template <typename T>
 __global__ __launch_bounds__(256) void bn_stats_final(const T* z, const float* part, int nchunks,
@@ -709,8 +712,8 @@ __global__ __launch_bounds__(256) void bn_bwd_partial(const T* dy, const T* y, c
     mu[i] = mean[cu * E + i];
   }
   if (rsub < rpi) {
-    // two rows' loads issued before they are accumulated (in row order)
-    constexpr int U = 2;
+    // four rows' loads issued before they are accumulated (in row order)
+    constexpr int U = 4;
     for (long long r = r0 + rsub; r < r1; r += U * rpi) {
       uint4 rg[U], rz[U], ry[U];
 #pragma unroll
@@ -808,78 +811,131 @@ __global__ void bn_bwd_apply(const T* dy, const T* y, const T* z, long long unit
 }
 
 // ---------------------------------------------------------------- pooling
-template <typename T>
-__global__ void maxpool_fwd_kernel(const T* x, int N, int H, int W, int C, int P, int Q, T* y,
-                                   uint8_t* arg) {
-  constexpr int E = Elt<T>::E;
-  const int cu = C / E;
-  const long long units = (long long)N * P * Q * cu;
-  for (long long u = blockIdx.x * (long long)blockDim.x + threadIdx.x; u < units;
-       u += (long long)gridDim.x * blockDim.x) {
-    const int c0 = (int)(u % cu) * E;
-    const long long pix = u / cu;
-    const int q = (int)(pix % Q), p = (int)((pix / Q) % P), n = (int)(pix / ((long long)P * Q));
-    float best[E];
-    int ba[E];
+// E window indices (bytes) of one 16-byte unit, moved as one 4- or 8-byte word.
+template <int E> struct ArgWord;
+template <> struct ArgWord<8> { using type = uint2; };
+template <> struct ArgWord<4> { using type = uint32_t; };
+template <int E> __device__ __forceinline__ void arg_load(const uint8_t* p, int (&a)[E]) {
+  union {
+    typename ArgWord<E>::type w;
+    uint8_t b[E];
+  } u;
+  u.w = *reinterpret_cast<const typename ArgWord<E>::type*>(p);
 #pragma unroll
-    for (int i = 0; i < E; ++i) {
-      best[i] = -INFINITY;
-      ba[i] = 0;
-    }
-    for (int r = 0; r < 3; ++r) {
-      const int h = 2 * p + r - 1;
-      if (h < 0 || h >= H) continue;
-      for (int s = 0; s < 3; ++s) {
-        const int w = 2 * q + s - 1;
-        if (w < 0 || w >= W) continue;
-        float v[E];
-        unit_to_f<T>(*reinterpret_cast<const uint4*>(x + (((long long)n * H + h) * W + w) * C + c0), v);
+  for (int i = 0; i < E; ++i) a[i] = u.b[i];
+}
+template <int E> __device__ __forceinline__ void arg_store(uint8_t* p, const int (&a)[E]) {
+  union {
+    typename ArgWord<E>::type w;
+    uint8_t b[E];
+  } u;
 #pragma unroll
-        for (int i = 0; i < E; ++i)
-          if (v[i] > best[i]) {
-            best[i] = v[i];
-            ba[i] = r * 3 + s;
-          }
-      }
-    }
-    reinterpret_cast<uint4*>(y)[u] = f_to_unit<T>(best);
-    if (arg) {
-#pragma unroll
-      for (int i = 0; i < E; ++i) arg[u * E + i] = (uint8_t)ba[i];
-    }
-  }
+  for (int i = 0; i < E; ++i) u.b[i] = (uint8_t)a[i];
+  *reinterpret_cast<typename ArgWord<E>::type*>(p) = u.w;
 }
 
+// 3x3 / stride 2 / pad 1 max pool.  One block covers 256 units (pixel x
+// 16-byte channel unit) of one output row; bpr blocks per row (the row index
+// from the block index is uniform, so no per-lane wide division).
 template <typename T>
-__global__ void maxpool_bwd_kernel(const T* dy, const uint8_t* arg, int N, int H, int W, int C,
-                                   int P, int Q, T* dx) {
+__global__ __launch_bounds__(256) void maxpool_fwd_kernel(const T* x, int N, int H, int W, int C,
+                                                          int P, int Q, int bpr, T* y,
+                                                          uint8_t* arg) {
   constexpr int E = Elt<T>::E;
   const int cu = C / E;
-  const long long units = (long long)N * H * W * cu;
-  for (long long u = blockIdx.x * (long long)blockDim.x + threadIdx.x; u < units;
-       u += (long long)gridDim.x * blockDim.x) {
-    const int c0 = (int)(u % cu) * E;
-    const long long pix = u / cu;
-    const int w = (int)(pix % W), h = (int)((pix / W) % H), n = (int)(pix / ((long long)H * W));
-    float acc[E];
+  const int row = blockIdx.x / bpr;  // n * P + p
+  const int t = (blockIdx.x - row * bpr) * 256 + threadIdx.x;
+  if (row >= N * P || t >= Q * cu) return;
+  const int q = t / cu, c0 = (t - q * cu) * E;
+  const int n = row / P, p = row - n * P;
+  float best[E];
+  int ba[E];
 #pragma unroll
-    for (int i = 0; i < E; ++i) acc[i] = 0.f;
-    for (int r = 0; r < 3; ++r) {
-      const int hp = h + 1 - r;
-      if (hp < 0 || (hp & 1) || (hp >> 1) >= P) continue;
-      for (int s = 0; s < 3; ++s) {
-        const int wp = w + 1 - s;
-        if (wp < 0 || (wp & 1) || (wp >> 1) >= Q) continue;
-        const long long o = (((long long)n * P + (hp >> 1)) * Q + (wp >> 1)) * C + c0;
-        float g[E];
-        unit_to_f<T>(*reinterpret_cast<const uint4*>(dy + o), g);
-#pragma unroll
-        for (int i = 0; i < E; ++i)
-          if (arg[o + i] == r * 3 + s) acc[i] += g[i];
-      }
-    }
-    reinterpret_cast<uint4*>(dx)[u] = f_to_unit<T>(acc);
+  for (int i = 0; i < E; ++i) {
+    best[i] = -INFINITY;
+    ba[i] = 0;
   }
+  // all nine window loads in flight before the comparisons (in window order)
+  uint4 raw[9];
+  bool ok[9];
+#pragma unroll
+  for (int r = 0; r < 3; ++r)
+#pragma unroll
+    for (int s = 0; s < 3; ++s) {
+      const int h = 2 * p + r - 1, w = 2 * q + s - 1;
+      ok[3 * r + s] = h >= 0 && h < H && w >= 0 && w < W;
+      raw[3 * r + s] = ok[3 * r + s]
+                           ? *reinterpret_cast<const uint4*>(x + (((long long)n * H + h) * W + w) * C + c0)
+                           : uint4{0, 0, 0, 0};
+    }
+#pragma unroll
+  for (int k = 0; k < 9; ++k) {
+    if (!ok[k]) continue;
+    float v[E];
+    unit_to_f<T>(raw[k], v);
+#pragma unroll
+    for (int i = 0; i < E; ++i)
+      if (v[i] > best[i]) {
+        best[i] = v[i];
+        ba[i] = k;
+      }
+  }
+  const long long o = ((long long)row * Q + q) * C + c0;
+  *reinterpret_cast<uint4*>(y + o) = f_to_unit<T>(best);
+  if (arg) arg_store<E>(arg + o, ba);
+}
+
+// Input gradient of the max pool: a gather over the (at most 2 x 2) windows
+// that contain the pixel, adding the output gradient of each whose recorded
+// maximum is this pixel.  Blocks as in the forward pass, over input rows.
+template <typename T>
+__global__ __launch_bounds__(256) void maxpool_bwd_kernel(const T* dy, const uint8_t* arg, int N,
+                                                          int H, int W, int C, int P, int Q,
+                                                          int bpr, T* dx) {
+  constexpr int E = Elt<T>::E;
+  const int cu = C / E;
+  const int row = blockIdx.x / bpr;  // n * H + h
+  const int t = (blockIdx.x - row * bpr) * 256 + threadIdx.x;
+  if (row >= N * H || t >= W * cu) return;
+  const int w = t / cu, c0 = (t - w * cu) * E;
+  const int n = row / H, h = row - n * H;
+  float acc[E];
+#pragma unroll
+  for (int i = 0; i < E; ++i) acc[i] = 0.f;
+  // window row / column offsets r, s with h + 1 - r and w + 1 - s even: one
+  // (even coordinate) or two (odd) of each; all loads in flight before the adds
+  const int r0 = (h & 1) ? 0 : 1, nr = (h & 1) ? 2 : 1;
+  const int s0 = (w & 1) ? 0 : 1, nsw = (w & 1) ? 2 : 1;
+  uint4 graw[4];
+  int a[4][E];
+  bool ok[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int r = r0 + 2 * (k >> 1), s = s0 + 2 * (k & 1);
+    const int hp = h + 1 - r, wp = w + 1 - s;
+    ok[k] = (k >> 1) < nr && (k & 1) < nsw && hp >= 0 && (hp >> 1) < P && wp >= 0 && (wp >> 1) < Q;
+    const long long o = (((long long)n * P + (hp >> 1)) * Q + (wp >> 1)) * C + c0;
+    if (ok[k]) {
+      graw[k] = *reinterpret_cast<const uint4*>(dy + o);
+      arg_load<E>(arg + o, a[k]);
+    } else {
+      graw[k] = uint4{0, 0, 0, 0};
+#pragma unroll
+      for (int i = 0; i < E; ++i) a[k][i] = -1;
+    }
+  }
+  // windows in (r, s) order, as a row-major walk over the 3 x 3 offsets
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    if (!ok[k]) continue;
+    const int r = r0 + 2 * (k >> 1), s = s0 + 2 * (k & 1);
+    float g[E];
+    unit_to_f<T>(graw[k], g);
+#pragma unroll
+    for (int i = 0; i < E; ++i)
+      if (a[k][i] == r * 3 + s) acc[i] += g[i];
+  }
+  *reinterpret_cast<uint4*>(dx + ((long long)row * W + w) * C + c0) = f_to_unit<T>(acc);
 }
 
 template <typename T>
@@ -1638,7 +1694,7 @@ hipError_t by_type(int dt, F&& f) {
 // partial kernel and the 64-row chunks GEMM epilogues and the classifier-head
 // backward leave; plus the per-channel coefficients of the large-M backward.
 size_t bn_partials_floats(long long M, int C) {
-  long long ch = bn_chunks(M);
+  long long ch = bn_chunks(M, C);
   if (bn_fold_ok(M, C)) ch = std::max(ch, cdivl(M, 64));
   return (size_t)ch * 2 * C + 3 * C;
 }
@@ -1647,7 +1703,7 @@ hipError_t bn_train_stats(int dt, const void* z, long long M, int C, const float
                           const float* beta, float* rm, float* rv, float* mean, float* invstd,
                           float* scale, float* shift, float* partials, hipStream_t stream) {
   if (M == 0) return hipSuccess;
-  const int nch = bn_chunks(M);
+  const int nch = bn_chunks(M, C);
   const long long rpc = cdivl(M, nch);
   return by_type(dt, [&](auto* tp) {
     using T = std::remove_pointer_t<decltype(tp)>;
@@ -1775,7 +1831,7 @@ hipError_t bn_backward(int dt, const void* dy, const void* y, const void* z, lon
                          gamma, mean, invstd, dgamma, dbeta, (T*)dz, (T*)g_out);
     }), "bn_bwd_apply", apply_bytes);
   }
-  const int nch = bn_chunks(M);
+  const int nch = bn_chunks(M, C);
   const long long rpc = cdivl(M, nch);
   float* coef = partials + (size_t)nch * 2 * C;
   const long long units = M * C / dtype_vec(dt);
@@ -1805,8 +1861,9 @@ hipError_t maxpool_fwd(int dt, const void* x, int N, int H, int W, int C, void* 
   TimedLaunch tl(stream);  // input once; output (and its window index)
   return tl.done(by_type(dt, [&](auto* tp) {
     using T = std::remove_pointer_t<decltype(tp)>;
-    hipLaunchKernelGGL(maxpool_fwd_kernel<T>, dim3(grid_for(units)), dim3(256), 0, stream,
-                       (const T*)x, N, H, W, C, P, Q, (T*)y, arg);
+    const int bpr = cdiv(Q * (C / Elt<T>::E), 256);
+    hipLaunchKernelGGL(maxpool_fwd_kernel<T>, dim3((unsigned)((long long)N * P * bpr)), dim3(256), 0,
+                       stream, (const T*)x, N, H, W, C, P, Q, bpr, (T*)y, arg);
   }), "maxpool_fwd", (double)N * C * ((double)H * W * es + (double)P * Q * (es + (arg ? 1 : 0))));
 }
 
@@ -1819,8 +1876,9 @@ hipError_t maxpool_bwd(int dt, const void* dy, const uint8_t* arg, int N, int H,
   TimedLaunch tl(stream);  // output gradient and window index once; input gradient
   return tl.done(by_type(dt, [&](auto* tp) {
     using T = std::remove_pointer_t<decltype(tp)>;
-    hipLaunchKernelGGL(maxpool_bwd_kernel<T>, dim3(grid_for(units)), dim3(256), 0, stream,
-                       (const T*)dy, arg, N, H, W, C, P, Q, (T*)dx);
+    const int bpr = cdiv(W * (C / Elt<T>::E), 256);
+    hipLaunchKernelGGL(maxpool_bwd_kernel<T>, dim3((unsigned)((long long)N * H * bpr)), dim3(256), 0,
+                       stream, (const T*)dy, arg, N, H, W, C, P, Q, bpr, (T*)dx);
   }), "maxpool_bwd", (double)N * C * ((double)P * Q * (es + 1) + (double)H * W * es));
 }
 
