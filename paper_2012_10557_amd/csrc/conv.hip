@@ -629,7 +629,7 @@ struct DmaFwdOp {
   int split;
 
   // reduction stages [s0, s1) of a split: 64-element steps of R*S*C
-  static __device__ void stage_range(const Args& a, int split, int& s0, int& s1) {
+  static __device__ void stage_range(const Args& a, int split, int n0, int& s0, int& s1) {
     const int ns = a.g.R * a.g.S * a.g.C / 64;
     s0 = min(ns, split * a.so.stages_per_split);
     s1 = min(ns, s0 + a.so.stages_per_split);
@@ -639,7 +639,7 @@ struct DmaFwdOp {
     const ConvGeom& g = a.g;
     split = split_;
     Ktot = (long long)g.R * g.S * g.C;
-    stage_range(a, split, s_begin, s_end);
+    stage_range(a, split, n0, s_begin, s_end);
     const int npix = g.N * g.P * g.Q;
     const int r8 = lane >> 3, u = (lane & 7) ^ r8;
 #pragma unroll
@@ -759,7 +759,7 @@ struct DmaDgradOp {
   int split;
 
   // reduction stages [s0, s1) of a split: 64-element steps of R*S*K
-  static __device__ void stage_range(const Args& a, int split, int& s0, int& s1) {
+  static __device__ void stage_range(const Args& a, int split, int n0, int& s0, int& s1) {
     const int ns = a.g.R * a.g.S * a.g.K / 64;
     s0 = min(ns, split * a.so.stages_per_split);
     s1 = min(ns, s0 + a.so.stages_per_split);
@@ -769,7 +769,7 @@ struct DmaDgradOp {
     const ConvGeom& g = a.g;
     split = split_;
     Ktot = (long long)g.R * g.S * g.K;
-    stage_range(a, split, s_begin, s_end);
+    stage_range(a, split, n0, s_begin, s_end);
     const int npix = g.N * g.H * g.W;
     const int r8 = lane >> 3, u = (lane & 7) ^ r8;
 #pragma unroll
@@ -848,6 +848,156 @@ struct DmaDgradOp {
       load4<bf16>(a.res + off, r);
 #pragma unroll
       for (int i = 0; i < 4; ++i) v[i] += r[i];
+    }
+    store4_keep(a.dx + off, v);
+    return true;
+  }
+};
+
+// Stride-2 data gradient by parity class.  Input pixel (h, w) = (2 i + ph,
+// 2 j + pw) receives exactly the taps r = r0, r0 + 2, ... (r0 = (ph + pad)
+// mod 2) and s = s0, s0 + 2, ..., from output-gradient pixel
+// (i + (ph + pad - r) / 2, j + (pw + pad - s) / 2); the taps in between would
+// only multiply zeros.  Each parity class (ph, pw) is its own GEMM over the
+// class's pixels with a reduction over its own taps only: column tile ct
+// belongs to class ct mod 4 (so every range of tiles mixes the light and
+// heavy classes), class-local column (ct / 4) * BN + offset.  A class with no
+// taps (1x1 kernels, odd pixels) writes zeros (plus the residual).
+struct DmaDgradS2Args {
+  ConvGeom g;
+  const bf16* dy;
+  const bf16* wt;  // [C][R][S][K]
+  bf16* dx;
+  const bf16* res;
+  SplitOut so;
+  int tiles_m, tiles_n;
+  BnEpi bn;        // unused (no BatchNorm-statistics epilogue on this path)
+};
+
+struct S2Class {
+  int ph, pw, hc, wc, r0, nr, s0, nsc;
+};
+__host__ __device__ inline S2Class s2_class(const ConvGeom& g, int cls) {
+  S2Class k;
+  k.ph = cls >> 1;
+  k.pw = cls & 1;
+  k.hc = (g.H - k.ph + 1) / 2;  // rows h = 2 i + ph < H
+  k.wc = (g.W - k.pw + 1) / 2;
+  k.r0 = (k.ph + g.pad) & 1;
+  k.nr = (g.R - k.r0 + 1) / 2;
+  k.s0 = (k.pw + g.pad) & 1;
+  k.nsc = (g.S - k.s0 + 1) / 2;
+  return k;
+}
+
+template <int BM, int BN>
+struct DmaDgradS2Op {
+  static constexpr int GA = BM / 8, IPW = (BM + BN) / 32;
+  using Args = DmaDgradS2Args;
+  int s_begin, s_end;
+  long long Ktot;
+  const bf16* ptr[IPW];
+  int pi[IPW], qj[IPW];  // output-gradient pixel of the class's first tap (r0, s0)
+  bool ok[IPW];
+  int tr, ts, tk;        // tap (r0 + 2 tr, s0 + 2 ts), channel offset
+  int r0, s0, nsc;
+  int split;
+
+  // reduction stages [s0, s1) of a split: 64-element steps over the class's
+  // taps x K
+  static __device__ void stage_range(const Args& a, int split, int n0, int& s0, int& s1) {
+    const S2Class k = s2_class(a.g, (n0 / BN) & 3);
+    const int ns = k.nr * k.nsc * a.g.K / 64;
+    s0 = min(ns, split * a.so.stages_per_split);
+    s1 = min(ns, s0 + a.so.stages_per_split);
+  }
+
+  __device__ void init(const Args& a, int m0, int n0, int split_, int wave, int lane) {
+    const ConvGeom& g = a.g;
+    split = split_;
+    Ktot = (long long)g.R * g.S * g.K;
+    stage_range(a, split, n0, s_begin, s_end);
+    const int ct = n0 / BN;
+    const S2Class k = s2_class(g, ct & 3);
+    r0 = k.r0;
+    s0 = k.s0;
+    nsc = k.nsc;
+    const int mc = g.N * k.hc * k.wc, lbase = (ct >> 2) * BN;
+    const int r8 = lane >> 3, u = (lane & 7) ^ r8;
+#pragma unroll
+    for (int j = 0; j < IPW; ++j) {
+      const int oct = wave + 4 * j;
+      if (oct < GA) {
+        const int row = m0 + oct * 8 + r8;
+        ok[j] = row < g.C;
+        ptr[j] = a.wt + (ok[j] ? row : 0) * Ktot + u * 8;
+        pi[j] = qj[j] = 0;
+      } else {
+        const int l = lbase + (oct - GA) * 8 + r8;
+        ok[j] = l < mc;
+        const int ll = ok[j] ? l : 0;
+        const int n = ll / (k.hc * k.wc), rem = ll - n * (k.hc * k.wc);
+        const int i = rem / k.wc, jj = rem - i * k.wc;
+        pi[j] = i + (k.ph + g.pad - k.r0) / 2;
+        qj[j] = jj + (k.pw + g.pad - k.s0) / 2;
+        ptr[j] = a.dy + (long long)n * g.P * g.Q * g.K + u * 8;
+      }
+    }
+    const int k0 = s_begin * 64;
+    const int rs = k0 / g.K;
+    tk = k0 - rs * g.K;
+    tr = rs / max(nsc, 1);
+    ts = rs - tr * max(nsc, 1);
+  }
+  __device__ void issue(const Args& a, int st, uint4* slot, int wave, const void* zero) {
+    const ConvGeom& g = a.g;
+    (void)st;
+    const int woff = ((r0 + 2 * tr) * g.S + (s0 + 2 * ts)) * g.K + tk;
+#pragma unroll
+    for (int j = 0; j < IPW; ++j) {
+      const int oct = wave + 4 * j;
+      const void* src;
+      if (oct < GA) {
+        src = ok[j] ? (const void*)(ptr[j] + woff) : zero;
+      } else {
+        const int p = pi[j] - tr, q = qj[j] - ts;
+        const bool in = ok[j] && (unsigned)p < (unsigned)g.P && (unsigned)q < (unsigned)g.Q;
+        src = in ? (const void*)(ptr[j] + ((p * g.Q + q) * g.K + tk)) : zero;
+      }
+      dma16(src, slot + oct * 64);
+    }
+    tk += 64;
+    if (tk >= g.K) {
+      tk = 0;
+      if (++ts == nsc) {
+        ts = 0;
+        ++tr;
+      }
+    }
+  }
+  static __device__ int chans(const Args& a) { return a.g.C; }
+  static __device__ int pixels(const Args& a) { return a.g.N * a.g.H * a.g.W; }
+  __device__ bool out4(const Args& a, int row, int col, float (&v)[4]) {
+    const ConvGeom& g = a.g;
+    const int ct = col / BN;
+    const S2Class k = s2_class(g, ct & 3);
+    const int l = (ct >> 2) * BN + (col - ct * BN);
+    if (row >= g.C || l >= g.N * k.hc * k.wc) return false;
+    const int n = l / (k.hc * k.wc), rem = l - n * (k.hc * k.wc);
+    const int i = rem / k.wc, jj = rem - i * k.wc;
+    const long long pix = ((long long)n * g.H + 2 * i + k.ph) * g.W + 2 * jj + k.pw;
+    const long long off = pix * g.C + row;
+    if (a.so.splits > 1) {
+      const long long npix = (long long)g.N * g.H * g.W;
+      float* dst = a.so.part + (long long)split * npix * g.C + off;
+      *reinterpret_cast<float4*>(dst) = make_float4(v[0], v[1], v[2], v[3]);
+      return false;
+    }
+    if (a.res) {
+      float r[4];
+      load4<bf16>(a.res + off, r);
+#pragma unroll
+      for (int i2 = 0; i2 < 4; ++i2) v[i2] += r[i2];
     }
     store4_keep(a.dx + off, v);
     return true;
@@ -1106,7 +1256,7 @@ __global__ __launch_bounds__((BM / WTM) * (BN / WTN) * 64 + WS_LOADERS * 64) voi
   const int split = item / tiles, t = item - split * tiles;
   const int m0 = (t % a.tiles_m) * BM, n0 = (t / a.tiles_m) * BN;
   int s0, s1;
-  Op::stage_range(a, split, s0, s1);
+  Op::stage_range(a, split, n0, s0, s1);
 
   // The two roles run separate loops (their registers are never live
   // together) with the same barrier count: one before the loop, one per stage.
@@ -2663,6 +2813,45 @@ hipError_t conv_fwd_dma(const ConvGeom& g, const void* x, const void* w, void* y
   return split_finish<bf16>(ws, p.splits, npix, g.K, epi, y, stream);
 }
 
+// Stride-2 bf16 data gradient by parity class (DmaDgradS2Op): the GEMM plan
+// is chosen for the average reduction length (a quarter of the taps); the
+// split length covers the longest class.
+DmaPlan plan_dgrad_s2(const ConvGeom& g, bool allow_split) {
+  const int kc = g.K / 64;
+  int ns_max = 0, ns_sum = 0;
+  for (int c = 0; c < 4; ++c) {
+    const S2Class k = s2_class(g, c);
+    ns_max = std::max(ns_max, k.nr * k.nsc * kc);
+    ns_sum += k.nr * k.nsc * kc;
+  }
+  const long long npix = (long long)g.N * g.H * g.W;
+  DmaPlan p = plan_dma(g.C, npix, std::max(1, cdiv(ns_sum, 4)), allow_split);
+  if (!allow_split) p.splits = 1;
+  p.sps = std::max(1, cdiv(ns_max, p.splits));
+  return p;
+}
+
+hipError_t conv_dgrad_s2(const ConvGeom& g, const void* dy, const void* wt, void* dx,
+                         const void* res, float* ws, size_t ws_floats, hipStream_t stream) {
+  const long long npix = (long long)g.N * g.H * g.W;
+  DmaPlan p = plan_dgrad_s2(g, ws != nullptr);
+  if (p.splits > 1 && (size_t)p.splits * npix * g.C > ws_floats) p = plan_dgrad_s2(g, false);
+  long long ctiles = 0;
+  for (int c = 0; c < 4; ++c) {
+    const S2Class k = s2_class(g, c);
+    ctiles = std::max(ctiles, cdivl((long long)g.N * k.hc * k.wc, p.bn));
+  }
+  const long long cols = 4 * ctiles * p.bn;
+  DmaDgradS2Args a{g, (const bf16*)dy, (const bf16*)wt, (bf16*)dx, (const bf16*)res,
+                   SplitOut{ws, p.splits, p.sps}, 0, 0, BnEpi{}};
+  hipError_t e = dispatch_dma<DmaDgradS2Op>(a, p, cols, g.C, stream,
+                                           conv_cost(g, g.C, sizeof(bf16), false), "conv_dgrad_s2");
+  if (e != hipSuccess || p.splits <= 1) return e;
+  ConvEpilogue ep;
+  ep.res = res;
+  return split_finish<bf16>(ws, p.splits, npix, g.C, ep, dx, stream);
+}
+
 // bf16 data gradient with K % 64 == 0 on the direct-to-LDS path.
 hipError_t conv_dgrad_dma(const ConvGeom& g, const void* dy, const void* wt, void* dx,
                           const void* res, float* ws, size_t ws_floats, hipStream_t stream,
@@ -2674,6 +2863,10 @@ hipError_t conv_dgrad_dma(const ConvGeom& g, const void* dy, const void* wt, voi
     ep.res = res;
     return conv64(g, true, dy, wt, dx, ep, stream);
   }
+  // (1x1 kernels: only one class has a tap and its reduction is too short to
+  // amortise a tile's pipeline fill; the plain GEMM measured faster)
+  if (g.stride == 2 && g.R * g.S > 1 && !(sink && sink->bwd && bn_fold_path(npix, g.C)))
+    return conv_dgrad_s2(g, dy, wt, dx, res, ws, ws_floats, stream);
   DmaPlan p = plan_dma(g.C, npix, ns, ws != nullptr);
   if (p.splits > 1 && (size_t)p.splits * npix * g.C > ws_floats) p = {p.bm, p.bn, 1, ns, p.ws};
   DmaDgradArgs a{g, (const bf16*)dy, (const bf16*)wt, (bf16*)dx, (const bf16*)res,
@@ -2803,7 +2996,8 @@ size_t conv_split_workspace_floats(int dt, const ConvGeom& g, bool dgrad) {
   const int E = dtype_vec(dt);
   if (dt == DT_BF16 && dgrad) {
     const long long npix = (long long)g.N * g.H * g.W;
-    const DmaPlan p = plan_dma(g.C, npix, g.R * g.S * g.K / 64, true);
+    const DmaPlan p = g.stride == 2 && g.R * g.S > 1 ? plan_dgrad_s2(g, true)
+                                                     : plan_dma(g.C, npix, g.R * g.S * g.K / 64, true);
     return p.splits > 1 ? (size_t)p.splits * npix * g.C : 0;
   }
   if (dt == DT_BF16 && g.C % 64 == 0) {
