@@ -59,6 +59,39 @@ inline int bn_chunks(long long M, int C) {
   return (int)c;
 }
 
+// The ReLU mask of a BatchNorm output recomputed from its input: the forward
+// pass stored y = relu((z - mean) * (gamma * invstd) + beta) as T (one fused
+// multiply-add, as below), so y > 0 exactly when that value rounded to T is.
+// mb (beta) null: no recomputed mask.
+template <int E>
+__device__ __forceinline__ void mask_coef(const float* gamma, const float* invstd, const float* mb,
+                                          int c0, float (&sc)[E], float (&be)[E]) {
+  float ga[E], is[E];
+  chan_load<E>(gamma, c0, ga);
+  chan_load<E>(invstd, c0, is);
+  chan_load<E>(mb, c0, be);
+#pragma unroll
+  for (int i = 0; i < E; ++i) sc[i] = ga[i] * is[i];
+}
+template <typename T, int E>
+__device__ __forceinline__ void apply_mask(const float (&sc)[E], const float (&be)[E],
+                                           const float (&mu)[E], const float (&zz)[E],
+                                           float (&g)[E]) {
+#pragma unroll
+  for (int i = 0; i < E; ++i) {
+    const float t = __builtin_fmaf(zz[i] - mu[i], sc[i], be[i]);
+    g[i] = to_f((T)t) > 0.f ? g[i] : 0.f;
+  }
+}
+template <typename T, int E>
+__device__ __forceinline__ void mask_from_z(const float* gamma, const float* invstd,
+                                            const float* mb, int c0, const float (&mu)[E],
+                                            const float (&zz)[E], float (&g)[E]) {
+  float sc[E], be[E];
+  mask_coef<E>(gamma, invstd, mb, c0, sc, be);
+  apply_mask<T, E>(sc, be, mu, zz, g);
+}
+
 // --------------------------------------------------------- BN statistics
 // Per chunk of rows: shifted sums S1 = sum(z - K), S2 = sum((z - K)^2) with the
 // shift K[c] = z[0][c]; all chunks share K, so the final sums are plain adds.
@@ -208,7 +241,7 @@ __global__ void bn_apply_kernel(const T* z, long long units, int C, const float*
 #pragma unroll
     for (int i = 0; i < E; ++i) {
       // (z - mean) * scale + beta: no cancellation when invstd is large
-      float t = (v[i] - mu[i]) * sc[i] + be[i];
+      float t = __builtin_fmaf(v[i] - mu[i], sc[i], be[i]);
       if (res) t += r[i];
       if (relu) t = relu_nan(t);
       v[i] = t;
@@ -238,8 +271,9 @@ inline bool bn_fold_ok(long long M, int C) {
 // S1 = sum g, S2 = sum g (z - mean).  Row slices are added in slice order.
 template <typename T, bool BWD>
 __global__ __launch_bounds__(256) void bn_group_partial(const T* z, const T* dy, const T* y,
-                                                        const float* mean, long long M, int C,
-                                                        float* part) {
+                                                        const float* mean, const float* gamma,
+                                                        const float* invstd, const float* mb,
+                                                        long long M, int C, float* part) {
   constexpr int E = Elt<T>::E, UG = BN_GROUP / E, RI = 256 / UG, RPT = BN_FOLD_ROWS / RI;
   const int t = threadIdx.x, u = t % UG, rs = t / UG;
   const int c0 = blockIdx.y * BN_GROUP + u * E;
@@ -250,8 +284,9 @@ __global__ __launch_bounds__(256) void bn_group_partial(const T* z, const T* dy,
 #pragma unroll
   for (int i = 0; i < E; ++i) s1[i] = s2[i] = 0.f;
   if constexpr (BWD) {
-    float mu[E];
+    float mu[E], msc[E], mbe[E];
     chan_load<E>(mean, c0, mu);
+    if (mb) mask_coef<E>(gamma, invstd, mb, c0, msc, mbe);
 #pragma unroll
     for (int q = 0; q < RPT; ++q) {
       const long long r = r0 + rs + (long long)RI * q;
@@ -265,6 +300,8 @@ __global__ __launch_bounds__(256) void bn_group_partial(const T* z, const T* dy,
         unit_to_f<T>(*reinterpret_cast<const uint4*>(y + off), yy);
 #pragma unroll
         for (int i = 0; i < E; ++i) g[i] = yy[i] > 0.f ? g[i] : 0.f;
+      } else if (mb) {
+        apply_mask<T, E>(msc, mbe, mu, v, g);
       }
 #pragma unroll
       for (int i = 0; i < E; ++i) {
@@ -468,7 +505,7 @@ __global__ __launch_bounds__(256) void bn_fold_apply(const T* z, const float* pa
     if (res) unit_to_f<T>(*reinterpret_cast<const uint4*>(res + off), q);
 #pragma unroll
     for (int i = 0; i < E; ++i) {
-      float o = (v[i] - mu[i]) * sc[i] + be[i];
+      float o = __builtin_fmaf(v[i] - mu[i], sc[i], be[i]);
       if (res) o += q[i];
       if (relu) o = relu_nan(o);
       v[i] = o;
@@ -485,8 +522,9 @@ __global__ __launch_bounds__(256) void bn_bwd_fold_apply(const T* dy, const T* y
                                                          const float* part, int nch, long long M,
                                                          int C, long long rpb,
                                                          const float* gamma, const float* mean,
-                                                         const float* invstd, float* dgamma,
-                                                         float* dbeta, T* dz, T* g_out) {
+                                                         const float* invstd, const float* mb,
+                                                         float* dgamma, float* dbeta, T* dz,
+                                                         T* g_out) {
   constexpr int E = Elt<T>::E, UG = BN_GROUP / E, RI = 256 / UG;
   __shared__ float cf[4][BN_GROUP];
   const int t = threadIdx.x;
@@ -518,6 +556,8 @@ __global__ __launch_bounds__(256) void bn_bwd_fold_apply(const T* dy, const T* y
   }
   const long long r0 = blockIdx.x * rpb, r1 = std::min<long long>(M, r0 + rpb);
   const int c0 = blockIdx.y * BN_GROUP + u * E;
+  float msc[E], mbe[E];
+  if (mb) mask_coef<E>(gamma, invstd, mb, c0, msc, mbe);
   for (long long r = r0 + rs; r < r1; r += RI) {
     const long long off = r * C + c0;
     float g[E], zz[E], o[E];
@@ -528,6 +568,8 @@ __global__ __launch_bounds__(256) void bn_bwd_fold_apply(const T* dy, const T* y
       unit_to_f<T>(*reinterpret_cast<const uint4*>(y + off), yy);
 #pragma unroll
       for (int i = 0; i < E; ++i) g[i] = yy[i] > 0.f ? g[i] : 0.f;
+    } else if (mb) {
+      apply_mask<T, E>(msc, mbe, mu, zz, g);
     }
     if (g_out) *reinterpret_cast<uint4*>(g_out + off) = f_to_unit<T>(g);
 #pragma unroll
@@ -697,7 +739,9 @@ template <typename T>
 __global__ __launch_bounds__(256) void bn_bwd_partial(const T* dy, const T* y, const T* z,
                                                       long long M, int C,
                                                       long long rows_per_chunk,
-                                                      const float* mean, float* part) {
+                                                      const float* mean, const float* gamma,
+                                                      const float* invstd, const float* mb,
+                                                      float* part) {
   constexpr int E = Elt<T>::E;
   const int tpr = C / E;
   const int rpi = 256 / tpr;
@@ -705,12 +749,14 @@ __global__ __launch_bounds__(256) void bn_bwd_partial(const T* dy, const T* y, c
   const int cu = t % tpr, rsub = t / tpr;
   const long long r0 = blockIdx.x * rows_per_chunk;
   const long long r1 = std::min<long long>(M, r0 + rows_per_chunk);
-  float s1[E], s2[E], mu[E];
+  float s1[E], s2[E], mu[E], msc[E], mbe[E];
 #pragma unroll
   for (int i = 0; i < E; ++i) {
     s1[i] = s2[i] = 0.f;
     mu[i] = mean[cu * E + i];
+    msc[i] = mbe[i] = 0.f;
   }
+  if (mb) mask_coef<E>(gamma, invstd, mb, cu * E, msc, mbe);
   if (rsub < rpi) {
     // four rows' loads issued before they are accumulated (in row order)
     constexpr int U = 4;
@@ -736,6 +782,8 @@ __global__ __launch_bounds__(256) void bn_bwd_partial(const T* dy, const T* y, c
           unit_to_f<T>(ry[q], yy);
 #pragma unroll
           for (int i = 0; i < E; ++i) g[i] = yy[i] > 0.f ? g[i] : 0.f;
+        } else if (mb) {
+          apply_mask<T, E>(msc, mbe, mu, zz, g);
         }
 #pragma unroll
         for (int i = 0; i < E; ++i) {
@@ -784,7 +832,8 @@ __global__ __launch_bounds__(256) void bn_bwd_final(const float* part, int nchun
 
 template <typename T>
 __global__ void bn_bwd_apply(const T* dy, const T* y, const T* z, long long units, int C,
-                             const float* mean, const float* coef, T* dz, T* g_out) {
+                             const float* mean, const float* coef, const float* gamma,
+                             const float* invstd, const float* mb, T* dz, T* g_out) {
   constexpr int E = Elt<T>::E;
   for (long long u = blockIdx.x * (long long)blockDim.x + threadIdx.x; u < units;
        u += (long long)gridDim.x * blockDim.x) {
@@ -792,18 +841,20 @@ __global__ void bn_bwd_apply(const T* dy, const T* y, const T* z, long long unit
     float g[E], zz[E];
     unit_to_f<T>(reinterpret_cast<const uint4*>(dy)[u], g);
     unit_to_f<T>(reinterpret_cast<const uint4*>(z)[u], zz);
+    float o[E], ca[E], cb[E], cc[E], mu[E];
+    chan_load<E>(mean, c0, mu);
     if (y) {
       float yy[E];
       unit_to_f<T>(reinterpret_cast<const uint4*>(y)[u], yy);
 #pragma unroll
       for (int i = 0; i < E; ++i) g[i] = yy[i] > 0.f ? g[i] : 0.f;
+    } else if (mb) {
+      mask_from_z<T, E>(gamma, invstd, mb, c0, mu, zz, g);
     }
     if (g_out) reinterpret_cast<uint4*>(g_out)[u] = f_to_unit<T>(g);
-    float o[E], ca[E], cb[E], cc[E], mu[E];
     chan_load<E>(coef, c0, ca);
     chan_load<E>(coef + C, c0, cb);
     chan_load<E>(coef + 2 * C, c0, cc);
-    chan_load<E>(mean, c0, mu);
 #pragma unroll
     for (int i = 0; i < E; ++i) o[i] = ca[i] * g[i] + cb[i] + cc[i] * (zz[i] - mu[i]);
     reinterpret_cast<uint4*>(dz)[u] = f_to_unit<T>(o);
@@ -837,10 +888,16 @@ template <int E> __device__ __forceinline__ void arg_store(uint8_t* p, const int
 // 3x3 / stride 2 / pad 1 max pool.  One block covers 256 units (pixel x
 // 16-byte channel unit) of one output row; bpr blocks per row (the row index
 // from the block index is uniform, so no per-lane wide division).
-template <typename T>
+// BNR: x is a BatchNorm input z and the pooled values are the BatchNorm +
+// ReLU outputs relu((z - mean) * scale + beta), rounded to T exactly as the
+// standalone apply kernel stores them (so the window maxima and their
+// indices are those of the stored activation).
+template <typename T, bool BNR = false>
 __global__ __launch_bounds__(256) void maxpool_fwd_kernel(const T* x, int N, int H, int W, int C,
                                                           int P, int Q, int bpr, T* y,
-                                                          uint8_t* arg) {
+                                                          uint8_t* arg, const float* mean,
+                                                          const float* scale,
+                                                          const float* beta) {
   constexpr int E = Elt<T>::E;
   const int cu = C / E;
   const int row = blockIdx.x / bpr;  // n * P + p
@@ -848,6 +905,12 @@ __global__ __launch_bounds__(256) void maxpool_fwd_kernel(const T* x, int N, int
   if (row >= N * P || t >= Q * cu) return;
   const int q = t / cu, c0 = (t - q * cu) * E;
   const int n = row / P, p = row - n * P;
+  float mu[E], sc[E], be[E];
+  if constexpr (BNR) {
+    chan_load<E>(mean, c0, mu);
+    chan_load<E>(scale, c0, sc);
+    chan_load<E>(beta, c0, be);
+  }
   float best[E];
   int ba[E];
 #pragma unroll
@@ -873,6 +936,10 @@ __global__ __launch_bounds__(256) void maxpool_fwd_kernel(const T* x, int N, int
     if (!ok[k]) continue;
     float v[E];
     unit_to_f<T>(raw[k], v);
+    if constexpr (BNR) {
+#pragma unroll
+      for (int i = 0; i < E; ++i) v[i] = to_f((T)relu_nan(__builtin_fmaf(v[i] - mu[i], sc[i], be[i])));
+    }
 #pragma unroll
     for (int i = 0; i < E; ++i)
       if (v[i] > best[i]) {
@@ -1769,7 +1836,8 @@ hipError_t bn_train_forward(int dt, const void* z, long long M, int C, const flo
       using T = std::remove_pointer_t<decltype(tp)>;
       hipLaunchKernelGGL((bn_group_partial<T, false>), dim3(nch, groups), dim3(256), 0, stream,
                          (const T*)z, (const T*)nullptr, (const T*)nullptr, (const float*)nullptr,
-                         M, C, partials);
+                         (const float*)nullptr, (const float*)nullptr, (const float*)nullptr, M, C,
+                         partials);
     }), "bn_fwd_stats", act);
     if (e != hipSuccess) return e;
   }
@@ -1804,8 +1872,9 @@ hipError_t bn_fold(const float* params, const long long* tab, int n, float* out,
 hipError_t bn_backward(int dt, const void* dy, const void* y, const void* z, long long M, int C,
                        const float* gamma, const float* mean, const float* invstd, float* dgamma,
                        float* dbeta, void* dz, void* g_out, float* partials, hipStream_t stream,
-                       int ready_rows) {
+                       int ready_rows, const float* relu_beta) {
   if (M == 0) return hipSuccess;
+  if (y && relu_beta) return hipErrorInvalidValue;
   if (ready_rows != 0 && ((ready_rows != 64 && ready_rows != BN_FOLD_ROWS) || !bn_fold_ok(M, C)))
     return hipErrorInvalidValue;
   const double act = (double)M * C * dtype_size(dt);
@@ -1819,7 +1888,8 @@ hipError_t bn_backward(int dt, const void* dy, const void* y, const void* z, lon
       hipError_t e = tp_.done(by_type(dt, [&](auto* tp) {
         using T = std::remove_pointer_t<decltype(tp)>;
         hipLaunchKernelGGL((bn_group_partial<T, true>), dim3(nf, groups), dim3(256), 0, stream,
-                           (const T*)z, (const T*)dy, (const T*)y, mean, M, C, partials);
+                           (const T*)z, (const T*)dy, (const T*)y, mean, gamma, invstd, relu_beta,
+                           M, C, partials);
       }), "bn_bwd_stats", act * (y ? 3 : 2));
       if (e != hipSuccess) return e;
     }
@@ -1828,7 +1898,7 @@ hipError_t bn_backward(int dt, const void* dy, const void* y, const void* z, lon
       using T = std::remove_pointer_t<decltype(tp)>;
       hipLaunchKernelGGL(bn_bwd_fold_apply<T>, dim3((unsigned)cdivl(M, rpb), groups), dim3(256), 0,
                          stream, (const T*)dy, (const T*)y, (const T*)z, partials, nf, M, C, rpb,
-                         gamma, mean, invstd, dgamma, dbeta, (T*)dz, (T*)g_out);
+                         gamma, mean, invstd, relu_beta, dgamma, dbeta, (T*)dz, (T*)g_out);
     }), "bn_bwd_apply", apply_bytes);
   }
   const int nch = bn_chunks(M, C);
@@ -1839,7 +1909,8 @@ hipError_t bn_backward(int dt, const void* dy, const void* y, const void* z, lon
   hipError_t e = ts.done(by_type(dt, [&](auto* tp) {
     using T = std::remove_pointer_t<decltype(tp)>;
     hipLaunchKernelGGL(bn_bwd_partial<T>, dim3(nch), dim3(256), 0, stream, (const T*)dy,
-                       (const T*)y, (const T*)z, M, C, rpc, mean, partials);
+                       (const T*)y, (const T*)z, M, C, rpc, mean, gamma, invstd, relu_beta,
+                       partials);
     hipLaunchKernelGGL(bn_bwd_final, dim3(cdiv(C, FIN_CH)), dim3(256), 0, stream, partials, nch, M, C,
                        gamma, invstd, dgamma, dbeta, coef);
   }), "bn_bwd_stats", act * (y ? 3 : 2));
@@ -1848,7 +1919,8 @@ hipError_t bn_backward(int dt, const void* dy, const void* y, const void* z, lon
   return ta.done(by_type(dt, [&](auto* tp) {
     using T = std::remove_pointer_t<decltype(tp)>;
     hipLaunchKernelGGL(bn_bwd_apply<T>, dim3(grid_for(units)), dim3(256), 0, stream, (const T*)dy,
-                       (const T*)y, (const T*)z, units, C, mean, coef, (T*)dz, (T*)g_out);
+                       (const T*)y, (const T*)z, units, C, mean, coef, gamma, invstd, relu_beta,
+                       (T*)dz, (T*)g_out);
   }), "bn_bwd_apply", apply_bytes);
 }
 
@@ -1863,8 +1935,32 @@ hipError_t maxpool_fwd(int dt, const void* x, int N, int H, int W, int C, void* 
     using T = std::remove_pointer_t<decltype(tp)>;
     const int bpr = cdiv(Q * (C / Elt<T>::E), 256);
     hipLaunchKernelGGL(maxpool_fwd_kernel<T>, dim3((unsigned)((long long)N * P * bpr)), dim3(256), 0,
-                       stream, (const T*)x, N, H, W, C, P, Q, bpr, (T*)y, arg);
+                       stream, (const T*)x, N, H, W, C, P, Q, bpr, (T*)y, arg,
+                       (const float*)nullptr, (const float*)nullptr, (const float*)nullptr);
   }), "maxpool_fwd", (double)N * C * ((double)H * W * es + (double)P * Q * (es + (arg ? 1 : 0))));
+}
+
+hipError_t bn_relu_maxpool_train(int dt, const void* z, int N, int H, int W, int C,
+                                 const float* gamma, const float* beta, float* rm, float* rv,
+                                 float* mean, float* invstd, float* scale, float* shift,
+                                 float* partials, void* y, uint8_t* arg, hipStream_t stream) {
+  const long long M = (long long)N * H * W;
+  if (M == 0) return hipSuccess;
+  const int P = (H - 1) / 2 + 1, Q = (W - 1) / 2 + 1;
+  const size_t es = dtype_size(dt);
+  TimedLaunch ts(stream);
+  hipError_t e = ts.done(bn_train_stats(dt, z, M, C, gamma, beta, rm, rv, mean, invstd, scale,
+                                        shift, partials, stream),
+                         "bn_fwd_stats", (double)M * C * es);
+  if (e != hipSuccess) return e;
+  TimedLaunch tl(stream);  // BatchNorm input once; pooled output and its window index
+  return tl.done(by_type(dt, [&](auto* tp) {
+    using T = std::remove_pointer_t<decltype(tp)>;
+    const int bpr = cdiv(Q * (C / Elt<T>::E), 256);
+    hipLaunchKernelGGL((maxpool_fwd_kernel<T, true>), dim3((unsigned)((long long)N * P * bpr)),
+                       dim3(256), 0, stream, (const T*)z, N, H, W, C, P, Q, bpr, (T*)y, arg, mean,
+                       scale, beta);
+  }), "bn_relu_maxpool", (double)N * C * ((double)H * W * es + (double)P * Q * (es + (arg ? 1 : 0))));
 }
 
 hipError_t maxpool_bwd(int dt, const void* dy, const uint8_t* arg, int N, int H, int W, int C,

@@ -174,13 +174,24 @@ hipError_t bn_fold(const float* params, const long long* tab, int n, float* out,
 // g = dy * [y > 0]; dgamma = sum g*xhat; dbeta = sum g;
 // dz = gamma*invstd*(g - dbeta/M - xhat*dgamma/M).  Writes dgamma/dbeta and
 // dz; when g_out != null also writes g.
-// ready_rows: as for bn_train_forward.
+// ready_rows: as for bn_train_forward.  relu_beta (with y null): the output
+// was y = relu(BN(z)) with no residual and this beta; the mask is recomputed
+// from z, mean, gamma * invstd and beta exactly as the forward pass rounded
+// y, so y need not be read.
 hipError_t bn_backward(int dt, const void* dy, const void* y, const void* z, long long M, int C,
                        const float* gamma, const float* mean, const float* invstd, float* dgamma,
                        float* dbeta, void* dz, void* g_out, float* partials, hipStream_t stream,
-                       int ready_rows = 0);
+                       int ready_rows = 0, const float* relu_beta = nullptr);
 
 // ------------------------------------------------------------------ pooling
+// Train-mode BatchNorm statistics of z [N, H, W, C] (as bn_train_stats),
+// then the 3x3 / stride 2 / pad 1 max pool of relu(BN(z)) computed on load:
+// y and arg as maxpool_fwd would give for the stored BatchNorm + ReLU output,
+// which is never written.  `partials`: bn_partials_floats(N * H * W, C).
+hipError_t bn_relu_maxpool_train(int dt, const void* z, int N, int H, int W, int C,
+                                 const float* gamma, const float* beta, float* rm, float* rv,
+                                 float* mean, float* invstd, float* scale, float* shift,
+                                 float* partials, void* y, uint8_t* arg, hipStream_t stream);
 hipError_t maxpool_fwd(int dt, const void* x, int N, int H, int W, int C, void* y, uint8_t* arg,
                        hipStream_t stream);
 hipError_t maxpool_bwd(int dt, const void* dy, const uint8_t* arg, int N, int H, int W, int C,

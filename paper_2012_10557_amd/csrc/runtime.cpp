@@ -714,9 +714,17 @@ static hipError_t train_forward(TrainJob& j, int nb) {
       EKYA_HIP(conv_fwd(dt, cg, cur, shadow_at(net, j.shadow, net.conv[0].sh_krsc), j.stem_Z,
                         ConvEpilogue(), j.ws, j.ws_floats, st, &sk));
       const long long M = (long long)nb * cg.P * cg.Q;
-      EKYA_HIP(bn_train(net.conv[0].bn, j.stem_Z, M, nullptr, 1, j.stem_A, sk.done ? sk.rows : 0));
       void* xm = j.acts[0].X;
-      EKYA_HIP(maxpool_fwd(dt, j.stem_A, nb, j.geo.sh, j.geo.sw, 64, xm, j.stem_arg, st));
+      if (sk.done || bn_fold_path(M, 64)) {  // the two-launch BatchNorm, then the pool
+        EKYA_HIP(bn_train(net.conv[0].bn, j.stem_Z, M, nullptr, 1, j.stem_A, sk.rows));
+        EKYA_HIP(maxpool_fwd(dt, j.stem_A, nb, j.geo.sh, j.geo.sw, 64, xm, j.stem_arg, st));
+      } else {  // BatchNorm + ReLU applied inside the pool: stem_A is never written
+        const BnL& b = net.bn[net.conv[0].bn];
+        EKYA_HIP(bn_relu_maxpool_train(dt, j.stem_Z, nb, j.geo.sh, j.geo.sw, 64, j.master + b.g,
+                                       j.master + b.b, j.master + b.rm, j.master + b.rv,
+                                       bnp(j.bn_mean, b), bnp(j.bn_invstd, b), bnp(j.bn_scale, b),
+                                       bnp(j.bn_shift, b), j.bn_ws, xm, j.stem_arg, st));
+      }
       cur = xm;
       continue;
     }
@@ -819,6 +827,13 @@ static hipError_t train_backward(TrainJob& j, int nb, const int32_t* fid, float*
                        bnp(j.bn_invstd, b), j.grad + b.g, j.grad + b.b, dz, gout, j.bn_ws, st,
                        ready);
   };
+  // a BatchNorm + ReLU with no residual: its mask recomputed from z
+  auto bn_bwd_relu = [&](int bi, const void* dy, const void* z, long long M, void* dz, int ready) {
+    const BnL& b = net.bn[bi];
+    return bn_backward(dt, dy, nullptr, z, M, b.C, j.master + b.g, bnp(j.bn_mean, b),
+                       bnp(j.bn_invstd, b), j.grad + b.g, j.grad + b.b, dz, nullptr, j.bn_ws, st,
+                       ready, j.master + b.b);
+  };
   // statistics sink of the BatchNorm whose dy a data gradient produces
   auto sink_for = [&](int bni, const void* ymask, const void* z) {
     BnStatsSink k;
@@ -920,7 +935,7 @@ static hipError_t train_backward(TrainJob& j, int nb, const int32_t* fid, float*
       EKYA_HIP(reuse(par));
       EKYA_HIP(maxpool_bwd(dt, dout, j.stem_arg, nb, j.geo.sh, j.geo.sw, 64, gA, st));
       const long long M = (long long)nb * j.geo.sh * j.geo.sw;
-      EKYA_HIP(bn_bwd(net.conv[0].bn, gA, j.stem_A, j.stem_Z, M, j.gz1[par], nullptr, 0));
+      EKYA_HIP(bn_bwd_relu(net.conv[0].bn, gA, j.stem_Z, M, j.gz1[par], 0));
       EKYA_HIP(wgrad(0, j.x0, j.gz1[par], true, false));
       break;
     }
