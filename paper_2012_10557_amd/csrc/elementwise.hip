@@ -1005,6 +1005,163 @@ __global__ __launch_bounds__(256) void maxpool_bwd_kernel(const T* dy, const uin
   *reinterpret_cast<uint4*>(dx + ((long long)row * W + w) * C + c0) = f_to_unit<T>(acc);
 }
 
+// ------------------------------- max pool backward inside the BatchNorm backward
+// For a BatchNorm + ReLU whose output went only into the 3x3 / stride 2 /
+// pad 1 max pool (the stem, 64 channels): the gradient at output pixel
+// (n, h, w) is gathered from the pooled gradient and window indices exactly as
+// maxpool_bwd_kernel computes it (windows in (r, s) order) and rounded to T as
+// that kernel stores it; the ReLU mask is recomputed from z.  So the partial
+// sums and the input gradient equal those of maxpool_bwd followed by
+// bn_backward, without the full-size gradient being written or read.
+// Input rows 2p and 2p + 1 take their gradient from pooled rows p and p + 1
+// only: a block stages those two pooled rows (gradient and indices) in LDS,
+// then gathers from there while it streams the two rows of z.
+struct PoolSrc {
+  const void* dy;      // pooled gradient [N][P][Q][C]
+  const uint8_t* arg;  // window indices, same layout
+  int H, W, P, Q;
+};
+constexpr int POOLBN_C = 64;
+constexpr int POOLBN_QMAX = 128;
+
+template <typename T>
+struct PoolRows {
+  static constexpr int E = Elt<T>::E, CU = POOLBN_C / E;
+  // pooled rows p, p + 1 (zero beyond the image): units [2][Q][CU], indices [2][Q][C]
+  uint4 g[2 * POOLBN_QMAX * CU];
+  uint8_t a[2 * POOLBN_QMAX * POOLBN_C];
+};
+
+// Stage pooled rows p, p + 1 of image n; all threads take part.
+template <typename T>
+__device__ __forceinline__ void pool_rows_stage(const PoolSrc& ps, int n, int p, PoolRows<T>& sm) {
+  constexpr int E = Elt<T>::E, CU = POOLBN_C / E;
+  const int nu = 2 * ps.Q * CU;                    // 16-byte units of the gradient
+  const int na = 2 * ps.Q * POOLBN_C / 16;         // 16-byte units of the indices
+  for (int i = threadIdx.x; i < nu; i += blockDim.x) {
+    const int rr = i / (ps.Q * CU), rem = i - rr * (ps.Q * CU);
+    const int pp = p + rr;
+    sm.g[i] = pp < ps.P ? reinterpret_cast<const uint4*>(ps.dy)[((long long)n * ps.P + pp) * ps.Q * CU + rem]
+                        : uint4{0, 0, 0, 0};
+  }
+  for (int i = threadIdx.x; i < na; i += blockDim.x) {
+    const int per = ps.Q * POOLBN_C / 16;
+    const int rr = i / per, rem = i - rr * per;
+    const int pp = p + rr;
+    reinterpret_cast<uint4*>(sm.a)[i] =
+        pp < ps.P ? reinterpret_cast<const uint4*>(ps.arg)[((long long)n * ps.P + pp) * per + rem]
+                  : uint4{0, 0, 0, 0};
+  }
+}
+
+// Gradient of unit cu of input pixel (h = 2p + hh, w), from the staged rows.
+template <typename T>
+__device__ __forceinline__ void pool_rows_grad(const PoolSrc& ps, const PoolRows<T>& sm, int nrows,
+                                               int hh, int w, int cu, float (&g)[Elt<T>::E]) {
+  constexpr int E = Elt<T>::E, CU = POOLBN_C / E;
+  float acc[E];
+#pragma unroll
+  for (int i = 0; i < E; ++i) acc[i] = 0.f;
+  // h = 2p: window row r = 1 (pooled row p); h = 2p + 1: r = 0 (row p + 1), r = 2 (row p)
+  const int r0 = hh ? 0 : 1, nr = hh ? 2 : 1;
+  const int s0 = (w & 1) ? 0 : 1, nsw = (w & 1) ? 2 : 1;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    if ((k >> 1) >= nr || (k & 1) >= nsw) continue;
+    const int r = r0 + 2 * (k >> 1), s = s0 + 2 * (k & 1);
+    const int rr = hh + 1 - r >= 0 ? (hh + 1 - r) >> 1 : -1;  // staged row: 0 (p) or 1 (p + 1)
+    const int wp = w + 1 - s;
+    if (rr < 0 || rr >= nrows || wp < 0 || (wp >> 1) >= ps.Q) continue;
+    const int q = wp >> 1;
+    float v[E];
+    unit_to_f<T>(sm.g[(rr * ps.Q + q) * CU + cu], v);
+    const uint8_t* ap = sm.a + (rr * ps.Q + q) * POOLBN_C + cu * E;
+#pragma unroll
+    for (int i = 0; i < E; ++i)
+      if (ap[i] == r * 3 + s) acc[i] += v[i];
+  }
+#pragma unroll
+  for (int i = 0; i < E; ++i) g[i] = to_f((T)acc[i]);
+}
+
+// STATS: partial sums S_g, S_gx of block b's rp row pairs into part[b];
+// otherwise dz of one row pair per block.
+template <typename T, bool STATS>
+__global__ __launch_bounds__(256) void bn_bwd_pool_kernel(PoolSrc ps, const T* z, int N, int rp,
+                                                          const float* mean, const float* coef,
+                                                          const float* gamma, const float* invstd,
+                                                          const float* mb, float* part, T* dz) {
+  constexpr int E = Elt<T>::E, CU = POOLBN_C / E;
+  static_assert(256 % CU == 0, "a thread keeps its channel unit");
+  __shared__ PoolRows<T> sm;
+  const int t = threadIdx.x, cu = t % CU, c0 = cu * E;
+  float mu[E], msc[E], mbe[E], ca[E], cb[E], cc[E], s1[E], s2[E];
+  chan_load<E>(mean, c0, mu);
+  mask_coef<E>(gamma, invstd, mb, c0, msc, mbe);
+  if constexpr (!STATS) {
+    chan_load<E>(coef, c0, ca);
+    chan_load<E>(coef + POOLBN_C, c0, cb);
+    chan_load<E>(coef + 2 * POOLBN_C, c0, cc);
+  }
+#pragma unroll
+  for (int i = 0; i < E; ++i) s1[i] = s2[i] = 0.f;
+  const int pairs = N * ps.P;
+  const int k0 = blockIdx.x * rp, k1 = min(pairs, k0 + rp);
+  const int nunits = 2 * ps.W * CU;
+  for (int k = k0; k < k1; ++k) {
+    const int n = k / ps.P, p = k - n * ps.P;
+    __syncthreads();  // the previous pair's staged rows are no longer read
+    pool_rows_stage<T>(ps, n, p, sm);
+    __syncthreads();
+    for (int u = t; u < nunits; u += 256) {
+      const int hh = u / (ps.W * CU), rem = u - hh * (ps.W * CU);
+      const int w = rem / CU;
+      const int h = 2 * p + hh;
+      if (h >= ps.H) break;
+      const long long off = (((long long)n * ps.H + h) * ps.W + w) * POOLBN_C + c0;
+      float g[E], zz[E];
+      unit_to_f<T>(*reinterpret_cast<const uint4*>(z + off), zz);
+      pool_rows_grad<T>(ps, sm, p + 1 < ps.P ? 2 : 1, hh, w, cu, g);
+      apply_mask<T, E>(msc, mbe, mu, zz, g);
+      if constexpr (STATS) {
+#pragma unroll
+        for (int i = 0; i < E; ++i) {
+          s1[i] += g[i];
+          s2[i] += g[i] * (zz[i] - mu[i]);
+        }
+      } else {
+        float o[E];
+#pragma unroll
+        for (int i = 0; i < E; ++i) o[i] = ca[i] * g[i] + cb[i] + cc[i] * (zz[i] - mu[i]);
+        *reinterpret_cast<uint4*>(dz + off) = f_to_unit<T>(o);
+      }
+    }
+  }
+  if constexpr (STATS) {
+    // threads t, t + CU, ... share channel unit cu: added in thread order
+    __syncthreads();
+    float* sh = reinterpret_cast<float*>(&sm);  // 2 x 256 x E floats (<= the staging area)
+#pragma unroll
+    for (int i = 0; i < E; ++i) {
+      sh[t * E + i] = s1[i];
+      sh[256 * E + t * E + i] = s2[i];
+    }
+    __syncthreads();
+    if (t < POOLBN_C) {
+      const int u = t / E, i = t % E;
+      float a = 0.f, bsum = 0.f;
+      for (int j = u; j < 256; j += CU) {
+        a += sh[j * E + i];
+        bsum += sh[256 * E + j * E + i];
+      }
+      part[(long long)blockIdx.x * 2 * POOLBN_C + t] = a;
+      part[(long long)blockIdx.x * 2 * POOLBN_C + POOLBN_C + t] = bsum;
+    }
+  }
+}
+static_assert(sizeof(PoolRows<float>) >= 2 * 256 * 4 * sizeof(float), "reduction fits the staging area");
+static_assert(sizeof(PoolRows<bf16>) >= 2 * 256 * 8 * sizeof(float), "reduction fits the staging area");
+
 template <typename T>
 __global__ void avgpool_fwd_kernel(const T* x, int N, int HW, int C, float* f) {
   const long long n_out = (long long)N * C;
@@ -1922,6 +2079,43 @@ hipError_t bn_backward(int dt, const void* dy, const void* y, const void* z, lon
                        (const T*)y, (const T*)z, units, C, mean, coef, gamma, invstd, relu_beta,
                        (T*)dz, (T*)g_out);
   }), "bn_bwd_apply", apply_bytes);
+}
+
+bool bn_backward_pool_ok(int C, int H, int W) {
+  return C == POOLBN_C && (W + 1) / 2 <= POOLBN_QMAX && H >= 1 && W >= 1;
+}
+
+hipError_t bn_backward_pool(int dt, const void* dy_pool, const uint8_t* arg, const void* z, int N,
+                            int H, int W, int C, const float* gamma, const float* beta,
+                            const float* mean, const float* invstd, float* dgamma, float* dbeta,
+                            void* dz, float* partials, hipStream_t stream) {
+  const long long M = (long long)N * H * W;
+  if (M == 0) return hipSuccess;
+  if (M >= (1LL << 31) || !bn_backward_pool_ok(C, H, W)) return hipErrorInvalidValue;
+  const int P = (H - 1) / 2 + 1, Q = (W - 1) / 2 + 1;
+  const PoolSrc ps{dy_pool, arg, H, W, P, Q};
+  const int pairs = N * P;
+  // at most as many partial rows as bn_partials_floats(M, C) provides
+  const int rp = cdiv(pairs, bn_chunks(M, C)), nch = cdiv(pairs, rp);
+  float* coef = partials + (size_t)nch * 2 * C;
+  const size_t es = dtype_size(dt);
+  const double act = (double)M * C * es, pooled = (double)N * P * Q * C * (es + 1);
+  TimedLaunch ts(stream);  // z; the pooled gradient and its window indices
+  hipError_t e = ts.done(by_type(dt, [&](auto* tp) {
+    using T = std::remove_pointer_t<decltype(tp)>;
+    hipLaunchKernelGGL((bn_bwd_pool_kernel<T, true>), dim3(nch), dim3(256), 0, stream, ps,
+                       (const T*)z, N, rp, mean, (const float*)nullptr, gamma, invstd, beta,
+                       partials, (T*)nullptr);
+    hipLaunchKernelGGL(bn_bwd_final, dim3(cdiv(C, FIN_CH)), dim3(256), 0, stream, partials, nch, M, C,
+                       gamma, invstd, dgamma, dbeta, coef);
+  }), "bn_bwd_stats", act + pooled);
+  if (e != hipSuccess) return e;
+  TimedLaunch ta(stream);  // z and the pooled gradient read, dz written
+  return ta.done(by_type(dt, [&](auto* tp) {
+    using T = std::remove_pointer_t<decltype(tp)>;
+    hipLaunchKernelGGL((bn_bwd_pool_kernel<T, false>), dim3(pairs), dim3(256), 0, stream, ps,
+                       (const T*)z, N, 1, mean, coef, gamma, invstd, beta, (float*)nullptr, (T*)dz);
+  }), "bn_bwd_apply", 2 * act + pooled);
 }
 
 hipError_t maxpool_fwd(int dt, const void* x, int N, int H, int W, int C, void* y, uint8_t* arg,

@@ -183,6 +183,19 @@ hipError_t bn_backward(int dt, const void* dy, const void* y, const void* z, lon
                        float* dbeta, void* dz, void* g_out, float* partials, hipStream_t stream,
                        int ready_rows = 0, const float* relu_beta = nullptr);
 
+// Backward of a train-mode BatchNorm + ReLU (no residual) whose output went
+// only into the 3x3 / stride 2 / pad 1 max pool: dz [N, H, W, C] from the
+// pooled gradient dy_pool and window indices arg ([N, P, Q, C]), equal to
+// maxpool_bwd followed by bn_backward with the mask recomputed from z (beta:
+// the BatchNorm's shift), without the full-size gradient in memory;
+// `partials`: bn_partials_floats(N * H * W, C).
+// bn_backward_pool_ok: the shapes it takes (64 channels, pooled width <= 128).
+bool bn_backward_pool_ok(int C, int H, int W);
+hipError_t bn_backward_pool(int dt, const void* dy_pool, const uint8_t* arg, const void* z, int N,
+                            int H, int W, int C, const float* gamma, const float* beta,
+                            const float* mean, const float* invstd, float* dgamma, float* dbeta,
+                            void* dz, float* partials, hipStream_t stream);
+
 // ------------------------------------------------------------------ pooling
 // Train-mode BatchNorm statistics of z [N, H, W, C] (as bn_train_stats),
 // then the 3x3 / stride 2 / pad 1 max pool of relu(BN(z)) computed on load:

@@ -933,9 +933,17 @@ static hipError_t train_backward(TrainJob& j, int nb, const int32_t* fid, float*
       // stem: max-pool backward, BN + ReLU backward, weight gradient
       const int par = blk_count & 1;
       EKYA_HIP(reuse(par));
-      EKYA_HIP(maxpool_bwd(dt, dout, j.stem_arg, nb, j.geo.sh, j.geo.sw, 64, gA, st));
       const long long M = (long long)nb * j.geo.sh * j.geo.sw;
-      EKYA_HIP(bn_bwd_relu(net.conv[0].bn, gA, j.stem_Z, M, j.gz1[par], 0));
+      if (bn_fold_path(M, 64) || !bn_backward_pool_ok(64, j.geo.sh, j.geo.sw)) {
+        EKYA_HIP(maxpool_bwd(dt, dout, j.stem_arg, nb, j.geo.sh, j.geo.sw, 64, gA, st));
+        EKYA_HIP(bn_bwd_relu(net.conv[0].bn, gA, j.stem_Z, M, j.gz1[par], 0));
+      } else {  // the pool's backward gathered inside the BatchNorm backward
+        const BnL& b = net.bn[net.conv[0].bn];
+        EKYA_HIP(bn_backward_pool(dt, dout, j.stem_arg, j.stem_Z, nb, j.geo.sh, j.geo.sw, 64,
+                                  j.master + b.g, j.master + b.b, bnp(j.bn_mean, b),
+                                  bnp(j.bn_invstd, b), j.grad + b.g, j.grad + b.b, j.gz1[par],
+                                  j.bn_ws, st));
+      }
       EKYA_HIP(wgrad(0, j.x0, j.gz1[par], true, false));
       break;
     }
