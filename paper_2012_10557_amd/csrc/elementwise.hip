@@ -1022,7 +1022,7 @@ struct PoolSrc {
   int H, W, P, Q;
 };
 constexpr int POOLBN_C = 64;
-constexpr int POOLBN_QMAX = 128;
+constexpr int POOLBN_QMAX = 64;  // pooled width (stem output width up to 128)
 
 template <typename T>
 struct PoolRows {
@@ -1074,11 +1074,12 @@ __device__ __forceinline__ void pool_rows_grad(const PoolSrc& ps, const PoolRows
     if (rr < 0 || rr >= nrows || wp < 0 || (wp >> 1) >= ps.Q) continue;
     const int q = wp >> 1;
     float v[E];
+    int a[E];
     unit_to_f<T>(sm.g[(rr * ps.Q + q) * CU + cu], v);
-    const uint8_t* ap = sm.a + (rr * ps.Q + q) * POOLBN_C + cu * E;
+    arg_load<E>(sm.a + (rr * ps.Q + q) * POOLBN_C + cu * E, a);  // one 4- or 8-byte LDS read
 #pragma unroll
     for (int i = 0; i < E; ++i)
-      if (ap[i] == r * 3 + s) acc[i] += v[i];
+      if (a[i] == r * 3 + s) acc[i] += v[i];
   }
 #pragma unroll
   for (int i = 0; i < E; ++i) g[i] = to_f((T)acc[i]);
@@ -2082,7 +2083,7 @@ hipError_t bn_backward(int dt, const void* dy, const void* y, const void* z, lon
 }
 
 bool bn_backward_pool_ok(int C, int H, int W) {
-  return C == POOLBN_C && (W + 1) / 2 <= POOLBN_QMAX && H >= 1 && W >= 1;
+  return C == POOLBN_C && W <= 2 * POOLBN_QMAX && H >= 1 && W >= 1;
 }
 
 hipError_t bn_backward_pool(int dt, const void* dy_pool, const uint8_t* arg, const void* z, int N,

@@ -189,7 +189,7 @@ hipError_t bn_backward(int dt, const void* dy, const void* y, const void* z, lon
 // maxpool_bwd followed by bn_backward with the mask recomputed from z (beta:
 // the BatchNorm's shift), without the full-size gradient in memory;
 // `partials`: bn_partials_floats(N * H * W, C).
-// bn_backward_pool_ok: the shapes it takes (64 channels, pooled width <= 128).
+// bn_backward_pool_ok: the shapes it takes (64 channels, width W <= 128).
 bool bn_backward_pool_ok(int C, int H, int W);
 hipError_t bn_backward_pool(int dt, const void* dy_pool, const uint8_t* arg, const void* z, int N,
                             int H, int W, int C, const float* gamma, const float* beta,
