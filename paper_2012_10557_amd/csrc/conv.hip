@@ -2607,13 +2607,15 @@ DmaPlan plan_dma(int rows, long long cols, int ns, bool allow_split) {
   if (rows % 256 == 0 && ns >= 8) {
     // warp-specialised 256 x 128 tiles, one block per CU: split the
     // reduction until the blocks about fill the chip once (>= 4 stages
-    // each) -- unless that would take a split of >= 2 and 128 x 64 tiles
-    // already give half a chip of blocks without one, which saves the fp32
-    // partials' round trip
+    // each) -- unless there are fewer than a quarter chip of them and
+    // 128 x 64 tiles already give half a chip of blocks without a split,
+    // which saves the fp32 partials' round trip (measured: at 98 tiles, e.g.
+    // 512 channels x 6272 pixels, two splits of 256 x 128 beat 392 unsplit
+    // 128 x 64 tiles by a quarter)
     const long long tiles = (long long)(rows / 256) * cdivl(cols, 128);
     if (tiles >= 256 || !allow_split) return {256, 128, 1, ns, true};
     const long long small = (long long)(rows / 128) * cdivl(cols, 64);
-    if (tiles < 128 && small >= 128) return {128, 64, 1, ns, true};
+    if (tiles < 64 && small >= 128) return {128, 64, 1, ns, true};
     int s = (int)std::min<long long>(256 / tiles, 16);
     s = std::max(1, std::min(s, std::max(1, ns / 4)));
     const int sps = cdiv(ns, s);

@@ -153,46 +153,48 @@ __global__ __launch_bounds__(256) void bn_stats_partial(const T* z, long long M,
   }
 }
 
-// Fixed-order sum over chunks of the two partial rows of channel c: a block
-// handles FIN_CH channels with FIN_SL threads each (thread slice k sums chunks
-// k, k + FIN_SL, ... -- at most FIN_PER of them, all loads issued before the
-// adds, so one round of latency), and the slice sums are added in slice order
-// in double.  Returns true for the one thread per channel that holds the
-// totals.
-constexpr int FIN_CH = 4;
-constexpr int FIN_SL = 64;
+// Fixed-order sum over chunks of the two partial rows of channel c: one
+// block per channel, thread k sums chunks k, k + 256, ... (at most FIN_PER,
+// all loads issued before the adds), then the 256 thread sums are added
+// pairwise in double in a fixed tree (thread k with k + 128, ...).  Returns
+// true for the thread that holds the totals.
+constexpr int FIN_CH = 1;
+constexpr int FIN_SL = 256;
 constexpr int FIN_PER = BN_MAX_CHUNKS / FIN_SL;
 __device__ __forceinline__ bool chunk_sums(const float* part, int nchunks, int C, double& a,
                                            double& b) {
-  __shared__ float sa[FIN_SL][FIN_CH], sb[FIN_SL][FIN_CH];
-  const int lc = threadIdx.x % FIN_CH, slice = threadIdx.x / FIN_CH;
-  const int c = blockIdx.x * FIN_CH + lc;
+  __shared__ double sa[FIN_SL], sb[FIN_SL];
+  const int k = threadIdx.x, c = blockIdx.x;
   float x = 0.f, y = 0.f;
-  if (c < C) {
+  {
     float v1[FIN_PER], v2[FIN_PER];
 #pragma unroll
     for (int u = 0; u < FIN_PER; ++u) {
-      const int k = slice + FIN_SL * u;
-      v1[u] = k < nchunks ? part[(long long)k * 2 * C + c] : 0.f;
-      v2[u] = k < nchunks ? part[(long long)k * 2 * C + C + c] : 0.f;
+      const int ch = k + FIN_SL * u;
+      v1[u] = ch < nchunks ? part[(long long)ch * 2 * C + c] : 0.f;
+      v2[u] = ch < nchunks ? part[(long long)ch * 2 * C + C + c] : 0.f;
     }
 #pragma unroll
     for (int u = 0; u < FIN_PER; ++u)
-      if (slice + FIN_SL * u < nchunks) {
+      if (k + FIN_SL * u < nchunks) {
         x += v1[u];
         y += v2[u];
       }
   }
-  sa[slice][lc] = x;
-  sb[slice][lc] = y;
+  sa[k] = x;
+  sb[k] = y;
   __syncthreads();
-  if (slice != 0 || c >= C) return false;
-  a = 0.0;
-  b = 0.0;
-  for (int k = 0; k < FIN_SL; ++k) {
-    a += (double)sa[k][lc];
-    b += (double)sb[k][lc];
+#pragma unroll
+  for (int h = FIN_SL / 2; h >= 1; h >>= 1) {
+    if (k < h) {
+      sa[k] += sa[k + h];
+      sb[k] += sb[k + h];
+    }
+    __syncthreads();
   }
+  if (k != 0) return false;
+  a = sa[0];
+  b = sb[0];
   return true;
 }
 static_assert(FIN_CH * FIN_SL == 256, "chunk_sums runs in 256-thread blocks");
@@ -205,7 +207,7 @@ __global__ __launch_bounds__(256) void bn_stats_final(const T* z, const float* p
                                                       float* shift) {
   double a, b;
   if (!chunk_sums(part, nchunks, C, a, b)) return;
-  const int c = blockIdx.x * FIN_CH + (threadIdx.x & (FIN_CH - 1));
+  const int c = blockIdx.x;
   const double Kc = (double)to_f(z[c]);
   const double d = a / (double)M;
   double var = b / (double)M - d * d;
@@ -818,7 +820,7 @@ __global__ __launch_bounds__(256) void bn_bwd_final(const float* part, int nchun
                                                     float* dgamma, float* dbeta, float* coef) {
   double sg, sgx;
   if (!chunk_sums(part, nchunks, C, sg, sgx)) return;
-  const int c = blockIdx.x * FIN_CH + (threadIdx.x & (FIN_CH - 1));
+  const int c = blockIdx.x;
   const float is = invstd[c];
   const float db = (float)sg;
   const float dg = (float)(sgx * (double)is);
