@@ -5,8 +5,12 @@ window with 400 held-out frames.  Checks: concurrent and sequential sweeps are
 bitwise equal; the per-epoch GPU time is deterministic in the way the paper's
 profiler relies on (an epoch of a 2-epoch run costs what the 1-epoch run's
 epoch costs; a larger subset costs in proportion to its SGD steps), within
-15%; and one candidate per depth follows the stored oracle run (first-epoch
-loss within 2e-2, held-out accuracy within one percentage point)."""
+15%; and one candidate per depth follows the stored oracle run: first-epoch
+loss within 2e-2, held-out correct count within one percentage point (4 of
+400 frames) plus the frames the oracle itself leaves near a tie -- top-2
+logit margin below 2 x 2e-2 x the frame's logit scale max_j sum_i |W_ji f_i|
+(a relative error of 2e-2 in the pooled features f moves each logit by at
+most 2e-2 times that scale, so such frames may change label)."""
 import json
 import os
 
@@ -104,7 +108,13 @@ def test_one_candidate_per_depth_follows_oracle(sweeps):
               f"vs {ref['heldout_acc']}")
         assert got["n_train"] == ref["n_train"]
         assert abs(got["epoch_loss"][0] - ref["epoch_loss"][0]) <= TOL["bf16"] * abs(ref["epoch_loss"][0])
-        assert abs(got["heldout_acc"][0] - ref["heldout_acc"][0]) <= 0.01 + 1e-6
+        near = int((np.asarray(ref["heldout_margin"])
+                    < 2 * TOL["bf16"] * np.asarray(ref["heldout_scale"])).sum())
+        n_held = len(ref["heldout_margin"])
+        got_correct = round(got["heldout_acc"][0] * n_held)
+        print(f"k={ref['k']}: {got_correct} vs {ref['n_correct'][0]} correct of {n_held}, "
+              f"{near} frames near a tie")
+        assert abs(got_correct - ref["n_correct"][0]) <= round(0.01 * n_held) + near
 
 
 def test_profiles_feed_extrapolation_and_the_scheduler(sweeps):
