@@ -1911,6 +1911,192 @@ __global__ __launch_bounds__(C64_NT) void conv64_kernel(Conv64Args a) {
   }
 }
 
+// ---------------------------- all-taps weight gradient, warp-specialised
+// The same work, layout of one stage and per-wave tiles as wgrad_tap_kernel,
+// with the conv64_kernel arrangement of the copies: a fifth wave issues every
+// direct-to-LDS copy of a 4-slot ring (input rows 0-103 -- the tile's 100
+// pixels and 4 zero rows, 13 copies -- then the 64 output-gradient rows, 8
+// copies) and never stores, so it keeps three stages in flight (63 copies:
+// the vector-memory counter's limit) while waiting for the oldest; the four
+// compute waves only wait on barriers, and their transposed LDS reads run a
+// tap ahead of the MFMAs.  One block per CU.
+constexpr int TAPW_IN = 104;                          // staged input pixel rows
+constexpr int TAPW_IN_COPIES = TAPW_IN / 8;
+constexpr int TAPW_COPIES = TAPW_IN_COPIES + 8;       // 21 per stage
+constexpr int TAPW_STAGE = (TAPW_IN + 64) * 128;
+constexpr int TAPW_NST = 4;
+constexpr int TAPW_NT = 320;
+static_assert((TAPW_NST - 1) * TAPW_COPIES <= 63, "vector-memory counter");
+
+// Copy ins (0 .. 20) of the copy wave: rows 8 ins .. + 7 of the stage, 16-byte
+// segment lane % 8 -- the pixel and unit placement of tap_slot.
+__host__ __device__ inline TapSlot tapw_slot(int W, int C, int Q, int K, int c0, int k0, int lane,
+                                             int ins) {
+  const int sl = lane & 7;
+  TapSlot t;
+  if (ins < TAPW_IN_COPIES) {
+    const int pix = 8 * ins + (lane >> 3);  // < TAPW_IN
+    const int u = 2 * ((sl >> 1) ^ (pix & 3)) + (sl & 1);
+    const int ty = pix / 10, tx = pix - 10 * (pix / 10);
+    t.sy = pix < 100 ? ty - 1 : -(1 << 24);
+    t.sx = tx - 1;
+    t.off = pix < 100 ? (t.sy * W + t.sx) * C + c0 + u * 8 : 0;
+  } else {
+    const int pix = 8 * (ins - TAPW_IN_COPIES) + (lane >> 3);
+    const int u = 2 * ((sl >> 1) ^ (pix & 3)) + (sl & 1);
+    t.sy = pix >> 3;
+    t.sx = pix & 7;
+    t.off = (t.sy * Q + t.sx) * K + k0 + u * 8;
+  }
+  return t;
+}
+
+// One stage's MFMAs of compute wave WAVE from the ring slot at smem: the wave
+// is a template parameter, so each read's pixel offset is an immediate over
+// one of the lane's base offsets -- ao[v][cg]: input pixel
+// base + d with d = v mod 4, channel group cg (the 32-byte unit swizzle by
+// pixel mod 4 included); bo[j]: output-gradient pixel, channel group j.
+template <int WAVE>
+__device__ __forceinline__ void tapw_stage(const char* smem, const int (&ao)[4][4],
+                                           const int (&bo)[4], f32x4 (&acc)[9][4]) {
+  constexpr int S0 = 0;
+#pragma unroll
+  for (int kf = 0; kf < 2; ++kf) {
+    uint4 fb[4];
+#pragma unroll
+    for (int half = 0; half < 2; ++half) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int d = kf * 32 + half * 4;  // output-gradient pixel offset
+        const uint2 v = lds_read_tr16(smem + S0 + TAPW_IN * 128 + d * 128 + bo[j]);
+        if (half == 0) { fb[j].x = v.x; fb[j].y = v.y; } else { fb[j].z = v.x; fb[j].w = v.y; }
+      }
+    }
+#pragma unroll
+    for (int t = 0; t < 9; ++t) {
+      const int T = 9 * WAVE + t, tap = T >> 2, cg = T & 3;
+      const int r = tap / 3, s = tap - 3 * (tap / 3);
+      uint4 fa;
+#pragma unroll
+      for (int half = 0; half < 2; ++half) {
+        const int d = kf * 40 + r * 10 + half * 4 + s;  // input pixel offset from the lane's
+        const uint2 v = lds_read_tr16(smem + S0 + d * 128 + ao[d & 3][cg]);
+        if (half == 0) { fa.x = v.x; fa.y = v.y; } else { fa.z = v.x; fa.w = v.y; }
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) mma_unit(acc[t][j], fa, fb[j], (bf16*)nullptr);
+    }
+  }
+  // scheduling groups (0x100: LDS reads, 0x008: MFMAs): each k-step's
+  // output-gradient fragments and first two input fragments, then a tap's
+  // MFMAs beside the reads of the tap two ahead
+#pragma unroll
+  for (int kf = 0; kf < 2; ++kf) {
+    __builtin_amdgcn_sched_group_barrier(0x100, 12, 0);
+#pragma unroll
+    for (int t = 0; t < 7; ++t) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+  }
+}
+
+// Compute wave WAVE's whole loop (its accumulators live in one arm of the
+// kernel's switch on the wave) and its partial sums; the stage loop is
+// one barrier before each stage.
+template <int WAVE>
+__device__ __forceinline__ void tapw_compute(const char* smem, int ns, int lane, float* out,
+                                             long long RSC, int K, int c0, int k0, int split) {
+  f32x4 acc[9][4];
+#pragma unroll
+  for (int i = 0; i < 9; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  // the lane's read offsets: input pixel base gq * 10 + jr of the staged
+  // 10-wide tile, output-gradient pixel gq * 8 + jr of the patch (whose
+  // pixel mod 4 is jr at every offset the stage adds)
+  const int gq = lane >> 4, jr = (lane & 15) >> 2, qd = lane & 3;
+  const int ib = gq * 10 + jr, ob = gq * 8 + jr;
+  int ao[4][4], bo[4];
+#pragma unroll
+  for (int v = 0; v < 4; ++v)
+#pragma unroll
+    for (int cg = 0; cg < 4; ++cg) ao[v][cg] = ib * 128 + ((cg ^ ((ib + v) & 3)) * 32) + qd * 8;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) bo[j] = ob * 128 + ((j ^ jr) * 32) + qd * 8;
+  for (int st = 0; st < ns; ++st) {
+    stage_barrier();
+    tapw_stage<WAVE>(smem + (st % TAPW_NST) * TAPW_STAGE, ao, bo, acc);
+  }
+  const int lr = lane & 15, lg = lane >> 4;
+#pragma unroll
+  for (int t = 0; t < 9; ++t) {
+    const int T = 9 * WAVE + t, tap = T >> 2, cg = T & 3;
+    const long long row = (long long)tap * (RSC / 9) + c0 + 16 * cg + 4 * lg;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int col = k0 + 16 * j + lr;
+      float* dst = out + ((long long)split * K + col) * RSC + row;
+      *reinterpret_cast<float4*>(dst) =
+          make_float4(acc[t][j][0], acc[t][j][1], acc[t][j][2], acc[t][j][3]);
+    }
+  }
+}
+
+__global__ __launch_bounds__(TAPW_NT) void wgrad_tapw_kernel(WgTapArgs a) {
+  static_assert(TAPW_NST - 2 <= 2, "c64_wait covers at most 2 later stages");
+  __shared__ __align__(16) char smem[TAPW_NST * TAPW_STAGE];
+  const int H = a.g.H, W = a.g.W, C = a.g.C, K = a.g.K, P = a.g.P, Q = a.g.Q, N = a.g.N;
+  const int tiles_c = a.t.tiles_c, px_n = a.t.px_n, per_img = a.t.py_n * a.t.px_n;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int tiles = tiles_c * a.t.tiles_k;
+  const int item = xcd_tile(blockIdx.x, tiles * a.t.splits);
+  const int split = item / tiles, tile = item - split * tiles;
+  const int c0 = (tile % tiles_c) * 64, k0 = (tile / tiles_c) * 64;
+  const int q0 = split * a.t.pps;
+  const int ns = max(0, min(N * per_img, q0 + a.t.pps) - q0);
+
+  if (wave == 4) {
+    const void* const zero = g_zero_unit;
+    auto issue = [&](int st) {
+      const int q = q0 + st;
+      const int n = q / per_img, rem = q - n * per_img;
+      const int pyi = rem / px_n;
+      const int py0 = 8 * pyi, px0 = 8 * (rem - pyi * px_n);
+      const bf16* xb = a.x + ((long long)n * H * W + (long long)py0 * W + px0) * C;
+      const bf16* db = a.dy + ((long long)n * P * Q + (long long)py0 * Q + px0) * K;
+      char* slot = smem + (st % TAPW_NST) * TAPW_STAGE;
+#pragma unroll
+      for (int ins = 0; ins < TAPW_COPIES; ++ins) {
+        const TapSlot sl = tapw_slot(W, C, Q, K, c0, k0, lane, ins);
+        const bool x = ins < TAPW_IN_COPIES;
+        const bool in = x ? (unsigned)(py0 + sl.sy) < (unsigned)H && (unsigned)(px0 + sl.sx) < (unsigned)W
+                          : py0 + sl.sy < P && px0 + sl.sx < Q;
+        const void* src = in ? (const void*)((x ? xb : db) + sl.off) : zero;
+        dma16(src, reinterpret_cast<uint4*>(slot + ins * 1024));
+      }
+    };
+    for (int st = 0; st < min(ns, TAPW_NST - 1); ++st) issue(st);
+    for (int st = 0; st < ns; ++st) {
+      c64_wait<TAPW_COPIES>(min(ns - 1 - st, TAPW_NST - 2));
+      stage_barrier();
+      // every compute wave is past stage st - 1: refill its slot
+      if (st + TAPW_NST - 1 < ns) issue(st + TAPW_NST - 1);
+    }
+    return;
+  }
+
+  const long long RSC = 9LL * C;
+  switch (wave) {
+    case 0: tapw_compute<0>(smem, ns, lane, a.out, RSC, K, c0, k0, split); break;
+    case 1: tapw_compute<1>(smem, ns, lane, a.out, RSC, K, c0, k0, split); break;
+    case 2: tapw_compute<2>(smem, ns, lane, a.out, RSC, K, c0, k0, split); break;
+    default: tapw_compute<3>(smem, ns, lane, a.out, RSC, K, c0, k0, split); break;
+  }
+}
+
 // ---------------------------------------------- weight gradient of the stem
 // dw[k][r][s][c] = sum over output pixels of dy[pix][k] * x(2p + r - 3,
 // 2q + s - 3)[c] for the 7x7 / stride 2 / pad 3 stem on frames stored with
@@ -3098,8 +3284,8 @@ hipError_t conv_wgrad_dma(const ConvGeom& g, const void* x, const void* dy, floa
   const dim3 grid(a.tiles_m * a.tiles_n, p.splits);
   if (p.tap.splits > 0) {
     const WgTapArgs ta{g, p.tap, (const bf16*)x, (const bf16*)dy, out};
-    hipLaunchKernelGGL((wgrad_tap_kernel<2>),
-                       dim3(p.tap.tiles_c * p.tap.tiles_k * p.tap.splits), dim3(NT), 0, stream, ta);
+    hipLaunchKernelGGL(wgrad_tapw_kernel, dim3(p.tap.tiles_c * p.tap.tiles_k * p.tap.splits),
+                       dim3(TAPW_NT), 0, stream, ta);
   } else if (p.bm == 256)
     hipLaunchKernelGGL((wgrad_ws_kernel<256, 128, 3>), dim3(a.tiles_m * a.tiles_n * p.splits),
                        dim3(8 * 64 + WS_LOADERS * 64), 0, stream, a);
