@@ -1494,60 +1494,24 @@ __global__ __launch_bounds__(NT) void wgrad_dma_kernel(WgDmaArgs a) {
 // s ^ (p mod 4); an 8-byte transpose read (ds_read_b64_tr_b16) takes 4
 // pixels x 16 channels per 16-lane group, member m supplying pixel m / 4,
 // channels 4 (m % 4) .. +3, and hands lane i channel i's 4 pixels; two reads
-// make a lane's MFMA operand of 8 pixels (one patch row).  Wave w owns row
-// tiles 9 w .. 9 w + 8 of the 36 (tap t / 4, channels 16 (t % 4) ..) and all 4
-// column tiles; the output-gradient fragments are read once per k-step and
-// used by the nine row tiles.  Every wave issues the same six copies per
-// stage: 16 instructions of input pixels (100 used, 28 zero rows) and 8 of
-// output-gradient pixels.
+// make a lane's MFMA operand of 8 pixels (one patch row).  Compute wave w
+// owns row tiles 9 w .. 9 w + 8 of the 36 (tap t / 4, channels 16 (t % 4) ..)
+// and all 4 column tiles; the output-gradient fragments are read once per
+// k-step and used by the nine row tiles.
 struct TapGeom {
   int tiles_c, tiles_k, splits, pps;  // pps: patches per split
   int py_n, px_n;                     // patches down / across an image
   __host__ __device__ int n_patches(int N) const { return N * py_n * px_n; }
 };
 
-constexpr int TAP_IN_PIX = 128;                       // staged input pixel rows (100 used)
-constexpr int TAP_STAGE = (TAP_IN_PIX + 64) * 128;    // bytes per stage
-constexpr int TAP_INS = (TAP_IN_PIX + 64) / 8;        // 1024-byte copies per stage
-constexpr int TAP_LPS = TAP_INS / 4;                  // copies per wave and stage
-
-// Copy slot j (instruction wave + 4 j) of `lane`: slots 0-3 stage input
-// pixel rows, 4-5 output-gradient rows.  sy, sx: the pixel's offset from the
-// patch origin (input rows start one pixel up and left; unused rows get an
-// offset that no patch brings inside the image); off: its element offset in
-// the operand relative to the patch origin's pixel, channel block included.
-// Shared by the kernel and the host-side bounds check.
+// A staged pixel row of a copy: sy, sx its offset from the patch origin
+// (input rows start one pixel up and left; unused rows get an offset that no
+// patch brings inside the image); off its element offset in the operand
+// relative to the patch origin's pixel, channel block included.  Shared by
+// the kernels and the host-side bounds checks.
 struct TapSlot {
   int sy, sx, off;
 };
-__host__ __device__ inline TapSlot tap_slot(int W, int C, int Q, int K, int c0, int k0, int wave,
-                                            int lane, int j) {
-  const int ins = wave + 4 * j, sl = lane & 7;
-  TapSlot t;
-  if (j < 4) {
-    const int pix = 8 * ins + (lane >> 3);  // < TAP_IN_PIX
-    const int u = 2 * ((sl >> 1) ^ (pix & 3)) + (sl & 1);
-    const int ty = pix / 10, tx = pix - 10 * (pix / 10);
-    t.sy = pix < 100 ? ty - 1 : -(1 << 24);
-    t.sx = tx - 1;
-    t.off = pix < 100 ? (t.sy * W + t.sx) * C + c0 + u * 8 : 0;
-  } else {
-    const int pix = 8 * (ins - TAP_IN_PIX / 8) + (lane >> 3);
-    const int u = 2 * ((sl >> 1) ^ (pix & 3)) + (sl & 1);
-    t.sy = pix >> 3;
-    t.sx = pix & 7;
-    t.off = (t.sy * Q + t.sx) * K + k0 + u * 8;
-  }
-  return t;
-}
-// Whether slot j's pixel of the patch at (py0, px0) lies inside its operand.
-__host__ __device__ inline bool tap_slot_in(const TapSlot& t, int j, int py0, int px0, int H,
-                                            int W, int P, int Q) {
-  if (j < 4)
-    return (unsigned)(py0 + t.sy) < (unsigned)H && (unsigned)(px0 + t.sx) < (unsigned)W;
-  return py0 + t.sy < P && px0 + t.sx < Q;
-}
-
 struct WgTapArgs {
   ConvGeom g;
   TapGeom t;
@@ -1555,104 +1519,6 @@ struct WgTapArgs {
   const bf16* dy;
   float* out;  // [split][K][9 C]
 };
-
-template <int NST>
-__global__ __launch_bounds__(NT, 2) void wgrad_tap_kernel(WgTapArgs a) {
-  __shared__ __align__(16) char smem[NST * TAP_STAGE];
-  const int H = a.g.H, W = a.g.W, C = a.g.C, K = a.g.K, P = a.g.P, Q = a.g.Q, N = a.g.N;
-  const int tiles_c = a.t.tiles_c, px_n = a.t.px_n, per_img = a.t.py_n * a.t.px_n;
-  const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int tiles = tiles_c * a.t.tiles_k;
-  const int item = xcd_tile(blockIdx.x, tiles * a.t.splits);
-  const int split = item / tiles, tile = item - split * tiles;
-  const int c0 = (tile % tiles_c) * 64, k0 = (tile / tiles_c) * 64;
-  const int q0 = split * a.t.pps;
-  const int ns = max(0, min(N * per_img, q0 + a.t.pps) - q0);
-  const bf16* const xg = a.x;
-  const bf16* const dyg = a.dy;
-  const void* const zero = g_zero_unit;
-  TapSlot sl[TAP_LPS];
-#pragma unroll
-  for (int j = 0; j < TAP_LPS; ++j) sl[j] = tap_slot(W, C, Q, K, c0, k0, wave, lane, j);
-
-  auto issue = [&](int st, char* slot) {
-    const int q = q0 + st;
-    const int n = q / per_img, rem = q - n * per_img;
-    const int pyi = rem / px_n;
-    const int py0 = 8 * pyi, px0 = 8 * (rem - pyi * px_n);
-    const bf16* xb = xg + ((long long)n * H * W + (long long)py0 * W + px0) * C;
-    const bf16* db = dyg + ((long long)n * P * Q + (long long)py0 * Q + px0) * K;
-#pragma unroll
-    for (int j = 0; j < TAP_LPS; ++j) {
-      const bool in = tap_slot_in(sl[j], j, py0, px0, H, W, P, Q);
-      const void* src = in ? (const void*)((j < 4 ? xb : db) + sl[j].off) : zero;
-      dma16(src, reinterpret_cast<uint4*>(slot + (wave + 4 * j) * 1024));
-    }
-  };
-
-  f32x4 acc[9][4];
-#pragma unroll
-  for (int i = 0; i < 9; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-#pragma unroll
-  for (int st = 0; st < NST - 1; ++st)
-    if (st < ns) issue(st, smem + st * TAP_STAGE);
-  const int gq = lane >> 4, jr = (lane & 15) >> 2, qd = lane & 3;
-  for (int st = 0; st < ns; ++st) {
-    // stage st's copies are the oldest; later stages' may stay in flight
-    if (st + NST - 2 < ns) wait_vmcnt<(NST - 2) * TAP_LPS>(); else wait_vmcnt<0>();
-    stage_barrier();
-    if (st + NST - 1 < ns) issue(st + NST - 1, smem + ((st + NST - 1) % NST) * TAP_STAGE);
-    const char* As = smem + (st % NST) * TAP_STAGE;
-    const char* Bs = As + TAP_IN_PIX * 128;
-#pragma unroll
-    for (int kf = 0; kf < 2; ++kf) {
-      const int py = kf * 4 + gq;  // this lane's patch row
-      uint4 fb[4];
-#pragma unroll
-      for (int half = 0; half < 2; ++half) {
-        const int p = py * 8 + half * 4 + jr;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const uint2 v = lds_read_tr16(Bs + p * 128 + ((j ^ (p & 3)) * 32) + qd * 8);
-          if (half == 0) { fb[j].x = v.x; fb[j].y = v.y; } else { fb[j].z = v.x; fb[j].w = v.y; }
-        }
-      }
-#pragma unroll
-      for (int t = 0; t < 9; ++t) {
-        const int T = 9 * wave + t, tap = T >> 2, cg = T & 3;
-        const int r = tap / 3, s = tap - 3 * (tap / 3);
-        uint4 fa;
-#pragma unroll
-        for (int half = 0; half < 2; ++half) {
-          const int ip = (py + r) * 10 + half * 4 + jr + s;
-          const uint2 v = lds_read_tr16(As + ip * 128 + ((cg ^ (ip & 3)) * 32) + qd * 8);
-          if (half == 0) { fa.x = v.x; fa.y = v.y; } else { fa.z = v.x; fa.w = v.y; }
-        }
-#pragma unroll
-        for (int j = 0; j < 4; ++j) mma_unit(acc[t][j], fa, fb[j], (bf16*)nullptr);
-      }
-    }
-  }
-
-  const long long RSC = 9LL * C;
-  const int lr = lane & 15, lg = lane >> 4;
-#pragma unroll
-  for (int t = 0; t < 9; ++t) {
-    const int T = 9 * wave + t, tap = T >> 2, cg = T & 3;
-    const long long row = (long long)tap * C + c0 + 16 * cg + 4 * lg;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int col = k0 + 16 * j + lr;
-      float* dst = a.out + ((long long)split * K + col) * RSC + row;
-      *reinterpret_cast<float4*>(dst) =
-          make_float4(acc[t][j][0], acc[t][j][1], acc[t][j][2], acc[t][j][3]);
-    }
-  }
-}
 
 // ------------------------------------ 3x3 / stride 1 convolution, 64 -> 64
 // out[pix][o] = sum over taps (r, s) and input channels i of
@@ -1912,8 +1778,8 @@ __global__ __launch_bounds__(C64_NT) void conv64_kernel(Conv64Args a) {
 }
 
 // ---------------------------- all-taps weight gradient, warp-specialised
-// The same work, layout of one stage and per-wave tiles as wgrad_tap_kernel,
-// with the conv64_kernel arrangement of the copies: a fifth wave issues every
+// The stage layout and per-wave tiles above, with the conv64_kernel
+// arrangement of the copies: a fifth wave issues every
 // direct-to-LDS copy of a 4-slot ring (input rows 0-103 -- the tile's 100
 // pixels and 4 zero rows, 13 copies -- then the 64 output-gradient rows, 8
 // copies) and never stores, so it keeps three stages in flight (63 copies:
@@ -1929,7 +1795,8 @@ constexpr int TAPW_NT = 320;
 static_assert((TAPW_NST - 1) * TAPW_COPIES <= 63, "vector-memory counter");
 
 // Copy ins (0 .. 20) of the copy wave: rows 8 ins .. + 7 of the stage, 16-byte
-// segment lane % 8 -- the pixel and unit placement of tap_slot.
+// segment lane % 8 (global 16-byte unit u of the pixel in segment position
+// u ^ 2 (p mod 4), i.e. 32-byte segments swizzled by pixel mod 4).
 __host__ __device__ inline TapSlot tapw_slot(int W, int C, int Q, int K, int c0, int k0, int lane,
                                              int ins) {
   const int sl = lane & 7;
@@ -3215,14 +3082,18 @@ struct WgDmaPlan {
   TapGeom tap;  // tap.splits > 0: the all-taps kernel (3x3, stride 1)
 };
 bool wgrad_dma_ok(int dt, const ConvGeom& g) { return dt == DT_BF16 && g.C % 64 == 0 && g.K % 64 == 0; }
-// Blocks the all-taps weight gradient aims for (one per CU).
+// Blocks the all-taps weight gradient aims for: one per CU, or one per two
+// CUs when it runs beside the data-gradient chain on another stream (more
+// measured slower there: the chain on the critical path then waits for CUs
+// and bandwidth the weight gradient holds).
 constexpr int TAP_TARGET_BLOCKS = 256;
+constexpr int TAP_SHARED_BLOCKS = 128;
 bool wgrad_tap_ok(const ConvGeom& g) {
   return g.R == 3 && g.S == 3 && g.stride == 1 && g.pad == 1 && g.P == g.H && g.Q == g.W &&
          g.C % 64 == 0 && g.K % 64 == 0 && (long long)g.N * g.H * g.W * g.C < (1LL << 40) &&
          (long long)g.N * g.P * g.Q * g.K < (1LL << 40);
 }
-TapGeom plan_wgrad_tap(const ConvGeom& g) {
+TapGeom plan_wgrad_tap(const ConvGeom& g, bool shared) {
   TapGeom t;
   t.tiles_c = g.C / 64;
   t.tiles_k = g.K / 64;
@@ -3230,14 +3101,14 @@ TapGeom plan_wgrad_tap(const ConvGeom& g) {
   t.px_n = (g.Q + 7) / 8;
   const long long np = (long long)g.N * t.py_n * t.px_n;
   const long long tiles = (long long)t.tiles_c * t.tiles_k;
-  long long s = std::max(1LL, std::min(np, cdivl(TAP_TARGET_BLOCKS, tiles)));
+  long long s = std::max(1LL, std::min(np, cdivl(shared ? TAP_SHARED_BLOCKS : TAP_TARGET_BLOCKS, tiles)));
   t.pps = (int)cdivl(np, s);
   t.splits = (int)cdivl(np, t.pps);
   return t;
 }
-WgDmaPlan plan_wgrad_dma(const ConvGeom& g) {
+WgDmaPlan plan_wgrad_dma(const ConvGeom& g, bool shared = false) {
   if (wgrad_tap_ok(g)) {
-    const TapGeom t = plan_wgrad_tap(g);
+    const TapGeom t = plan_wgrad_tap(g, shared);
     return {576, 64, t.splits, 0, t};
   }
   const long long M = (long long)g.N * g.P * g.Q;
@@ -3267,8 +3138,8 @@ struct WPlan {
 
 // dw == nullptr: leave the split partials (one split included) in `partials`.
 hipError_t conv_wgrad_dma(const ConvGeom& g, const void* x, const void* dy, float* partials,
-                          float* dw, hipStream_t stream) {
-  const WgDmaPlan p = plan_wgrad_dma(g);
+                          float* dw, hipStream_t stream, bool shared = false) {
+  const WgDmaPlan p = plan_wgrad_dma(g, shared);
   float* out = (p.splits > 1 || !dw) ? partials : dw;
   WgDmaArgs a{g, (const bf16*)x, (const bf16*)dy, out, p.mps, 0, 0, p.splits};
   a.tiles_m = g.R * g.S * g.C / p.bm;
@@ -3337,10 +3208,10 @@ size_t conv_wgrad_partials_floats(int dt, const ConvGeom& g) {
 }
 
 hipError_t conv_wgrad_partials(int dt, const ConvGeom& g, const void* x, const void* dy,
-                               float* partials, int* splits, hipStream_t stream) {
+                               float* partials, int* splits, hipStream_t stream, bool shared) {
   if (!conv_wgrad_partials_ok(dt, g) || !partials) return hipErrorInvalidValue;
-  *splits = plan_wgrad_dma(g).splits;
-  return conv_wgrad_dma(g, x, dy, partials, nullptr, stream);
+  *splits = plan_wgrad_dma(g, shared).splits;
+  return conv_wgrad_dma(g, x, dy, partials, nullptr, stream, shared);
 }
 
 namespace {

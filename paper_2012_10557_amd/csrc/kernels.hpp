@@ -133,8 +133,11 @@ hipError_t conv_wgrad(int dt, const ConvGeom& g, const void* x, const void* dy, 
 // after the partials.
 bool conv_wgrad_partials_ok(int dt, const ConvGeom& g);
 size_t conv_wgrad_partials_floats(int dt, const ConvGeom& g);
+// shared: the launch runs beside other work on another stream (the
+// all-taps kernel then takes about half the CUs; fewer splits).
 hipError_t conv_wgrad_partials(int dt, const ConvGeom& g, const void* x, const void* dy,
-                               float* partials, int* splits, hipStream_t stream);
+                               float* partials, int* splits, hipStream_t stream,
+                               bool shared = false);
 
 // ---------------------------------------------------------------- BatchNorm
 // Per-channel statistics of z[M, C] (NHWC rows).  Writes mean and 1/sqrt(var+eps)

@@ -895,7 +895,7 @@ static hipError_t train_backward(TrainJob& j, int nb, const int32_t* fid, float*
     if (!main && deferred >= 0) EKYA_HIP(fork());  // ws2 still holds the deferred partials
     if (fused_update(net, c)) {
       int splits = 0;
-      EKYA_HIP(conv_wgrad_partials(dt, cg, x, dy, scratch, &splits, q));
+      EKYA_HIP(conv_wgrad_partials(dt, cg, x, dy, scratch, &splits, q, two && !main));
       if (!main && dgrad_after) {
         deferred = ci;
         deferred_splits = splits;
