@@ -2333,10 +2333,69 @@ constexpr int STEM_NT = 512;
 constexpr int SP_QMAX = STEM_QMAX / 2;  // pool columns
 __device__ __forceinline__ float gt_max(float m, float v) { return v > m ? v : m; }
 
+// One wave's share of a stem output row: column blocks T0 .. T0 + TN - 1
+// (16 columns each) for all 64 channels, written straight to y with the
+// epilogue applied.  A row is done in two such parts so the accumulators take
+// 64 registers, not 112, and two blocks fit on a CU; the first part's stores
+// are in flight while the second part runs its MFMAs.
+template <int T0, int TN>
+__device__ __forceinline__ void stem_row_part(const bf16* wl, const uint2* prow0, int lr, int kc,
+                                              int tq, int Q, bf16* yrow, const ConvEpilogue& epi) {
+  if (T0 >= tq) return;  // wave-uniform
+  f32x4 acc[4][TN];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int t = 0; t < TN; ++t) acc[i][t] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll 1
+  for (int r = 0; r < 7; ++r) {
+    uint4 fa[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      fa[i] = *reinterpret_cast<const uint4*>(wl + (i * 16 + lr) * STEM_WROW + r * 32 + kc * 8);
+    const uint2* prow = prow0 + r * STEM_PATCH_W;
+    uint4 fb[TN];
+#pragma unroll
+    for (int t = 0; t < TN; ++t)
+      fb[t] = *reinterpret_cast<const uint4*>(prow + 2 * ((T0 + t) * 16 + lr) + 2 * kc);
+#pragma unroll
+    for (int t = 0; t < TN; ++t) {
+      if (T0 + t < tq) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) mma_unit(acc[i][t], fa[i], fb[t], (bf16*)nullptr);
+      }
+    }
+  }
+#pragma unroll
+  for (int t = 0; t < TN; ++t) {
+    const int q = (T0 + t) * 16 + lr;
+    if (T0 + t >= tq || q >= Q) continue;
+    bf16* dst = yrow + (long long)q * 64;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int k = i * 16 + 4 * kc;
+      float v[4] = {acc[i][t][0], acc[i][t][1], acc[i][t][2], acc[i][t][3]};
+      if (epi.scale) {
+        const float4 s4 = *reinterpret_cast<const float4*>(epi.scale + k);
+        v[0] *= s4.x; v[1] *= s4.y; v[2] *= s4.z; v[3] *= s4.w;
+      }
+      if (epi.shift) {
+        const float4 b4 = *reinterpret_cast<const float4*>(epi.shift + k);
+        v[0] += b4.x; v[1] += b4.y; v[2] += b4.z; v[3] += b4.w;
+      }
+      if (epi.relu) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = relu_nan(v[e]);
+      }
+      store4<bf16>(dst + k, v);
+    }
+  }
+}
+
 // RAW: x is [.][H][W][3] frames (image n at idx[n] when idx != null) read
 // with three 2-byte loads per pixel, instead of the 8-channel padded input.
 template <bool RAW, bool POOL = false>
-__global__ __launch_bounds__(STEM_NT + (POOL ? 64 : 0)) void stem_kernel(
+__global__ __launch_bounds__(STEM_NT + (POOL ? 64 : 0), POOL ? 1 : 4) void stem_kernel(
     const bf16* x, const int32_t* idx, const bf16* wk, bf16* y, ConvEpilogue epi, int N, int H,
     int W, int P, int Q) {
   constexpr int ROWS = POOL ? STEM_ROWS + 1 : STEM_ROWS, NT = ROWS * 64;
@@ -2373,34 +2432,48 @@ __global__ __launch_bounds__(STEM_NT + (POOL ? 64 : 0)) void stem_kernel(
   // input rows 2 p0 - 3 .. 2 p0 + 2 ROWS + 1, columns -3 .. pw - 4 (zero outside the frame)
   const long long img_n = (RAW && idx) ? idx[n] : n;
   const bf16* img = x + img_n * H * W * (RAW ? 3 : 8);
-  const int total = IN_ROWS * pw;
-  for (int i0 = threadIdx.x; i0 < total; i0 += 8 * NT) {
-    uint2 v[8];
+  // wave v stages rows v, v + ROWS, v + 2 ROWS; lane l columns l + 64 u
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  static_assert(IN_ROWS <= 3 * ROWS && STEM_PATCH_W <= 4 * 64, "staging covers the patch");
+  {
+    uint2 v[3][4];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const int i = i0 + u * NT, pr = i / pw, pc = i % pw;
-      const int h = 2 * p0 - 3 + pr, w = pc - 3;
-      const bool in = i < total && (unsigned)h < (unsigned)H && (unsigned)w < (unsigned)W;
-      if (RAW) {
-        const unsigned short* px =
-            reinterpret_cast<const unsigned short*>(img + ((long long)h * W + w) * 3);
-        v[u] = in ? make_uint2((unsigned)px[0] | ((unsigned)px[1] << 16), (unsigned)px[2])
-                  : make_uint2(0u, 0u);
-      } else {
-        v[u] = in ? *reinterpret_cast<const uint2*>(img + ((long long)h * W + w) * 8)
-                  : make_uint2(0u, 0u);
+    for (int rr = 0; rr < 3; ++rr)
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int pr = wave + rr * ROWS, pc = lane + 64 * u;
+        const int h = 2 * p0 - 3 + pr, w = pc - 3;
+        const bool in = pr < IN_ROWS && pc < pw && (unsigned)h < (unsigned)H && (unsigned)w < (unsigned)W;
+        if (RAW) {
+          const unsigned short* px =
+              reinterpret_cast<const unsigned short*>(img + ((long long)h * W + w) * 3);
+          v[rr][u] = in ? make_uint2((unsigned)px[0] | ((unsigned)px[1] << 16), (unsigned)px[2])
+                        : make_uint2(0u, 0u);
+        } else {
+          v[rr][u] = in ? *reinterpret_cast<const uint2*>(img + ((long long)h * W + w) * 8)
+                        : make_uint2(0u, 0u);
+        }
       }
-    }
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const int i = i0 + u * NT;
-      if (i < total) patch[(i / pw) * STEM_PATCH_W + i % pw] = v[u];
-    }
+    for (int rr = 0; rr < 3; ++rr)
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int pr = wave + rr * ROWS, pc = lane + 64 * u;
+        if (pr < IN_ROWS && pc < pw) patch[pr * STEM_PATCH_W + pc] = v[rr][u];
+      }
   }
   __syncthreads();
 
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int lr = lane & 15, kc = lane >> 4;
+  if constexpr (!POOL) {
+    const int p = p0 + wave;
+    if (p >= P) return;
+    bf16* yrow = y + ((long long)n * P + p) * Q * 64;
+    const uint2* prow0 = patch + 2 * wave * STEM_PATCH_W;
+    stem_row_part<0, 4>(wl, prow0, lr, kc, tq, Q, yrow, epi);
+    stem_row_part<4, STEM_TQ - 4>(wl, prow0, lr, kc, tq, Q, yrow, epi);
+    return;
+  }
   {
     const int lp = wave;  // output row within the block
     const int p = p0 + lp;
@@ -2507,31 +2580,6 @@ __global__ __launch_bounds__(STEM_NT + (POOL ? 64 : 0)) void stem_kernel(
         float lo4[4] = {best[0], best[1], best[2], best[3]}, hi4[4] = {best[4], best[5], best[6], best[7]};
         store4<bf16>(dst, lo4);
         store4<bf16>(dst + 4, hi4);
-      }
-      return;
-    }
-#pragma unroll
-    for (int t = 0; t < STEM_TQ; ++t) {
-      const int q = t * 16 + lr;
-      if (t >= tq || q >= Q) continue;
-      bf16* dst = y + (((long long)n * P + p) * Q + q) * 64;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int k = i * 16 + 4 * lg;
-        float v[4] = {acc[i][t][0], acc[i][t][1], acc[i][t][2], acc[i][t][3]};
-        if (epi.scale) {
-          const float4 s4 = *reinterpret_cast<const float4*>(epi.scale + k);
-          v[0] *= s4.x; v[1] *= s4.y; v[2] *= s4.z; v[3] *= s4.w;
-        }
-        if (epi.shift) {
-          const float4 b4 = *reinterpret_cast<const float4*>(epi.shift + k);
-          v[0] += b4.x; v[1] += b4.y; v[2] += b4.z; v[3] += b4.w;
-        }
-        if (epi.relu) {
-#pragma unroll
-          for (int e = 0; e < 4; ++e) v[e] = relu_nan(v[e]);
-        }
-        store4<bf16>(dst + k, v);
       }
     }
   }
