@@ -3,6 +3,7 @@
 // momentum; frame gather / padding / resize; weight repacking.  Every
 // reduction is two-level with a fixed order, so results do not depend on
 // scheduling (concurrent and sequential runs are bitwise equal).
+#include <climits>
 #include <algorithm>
 #include <type_traits>
 
@@ -1012,9 +1013,10 @@ __global__ __launch_bounds__(256) void maxpool_bwd_kernel(const T* dy, const uin
 // pad 1 max pool (the stem, 64 channels): the gradient at output pixel
 // (n, h, w) is gathered from the pooled gradient and window indices exactly as
 // maxpool_bwd_kernel computes it (windows in (r, s) order) and rounded to T as
-// that kernel stores it; the ReLU mask is recomputed from z.  So the partial
-// sums and the input gradient equal those of maxpool_bwd followed by
-// bn_backward, without the full-size gradient being written or read.
+// that kernel stores it; the ReLU mask is recomputed from z.  So every
+// element's gradient is the one bn_backward would read after maxpool_bwd
+// (the statistics add the same terms, grouped differently), without the
+// full-size gradient being written or read.
 // Input rows 2p and 2p + 1 take their gradient from pooled rows p and p + 1
 // only: a block stages those two pooled rows (gradient and indices) in LDS,
 // then gathers from there while it streams the two rows of z.
@@ -1029,73 +1031,115 @@ constexpr int POOLBN_QMAX = 64;  // pooled width (stem output width up to 128)
 template <typename T>
 struct PoolRows {
   static constexpr int E = Elt<T>::E, CU = POOLBN_C / E;
-  // pooled rows p, p + 1 (zero beyond the image): units [2][Q][CU], indices [2][Q][C]
-  uint4 g[2 * POOLBN_QMAX * CU];
-  uint8_t a[2 * POOLBN_QMAX * POOLBN_C];
+  // pooled rows p, p + 1 (zero beyond the image), each Q + 1 columns wide:
+  // units [2][Q + 1][CU], indices [2][Q + 1][C]; column Q stays zero, the
+  // right neighbour of an odd last input column
+  uint4 g[2 * (POOLBN_QMAX + 1) * CU];
+  uint8_t a[2 * (POOLBN_QMAX + 1) * POOLBN_C];
 };
 
-// Stage pooled rows p, p + 1 of image n; all threads take part.
+// Pooled rows p, p + 1 of image n, held in registers between their loads and
+// their LDS writes so that a thread's loads are all in flight together: a
+// 256-thread block covers the 2 x POOLBN_QMAX x CU gradient units in GPT
+// loads per thread and the index units in APT.
 template <typename T>
-__device__ __forceinline__ void pool_rows_stage(const PoolSrc& ps, int n, int p, PoolRows<T>& sm) {
-  constexpr int E = Elt<T>::E, CU = POOLBN_C / E;
-  const int nu = 2 * ps.Q * CU;                    // 16-byte units of the gradient
-  const int na = 2 * ps.Q * POOLBN_C / 16;         // 16-byte units of the indices
-  for (int i = threadIdx.x; i < nu; i += blockDim.x) {
-    const int rr = i / (ps.Q * CU), rem = i - rr * (ps.Q * CU);
-    const int pp = p + rr;
-    sm.g[i] = pp < ps.P ? reinterpret_cast<const uint4*>(ps.dy)[((long long)n * ps.P + pp) * ps.Q * CU + rem]
-                        : uint4{0, 0, 0, 0};
+struct PoolRowsRegs {
+  static constexpr int CU = POOLBN_C / Elt<T>::E;
+  static constexpr int GPT = 2 * POOLBN_QMAX * CU / 256, APT = 2 * POOLBN_QMAX * POOLBN_C / 16 / 256;
+  uint4 g[GPT], a[APT];
+};
+
+template <typename T>
+__device__ __forceinline__ void pool_rows_load(const PoolSrc& ps, int n, int p, int tid,
+                                               PoolRowsRegs<T>& r) {
+  using R = PoolRowsRegs<T>;
+  const int per_g = ps.Q * R::CU, per_a = ps.Q * POOLBN_C / 16;
+#pragma unroll
+  for (int j = 0; j < R::GPT; ++j) {
+    const int i = tid + 256 * j, rr = i >= per_g, rem = i - rr * per_g;
+    r.g[j] = i < 2 * per_g && p + rr < ps.P
+                 ? reinterpret_cast<const uint4*>(ps.dy)[((long long)n * ps.P + p + rr) * per_g + rem]
+                 : uint4{0, 0, 0, 0};
   }
-  for (int i = threadIdx.x; i < na; i += blockDim.x) {
-    const int per = ps.Q * POOLBN_C / 16;
-    const int rr = i / per, rem = i - rr * per;
-    const int pp = p + rr;
-    reinterpret_cast<uint4*>(sm.a)[i] =
-        pp < ps.P ? reinterpret_cast<const uint4*>(ps.arg)[((long long)n * ps.P + pp) * per + rem]
-                  : uint4{0, 0, 0, 0};
+#pragma unroll
+  for (int j = 0; j < R::APT; ++j) {
+    const int i = tid + 256 * j, rr = i >= per_a, rem = i - rr * per_a;
+    r.a[j] = i < 2 * per_a && p + rr < ps.P
+                 ? reinterpret_cast<const uint4*>(ps.arg)[((long long)n * ps.P + p + rr) * per_a + rem]
+                 : uint4{0, 0, 0, 0};
   }
 }
 
-// Gradient of unit cu of input pixel (h = 2p + hh, w), from the staged rows.
 template <typename T>
-__device__ __forceinline__ void pool_rows_grad(const PoolSrc& ps, const PoolRows<T>& sm, int nrows,
-                                               int hh, int w, int cu, float (&g)[Elt<T>::E]) {
+__device__ __forceinline__ void pool_rows_store(const PoolSrc& ps, const PoolRowsRegs<T>& r, int tid,
+                                                PoolRows<T>& sm) {
+  using R = PoolRowsRegs<T>;
+  const int per_g = ps.Q * R::CU, per_a = ps.Q * POOLBN_C / 16;
+#pragma unroll
+  for (int j = 0; j < R::GPT; ++j) {
+    const int i = tid + 256 * j, rr = i >= per_g;
+    if (i < 2 * per_g) sm.g[i + rr * R::CU] = r.g[j];
+  }
+#pragma unroll
+  for (int j = 0; j < R::APT; ++j) {
+    const int i = tid + 256 * j, rr = i >= per_a;
+    if (i < 2 * per_a) reinterpret_cast<uint4*>(sm.a)[i + rr * (POOLBN_C / 16)] = r.a[j];
+  }
+}
+
+// The zero column Q of both staged rows (written once; staging never touches it).
+template <typename T>
+__device__ __forceinline__ void pool_rows_zero_pad(const PoolSrc& ps, PoolRows<T>& sm) {
+  constexpr int CU = POOLBN_C / Elt<T>::E, AU = POOLBN_C / 16;
+  const int t = threadIdx.x;
+  if (t < 2 * CU) sm.g[((t / CU) * (ps.Q + 1) + ps.Q) * CU + t % CU] = uint4{0, 0, 0, 0};
+  if (t < 2 * AU)
+    reinterpret_cast<uint4*>(sm.a)[((t / AU) * (ps.Q + 1) + ps.Q) * AU + t % AU] = uint4{0, 0, 0, 0};
+}
+
+// Gradient of unit cu of input pixel (h = 2p + hh, w), from the staged rows.
+// Row parity hh and column parity w & 1 fix which windows hold the pixel: an
+// even row only window row r = 1 of pooled row p; an odd row r = 0 of row
+// p + 1 and r = 2 of row p; an even column only s = 1 of pooled column w / 2;
+// an odd column s = 0 of (w + 1) / 2 and s = 2 of (w - 1) / 2.  Both parities
+// are the same across a wave, so the candidates are taken in (r, s) order
+// with branches that never split a wave.
+template <typename T>
+__device__ __forceinline__ void pool_rows_grad(const PoolSrc& ps, const PoolRows<T>& sm, int hh,
+                                               int par, int w, int cu, float (&g)[Elt<T>::E]) {
   constexpr int E = Elt<T>::E, CU = POOLBN_C / E;
   float acc[E];
 #pragma unroll
   for (int i = 0; i < E; ++i) acc[i] = 0.f;
-  // h = 2p: window row r = 1 (pooled row p); h = 2p + 1: r = 0 (row p + 1), r = 2 (row p)
-  const int r0 = hh ? 0 : 1, nr = hh ? 2 : 1;
-  const int s0 = (w & 1) ? 0 : 1, nsw = (w & 1) ? 2 : 1;
+  const int Q1 = ps.Q + 1;
 #pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    if ((k >> 1) >= nr || (k & 1) >= nsw) continue;
-    const int r = r0 + 2 * (k >> 1), s = s0 + 2 * (k & 1);
-    const int rr = hh + 1 - r >= 0 ? (hh + 1 - r) >> 1 : -1;  // staged row: 0 (p) or 1 (p + 1)
-    const int wp = w + 1 - s;
-    if (rr < 0 || rr >= nrows || wp < 0 || (wp >> 1) >= ps.Q) continue;
-    const int q = wp >> 1;
-    float v[E];
-    int a[E];
-    unit_to_f<T>(sm.g[(rr * ps.Q + q) * CU + cu], v);
-    arg_load<E>(sm.a + (rr * ps.Q + q) * POOLBN_C + cu * E, a);  // one 4- or 8-byte LDS read
+  for (int kr = 0; kr < 2; ++kr) {
+    if (kr > hh) break;
+    const int r = hh ? 2 * kr : 1, rr = hh ? 1 - kr : 0;
 #pragma unroll
-    for (int i = 0; i < E; ++i)
-      if (a[i] == r * 3 + s) acc[i] += v[i];
+    for (int ks = 0; ks < 2; ++ks) {
+      if (ks > par) break;
+      const int s = par ? 2 * ks : 1, q = (w + 1 - s) >> 1;  // q <= Q (the zero column)
+      float v[E];
+      int a[E];
+      unit_to_f<T>(sm.g[(rr * Q1 + q) * CU + cu], v);
+      arg_load<E>(sm.a + (rr * Q1 + q) * POOLBN_C + cu * E, a);  // one 4- or 8-byte LDS read
+#pragma unroll
+      for (int i = 0; i < E; ++i)
+        if (a[i] == r * 3 + s) acc[i] += v[i];
+    }
   }
 #pragma unroll
   for (int i = 0; i < E; ++i) g[i] = to_f((T)acc[i]);
 }
 
 // STATS: partial sums S_g, S_gx of block b's rp row pairs into part[b];
-// otherwise dz of one row pair per block.
+// otherwise dz of block b's rp row pairs.
 template <typename T, bool STATS>
-__global__ __launch_bounds__(256) void bn_bwd_pool_kernel(PoolSrc ps, const T* z, int N, int rp,
-                                                          const float* mean, const float* coef,
-                                                          const float* gamma, const float* invstd,
-                                                          const float* mb, float* part, T* dz) {
+__global__ __launch_bounds__(256, STATS ? 4 : 1) void bn_bwd_pool_kernel(
+    PoolSrc ps, const T* z, int N, int rp, const float* mean, const float* coef,
+    const float* gamma, const float* invstd, const float* mb, float* part, T* dz) {
   constexpr int E = Elt<T>::E, CU = POOLBN_C / E;
-  static_assert(256 % CU == 0, "a thread keeps its channel unit");
   __shared__ PoolRows<T> sm;
   const int t = threadIdx.x, cu = t % CU, c0 = cu * E;
   float mu[E], msc[E], mbe[E], ca[E], cb[E], cc[E], s1[E], s2[E];
@@ -1110,21 +1154,48 @@ __global__ __launch_bounds__(256) void bn_bwd_pool_kernel(PoolSrc ps, const T* z
   for (int i = 0; i < E; ++i) s1[i] = s2[i] = 0.f;
   const int pairs = N * ps.P;
   const int k0 = blockIdx.x * rp, k1 = min(pairs, k0 + rp);
-  const int nunits = 2 * ps.W * CU;
+  // units by parity class (hh, w & 1): class c = 2 hh + (w & 1) takes
+  // units [c G, c G + G), G = GW x 64 so a wave stays in one class; within a
+  // class unit i is column 2 (i / CU) + (w & 1), channel unit i % CU.  A
+  // wave's units of a pair are 64 (wave + 4 j) + lane, so its class for
+  // step j is (wave + 4 j) / GW, a scalar.
+  const int GW = cdiv(cdiv(ps.W, 2) * CU, 64), G = GW * 64;
+  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
+  constexpr int ZPT = 4 * ((POOLBN_QMAX * CU + 63) / 64) * 64 / 256;
+  static_assert(256 % CU == 0 && 64 % CU == 0, "a thread keeps its channel unit");
+  pool_rows_zero_pad<T>(ps, sm);  // ordered before any read by the first pair's barriers
   for (int k = k0; k < k1; ++k) {
     const int n = k / ps.P, p = k - n * ps.P;
+    // the per-unit offsets and predicates are recomputed each pair from an
+    // opaque copy of the thread index: hoisted out of the loop they would
+    // occupy most of the register file
+    int tl = t;
+    asm volatile("" : "+v"(tl));
+    const long long base = ((long long)n * ps.H + 2 * p) * ps.W * POOLBN_C + c0;
+    // z of the pair and its two pooled rows are loaded together before any is used
+    uint4 zr[ZPT];
+#pragma unroll
+    for (int j = 0; j < ZPT; ++j) {
+      const int cls = (wave + 4 * j) / GW, hh = cls >> 1;
+      const int w = 2 * ((tl + 256 * j - cls * G) / CU) + (cls & 1);
+      zr[j] = cls < 4 && w < ps.W && 2 * p + hh < ps.H
+                  ? *reinterpret_cast<const uint4*>(z + base + ((long long)hh * ps.W + w) * POOLBN_C)
+                  : uint4{0, 0, 0, 0};
+    }
+    PoolRowsRegs<T> pr;
+    pool_rows_load<T>(ps, n, p, tl, pr);
     __syncthreads();  // the previous pair's staged rows are no longer read
-    pool_rows_stage<T>(ps, n, p, sm);
+    pool_rows_store<T>(ps, pr, tl, sm);
     __syncthreads();
-    for (int u = t; u < nunits; u += 256) {
-      const int hh = u / (ps.W * CU), rem = u - hh * (ps.W * CU);
-      const int w = rem / CU;
-      const int h = 2 * p + hh;
-      if (h >= ps.H) break;
-      const long long off = (((long long)n * ps.H + h) * ps.W + w) * POOLBN_C + c0;
+#pragma unroll
+    for (int j = 0; j < ZPT; ++j) {
+      const int cls = (wave + 4 * j) / GW, hh = cls >> 1;
+      if (cls >= 4 || 2 * p + hh >= ps.H) continue;  // wave-uniform
+      const int w = 2 * ((tl + 256 * j - cls * G) / CU) + (cls & 1);
+      if (w >= ps.W) continue;
       float g[E], zz[E];
-      unit_to_f<T>(*reinterpret_cast<const uint4*>(z + off), zz);
-      pool_rows_grad<T>(ps, sm, p + 1 < ps.P ? 2 : 1, hh, w, cu, g);
+      unit_to_f<T>(zr[j], zz);
+      pool_rows_grad<T>(ps, sm, hh, cls & 1, w, cu, g);
       apply_mask<T, E>(msc, mbe, mu, zz, g);
       if constexpr (STATS) {
 #pragma unroll
@@ -1136,8 +1207,10 @@ __global__ __launch_bounds__(256) void bn_bwd_pool_kernel(PoolSrc ps, const T* z
         float o[E];
 #pragma unroll
         for (int i = 0; i < E; ++i) o[i] = ca[i] * g[i] + cb[i] + cc[i] * (zz[i] - mu[i]);
-        *reinterpret_cast<uint4*>(dz + off) = f_to_unit<T>(o);
+        *reinterpret_cast<uint4*>(dz + base + ((long long)hh * ps.W + w) * POOLBN_C) = f_to_unit<T>(o);
       }
+      // one unit's LDS reads at a time: hoisting them all costs the whole register file
+      __builtin_amdgcn_sched_barrier(0);
     }
   }
   if constexpr (STATS) {
@@ -1709,6 +1782,22 @@ __global__ void frames_to_padded_kernel(const T* src, const int32_t* idx, int n,
   }
 }
 
+// 2-byte elements, 8 stored channels, an even pixel count per frame: a lane
+// expands two adjacent pixels (three dwords of 3-channel input, 4-byte
+// aligned) into two 16-byte pixels; blockIdx.y is the frame.
+__global__ void frames_to_padded8_kernel(const uint32_t* src, const int32_t* idx, int pairs,
+                                         uint4* dst) {
+  const int f = blockIdx.y;
+  const long long sf = idx ? idx[f] : f;
+  const uint32_t* s = src + sf * pairs * 3;
+  uint4* d = dst + (long long)f * pairs * 2;
+  for (int t = blockIdx.x * blockDim.x + threadIdx.x; t < pairs; t += gridDim.x * blockDim.x) {
+    const uint32_t a = s[3 * t], b = s[3 * t + 1], c = s[3 * t + 2];
+    d[2 * t] = make_uint4(a, b & 0xFFFFu, 0u, 0u);
+    d[2 * t + 1] = make_uint4((b >> 16) | (c << 16), c >> 16, 0u, 0u);
+  }
+}
+
 __device__ __forceinline__ void src_coord(int dst, int n_in, int n_out, int& i0, int& i1,
                                           float& lam) {
   float s = ((float)dst + 0.5f) * ((float)n_in / (float)n_out) - 0.5f;
@@ -2099,6 +2188,7 @@ hipError_t bn_backward_pool(int dt, const void* dy_pool, const uint8_t* arg, con
   const PoolSrc ps{dy_pool, arg, H, W, P, Q};
   const int pairs = N * P;
   // at most as many partial rows as bn_partials_floats(M, C) provides
+  // at most as many partial rows as bn_partials_floats(M, C) provides
   const int rp = cdiv(pairs, bn_chunks(M, C)), nch = cdiv(pairs, rp);
   float* coef = partials + (size_t)nch * 2 * C;
   const size_t es = dtype_size(dt);
@@ -2111,14 +2201,14 @@ hipError_t bn_backward_pool(int dt, const void* dy_pool, const uint8_t* arg, con
                        partials, (T*)nullptr);
     hipLaunchKernelGGL(bn_bwd_final, dim3(cdiv(C, FIN_CH)), dim3(256), 0, stream, partials, nch, M, C,
                        gamma, invstd, dgamma, dbeta, coef);
-  }), "bn_bwd_stats", act + pooled);
+  }), "bn_bwd_pool_stats", act + pooled);
   if (e != hipSuccess) return e;
   TimedLaunch ta(stream);  // z and the pooled gradient read, dz written
   return ta.done(by_type(dt, [&](auto* tp) {
     using T = std::remove_pointer_t<decltype(tp)>;
     hipLaunchKernelGGL((bn_bwd_pool_kernel<T, false>), dim3(pairs), dim3(256), 0, stream, ps,
                        (const T*)z, N, 1, mean, coef, gamma, invstd, beta, (float*)nullptr, (T*)dz);
-  }), "bn_bwd_apply", 2 * act + pooled);
+  }), "bn_bwd_pool_apply", 2 * act + pooled);
 }
 
 hipError_t maxpool_fwd(int dt, const void* x, int N, int H, int W, int C, void* y, uint8_t* arg,
@@ -2303,11 +2393,20 @@ hipError_t frames_to_padded(int dt, const void* frames, const int32_t* idx, int 
   const long long hw = (long long)H * W;
   if (n == 0) return hipSuccess;
   TimedLaunch tl(stream);
+  const double bytes = (double)n * hw * (3 + Cp) * dtype_size(dt);
+  if (dtype_size(dt) == 2 && Cp == 8 && hw % 2 == 0 && hw / 2 <= INT_MAX / 3 &&
+      (reinterpret_cast<uintptr_t>(frames) & 3) == 0 && (reinterpret_cast<uintptr_t>(dst) & 15) == 0 &&
+      n <= 65535) {
+    const int pairs = (int)(hw / 2);
+    hipLaunchKernelGGL(frames_to_padded8_kernel, dim3(std::min(cdiv(pairs, 256), 4096), n), dim3(256),
+                       0, stream, (const uint32_t*)frames, idx, pairs, (uint4*)dst);
+    return tl.done(hipGetLastError(), "frames_to_padded", bytes);
+  }
   return tl.done(by_type(dt, [&](auto* tp) {
     using T = std::remove_pointer_t<decltype(tp)>;
     hipLaunchKernelGGL(frames_to_padded_kernel<T>, dim3(grid_for(n * hw)), dim3(256), 0, stream,
                        (const T*)frames, idx, n, hw, Cp, (T*)dst);
-  }), "frames_to_padded", (double)n * hw * (3 + Cp) * dtype_size(dt));
+  }), "frames_to_padded", bytes);
 }
 
 hipError_t resize_to_padded(int dt, const void* frames, int n, int H, int W, int r, int Cp,
