@@ -166,6 +166,33 @@ def roofline_of(gemm, mem):
     return roofline, by_kind, hbm
 
 
+COPY_BYTES = 1 << 28  # calibration copy of the traffic probe
+
+
+def traffic_probe(binding, torch):
+    """The all-taps weight gradients of one full-depth batch -- the 3x3
+    stride-1 convolutions of the step (4 at 56 px x 64 channels, 3 at 28 x 128,
+    3 at 14 x 256, 3 at 7 x 512; batch 128, bf16) -- through the C-ABI op, then
+    one device-to-device copy of COPY_BYTES whose counts calibrate the
+    FETCH_SIZE / WRITE_SIZE counters.  Meant to run under rocprofv3 --pmc."""
+    dev = torch.device("cuda:0")
+    gen = torch.Generator().manual_seed(0)
+    launches = 0
+    for hw, c, count in ((56, 64, 4), (28, 128, 3), (14, 256, 3), (7, 512, 3)):
+        x = (torch.rand(128, hw, hw, c, generator=gen) - 0.5).to(torch.bfloat16).to(dev)
+        dy = (torch.rand(128, hw, hw, c, generator=gen) - 0.5).to(torch.bfloat16).to(dev)
+        for _ in range(count):
+            binding.ekya_op_conv2d_wgrad(x, dy, (c, c, 3, 3), 1, 1)
+            launches += 1
+    src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"probe": "traffic", "kernel": "conv_wgrad<bf16,taps9,64>", "launches": launches,
+                      "copy_bytes": COPY_BYTES}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -177,6 +204,9 @@ def main():
     ap.add_argument("--timing-all-steps", action="store_true",
                     help="per-kernel timing (serial schedule) on every step, so that a profiler "
                          "run of this command measures the kernels as the roofline does")
+    ap.add_argument("--traffic-probe", action="store_true",
+                    help="run only the dominant kernel's launches of one batch and a calibration "
+                         "copy (for rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE passes), then exit")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -189,6 +219,9 @@ def main():
     from paper_2012_10557_amd import binding
     from synth import kaiming_resnet18_weights
 
+    if args.traffic_probe:
+        traffic_probe(binding, torch)
+        return
     dev = torch.device("cuda:0")
     w = FULL
     t_gen = time.perf_counter()
