@@ -1982,14 +1982,51 @@ constexpr int STEM_WG_ROWS = 22, STEM_WG_PITCH = 24;
 constexpr int STEM_WG_X = STEM_WG_ROWS * STEM_WG_PITCH * 8;  // input bytes per stage
 constexpr int STEM_WG_STAGE = STEM_WG_X + 64 * 128;
 
+// The stem's BatchNorm + ReLU + max-pool backward, for the weight gradient to
+// form its output gradient itself (POOLBWD): dy at stem pixel (h, w) is the
+// pooled gradient summed over the pool windows holding (h, w) whose stored
+// index names it (windows in (r, s) order, the sum rounded to bf16 as the
+// separate pool backward stores it), masked by ReLU (the mask recomputed
+// from z: the rounded fma((z - mean), gamma * invstd, beta) > 0), then
+// dz = coef0 * g + coef1 + coef2 * (z - mean) rounded to bf16 -- the
+// BatchNorm backward with coefficients from its statistics pass.
+struct StemPoolBwd {
+  const bf16* z;       // BatchNorm input [N][P][Q][64]
+  const bf16* dyp;     // pooled gradient [N][PP][PQ][64]
+  const uint8_t* arg;  // window indices (r * 3 + s), same layout
+  const float *mean, *coef, *gamma, *invstd, *beta;  // coef: [3][64]
+  int PP, PQ;
+};
+
 struct StemWgArgs {
   ConvGeom g;
   const bf16* x;   // [N][H][W][8]
-  const bf16* dy;  // [N][P][Q][64]
+  const bf16* dy;  // [N][P][Q][64] (unused with POOLBWD)
   float* out;      // [split][64][49][4]
   int splits, pps, py_n, px_n;
+  StemPoolBwd pb;
 };
 
+__device__ __forceinline__ void bf16x8_to_f(const uint4 u, float (&v)[8]) {
+  const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    v[2 * i] = __builtin_bit_cast(float, w[i] << 16);
+    v[2 * i + 1] = __builtin_bit_cast(float, w[i] & 0xFFFF0000u);
+  }
+}
+__device__ __forceinline__ uint32_t bf16x2_bits(float a, float b) {
+  return (uint32_t)__builtin_bit_cast(uint16_t, (bf16)a) |
+         ((uint32_t)__builtin_bit_cast(uint16_t, (bf16)b) << 16);
+}
+
+// With POOLBWD, wave w forms the output gradient of the stage's pixels of
+// parity class w (row parity w >> 1, column parity w & 1), then of class
+// 3 - w: 1 + 4 or 2 + 2 pool windows per pixel, the same class across the
+// wave.  Lane l takes channel unit l % 8 of pixel l / 8 of its half of the
+// class (16 pixels, two halves); its loads for the next stage are issued
+// before this stage's MFMAs.
+template <bool POOLBWD>
 __global__ __launch_bounds__(NT, 2) void wgrad_stem_kernel(StemWgArgs a) {
   constexpr int NST = 2;
   __shared__ __align__(16) char smem[NST * STEM_WG_STAGE];
@@ -2056,6 +2093,100 @@ __global__ __launch_bounds__(NT, 2) void wgrad_stem_kernel(StemWgArgs a) {
     }
   };
 
+  // POOLBWD: channel unit u of the lane, its per-channel constants, and the
+  // next stage's z and pool-window loads
+  const int pu = lane & 7;
+  float pmu[8], psc[8], pbe[8], pca[8], pcb[8], pcc[8];
+  if (POOLBWD) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int c = 8 * pu + i;
+      pmu[i] = a.pb.mean[c];
+      psc[i] = a.pb.gamma[c] * a.pb.invstd[c];
+      pbe[i] = a.pb.beta[c];
+      pca[i] = a.pb.coef[c];
+      pcb[i] = a.pb.coef[64 + c];
+      pcc[i] = a.pb.coef[128 + c];
+    }
+  }
+  uint4 pz[2], pg[2][4];
+  uint2 pa[2][4];
+  // stage pixel of half j: class cls = (j ? 3 - wave : wave), pixel k = 8 j + lane / 8 of it
+  auto pix_of = [&](int j, int& dsy, int& dsx) {
+    const int cls = j ? 3 - wave : wave, k = 8 * j + (lane >> 3);
+    dsy = 2 * (k >> 2) + (cls >> 1);
+    dsx = 2 * (k & 3) + (cls & 1);
+  };
+  auto pb_load = [&](int st) {
+    int n, py0, px0;
+    origin(st, n, py0, px0);
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int cls = j ? 3 - wave : wave, hp = cls >> 1, wp = cls & 1;
+      int dsy, dsx;
+      pix_of(j, dsy, dsx);
+      const int h = py0 + dsy, w = px0 + dsx;
+      const bool in = h < P && w < Q;
+      pz[j] = in ? *reinterpret_cast<const uint4*>(a.pb.z + (((long long)n * P + h) * Q + w) * 64 + 8 * pu)
+                 : make_uint4(0u, 0u, 0u, 0u);
+#pragma unroll
+      for (int kr = 0; kr < 2; ++kr)
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+          if (kr > hp || ks > wp) continue;  // wave-uniform
+          // odd row: window row r = 0 of pooled row h / 2 + 1, then r = 2 of h / 2;
+          // odd column likewise with s; even: r (s) = 1 of h / 2 (w / 2)
+          const int pr = (h >> 1) + (hp && kr == 0 ? 1 : 0);
+          const int pc = wp ? (ks == 0 ? (w + 1) >> 1 : (w - 1) >> 1) : (w >> 1);
+          const bool ok = in && pr < a.pb.PP && pc < a.pb.PQ;
+          const long long off = (((long long)n * a.pb.PP + pr) * a.pb.PQ + pc) * 64 + 8 * pu;
+          pg[j][2 * kr + ks] = ok ? *reinterpret_cast<const uint4*>(a.pb.dyp + off) : make_uint4(0u, 0u, 0u, 0u);
+          pa[j][2 * kr + ks] = ok ? *reinterpret_cast<const uint2*>(a.pb.arg + off)
+                                  : make_uint2(0xFFFFFFFFu, 0xFFFFFFFFu);
+        }
+    }
+  };
+  // the output gradient from the loaded values, into the stage's LDS slot
+  auto pb_store = [&](char* slot) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int cls = j ? 3 - wave : wave, hp = cls >> 1, wp = cls & 1;
+      int dsy, dsx;
+      pix_of(j, dsy, dsx);
+      float zz[8], acc8[8];
+      bf16x8_to_f(pz[j], zz);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) acc8[i] = 0.f;
+#pragma unroll
+      for (int kr = 0; kr < 2; ++kr)
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+          if (kr > hp || ks > wp) continue;  // wave-uniform
+          const int r = hp ? 2 * kr : 1, sw = wp ? 2 * ks : 1, code = r * 3 + sw;
+          float gv[8];
+          bf16x8_to_f(pg[j][2 * kr + ks], gv);
+          const uint2 av = pa[j][2 * kr + ks];
+#pragma unroll
+          for (int i = 0; i < 8; ++i) {
+            const int ai = (int)(((i < 4 ? av.x : av.y) >> (8 * (i & 3))) & 0xFFu);
+            if (ai == code) acc8[i] += gv[i];
+          }
+        }
+      float o[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const float g = (float)(bf16)acc8[i];
+        const float t = __builtin_fmaf(zz[i] - pmu[i], psc[i], pbe[i]);
+        const float gm = (float)(bf16)t > 0.f ? g : 0.f;
+        o[i] = pca[i] * gm + pcb[i] + pcc[i] * (zz[i] - pmu[i]);
+      }
+      const int pix = dsy * 8 + dsx, pos = 2 * ((pu >> 1) ^ (pix & 3)) + (pu & 1);
+      *reinterpret_cast<uint4*>(slot + STEM_WG_X + pix * 128 + pos * 16) =
+          make_uint4(bf16x2_bits(o[0], o[1]), bf16x2_bits(o[2], o[3]), bf16x2_bits(o[4], o[5]),
+                     bf16x2_bits(o[6], o[7]));
+    }
+  };
+
   f32x4 acc[4][4];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
@@ -2064,9 +2195,13 @@ __global__ __launch_bounds__(NT, 2) void wgrad_stem_kernel(StemWgArgs a) {
 
   if (ns > 0) {
     load_x(0);
-    issue_dy(0, smem);
+    if (POOLBWD)
+      pb_load(0);
+    else
+      issue_dy(0, smem);
     wait_vmcnt<0>();
     store_x(smem);
+    if (POOLBWD) pb_store(smem);
   }
   const int gq = lane >> 4, jr = (lane & 15) >> 2, qd = lane & 3;
   for (int st = 0; st < ns; ++st) {
@@ -2075,7 +2210,10 @@ __global__ __launch_bounds__(NT, 2) void wgrad_stem_kernel(StemWgArgs a) {
     char* nslot = smem + ((st + 1) % NST) * STEM_WG_STAGE;
     if (next) {
       load_x(st + 1);
-      issue_dy(st + 1, nslot);
+      if (POOLBWD)
+        pb_load(st + 1);
+      else
+        issue_dy(st + 1, nslot);
     }
     const char* Xs = smem + (st % NST) * STEM_WG_STAGE;
     const char* Bs = Xs + STEM_WG_X;
@@ -2112,6 +2250,7 @@ __global__ __launch_bounds__(NT, 2) void wgrad_stem_kernel(StemWgArgs a) {
     if (next) {
       wait_vmcnt<0>();
       store_x(nslot);  // that slot was last read before this stage's barrier
+      if (POOLBWD) pb_store(nslot);
     }
   }
 
@@ -3268,7 +3407,7 @@ bool stem_wgrad_ok(int dt, const ConvGeom& g, int C0) {
          g.stride == 2 && g.pad == 3 && g.P == (g.H - 1) / 2 + 1 && g.Q == (g.W - 1) / 2 + 1 &&
          g.P >= 1 && g.Q >= 1 && (long long)g.N * g.H * g.W * 8 < (1LL << 40);
 }
-constexpr int STEM_WG_BLOCKS = 256;
+constexpr int STEM_WG_BLOCKS = 512;
 StemWgArgs plan_stem_wgrad(const ConvGeom& g) {
   StemWgArgs a{};
   a.g = g;
@@ -3285,8 +3424,9 @@ size_t stem_wgrad_floats(const ConvGeom& g) {
   return (size_t)(s + conv_update_groups(s)) * 64 * 49 * 4;
 }
 hipError_t stem_wgrad(const ConvGeom& g, const void* x, const void* dy, float* partials, float* dw,
-                      hipStream_t stream) {
+                      hipStream_t stream, const StemPoolBwd* pb = nullptr) {
   StemWgArgs a = plan_stem_wgrad(g);
+  if (pb) a.pb = *pb;
   a.x = (const bf16*)x;
   a.dy = (const bf16*)dy;
   a.out = partials;
@@ -3298,11 +3438,15 @@ hipError_t stem_wgrad(const ConvGeom& g, const void* x, const void* dy, float* p
     e1 = t->take();
     EKYA_HIP(hipEventRecord(e0, stream));
   }
-  hipLaunchKernelGGL(wgrad_stem_kernel, dim3(a.splits), dim3(NT), 0, stream, a);
+  if (pb)
+    hipLaunchKernelGGL(wgrad_stem_kernel<true>, dim3(a.splits), dim3(NT), 0, stream, a);
+  else
+    hipLaunchKernelGGL(wgrad_stem_kernel<false>, dim3(a.splits), dim3(NT), 0, stream, a);
   hipError_t e = hipGetLastError();
   if (t && e == hipSuccess) {
     EKYA_HIP(hipEventRecord(e1, stream));
-    t->recs.push_back({"conv_wgrad<bf16,stem>", cost.flops, cost.bytes, e0, e1});
+    t->recs.push_back({pb ? "conv_wgrad<bf16,stem+pool_bwd>" : "conv_wgrad<bf16,stem>", cost.flops,
+                       cost.bytes, e0, e1});
   }
   EKYA_HIP(e);
   const long long n = 64LL * 49 * 4;
@@ -3412,6 +3556,19 @@ hipError_t conv_dgrad(int dt, const ConvGeom& g, const void* dy, const void* wt,
                       : conv_dgrad_t<bf16>(g, dy, wt, dx, res, ws, ws_floats, stream, sink);
 }
 
+
+bool stem_wgrad_pool_ok(int dt, const ConvGeom& g) { return stem_wgrad_ok(dt, g, 3); }
+
+hipError_t conv_wgrad_stem_pool(const ConvGeom& g, const void* x, const void* z,
+                                const void* dy_pool, const uint8_t* arg, const float* mean,
+                                const float* coef, const float* gamma, const float* invstd,
+                                const float* beta, float* partials, float* dw, hipStream_t stream) {
+  if (!stem_wgrad_pool_ok(DT_BF16, g)) return hipErrorInvalidValue;
+  if (g.N == 0) return hipSuccess;
+  StemPoolBwd pb{(const bf16*)z, (const bf16*)dy_pool, arg, mean, coef, gamma, invstd, beta,
+                 (g.P - 1) / 2 + 1, (g.Q - 1) / 2 + 1};
+  return stem_wgrad(g, x, nullptr, partials, dw, stream, &pb);
+}
 
 hipError_t conv_wgrad(int dt, const ConvGeom& g, const void* x, const void* dy, float* partials,
                       float* dw, int C0, hipStream_t stream) {

@@ -2177,24 +2177,26 @@ bool bn_backward_pool_ok(int C, int H, int W) {
   return C == POOLBN_C && W <= 2 * POOLBN_QMAX && H >= 1 && W >= 1;
 }
 
-hipError_t bn_backward_pool(int dt, const void* dy_pool, const uint8_t* arg, const void* z, int N,
-                            int H, int W, int C, const float* gamma, const float* beta,
-                            const float* mean, const float* invstd, float* dgamma, float* dbeta,
-                            void* dz, float* partials, hipStream_t stream) {
+hipError_t bn_backward_pool_stats(int dt, const void* dy_pool, const uint8_t* arg, const void* z,
+                                  int N, int H, int W, int C, const float* gamma, const float* beta,
+                                  const float* mean, const float* invstd, float* dgamma,
+                                  float* dbeta, float* partials, const float** coef_out,
+                                  hipStream_t stream) {
   const long long M = (long long)N * H * W;
+  *coef_out = partials;
   if (M == 0) return hipSuccess;
   if (M >= (1LL << 31) || !bn_backward_pool_ok(C, H, W)) return hipErrorInvalidValue;
   const int P = (H - 1) / 2 + 1, Q = (W - 1) / 2 + 1;
   const PoolSrc ps{dy_pool, arg, H, W, P, Q};
   const int pairs = N * P;
   // at most as many partial rows as bn_partials_floats(M, C) provides
-  // at most as many partial rows as bn_partials_floats(M, C) provides
   const int rp = cdiv(pairs, bn_chunks(M, C)), nch = cdiv(pairs, rp);
   float* coef = partials + (size_t)nch * 2 * C;
+  *coef_out = coef;
   const size_t es = dtype_size(dt);
   const double act = (double)M * C * es, pooled = (double)N * P * Q * C * (es + 1);
   TimedLaunch ts(stream);  // z; the pooled gradient and its window indices
-  hipError_t e = ts.done(by_type(dt, [&](auto* tp) {
+  return ts.done(by_type(dt, [&](auto* tp) {
     using T = std::remove_pointer_t<decltype(tp)>;
     hipLaunchKernelGGL((bn_bwd_pool_kernel<T, true>), dim3(nch), dim3(256), 0, stream, ps,
                        (const T*)z, N, rp, mean, (const float*)nullptr, gamma, invstd, beta,
@@ -2202,7 +2204,23 @@ hipError_t bn_backward_pool(int dt, const void* dy_pool, const uint8_t* arg, con
     hipLaunchKernelGGL(bn_bwd_final, dim3(cdiv(C, FIN_CH)), dim3(256), 0, stream, partials, nch, M, C,
                        gamma, invstd, dgamma, dbeta, coef);
   }), "bn_bwd_pool_stats", act + pooled);
+}
+
+hipError_t bn_backward_pool(int dt, const void* dy_pool, const uint8_t* arg, const void* z, int N,
+                            int H, int W, int C, const float* gamma, const float* beta,
+                            const float* mean, const float* invstd, float* dgamma, float* dbeta,
+                            void* dz, float* partials, hipStream_t stream) {
+  const long long M = (long long)N * H * W;
+  if (M == 0) return hipSuccess;
+  const float* coef = nullptr;
+  hipError_t e = bn_backward_pool_stats(dt, dy_pool, arg, z, N, H, W, C, gamma, beta, mean, invstd,
+                                        dgamma, dbeta, partials, &coef, stream);
   if (e != hipSuccess) return e;
+  const int P = (H - 1) / 2 + 1, Q = (W - 1) / 2 + 1;
+  const PoolSrc ps{dy_pool, arg, H, W, P, Q};
+  const int pairs = N * P;
+  const size_t es = dtype_size(dt);
+  const double act = (double)M * C * es, pooled = (double)N * P * Q * C * (es + 1);
   TimedLaunch ta(stream);  // z and the pooled gradient read, dz written
   return ta.done(by_type(dt, [&](auto* tp) {
     using T = std::remove_pointer_t<decltype(tp)>;

@@ -127,6 +127,17 @@ size_t conv_wgrad_workspace_floats(int dt, const ConvGeom& g);
 // dy x im2col(x); deterministic split-K through `partials`.
 hipError_t conv_wgrad(int dt, const ConvGeom& g, const void* x, const void* dy, float* partials,
                       float* dw, int C0, hipStream_t stream);
+// The bf16 stem's weight gradient (as conv_wgrad with C0 = 3) whose output
+// gradient is the stem's BatchNorm + ReLU + 3x3/2 max-pool backward, formed
+// while it is staged: z the BatchNorm input [N][P][Q][64], dy_pool / arg the
+// pooled gradient and window indices, mean and coef (bn_backward_pool_stats)
+// its coefficients, gamma, invstd and beta the ReLU mask's.  The same values
+// as bn_backward_pool followed by conv_wgrad, without dz in memory.
+bool stem_wgrad_pool_ok(int dt, const ConvGeom& g);
+hipError_t conv_wgrad_stem_pool(const ConvGeom& g, const void* x, const void* z,
+                                const void* dy_pool, const uint8_t* arg, const float* mean,
+                                const float* coef, const float* gamma, const float* invstd,
+                                const float* beta, float* partials, float* dw, hipStream_t stream);
 // The weight gradient left as fp32 split partials [splits][K][R][S][C] (one
 // split included) for conv_weight_update: bf16 with C and K multiples of 64.
 // conv_wgrad_partials_floats includes the scratch conv_weight_update needs
@@ -198,6 +209,15 @@ hipError_t bn_backward_pool(int dt, const void* dy_pool, const uint8_t* arg, con
                             int H, int W, int C, const float* gamma, const float* beta,
                             const float* mean, const float* invstd, float* dgamma, float* dbeta,
                             void* dz, float* partials, hipStream_t stream);
+// Its statistics pass alone: dgamma, dbeta and the input-gradient
+// coefficients dz = coef[c] * g + coef[C + c] + coef[2 C + c] * (z - mean),
+// *coef pointing into `partials`, for a consumer that forms dz itself
+// (conv_wgrad_stem_pool).
+hipError_t bn_backward_pool_stats(int dt, const void* dy_pool, const uint8_t* arg, const void* z,
+                                  int N, int H, int W, int C, const float* gamma, const float* beta,
+                                  const float* mean, const float* invstd, float* dgamma,
+                                  float* dbeta, float* partials, const float** coef,
+                                  hipStream_t stream);
 
 // ------------------------------------------------------------------ pooling
 // Train-mode BatchNorm statistics of z [N, H, W, C] (as bn_train_stats),

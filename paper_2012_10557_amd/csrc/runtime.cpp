@@ -939,6 +939,19 @@ static hipError_t train_backward(TrainJob& j, int nb, const int32_t* fid, float*
         EKYA_HIP(bn_bwd_relu(net.conv[0].bn, gA, j.stem_Z, M, j.gz1[par], 0));
       } else {  // the pool's backward gathered inside the BatchNorm backward
         const BnL& b = net.bn[net.conv[0].bn];
+        const ConvGeom cg = conv_geom(net, j.geo, 0, nb);
+        if (stem_wgrad_pool_ok(dt, cg)) {
+          // the weight gradient forms the stem's output gradient itself
+          const float* coef = nullptr;
+          EKYA_HIP(bn_backward_pool_stats(dt, dout, j.stem_arg, j.stem_Z, nb, j.geo.sh, j.geo.sw,
+                                          64, j.master + b.g, j.master + b.b, bnp(j.bn_mean, b),
+                                          bnp(j.bn_invstd, b), j.grad + b.g, j.grad + b.b,
+                                          j.bn_ws, &coef, st));
+          EKYA_HIP(conv_wgrad_stem_pool(cg, j.x0, j.stem_Z, dout, j.stem_arg, bnp(j.bn_mean, b),
+                                        coef, j.master + b.g, bnp(j.bn_invstd, b),
+                                        j.master + b.b, j.ws, j.grad + net.conv[0].off, st));
+          break;
+        }
         EKYA_HIP(bn_backward_pool(dt, dout, j.stem_arg, j.stem_Z, nb, j.geo.sh, j.geo.sw, 64,
                                   j.master + b.g, j.master + b.b, bnp(j.bn_mean, b),
                                   bnp(j.bn_invstd, b), j.grad + b.g, j.grad + b.b, j.gz1[par],
