@@ -3269,12 +3269,13 @@ struct WgDmaPlan {
   TapGeom tap;  // tap.splits > 0: the all-taps kernel (3x3, stride 1)
 };
 bool wgrad_dma_ok(int dt, const ConvGeom& g) { return dt == DT_BF16 && g.C % 64 == 0 && g.K % 64 == 0; }
-// Blocks the all-taps weight gradient aims for: one per CU, or one per two
-// CUs when it runs beside the data-gradient chain on another stream (more
-// measured slower there: the chain on the critical path then waits for CUs
-// and bandwidth the weight gradient holds).
+// Blocks the all-taps weight gradient aims for: one per CU, or 96 when it
+// runs beside the data-gradient chain on another stream (measured on the
+// full-depth batch-128 step: 128 blocks 0.6% and 64 blocks 3% slower, 256
+// slower still -- the chain on the critical path waits for the CUs and
+// bandwidth the weight gradient holds, or for the weight gradient itself).
 constexpr int TAP_TARGET_BLOCKS = 256;
-constexpr int TAP_SHARED_BLOCKS = 128;
+constexpr int TAP_SHARED_BLOCKS = 96;
 bool wgrad_tap_ok(const ConvGeom& g) {
   return g.R == 3 && g.S == 3 && g.stride == 1 && g.pad == 1 && g.P == g.H && g.Q == g.W &&
          g.C % 64 == 0 && g.K % 64 == 0 && (long long)g.N * g.H * g.W * g.C < (1LL << 40) &&

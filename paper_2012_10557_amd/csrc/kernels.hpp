@@ -145,7 +145,7 @@ hipError_t conv_wgrad_stem_pool(const ConvGeom& g, const void* x, const void* z,
 bool conv_wgrad_partials_ok(int dt, const ConvGeom& g);
 size_t conv_wgrad_partials_floats(int dt, const ConvGeom& g);
 // shared: the launch runs beside other work on another stream (the
-// all-taps kernel then takes about half the CUs; fewer splits).
+// all-taps kernel then takes about 96 blocks, under half the CUs).
 hipError_t conv_wgrad_partials(int dt, const ConvGeom& g, const void* x, const void* dy,
                                float* partials, int* splits, hipStream_t stream,
                                bool shared = false);
