@@ -1715,9 +1715,16 @@ static hipError_t infer_frames(const Net& net, const Geo& geo, const float* mast
   for (int i0 = 0; i0 < n; i0 += per) {
     const int cnt = std::min(per, n - i0);
     const void* src = reinterpret_cast<const char*>(frames) + i0 * fbytes;
-    if (resolution == H && resolution == W && stem_frames_ok(net.dt, conv_geom(net, geo, 0, cnt))) {
+    const bool raw_ok = stem_frames_ok(net.dt, conv_geom(net, geo, 0, cnt));
+    if (resolution == H && resolution == W && raw_ok) {
       EKYA_HIP(eval_forward(net, geo, shadow, fold, master, 0, 5, src, cnt, eb, eb.logits, stream,
                             true));  // the stem reads the frames
+    } else if (raw_ok) {
+      // resized to 3-channel frames, which the stem reads as it reads the
+      // originals (the same staged bytes as an 8-channel padded copy)
+      EKYA_HIP(resize_to_padded(net.dt, src, cnt, H, W, resolution, 3, ib.padded, stream));
+      EKYA_HIP(eval_forward(net, geo, shadow, fold, master, 0, 5, ib.padded, cnt, eb, eb.logits,
+                            stream, true));
     } else {
       if (resolution == H && resolution == W)
         EKYA_HIP(frames_to_padded(net.dt, src, nullptr, cnt, H, W, net.conv[0].cin_pad, ib.padded,
