@@ -863,6 +863,11 @@ struct DmaDgradOp {
 // belongs to class ct mod 4 (so every range of tiles mixes the light and
 // heavy classes), class-local column (ct / 4) * BN + offset.  A class with no
 // taps (1x1 kernels, odd pixels) writes zeros (plus the residual).
+// With dy2: a 1x1 / stride-2 / pad-0 convolution on the same input (a
+// projection shortcut) adds its data gradient, which reaches only the class
+// (0, 0) pixels (2 i, 2 j): from its output-gradient pixel (i, j), the same
+// pixel as that class's single 3x3 tap (pad 1) -- so the class's reduction
+// runs K2 / 64 more stages over [dy2 | wt2] and no residual is read.
 struct DmaDgradS2Args {
   ConvGeom g;
   const bf16* dy;
@@ -872,6 +877,9 @@ struct DmaDgradS2Args {
   SplitOut so;
   int tiles_m, tiles_n;
   BnEpi bn;        // unused (no BatchNorm-statistics epilogue on this path)
+  const bf16* dy2 = nullptr;  // shortcut output gradient [N][P][Q][K2]
+  const bf16* wt2 = nullptr;  // shortcut weights [C][1][1][K2]
+  int K2 = 0;
 };
 
 struct S2Class {
@@ -897,17 +905,23 @@ struct DmaDgradS2Op {
   int s_begin, s_end;
   long long Ktot;
   const bf16* ptr[IPW];
+  const bf16* ptr2[IPW];  // the shortcut's operands (class (0, 0) with dy2)
   int pi[IPW], qj[IPW];  // output-gradient pixel of the class's first tap (r0, s0)
   bool ok[IPW];
   int tr, ts, tk;        // tap (r0 + 2 tr, s0 + 2 ts), channel offset
-  int r0, s0, nsc;
+  int r0, s0, nr, nsc;
+  bool ext;              // in the shortcut's stages
   int split;
 
-  // reduction stages [s0, s1) of a split: 64-element steps over the class's
-  // taps x K
+  // stages of a column tile's class: 64-element steps over the class's taps
+  // x K, then (class (0, 0) with dy2) over K2
+  static __device__ int class_stages(const Args& a, int ct) {
+    const S2Class k = s2_class(a.g, ct & 3);
+    return k.nr * k.nsc * a.g.K / 64 + ((ct & 3) == 0 && a.dy2 ? a.K2 / 64 : 0);
+  }
+  // reduction stages [s0, s1) of a split
   static __device__ void stage_range(const Args& a, int split, int n0, int& s0, int& s1) {
-    const S2Class k = s2_class(a.g, (n0 / BN) & 3);
-    const int ns = k.nr * k.nsc * a.g.K / 64;
+    const int ns = class_stages(a, n0 / BN);
     s0 = min(ns, split * a.so.stages_per_split);
     s1 = min(ns, s0 + a.so.stages_per_split);
   }
@@ -921,7 +935,9 @@ struct DmaDgradS2Op {
     const S2Class k = s2_class(g, ct & 3);
     r0 = k.r0;
     s0 = k.s0;
+    nr = k.nr;
     nsc = k.nsc;
+    const bool sc = (ct & 3) == 0 && a.dy2;
     const int mc = g.N * k.hc * k.wc, lbase = (ct >> 2) * BN;
     const int r8 = lane >> 3, u = (lane & 7) ^ r8;
 #pragma unroll
@@ -931,6 +947,7 @@ struct DmaDgradS2Op {
         const int row = m0 + oct * 8 + r8;
         ok[j] = row < g.C;
         ptr[j] = a.wt + (ok[j] ? row : 0) * Ktot + u * 8;
+        ptr2[j] = sc ? a.wt2 + (long long)(ok[j] ? row : 0) * a.K2 + u * 8 : a.wt;
         pi[j] = qj[j] = 0;
       } else {
         const int l = lbase + (oct - GA) * 8 + r8;
@@ -941,17 +958,42 @@ struct DmaDgradS2Op {
         pi[j] = i + (k.ph + g.pad - k.r0) / 2;
         qj[j] = jj + (k.pw + g.pad - k.s0) / 2;
         ptr[j] = a.dy + (long long)n * g.P * g.Q * g.K + u * 8;
+        ptr2[j] = sc ? a.dy2 + (long long)n * g.P * g.Q * a.K2 + u * 8 : a.dy;
       }
     }
-    const int k0 = s_begin * 64;
-    const int rs = k0 / g.K;
-    tk = k0 - rs * g.K;
-    tr = rs / max(nsc, 1);
-    ts = rs - tr * max(nsc, 1);
+    const int k0 = s_begin * 64, kmain = nr * nsc * g.K;
+    ext = k0 >= kmain;
+    if (ext) {
+      tk = k0 - kmain;
+      tr = ts = 0;
+    } else {
+      const int rs = k0 / g.K;
+      tk = k0 - rs * g.K;
+      tr = rs / max(nsc, 1);
+      ts = rs - tr * max(nsc, 1);
+    }
   }
   __device__ void issue(const Args& a, int st, uint4* slot, int wave, const void* zero) {
     const ConvGeom& g = a.g;
     (void)st;
+    if (ext) {
+      // the shortcut: output-gradient pixel (i, j) = the class's tap pixel
+#pragma unroll
+      for (int j = 0; j < IPW; ++j) {
+        const int oct = wave + 4 * j;
+        const void* src;
+        if (oct < GA) {
+          src = ok[j] ? (const void*)(ptr2[j] + tk) : zero;
+        } else {
+          const int p = pi[j], q = qj[j];
+          const bool in = ok[j] && (unsigned)p < (unsigned)g.P && (unsigned)q < (unsigned)g.Q;
+          src = in ? (const void*)(ptr2[j] + ((p * g.Q + q) * a.K2 + tk)) : zero;
+        }
+        dma16(src, slot + oct * 64);
+      }
+      tk += 64;
+      return;
+    }
     const int woff = ((r0 + 2 * tr) * g.S + (s0 + 2 * ts)) * g.K + tk;
 #pragma unroll
     for (int j = 0; j < IPW; ++j) {
@@ -971,7 +1013,7 @@ struct DmaDgradS2Op {
       tk = 0;
       if (++ts == nsc) {
         ts = 0;
-        ++tr;
+        if (++tr == nr) ext = true;  // (tk = 0: the shortcut's first stage)
       }
     }
   }
@@ -3058,13 +3100,15 @@ hipError_t conv_fwd_dma(const ConvGeom& g, const void* x, const void* w, void* y
 // Stride-2 bf16 data gradient by parity class (DmaDgradS2Op): the GEMM plan
 // is chosen for the average reduction length (a quarter of the taps); the
 // split length covers the longest class.
-DmaPlan plan_dgrad_s2(const ConvGeom& g, bool allow_split) {
+// k2: channels of a folded shortcut (class (0, 0) only), 0 for none
+DmaPlan plan_dgrad_s2(const ConvGeom& g, bool allow_split, int k2 = 0) {
   const int kc = g.K / 64;
   int ns_max = 0, ns_sum = 0;
   for (int c = 0; c < 4; ++c) {
     const S2Class k = s2_class(g, c);
-    ns_max = std::max(ns_max, k.nr * k.nsc * kc);
-    ns_sum += k.nr * k.nsc * kc;
+    const int ns = k.nr * k.nsc * kc + (c == 0 ? k2 / 64 : 0);
+    ns_max = std::max(ns_max, ns);
+    ns_sum += ns;
   }
   const long long npix = (long long)g.N * g.H * g.W;
   DmaPlan p = plan_dma(g.C, npix, std::max(1, cdiv(ns_sum, 4)), allow_split);
@@ -3074,10 +3118,11 @@ DmaPlan plan_dgrad_s2(const ConvGeom& g, bool allow_split) {
 }
 
 hipError_t conv_dgrad_s2(const ConvGeom& g, const void* dy, const void* wt, void* dx,
-                         const void* res, float* ws, size_t ws_floats, hipStream_t stream) {
+                         const void* res, float* ws, size_t ws_floats, hipStream_t stream,
+                         const void* dy2 = nullptr, const void* wt2 = nullptr, int K2 = 0) {
   const long long npix = (long long)g.N * g.H * g.W;
-  DmaPlan p = plan_dgrad_s2(g, ws != nullptr);
-  if (p.splits > 1 && (size_t)p.splits * npix * g.C > ws_floats) p = plan_dgrad_s2(g, false);
+  DmaPlan p = plan_dgrad_s2(g, ws != nullptr, K2);
+  if (p.splits > 1 && (size_t)p.splits * npix * g.C > ws_floats) p = plan_dgrad_s2(g, false, K2);
   long long ctiles = 0;
   for (int c = 0; c < 4; ++c) {
     const S2Class k = s2_class(g, c);
@@ -3086,8 +3131,16 @@ hipError_t conv_dgrad_s2(const ConvGeom& g, const void* dy, const void* wt, void
   const long long cols = 4 * ctiles * p.bn;
   DmaDgradS2Args a{g, (const bf16*)dy, (const bf16*)wt, (bf16*)dx, (const bf16*)res,
                    SplitOut{ws, p.splits, p.sps}, 0, 0, BnEpi{}};
-  hipError_t e = dispatch_dma<DmaDgradS2Op>(a, p, cols, g.C, stream,
-                                           conv_cost(g, g.C, sizeof(bf16), false), "conv_dgrad_s2");
+  Cost cost = conv_cost(g, g.C, sizeof(bf16), false);
+  if (dy2) {
+    a.dy2 = (const bf16*)dy2;
+    a.wt2 = (const bf16*)wt2;
+    a.K2 = K2;
+    cost.flops += 2.0 * g.N * g.P * g.Q * (double)K2 * g.C;
+    cost.bytes += ((double)g.N * g.P * g.Q * K2 + (double)K2 * g.C) * sizeof(bf16);
+  }
+  hipError_t e = dispatch_dma<DmaDgradS2Op>(a, p, cols, g.C, stream, cost,
+                                           dy2 ? "conv_dgrad_s2+shortcut" : "conv_dgrad_s2");
   if (e != hipSuccess || p.splits <= 1) return e;
   ConvEpilogue ep;
   ep.res = res;
@@ -3546,6 +3599,21 @@ hipError_t conv_fwd(int dt, const ConvGeom& g, const void* x, const void* w, voi
   if (g.N * g.P * g.Q == 0) return hipSuccess;
   return dt == DT_F32 ? conv_fwd_t<float>(g, x, w, y, epi, ws, ws_floats, stream, sink)
                       : conv_fwd_t<bf16>(g, x, w, y, epi, ws, ws_floats, stream, sink);
+}
+
+bool conv_dgrad_s2_shortcut_ok(int dt, const ConvGeom& g, const ConvGeom& gs) {
+  return dt == DT_BF16 && g.stride == 2 && g.R == 3 && g.S == 3 && g.pad == 1 &&
+         g.K % 64 == 0 && g.C % 64 == 0 && gs.stride == 2 && gs.R == 1 && gs.S == 1 &&
+         gs.pad == 0 && gs.K % 64 == 0 && gs.N == g.N && gs.H == g.H && gs.W == g.W &&
+         gs.C == g.C && gs.P == g.P && gs.Q == g.Q;
+}
+
+hipError_t conv_dgrad_s2_shortcut(const ConvGeom& g, const void* dy, const void* wt,
+                                  const ConvGeom& gs, const void* dy_sc, const void* wt_sc,
+                                  void* dx, float* ws, size_t ws_floats, hipStream_t stream) {
+  if (!conv_dgrad_s2_shortcut_ok(DT_BF16, g, gs) || !dy_sc || !wt_sc) return hipErrorInvalidValue;
+  if (g.N * g.H * g.W == 0) return hipSuccess;
+  return conv_dgrad_s2(g, dy, wt, dx, nullptr, ws, ws_floats, stream, dy_sc, wt_sc, gs.K);
 }
 
 hipError_t conv_dgrad(int dt, const ConvGeom& g, const void* dy, const void* wt, void* dx,

@@ -118,6 +118,15 @@ hipError_t conv_dgrad(int dt, const ConvGeom& g, const void* dy, const void* w_c
                       const void* res, float* ws, size_t ws_floats, hipStream_t stream,
                       BnStatsSink* sink = nullptr);
 size_t conv_split_workspace_floats(int dt, const ConvGeom& g, bool dgrad);
+// The bf16 data gradient of a 3x3 / stride-2 / pad-1 convolution g plus that
+// of a 1x1 / stride-2 / pad-0 convolution gs on the same input (a projection
+// shortcut; dy_sc its output gradient, wt_sc its weights [C][1][1][K2]) in
+// one launch: dx = dgrad(g) + dgrad(gs), the shortcut's part folded into the
+// reduction of the pixels (2 i, 2 j) it reaches.  No residual.
+bool conv_dgrad_s2_shortcut_ok(int dt, const ConvGeom& g, const ConvGeom& gs);
+hipError_t conv_dgrad_s2_shortcut(const ConvGeom& g, const void* dy, const void* wt,
+                                  const ConvGeom& gs, const void* dy_sc, const void* wt_sc,
+                                  void* dx, float* ws, size_t ws_floats, hipStream_t stream);
 // Split count and partial-buffer size (floats) the weight gradient will use;
 // g.C0 must be the real channel count later passed to conv_wgrad as C0 (the
 // bf16 stem, 3 channels stored as 8, has its own kernel and scratch).

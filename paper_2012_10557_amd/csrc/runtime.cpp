@@ -521,7 +521,9 @@ struct TrainJob {
   int ckpt_every = 0;
 };
 
-static_assert(3 * 8 + 1 <= TrainJob::kForks / 2, "fork events for a full-depth backward pass");
+// three forks per residual block, one more per projection shortcut whose
+// data gradient is folded into conv1's, the end join
+static_assert(3 * 8 + 3 + 1 <= TrainJob::kForks / 2, "fork events for a full-depth backward pass");
 
 static size_t ws_floats(const TrainJob& j) {
   const Net& net = *j.net;
@@ -982,12 +984,20 @@ static hipError_t train_backward(TrainJob& j, int nb, const int32_t* fid, float*
       // After each fork the data-gradient work is queued on st before the
       // weight-gradient work on st2, so the critical chain is dispatched first.
       EKYA_HIP(fork());
+      // a projection shortcut beside a stride-2 conv1: its data gradient is
+      // folded into conv1's (no full-size partial gradient in between),
+      // unless conv1's data gradient has to leave the next block's
+      // BatchNorm statistics (the small-batch path)
+      const bool next_sink = bi > 0 && net.blk[bi - 1].stage >= j.lowest;
+      const ConvGeom gd = b.cd >= 0 ? conv_geom(net, j.geo, b.cd, nb) : g1;
+      const bool fold_sc = b.cd >= 0 && need_dx && conv_dgrad_s2_shortcut_ok(dt, g1, gd) &&
+                           !(next_sink && bn_fold_path((long long)nb * g1.H * g1.W, g1.C));
       const void* dx_sc = gG;
-      if (b.cd >= 0 && need_dx) EKYA_HIP(dgrad(b.cd, gZd, dnext, nullptr, nb, nullptr));
+      if (b.cd >= 0 && need_dx && !fold_sc) EKYA_HIP(dgrad(b.cd, gZd, dnext, nullptr, nb, nullptr));
       if (b.cd >= 0) dx_sc = dnext;
       BnStatsSink sk1 = sink_for(net.conv[b.c1].bn, t.A1, t.Z1);
       EKYA_HIP(dgrad(b.c2, gZ2, gA, nullptr, nb, &sk1));
-      if (b.cd >= 0) EKYA_HIP(wgrad(b.cd, t.X, gZd, false, need_dx));
+      if (b.cd >= 0 && !fold_sc) EKYA_HIP(wgrad(b.cd, t.X, gZd, false, need_dx));
       EKYA_HIP(wgrad(b.c2, t.A1, gZ2, false, true));
       EKYA_HIP(bn_bwd(net.conv[b.c1].bn, gA, t.A1, t.Z1, M, gZ1, nullptr, sk1.done ? sk1.rows : 0));
       if (need_dx) {
@@ -995,12 +1005,22 @@ static hipError_t train_backward(TrainJob& j, int nb, const int32_t* fid, float*
         // dOut of the block processed next (bi - 1): its conv2 BatchNorm's statistics
         BnStatsSink skn;
         BnStatsSink* psk = nullptr;
-        if (bi > 0 && net.blk[bi - 1].stage >= j.lowest) {
+        if (next_sink) {
           const BlockL& nbk = net.blk[bi - 1];
           skn = sink_for(net.conv[nbk.c2].bn, j.acts[bi - 1].OUT, j.acts[bi - 1].Z2);
           psk = &skn;
         }
-        EKYA_HIP(dgrad(b.c1, gZ1, dnext, dx_sc, nb, psk));
+        if (fold_sc) {
+          EKYA_HIP(conv_dgrad_s2_shortcut(g1, gZ1, shadow_at(net, j.shadow, net.conv[b.c1].sh_crsk),
+                                          gd, gZd, shadow_at(net, j.shadow, net.conv[b.cd].sh_crsk),
+                                          dnext, j.ws, j.ws_floats, st));
+          // the shortcut's weights are read up to here: its weight gradient
+          // and momentum step go on st2 only after a fork behind that launch
+          EKYA_HIP(fork());
+          EKYA_HIP(wgrad(b.cd, t.X, gZd, false, false));
+        } else {
+          EKYA_HIP(dgrad(b.c1, gZ1, dnext, dx_sc, nb, psk));
+        }
         dout_ready = (psk && psk->done) ? psk->rows : 0;
       } else if (deferred >= 0) {
         // no later work on st reads the conv2 weights: the deferred momentum
