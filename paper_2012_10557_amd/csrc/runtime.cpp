@@ -999,7 +999,13 @@ static hipError_t train_backward(TrainJob& j, int nb, const int32_t* fid, float*
       EKYA_HIP(dgrad(b.c2, gZ2, gA, nullptr, nb, &sk1));
       if (b.cd >= 0 && !fold_sc) EKYA_HIP(wgrad(b.cd, t.X, gZd, false, need_dx));
       EKYA_HIP(wgrad(b.c2, t.A1, gZ2, false, true));
-      EKYA_HIP(bn_bwd(net.conv[b.c1].bn, gA, t.A1, t.Z1, M, gZ1, nullptr, sk1.done ? sk1.rows : 0));
+      // conv1's BatchNorm + ReLU has no residual: its ReLU mask is recomputed
+      // from Z1 (exactly the stored A1 > 0) instead of reading A1, unless the
+      // statistics were already taken with A1 in conv2's data gradient
+      if (sk1.done)
+        EKYA_HIP(bn_bwd(net.conv[b.c1].bn, gA, t.A1, t.Z1, M, gZ1, nullptr, sk1.rows));
+      else
+        EKYA_HIP(bn_bwd_relu(net.conv[b.c1].bn, gA, t.Z1, M, gZ1, 0));
       if (need_dx) {
         EKYA_HIP(fork());
         // dOut of the block processed next (bi - 1): its conv2 BatchNorm's statistics
