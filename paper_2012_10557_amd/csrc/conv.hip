@@ -2013,8 +2013,9 @@ __global__ __launch_bounds__(TAPW_NT) void wgrad_tapw_kernel(WgTapArgs a) {
 // channels 0-3, the fourth a zero pad) and reduces over 8 x 8 patches of output
 // pixels.  A stage stages the patch's 22 x 22 input pixels (channels 0-3,
 // 8 bytes, through registers; rows of 24 pixels) and its 64 output-gradient
-// pixels (128-byte rows, direct copies, segments swizzled as in the all-taps
-// kernel).  Taps are taken in 2 x 2 blocks (r and s from 0 to 7; taps 7
+// pixels (128-byte rows, direct copies -- or, with the pooled BatchNorm
+// backward folded in, computed and stored by the waves -- segments swizzled as
+// in the all-taps kernel).  Taps are taken in 2 x 2 blocks (r and s from 0 to 7; taps 7
 // compute into discarded rows): a 16-row MFMA tile is 4 taps x 4 channels,
 // its transpose read has member m supply pixel m / 4 of tap m % 4, and with
 // rows of 24 pixels the 16 members' 8-byte slots differ modulo 128 bytes
@@ -3461,6 +3462,8 @@ bool stem_wgrad_ok(int dt, const ConvGeom& g, int C0) {
          g.stride == 2 && g.pad == 3 && g.P == (g.H - 1) / 2 + 1 && g.Q == (g.W - 1) / 2 + 1 &&
          g.P >= 1 && g.Q >= 1 && (long long)g.N * g.H * g.W * 8 < (1LL << 40);
 }
+// two blocks per CU: with the pooled BatchNorm backward folded in, one
+// block's gradient arithmetic overlaps the other's MFMAs
 constexpr int STEM_WG_BLOCKS = 512;
 StemWgArgs plan_stem_wgrad(const ConvGeom& g) {
   StemWgArgs a{};
