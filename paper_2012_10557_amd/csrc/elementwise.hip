@@ -84,14 +84,6 @@ __device__ __forceinline__ void apply_mask(const float (&sc)[E], const float (&b
     g[i] = to_f((T)t) > 0.f ? g[i] : 0.f;
   }
 }
-template <typename T, int E>
-__device__ __forceinline__ void mask_from_z(const float* gamma, const float* invstd,
-                                            const float* mb, int c0, const float (&mu)[E],
-                                            const float (&zz)[E], float (&g)[E]) {
-  float sc[E], be[E];
-  mask_coef<E>(gamma, invstd, mb, c0, sc, be);
-  apply_mask<T, E>(sc, be, mu, zz, g);
-}
 
 // --------------------------------------------------------- BN statistics
 // Per chunk of rows: shifted sums S1 = sum(z - K), S2 = sum((z - K)^2) with the
@@ -227,29 +219,53 @@ __global__ __launch_bounds__(256) void bn_stats_final(const T* z, const float* p
   }
 }
 
-template <typename T>
-__global__ void bn_apply_kernel(const T* z, long long units, int C, const float* mean,
-                                const float* scale, const float* beta, const T* res, int relu,
-                                T* y) {
+// One thread takes units u0, u0 + S, u0 + 2S, ... (S the grid's thread
+// count).  SAME: S is a multiple of the C / E units of a row, so all of a
+// thread's units hold the same channels and their coefficients are loaded
+// once.  The loads of BN_AU units are issued before any is used.
+constexpr int BN_AU = 2;
+template <typename T, bool SAME>
+__global__ __launch_bounds__(256) void bn_apply_kernel(const T* z, long long units, int C,
+                                                       const float* mean, const float* scale,
+                                                       const float* beta, const T* res, int relu,
+                                                       T* y) {
   constexpr int E = Elt<T>::E;
-  for (long long u = blockIdx.x * (long long)blockDim.x + threadIdx.x; u < units;
-       u += (long long)gridDim.x * blockDim.x) {
-    const int c0 = (int)((u * E) % C);
-    float v[E], r[E], mu[E], sc[E], be[E];
-    unit_to_f<T>(reinterpret_cast<const uint4*>(z)[u], v);
-    if (res) unit_to_f<T>(reinterpret_cast<const uint4*>(res)[u], r);
+  const long long S = (long long)gridDim.x * blockDim.x;
+  const long long u0 = blockIdx.x * (long long)blockDim.x + threadIdx.x;
+  float mu[E], sc[E], be[E];
+  auto coefs = [&](int c0) {
     chan_load<E>(mean, c0, mu);
     chan_load<E>(scale, c0, sc);
     chan_load<E>(beta, c0, be);
+  };
+  if (SAME) coefs((int)((u0 * E) % C));
+  for (long long u = u0; u < units; u += BN_AU * S) {
+    uint4 rv[BN_AU], rr[BN_AU];
 #pragma unroll
-    for (int i = 0; i < E; ++i) {
-      // (z - mean) * scale + beta: no cancellation when invstd is large
-      float t = __builtin_fmaf(v[i] - mu[i], sc[i], be[i]);
-      if (res) t += r[i];
-      if (relu) t = relu_nan(t);
-      v[i] = t;
+    for (int q = 0; q < BN_AU; ++q) {
+      const long long uq = u + q * S;
+      const bool in = uq < units;
+      rv[q] = in ? reinterpret_cast<const uint4*>(z)[uq] : uint4{0, 0, 0, 0};
+      rr[q] = (in && res) ? reinterpret_cast<const uint4*>(res)[uq] : uint4{0, 0, 0, 0};
     }
-    reinterpret_cast<uint4*>(y)[u] = f_to_unit<T>(v);
+#pragma unroll
+    for (int q = 0; q < BN_AU; ++q) {
+      const long long uq = u + q * S;
+      if (uq >= units) break;
+      if (!SAME) coefs((int)((uq * E) % C));
+      float v[E], r[E];
+      unit_to_f<T>(rv[q], v);
+      if (res) unit_to_f<T>(rr[q], r);
+#pragma unroll
+      for (int i = 0; i < E; ++i) {
+        // (z - mean) * scale + beta: no cancellation when invstd is large
+        float t = __builtin_fmaf(v[i] - mu[i], sc[i], be[i]);
+        if (res) t += r[i];
+        if (relu) t = relu_nan(t);
+        v[i] = t;
+      }
+      reinterpret_cast<uint4*>(y)[uq] = f_to_unit<T>(v);
+    }
   }
 }
 
@@ -833,34 +849,56 @@ __global__ __launch_bounds__(256) void bn_bwd_final(const float* part, int nchun
   coef[2 * C + c] = -a * is * dg / (float)M;
 }
 
-template <typename T>
-__global__ void bn_bwd_apply(const T* dy, const T* y, const T* z, long long units, int C,
-                             const float* mean, const float* coef, const float* gamma,
-                             const float* invstd, const float* mb, T* dz, T* g_out) {
+// Units per thread as in bn_apply_kernel.
+template <typename T, bool SAME>
+__global__ __launch_bounds__(256) void bn_bwd_apply(const T* dy, const T* y, const T* z,
+                                                    long long units, int C, const float* mean,
+                                                    const float* coef, const float* gamma,
+                                                    const float* invstd, const float* mb, T* dz,
+                                                    T* g_out) {
   constexpr int E = Elt<T>::E;
-  for (long long u = blockIdx.x * (long long)blockDim.x + threadIdx.x; u < units;
-       u += (long long)gridDim.x * blockDim.x) {
-    const int c0 = (int)((u * E) % C);
-    float g[E], zz[E];
-    unit_to_f<T>(reinterpret_cast<const uint4*>(dy)[u], g);
-    unit_to_f<T>(reinterpret_cast<const uint4*>(z)[u], zz);
-    float o[E], ca[E], cb[E], cc[E], mu[E];
+  const long long S = (long long)gridDim.x * blockDim.x;
+  const long long u0 = blockIdx.x * (long long)blockDim.x + threadIdx.x;
+  float mu[E], ca[E], cb[E], cc[E], msc[E], mbe[E];
+  auto coefs = [&](int c0) {
     chan_load<E>(mean, c0, mu);
-    if (y) {
-      float yy[E];
-      unit_to_f<T>(reinterpret_cast<const uint4*>(y)[u], yy);
-#pragma unroll
-      for (int i = 0; i < E; ++i) g[i] = yy[i] > 0.f ? g[i] : 0.f;
-    } else if (mb) {
-      mask_from_z<T, E>(gamma, invstd, mb, c0, mu, zz, g);
-    }
-    if (g_out) reinterpret_cast<uint4*>(g_out)[u] = f_to_unit<T>(g);
     chan_load<E>(coef, c0, ca);
     chan_load<E>(coef + C, c0, cb);
     chan_load<E>(coef + 2 * C, c0, cc);
+    if (!y && mb) mask_coef<E>(gamma, invstd, mb, c0, msc, mbe);
+  };
+  if (SAME) coefs((int)((u0 * E) % C));
+  for (long long u = u0; u < units; u += BN_AU * S) {
+    uint4 rg[BN_AU], rz[BN_AU], ry[BN_AU];
 #pragma unroll
-    for (int i = 0; i < E; ++i) o[i] = ca[i] * g[i] + cb[i] + cc[i] * (zz[i] - mu[i]);
-    reinterpret_cast<uint4*>(dz)[u] = f_to_unit<T>(o);
+    for (int q = 0; q < BN_AU; ++q) {
+      const long long uq = u + q * S;
+      const bool in = uq < units;
+      rg[q] = in ? reinterpret_cast<const uint4*>(dy)[uq] : uint4{0, 0, 0, 0};
+      rz[q] = in ? reinterpret_cast<const uint4*>(z)[uq] : uint4{0, 0, 0, 0};
+      ry[q] = (in && y) ? reinterpret_cast<const uint4*>(y)[uq] : uint4{0, 0, 0, 0};
+    }
+#pragma unroll
+    for (int q = 0; q < BN_AU; ++q) {
+      const long long uq = u + q * S;
+      if (uq >= units) break;
+      if (!SAME) coefs((int)((uq * E) % C));
+      float g[E], zz[E], o[E];
+      unit_to_f<T>(rg[q], g);
+      unit_to_f<T>(rz[q], zz);
+      if (y) {
+        float yy[E];
+        unit_to_f<T>(ry[q], yy);
+#pragma unroll
+        for (int i = 0; i < E; ++i) g[i] = yy[i] > 0.f ? g[i] : 0.f;
+      } else if (mb) {
+        apply_mask<T, E>(msc, mbe, mu, zz, g);
+      }
+      if (g_out) reinterpret_cast<uint4*>(g_out)[uq] = f_to_unit<T>(g);
+#pragma unroll
+      for (int i = 0; i < E; ++i) o[i] = ca[i] * g[i] + cb[i] + cc[i] * (zz[i] - mu[i]);
+      reinterpret_cast<uint4*>(dz)[uq] = f_to_unit<T>(o);
+    }
   }
 }
 
@@ -2106,8 +2144,14 @@ hipError_t bn_apply(int dt, const void* z, long long M, int C, const float* mean
   if (units == 0) return hipSuccess;
   return by_type(dt, [&](auto* tp) {
     using T = std::remove_pointer_t<decltype(tp)>;
-    hipLaunchKernelGGL(bn_apply_kernel<T>, dim3(grid_for(units)), dim3(256), 0, stream,
-                       (const T*)z, units, C, mean, scale, beta, (const T*)res, relu, (T*)y);
+    const int grid = grid_for(units, 256 * BN_AU);
+    const int upr = C / Elt<T>::E;  // units per row
+    if ((256LL * grid) % upr == 0)
+      hipLaunchKernelGGL((bn_apply_kernel<T, true>), dim3(grid), dim3(256), 0, stream, (const T*)z,
+                         units, C, mean, scale, beta, (const T*)res, relu, (T*)y);
+    else
+      hipLaunchKernelGGL((bn_apply_kernel<T, false>), dim3(grid), dim3(256), 0, stream,
+                         (const T*)z, units, C, mean, scale, beta, (const T*)res, relu, (T*)y);
   });
 }
 
@@ -2167,9 +2211,16 @@ hipError_t bn_backward(int dt, const void* dy, const void* y, const void* z, lon
   TimedLaunch ta(stream);
   return ta.done(by_type(dt, [&](auto* tp) {
     using T = std::remove_pointer_t<decltype(tp)>;
-    hipLaunchKernelGGL(bn_bwd_apply<T>, dim3(grid_for(units)), dim3(256), 0, stream, (const T*)dy,
-                       (const T*)y, (const T*)z, units, C, mean, coef, gamma, invstd, relu_beta,
-                       (T*)dz, (T*)g_out);
+    const int grid = grid_for(units, 256 * BN_AU);
+    const int upr = C / Elt<T>::E;  // units per row
+    if ((256LL * grid) % upr == 0)
+      hipLaunchKernelGGL((bn_bwd_apply<T, true>), dim3(grid), dim3(256), 0, stream, (const T*)dy,
+                         (const T*)y, (const T*)z, units, C, mean, coef, gamma, invstd, relu_beta,
+                         (T*)dz, (T*)g_out);
+    else
+      hipLaunchKernelGGL((bn_bwd_apply<T, false>), dim3(grid), dim3(256), 0, stream, (const T*)dy,
+                         (const T*)y, (const T*)z, units, C, mean, coef, gamma, invstd, relu_beta,
+                         (T*)dz, (T*)g_out);
   }), "bn_bwd_apply", apply_bytes);
 }
 
