@@ -927,8 +927,11 @@ template <int E> __device__ __forceinline__ void arg_store(uint8_t* p, const int
 }
 
 // 3x3 / stride 2 / pad 1 max pool.  One block covers 256 units (pixel x
-// 16-byte channel unit) of one output row; bpr blocks per row (the row index
-// from the block index is uniform, so no per-lane wide division).
+// 16-byte channel unit) of a pair of output rows p, p + 1 (p even; the
+// second absent for the last row of an odd P); bpr blocks per row pair (the
+// pair index from the block index is uniform, so no per-lane wide division).
+// The two windows of a thread share input row 2p + 1: its five input rows
+// are loaded once, and each element converted once.
 // BNR: x is a BatchNorm input z and the pooled values are the BatchNorm +
 // ReLU outputs relu((z - mean) * scale + beta), rounded to T exactly as the
 // standalone apply kernel stores them (so the window maxima and their
@@ -941,39 +944,42 @@ __global__ __launch_bounds__(256) void maxpool_fwd_kernel(const T* x, int N, int
                                                           const float* beta) {
   constexpr int E = Elt<T>::E;
   const int cu = C / E;
-  const int row = blockIdx.x / bpr;  // n * P + p
-  const int t = (blockIdx.x - row * bpr) * 256 + threadIdx.x;
-  if (row >= N * P || t >= Q * cu) return;
+  const int PR = (P + 1) / 2;
+  const int pair = blockIdx.x / bpr;  // n * PR + p / 2
+  const int t = (blockIdx.x - pair * bpr) * 256 + threadIdx.x;
+  if (pair >= N * PR || t >= Q * cu) return;
   const int q = t / cu, c0 = (t - q * cu) * E;
-  const int n = row / P, p = row - n * P;
+  const int n = pair / PR, p = 2 * (pair - n * PR);
+  const bool two = p + 1 < P;
   float mu[E], sc[E], be[E];
   if constexpr (BNR) {
     chan_load<E>(mean, c0, mu);
     chan_load<E>(scale, c0, sc);
     chan_load<E>(beta, c0, be);
   }
-  float best[E];
-  int ba[E];
+  float best0[E], best1[E];
+  int ba0[E], ba1[E];
 #pragma unroll
   for (int i = 0; i < E; ++i) {
-    best[i] = -INFINITY;
-    ba[i] = 0;
+    best0[i] = best1[i] = -INFINITY;
+    ba0[i] = ba1[i] = 0;
   }
-  // all nine window loads in flight before the comparisons (in window order)
-  uint4 raw[9];
-  bool ok[9];
+  // all fifteen loads in flight before the comparisons; input row rr is
+  // window row rr of output row p and window row rr - 2 of output row p + 1
+  uint4 raw[15];
+  bool ok[15];
 #pragma unroll
-  for (int r = 0; r < 3; ++r)
+  for (int rr = 0; rr < 5; ++rr)
 #pragma unroll
     for (int s = 0; s < 3; ++s) {
-      const int h = 2 * p + r - 1, w = 2 * q + s - 1;
-      ok[3 * r + s] = h >= 0 && h < H && w >= 0 && w < W;
-      raw[3 * r + s] = ok[3 * r + s]
-                           ? *reinterpret_cast<const uint4*>(x + (((long long)n * H + h) * W + w) * C + c0)
-                           : uint4{0, 0, 0, 0};
+      const int h = 2 * p + rr - 1, w = 2 * q + s - 1;
+      ok[3 * rr + s] = (rr < 3 || two) && h >= 0 && h < H && w >= 0 && w < W;
+      raw[3 * rr + s] = ok[3 * rr + s]
+                            ? *reinterpret_cast<const uint4*>(x + (((long long)n * H + h) * W + w) * C + c0)
+                            : uint4{0, 0, 0, 0};
     }
 #pragma unroll
-  for (int k = 0; k < 9; ++k) {
+  for (int k = 0; k < 15; ++k) {
     if (!ok[k]) continue;
     float v[E];
     unit_to_f<T>(raw[k], v);
@@ -981,16 +987,31 @@ __global__ __launch_bounds__(256) void maxpool_fwd_kernel(const T* x, int N, int
 #pragma unroll
       for (int i = 0; i < E; ++i) v[i] = to_f((T)relu_nan(__builtin_fmaf(v[i] - mu[i], sc[i], be[i])));
     }
+    if (k < 9) {  // windows in (r, s) order: the first maximum wins
 #pragma unroll
-    for (int i = 0; i < E; ++i)
-      if (v[i] > best[i]) {
-        best[i] = v[i];
-        ba[i] = k;
-      }
+      for (int i = 0; i < E; ++i)
+        if (v[i] > best0[i]) {
+          best0[i] = v[i];
+          ba0[i] = k;
+        }
+    }
+    if (k >= 6) {
+#pragma unroll
+      for (int i = 0; i < E; ++i)
+        if (v[i] > best1[i]) {
+          best1[i] = v[i];
+          ba1[i] = k - 6;
+        }
+    }
   }
-  const long long o = ((long long)row * Q + q) * C + c0;
-  *reinterpret_cast<uint4*>(y + o) = f_to_unit<T>(best);
-  if (arg) arg_store<E>(arg + o, ba);
+  const long long o = (((long long)n * P + p) * Q + q) * C + c0;
+  *reinterpret_cast<uint4*>(y + o) = f_to_unit<T>(best0);
+  if (arg) arg_store<E>(arg + o, ba0);
+  if (two) {
+    const long long o1 = o + (long long)Q * C;
+    *reinterpret_cast<uint4*>(y + o1) = f_to_unit<T>(best1);
+    if (arg) arg_store<E>(arg + o1, ba1);
+  }
 }
 
 // Input gradient of the max pool: a gather over the (at most 2 x 2) windows
@@ -2290,7 +2311,8 @@ hipError_t maxpool_fwd(int dt, const void* x, int N, int H, int W, int C, void* 
   return tl.done(by_type(dt, [&](auto* tp) {
     using T = std::remove_pointer_t<decltype(tp)>;
     const int bpr = cdiv(Q * (C / Elt<T>::E), 256);
-    hipLaunchKernelGGL(maxpool_fwd_kernel<T>, dim3((unsigned)((long long)N * P * bpr)), dim3(256), 0,
+    hipLaunchKernelGGL(maxpool_fwd_kernel<T>, dim3((unsigned)((long long)N * ((P + 1) / 2) * bpr)),
+                       dim3(256), 0,
                        stream, (const T*)x, N, H, W, C, P, Q, bpr, (T*)y, arg,
                        (const float*)nullptr, (const float*)nullptr, (const float*)nullptr);
   }), "maxpool_fwd", (double)N * C * ((double)H * W * es + (double)P * Q * (es + (arg ? 1 : 0))));
@@ -2313,7 +2335,7 @@ hipError_t bn_relu_maxpool_train(int dt, const void* z, int N, int H, int W, int
   return tl.done(by_type(dt, [&](auto* tp) {
     using T = std::remove_pointer_t<decltype(tp)>;
     const int bpr = cdiv(Q * (C / Elt<T>::E), 256);
-    hipLaunchKernelGGL((maxpool_fwd_kernel<T, true>), dim3((unsigned)((long long)N * P * bpr)),
+    hipLaunchKernelGGL((maxpool_fwd_kernel<T, true>), dim3((unsigned)((long long)N * ((P + 1) / 2) * bpr)),
                        dim3(256), 0, stream, (const T*)z, N, H, W, C, P, Q, bpr, (T*)y, arg, mean,
                        scale, beta);
   }), "bn_relu_maxpool", (double)N * C * ((double)H * W * es + (double)P * Q * (es + (arg ? 1 : 0))));
